@@ -1,0 +1,199 @@
+/*
+ * fcm.h -- Fused Convolutional Modules (FCMs) for AMD Instinct MI355X (gfx950).
+ *
+ * C ABI of libfcm.so. Implements the fused depthwise (DW) / pointwise (PW) convolution
+ * kernels of Qararyah et al., "Fusing Depthwise and Pointwise Convolutions for
+ * Efficient Inference on GPUs" (arXiv 2404.19331), and the FusePlanner cost model that
+ * chooses their tiling.
+ *
+ *   fcm_dw_pw     DW -> PW in one kernel (Sec. III-A "DWPW"; the depthwise separable
+ *                 convolution of Sec. II-B). The DW output tile never leaves the chip.
+ *   fcm_pw_dw     PW -> DW in one kernel (Sec. III-A "PWDW" / "PWDW_R"): the PW output is
+ *                 recomputed on the DW halo of each spatial tile (Sec. II-D), or computed
+ *                 once when a tile spans the whole plane.
+ *   fcm_pw_dw_pw  PW -> DW -> PW in one kernel (the inverted-residual block of Sec. II-B,
+ *                 three layers fused; the paper's modules fuse two).
+ *   fcm_dw, fcm_pw  single layers ("layer-by-layer", LBL, Sec. II-D and V-C): the
+ *                 unfused comparison, built from the same tiles and dataflow.
+ *   fcm_plan      FusePlanner (Sec. IV): global-memory-access estimates of the LBL and
+ *                 fused kernels (Eq. 1-4) and the tiling that minimises them.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  * Tensors are caller-owned DEVICE pointers (e.g. PyTorch tensors). The library never
+ *    allocates, frees or synchronises; every launch is asynchronous on `stream`
+ *    (a hipStream_t; NULL = the null stream).
+ *  * Activations: x is [n, c, h, w] (FCM_NCHW) or [n, h, w, c] (FCM_NHWC), dense,
+ *    row-major. The output uses the same layout.
+ *  * Weights are canonical regardless of layout: depthwise [c][k][k] (PyTorch
+ *    [c, 1, k, k]); pointwise [c_out][c_in] (PyTorch [c_out, c_in, 1, 1]).
+ *  * Element types: FCM_F32 float; FCM_BF16 bfloat16 (raw 16-bit patterns; computed with
+ *    fp32 accumulation, each stage's result rounded to bfloat16, nearest-even);
+ *    FCM_I8 int8 (int32 accumulation, each stage requantised to int8 by
+ *    desc->rq[stage], Sec. III-B).
+ *  * Biases (folded normalisation, Sec. III-A "convolution-normalisation-activation")
+ *    may be NULL (= zero): float for F32/BF16, int32 for I8.
+ *  * Depthwise geometry: square k x k, stride `stride`, symmetric zero padding `pad`,
+ *    channel multiplier 1; output h_o = (h + 2*pad - k)/stride + 1 (same for w).
+ *  * Each conv stage computes conv -> +bias -> activation -> cast. act[i]/rq[i] belong to
+ *    the i-th convolution in execution order.
+ *  * Pointers must be aligned to their element size; 16-byte aligned tensors with
+ *    16-byte multiple channel rows take the vector path (same results either way).
+ *  * Errors are returned synchronously as fcm_status; fcm_last_error() gives a
+ *    thread-local message. No exception crosses the ABI. Thread-safe.
+ */
+#ifndef FCM_H_
+#define FCM_H_
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  FCM_OK = 0,
+  FCM_EINVAL = 1,        /* NULL tensor, non-positive size, bad geometry or requant  */
+  FCM_EUNSUPPORTED = 2,  /* valid but not built: k not in {3,5}, stride not in {1,2},
+                            int8 with RELU6, plan that no compiled kernel implements,
+                            tile that does not fit in LDS                              */
+  FCM_EDEVICE = 3        /* HIP reported an error at launch                          */
+} fcm_status;
+
+typedef enum { FCM_F32 = 0, FCM_BF16 = 1, FCM_I8 = 2 } fcm_dtype;
+typedef enum { FCM_NCHW = 0, FCM_NHWC = 1 } fcm_layout;
+typedef enum { FCM_ACT_NONE = 0, FCM_ACT_RELU = 1, FCM_ACT_RELU6 = 2 } fcm_act;
+
+/* Module selector for fcm_plan. */
+typedef enum {
+  FCM_OP_DW_PW = 0,
+  FCM_OP_PW_DW = 1,
+  FCM_OP_PW_DW_PW = 2,
+  FCM_OP_DW = 3,
+  FCM_OP_PW = 4
+} fcm_op;
+
+/* int8 requantisation of a stage: q = clamp(rne(acc * mult / 2^shift), qmin, qmax),
+ * rne = round half to even, acc = int32 accumulator + int32 bias.
+ * Constraints: 0 <= shift <= 62, -128 <= qmin <= qmax <= 127. Ignored for float types. */
+typedef struct {
+  int32_t mult;
+  int32_t shift;
+  int32_t qmin;
+  int32_t qmax;
+} fcm_requant;
+
+/* One descriptor for every entry point; fields a module does not use are ignored.
+ *   fcm_dw_pw:    c_in channels -> DW -> PW -> c_out          (c_mid must equal c_in)
+ *   fcm_pw_dw:    c_in -> PW -> c_mid -> DW                   (c_out must equal c_mid)
+ *   fcm_pw_dw_pw: c_in -> PW -> c_mid -> DW -> PW -> c_out
+ *   fcm_dw:       c_in channels, uses act[0], rq[0]
+ *   fcm_pw:       c_in -> c_out on the h x w grid (k, stride, pad ignored), act[0], rq[0] */
+typedef struct {
+  int32_t n, h, w;
+  int32_t c_in, c_mid, c_out;
+  int32_t k, stride, pad;
+  int32_t dtype;   /* fcm_dtype  */
+  int32_t layout;  /* fcm_layout */
+  int32_t act[3];  /* fcm_act per conv stage, execution order */
+  fcm_requant rq[3];
+} fcm_desc;
+
+/* GPU description for the planner (Sec. IV: number of SMs, L1/shared-memory size).
+ * On CDNA4 a workgroup's share of the compute unit's LDS plays the role of the paper's
+ * L1/shared memory. Pass NULL to fcm_plan for the MI355X defaults
+ * (256 CUs, 8 XCDs, wave64, 160 KiB LDS per CU and per workgroup, 4 MiB L2 per XCD,
+ * 256 MiB Infinity Cache, 8 TB/s HBM3E). */
+typedef struct {
+  int32_t num_cus;
+  int32_t num_xcds;
+  int32_t wave_size;
+  int32_t lds_per_wg;   /* bytes */
+  int32_t lds_per_cu;   /* bytes */
+  int64_t l2_per_xcd;   /* bytes */
+  int64_t mall_bytes;   /* bytes */
+  double hbm_bytes_per_s;
+} fcm_hw_desc;
+
+/* A tiling chosen by fcm_plan (or filled in by the caller and validated at launch).
+ * tile_h x tile_w output pixels per workgroup; c_block channels staged per step (the
+ * contraction chunk, or the depthwise channel block); co_block output channels per
+ * workgroup (dw_pw, pw: PW outputs; pw_dw, dw: intermediate/depthwise channels;
+ * pw_dw_pw: intermediate-channel chunk). All byte figures are for the whole call. */
+typedef struct {
+  int32_t op;            /* fcm_op */
+  int32_t tile_h, tile_w;
+  int32_t c_block;
+  int32_t co_block;
+  int32_t variant;       /* compiled kernel family member implementing the plan */
+  int32_t waves;         /* waves per workgroup (64 lanes each) */
+  int32_t lds_bytes;     /* dynamic LDS per workgroup */
+  int32_t workgroups;
+  int32_t fuse;          /* planner verdict: 1 if the fused estimate < layer-by-layer */
+  int64_t bytes_ideal;          /* input + weights + output, each once                  */
+  int64_t bytes_tiled;          /* per-workgroup loads + stores of this tiling (exact)  */
+  int64_t bytes_paper;          /* Eq. 1-4 estimate of this module at this tiling        */
+  int64_t bytes_lbl_paper;      /* Eq. 2/3 estimate of the layer-by-layer chain          */
+  int64_t bytes_lbl_ideal;      /* layer-by-layer ideal: adds each intermediate twice    */
+  double redundancy;     /* recomputed fraction of the first conv (PW->DW halo); 0 else */
+} fcm_plan_t;
+
+/* FusePlanner. Chooses the tiling of `op` for `desc` on `hw` (NULL = MI355X) among the
+ * tilings the compiled kernels implement: minimises bytes_tiled subject to the LDS limit
+ * and to #workgroups >= #CUs where any tiling reaches it (Sec. IV-A constraints),
+ * ties broken by more workgroups (up to 2 per CU), then larger tiles. Host-only,
+ * integer arithmetic, deterministic; results are cached per (op, desc, hw).
+ * Returns FCM_EINVAL / FCM_EUNSUPPORTED like the launch entry points. */
+fcm_status fcm_plan(int32_t op, const fcm_desc* desc, const fcm_hw_desc* hw, fcm_plan_t* out);
+
+/* Evaluate a caller-chosen tiling (plan->op, tile_h, tile_w, c_block, co_block,
+ * variant) without searching: fills every other field, or fails with
+ * FCM_EUNSUPPORTED if no compiled kernel implements it. */
+fcm_status fcm_plan_evaluate(const fcm_desc* desc, const fcm_hw_desc* hw, fcm_plan_t* plan);
+
+/* DW -> PW module: y = act1(PW(act0(DW(x) + b_dw)) + b_pw).
+ *   x [n, c_in, h, w] | w_dw [c_in][k][k] | b_dw [c_in] | w_pw [c_out][c_in] |
+ *   b_pw [c_out] | y [n, c_out, h_o, w_o] (layout order as desc->layout).
+ * plan may be NULL (fcm_plan is called and cached). */
+fcm_status fcm_dw_pw(const fcm_desc* desc, const void* x, const void* w_dw, const void* b_dw,
+                     const void* w_pw, const void* b_pw, void* y, const fcm_plan_t* plan,
+                     void* stream);
+
+/* PW -> DW module: y = act1(DW(pad0(act0(PW(x) + b_pw))) + b_dw); the DW input is zero
+ * outside the image (never act0(b_pw)).
+ *   x [n, c_in, h, w] | w_pw [c_mid][c_in] | b_pw [c_mid] | w_dw [c_mid][k][k] |
+ *   b_dw [c_mid] | y [n, c_mid, h_o, w_o]. */
+fcm_status fcm_pw_dw(const fcm_desc* desc, const void* x, const void* w_pw, const void* b_pw,
+                     const void* w_dw, const void* b_dw, void* y, const fcm_plan_t* plan,
+                     void* stream);
+
+/* PW -> DW -> PW module (inverted residual, no skip connection):
+ *   x [n, c_in, h, w] | w_pw1 [c_mid][c_in] | w_dw [c_mid][k][k] | w_pw2 [c_out][c_mid] |
+ *   biases [c_mid], [c_mid], [c_out] | y [n, c_out, h_o, w_o]. */
+fcm_status fcm_pw_dw_pw(const fcm_desc* desc, const void* x, const void* w_pw1,
+                        const void* b_pw1, const void* w_dw, const void* b_dw,
+                        const void* w_pw2, const void* b_pw2, void* y, const fcm_plan_t* plan,
+                        void* stream);
+
+/* Single depthwise layer (layer-by-layer baseline): y [n, c_in, h_o, w_o]. */
+fcm_status fcm_dw(const fcm_desc* desc, const void* x, const void* w_dw, const void* b_dw,
+                  void* y, const fcm_plan_t* plan, void* stream);
+
+/* Single pointwise layer (layer-by-layer baseline): y [n, c_out, h, w]. */
+fcm_status fcm_pw(const fcm_desc* desc, const void* x, const void* w_pw, const void* b_pw,
+                  void* y, const fcm_plan_t* plan, void* stream);
+
+/* Human-readable name of a status code (static storage). */
+const char* fcm_status_string(fcm_status status);
+
+/* Detail of the last failure on the calling thread ("" if none). */
+const char* fcm_last_error(void);
+
+/* Library version string. */
+const char* fcm_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FCM_H_ */

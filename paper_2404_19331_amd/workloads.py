@@ -1,0 +1,225 @@
+"""Seeded synthetic workloads for the fused DW/PW modules.
+
+This module only describes layer shapes and draws seeded random tensors. It holds none
+of the modules' arithmetic; both the CPU oracle and the HIP path consume what it
+produces, so the same bytes reach both.
+
+Shapes follow the layers the paper evaluates (arXiv 2404.19331, Sec. V-B: MobileNet
+v1/v2-style depthwise separable and inverted-residual blocks, and convolutional ViT
+token grids) plus an EfficientNet-style int8 MBConv pair. Values are synthetic: the
+modules' timing does not depend on them, and no trained weights are used.
+
+Recipe (every array drawn on the CPU with numpy's PCG64 in the order x, then the
+weights in execution order):
+  * x:  U[-1, 1] ("u11"), N(0, 1) ("n01"), U{-127..127} ("i8"), U{-8..8} ("i8small")
+  * float weights: N(0, 1/fan_in); fan_in = K*K for depthwise, C_in for pointwise
+  * int8 weights: U{-127..127} ("i8") or U{-8..8} ("i8small")
+  * bf16 tensors: drawn in float32, then rounded to bfloat16 (nearest-even)
+  * biases: none for the named configurations; tests that exercise bias draw
+    N(0, 0.25) (float) or U{-2000..2000} (int32).
+"""
+from dataclasses import dataclass, field, replace
+from typing import Tuple
+
+import numpy as np
+
+BASE_SEED = 2404_19331
+
+ACT3 = Tuple[str, str, str]
+RQ = Tuple[int, int, int, int]  # (mult, shift, qmin, qmax)
+
+RQ_C4 = (1, 8, -127, 127)  # per-tensor scale 2^-8, symmetric int8 range
+
+
+@dataclass(frozen=True)
+class Case:
+    """One module invocation: module name, geometry, precision, layout, epilogues."""
+    op: str                      # dw_pw | pw_dw | pw_dw_pw | dw | pw
+    n: int
+    h: int
+    w: int
+    c_in: int
+    c_mid: int
+    c_out: int
+    k: int = 3
+    stride: int = 1
+    pad: int = 1
+    dtype: str = "f32"           # f32 | bf16 | i8
+    layout: str = "nchw"         # nchw | nhwc
+    act: ACT3 = ("none", "none", "none")
+    rq: Tuple[RQ, RQ, RQ] = ((1, 0, -127, 127),) * 3
+    dist_x: str = "u11"
+    dist_w: str = "fan_in"
+    bias: bool = False
+    seed: int = BASE_SEED
+    name: str = ""
+
+    def with_(self, **kw):
+        return replace(self, **kw)
+
+    def as_dict(self):
+        return dict(op=self.op, n=self.n, h=self.h, w=self.w, c_in=self.c_in, c_mid=self.c_mid,
+                    c_out=self.c_out, k=self.k, stride=self.stride, pad=self.pad,
+                    dtype=self.dtype, layout=self.layout, act=list(self.act),
+                    rq=[list(r) for r in self.rq], name=self.name)
+
+
+def _x_shape(case):
+    if case.layout == "nchw":
+        return (case.n, case.c_in, case.h, case.w)
+    return (case.n, case.h, case.w, case.c_in)
+
+
+def _to_bf16_bits(a):
+    import torch  # conversion only (round to nearest even), CPU
+    t = torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(torch.bfloat16)
+    return t.view(torch.int16).numpy().view(np.uint16).copy()
+
+
+def _draw_x(rng, case):
+    shape = _x_shape(case)
+    d = case.dist_x
+    if d == "u11":
+        a = rng.uniform(-1.0, 1.0, size=shape)
+    elif d == "n01":
+        a = rng.standard_normal(size=shape)
+    elif d == "i8":
+        return rng.integers(-127, 128, size=shape, dtype=np.int64).astype(np.int8)
+    elif d == "i8small":
+        return rng.integers(-8, 9, size=shape, dtype=np.int64).astype(np.int8)
+    else:
+        raise ValueError(d)
+    return _cast_float(a, case.dtype)
+
+
+def _cast_float(a, dtype):
+    if dtype == "f32":
+        return a.astype(np.float32)
+    if dtype == "bf16":
+        return _to_bf16_bits(a.astype(np.float32))
+    if dtype == "f64":
+        return a.astype(np.float64)
+    raise ValueError(dtype)
+
+
+def _draw_w(rng, case, shape, fan_in):
+    if case.dtype == "i8":
+        lo, hi = (-8, 8) if case.dist_w == "i8small" else (-127, 127)
+        return rng.integers(lo, hi + 1, size=shape, dtype=np.int64).astype(np.int8)
+    a = rng.standard_normal(size=shape) * np.sqrt(1.0 / fan_in)
+    return _cast_float(a, case.dtype)
+
+
+def _draw_b(rng, case, cnt):
+    if not case.bias:
+        return None
+    if case.dtype == "i8":
+        return rng.integers(-2000, 2001, size=cnt, dtype=np.int64).astype(np.int32)
+    b = rng.normal(0.0, 0.25, size=cnt)
+    return b.astype(np.float64 if case.dtype == "f64" else np.float32)
+
+
+def make_inputs(case, seed=None):
+    """Seeded inputs of a case as a dict of contiguous numpy arrays in storage format
+    (float32, uint16 bfloat16 bits, int8, float64). Keys depend on the module."""
+    rng = np.random.default_rng(case.seed if seed is None else seed)
+    out = {"x": _draw_x(rng, case)}
+    k = case.k
+    if case.op == "dw_pw":
+        out["w_dw"] = _draw_w(rng, case, (case.c_in, k, k), k * k)
+        out["w_pw"] = _draw_w(rng, case, (case.c_out, case.c_in), case.c_in)
+        out["b_dw"] = _draw_b(rng, case, case.c_in)
+        out["b_pw"] = _draw_b(rng, case, case.c_out)
+    elif case.op == "pw_dw":
+        out["w_pw"] = _draw_w(rng, case, (case.c_mid, case.c_in), case.c_in)
+        out["w_dw"] = _draw_w(rng, case, (case.c_mid, k, k), k * k)
+        out["b_pw"] = _draw_b(rng, case, case.c_mid)
+        out["b_dw"] = _draw_b(rng, case, case.c_mid)
+    elif case.op == "pw_dw_pw":
+        out["w_pw1"] = _draw_w(rng, case, (case.c_mid, case.c_in), case.c_in)
+        out["w_dw"] = _draw_w(rng, case, (case.c_mid, k, k), k * k)
+        out["w_pw2"] = _draw_w(rng, case, (case.c_out, case.c_mid), case.c_mid)
+        out["b_pw1"] = _draw_b(rng, case, case.c_mid)
+        out["b_dw"] = _draw_b(rng, case, case.c_mid)
+        out["b_pw2"] = _draw_b(rng, case, case.c_out)
+    elif case.op == "dw":
+        out["w_dw"] = _draw_w(rng, case, (case.c_in, k, k), k * k)
+        out["b_dw"] = _draw_b(rng, case, case.c_in)
+    elif case.op == "pw":
+        out["w_pw"] = _draw_w(rng, case, (case.c_out, case.c_in), case.c_in)
+        out["b_pw"] = _draw_b(rng, case, case.c_out)
+    else:
+        raise ValueError(case.op)
+    return out
+
+
+# ---------------------------------------------------------------------------
+# Named configurations
+# ---------------------------------------------------------------------------
+
+# MobileNetV1 (width 1.0, 224x224 input) depthwise-separable layers:
+# (input spatial size, channels, depthwise stride, pointwise output channels)
+MOBILENET_V1 = [
+    (112, 32, 1, 64), (112, 64, 2, 128), (56, 128, 1, 128), (56, 128, 2, 256),
+    (28, 256, 1, 256), (28, 256, 2, 512), (14, 512, 1, 512), (14, 512, 1, 512),
+    (14, 512, 1, 512), (14, 512, 1, 512), (14, 512, 1, 512), (14, 512, 2, 1024),
+    (7, 1024, 1, 1024),
+]
+
+VIT_GRIDS = [(56, 64, 192), (28, 192, 384), (14, 384, 768)]
+
+
+def config_c1():
+    """DW3x3+ReLU -> PW 32->64 +ReLU, fp32 NCHW, batch 1, 56x56."""
+    return [Case("dw_pw", 1, 56, 56, 32, 32, 64, 3, 1, 1, "f32", "nchw", ("relu", "relu", "none"),
+                 dist_x="u11", seed=BASE_SEED + 1, name="C1 dwpw 56x56x32->64 f32 b1")]
+
+
+def config_c2():
+    """Inverted residual PW 24->144 ReLU6, DW3x3 ReLU6, PW 144->24 linear, fp32, b1, 56x56."""
+    return [Case("pw_dw_pw", 1, 56, 56, 24, 144, 24, 3, 1, 1, "f32", "nchw",
+                 ("relu6", "relu6", "none"), dist_x="u11", seed=BASE_SEED + 2,
+                 name="C2 pwdwpw 56x56 24->144->24 f32 b1")]
+
+
+def config_c3(batches=(1, 32)):
+    """All 13 MobileNetV1 DW3x3+PW layers, bf16 NHWC, ReLU after each conv."""
+    out = []
+    for b in batches:
+        for li, (hw, c, s, co) in enumerate(MOBILENET_V1, start=1):
+            out.append(Case("dw_pw", b, hw, hw, c, c, co, 3, s, 1, "bf16", "nhwc",
+                            ("relu", "relu", "none"), dist_x="u11",
+                            seed=BASE_SEED + 3 + 100 * li + b,
+                            name="C3 L%d %dx%dx%d s%d ->%d bf16 b%d" % (li, hw, hw, c, s, co, b)))
+    return out
+
+
+def config_c4():
+    """EfficientNet-B0-style int8 MBConv DW5x5+PW pairs, NHWC, batch 8, requant 2^-8 RNE."""
+    rq = (RQ_C4, RQ_C4, RQ_C4)
+    return [
+        Case("dw_pw", 8, 112, 112, 96, 96, 24, 5, 2, 2, "i8", "nhwc", ("none",) * 3, rq,
+             dist_x="i8", dist_w="i8", seed=BASE_SEED + 4 + 100,
+             name="C4a dwpw5x5s2 112x112x96->24 i8 b8"),
+        Case("dw_pw", 8, 14, 14, 480, 480, 112, 5, 1, 2, "i8", "nhwc", ("none",) * 3, rq,
+             dist_x="i8", dist_w="i8", seed=BASE_SEED + 4 + 200,
+             name="C4b dwpw5x5s1 14x14x480->112 i8 b8"),
+    ]
+
+
+def config_c5():
+    """Convolutional-ViT token-grid DW3x3+PW projections, bf16 NHWC, batch 64, linear."""
+    return [Case("dw_pw", 64, hw, hw, c, c, co, 3, 1, 1, "bf16", "nhwc", ("none",) * 3,
+                 dist_x="n01", seed=BASE_SEED + 5 + 100 * i,
+                 name="C5 %dx%dx%d->%d bf16 b64" % (hw, hw, c, co))
+            for i, (hw, c, co) in enumerate(VIT_GRIDS, start=1)]
+
+
+CONFIGS = {"C1": config_c1, "C2": config_c2, "C3": config_c3, "C4": config_c4, "C5": config_c5}
+
+
+def all_cases():
+    out = []
+    for f in CONFIGS.values():
+        out.extend(f())
+    return out

@@ -1,0 +1,487 @@
+"""Pins of the CPU oracle against things other than itself (CPU only).
+
+Each test compares the oracle with a result the mathematics fixes independently:
+library routines for the special cases (scipy correlation for a depthwise plane,
+numpy matmul for a 1x1 conv, torch's dense/grouped conv2d in float64 for the
+compositions), hand-worked values, exact invariants (identity kernels, power-of-two
+homogeneity, layout/batch independence), and exact integer/rational arithmetic for
+requantisation. Shapes are non-square with C != C_out so that a transposed operand or a
+swapped index fails at least one test.
+"""
+import itertools
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+import scipy.signal
+import torch
+import torch.nn.functional as F
+
+import oracle
+from paper_2404_19331_amd.workloads import Case, make_inputs
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _nchw(a, layout):
+    return a if layout == "nchw" else np.transpose(a, (0, 3, 1, 2))
+
+
+def _to_layout(a, layout):
+    a = np.ascontiguousarray(a)
+    return a if layout == "nchw" else np.ascontiguousarray(np.transpose(a, (0, 2, 3, 1)))
+
+
+def _rand(rng, shape):
+    return rng.standard_normal(shape)
+
+
+def _bf16_np(a):
+    t = torch.from_numpy(np.asarray(a, dtype=np.float32)).to(torch.bfloat16)
+    return t.view(torch.int16).numpy().view(np.uint16).copy()
+
+
+def _bf16_to_f32(bits):
+    return (bits.astype(np.uint32) << 16).view(np.float32)
+
+
+# --------------------------------------------------------------------------------------
+# Depthwise and pointwise layers against library routines (float64, exact mode)
+# --------------------------------------------------------------------------------------
+
+DW_GEOMS = [(3, 1, 1), (3, 2, 1), (3, 1, 0), (5, 1, 2), (5, 2, 2), (5, 2, 1), (2, 1, 0), (1, 1, 0), (7, 2, 3)]
+
+
+@pytest.mark.parametrize("k,s,p", DW_GEOMS)
+@pytest.mark.parametrize("layout", ["nchw", "nhwc"])
+def test_dw_matches_scipy_correlate(k, s, p, layout):
+    rng = np.random.default_rng(100 + 10 * k + s + p)
+    n, c, h, w = 2, 3, 9, 7
+    if h + 2 * p < k:
+        pytest.skip("degenerate")
+    x = _rand(rng, (n, c, h, w))
+    wd = _rand(rng, (c, k, k))
+    bd = _rand(rng, (c,))
+    case = dict(n=n, h=h, w=w, c_in=c, c_mid=c, c_out=c, k=k, stride=s, pad=p, dtype="f64",
+                layout=layout, act=["none"] * 3)
+    y = _nchw(oracle.dw(case, _to_layout(x, layout), wd, bd), layout)
+    for b in range(n):
+        for ch in range(c):
+            xp = np.pad(x[b, ch], p)
+            ref = scipy.signal.correlate2d(xp, wd[ch], mode="valid")[::s, ::s] + bd[ch]
+            np.testing.assert_allclose(y[b, ch], ref, rtol=1e-12, atol=1e-12)
+
+
+@pytest.mark.parametrize("layout", ["nchw", "nhwc"])
+def test_pw_matches_matmul(layout):
+    rng = np.random.default_rng(7)
+    n, c, co, h, w = 2, 5, 3, 4, 6
+    x = _rand(rng, (n, c, h, w))
+    wp = _rand(rng, (co, c))
+    bp = _rand(rng, (co,))
+    case = dict(n=n, h=h, w=w, c_in=c, c_mid=c, c_out=co, k=1, stride=1, pad=0, dtype="f64",
+                layout=layout)
+    y = _nchw(oracle.pw(case, _to_layout(x, layout), wp, bp), layout)
+    ref = np.matmul(wp, x.reshape(n, c, h * w)).reshape(n, co, h, w) + bp[None, :, None, None]
+    np.testing.assert_allclose(y, ref, rtol=1e-12, atol=1e-12)
+
+
+# --------------------------------------------------------------------------------------
+# Compositions against torch's dense / grouped conv2d in float64
+# --------------------------------------------------------------------------------------
+
+@pytest.mark.parametrize("k,s,p", [(3, 1, 1), (3, 2, 1), (5, 2, 2), (5, 1, 2)])
+def test_dw_pw_equals_dense_conv(k, s, p):
+    """With no activation between them, DW then PW equals one standard convolution
+    with W[o,c,u,v] = P[o,c] * Wd[c,u,v]; a DW bias folds into the PW bias."""
+    rng = np.random.default_rng(11 + k + s)
+    n, c, co, h, w = 2, 4, 6, 10, 8
+    x = _rand(rng, (n, c, h, w))
+    wd, bd = _rand(rng, (c, k, k)), _rand(rng, (c,))
+    wp, bp = _rand(rng, (co, c)), _rand(rng, (co,))
+    case = dict(n=n, h=h, w=w, c_in=c, c_mid=c, c_out=co, k=k, stride=s, pad=p, dtype="f64",
+                layout="nchw", act=["none"] * 3)
+    y = oracle.dw_pw(case, x, wd, bd, wp, bp)
+    wdense = torch.from_numpy(wp[:, :, None, None] * wd[None, :, :, :])
+    beff = torch.from_numpy(bp + wp @ bd)
+    ref = F.conv2d(torch.from_numpy(x), wdense, beff, stride=s, padding=p).numpy()
+    np.testing.assert_allclose(y, ref, rtol=1e-11, atol=1e-11)
+
+
+@pytest.mark.parametrize("act", [("relu", "relu"), ("relu6", "none"), ("none", "relu6")])
+def test_dw_pw_with_activation_matches_torch(act):
+    rng = np.random.default_rng(12)
+    n, c, co, h, w, k, s, p = 1, 4, 5, 7, 9, 3, 2, 1
+    x = _rand(rng, (n, c, h, w)) * 4
+    wd, bd = _rand(rng, (c, k, k)), _rand(rng, (c,))
+    wp, bp = _rand(rng, (co, c)), _rand(rng, (co,))
+    case = dict(n=n, h=h, w=w, c_in=c, c_mid=c, c_out=co, k=k, stride=s, pad=p, dtype="f64",
+                layout="nchw", act=list(act) + ["none"])
+    y = oracle.dw_pw(case, x, wd, bd, wp, bp)
+    acts = {"none": lambda t: t, "relu": F.relu, "relu6": F.relu6}
+    t = F.conv2d(torch.from_numpy(x), torch.from_numpy(wd[:, None]), torch.from_numpy(bd),
+                 stride=s, padding=p, groups=c)
+    t = acts[act[0]](t)
+    t = F.conv2d(t, torch.from_numpy(wp[:, :, None, None]), torch.from_numpy(bp))
+    t = acts[act[1]](t)
+    np.testing.assert_allclose(y, t.numpy(), rtol=1e-11, atol=1e-11)
+
+
+@pytest.mark.parametrize("k,s,p", [(3, 1, 1), (3, 2, 1), (5, 2, 2)])
+def test_pw_dw_border_is_zero_not_activated_bias(k, s, p):
+    """PW->DW: the DW zero-pads its own input, so intermediate positions outside the
+    image are 0 even when act(PW bias) != 0 (ReLU6 with positive biases)."""
+    rng = np.random.default_rng(13)
+    n, ci, cm, h, w = 2, 3, 5, 8, 6
+    x = _rand(rng, (n, ci, h, w))
+    wp, bp = _rand(rng, (cm, ci)), np.abs(_rand(rng, (cm,))) + 0.5
+    wd, bd = _rand(rng, (cm, k, k)), _rand(rng, (cm,))
+    case = dict(n=n, h=h, w=w, c_in=ci, c_mid=cm, c_out=cm, k=k, stride=s, pad=p, dtype="f64",
+                layout="nchw", act=["relu6", "relu", "none"])
+    y = oracle.pw_dw(case, x, wp, bp, wd, bd)
+    e = F.relu6(F.conv2d(torch.from_numpy(x), torch.from_numpy(wp[:, :, None, None]), torch.from_numpy(bp)))
+    ref = F.relu(F.conv2d(e, torch.from_numpy(wd[:, None]), torch.from_numpy(bd), stride=s,
+                          padding=p, groups=cm)).numpy()
+    np.testing.assert_allclose(y, ref, rtol=1e-11, atol=1e-11)
+    # the wrong reading (pad with act(bias)) differs at the border
+    e_wrong = F.pad(e, (p, p, p, p), value=0.0)
+    e_wrong[:, :, :p, :] = F.relu6(torch.from_numpy(bp))[None, :, None, None]
+    wrong = F.relu(F.conv2d(e_wrong, torch.from_numpy(wd[:, None]), torch.from_numpy(bd), stride=s,
+                            groups=cm)).numpy()
+    assert np.max(np.abs(wrong - y)) > 1e-3
+
+
+def test_pw_dw_equals_dense_conv_without_activation():
+    rng = np.random.default_rng(14)
+    n, ci, cm, h, w, k, s, p = 1, 4, 6, 7, 8, 3, 2, 1
+    x = _rand(rng, (n, ci, h, w))
+    wp, wd = _rand(rng, (cm, ci)), _rand(rng, (cm, k, k))
+    case = dict(n=n, h=h, w=w, c_in=ci, c_mid=cm, c_out=cm, k=k, stride=s, pad=p, dtype="f64",
+                layout="nchw", act=["none"] * 3)
+    y = oracle.pw_dw(case, x, wp, None, wd, None)
+    wdense = torch.from_numpy(wd[:, None, :, :] * wp[:, :, None, None])  # [cm, ci, k, k]
+    ref = F.conv2d(torch.from_numpy(x), wdense, stride=s, padding=p).numpy()
+    np.testing.assert_allclose(y, ref, rtol=1e-11, atol=1e-11)
+
+
+@pytest.mark.parametrize("layout", ["nchw", "nhwc"])
+def test_pw_dw_pw_matches_torch(layout):
+    rng = np.random.default_rng(15)
+    n, ci, cm, co, h, w, k, s, p = 2, 3, 8, 5, 9, 7, 3, 1, 1
+    x = _rand(rng, (n, ci, h, w)) * 3
+    w1, b1 = _rand(rng, (cm, ci)), _rand(rng, (cm,))
+    wd, bd = _rand(rng, (cm, k, k)), _rand(rng, (cm,))
+    w2, b2 = _rand(rng, (co, cm)), _rand(rng, (co,))
+    case = dict(n=n, h=h, w=w, c_in=ci, c_mid=cm, c_out=co, k=k, stride=s, pad=p, dtype="f64",
+                layout=layout, act=["relu6", "relu6", "none"])
+    y = _nchw(oracle.pw_dw_pw(case, _to_layout(x, layout), w1, b1, wd, bd, w2, b2), layout)
+    t = F.relu6(F.conv2d(torch.from_numpy(x), torch.from_numpy(w1[:, :, None, None]), torch.from_numpy(b1)))
+    t = F.relu6(F.conv2d(t, torch.from_numpy(wd[:, None]), torch.from_numpy(bd), stride=s, padding=p, groups=cm))
+    t = F.conv2d(t, torch.from_numpy(w2[:, :, None, None]), torch.from_numpy(b2))
+    np.testing.assert_allclose(y, t.numpy(), rtol=1e-11, atol=1e-11)
+
+
+# --------------------------------------------------------------------------------------
+# Hand-worked examples (tests/golden/hand_dw_examples.txt)
+# --------------------------------------------------------------------------------------
+
+def _golden_dw():
+    rows = []
+    with open(os.path.join(GOLDEN, "hand_dw_examples.txt")) as f:
+        for line in f:
+            if line.startswith("#") or not line.strip():
+                continue
+            name, hw, ksp, xs, ws, ys = (t.strip() for t in line.split("|"))
+            h, w = map(int, hw.split())
+            k, s, p = map(int, ksp.split())
+            rows.append((name, h, w, k, s, p, list(map(float, xs.split())),
+                         list(map(float, ws.split())), list(map(float, ys.split()))))
+    return rows
+
+
+@pytest.mark.parametrize("row", _golden_dw(), ids=lambda r: r[0])
+@pytest.mark.parametrize("dtype", ["f64", "f32", "bf16"])
+def test_hand_worked_dw_examples(row, dtype):
+    name, h, w, k, s, p, xs, ws, ys = row
+    conv = {"f64": np.float64, "f32": np.float32}
+    enc = (lambda a: _bf16_np(a)) if dtype == "bf16" else (lambda a: np.asarray(a, conv[dtype]))
+    case = dict(n=1, h=h, w=w, c_in=1, c_mid=1, c_out=1, k=k, stride=s, pad=p, dtype=dtype, layout="nchw")
+    x = enc(np.array(xs).reshape(1, 1, h, w))
+    wd = enc(np.array(ws).reshape(1, k, k))
+    y = oracle.dw(case, x, wd, None)
+    yv = _bf16_to_f32(y) if dtype == "bf16" else y
+    assert yv.ravel().tolist() == ys
+    # followed by a 1x1 conv of weight 2: every value doubles
+    y2 = oracle.dw_pw(case, x, wd, None, enc(np.array([[2.0]])), None)
+    y2v = _bf16_to_f32(y2) if dtype == "bf16" else y2
+    assert y2v.ravel().tolist() == [2 * v for v in ys]
+
+
+# --------------------------------------------------------------------------------------
+# Exact invariants
+# --------------------------------------------------------------------------------------
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "i8"])
+@pytest.mark.parametrize("s", [1, 2])
+@pytest.mark.parametrize("act", ["none", "relu"])
+def test_identity_kernels_are_exact(dtype, s, act):
+    """Centre-delta DW and identity PW: y = act(x[:, :, ::s, ::s]) bit-exactly."""
+    case = Case("dw_pw", 2, 9, 7, 6, 6, 6, 3, s, 1, dtype, "nchw", (act, act, "none"),
+                ((1, 0, -128, 127),) * 3, dist_x="i8" if dtype == "i8" else "n01", seed=5)
+    inp = make_inputs(case)
+    x = inp["x"]
+    one = {"f32": np.float32(1), "bf16": np.uint16(0x3F80), "i8": np.int8(1)}[dtype]
+    wd = np.zeros((6, 3, 3), dtype=x.dtype)
+    wd[:, 1, 1] = one
+    wp = np.zeros((6, 6), dtype=x.dtype)
+    np.fill_diagonal(wp, one)
+    y = oracle.dw_pw(case, x, wd, None, wp, None)
+    ref = x[:, :, ::s, ::s]
+    if act == "relu":
+        if dtype == "bf16":
+            ref = np.where(_bf16_to_f32(ref) > 0, ref, np.uint16(0))
+        else:
+            ref = np.maximum(ref, 0).astype(x.dtype)
+    assert np.array_equal(y, ref)
+    # isolated stages: delta DW -> y = PW(x); identity PW -> y = DW(x)
+    if dtype != "i8" and act == "none" and s == 1:
+        y1 = oracle.dw_pw(case, x, wd, None, inp["w_pw"], None)
+        y2 = oracle.pw(case.with_(op="pw", k=1, pad=0), x, inp["w_pw"], None)
+        assert np.array_equal(y1, y2)
+        y3 = oracle.dw_pw(case, x, inp["w_dw"], None, wp, None)
+        y4 = oracle.dw(case.with_(op="dw"), x, inp["w_dw"], None)
+        assert np.array_equal(y3, y4)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("op", ["dw_pw", "pw_dw", "pw_dw_pw"])
+def test_power_of_two_homogeneity_is_bit_exact(dtype, op):
+    """f(2^k x) = 2^k f(x) exactly (act none/relu, biases scaled alike)."""
+    case = Case(op, 1, 8, 6, 4, 8 if op != "dw_pw" else 4, 5 if op == "pw_dw_pw" else (8 if op == "pw_dw" else 6),
+                3, 1, 1, dtype, "nhwc", ("relu", "relu", "none"), dist_x="n01", bias=True, seed=9)
+    inp = make_inputs(case)
+    y = oracle.run(op, case, inp)
+    scaled = dict(inp)
+    if dtype == "f32":
+        scaled["x"] = (inp["x"] * np.float32(8)).astype(np.float32)
+        yv = y
+    else:
+        scaled["x"] = _bf16_np(_bf16_to_f32(inp["x"]) * 8)
+        yv = _bf16_to_f32(y)
+    # every stage then sees 8x inputs with unchanged weights, so every bias scales by 8
+    for key in ("b_dw", "b_pw", "b_pw1", "b_pw2"):
+        if scaled.get(key) is not None:
+            scaled[key] = (scaled[key] * np.float32(8)).astype(np.float32)
+    y8 = oracle.run(op, case, scaled)
+    y8v = y8 if dtype == "f32" else _bf16_to_f32(y8)
+    assert np.array_equal(y8v, (yv * 8).astype(np.float32))
+
+
+def test_linearity_within_rounding():
+    case = Case("dw_pw", 1, 9, 9, 5, 5, 7, 3, 2, 1, "f64", "nchw", dist_x="n01", seed=3)
+    a = make_inputs(case)
+    b = make_inputs(case, seed=4)
+    xa, xb = a["x"], b["x"]
+    ya = oracle.dw_pw(case, xa, a["w_dw"], None, a["w_pw"], None)
+    yb = oracle.dw_pw(case, xb, a["w_dw"], None, a["w_pw"], None)
+    yab = oracle.dw_pw(case, 0.75 * xa - 2.5 * xb, a["w_dw"], None, a["w_pw"], None)
+    np.testing.assert_allclose(yab, 0.75 * ya - 2.5 * yb, rtol=1e-12, atol=1e-12)
+    # bilinear in (Wd, P)
+    yw = oracle.dw_pw(case, xa, 3 * a["w_dw"], None, -2 * a["w_pw"], None)
+    np.testing.assert_allclose(yw, -6 * ya, rtol=1e-12, atol=1e-12)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "i8"])
+@pytest.mark.parametrize("op", ["dw_pw", "pw_dw", "pw_dw_pw"])
+def test_layout_and_batch_independence(dtype, op):
+    rq = ((1, 4, -127, 127),) * 3
+    case = Case(op, 3, 7, 10, 6, 6 if op == "dw_pw" else 10, 4 if op != "pw_dw" else 10, 3, 2, 1,
+                dtype, "nchw", ("relu", "none", "relu"), rq,
+                dist_x="i8small" if dtype == "i8" else "n01", dist_w="i8small", bias=True, seed=21)
+    inp = make_inputs(case)
+    y = oracle.run(op, case, inp)
+    nh = dict(inp)
+    nh["x"] = np.ascontiguousarray(np.transpose(inp["x"], (0, 2, 3, 1)))
+    y_nhwc = oracle.run(op, case.with_(layout="nhwc"), nh)
+    assert np.array_equal(np.transpose(y_nhwc, (0, 3, 1, 2)), y)
+    for b in range(case.n):
+        one = dict(inp)
+        one["x"] = np.ascontiguousarray(inp["x"][b:b + 1])
+        assert np.array_equal(oracle.run(op, case.with_(n=1), one), y[b:b + 1])
+
+
+def test_f32_path_rounds_exact_result_once_per_stage():
+    """Single stage: the f32 result is the exact (f64) result rounded to float32."""
+    case = Case("dw", 2, 11, 9, 5, 5, 5, 3, 1, 1, "f32", "nchw", dist_x="n01", bias=True, seed=31)
+    inp = make_inputs(case)
+    y32 = oracle.dw(case, inp["x"], inp["w_dw"], inp["b_dw"])
+    c64 = case.with_(dtype="f64")
+    y64 = oracle.dw(c64, inp["x"].astype(np.float64), inp["w_dw"].astype(np.float64),
+                    inp["b_dw"].astype(np.float64))
+    assert np.array_equal(y32, y64.astype(np.float32))
+
+
+def test_relu6_clamps():
+    case = dict(n=1, h=1, w=3, c_in=1, c_mid=1, c_out=1, k=1, stride=1, pad=0, dtype="f64",
+                layout="nchw", act=["relu6"] * 3)
+    y = oracle.pw(case, np.array([[[[-3.0, 2.5, 9.0]]]]), np.array([[1.0]]), None)
+    assert y.ravel().tolist() == [0.0, 2.5, 6.0]
+
+
+# --------------------------------------------------------------------------------------
+# Integer path
+# --------------------------------------------------------------------------------------
+
+def _golden_rq():
+    rows = []
+    with open(os.path.join(GOLDEN, "requant_rne.txt")) as f:
+        for line in f:
+            if line.startswith("#") or not line.strip():
+                continue
+            rows.append(tuple(int(t) for t in line.split()))
+    return rows
+
+
+@pytest.mark.parametrize("row", _golden_rq())
+def test_requant_table(row):
+    acc, mult, shift, qmin, qmax, expected = row
+    assert oracle.requant(acc, mult, shift, qmin, qmax) == expected
+
+
+def _rq_fraction(acc, mult, shift, qmin, qmax):
+    q = round(Fraction(acc * mult, 2 ** shift))  # Python rounds half to even
+    return max(qmin, min(qmax, q))
+
+
+def test_requant_exhaustive_against_fraction():
+    for shift in (0, 1, 2, 3, 8):
+        for mult in (1, 3, 7):
+            for acc in range(-1200, 1201):
+                assert oracle.requant(acc, mult, shift, -127, 127) == _rq_fraction(acc, mult, shift, -127, 127)
+    big = [2 ** 31 - 1, -2 ** 31, 123456789, -987654321]
+    for acc in big:
+        for mult, shift in ((1, 8), (1073741824, 40), (12345, 20)):
+            assert oracle.requant(acc, mult, shift, -128, 127) == _rq_fraction(acc, mult, shift, -128, 127)
+
+
+def _int_conv_reference(x, wd, bd, wp, bp, k, s, p, rq, acts):
+    """DW -> requant -> PW -> requant using float64 conv (exact for these magnitudes)
+    and Fraction rounding."""
+    t = F.conv2d(torch.from_numpy(x.astype(np.float64)), torch.from_numpy(wd.astype(np.float64)[:, None]),
+                 stride=s, padding=p, groups=x.shape[1]).numpy()
+    t = np.rint(t).astype(np.int64)
+    if bd is not None:
+        t = t + bd.astype(np.int64)[None, :, None, None]
+    rqv = np.vectorize(lambda a: _rq_fraction(int(a), *rq[0]))
+    m = rqv(t)
+    if acts[0] == "relu":
+        m = np.maximum(m, 0)
+    u = F.conv2d(torch.from_numpy(m.astype(np.float64)), torch.from_numpy(wp.astype(np.float64)[:, :, None, None])).numpy()
+    u = np.rint(u).astype(np.int64)
+    if bp is not None:
+        u = u + bp.astype(np.int64)[None, :, None, None]
+    y = np.vectorize(lambda a: _rq_fraction(int(a), *rq[1]))(u)
+    if acts[1] == "relu":
+        y = np.maximum(y, 0)
+    return y.astype(np.int8)
+
+
+@pytest.mark.parametrize("dist,rq", [("i8", (1, 8, -127, 127)), ("i8small", (1, 4, -127, 127)), ("i8", (5, 11, -128, 127))])
+@pytest.mark.parametrize("act", [("none", "none"), ("relu", "relu")])
+def test_int8_dw_pw_matches_integer_reference(dist, rq, act):
+    case = Case("dw_pw", 2, 9, 8, 12, 12, 5, 5, 2, 2, "i8", "nchw", act + ("none",), (rq, rq, rq),
+                dist_x=dist, dist_w=dist, bias=True, seed=41)
+    inp = make_inputs(case)
+    y = oracle.dw_pw(case, inp["x"], inp["w_dw"], inp["b_dw"], inp["w_pw"], inp["b_pw"])
+    ref = _int_conv_reference(inp["x"], inp["w_dw"], inp["b_dw"], inp["w_pw"], inp["b_pw"],
+                              5, 2, 2, (rq, rq), act)
+    assert np.array_equal(y, ref)
+
+
+def test_int8_saturation_fraction_matches_analysis():
+    """U{-127..127} inputs and weights with 5x5 DW and scale 2^-8 saturate heavily
+    (analysis: sigma(acc/256) ~ 106, about 23% of DW outputs at +-127)."""
+    case = Case("dw", 1, 40, 40, 16, 16, 16, 5, 1, 2, "i8", "nchw", rq=((1, 8, -127, 127),) * 3,
+                dist_x="i8", dist_w="i8", seed=42)
+    inp = make_inputs(case)
+    y = oracle.dw(case, inp["x"], inp["w_dw"], None)
+    interior = y[:, :, 2:-2, 2:-2]
+    frac = np.mean(np.abs(interior.astype(np.int32)) == 127)
+    assert 0.15 < frac < 0.32
+
+
+def test_int32_overflow_is_reported():
+    case = dict(n=1, h=1, w=1, c_in=1, c_mid=1, c_out=1, k=1, stride=1, pad=0, dtype="i8",
+                layout="nchw", rq=[(1, 0, -127, 127)] * 3)
+    x = np.array([[[[127]]]], dtype=np.int8)
+    w = np.array([[127]], dtype=np.int8)
+    b = np.array([2 ** 31 - 100], dtype=np.int32)
+    with pytest.raises(oracle.OracleError):
+        oracle.pw(case, x, w, b)
+
+
+def test_int8_relu6_unsupported():
+    case = dict(n=1, h=1, w=1, c_in=1, c_mid=1, c_out=1, k=1, stride=1, pad=0, dtype="i8",
+                layout="nchw", act=["relu6"] * 3, rq=[(1, 0, -127, 127)] * 3)
+    with pytest.raises(oracle.OracleError):
+        oracle.pw(case, np.zeros((1, 1, 1, 1), np.int8), np.zeros((1, 1), np.int8), None)
+
+
+# --------------------------------------------------------------------------------------
+# bfloat16 rounding
+# --------------------------------------------------------------------------------------
+
+def test_bf16_rounding_matches_torch():
+    rng = np.random.default_rng(51)
+    vals = np.concatenate([
+        rng.standard_normal(4000).astype(np.float32) * np.float32(3.0),
+        np.array([1.0 + 2 ** -8, 1.0 + 3 * 2 ** -8, -(1.0 + 2 ** -8), 3.4e38, -3.4e38, 1e-40, 0.0, -0.0,
+                  np.inf, -np.inf, 65504.0, 1.00390625, 1.01171875], dtype=np.float32),
+    ])
+    ref = _bf16_np(vals)
+    got = np.array([oracle.bf16_bits(v) for v in vals], dtype=np.uint16)
+    assert np.array_equal(got, ref)
+    assert oracle.bf16_bits(1.0 + 2 ** -8) == 0x3F80  # tie -> even (down)
+    assert oracle.bf16_bits(1.0 + 3 * 2 ** -8) == 0x3F82  # tie -> even (up)
+    assert oracle.bf16_bits(3.4e38) == 0x7F80  # rounds up to +inf
+    nan = oracle.bf16_bits(float("nan"))
+    assert (nan & 0x7F80) == 0x7F80 and (nan & 0x7F) != 0
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "i8"])
+@pytest.mark.parametrize("op", ["dw_pw", "pw_dw", "pw_dw_pw"])
+def test_module_equals_chain_of_single_layers(dtype, op):
+    """A module computes exactly its layer-by-layer chain: each stage's output is cast to
+    the storage precision before the next stage reads it (fusion moves data only). Each
+    single layer is pinned above (exact result rounded once), so this pins the
+    intermediate casts."""
+    rq = ((1, 6, -127, 127), (3, 9, -127, 127), (1, 7, -127, 127))
+    cm = 6 if op == "dw_pw" else 9
+    co = {"dw_pw": 5, "pw_dw": 9, "pw_dw_pw": 4}[op]
+    case = Case(op, 2, 9, 8, 6, cm, co, 3, 2, 1, dtype, "nhwc", ("relu", "relu6" if dtype != "i8" else "none", "relu"),
+                rq, dist_x="i8small" if dtype == "i8" else "n01", dist_w="i8small", bias=True, seed=61)
+    inp = make_inputs(case)
+    y = oracle.run(op, case, inp)
+    base = dict(n=2, dtype=dtype, layout="nhwc")
+
+    def stage_dw(t, h, w, c, wd, bd, i):
+        return oracle.dw(dict(base, h=h, w=w, c_in=c, c_mid=c, c_out=c, k=3, stride=2, pad=1,
+                              act=[case.act[i]] * 3, rq=[rq[i]] * 3), t, wd, bd)
+
+    def stage_pw(t, h, w, ci, co_, wp, bp, i):
+        return oracle.pw(dict(base, h=h, w=w, c_in=ci, c_mid=co_, c_out=co_, k=1, stride=1, pad=0,
+                              act=[case.act[i]] * 3, rq=[rq[i]] * 3), t, wp, bp)
+
+    ho, wo = oracle.out_hw(9, 8, 3, 2, 1)
+    if op == "dw_pw":
+        m = stage_dw(inp["x"], 9, 8, 6, inp["w_dw"], inp["b_dw"], 0)
+        ref = stage_pw(m, ho, wo, 6, co, inp["w_pw"], inp["b_pw"], 1)
+    elif op == "pw_dw":
+        m = stage_pw(inp["x"], 9, 8, 6, cm, inp["w_pw"], inp["b_pw"], 0)
+        ref = stage_dw(m, 9, 8, cm, inp["w_dw"], inp["b_dw"], 1)
+    else:
+        m = stage_pw(inp["x"], 9, 8, 6, cm, inp["w_pw1"], inp["b_pw1"], 0)
+        m = stage_dw(m, 9, 8, cm, inp["w_dw"], inp["b_dw"], 1)
+        ref = stage_pw(m, ho, wo, cm, co, inp["w_pw2"], inp["b_pw2"], 2)
+    assert np.array_equal(y, ref)

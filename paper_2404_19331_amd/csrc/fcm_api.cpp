@@ -1,0 +1,277 @@
+// fcm_api.cpp -- the C ABI of libfcm.so: argument validation, plan lookup, kernel
+// argument marshalling and launch. No allocation, no synchronisation.
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "fcm_host.h"
+
+namespace fcm {
+
+static thread_local std::string g_last_error;
+
+fcm_status fail(fcm_status st, const std::string& msg) {
+  g_last_error = msg;
+  return st;
+}
+
+const Variant* all_variants(int* count) {
+  static std::vector<Variant> all = [] {
+    std::vector<Variant> v;
+    const Variant* (*fns[])(int*) = {variants_dwpw_f32, variants_dwpw_bf16, variants_dwpw_i8, variants_pwdw,
+                                     variants_pwdwpw};
+    for (auto fn : fns) {
+      int n = 0;
+      const Variant* t = fn(&n);
+      v.insert(v.end(), t, t + n);
+    }
+    return v;
+  }();
+  *count = (int)all.size();
+  return all.data();
+}
+
+static bool uses_dw(int op) { return op != FCM_OP_PW; }
+
+fcm_status validate(int op, const fcm_desc* d) {
+  if (op < FCM_OP_DW_PW || op > FCM_OP_PW) return fail(FCM_EINVAL, "unknown module");
+  if (!d) return fail(FCM_EINVAL, "descriptor is NULL");
+  if (d->n <= 0 || d->h <= 0 || d->w <= 0 || d->c_in <= 0)
+    return fail(FCM_EINVAL, "n, h, w and c_in must be positive");
+  if (d->dtype < FCM_F32 || d->dtype > FCM_I8) return fail(FCM_EINVAL, "unknown dtype");
+  if (d->layout != FCM_NCHW && d->layout != FCM_NHWC) return fail(FCM_EINVAL, "unknown layout");
+  const int stages = op == FCM_OP_PW_DW_PW ? 3 : ((op == FCM_OP_DW || op == FCM_OP_PW) ? 1 : 2);
+  for (int i = 0; i < stages; ++i) {
+    if (d->act[i] < FCM_ACT_NONE || d->act[i] > FCM_ACT_RELU6) return fail(FCM_EINVAL, "unknown activation");
+    if (d->dtype == FCM_I8) {
+      const fcm_requant& r = d->rq[i];
+      if (r.shift < 0 || r.shift > 62) return fail(FCM_EINVAL, "requant shift must be in [0, 62]");
+      if (r.qmin < -128 || r.qmax > 127 || r.qmin > r.qmax)
+        return fail(FCM_EINVAL, "requant range must satisfy -128 <= qmin <= qmax <= 127");
+      if (d->act[i] == FCM_ACT_RELU6) return fail(FCM_EUNSUPPORTED, "int8 supports NONE and RELU activations");
+    }
+  }
+  switch (op) {
+    case FCM_OP_DW_PW:
+      if (d->c_out <= 0) return fail(FCM_EINVAL, "c_out must be positive");
+      if (d->c_mid != d->c_in) return fail(FCM_EINVAL, "dw_pw: c_mid must equal c_in");
+      break;
+    case FCM_OP_PW_DW:
+      if (d->c_mid <= 0) return fail(FCM_EINVAL, "c_mid must be positive");
+      if (d->c_out != d->c_mid) return fail(FCM_EINVAL, "pw_dw: c_out must equal c_mid");
+      break;
+    case FCM_OP_PW_DW_PW:
+      if (d->c_mid <= 0 || d->c_out <= 0) return fail(FCM_EINVAL, "c_mid and c_out must be positive");
+      break;
+    case FCM_OP_PW:
+      if (d->c_out <= 0) return fail(FCM_EINVAL, "c_out must be positive");
+      break;
+    default:
+      break;
+  }
+  if (uses_dw(op)) {
+    if (d->k <= 0 || d->stride <= 0 || d->pad < 0) return fail(FCM_EINVAL, "k and stride must be positive, pad >= 0");
+    if (d->pad >= d->k) return fail(FCM_EINVAL, "pad must be smaller than k");
+    if (d->h + 2 * d->pad < d->k || d->w + 2 * d->pad < d->k) return fail(FCM_EINVAL, "output would be empty");
+    if (d->k != 3 && d->k != 5) return fail(FCM_EUNSUPPORTED, "depthwise k must be 3 or 5");
+    if (d->stride != 1 && d->stride != 2) return fail(FCM_EUNSUPPORTED, "depthwise stride must be 1 or 2");
+  }
+  const int64_t big = (int64_t)d->n * d->h * d->w;
+  const int64_t cmax = std::max(std::max(d->c_in, d->c_mid), d->c_out);
+  if (big * cmax > (int64_t)1 << 40) return fail(FCM_EUNSUPPORTED, "tensor too large");
+  return FCM_OK;
+}
+
+static bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+static fcm_status check_alignment(const void* p, int elt, const char* what) {
+  if (p && ((uintptr_t)p % (uintptr_t)elt) != 0)
+    return fail(FCM_EINVAL, std::string(what) + " is not aligned to its element size");
+  return FCM_OK;
+}
+
+struct Tensors {
+  const void* x;
+  const void* w[3];
+  const void* b[3];
+  void* y;
+};
+
+static fcm_status run(int op, const fcm_desc* d, const Tensors& t, const fcm_plan_t* plan_in, void* stream) {
+  fcm_status st = validate(op, d);
+  if (st != FCM_OK) return st;
+  const int nw = op == FCM_OP_PW_DW_PW ? 3 : ((op == FCM_OP_DW || op == FCM_OP_PW) ? 1 : 2);
+  if (!t.x || !t.y) return fail(FCM_EINVAL, "x and y must not be NULL");
+  for (int i = 0; i < nw; ++i)
+    if (!t.w[i]) return fail(FCM_EINVAL, "weights must not be NULL");
+  const Geom g = geometry(op, d);
+  const int e = g.elt;
+  if ((st = check_alignment(t.x, e, "x")) || (st = check_alignment(t.y, e, "y"))) return st;
+  for (int i = 0; i < nw; ++i) {
+    if ((st = check_alignment(t.w[i], e, "weights"))) return st;
+    if ((st = check_alignment(t.b[i], 4, "bias"))) return st;
+  }
+
+  const fcm_hw_desc hw = default_hw();
+  fcm_plan_t p;
+  if (plan_in) {
+    if (plan_in->op != op) return fail(FCM_EINVAL, "plan was made for another module");
+    p = *plan_in;
+    if ((st = evaluate_plan(g, d, hw, &p)) != FCM_OK) return st;
+  } else {
+    if ((st = find_plan(op, d, &hw, &p)) != FCM_OK) return st;
+  }
+  int nv = 0;
+  const Variant* vs = all_variants(&nv);
+  const Variant& v = vs[p.variant];
+
+  KArgs a;
+  memset(&a, 0, sizeof(a));
+  a.x = t.x;
+  a.y = t.y;
+  a.w1 = t.w[0];
+  a.b1 = t.b[0];
+  a.w2 = t.w[1];
+  a.b2 = t.b[1];
+  a.w3 = t.w[2];
+  a.b3 = t.b[2];
+  a.N = g.n;
+  a.H = g.h;
+  a.W = g.w;
+  a.Ci = g.ci;
+  a.Cm = g.cm;
+  a.Co = g.co;
+  a.Ho = g.ho;
+  a.Wo = g.wo;
+  a.pad = g.pad;
+  a.layout = d->layout;
+  a.TH = p.tile_h;
+  a.TW = p.tile_w;
+  a.CB = p.c_block;
+  a.COB = p.co_block;
+  a.tiles_y = ceil_div(g.ho, p.tile_h);
+  a.tiles_x = ceil_div(g.wo, p.tile_w);
+  const int last = (g.family == FAM_PWDW || g.family == FAM_DW) ? g.cm : g.co;
+  a.n_cb = ceil_div(last, p.co_block);
+  for (int i = 0; i < 3; ++i) {
+    a.act[i] = d->act[i];
+    a.rq[i].mult = d->rq[i].mult;
+    a.rq[i].shift = d->rq[i].shift;
+    a.rq[i].qmin = d->rq[i].qmin;
+    a.rq[i].qmax = d->rq[i].qmax;
+  }
+  // vector paths: 16-byte aligned base and 16-byte multiple rows
+  const int xc = g.family == FAM_DW ? g.cm : g.ci;
+  a.vec_x = aligned16(t.x) && (xc * e) % 16 == 0;
+  a.vec_y = aligned16(t.y) && (last * e) % 16 == 0;
+  switch (g.family) {
+    case FAM_DWPW: a.vec_w2 = aligned16(t.w[1]) && (g.ci * e) % 16 == 0; break;
+    case FAM_PW: a.vec_w1 = aligned16(t.w[0]) && (g.ci * e) % 16 == 0; break;
+    case FAM_PWDW: a.vec_w1 = aligned16(t.w[0]) && (g.ci * e) % 16 == 0; break;
+    case FAM_PWDWPW:
+      a.vec_w1 = aligned16(t.w[0]) && (g.ci * e) % 16 == 0;
+      a.vec_w3 = aligned16(t.w[2]) && (g.cm * e) % 16 == 0;
+      break;
+    default: break;
+  }
+  switch (g.family) {
+    case FAM_DWPW:
+    case FAM_PW:
+      a.L = lds_layout_dwpw(g.dtype, g.k, g.s, g.family == FAM_DWPW, p.tile_h, p.tile_w, p.c_block, p.co_block);
+      break;
+    case FAM_PWDW:
+    case FAM_DW:
+      a.L = lds_layout_pwdw(g.dtype, g.k, g.s, g.family == FAM_PWDW, p.tile_h, p.tile_w, p.c_block, p.co_block);
+      break;
+    default:
+      a.L = lds_layout_pwdwpw(g.dtype, g.k, g.s, p.tile_h, p.tile_w, g.ci, p.c_block, p.co_block);
+      break;
+  }
+  const int rc = v.launch(a, p.workgroups, stream);
+  if (rc != 0)
+    return fail(FCM_EDEVICE, std::string("kernel launch failed: ") + hipGetErrorString((hipError_t)rc) + " (" +
+                                 v.name + ")");
+  return FCM_OK;
+}
+
+}  // namespace fcm
+
+using namespace fcm;
+
+extern "C" {
+
+fcm_status fcm_plan(int32_t op, const fcm_desc* desc, const fcm_hw_desc* hw, fcm_plan_t* out) {
+  if (!out) return fail(FCM_EINVAL, "output plan is NULL");
+  fcm_status st = validate(op, desc);
+  if (st != FCM_OK) return st;
+  return find_plan(op, desc, hw, out);
+}
+
+fcm_status fcm_plan_evaluate(const fcm_desc* desc, const fcm_hw_desc* hw, fcm_plan_t* plan) {
+  if (!plan) return fail(FCM_EINVAL, "plan is NULL");
+  fcm_status st = validate(plan->op, desc);
+  if (st != FCM_OK) return st;
+  const fcm_hw_desc h = hw ? *hw : default_hw();
+  const Geom g = geometry(plan->op, desc);
+  st = evaluate_plan(g, desc, h, plan);
+  if (st != FCM_OK) return st;
+  // the layer-by-layer figures and the verdict come from the searched plan
+  fcm_plan_t ref;
+  st = find_plan(plan->op, desc, &h, &ref);
+  if (st != FCM_OK) return st;
+  plan->bytes_lbl_paper = ref.bytes_lbl_paper;
+  plan->bytes_lbl_ideal = ref.bytes_lbl_ideal;
+  plan->fuse = plan->bytes_paper < plan->bytes_lbl_paper ? 1 : 0;
+  if (plan->op == FCM_OP_DW || plan->op == FCM_OP_PW) plan->fuse = 0;
+  return FCM_OK;
+}
+
+fcm_status fcm_dw_pw(const fcm_desc* desc, const void* x, const void* w_dw, const void* b_dw, const void* w_pw,
+                     const void* b_pw, void* y, const fcm_plan_t* plan, void* stream) {
+  Tensors t = {x, {w_dw, w_pw, nullptr}, {b_dw, b_pw, nullptr}, y};
+  return run(FCM_OP_DW_PW, desc, t, plan, stream);
+}
+
+fcm_status fcm_pw_dw(const fcm_desc* desc, const void* x, const void* w_pw, const void* b_pw, const void* w_dw,
+                     const void* b_dw, void* y, const fcm_plan_t* plan, void* stream) {
+  Tensors t = {x, {w_pw, w_dw, nullptr}, {b_pw, b_dw, nullptr}, y};
+  return run(FCM_OP_PW_DW, desc, t, plan, stream);
+}
+
+fcm_status fcm_pw_dw_pw(const fcm_desc* desc, const void* x, const void* w_pw1, const void* b_pw1, const void* w_dw,
+                        const void* b_dw, const void* w_pw2, const void* b_pw2, void* y, const fcm_plan_t* plan,
+                        void* stream) {
+  Tensors t = {x, {w_pw1, w_dw, w_pw2}, {b_pw1, b_dw, b_pw2}, y};
+  return run(FCM_OP_PW_DW_PW, desc, t, plan, stream);
+}
+
+fcm_status fcm_dw(const fcm_desc* desc, const void* x, const void* w_dw, const void* b_dw, void* y,
+                  const fcm_plan_t* plan, void* stream) {
+  Tensors t = {x, {w_dw, nullptr, nullptr}, {b_dw, nullptr, nullptr}, y};
+  return run(FCM_OP_DW, desc, t, plan, stream);
+}
+
+fcm_status fcm_pw(const fcm_desc* desc, const void* x, const void* w_pw, const void* b_pw, void* y,
+                  const fcm_plan_t* plan, void* stream) {
+  Tensors t = {x, {w_pw, nullptr, nullptr}, {b_pw, nullptr, nullptr}, y};
+  return run(FCM_OP_PW, desc, t, plan, stream);
+}
+
+const char* fcm_status_string(fcm_status status) {
+  switch (status) {
+    case FCM_OK: return "FCM_OK";
+    case FCM_EINVAL: return "FCM_EINVAL: invalid argument";
+    case FCM_EUNSUPPORTED: return "FCM_EUNSUPPORTED: not supported by the compiled kernels";
+    case FCM_EDEVICE: return "FCM_EDEVICE: HIP error";
+  }
+  return "unknown fcm_status";
+}
+
+const char* fcm_last_error(void) { return g_last_error.c_str(); }
+
+const char* fcm_version(void) { return "fcm 0.1.0 (gfx950)"; }
+
+}  // extern "C"

@@ -1,0 +1,481 @@
+// fcm_device.h -- device building blocks shared by the fused-module kernels (gfx950).
+//
+// Every kernel is a composition of the same four steps (Sec. III-B of arXiv 2404.19331
+// describes the module skeleton: stage what the first convolution needs, compute it into
+// an on-chip communication buffer, synchronise, compute the second convolution from that
+// buffer and write only its output):
+//   stage_*      global -> LDS, 16-byte vector loads where alignment allows, zero fill
+//                outside the image and beyond the channel count;
+//   dw_compute   depthwise KxK stencil from an LDS tile [rows][cols][channels] into an LDS
+//                tile [pixels][channels] (+bias, activation, cast);
+//   mma_chunk    pointwise contraction on MFMA: acc[m][p] += A[m][k] * B[p][k] with both
+//                operands rows of k-contiguous data in LDS (16x16 output tiles per MFMA);
+//   store_tile   LDS tile [pixels][channels] -> global NCHW/NHWC, 16-byte stores.
+// The layouts in LDS are the same for every module, so the layer-by-layer kernels are
+// the fused ones with a stage switched off (the paper's LBL baselines share the fused
+// kernels' dataflow, Sec. V-C).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <type_traits>
+
+#include "fcm_internal.h"
+
+namespace fcm {
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+constexpr int kThreads = 256;  // 4 waves of 64 lanes per workgroup
+
+// ------------------------------------------------------------------------------------
+// Element-type traits.
+//   KB:  contraction elements consumed per 16-byte-per-lane MFMA operand step
+//        (4 lane groups x 16 bytes = 64 bytes of k per row)
+//   CPT: channels per depthwise thread-vector
+// ------------------------------------------------------------------------------------
+struct TF32 {
+  using T = float;
+  using Acc = float;
+  using AccV = f32x4;
+  static constexpr int ELT = 4, KB = 16, CPT = 4;
+};
+struct TBF16 {
+  using T = uint16_t;
+  using Acc = float;
+  using AccV = f32x4;
+  static constexpr int ELT = 2, KB = 32, CPT = 8;
+};
+struct TI8 {
+  using T = int8_t;
+  using Acc = int32_t;
+  using AccV = i32x4;
+  static constexpr int ELT = 1, KB = 64, CPT = 8;
+};
+
+// ------------------------------------------------------------------------------------
+// Scalar conversions / epilogue arithmetic
+// ------------------------------------------------------------------------------------
+__device__ __forceinline__ float bf16_to_f32(uint32_t b) { return __uint_as_float(b << 16); }
+
+// float -> bfloat16, round to nearest, ties to even; NaN stays a quiet NaN.
+__device__ __forceinline__ uint32_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x007fffffu)) return (u >> 16) | 0x40u;
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return u >> 16;
+}
+
+__device__ __forceinline__ float act_f(float v, int act) {
+  if (act == ACT_RELU) return fmaxf(v, 0.0f);
+  if (act == ACT_RELU6) return fminf(fmaxf(v, 0.0f), 6.0f);
+  return v;
+}
+
+// q = clamp(round_half_even(acc * mult / 2^shift), qmin, qmax), then ReLU if asked.
+__device__ __forceinline__ int32_t requant(int32_t acc, const Requant& rq, int act) {
+  int64_t t = (int64_t)acc * (int64_t)rq.mult;
+  int64_t q = t;
+  if (rq.shift > 0) {
+    q = t >> rq.shift;
+    int64_t r = t - (q << rq.shift);
+    int64_t half = (int64_t)1 << (rq.shift - 1);
+    q += (r > half || (r == half && (q & 1))) ? 1 : 0;
+  }
+  q = q < rq.qmin ? rq.qmin : q;
+  q = q > rq.qmax ? rq.qmax : q;
+  if (act == ACT_RELU && q < 0) q = 0;
+  return (int32_t)q;
+}
+
+// Finish one accumulator (+bias, activation, cast) into storage bits.
+template <class DT>
+struct Fin;
+template <>
+struct Fin<TF32> {
+  __device__ static __forceinline__ uint32_t apply(float acc, float bias, int act, const Requant&) {
+    return __float_as_uint(act_f(acc + bias, act));
+  }
+};
+template <>
+struct Fin<TBF16> {
+  __device__ static __forceinline__ uint32_t apply(float acc, float bias, int act, const Requant&) {
+    return f32_to_bf16(act_f(acc + bias, act));
+  }
+};
+template <>
+struct Fin<TI8> {
+  __device__ static __forceinline__ uint32_t apply(int32_t acc, int32_t bias, int act, const Requant& rq) {
+    return (uint32_t)(requant(acc + bias, rq, act) & 0xff);
+  }
+};
+
+// Bias element as the accumulator type (float for float paths, int32 for int8).
+template <class DT>
+__device__ __forceinline__ typename DT::Acc load_bias(const void* b, int i) {
+  if (!b) return typename DT::Acc(0);
+  if constexpr (std::is_same<DT, TI8>::value)
+    return ((const int32_t*)b)[i];
+  else
+    return ((const float*)b)[i];
+}
+
+// Store 4 consecutive finished values (bits) at an LDS address.
+template <class DT>
+__device__ __forceinline__ void lds_store4(char* p, uint32_t v0, uint32_t v1, uint32_t v2, uint32_t v3) {
+  if constexpr (DT::ELT == 4) {
+    *(u32x4*)p = u32x4{v0, v1, v2, v3};
+  } else if constexpr (DT::ELT == 2) {
+    *(u32x2*)p = u32x2{v0 | (v1 << 16), v2 | (v3 << 16)};
+  } else {
+    *(uint32_t*)p = v0 | (v1 << 8) | (v2 << 16) | (v3 << 24);
+  }
+}
+
+// ------------------------------------------------------------------------------------
+// MFMA: one 16-byte-per-lane operand step into a 16x16 accumulator tile.
+// Lane l supplies row (l % 16) of A and column (l % 16) of B, and the 16 bytes at
+// k-offset (l / 16) * 16 bytes of the step. A and B use the same k assignment, so any
+// order of k inside a step is a valid contraction. Output: lane l holds
+// C[m = 4 * (l / 16) + v][n = l % 16], v = 0..3.
+// ------------------------------------------------------------------------------------
+__device__ __forceinline__ void mma16(TF32, f32x4& c, const u32x4& a, const u32x4& b) {
+  c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.x), __uint_as_float(b.x), c, 0, 0, 0);
+  c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.y), __uint_as_float(b.y), c, 0, 0, 0);
+  c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.z), __uint_as_float(b.z), c, 0, 0, 0);
+  c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.w), __uint_as_float(b.w), c, 0, 0, 0);
+}
+__device__ __forceinline__ void mma16(TBF16, f32x4& c, const u32x4& a, const u32x4& b) {
+  c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c,
+                                               0, 0, 0);
+}
+__device__ __forceinline__ void mma16(TI8, i32x4& c, const u32x4& a, const u32x4& b) {
+  c = __builtin_amdgcn_mfma_i32_16x16x64_i8(__builtin_bit_cast(i32x4, a), __builtin_bit_cast(i32x4, b), c, 0, 0,
+                                             0);
+}
+
+// acc[i][j] += A[m_base + 16i .. +16][0..K) * B[n_base + 16j .. +16][0..K)^T
+// A, B: LDS, rows of K contiguous elements at byte strides as_, bs_ (multiples of 16).
+template <class DT, int TMW, int TNW>
+__device__ __forceinline__ void mma_chunk(typename DT::AccV (&acc)[TMW][TNW], const char* A, int as_,
+                                          const char* B, int bs_, int K, int m_base, int n_base, int m_act,
+                                          int n_act) {
+  const int lane = threadIdx.x & 63;
+  const int r = lane & 15, g = lane >> 4;
+  const int nkb = K / DT::KB;
+  const char* pa = A + (m_base + r) * as_ + g * 16;
+  const char* pb = B + (n_base + r) * bs_ + g * 16;
+#pragma unroll 1
+  for (int kb = 0; kb < nkb; ++kb) {
+    u32x4 a[TMW], b[TNW];
+#pragma unroll
+    for (int i = 0; i < TMW; ++i)
+      if (i < m_act) a[i] = *(const u32x4*)(pa + i * 16 * as_ + kb * 64);
+#pragma unroll
+    for (int j = 0; j < TNW; ++j)
+      if (j < n_act) b[j] = *(const u32x4*)(pb + j * 16 * bs_ + kb * 64);
+#pragma unroll
+    for (int i = 0; i < TMW; ++i)
+#pragma unroll
+      for (int j = 0; j < TNW; ++j)
+        if (i < m_act && j < n_act) mma16(DT{}, acc[i][j], a[i], b[j]);
+  }
+}
+
+// ------------------------------------------------------------------------------------
+// Staging: global -> LDS
+// ------------------------------------------------------------------------------------
+
+// Haloed input window rows [iy0, iy0+IH) x cols [ix0, ix0+IW), channels [c0, c0+CB) into
+// LDS as [IH*IW pixels][CB] with pixel stride ps bytes. Zero outside the image and for
+// channels >= C. vec: C*ELT % 16 == 0 and x 16-byte aligned.
+template <class DT>
+__device__ __forceinline__ void stage_input(char* s, int ps, const typename DT::T* __restrict__ x, int layout, int n, int C,
+                            int H, int W, int iy0, int ix0, int IH, int IW, int c0, int CB, bool vec) {
+  using T = typename DT::T;
+  constexpr int VE = 16 / DT::ELT;
+  if (layout == LAYOUT_NHWC) {
+    if (vec) {
+      const int nv = CB / VE;
+      const int total = IH * IW * nv;
+#pragma unroll 1
+  for (int i = threadIdx.x; i < total; i += kThreads) {
+        const int v = i % nv, pix = i / nv;
+        const int py = pix / IW, px = pix - py * IW;
+        const int gy = iy0 + py, gx = ix0 + px, c = c0 + v * VE;
+        u32x4 val = {0u, 0u, 0u, 0u};
+        if ((unsigned)gy < (unsigned)H && (unsigned)gx < (unsigned)W && c < C)
+          val = *(const u32x4*)(x + (((size_t)n * H + gy) * W + gx) * C + c);
+        *(u32x4*)(s + pix * ps + v * 16) = val;
+      }
+    } else {
+      const int total = IH * IW * CB;
+#pragma unroll 1
+  for (int i = threadIdx.x; i < total; i += kThreads) {
+        const int ci = i % CB, pix = i / CB;
+        const int py = pix / IW, px = pix - py * IW;
+        const int gy = iy0 + py, gx = ix0 + px, c = c0 + ci;
+        T val = T(0);
+        if ((unsigned)gy < (unsigned)H && (unsigned)gx < (unsigned)W && c < C)
+          val = x[(((size_t)n * H + gy) * W + gx) * C + c];
+        *(T*)(s + pix * ps + ci * DT::ELT) = val;
+      }
+    }
+  } else {
+    const int total = CB * IH * IW;
+#pragma unroll 1
+  for (int i = threadIdx.x; i < total; i += kThreads) {
+      const int px = i % IW;
+      const int t = i / IW;
+      const int py = t % IH, ci = t / IH;
+      const int gy = iy0 + py, gx = ix0 + px, c = c0 + ci;
+      T val = T(0);
+      if ((unsigned)gy < (unsigned)H && (unsigned)gx < (unsigned)W && c < C)
+        val = x[(((size_t)n * C + c) * H + gy) * W + gx];
+      *(T*)(s + (py * IW + px) * ps + ci * DT::ELT) = val;
+    }
+  }
+}
+
+// Rows [r0, r0+rows) x cols [c0, c0+CB) of a row-major [R][Cc] matrix into LDS rows of
+// stride rs bytes; zero beyond R or Cc. vec: Cc*ELT % 16 == 0 and w 16-byte aligned.
+template <class DT>
+__device__ __forceinline__ void stage_rows(char* s, int rs, const typename DT::T* __restrict__ w, int R, int Cc, int r0, int rows,
+                           int c0, int CB, bool vec) {
+  using T = typename DT::T;
+  constexpr int VE = 16 / DT::ELT;
+  if (vec) {
+    const int nv = CB / VE;
+    const int total = rows * nv;
+#pragma unroll 1
+  for (int i = threadIdx.x; i < total; i += kThreads) {
+      const int v = i % nv, r = i / nv;
+      const int gr = r0 + r, c = c0 + v * VE;
+      u32x4 val = {0u, 0u, 0u, 0u};
+      if (gr < R && c < Cc) val = *(const u32x4*)(w + (size_t)gr * Cc + c);
+      *(u32x4*)(s + r * rs + v * 16) = val;
+    }
+  } else {
+    const int total = rows * CB;
+#pragma unroll 1
+  for (int i = threadIdx.x; i < total; i += kThreads) {
+      const int ci = i % CB, r = i / CB;
+      const int gr = r0 + r, c = c0 + ci;
+      T val = T(0);
+      if (gr < R && c < Cc) val = w[(size_t)gr * Cc + c];
+      *(T*)(s + r * rs + ci * DT::ELT) = val;
+    }
+  }
+}
+
+// Depthwise weights [C][K][K] (channels c0..c0+CB) as accumulator-type values in LDS
+// laid out [K*K taps][CB], followed by the bias [CB]. Zero for channels >= C.
+template <class DT, int K>
+__device__ __forceinline__ void stage_dw_weights(typename DT::Acc* s, const typename DT::T* __restrict__ wd, const void* bd, int C,
+                                 int c0, int CB) {
+  using Acc = typename DT::Acc;
+  const int total = (K * K + 1) * CB;
+#pragma unroll 1
+  for (int i = threadIdx.x; i < total; i += kThreads) {
+    const int ci = i % CB, tap = i / CB;
+    const int c = c0 + ci;
+    Acc v = Acc(0);
+    if (c < C) {
+      if (tap < K * K) {
+        if constexpr (std::is_same<DT, TBF16>::value)
+          v = bf16_to_f32(((const uint16_t*)wd)[(size_t)c * K * K + tap]);
+        else
+          v = (Acc)wd[(size_t)c * K * K + tap];
+      } else {
+        v = load_bias<DT>(bd, c);
+      }
+    }
+    s[i] = v;
+  }
+}
+
+// ------------------------------------------------------------------------------------
+// Depthwise stencil: LDS input [rows][cols][CB] (pixel stride ips) -> LDS output
+// [TH*TW pixels][CB] (pixel stride ops), act + cast per stage. Each thread computes CPT
+// channels of R horizontally adjacent output pixels, reusing each loaded input row
+// across the K horizontal taps and the R pixels. TW must be a multiple of R.
+// ------------------------------------------------------------------------------------
+template <class DT>
+struct Vec;  // CPT channels of one pixel, unpacked to the accumulator type
+template <>
+struct Vec<TF32> {
+  u32x4 raw;
+  __device__ __forceinline__ void load(const char* p) { raw = *(const u32x4*)p; }
+  __device__ __forceinline__ float get(int e) const { return __uint_as_float(raw[e]); }
+};
+template <>
+struct Vec<TBF16> {
+  u32x4 raw;
+  __device__ __forceinline__ void load(const char* p) { raw = *(const u32x4*)p; }
+  __device__ __forceinline__ float get(int e) const {
+    const uint32_t w = raw[e >> 1];
+    return (e & 1) ? __uint_as_float(w & 0xffff0000u) : __uint_as_float(w << 16);
+  }
+};
+template <>
+struct Vec<TI8> {
+  u32x2 raw;
+  __device__ __forceinline__ void load(const char* p) { raw = *(const u32x2*)p; }
+  __device__ __forceinline__ int32_t get(int e) const {
+    const uint32_t w = raw[e >> 2];
+    return (int32_t)(int8_t)((w >> ((e & 3) * 8)) & 0xff);
+  }
+};
+
+template <class DT, int K, int S, int R>
+__device__ __forceinline__ void dw_compute(const char* sin, int ips, int IW, const typename DT::Acc* swd, int CB, int TH, int TW,
+                           int act, const Requant& rq, char* sout, int ops) {
+  using Acc = typename DT::Acc;
+  constexpr int CPT = DT::CPT;
+  constexpr int NIN = (R - 1) * S + K;
+  const int ng = CB / CPT;
+  const int spr = TW / R;
+  const int tasks = ng * TH * spr;
+#pragma unroll 1
+  for (int t = threadIdx.x; t < tasks; t += kThreads) {
+    const int g = t % ng, seg = t / ng;
+    const int ty = seg / spr, tx0 = (seg - ty * spr) * R;
+    Acc acc[R][CPT];
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+#pragma unroll
+      for (int e = 0; e < CPT; ++e) acc[r][e] = Acc(0);
+    const Acc* wg = swd + g * CPT;
+    // One kernel row per iteration (not unrolled): bounds the live registers to one row of
+    // inputs, K weight vectors and the R x CPT accumulators.
+#pragma unroll 1
+    for (int ky = 0; ky < K; ++ky) {
+      const char* row = sin + ((ty * S + ky) * IW + tx0 * S) * ips + g * CPT * DT::ELT;
+      Vec<DT> in[NIN];
+#pragma unroll
+      for (int j = 0; j < NIN; ++j) in[j].load(row + j * ips);
+#pragma unroll
+      for (int kx = 0; kx < K; ++kx) {
+        const Acc* wt = wg + (ky * K + kx) * CB;
+#pragma unroll
+        for (int e = 0; e < CPT; ++e) {
+          const Acc wv = wt[e];
+#pragma unroll
+          for (int r = 0; r < R; ++r) acc[r][e] += wv * in[r * S + kx].get(e);
+        }
+      }
+    }
+    const Acc* bias = swd + K * K * CB + g * CPT;
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      char* o = sout + (ty * TW + tx0 + r) * ops + g * CPT * DT::ELT;
+#pragma unroll
+      for (int e = 0; e < CPT; e += 4) {
+        lds_store4<DT>(o + e * DT::ELT, Fin<DT>::apply(acc[r][e + 0], bias[e + 0], act, rq),
+                       Fin<DT>::apply(acc[r][e + 1], bias[e + 1], act, rq),
+                       Fin<DT>::apply(acc[r][e + 2], bias[e + 2], act, rq),
+                       Fin<DT>::apply(acc[r][e + 3], bias[e + 3], act, rq));
+      }
+    }
+  }
+}
+
+// ------------------------------------------------------------------------------------
+// Accumulator tiles -> LDS tile [pixels][channels] (finished values).
+// acc[i][j] holds rows m = m_base + 16i + 4*(lane/16) + v, columns n = n_base + 16j + lane%16
+// of C[m = channel][n = pixel].
+// m_wr >= m_act tiles are written; tiles the MFMA loop skipped hold zero accumulators
+// and come out as act(0 + 0) = 0 (bias is masked beyond m_valid).
+// mask_iw > 0: pixel n is a position of an IW-wide window starting at (iy0, ix0) and
+// positions outside [0,H)x[0,W) are written as zero (PW output feeding a zero-padded DW).
+// ------------------------------------------------------------------------------------
+template <class DT, int TMW, int TNW>
+__device__ __forceinline__ void acc_to_lds(const typename DT::AccV (&acc)[TMW][TNW], int m_base, int n_base,
+                                           int m_wr, int n_act, const void* bias, int bias_off, int m_valid,
+                                           int act, const Requant& rq, char* so, int rs, int mask_iw, int iy0,
+                                           int ix0, int H, int W) {
+  const int lane = threadIdx.x & 63;
+  const int r = lane & 15, g = lane >> 4;
+#pragma unroll
+  for (int i = 0; i < TMW; ++i) {
+    if (i >= m_wr) continue;
+    const int m = m_base + i * 16 + 4 * g;
+    typename DT::Acc b[4];
+#pragma unroll
+    for (int v = 0; v < 4; ++v) b[v] = (m + v < m_valid) ? load_bias<DT>(bias, bias_off + m + v) : 0;
+#pragma unroll
+    for (int j = 0; j < TNW; ++j) {
+      if (j >= n_act) continue;
+      const int n = n_base + j * 16 + r;
+      uint32_t o[4];
+#pragma unroll
+      for (int v = 0; v < 4; ++v) o[v] = Fin<DT>::apply(acc[i][j][v], b[v], act, rq);
+      if (mask_iw > 0) {
+        const int qy = n / mask_iw, qx = n - qy * mask_iw;
+        const int gy = iy0 + qy, gx = ix0 + qx;
+        if (!((unsigned)gy < (unsigned)H && (unsigned)gx < (unsigned)W)) o[0] = o[1] = o[2] = o[3] = 0u;
+      }
+      lds_store4<DT>(so + n * rs + m * DT::ELT, o[0], o[1], o[2], o[3]);
+    }
+  }
+}
+
+// LDS tile [TH*TW pixels][cb] (stride rs) -> y at output pixel (oy0, ox0), channels
+// [c0, c0+cb) of a tensor with Cy channels and Ho x Wo pixels. vec: Cy*ELT % 16 == 0,
+// cb*ELT % 16 == 0 and y 16-byte aligned.
+template <class DT>
+__device__ __forceinline__ void store_tile(const char* so, int rs, typename DT::T* __restrict__ y, int layout, int n, int Cy,
+                           int Ho, int Wo, int oy0, int ox0, int TH, int TW, int c0, int cb, bool vec) {
+  using T = typename DT::T;
+  constexpr int VE = 16 / DT::ELT;
+  if (layout == LAYOUT_NHWC) {
+    if (vec) {
+      const int nv = cb / VE;
+      const int total = TH * TW * nv;
+#pragma unroll 1
+  for (int i = threadIdx.x; i < total; i += kThreads) {
+        const int v = i % nv, p = i / nv;
+        const int ty = p / TW, tx = p - ty * TW;
+        const int oy = oy0 + ty, ox = ox0 + tx;
+        if (oy < Ho && ox < Wo)
+          *(u32x4*)(y + (((size_t)n * Ho + oy) * Wo + ox) * Cy + c0 + v * VE) = *(const u32x4*)(so + p * rs + v * 16);
+      }
+    } else {
+      const int total = TH * TW * cb;
+#pragma unroll 1
+  for (int i = threadIdx.x; i < total; i += kThreads) {
+        const int c = i % cb, p = i / cb;
+        const int ty = p / TW, tx = p - ty * TW;
+        const int oy = oy0 + ty, ox = ox0 + tx;
+        if (oy < Ho && ox < Wo) y[(((size_t)n * Ho + oy) * Wo + ox) * Cy + c0 + c] = *(const T*)(so + p * rs + c * DT::ELT);
+      }
+    }
+  } else {
+    const int total = cb * TH * TW;
+#pragma unroll 1
+  for (int i = threadIdx.x; i < total; i += kThreads) {
+      const int tx = i % TW;
+      const int t = i / TW;
+      const int ty = t % TH, c = t / TH;
+      const int oy = oy0 + ty, ox = ox0 + tx;
+      if (oy < Ho && ox < Wo)
+        y[(((size_t)n * Cy + c0 + c) * Ho + oy) * Wo + ox] = *(const T*)(so + (ty * TW + tx) * rs + c * DT::ELT);
+    }
+  }
+}
+
+// Workgroup id -> logical tile id such that consecutive logical ids land on the same XCD
+// (workgroups are dispatched round-robin over the 8 XCDs, each with its own L2), so the
+// output-channel blocks of one spatial tile and its neighbours share an L2.
+__device__ __forceinline__ int xcd_remap(int b, int G) {
+  const int q = G / kNumXcd, r = G % kNumXcd;
+  const int x = b % kNumXcd;
+  return x * q + (x < r ? x : r) + b / kNumXcd;
+}
+
+}  // namespace fcm

@@ -1,0 +1,37 @@
+// fcm_host.h -- host-side internals shared by the planner and the C ABI.
+#pragma once
+
+#include <string>
+
+#include "../../include/fcm.h"
+#include "fcm_internal.h"
+
+namespace fcm {
+
+// Record a failure message for fcm_last_error() and return the status.
+fcm_status fail(fcm_status st, const std::string& msg);
+
+// Argument checks common to fcm_plan and every launch entry point.
+fcm_status validate(int op, const fcm_desc* d);
+
+// Geometry derived from a descriptor for one module.
+struct Geom {
+  int op, family;
+  int n, h, w;          // input
+  int ci, cm, co;       // input / intermediate / output channels of the module
+  int k, s, pad;        // depthwise (1, 1, 0 for the pointwise layer)
+  int ho, wo;           // output
+  int dtype, elt;
+};
+Geom geometry(int op, const fcm_desc* d);
+
+// Fill every derived field of a plan whose op/tile/c_block/co_block/variant are set.
+// Returns FCM_EUNSUPPORTED if the variant cannot implement the tiling.
+fcm_status evaluate_plan(const Geom& g, const fcm_desc* d, const fcm_hw_desc& hw, fcm_plan_t* p);
+
+// Search (cached). plan_out is fully filled on success.
+fcm_status find_plan(int op, const fcm_desc* d, const fcm_hw_desc* hw, fcm_plan_t* plan_out);
+
+fcm_hw_desc default_hw();
+
+}  // namespace fcm

@@ -1,0 +1,204 @@
+// fcm_internal.h -- definitions shared by the host library (planner, C ABI) and the
+// kernels: kernel argument blocks, the LDS layout of each kernel family, and the table
+// of compiled kernel variants.
+#pragma once
+
+#include <stdint.h>
+#include <type_traits>
+
+#ifdef __HIPCC__
+#define FCM_HD __host__ __device__
+#else
+#define FCM_HD
+#endif
+
+namespace fcm {
+
+constexpr int kNumXcd = 8;
+constexpr int kMaxLdsPerWg = 160 * 1024;
+
+enum { LAYOUT_NCHW = 0, LAYOUT_NHWC = 1 };
+enum { ACT_NONE = 0, ACT_RELU = 1, ACT_RELU6 = 2 };
+enum { DT_F32 = 0, DT_BF16 = 1, DT_I8 = 2 };
+
+// Kernel families. A "variant" is one compiled instance of a family.
+enum Family {
+  FAM_DWPW = 0,    // DW -> PW (fused)
+  FAM_PW = 1,      // PW alone (family DWPW with the DW stage off)
+  FAM_PWDW = 2,    // PW -> DW (fused, halo recomputed)
+  FAM_DW = 3,      // DW alone (family PWDW with the PW stage off)
+  FAM_PWDWPW = 4,  // PW -> DW -> PW (fused)
+};
+
+struct Requant {
+  int32_t mult, shift, qmin, qmax;
+};
+
+FCM_HD inline int elt_size(int dt) { return dt == DT_F32 ? 4 : (dt == DT_BF16 ? 2 : 1); }
+// contraction elements per MFMA operand step (64 bytes of k per row)
+FCM_HD inline int k_block(int dt) { return 64 / elt_size(dt); }
+FCM_HD inline int round_up(int a, int b) { return (a + b - 1) / b * b; }
+FCM_HD inline int ceil_div(int a, int b) { return (a + b - 1) / b; }
+
+// ---------------------------------------------------------------------------------
+// LDS layout: byte offsets of each buffer and row strides. Rows are padded by 16 bytes
+// so that the 16 lanes reading one MFMA operand column hit distinct banks.
+// ---------------------------------------------------------------------------------
+struct LdsLayout {
+  int off_in, ps_in;    // staged input window (pixel stride)
+  int off_w, rs_w;      // first pointwise weight block
+  int off_wd;           // depthwise weights [K*K][cb] + bias [cb] (4-byte values)
+  int off_e, rs_e;      // intermediate (PW output over the halo window) [Q][mb]
+  int off_d, rs_d;      // depthwise output [P][cb]
+  int off_w2, rs_w2;    // second pointwise weight block
+  int off_out, rs_out;  // output tile [P][cob]
+  int bytes;
+};
+
+// DW->PW (has_dw) and PW alone. Tile TH x TW output pixels, contraction chunk CB,
+// output-channel block COB.
+FCM_HD inline LdsLayout lds_layout_dwpw(int dt, int K, int S, bool has_dw, int TH, int TW, int CB, int COB) {
+  LdsLayout L = {};
+  const int e = elt_size(dt);
+  const int P = TH * TW, P16 = round_up(P, 16);
+  const int IH = has_dw ? (TH - 1) * S + K : TH, IW = has_dw ? (TW - 1) * S + K : TW;
+  int rows_in = IH * IW;
+  if (!has_dw && rows_in < P16) rows_in = P16;
+  L.ps_in = CB * e + 16;
+  L.off_in = 0;
+  int off = rows_in * L.ps_in;
+  if (has_dw) {
+    L.rs_d = CB * e + 16;
+    L.off_d = off;
+    off += P16 * L.rs_d;
+  }
+  L.rs_w = CB * e + 16;
+  L.off_w = off;
+  off += round_up(COB, 16) * L.rs_w;
+  if (has_dw) {
+    L.off_wd = off;
+    off += (K * K + 1) * CB * 4;
+  }
+  L.rs_out = COB * e + 16;
+  L.off_out = 0;
+  const int out_bytes = P16 * L.rs_out;
+  L.bytes = round_up(off > out_bytes ? off : out_bytes, 16);
+  return L;
+}
+
+// PW->DW (has_pw) and DW alone. Tile TH x TW outputs; Q = haloed window positions;
+// CB = input-channel chunk of the PW contraction; MB = intermediate-channel block.
+FCM_HD inline LdsLayout lds_layout_pwdw(int dt, int K, int S, bool has_pw, int TH, int TW, int CB, int MB) {
+  LdsLayout L = {};
+  const int e = elt_size(dt);
+  const int P16 = round_up(TH * TW, 16);
+  const int IH = (TH - 1) * S + K, IW = (TW - 1) * S + K;
+  const int Q16 = round_up(IH * IW, 16);
+  int off = 0;
+  L.rs_e = MB * e + 16;
+  L.off_e = 0;
+  off = Q16 * L.rs_e;
+  if (has_pw) {
+    L.ps_in = CB * e + 16;
+    L.off_in = off;
+    off += Q16 * L.ps_in;
+    L.rs_w = CB * e + 16;
+    L.off_w = off;
+    off += round_up(MB, 16) * L.rs_w;
+  } else {
+    L.ps_in = L.rs_e;
+    L.off_in = L.off_e;
+  }
+  L.off_wd = off;
+  off += (K * K + 1) * MB * 4;
+  L.rs_out = MB * e + 16;
+  L.off_out = off;
+  off += P16 * L.rs_out;
+  L.bytes = round_up(off, 16);
+  return L;
+}
+
+// PW->DW->PW. Whole input channel range CIN staged once (padded to the MFMA step),
+// intermediate chunk MB, output-channel block COB.
+FCM_HD inline LdsLayout lds_layout_pwdwpw(int dt, int K, int S, int TH, int TW, int CIN, int MB, int COB) {
+  LdsLayout L = {};
+  const int e = elt_size(dt);
+  const int P16 = round_up(TH * TW, 16);
+  const int IH = (TH - 1) * S + K, IW = (TW - 1) * S + K;
+  const int Q16 = round_up(IH * IW, 16);
+  const int CIP = round_up(CIN, k_block(dt));
+  int off = 0;
+  L.ps_in = CIP * e + 16;
+  L.off_in = off;
+  off += Q16 * L.ps_in;
+  L.rs_w = CIP * e + 16;
+  L.off_w = off;
+  off += round_up(MB, 16) * L.rs_w;
+  L.rs_e = MB * e + 16;
+  L.off_e = off;
+  off += Q16 * L.rs_e;
+  L.off_wd = off;
+  off += (K * K + 1) * MB * 4;
+  L.rs_d = MB * e + 16;
+  L.off_d = off;
+  off += P16 * L.rs_d;
+  L.rs_w2 = MB * e + 16;
+  L.off_w2 = off;
+  off += round_up(COB, 16) * L.rs_w2;
+  L.rs_out = COB * e + 16;
+  L.off_out = 0;
+  const int out_bytes = P16 * L.rs_out;
+  L.bytes = round_up(off > out_bytes ? off : out_bytes, 16);
+  return L;
+}
+
+// ---------------------------------------------------------------------------------
+// Kernel argument block (one struct for all families; unused fields ignored).
+// ---------------------------------------------------------------------------------
+struct KArgs {
+  const void* x;
+  const void* w1;  // first conv weights  (dwpw/dw: depthwise; pw, pwdw, pwdwpw: pointwise)
+  const void* b1;
+  const void* w2;  // second conv weights (dwpw: pointwise; pwdw, pwdwpw: depthwise)
+  const void* b2;
+  const void* w3;  // third conv weights  (pwdwpw: pointwise)
+  const void* b3;
+  void* y;
+  int N, H, W;        // input
+  int Ci, Cm, Co;     // channels: input, intermediate, output
+  int Ho, Wo, pad;
+  int layout;
+  int TH, TW, CB, COB;  // tile, contraction chunk, channel block (see fcm_plan_t)
+  int tiles_y, tiles_x, n_cb;  // grid decomposition: N x tiles_y x tiles_x x n_cb
+  int act[3];
+  Requant rq[3];
+  int vec_x, vec_w1, vec_w2, vec_w3, vec_y;
+  LdsLayout L;
+};
+
+// One compiled kernel instance and the tilings it implements.
+typedef int (*LaunchFn)(const KArgs& a, int grid, void* stream);
+
+struct Variant {
+  int family;
+  int dtype;
+  int k, stride;    // depthwise geometry (1, 1 for the pointwise-only family)
+  int max_p;        // output pixels per tile (TH*TW), 0 = bounded by LDS only
+  int max_q;        // haloed input-window positions per tile, 0 = bounded by LDS only
+  int max_cob;      // channel block of the last convolution (COB / depthwise channel block)
+  int max_mb;       // intermediate-channel chunk (PW->DW->PW only), else 0
+  int dw_r;         // output pixels per depthwise thread (TW must be a multiple), 0 = no DW
+  LaunchFn launch;
+  const char* name;
+};
+
+// Compiled variants of each translation unit, and all of them in a fixed order
+// (the index in that order is the plan's `variant`).
+const Variant* variants_dwpw_f32(int* count);
+const Variant* variants_dwpw_bf16(int* count);
+const Variant* variants_dwpw_i8(int* count);
+const Variant* variants_pwdw(int* count);
+const Variant* variants_pwdwpw(int* count);
+const Variant* all_variants(int* count);
+
+}  // namespace fcm

@@ -1,0 +1,277 @@
+// fcm_kernels.h -- the three kernel families and their host launchers (gfx950).
+//
+//   k_dwpw    DW -> PW module (Sec. III "DWPW") and, with the DW stage off, the
+//             layer-by-layer PW kernel. Workgroup = (image, spatial tile, output-channel
+//             block). For each input-channel chunk: stage the haloed input window, run the
+//             depthwise stencil into an LDS tile, contract it with the pointwise weights on
+//             MFMA; the accumulators stay in registers across chunks (output-stationary,
+//             Sec. III-A OS-LWS), and only the final output is written.
+//   k_pwdw    PW -> DW module (Sec. III "PWDW"/"PWDW_R") and, with the PW stage off, the
+//             layer-by-layer DW kernel. Workgroup = (image, spatial tile, intermediate-
+//             channel block). The PW is evaluated on the whole haloed window, so halo
+//             positions are recomputed by neighbouring tiles (Sec. II-D); positions outside
+//             the image are zero, being the DW's zero padding.
+//   k_pwdwpw  PW -> DW -> PW inverted residual in one kernel. Workgroup = (image, spatial
+//             tile, output-channel block). The input window is staged once; the
+//             intermediate channels stream through LDS in chunks, each chunk being expanded
+//             (MFMA), filtered (DW) and projected (MFMA) into output accumulators that stay
+//             in registers.
+#pragma once
+
+#include "fcm_device.h"
+
+namespace fcm {
+
+template <class DT, int K, int S, bool HAS_DW, int PMAX, int MMAX, int WM, int R>
+__global__ __launch_bounds__(kThreads) void k_dwpw(KArgs a) {
+  extern __shared__ __align__(16) char smem[];
+  using T = typename DT::T;
+  using Acc = typename DT::Acc;
+  using AccV = typename DT::AccV;
+  constexpr int WN = 4 / WM;
+  constexpr int TMW = MMAX / 16 / WM;
+  constexpr int TNW = PMAX / 16 / WN;
+  static_assert(TMW * WM * 16 == MMAX && TNW * WN * 16 == PMAX, "wave tiling");
+  const LdsLayout& L = a.L;
+
+  const int G = a.N * a.tiles_y * a.tiles_x * a.n_cb;
+  const int lid = xcd_remap(blockIdx.x, G);
+  const int cob = lid % a.n_cb;
+  int t = lid / a.n_cb;
+  const int tx = t % a.tiles_x;
+  t /= a.tiles_x;
+  const int ty = t % a.tiles_y, n = t / a.tiles_y;
+
+  const int oy0 = ty * a.TH, ox0 = tx * a.TW;
+  const int iy0 = HAS_DW ? oy0 * S - a.pad : oy0;
+  const int ix0 = HAS_DW ? ox0 * S - a.pad : ox0;
+  const int IH = HAS_DW ? (a.TH - 1) * S + K : a.TH;
+  const int IW = HAS_DW ? (a.TW - 1) * S + K : a.TW;
+  const int co0 = cob * a.COB;
+  const int cob_eff = min(a.COB, a.Co - co0);
+
+  const int wave = threadIdx.x >> 6, wm = wave / WN, wn = wave % WN;
+  const int m_tiles = ceil_div(cob_eff, 16), n_tiles = ceil_div(a.TH * a.TW, 16);
+  const int m_act = max(0, min(TMW, m_tiles - wm * TMW));
+  const int n_act = max(0, min(TNW, n_tiles - wn * TNW));
+
+  const T* x = (const T*)a.x;
+  const T* wd = (const T*)a.w1;
+  const T* wp = (const T*)(HAS_DW ? a.w2 : a.w1);
+  const void* bp = HAS_DW ? a.b2 : a.b1;
+  const int act_pw = HAS_DW ? a.act[1] : a.act[0];
+  const Requant rq_pw = HAS_DW ? a.rq[1] : a.rq[0];
+  const bool vec_wp = HAS_DW ? a.vec_w2 : a.vec_w1;
+
+  AccV acc[TMW][TNW];
+#pragma unroll
+  for (int i = 0; i < TMW; ++i)
+#pragma unroll
+    for (int j = 0; j < TNW; ++j) acc[i][j] = AccV{0, 0, 0, 0};
+
+  for (int c0 = 0; c0 < a.Ci; c0 += a.CB) {
+    stage_input<DT>(smem + L.off_in, L.ps_in, x, a.layout, n, a.Ci, a.H, a.W, iy0, ix0, IH, IW, c0, a.CB, a.vec_x);
+    stage_rows<DT>(smem + L.off_w, L.rs_w, wp, a.Co, a.Ci, co0, m_tiles * 16, c0, a.CB, vec_wp);
+    if constexpr (HAS_DW) stage_dw_weights<DT, K>((Acc*)(smem + L.off_wd), wd, a.b1, a.Ci, c0, a.CB);
+    __syncthreads();
+    const char* B = smem + L.off_in;
+    int bs = L.ps_in;
+    if constexpr (HAS_DW) {
+      dw_compute<DT, K, S, R>(smem + L.off_in, L.ps_in, IW, (const Acc*)(smem + L.off_wd), a.CB, a.TH, a.TW,
+                              a.act[0], a.rq[0], smem + L.off_d, L.rs_d);
+      __syncthreads();
+      B = smem + L.off_d;
+      bs = L.rs_d;
+    }
+    mma_chunk<DT, TMW, TNW>(acc, smem + L.off_w, L.rs_w, B, bs, a.CB, wm * TMW * 16, wn * TNW * 16, m_act, n_act);
+    __syncthreads();
+  }
+
+  acc_to_lds<DT, TMW, TNW>(acc, wm * TMW * 16, wn * TNW * 16, m_act, n_act, bp, co0, cob_eff, act_pw, rq_pw,
+                           smem + L.off_out, L.rs_out, 0, 0, 0, 0, 0);
+  __syncthreads();
+  store_tile<DT>(smem + L.off_out, L.rs_out, (T*)a.y, a.layout, n, a.Co, a.Ho, a.Wo, oy0, ox0, a.TH, a.TW, co0,
+                 cob_eff, a.vec_y && ((cob_eff * DT::ELT) % 16 == 0));
+}
+
+template <class DT, int K, int S, bool HAS_PW, int QMAX, int MMAX, int WM, int R>
+__global__ __launch_bounds__(kThreads) void k_pwdw(KArgs a) {
+  extern __shared__ __align__(16) char smem[];
+  using T = typename DT::T;
+  using Acc = typename DT::Acc;
+  using AccV = typename DT::AccV;
+  const LdsLayout& L = a.L;
+
+  const int G = a.N * a.tiles_y * a.tiles_x * a.n_cb;
+  const int lid = xcd_remap(blockIdx.x, G);
+  const int mb = lid % a.n_cb;
+  int t = lid / a.n_cb;
+  const int tx = t % a.tiles_x;
+  t /= a.tiles_x;
+  const int ty = t % a.tiles_y, n = t / a.tiles_y;
+
+  const int oy0 = ty * a.TH, ox0 = tx * a.TW;
+  const int iy0 = oy0 * S - a.pad, ix0 = ox0 * S - a.pad;
+  const int IH = (a.TH - 1) * S + K, IW = (a.TW - 1) * S + K;
+  const int MB = a.COB;
+  const int m0 = mb * MB;
+  const int mb_eff = min(MB, a.Cm - m0);
+  const T* x = (const T*)a.x;
+
+  if constexpr (HAS_PW) {
+    constexpr int WN = 4 / WM;
+    constexpr int TMW = MMAX / 16 / WM;
+    constexpr int TNW = QMAX / 16 / WN;
+    static_assert(TMW * WM * 16 == MMAX && TNW * WN * 16 == QMAX, "wave tiling");
+    const int wave = threadIdx.x >> 6, wm = wave / WN, wn = wave % WN;
+    const int m_tiles = ceil_div(mb_eff, 16), q_tiles = ceil_div(IH * IW, 16);
+    const int m_act = max(0, min(TMW, m_tiles - wm * TMW));
+    const int n_act = max(0, min(TNW, q_tiles - wn * TNW));
+    AccV acc[TMW][TNW];
+#pragma unroll
+    for (int i = 0; i < TMW; ++i)
+#pragma unroll
+      for (int j = 0; j < TNW; ++j) acc[i][j] = AccV{0, 0, 0, 0};
+    for (int c0 = 0; c0 < a.Ci; c0 += a.CB) {
+      stage_input<DT>(smem + L.off_in, L.ps_in, x, a.layout, n, a.Ci, a.H, a.W, iy0, ix0, IH, IW, c0, a.CB,
+                      a.vec_x);
+      stage_rows<DT>(smem + L.off_w, L.rs_w, (const T*)a.w1, a.Cm, a.Ci, m0, m_tiles * 16, c0, a.CB, a.vec_w1);
+      __syncthreads();
+      mma_chunk<DT, TMW, TNW>(acc, smem + L.off_w, L.rs_w, smem + L.off_in, L.ps_in, a.CB, wm * TMW * 16,
+                              wn * TNW * 16, m_act, n_act);
+      __syncthreads();
+    }
+    // PW output over the haloed window -> E [Q][MB]; zero outside the image.
+    acc_to_lds<DT, TMW, TNW>(acc, wm * TMW * 16, wn * TNW * 16, m_act, n_act, a.b1, m0, mb_eff, a.act[0], a.rq[0],
+                             smem + L.off_e, L.rs_e, IW, iy0, ix0, a.H, a.W);
+    stage_dw_weights<DT, K>((Acc*)(smem + L.off_wd), (const T*)a.w2, a.b2, a.Cm, m0, MB);
+  } else {
+    stage_input<DT>(smem + L.off_e, L.rs_e, x, a.layout, n, a.Cm, a.H, a.W, iy0, ix0, IH, IW, m0, MB, a.vec_x);
+    stage_dw_weights<DT, K>((Acc*)(smem + L.off_wd), (const T*)a.w1, a.b1, a.Cm, m0, MB);
+  }
+  __syncthreads();
+  const int act_dw = HAS_PW ? a.act[1] : a.act[0];
+  const Requant rq_dw = HAS_PW ? a.rq[1] : a.rq[0];
+  dw_compute<DT, K, S, R>(smem + L.off_e, L.rs_e, IW, (const Acc*)(smem + L.off_wd), MB, a.TH, a.TW, act_dw, rq_dw,
+                          smem + L.off_out, L.rs_out);
+  __syncthreads();
+  store_tile<DT>(smem + L.off_out, L.rs_out, (T*)a.y, a.layout, n, a.Cm, a.Ho, a.Wo, oy0, ox0, a.TH, a.TW, m0, mb_eff,
+                 a.vec_y && ((mb_eff * DT::ELT) % 16 == 0));
+}
+
+template <class DT, int K, int S, int QMAX, int MBMAX, int WM1, int OMAX, int PMAX, int WM2, int R>
+__global__ __launch_bounds__(kThreads) void k_pwdwpw(KArgs a) {
+  extern __shared__ __align__(16) char smem[];
+  using T = typename DT::T;
+  using Acc = typename DT::Acc;
+  using AccV = typename DT::AccV;
+  constexpr int WN1 = 4 / WM1, TMW1 = MBMAX / 16 / WM1, TNW1 = QMAX / 16 / WN1;
+  constexpr int WN2 = 4 / WM2, TMW2 = OMAX / 16 / WM2, TNW2 = PMAX / 16 / WN2;
+  static_assert(TMW1 * WM1 * 16 == MBMAX && TNW1 * WN1 * 16 == QMAX, "wave tiling 1");
+  static_assert(TMW2 * WM2 * 16 == OMAX && TNW2 * WN2 * 16 == PMAX, "wave tiling 2");
+  const LdsLayout& L = a.L;
+
+  const int G = a.N * a.tiles_y * a.tiles_x * a.n_cb;
+  const int lid = xcd_remap(blockIdx.x, G);
+  const int cob = lid % a.n_cb;
+  int t = lid / a.n_cb;
+  const int tx = t % a.tiles_x;
+  t /= a.tiles_x;
+  const int ty = t % a.tiles_y, n = t / a.tiles_y;
+
+  const int oy0 = ty * a.TH, ox0 = tx * a.TW;
+  const int iy0 = oy0 * S - a.pad, ix0 = ox0 * S - a.pad;
+  const int IH = (a.TH - 1) * S + K, IW = (a.TW - 1) * S + K;
+  const int CIP = round_up(a.Ci, DT::KB);
+  const int MB = a.CB;  // intermediate chunk
+  const int co0 = cob * a.COB, cob_eff = min(a.COB, a.Co - co0);
+
+  const int wave = threadIdx.x >> 6;
+  const int wm1 = wave / WN1, wn1 = wave % WN1, wm2 = wave / WN2, wn2 = wave % WN2;
+  const int q_tiles = ceil_div(IH * IW, 16), p_tiles = ceil_div(a.TH * a.TW, 16);
+  const int o_tiles = ceil_div(cob_eff, 16);
+  const int n_act1 = max(0, min(TNW1, q_tiles - wn1 * TNW1));
+  const int m_act2 = max(0, min(TMW2, o_tiles - wm2 * TMW2));
+  const int n_act2 = max(0, min(TNW2, p_tiles - wn2 * TNW2));
+
+  const T* x = (const T*)a.x;
+  stage_input<DT>(smem + L.off_in, L.ps_in, x, a.layout, n, a.Ci, a.H, a.W, iy0, ix0, IH, IW, 0, CIP, a.vec_x);
+
+  AccV acc2[TMW2][TNW2];
+#pragma unroll
+  for (int i = 0; i < TMW2; ++i)
+#pragma unroll
+    for (int j = 0; j < TNW2; ++j) acc2[i][j] = AccV{0, 0, 0, 0};
+
+  for (int m0 = 0; m0 < a.Cm; m0 += MB) {
+    const int mb_eff = min(MB, a.Cm - m0);
+    const int m_tiles = ceil_div(mb_eff, 16);
+    const int m_act1 = max(0, min(TMW1, m_tiles - wm1 * TMW1));
+    stage_rows<DT>(smem + L.off_w, L.rs_w, (const T*)a.w1, a.Cm, a.Ci, m0, m_tiles * 16, 0, CIP, a.vec_w1);
+    stage_dw_weights<DT, K>((Acc*)(smem + L.off_wd), (const T*)a.w2, a.b2, a.Cm, m0, MB);
+    stage_rows<DT>(smem + L.off_w2, L.rs_w2, (const T*)a.w3, a.Co, a.Cm, co0, o_tiles * 16, m0, MB, a.vec_w3);
+    __syncthreads();
+    {
+      AccV acc1[TMW1][TNW1];
+#pragma unroll
+      for (int i = 0; i < TMW1; ++i)
+#pragma unroll
+        for (int j = 0; j < TNW1; ++j) acc1[i][j] = AccV{0, 0, 0, 0};
+      mma_chunk<DT, TMW1, TNW1>(acc1, smem + L.off_w, L.rs_w, smem + L.off_in, L.ps_in, CIP, wm1 * TMW1 * 16,
+                                wn1 * TNW1 * 16, m_act1, n_act1);
+      // Every channel of the chunk is written (zeros beyond mb_eff), so the DW and the
+      // projection below never read uninitialised LDS.
+      const int m_wr1 = max(0, min(TMW1, MB / 16 - wm1 * TMW1));
+      acc_to_lds<DT, TMW1, TNW1>(acc1, wm1 * TMW1 * 16, wn1 * TNW1 * 16, m_wr1, n_act1, a.b1, m0, mb_eff, a.act[0],
+                                 a.rq[0], smem + L.off_e, L.rs_e, IW, iy0, ix0, a.H, a.W);
+    }
+    __syncthreads();
+    dw_compute<DT, K, S, R>(smem + L.off_e, L.rs_e, IW, (const Acc*)(smem + L.off_wd), MB, a.TH, a.TW, a.act[1],
+                            a.rq[1], smem + L.off_d, L.rs_d);
+    __syncthreads();
+    mma_chunk<DT, TMW2, TNW2>(acc2, smem + L.off_w2, L.rs_w2, smem + L.off_d, L.rs_d, MB, wm2 * TMW2 * 16,
+                              wn2 * TNW2 * 16, m_act2, n_act2);
+    __syncthreads();
+  }
+
+  acc_to_lds<DT, TMW2, TNW2>(acc2, wm2 * TMW2 * 16, wn2 * TNW2 * 16, m_act2, n_act2, a.b3, co0, cob_eff, a.act[2],
+                             a.rq[2], smem + L.off_out, L.rs_out, 0, 0, 0, 0, 0);
+  __syncthreads();
+  store_tile<DT>(smem + L.off_out, L.rs_out, (T*)a.y, a.layout, n, a.Co, a.Ho, a.Wo, oy0, ox0, a.TH, a.TW, co0,
+                 cob_eff, a.vec_y && ((cob_eff * DT::ELT) % 16 == 0));
+}
+
+// ------------------------------------------------------------------------------------
+// Host launchers
+// ------------------------------------------------------------------------------------
+template <class Kern>
+inline int launch_kernel(Kern fn, const KArgs& a, int grid, void* stream) {
+  if (a.L.bytes > 65536) {
+    hipError_t e = hipFuncSetAttribute((const void*)fn, hipFuncAttributeMaxDynamicSharedMemorySize, a.L.bytes);
+    if (e != hipSuccess) return (int)e;
+  }
+  hipLaunchKernelGGL(fn, dim3(grid), dim3(kThreads), a.L.bytes, (hipStream_t)stream, a);
+  return (int)hipGetLastError();
+}
+
+template <class DT, int K, int S, bool HAS_DW, int PMAX, int MMAX, int WM, int R>
+int launch_dwpw(const KArgs& a, int grid, void* stream) {
+  return launch_kernel(k_dwpw<DT, K, S, HAS_DW, PMAX, MMAX, WM, R>, a, grid, stream);
+}
+
+template <class DT, int K, int S, bool HAS_PW, int QMAX, int MMAX, int WM, int R>
+int launch_pwdw(const KArgs& a, int grid, void* stream) {
+  return launch_kernel(k_pwdw<DT, K, S, HAS_PW, QMAX, MMAX, WM, R>, a, grid, stream);
+}
+
+template <class DT, int K, int S, int QMAX, int MBMAX, int WM1, int OMAX, int PMAX, int WM2, int R>
+int launch_pwdwpw(const KArgs& a, int grid, void* stream) {
+  return launch_kernel(k_pwdwpw<DT, K, S, QMAX, MBMAX, WM1, OMAX, PMAX, WM2, R>, a, grid, stream);
+}
+
+template <class DT>
+constexpr int dtype_id() {
+  return std::is_same<DT, TF32>::value ? DT_F32 : (std::is_same<DT, TBF16>::value ? DT_BF16 : DT_I8);
+}
+
+}  // namespace fcm

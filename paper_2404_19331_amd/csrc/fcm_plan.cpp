@@ -1,0 +1,406 @@
+// fcm_plan.cpp -- FusePlanner for CDNA4 (arXiv 2404.19331, Sec. IV).
+//
+// For a module and a tiling, three global-memory figures are computed:
+//   * bytes_ideal: what the module must move at least (input + weights + output once);
+//   * bytes_tiled: what the tiled kernel loads and stores, workgroup by workgroup: the
+//     haloed input window of every workgroup clipped at the image border, the weight
+//     blocks each workgroup stages, and each output once. This is exact for the kernels
+//     in this library (sums of per-axis clipped extents);
+//   * bytes_paper: the paper's closed-form estimate: Eq. 1 (overlap), Eq. 2 (PW),
+//     Eq. 3 (DW), Eq. 4 (PW->DW) and the DW->PW / PW->DW->PW estimates built the same
+//     way (Sec. IV-B says the other modules follow the same construction).
+// The search enumerates the tilings the compiled kernels implement, keeps those whose
+// LDS footprint fits a workgroup (the paper's "tiles fit in L1/shared memory"
+// constraint), prefers tilings with at least one workgroup per CU (the paper's
+// "#tiles >= #SMs"), and minimises bytes_tiled. The fuse verdict compares the module's
+// estimate with the layer-by-layer chain's (Sec. IV-B: fuse when the fused estimate is
+// lower).
+#include <algorithm>
+#include <cstdlib>
+#include <cstring>
+#include <map>
+#include <mutex>
+#include <tuple>
+#include <vector>
+
+#include "fcm_host.h"
+
+namespace fcm {
+
+fcm_hw_desc default_hw() {
+  fcm_hw_desc hw;
+  hw.num_cus = 256;
+  hw.num_xcds = 8;
+  hw.wave_size = 64;
+  hw.lds_per_wg = kMaxLdsPerWg;
+  hw.lds_per_cu = kMaxLdsPerWg;
+  hw.l2_per_xcd = 4ll << 20;
+  hw.mall_bytes = 256ll << 20;
+  hw.hbm_bytes_per_s = 8.0e12;
+  return hw;
+}
+
+static int out_dim(int x, int k, int s, int p) { return (x + 2 * p - k) / s + 1; }
+
+Geom geometry(int op, const fcm_desc* d) {
+  Geom g = {};
+  g.op = op;
+  g.n = d->n;
+  g.h = d->h;
+  g.w = d->w;
+  g.dtype = d->dtype;
+  g.elt = elt_size(d->dtype);
+  g.k = d->k;
+  g.s = d->stride;
+  g.pad = d->pad;
+  switch (op) {
+    case FCM_OP_DW_PW: g.family = FAM_DWPW; g.ci = d->c_in; g.cm = d->c_in; g.co = d->c_out; break;
+    case FCM_OP_PW_DW: g.family = FAM_PWDW; g.ci = d->c_in; g.cm = d->c_mid; g.co = d->c_mid; break;
+    case FCM_OP_PW_DW_PW: g.family = FAM_PWDWPW; g.ci = d->c_in; g.cm = d->c_mid; g.co = d->c_out; break;
+    case FCM_OP_DW: g.family = FAM_DW; g.ci = d->c_in; g.cm = d->c_in; g.co = d->c_in; break;
+    default: g.family = FAM_PW; g.ci = d->c_in; g.cm = d->c_in; g.co = d->c_out; g.k = 1; g.s = 1; g.pad = 0; break;
+  }
+  g.ho = out_dim(g.h, g.k, g.s, g.pad);
+  g.wo = out_dim(g.w, g.k, g.s, g.pad);
+  return g;
+}
+
+// Sum over tiles t of |[t*T*S - P, t*T*S - P + (T-1)*S + K) intersected with [0, X)|:
+// the input rows (or columns) staged by all tiles along one axis.
+static int64_t staged_extent_sum(int X, int XO, int T, int K, int S, int P) {
+  const int nt = ceil_div(XO, T);
+  const int ext = (T - 1) * S + K;
+  int64_t sum = 0;
+  for (int t = 0; t < nt; ++t) {
+    const int lo = std::max(0, t * T * S - P), hi = std::min(X, t * T * S - P + ext);
+    if (hi > lo) sum += hi - lo;
+  }
+  return sum;
+}
+
+// Eq. 1 overlap, in elements per channel (and per image): (tiles_w - 1)(K - S) H +
+// (tiles_h - 1)(K - S) W; number of tiles along an axis = tiles covering the output.
+static int64_t eq1_overlap(int H, int W, int nty, int ntx, int K, int S) {
+  return (int64_t)(ntx - 1) * (K - S) * H + (int64_t)(nty - 1) * (K - S) * W;
+}
+
+struct Bytes {
+  int64_t ideal, tiled, paper;
+  double redundancy;
+};
+
+static Bytes module_bytes(const Geom& g, int TH, int TW, int COB) {
+  const int64_t e = g.elt, N = g.n;
+  const int nty = ceil_div(g.ho, TH), ntx = ceil_div(g.wo, TW);
+  const int64_t T = N * nty * ntx;  // spatial tiles
+  const int64_t SR = staged_extent_sum(g.h, g.ho, TH, g.k, g.s, g.pad);
+  const int64_t SC = staged_extent_sum(g.w, g.wo, TW, g.k, g.s, g.pad);
+  const int64_t staged = N * SR * SC;  // staged input positions over all spatial tiles
+  const int64_t x_el = N * g.h * g.w * (int64_t)g.ci;
+  const int64_t kk = (int64_t)g.k * g.k;
+  const int64_t ovl = N * eq1_overlap(g.h, g.w, nty, ntx, g.k, g.s);
+  Bytes b = {};
+  switch (g.family) {
+    case FAM_DWPW: {
+      const int64_t ncb = ceil_div(g.co, COB);
+      const int64_t y_el = N * g.ho * (int64_t)g.wo * g.co;
+      b.ideal = (x_el + g.ci * kk + (int64_t)g.co * g.ci + y_el) * e;
+      b.tiled = (ncb * staged * g.ci + T * (int64_t)g.co * g.ci + T * ncb * g.ci * kk + y_el) * e;
+      b.paper = ((2 * g.ci * ovl + x_el) * ncb + T * (int64_t)g.co * g.ci + T * ncb * g.ci * kk + y_el) * e;
+      break;
+    }
+    case FAM_PW: {
+      const int64_t ncb = ceil_div(g.co, COB);
+      const int64_t y_el = N * g.h * (int64_t)g.w * g.co;
+      b.ideal = (x_el + (int64_t)g.co * g.ci + y_el) * e;
+      b.tiled = (ncb * staged * g.ci + T * (int64_t)g.co * g.ci + y_el) * e;
+      // Eq. 2 (weight term counted per spatial tile)
+      b.paper = (ncb * x_el + y_el + T * (int64_t)g.co * g.ci) * e;
+      break;
+    }
+    case FAM_DW: {
+      const int64_t y_el = N * g.ho * (int64_t)g.wo * g.ci;
+      b.ideal = (x_el + g.ci * kk + y_el) * e;
+      b.tiled = (staged * g.ci + T * g.ci * kk + y_el) * e;
+      // Eq. 3
+      b.paper = (2 * g.ci * ovl + x_el + y_el + T * g.ci * kk) * e;
+      break;
+    }
+    case FAM_PWDW: {
+      const int64_t nmb = ceil_div(g.cm, COB);
+      const int64_t y_el = N * g.ho * (int64_t)g.wo * g.cm;
+      b.ideal = (x_el + (int64_t)g.cm * g.ci + g.cm * kk + y_el) * e;
+      b.tiled = (nmb * staged * g.ci + T * ((int64_t)g.cm * g.ci + g.cm * kk) + y_el) * e;
+      // Eq. 4 (+ output write); both weight-tile counts are the mid-channel blocks
+      b.paper = ((2 * g.ci * ovl + x_el) * nmb + T * (int64_t)g.cm * g.ci + T * g.cm * kk + y_el) * e;
+      b.redundancy = (double)(SR * SC) / ((double)g.h * g.w) - 1.0;
+      break;
+    }
+    case FAM_PWDWPW: {
+      const int64_t ncb = ceil_div(g.co, COB);
+      const int64_t y_el = N * g.ho * (int64_t)g.wo * g.co;
+      b.ideal = (x_el + (int64_t)g.cm * g.ci + g.cm * kk + (int64_t)g.co * g.cm + y_el) * e;
+      b.tiled = (ncb * staged * g.ci + T * ncb * ((int64_t)g.cm * g.ci + g.cm * kk) + T * (int64_t)g.co * g.cm +
+                 y_el) * e;
+      b.paper = ((2 * g.ci * ovl + x_el) * ncb + T * ncb * ((int64_t)g.cm * g.ci + g.cm * kk) +
+                 T * (int64_t)g.co * g.cm + y_el) * e;
+      b.redundancy = (double)(SR * SC) / ((double)g.h * g.w) - 1.0;
+      break;
+    }
+  }
+  return b;
+}
+
+// LDS bytes of a tiling (0 if the variant cannot implement it).
+static int tiling_lds(const Variant& v, const Geom& g, int TH, int TW, int CB, int COB) {
+  const int kb = k_block(g.dtype);
+  if (TH <= 0 || TW <= 0 || COB <= 0 || COB % 16) return 0;
+  if (v.dw_r && TW % v.dw_r) return 0;
+  if (COB > v.max_cob) return 0;
+  const int P = TH * TW;
+  const int Q = ((TH - 1) * g.s + g.k) * ((TW - 1) * g.s + g.k);
+  if (v.max_p && P > v.max_p) return 0;
+  if (v.max_q && Q > v.max_q) return 0;
+  switch (v.family) {
+    case FAM_DWPW:
+    case FAM_PW:
+      if (CB <= 0 || CB % kb) return 0;
+      return lds_layout_dwpw(g.dtype, g.k, g.s, v.family == FAM_DWPW, TH, TW, CB, COB).bytes;
+    case FAM_PWDW:
+      if (CB <= 0 || CB % kb) return 0;
+      return lds_layout_pwdw(g.dtype, g.k, g.s, true, TH, TW, CB, COB).bytes;
+    case FAM_DW:
+      if (CB != COB) return 0;
+      return lds_layout_pwdw(g.dtype, g.k, g.s, false, TH, TW, CB, COB).bytes;
+    case FAM_PWDWPW:
+      // CB = intermediate chunk: a multiple of both the MFMA M tile and its K step
+      if (CB <= 0 || CB % 16 || CB % kb || CB > v.max_mb) return 0;
+      return lds_layout_pwdwpw(g.dtype, g.k, g.s, TH, TW, g.ci, CB, COB).bytes;
+  }
+  return 0;
+}
+
+static bool variant_matches(const Variant& v, const Geom& g) {
+  if (v.family != g.family || v.dtype != g.dtype) return false;
+  if (g.family == FAM_PW) return true;
+  return v.k == g.k && v.stride == g.s;
+}
+
+fcm_status evaluate_plan(const Geom& g, const fcm_desc* d, const fcm_hw_desc& hw, fcm_plan_t* p) {
+  (void)d;
+  int nv = 0;
+  const Variant* vs = all_variants(&nv);
+  if (p->variant < 0 || p->variant >= nv) return fail(FCM_EUNSUPPORTED, "plan: unknown kernel variant");
+  const Variant& v = vs[p->variant];
+  if (!variant_matches(v, g)) return fail(FCM_EUNSUPPORTED, "plan: kernel variant does not implement this module");
+  const int lds = tiling_lds(v, g, p->tile_h, p->tile_w, p->c_block, p->co_block);
+  if (lds <= 0) return fail(FCM_EUNSUPPORTED, "plan: tiling not implemented by the kernel variant");
+  if (lds > hw.lds_per_wg) return fail(FCM_EUNSUPPORTED, "plan: tiling exceeds the LDS per workgroup");
+  const int nty = ceil_div(g.ho, p->tile_h), ntx = ceil_div(g.wo, p->tile_w);
+  const int last = (g.family == FAM_PWDW || g.family == FAM_DW) ? g.cm : g.co;
+  const int64_t wgs = (int64_t)g.n * nty * ntx * ceil_div(last, p->co_block);
+  if (wgs <= 0 || wgs > 0x7fffffff) return fail(FCM_EUNSUPPORTED, "plan: grid too large");
+  const Bytes b = module_bytes(g, p->tile_h, p->tile_w, p->co_block);
+  p->waves = 4;
+  p->lds_bytes = lds;
+  p->workgroups = (int32_t)wgs;
+  p->bytes_ideal = b.ideal;
+  p->bytes_tiled = b.tiled;
+  p->bytes_paper = b.paper;
+  p->redundancy = b.redundancy;
+  return FCM_OK;
+}
+
+// ---------------------------------------------------------------------------------
+// Search
+// ---------------------------------------------------------------------------------
+
+struct Cand {
+  fcm_plan_t p;
+  int64_t bytes;
+  int wgs;
+  int lds;
+  int area;
+  int cap;  // variant capacity (prefer the smallest that fits)
+};
+
+static std::vector<int> tile_ws(const Variant& v) {
+  if (v.dw_r) return {4, 8, 16, 32};
+  return {1, 2, 4, 7, 8, 14, 16, 28, 32, 56, 64};
+}
+
+static const int kTileH[] = {1, 2, 4, 7, 8, 14, 16, 28, 32};
+
+static fcm_status search(const Geom& g, const fcm_desc* d, const fcm_hw_desc& hw, fcm_plan_t* best_out) {
+  int nv = 0;
+  const Variant* vs = all_variants(&nv);
+  const int kb = k_block(g.dtype);
+  const int last = (g.family == FAM_PWDW || g.family == FAM_DW) ? g.cm : g.co;
+  std::vector<Cand> cands;
+  for (int vi = 0; vi < nv; ++vi) {
+    const Variant& v = vs[vi];
+    if (!variant_matches(v, g)) continue;
+    std::vector<int> cbs;
+    if (v.family == FAM_DW) {
+      cbs = {0};  // CB follows COB
+    } else if (v.family == FAM_PWDWPW) {
+      const int step = std::max(16, kb);
+      for (int c = step; c <= std::min(v.max_mb, round_up(g.cm, step)); c += step) cbs.push_back(c);
+    } else {
+      for (int c = kb; c <= std::min(round_up(g.ci, kb), 8 * kb); c *= 2) cbs.push_back(c);
+      if (round_up(g.ci, kb) < 8 * kb && std::find(cbs.begin(), cbs.end(), round_up(g.ci, kb)) == cbs.end())
+        cbs.push_back(round_up(g.ci, kb));
+    }
+    for (int TW : tile_ws(v)) {
+      if (TW > round_up(g.wo, v.dw_r ? v.dw_r : 1) && TW > 4) continue;
+      for (int TH : kTileH) {
+        if (TH > g.ho && TH > 1) continue;
+        for (int COB = 16; COB <= std::min(v.max_cob, round_up(last, 16)); COB += 16) {
+          for (int cb0 : cbs) {
+            const int CB = v.family == FAM_DW ? COB : cb0;
+            const int lds = tiling_lds(v, g, TH, TW, CB, COB);
+            if (lds <= 0 || lds > hw.lds_per_wg) continue;
+            Cand c;
+            memset(&c.p, 0, sizeof(c.p));
+            c.p.op = g.op;
+            c.p.tile_h = TH;
+            c.p.tile_w = TW;
+            c.p.c_block = CB;
+            c.p.co_block = COB;
+            c.p.variant = vi;
+            if (evaluate_plan(g, d, hw, &c.p) != FCM_OK) continue;
+            c.bytes = c.p.bytes_tiled;
+            c.wgs = c.p.workgroups;
+            c.lds = lds;
+            c.area = TH * TW;
+            c.cap = v.max_cob * 1024 + (v.max_p ? v.max_p : v.max_q);
+            cands.push_back(c);
+          }
+        }
+      }
+    }
+  }
+  if (cands.empty()) return fail(FCM_EUNSUPPORTED, "plan: no compiled kernel implements this shape");
+  bool any_full = false;
+  for (const Cand& c : cands) any_full |= c.wgs >= hw.num_cus;
+  const int target = 2 * hw.num_cus;
+  auto better = [&](const Cand& a, const Cand& b) {
+    // 1. the paper's occupancy constraint (#tiles >= #SMs) where reachable
+    const bool fa = a.wgs >= hw.num_cus, fb = b.wgs >= hw.num_cus;
+    if (any_full && fa != fb) return fa;
+    if (!any_full && a.wgs != b.wgs) return a.wgs > b.wgs;
+    // 2. fewest global bytes
+    if (a.bytes != b.bytes) return a.bytes < b.bytes;
+    // 3. two workgroups fit a CU's LDS
+    const bool ha = 2 * a.lds <= hw.lds_per_cu, hb = 2 * b.lds <= hw.lds_per_cu;
+    if (ha != hb) return ha;
+    // 4. more workgroups, up to two per CU
+    const int wa = std::min(a.wgs, target), wb = std::min(b.wgs, target);
+    if (wa != wb) return wa > wb;
+    // 5. larger tiles, larger channel chunks, smallest kernel capacity, lowest id
+    if (a.area != b.area) return a.area > b.area;
+    if (a.p.c_block != b.p.c_block) return a.p.c_block > b.p.c_block;
+    if (a.cap != b.cap) return a.cap < b.cap;
+    return a.p.variant < b.p.variant;
+  };
+  const Cand* best = &cands[0];
+  for (const Cand& c : cands)
+    if (better(c, *best)) best = &c;
+  *best_out = best->p;
+  return FCM_OK;
+}
+
+// Stage decomposition for the layer-by-layer estimate of a module.
+static void lbl_stages(int op, const fcm_desc* d, std::vector<std::pair<int, fcm_desc>>* out) {
+  fcm_desc s = *d;
+  auto one = [&](int sop, int h, int w, int ci, int co, int stage) {
+    fcm_desc t = *d;
+    t.h = h;
+    t.w = w;
+    t.c_in = ci;
+    t.c_mid = ci;
+    t.c_out = co;
+    t.act[0] = t.act[1] = t.act[2] = d->act[stage];
+    t.rq[0] = t.rq[1] = t.rq[2] = d->rq[stage];
+    if (sop == FCM_OP_PW) {
+      t.k = 1;
+      t.stride = 1;
+      t.pad = 0;
+    }
+    out->push_back({sop, t});
+  };
+  const int ho = out_dim(s.h, s.k, s.stride, s.pad), wo = out_dim(s.w, s.k, s.stride, s.pad);
+  switch (op) {
+    case FCM_OP_DW_PW:
+      one(FCM_OP_DW, s.h, s.w, s.c_in, s.c_in, 0);
+      one(FCM_OP_PW, ho, wo, s.c_in, s.c_out, 1);
+      break;
+    case FCM_OP_PW_DW:
+      one(FCM_OP_PW, s.h, s.w, s.c_in, s.c_mid, 0);
+      one(FCM_OP_DW, s.h, s.w, s.c_mid, s.c_mid, 1);
+      break;
+    case FCM_OP_PW_DW_PW:
+      one(FCM_OP_PW, s.h, s.w, s.c_in, s.c_mid, 0);
+      one(FCM_OP_DW, s.h, s.w, s.c_mid, s.c_mid, 1);
+      one(FCM_OP_PW, ho, wo, s.c_mid, s.c_out, 2);
+      break;
+    default:
+      break;
+  }
+}
+
+static std::mutex g_cache_mu;
+static std::map<std::vector<int64_t>, fcm_plan_t> g_cache;
+
+static std::vector<int64_t> cache_key(int op, const fcm_desc* d, const fcm_hw_desc& hw) {
+  std::vector<int64_t> k = {op, d->n, d->h, d->w, d->c_in, d->c_mid, d->c_out, d->k, d->stride, d->pad,
+                            d->dtype, hw.num_cus, hw.lds_per_wg, hw.lds_per_cu};
+  return k;
+}
+
+fcm_status find_plan(int op, const fcm_desc* d, const fcm_hw_desc* hw_in, fcm_plan_t* out) {
+  const fcm_hw_desc hw = hw_in ? *hw_in : default_hw();
+  if (hw.num_cus <= 0 || hw.lds_per_wg <= 0 || hw.lds_per_cu <= 0)
+    return fail(FCM_EINVAL, "plan: hardware description has non-positive sizes");
+  const std::vector<int64_t> key = cache_key(op, d, hw);
+  {
+    std::lock_guard<std::mutex> lock(g_cache_mu);
+    auto it = g_cache.find(key);
+    if (it != g_cache.end()) {
+      *out = it->second;
+      return FCM_OK;
+    }
+  }
+  const Geom g = geometry(op, d);
+  fcm_plan_t p;
+  fcm_status st = search(g, d, hw, &p);
+  if (st != FCM_OK) return st;
+  // layer-by-layer chain: each stage planned on its own (first pass of Sec. IV)
+  std::vector<std::pair<int, fcm_desc>> stages;
+  lbl_stages(op, d, &stages);
+  if (stages.empty()) {
+    p.bytes_lbl_paper = p.bytes_paper;
+    p.bytes_lbl_ideal = p.bytes_ideal;
+    p.fuse = 0;
+  } else {
+    int64_t lp = 0, li = 0;
+    for (auto& sd : stages) {
+      fcm_plan_t sp;
+      st = find_plan(sd.first, &sd.second, &hw, &sp);
+      if (st != FCM_OK) return st;
+      lp += sp.bytes_paper;
+      li += sp.bytes_ideal;
+    }
+    p.bytes_lbl_paper = lp;
+    p.bytes_lbl_ideal = li;
+    p.fuse = p.bytes_paper < lp ? 1 : 0;
+  }
+  {
+    std::lock_guard<std::mutex> lock(g_cache_mu);
+    g_cache[key] = p;
+  }
+  *out = p;
+  return FCM_OK;
+}
+
+}  // namespace fcm

@@ -1,0 +1,328 @@
+"""ctypes binding of libfcm.so (argument marshalling only).
+
+Every computation happens in the HIP kernels behind the C ABI (include/fcm.h). PyTorch
+provides device memory and the current stream; this module checks tensors, fills the
+descriptor, allocates the output tensor with torch when none is given, and calls the
+library. There is no fallback: if libfcm.so is missing or cannot load, importing the
+binding's functions raises.
+
+Entry points mirror the C ABI: dw_pw, pw_dw, pw_dw_pw, dw, pw, plan, plan_evaluate.
+Tensors: x is [n, c, h, w] (layout="nchw") or [n, h, w, c] (layout="nhwc");
+depthwise weights [c, k, k] (or [c, 1, k, k]); pointwise weights [c_out, c_in]
+(or [c_out, c_in, 1, 1]); biases float32 (float paths) or int32 (int8) or None.
+dtype follows x: float32, bfloat16, int8.
+"""
+import ctypes
+import os
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libfcm.so")
+
+OP = {"dw_pw": 0, "pw_dw": 1, "pw_dw_pw": 2, "dw": 3, "pw": 4}
+DTYPE = {"f32": 0, "bf16": 1, "i8": 2}
+LAYOUT = {"nchw": 0, "nhwc": 1}
+ACT = {"none": 0, "relu": 1, "relu6": 2}
+STATUS = {0: "FCM_OK", 1: "FCM_EINVAL", 2: "FCM_EUNSUPPORTED", 3: "FCM_EDEVICE"}
+
+
+class FcmError(RuntimeError):
+    def __init__(self, status, msg):
+        super().__init__("%s: %s" % (STATUS.get(status, status), msg))
+        self.status = status
+
+
+class Requant(ctypes.Structure):
+    _fields_ = [("mult", ctypes.c_int32), ("shift", ctypes.c_int32),
+                ("qmin", ctypes.c_int32), ("qmax", ctypes.c_int32)]
+
+
+class Desc(ctypes.Structure):
+    _fields_ = [("n", ctypes.c_int32), ("h", ctypes.c_int32), ("w", ctypes.c_int32),
+                ("c_in", ctypes.c_int32), ("c_mid", ctypes.c_int32), ("c_out", ctypes.c_int32),
+                ("k", ctypes.c_int32), ("stride", ctypes.c_int32), ("pad", ctypes.c_int32),
+                ("dtype", ctypes.c_int32), ("layout", ctypes.c_int32),
+                ("act", ctypes.c_int32 * 3), ("rq", Requant * 3)]
+
+
+class HwDesc(ctypes.Structure):
+    _fields_ = [("num_cus", ctypes.c_int32), ("num_xcds", ctypes.c_int32),
+                ("wave_size", ctypes.c_int32), ("lds_per_wg", ctypes.c_int32),
+                ("lds_per_cu", ctypes.c_int32), ("l2_per_xcd", ctypes.c_int64),
+                ("mall_bytes", ctypes.c_int64), ("hbm_bytes_per_s", ctypes.c_double)]
+
+
+class Plan(ctypes.Structure):
+    _fields_ = [("op", ctypes.c_int32), ("tile_h", ctypes.c_int32), ("tile_w", ctypes.c_int32),
+                ("c_block", ctypes.c_int32), ("co_block", ctypes.c_int32),
+                ("variant", ctypes.c_int32), ("waves", ctypes.c_int32),
+                ("lds_bytes", ctypes.c_int32), ("workgroups", ctypes.c_int32),
+                ("fuse", ctypes.c_int32),
+                ("bytes_ideal", ctypes.c_int64), ("bytes_tiled", ctypes.c_int64),
+                ("bytes_paper", ctypes.c_int64), ("bytes_lbl_paper", ctypes.c_int64),
+                ("bytes_lbl_ideal", ctypes.c_int64), ("redundancy", ctypes.c_double)]
+
+    def as_dict(self):
+        return {f: getattr(self, f) for f, _ in self._fields_}
+
+
+_lib = None
+
+
+def lib():
+    """Load libfcm.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise FcmError(-1, "libfcm.so not found at %s; build it with "
+                               "`python -m paper_2404_19331_amd.build`" % LIB_PATH)
+        L = ctypes.CDLL(LIB_PATH)
+        vp, dp, pp = ctypes.c_void_p, ctypes.POINTER(Desc), ctypes.POINTER(Plan)
+        hp = ctypes.POINTER(HwDesc)
+        L.fcm_plan.argtypes = [ctypes.c_int32, dp, hp, pp]
+        L.fcm_plan_evaluate.argtypes = [dp, hp, pp]
+        L.fcm_dw_pw.argtypes = [dp, vp, vp, vp, vp, vp, vp, pp, vp]
+        L.fcm_pw_dw.argtypes = [dp, vp, vp, vp, vp, vp, vp, pp, vp]
+        L.fcm_pw_dw_pw.argtypes = [dp, vp, vp, vp, vp, vp, vp, vp, vp, pp, vp]
+        L.fcm_dw.argtypes = [dp, vp, vp, vp, vp, pp, vp]
+        L.fcm_pw.argtypes = [dp, vp, vp, vp, vp, pp, vp]
+        for f in (L.fcm_plan, L.fcm_plan_evaluate, L.fcm_dw_pw, L.fcm_pw_dw, L.fcm_pw_dw_pw,
+                  L.fcm_dw, L.fcm_pw):
+            f.restype = ctypes.c_int
+        L.fcm_status_string.argtypes = [ctypes.c_int]
+        L.fcm_status_string.restype = ctypes.c_char_p
+        L.fcm_last_error.restype = ctypes.c_char_p
+        L.fcm_version.restype = ctypes.c_char_p
+        _lib = L
+    return _lib
+
+
+def last_error():
+    return lib().fcm_last_error().decode()
+
+
+def _check(st):
+    if st != 0:
+        raise FcmError(st, last_error())
+
+
+def make_desc(n, h, w, c_in, c_mid, c_out, k=3, stride=1, pad=1, dtype="f32", layout="nchw",
+              act=("none", "none", "none"), rq=None):
+    d = Desc()
+    d.n, d.h, d.w = n, h, w
+    d.c_in, d.c_mid, d.c_out = c_in, c_mid, c_out
+    d.k, d.stride, d.pad = k, stride, pad
+    d.dtype = DTYPE[dtype] if isinstance(dtype, str) else int(dtype)
+    d.layout = LAYOUT[layout] if isinstance(layout, str) else int(layout)
+    acts = (list(act) + ["none"] * 3)[:3]
+    for i, a in enumerate(acts):
+        d.act[i] = ACT[a] if isinstance(a, str) else int(a)
+    rqs = (list(rq or []) + [(1, 0, -128, 127)] * 3)[:3]
+    for i, r in enumerate(rqs):
+        d.rq[i].mult, d.rq[i].shift, d.rq[i].qmin, d.rq[i].qmax = (int(v) for v in r)
+    return d
+
+
+def desc_from_case(case):
+    """Descriptor from a workloads.Case (or any object/dict with the same fields)."""
+    g = (lambda k: case[k]) if isinstance(case, dict) else (lambda k: getattr(case, k))
+    return make_desc(g("n"), g("h"), g("w"), g("c_in"), g("c_mid"), g("c_out"), g("k"), g("stride"),
+                     g("pad"), g("dtype"), g("layout"), g("act"), g("rq"))
+
+
+def plan(op, desc, hw=None):
+    """FusePlanner: the tiling fcm_plan chooses, as a dict."""
+    p = Plan()
+    _check(lib().fcm_plan(OP[op], ctypes.byref(desc), ctypes.byref(hw) if hw else None, ctypes.byref(p)))
+    return p
+
+
+def plan_evaluate(op, desc, tile_h, tile_w, c_block, co_block, variant, hw=None):
+    p = Plan()
+    p.op, p.tile_h, p.tile_w, p.c_block, p.co_block, p.variant = OP[op], tile_h, tile_w, c_block, co_block, variant
+    _check(lib().fcm_plan_evaluate(ctypes.byref(desc), ctypes.byref(hw) if hw else None, ctypes.byref(p)))
+    return p
+
+
+# ------------------------------------------------------------------------------------
+# torch-facing entry points
+# ------------------------------------------------------------------------------------
+
+def _torch():
+    import torch
+    return torch
+
+
+def _dtype_name(t):
+    torch = _torch()
+    m = {torch.float32: "f32", torch.bfloat16: "bf16", torch.int8: "i8"}
+    if t.dtype not in m:
+        raise TypeError("unsupported dtype %s (float32, bfloat16, int8)" % t.dtype)
+    return m[t.dtype]
+
+
+def _dims(x, layout):
+    if x.dim() != 4:
+        raise ValueError("x must be 4-D")
+    if layout == "nchw":
+        n, c, h, w = x.shape
+    else:
+        n, h, w, c = x.shape
+    return int(n), int(c), int(h), int(w)
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _prep(x, tensors, biases, dt):
+    torch = _torch()
+    if not x.is_cuda:
+        raise ValueError("tensors must be on a GPU device")
+    for t in tensors:
+        if t is None:
+            raise ValueError("weights must not be None")
+        if t.device != x.device or t.dtype != x.dtype:
+            raise ValueError("weights must match x in device and dtype")
+        if not t.is_contiguous():
+            raise ValueError("weights must be contiguous")
+    bdt = torch.int32 if dt == "i8" else torch.float32
+    for b in biases:
+        if b is not None and (b.device != x.device or b.dtype != bdt or not b.is_contiguous()):
+            raise ValueError("bias must be a contiguous %s tensor on x's device" % bdt)
+    if not x.is_contiguous():
+        raise ValueError("x must be contiguous in its layout")
+
+
+def _out(x, layout, n, c, h, w, out):
+    torch = _torch()
+    shape = (n, c, h, w) if layout == "nchw" else (n, h, w, c)
+    if out is None:
+        return torch.empty(shape, dtype=x.dtype, device=x.device)
+    if tuple(out.shape) != shape or out.dtype != x.dtype or out.device != x.device or not out.is_contiguous():
+        raise ValueError("out must be a contiguous %s tensor of shape %s" % (x.dtype, shape))
+    return out
+
+
+def _stream(x, stream):
+    torch = _torch()
+    if stream is None:
+        stream = torch.cuda.current_stream(x.device)
+    return ctypes.c_void_p(stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
+
+
+def out_hw(h, w, k, stride, pad):
+    return (h + 2 * pad - k) // stride + 1, (w + 2 * pad - k) // stride + 1
+
+
+def _kk(w_dw):
+    return int(w_dw.shape[-1])
+
+
+def dw_pw(x, w_dw, w_pw, b_dw=None, b_pw=None, *, stride=1, pad=None, act=("none", "none"), rq=None,
+          layout="nchw", plan=None, out=None, stream=None):
+    """DW -> PW module in one kernel. Returns y [n, c_out, h_o, w_o] in `layout`."""
+    dt = _dtype_name(x)
+    n, c, h, w = _dims(x, layout)
+    k = _kk(w_dw)
+    pad = (k - 1) // 2 if pad is None else pad
+    co = int(w_pw.shape[0])
+    _prep(x, [w_dw, w_pw], [b_dw, b_pw], dt)
+    d = make_desc(n, h, w, c, c, co, k, stride, pad, dt, layout, act, rq)
+    ho, wo = out_hw(h, w, k, stride, pad)
+    y = _out(x, layout, n, co, ho, wo, out)
+    _check(lib().fcm_dw_pw(ctypes.byref(d), _ptr(x), _ptr(w_dw), _ptr(b_dw), _ptr(w_pw), _ptr(b_pw), _ptr(y),
+                           ctypes.byref(plan) if plan is not None else None, _stream(x, stream)))
+    return y
+
+
+def pw_dw(x, w_pw, w_dw, b_pw=None, b_dw=None, *, stride=1, pad=None, act=("none", "none"), rq=None,
+          layout="nchw", plan=None, out=None, stream=None):
+    """PW -> DW module in one kernel. Returns y [n, c_mid, h_o, w_o]."""
+    dt = _dtype_name(x)
+    n, c, h, w = _dims(x, layout)
+    k = _kk(w_dw)
+    pad = (k - 1) // 2 if pad is None else pad
+    cm = int(w_pw.shape[0])
+    _prep(x, [w_pw, w_dw], [b_pw, b_dw], dt)
+    d = make_desc(n, h, w, c, cm, cm, k, stride, pad, dt, layout, act, rq)
+    ho, wo = out_hw(h, w, k, stride, pad)
+    y = _out(x, layout, n, cm, ho, wo, out)
+    _check(lib().fcm_pw_dw(ctypes.byref(d), _ptr(x), _ptr(w_pw), _ptr(b_pw), _ptr(w_dw), _ptr(b_dw), _ptr(y),
+                           ctypes.byref(plan) if plan is not None else None, _stream(x, stream)))
+    return y
+
+
+def pw_dw_pw(x, w_pw1, w_dw, w_pw2, b_pw1=None, b_dw=None, b_pw2=None, *, stride=1, pad=None,
+             act=("none", "none", "none"), rq=None, layout="nchw", plan=None, out=None, stream=None):
+    """PW -> DW -> PW inverted residual in one kernel. Returns y [n, c_out, h_o, w_o]."""
+    dt = _dtype_name(x)
+    n, c, h, w = _dims(x, layout)
+    k = _kk(w_dw)
+    pad = (k - 1) // 2 if pad is None else pad
+    cm, co = int(w_pw1.shape[0]), int(w_pw2.shape[0])
+    _prep(x, [w_pw1, w_dw, w_pw2], [b_pw1, b_dw, b_pw2], dt)
+    d = make_desc(n, h, w, c, cm, co, k, stride, pad, dt, layout, act, rq)
+    ho, wo = out_hw(h, w, k, stride, pad)
+    y = _out(x, layout, n, co, ho, wo, out)
+    _check(lib().fcm_pw_dw_pw(ctypes.byref(d), _ptr(x), _ptr(w_pw1), _ptr(b_pw1), _ptr(w_dw), _ptr(b_dw),
+                              _ptr(w_pw2), _ptr(b_pw2), _ptr(y),
+                              ctypes.byref(plan) if plan is not None else None, _stream(x, stream)))
+    return y
+
+
+def dw(x, w_dw, b_dw=None, *, stride=1, pad=None, act="none", rq=None, layout="nchw", plan=None, out=None,
+       stream=None):
+    """Single depthwise layer (layer-by-layer kernel)."""
+    dt = _dtype_name(x)
+    n, c, h, w = _dims(x, layout)
+    k = _kk(w_dw)
+    pad = (k - 1) // 2 if pad is None else pad
+    _prep(x, [w_dw], [b_dw], dt)
+    d = make_desc(n, h, w, c, c, c, k, stride, pad, dt, layout, (act,), [rq] if rq else None)
+    ho, wo = out_hw(h, w, k, stride, pad)
+    y = _out(x, layout, n, c, ho, wo, out)
+    _check(lib().fcm_dw(ctypes.byref(d), _ptr(x), _ptr(w_dw), _ptr(b_dw), _ptr(y),
+                        ctypes.byref(plan) if plan is not None else None, _stream(x, stream)))
+    return y
+
+
+def pw(x, w_pw, b_pw=None, *, act="none", rq=None, layout="nchw", plan=None, out=None, stream=None):
+    """Single pointwise layer (layer-by-layer kernel)."""
+    dt = _dtype_name(x)
+    n, c, h, w = _dims(x, layout)
+    co = int(w_pw.shape[0])
+    _prep(x, [w_pw], [b_pw], dt)
+    d = make_desc(n, h, w, c, c, co, 1, 1, 0, dt, layout, (act,), [rq] if rq else None)
+    y = _out(x, layout, n, co, h, w, out)
+    _check(lib().fcm_pw(ctypes.byref(d), _ptr(x), _ptr(w_pw), _ptr(b_pw), _ptr(y),
+                        ctypes.byref(plan) if plan is not None else None, _stream(x, stream)))
+    return y
+
+
+# ------------------------------------------------------------------------------------
+# Layer-by-layer chains (the unfused comparison): each layer is its own kernel and every
+# intermediate feature map goes through device memory.
+# ------------------------------------------------------------------------------------
+
+def dw_then_pw(x, w_dw, w_pw, b_dw=None, b_pw=None, *, stride=1, pad=None, act=("none", "none"), rq=None,
+               layout="nchw", mid=None, out=None, stream=None):
+    rq = list(rq) if rq else [None, None]
+    m = dw(x, w_dw, b_dw, stride=stride, pad=pad, act=act[0], rq=rq[0], layout=layout, out=mid, stream=stream)
+    return pw(m, w_pw, b_pw, act=act[1], rq=rq[1], layout=layout, out=out, stream=stream)
+
+
+def pw_then_dw(x, w_pw, w_dw, b_pw=None, b_dw=None, *, stride=1, pad=None, act=("none", "none"), rq=None,
+               layout="nchw", mid=None, out=None, stream=None):
+    rq = list(rq) if rq else [None, None]
+    m = pw(x, w_pw, b_pw, act=act[0], rq=rq[0], layout=layout, out=mid, stream=stream)
+    return dw(m, w_dw, b_dw, stride=stride, pad=pad, act=act[1], rq=rq[1], layout=layout, out=out, stream=stream)
+
+
+def pw_then_dw_then_pw(x, w_pw1, w_dw, w_pw2, b_pw1=None, b_dw=None, b_pw2=None, *, stride=1, pad=None,
+                       act=("none", "none", "none"), rq=None, layout="nchw", mids=(None, None), out=None,
+                       stream=None):
+    rq = list(rq) if rq else [None, None, None]
+    m1 = pw(x, w_pw1, b_pw1, act=act[0], rq=rq[0], layout=layout, out=mids[0], stream=stream)
+    m2 = dw(m1, w_dw, b_dw, stride=stride, pad=pad, act=act[1], rq=rq[1], layout=layout, out=mids[1],
+            stream=stream)
+    return pw(m2, w_pw2, b_pw2, act=act[2], rq=rq[2], layout=layout, out=out, stream=stream)

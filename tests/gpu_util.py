@@ -1,0 +1,117 @@
+"""Helpers for the GPU parity tests: move seeded numpy inputs to the device, run the HIP
+path through the C ABI binding, compare against the CPU oracle at the stated tolerances."""
+import numpy as np
+
+import oracle
+from paper_2404_19331_amd import fcm
+
+# Tolerances (written once, used by every parity test):
+#   f32:  |g - r| <= 1e-4 + 1e-5 |r|                       (elementwise)
+#   bf16: |g - r| <= 2e-2 (|r| + rms(r))                   (relative, floor at the RMS of
+#         the reference so that outputs near zero are not held to a pure relative bound)
+#   i8:   bit-exact
+F32_ATOL, F32_RTOL = 1e-4, 1e-5
+BF16_RTOL = 2e-2
+
+
+def torch():
+    import torch as t
+    return t
+
+
+def to_dev(a, dtype):
+    t = torch()
+    if a is None:
+        return None
+    if a.dtype == np.uint16:  # bf16 bits
+        return t.from_numpy(a.view(np.int16).copy()).view(t.bfloat16).cuda()
+    return t.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def to_np(x):
+    t = torch()
+    x = x.detach().cpu()
+    if x.dtype == t.bfloat16:
+        return x.view(t.int16).numpy().view(np.uint16)
+    return x.numpy()
+
+
+def bf16_to_f32(bits):
+    return (bits.astype(np.uint32) << 16).view(np.float32)
+
+
+def values(a, dtype):
+    """Storage array -> float64 values for comparisons."""
+    if dtype == "bf16":
+        return bf16_to_f32(a).astype(np.float64)
+    return a.astype(np.float64)
+
+
+def assert_close(got, ref, dtype, what=""):
+    assert got.shape == ref.shape, (got.shape, ref.shape)
+    if dtype == "i8":
+        bad = np.argwhere(got != ref)
+        assert bad.size == 0, "%s: %d int8 mismatches, first at %s: got %d ref %d" % (
+            what, len(bad), tuple(bad[0]), got[tuple(bad[0])], ref[tuple(bad[0])])
+        return
+    g, r = values(got, dtype), values(ref, dtype)
+    assert np.all(np.isfinite(g)), "%s: non-finite output" % what
+    if dtype == "f32":
+        tol = F32_ATOL + F32_RTOL * np.abs(r)
+    else:
+        rms = np.sqrt(np.mean(r * r)) if r.size else 0.0
+        tol = BF16_RTOL * (np.abs(r) + rms)
+    err = np.abs(g - r)
+    bad = err > tol
+    if np.any(bad):
+        i = tuple(np.argwhere(bad)[0])
+        raise AssertionError("%s: %d/%d outside tolerance; first at %s got %r ref %r (max err %.3g)" % (
+            what, int(bad.sum()), bad.size, i, g[i], r[i], float(err.max())))
+
+
+def dev_inputs(inp, dtype):
+    return {k: to_dev(v, dtype) for k, v in inp.items()}
+
+
+def run_fused(case, d, plan=None, out=None):
+    """Run the case's module on the GPU through the C ABI. d: dict of device tensors."""
+    kw = dict(stride=case.stride, pad=case.pad, layout=case.layout, plan=plan, out=out)
+    rq = list(case.rq) if case.dtype == "i8" else None
+    if case.op == "dw_pw":
+        return fcm.dw_pw(d["x"], d["w_dw"], d["w_pw"], d.get("b_dw"), d.get("b_pw"), act=case.act[:2], rq=rq, **kw)
+    if case.op == "pw_dw":
+        return fcm.pw_dw(d["x"], d["w_pw"], d["w_dw"], d.get("b_pw"), d.get("b_dw"), act=case.act[:2], rq=rq, **kw)
+    if case.op == "pw_dw_pw":
+        return fcm.pw_dw_pw(d["x"], d["w_pw1"], d["w_dw"], d["w_pw2"], d.get("b_pw1"), d.get("b_dw"),
+                            d.get("b_pw2"), act=case.act, rq=rq, **kw)
+    if case.op == "dw":
+        return fcm.dw(d["x"], d["w_dw"], d.get("b_dw"), act=case.act[0], rq=rq[0] if rq else None, **kw)
+    if case.op == "pw":
+        kw.pop("stride"), kw.pop("pad")
+        return fcm.pw(d["x"], d["w_pw"], d.get("b_pw"), act=case.act[0], rq=rq[0] if rq else None, **kw)
+    raise ValueError(case.op)
+
+
+def run_unfused(case, d):
+    kw = dict(stride=case.stride, pad=case.pad, layout=case.layout)
+    rq = list(case.rq) if case.dtype == "i8" else None
+    if case.op == "dw_pw":
+        return fcm.dw_then_pw(d["x"], d["w_dw"], d["w_pw"], d.get("b_dw"), d.get("b_pw"), act=case.act[:2],
+                              rq=rq, **kw)
+    if case.op == "pw_dw":
+        return fcm.pw_then_dw(d["x"], d["w_pw"], d["w_dw"], d.get("b_pw"), d.get("b_dw"), act=case.act[:2],
+                              rq=rq, **kw)
+    if case.op == "pw_dw_pw":
+        return fcm.pw_then_dw_then_pw(d["x"], d["w_pw1"], d["w_dw"], d["w_pw2"], d.get("b_pw1"), d.get("b_dw"),
+                                      d.get("b_pw2"), act=case.act, rq=rq, **kw)
+    raise ValueError(case.op)
+
+
+def oracle_ref(case, inp):
+    return oracle.run(case.op, case, inp)
+
+
+def batch_slice(inp, idx):
+    out = dict(inp)
+    out["x"] = np.ascontiguousarray(inp["x"][idx])
+    return out

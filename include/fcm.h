@@ -192,6 +192,13 @@ const char* fcm_last_error(void);
 /* Library version string. */
 const char* fcm_version(void);
 
+/* Name of a compiled kernel variant (as fcm_plan_t.variant), e.g. for matching profiler
+ * output to plans; NULL if out of range. Static storage. */
+const char* fcm_variant_name(int32_t variant);
+
+/* Number of compiled kernel variants. */
+int32_t fcm_variant_count(void);
+
 #ifdef __cplusplus
 }
 #endif

@@ -22,7 +22,7 @@ const Variant* all_variants(int* count) {
   static std::vector<Variant> all = [] {
     std::vector<Variant> v;
     const Variant* (*fns[])(int*) = {variants_dwpw_f32, variants_dwpw_bf16, variants_dwpw_i8, variants_pwdw,
-                                     variants_pwdwpw};
+                                     variants_pwdwpw,   variants_v2_bf16,   variants_v2_f32,  variants_v2_i8};
     for (auto fn : fns) {
       int n = 0;
       const Variant* t = fn(&n);
@@ -116,13 +116,18 @@ static fcm_status run(int op, const fcm_desc* d, const Tensors& t, const fcm_pla
   }
 
   const fcm_hw_desc hw = default_hw();
+  // LDS-DMA kernels need 16-byte aligned tensors
+  bool aligned = aligned16(t.x) && aligned16(t.y);
+  for (int i = 0; i < nw; ++i) aligned = aligned && aligned16(t.w[i]);
   fcm_plan_t p;
   if (plan_in) {
     if (plan_in->op != op) return fail(FCM_EINVAL, "plan was made for another module");
     p = *plan_in;
     if ((st = evaluate_plan(g, d, hw, &p)) != FCM_OK) return st;
+    if (!aligned && variant_needs_alignment(p.variant))
+      return fail(FCM_EUNSUPPORTED, "plan's kernel needs 16-byte aligned tensors");
   } else {
-    if ((st = find_plan(op, d, &hw, &p)) != FCM_OK) return st;
+    if ((st = find_plan(op, d, &hw, &p, aligned)) != FCM_OK) return st;
   }
   int nv = 0;
   const Variant* vs = all_variants(&nv);
@@ -177,7 +182,10 @@ static fcm_status run(int op, const fcm_desc* d, const Tensors& t, const fcm_pla
       break;
     default: break;
   }
-  switch (g.family) {
+  if (v.gen == 2) {
+    a.L = LdsLayout{};
+    a.L.bytes = p.lds_bytes;
+  } else switch (g.family) {
     case FAM_DWPW:
     case FAM_PW:
       a.L = lds_layout_dwpw(g.dtype, g.k, g.s, g.family == FAM_DWPW, p.tile_h, p.tile_w, p.c_block, p.co_block);
@@ -273,5 +281,17 @@ const char* fcm_status_string(fcm_status status) {
 const char* fcm_last_error(void) { return g_last_error.c_str(); }
 
 const char* fcm_version(void) { return "fcm 0.1.0 (gfx950)"; }
+
+const char* fcm_variant_name(int32_t variant) {
+  int nv = 0;
+  const Variant* vs = all_variants(&nv);
+  return (variant >= 0 && variant < nv) ? vs[variant].name : nullptr;
+}
+
+int32_t fcm_variant_count(void) {
+  int nv = 0;
+  all_variants(&nv);
+  return nv;
+}
 
 }  // extern "C"

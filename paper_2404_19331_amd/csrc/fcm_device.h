@@ -189,114 +189,266 @@ __device__ __forceinline__ void mma_chunk(typename DT::AccV (&acc)[TMW][TNW], co
 
 // ------------------------------------------------------------------------------------
 // Staging: global -> LDS
+//
+// A copy job is a "loader": load(i, v) fetches item i into registers and returns where
+// it goes in LDS; store(s, d, v) writes it. staged_copy runs up to three jobs together:
+// in each round every thread issues kBatch loads per job before writing any of them, so
+// a thread keeps up to 3*kBatch global loads in flight.
+// Loads are unconditional: an item outside the image or the channel range reads a valid
+// clamped address and carries kZero in its destination, and the zero is substituted at
+// store time. (A load under a branch makes the compiler wait for it inside the branch,
+// which would serialise one memory latency per item.)
 // ------------------------------------------------------------------------------------
+constexpr int kBatch = 4;
+constexpr int kZero = 1 << 30;  // destination flag: store zero instead of the loaded value
+constexpr int kAux = 1 << 29;   // destination flag used by DwWeights: the item is a bias
+constexpr int kOffMask = (1 << 29) - 1;
+
+struct NullLoader {
+  using V = uint32_t;
+  __device__ __forceinline__ int load(int, V&) const { return -1; }
+  __device__ __forceinline__ void store(char*, int, const V&) const {}
+};
+
+template <int B, class LA, class LB, class LC>
+__device__ __forceinline__ void staged_copy(char* s, int ta, const LA& la, int tb, const LB& lb, int tc,
+                                            const LC& lc) {
+  const int tmax = max(ta, max(tb, tc));
+#pragma unroll 1
+  for (int base = threadIdx.x; base < tmax; base += kThreads * B) {
+    typename LA::V va[B];
+    typename LB::V vb[B];
+    typename LC::V vc[B];
+    int da[B], db[B], dc[B];
+#pragma unroll
+    for (int j = 0; j < B; ++j) {
+      const int i = base + j * kThreads;
+      // Callers pass NullLoader for an empty job, so a real loader always has t > 0 and
+      // its load needs no guard (a branch here would put the loads under control flow).
+      da[j] = la.load(min(i, ta - 1), va[j]);
+      db[j] = lb.load(min(i, tb - 1), vb[j]);
+      dc[j] = lc.load(min(i, tc - 1), vc[j]);
+      if (i >= ta) da[j] = -1;
+      if (i >= tb) db[j] = -1;
+      if (i >= tc) dc[j] = -1;
+    }
+#pragma unroll
+    for (int j = 0; j < B; ++j) {
+      if (da[j] >= 0) la.store(s, da[j], va[j]);
+      if (db[j] >= 0) lb.store(s, db[j], vb[j]);
+      if (dc[j] >= 0) lc.store(s, dc[j], vc[j]);
+    }
+  }
+}
+
+template <int B, class LA>
+__device__ __forceinline__ void staged_copy(char* s, int ta, const LA& la) {
+  staged_copy<B>(s, ta, la, 0, NullLoader{}, 0, NullLoader{});
+}
+
+__device__ __forceinline__ void store_vec(char* s, int d, const u32x4& v) {
+  *(u32x4*)(s + (d & kOffMask)) = (d & kZero) ? u32x4{0u, 0u, 0u, 0u} : v;
+}
+
+template <class T>
+__device__ __forceinline__ void store_elem(char* s, int d, const T& v) {
+  *(T*)(s + (d & kOffMask)) = (d & kZero) ? T(0) : v;
+}
 
 // Haloed input window rows [iy0, iy0+IH) x cols [ix0, ix0+IW), channels [c0, c0+CB) into
-// LDS as [IH*IW pixels][CB] with pixel stride ps bytes. Zero outside the image and for
-// channels >= C. vec: C*ELT % 16 == 0 and x 16-byte aligned.
+// LDS at `off` as [IH*IW pixels][CB] with pixel stride ps bytes. Zero outside the image
+// and for channels >= C.
 template <class DT>
-__device__ __forceinline__ void stage_input(char* s, int ps, const typename DT::T* __restrict__ x, int layout, int n, int C,
-                            int H, int W, int iy0, int ix0, int IH, int IW, int c0, int CB, bool vec) {
-  using T = typename DT::T;
-  constexpr int VE = 16 / DT::ELT;
-  if (layout == LAYOUT_NHWC) {
-    if (vec) {
-      const int nv = CB / VE;
-      const int total = IH * IW * nv;
-#pragma unroll 1
-  for (int i = threadIdx.x; i < total; i += kThreads) {
-        const int v = i % nv, pix = i / nv;
-        const int py = pix / IW, px = pix - py * IW;
-        const int gy = iy0 + py, gx = ix0 + px, c = c0 + v * VE;
-        u32x4 val = {0u, 0u, 0u, 0u};
-        if ((unsigned)gy < (unsigned)H && (unsigned)gx < (unsigned)W && c < C)
-          val = *(const u32x4*)(x + (((size_t)n * H + gy) * W + gx) * C + c);
-        *(u32x4*)(s + pix * ps + v * 16) = val;
-      }
-    } else {
-      const int total = IH * IW * CB;
-#pragma unroll 1
-  for (int i = threadIdx.x; i < total; i += kThreads) {
-        const int ci = i % CB, pix = i / CB;
-        const int py = pix / IW, px = pix - py * IW;
-        const int gy = iy0 + py, gx = ix0 + px, c = c0 + ci;
-        T val = T(0);
-        if ((unsigned)gy < (unsigned)H && (unsigned)gx < (unsigned)W && c < C)
-          val = x[(((size_t)n * H + gy) * W + gx) * C + c];
-        *(T*)(s + pix * ps + ci * DT::ELT) = val;
-      }
-    }
-  } else {
-    const int total = CB * IH * IW;
-#pragma unroll 1
-  for (int i = threadIdx.x; i < total; i += kThreads) {
-      const int px = i % IW;
-      const int t = i / IW;
-      const int py = t % IH, ci = t / IH;
-      const int gy = iy0 + py, gx = ix0 + px, c = c0 + ci;
-      T val = T(0);
-      if ((unsigned)gy < (unsigned)H && (unsigned)gx < (unsigned)W && c < C)
-        val = x[(((size_t)n * C + c) * H + gy) * W + gx];
-      *(T*)(s + (py * IW + px) * ps + ci * DT::ELT) = val;
-    }
+struct InputVec {  // NHWC, 16-byte vectors (C*ELT % 16 == 0, x 16-byte aligned)
+  using V = u32x4;
+  static constexpr int VE = 16 / DT::ELT;
+  const typename DT::T* x;
+  int n, C, H, W, iy0, ix0, IW, c0, nv, ps, off;
+  __device__ __forceinline__ int load(int i, V& v) const {
+    const int vv = i % nv, pix = i / nv;
+    const int py = pix / IW, px = pix - py * IW;
+    const int gy = iy0 + py, gx = ix0 + px, c = c0 + vv * VE;
+    const bool ok = (unsigned)gy < (unsigned)H && (unsigned)gx < (unsigned)W && c < C;
+    const size_t idx = ok ? (((size_t)n * H + gy) * W + gx) * C + c : 0;
+    v = *(const u32x4*)(x + idx);
+    return (off + pix * ps + vv * 16) | (ok ? 0 : kZero);
   }
-}
+  __device__ __forceinline__ void store(char* s, int d, const V& v) const { store_vec(s, d, v); }
+};
+
+template <class DT>
+struct InputElem {  // NHWC or NCHW, one element per item
+  using V = typename DT::T;
+  const typename DT::T* x;
+  int layout, n, C, H, W, iy0, ix0, IH, IW, c0, CB, ps, off;
+  __device__ __forceinline__ int load(int i, V& v) const {
+    int ci, py, px;
+    if (layout == LAYOUT_NHWC) {
+      ci = i % CB;
+      const int pix = i / CB;
+      py = pix / IW;
+      px = pix - py * IW;
+    } else {
+      px = i % IW;
+      const int t = i / IW;
+      py = t % IH;
+      ci = t / IH;
+    }
+    const int gy = iy0 + py, gx = ix0 + px, c = c0 + ci;
+    const bool ok = (unsigned)gy < (unsigned)H && (unsigned)gx < (unsigned)W && c < C;
+    const size_t idx = !ok ? 0
+                           : (layout == LAYOUT_NHWC ? (((size_t)n * H + gy) * W + gx) * C + c
+                                                    : (((size_t)n * C + c) * H + gy) * W + gx);
+    v = x[idx];
+    return (off + (py * IW + px) * ps + ci * DT::ELT) | (ok ? 0 : kZero);
+  }
+  __device__ __forceinline__ void store(char* s, int d, const V& v) const { store_elem(s, d, v); }
+};
 
 // Rows [r0, r0+rows) x cols [c0, c0+CB) of a row-major [R][Cc] matrix into LDS rows of
-// stride rs bytes; zero beyond R or Cc. vec: Cc*ELT % 16 == 0 and w 16-byte aligned.
+// stride rs bytes at `off`; zero beyond R or Cc.
 template <class DT>
-__device__ __forceinline__ void stage_rows(char* s, int rs, const typename DT::T* __restrict__ w, int R, int Cc, int r0, int rows,
-                           int c0, int CB, bool vec) {
-  using T = typename DT::T;
-  constexpr int VE = 16 / DT::ELT;
-  if (vec) {
-    const int nv = CB / VE;
-    const int total = rows * nv;
-#pragma unroll 1
-  for (int i = threadIdx.x; i < total; i += kThreads) {
-      const int v = i % nv, r = i / nv;
-      const int gr = r0 + r, c = c0 + v * VE;
-      u32x4 val = {0u, 0u, 0u, 0u};
-      if (gr < R && c < Cc) val = *(const u32x4*)(w + (size_t)gr * Cc + c);
-      *(u32x4*)(s + r * rs + v * 16) = val;
-    }
-  } else {
-    const int total = rows * CB;
-#pragma unroll 1
-  for (int i = threadIdx.x; i < total; i += kThreads) {
-      const int ci = i % CB, r = i / CB;
-      const int gr = r0 + r, c = c0 + ci;
-      T val = T(0);
-      if (gr < R && c < Cc) val = w[(size_t)gr * Cc + c];
-      *(T*)(s + r * rs + ci * DT::ELT) = val;
-    }
+struct RowsVec {  // Cc*ELT % 16 == 0 and w 16-byte aligned
+  using V = u32x4;
+  static constexpr int VE = 16 / DT::ELT;
+  const typename DT::T* w;
+  int R, Cc, r0, c0, nv, rs, off;
+  __device__ __forceinline__ int load(int i, V& v) const {
+    const int vv = i % nv, r = i / nv;
+    const int gr = r0 + r, c = c0 + vv * VE;
+    const bool ok = gr < R && c < Cc;
+    v = *(const u32x4*)(w + (ok ? (size_t)gr * Cc + c : 0));
+    return (off + r * rs + vv * 16) | (ok ? 0 : kZero);
   }
-}
+  __device__ __forceinline__ void store(char* s, int d, const V& v) const { store_vec(s, d, v); }
+};
 
-// Depthwise weights [C][K][K] (channels c0..c0+CB) as accumulator-type values in LDS
-// laid out [K*K taps][CB], followed by the bias [CB]. Zero for channels >= C.
+template <class DT>
+struct RowsElem {
+  using V = typename DT::T;
+  const typename DT::T* w;
+  int R, Cc, r0, c0, CB, rs, off;
+  __device__ __forceinline__ int load(int i, V& v) const {
+    const int ci = i % CB, r = i / CB;
+    const int gr = r0 + r, c = c0 + ci;
+    const bool ok = gr < R && c < Cc;
+    v = w[ok ? (size_t)gr * Cc + c : 0];
+    return (off + r * rs + ci * DT::ELT) | (ok ? 0 : kZero);
+  }
+  __device__ __forceinline__ void store(char* s, int d, const V& v) const { store_elem(s, d, v); }
+};
+
+// Depthwise weights [C][K][K] (channels c0..c0+CB) as accumulator-type values laid out
+// [K*K taps][CB] at `off`, followed by the bias [CB]. Zero for channels >= C and for a
+// NULL bias. The raw element is converted at store time.
 template <class DT, int K>
-__device__ __forceinline__ void stage_dw_weights(typename DT::Acc* s, const typename DT::T* __restrict__ wd, const void* bd, int C,
-                                 int c0, int CB) {
-  using Acc = typename DT::Acc;
-  const int total = (K * K + 1) * CB;
-#pragma unroll 1
-  for (int i = threadIdx.x; i < total; i += kThreads) {
+struct DwWeights {
+  using V = u32x2;  // {raw weight element, raw bias bits}; both always loaded, no branch
+  const typename DT::T* wd;
+  const void* bd;
+  int C, c0, CB, off;
+  __device__ __forceinline__ int load(int i, V& v) const {
     const int ci = i % CB, tap = i / CB;
     const int c = c0 + ci;
-    Acc v = Acc(0);
-    if (c < C) {
-      if (tap < K * K) {
-        if constexpr (std::is_same<DT, TBF16>::value)
-          v = bf16_to_f32(((const uint16_t*)wd)[(size_t)c * K * K + tap]);
-        else
-          v = (Acc)wd[(size_t)c * K * K + tap];
-      } else {
-        v = load_bias<DT>(bd, c);
-      }
-    }
-    s[i] = v;
+    const bool is_bias = tap >= K * K;
+    const bool ok = c < C && (!is_bias || bd != nullptr);
+    const int cc = c < C ? c : 0;
+    const size_t wi = (size_t)cc * K * K + (is_bias ? 0 : tap);
+    const uint32_t* bp = bd ? (const uint32_t*)bd : (const uint32_t*)wd;  // valid address either way
+    uint32_t w;
+    if constexpr (DT::ELT == 4)
+      w = ((const uint32_t*)wd)[wi];
+    else if constexpr (DT::ELT == 2)
+      w = ((const uint16_t*)wd)[wi];
+    else
+      w = (uint32_t)(uint8_t)((const int8_t*)wd)[wi];
+    v = V{w, bp[bd ? cc : 0]};
+    return (off + i * 4) | (ok ? 0 : kZero) | (is_bias ? kAux : 0);
   }
+  __device__ __forceinline__ void store(char* s, int d, const V& v) const {
+    uint32_t bits = v.x;
+    if constexpr (DT::ELT == 2) bits = v.x << 16;                             // bf16 -> f32
+    else if constexpr (DT::ELT == 1) bits = (uint32_t)(int32_t)(int8_t)v.x;   // i8 -> i32
+    if (d & kAux) bits = v.y;                                                 // float / int32 bias
+    *(uint32_t*)(s + (d & kOffMask)) = (d & kZero) ? 0u : bits;
+  }
+};
+
+template <class DT>
+__device__ __forceinline__ InputVec<DT> input_vec(const typename DT::T* x, int n, int C, int H, int W, int iy0,
+                                                  int ix0, int IW, int c0, int CB, int ps, int off) {
+  return InputVec<DT>{x, n, C, H, W, iy0, ix0, IW, c0, CB / InputVec<DT>::VE, ps, off};
+}
+template <class DT>
+__device__ __forceinline__ InputElem<DT> input_elem(const typename DT::T* x, int layout, int n, int C, int H, int W,
+                                                    int iy0, int ix0, int IH, int IW, int c0, int CB, int ps,
+                                                    int off) {
+  return InputElem<DT>{x, layout, n, C, H, W, iy0, ix0, IH, IW, c0, CB, ps, off};
+}
+template <class DT>
+__device__ __forceinline__ RowsVec<DT> rows_vec(const typename DT::T* w, int R, int Cc, int r0, int c0, int CB,
+                                                int rs, int off) {
+  return RowsVec<DT>{w, R, Cc, r0, c0, CB / RowsVec<DT>::VE, rs, off};
+}
+template <class DT>
+__device__ __forceinline__ RowsElem<DT> rows_elem(const typename DT::T* w, int R, int Cc, int r0, int c0, int CB,
+                                                  int rs, int off) {
+  return RowsElem<DT>{w, R, Cc, r0, c0, CB, rs, off};
+}
+
+// Stage a chunk: haloed input window (IH x IW x CB at off_in, pixel stride ps), `rows`
+// rows of a [R][Cc] weight matrix (columns c0..c0+CB at off_w, stride rs) and, with
+// K > 0, the depthwise weights + bias of channels cd0..cd0+CBD at off_wd.
+template <class DT, int K>
+__device__ __forceinline__ void stage_chunk(char* s, const typename DT::T* x, int layout, bool vec_x, int n, int C,
+                                            int H, int W, int iy0, int ix0, int IH, int IW, int c0, int CB, int ps,
+                                            int off_in, const typename DT::T* w, bool vec_w, int R, int Cc, int r0,
+                                            int rows, int rs, int off_w, const typename DT::T* wd, const void* bd,
+                                            int Cd, int cd0, int CBD, int off_wd) {
+  constexpr int VE = 16 / DT::ELT;
+  const int t_in = x ? IH * IW * CB : 0;
+  const int t_w = w ? rows * CB : 0;
+  const int t_d = K > 0 ? (K * K + 1) * CBD : 0;
+  const bool fast_in = layout == LAYOUT_NHWC && vec_x;
+  if (fast_in && (vec_w || t_w == 0)) {
+    const InputVec<DT> li = input_vec<DT>(x, n, C, H, W, iy0, ix0, IW, c0, CB, ps, off_in);
+    if constexpr (K > 0) {
+      const DwWeights<DT, K> ld{wd, bd, Cd, cd0, CBD, off_wd};
+      if (t_w > 0)
+        staged_copy<kBatch>(s, t_in / VE, li, t_w / VE, rows_vec<DT>(w, R, Cc, r0, c0, CB, rs, off_w), t_d, ld);
+      else
+        staged_copy<kBatch>(s, t_in / VE, li, 0, NullLoader{}, t_d, ld);
+    } else {
+      if (t_w > 0)
+        staged_copy<kBatch>(s, t_in / VE, li, t_w / VE, rows_vec<DT>(w, R, Cc, r0, c0, CB, rs, off_w), 0,
+                            NullLoader{});
+      else
+        staged_copy<kBatch>(s, t_in / VE, li);
+    }
+    return;
+  }
+  if (fast_in)
+    staged_copy<kBatch>(s, t_in / VE, input_vec<DT>(x, n, C, H, W, iy0, ix0, IW, c0, CB, ps, off_in));
+  else
+    staged_copy<kBatch>(s, t_in, input_elem<DT>(x, layout, n, C, H, W, iy0, ix0, IH, IW, c0, CB, ps, off_in));
+  if (t_w > 0) {
+    if (vec_w)
+      staged_copy<kBatch>(s, t_w / VE, rows_vec<DT>(w, R, Cc, r0, c0, CB, rs, off_w));
+    else
+      staged_copy<kBatch>(s, t_w, rows_elem<DT>(w, R, Cc, r0, c0, CB, rs, off_w));
+  }
+  if constexpr (K > 0) staged_copy<kBatch>(s, t_d, DwWeights<DT, K>{wd, bd, Cd, cd0, CBD, off_wd});
+}
+
+// Weight rows only (vector or element path).
+template <class DT>
+__device__ __forceinline__ void stage_rows(char* s, const typename DT::T* w, bool vec, int R, int Cc, int r0,
+                                           int rows, int c0, int CB, int rs, int off) {
+  constexpr int VE = 16 / DT::ELT;
+  if (vec)
+    staged_copy<kBatch>(s, rows * CB / VE, rows_vec<DT>(w, R, Cc, r0, c0, CB, rs, off));
+  else
+    staged_copy<kBatch>(s, rows * CB, rows_elem<DT>(w, R, Cc, r0, c0, CB, rs, off));
 }
 
 // ------------------------------------------------------------------------------------
@@ -407,7 +559,10 @@ __device__ __forceinline__ void acc_to_lds(const typename DT::AccV (&acc)[TMW][T
     const int m = m_base + i * 16 + 4 * g;
     typename DT::Acc b[4];
 #pragma unroll
-    for (int v = 0; v < 4; ++v) b[v] = (m + v < m_valid) ? load_bias<DT>(bias, bias_off + m + v) : 0;
+    for (int v = 0; v < 4; ++v) {  // unconditional load at a clamped index, then select
+      b[v] = load_bias<DT>(bias, bias_off + min(m + v, m_valid - 1));
+      if (m + v >= m_valid) b[v] = 0;
+    }
 #pragma unroll
     for (int j = 0; j < TNW; ++j) {
       if (j >= n_act) continue;

@@ -3,7 +3,7 @@
 
 #include <string>
 
-#include "../../include/fcm.h"
+#include "fcm.h"
 #include "fcm_internal.h"
 
 namespace fcm {
@@ -22,6 +22,7 @@ struct Geom {
   int k, s, pad;        // depthwise (1, 1, 0 for the pointwise layer)
   int ho, wo;           // output
   int dtype, elt;
+  int layout;
 };
 Geom geometry(int op, const fcm_desc* d);
 
@@ -29,8 +30,12 @@ Geom geometry(int op, const fcm_desc* d);
 // Returns FCM_EUNSUPPORTED if the variant cannot implement the tiling.
 fcm_status evaluate_plan(const Geom& g, const fcm_desc* d, const fcm_hw_desc& hw, fcm_plan_t* p);
 
-// Search (cached). plan_out is fully filled on success.
-fcm_status find_plan(int op, const fcm_desc* d, const fcm_hw_desc* hw, fcm_plan_t* plan_out);
+// Search (cached). plan_out is fully filled on success. allow_dma = false excludes the
+// kernels that need 16-byte aligned tensors (LDS-DMA staging).
+fcm_status find_plan(int op, const fcm_desc* d, const fcm_hw_desc* hw, fcm_plan_t* plan_out, bool allow_dma = true);
+
+// Whether a compiled variant stages through LDS-DMA (needs 16-byte aligned tensors).
+bool variant_needs_alignment(int variant);
 
 fcm_hw_desc default_hw();
 

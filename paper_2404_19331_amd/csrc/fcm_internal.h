@@ -152,6 +152,28 @@ FCM_HD inline LdsLayout lds_layout_pwdwpw(int dt, int K, int S, int TH, int TW, 
   return L;
 }
 
+// LDS-DMA kernels: bytes of channels per pixel row per staged chunk (one MFMA k-step).
+constexpr int kRowB = 64;
+
+// LDS bytes of the v2 kernels (host and device).
+FCM_HD inline int lds_dwpw2(int dt, int K, int S, bool has_dw, int TH, int TW, int CO_MAX, int COB) {
+  const int e = elt_size(dt);
+  const int KE = has_dw ? K : 1, SE = has_dw ? S : 1;
+  const int npin = ((TH - 1) * SE + KE) * ((TW - 1) * SE + KE);
+  const int in_bytes = (npin + 15) / 16 * 1024;
+  const int cb = kRowB / e;
+  const int wd = has_dw ? ((KE * KE + 1) * cb * 4 + 15) / 16 * 16 : 0;
+  const int buf = in_bytes + CO_MAX * kRowB + wd;
+  const int out = TH * TW * (COB * e + 16);
+  return 2 * buf > out ? 2 * buf : out;
+}
+
+FCM_HD inline int lds_dw2(int dt, int K, int S, int TH, int TW) {
+  const int e = elt_size(dt);
+  const int npin = ((TH - 1) * S + K) * ((TW - 1) * S + K);
+  return (npin + 15) / 16 * 1024 + ((K * K + 1) * (kRowB / e) * 4 + 15) / 16 * 16;
+}
+
 // ---------------------------------------------------------------------------------
 // Kernel argument block (one struct for all families; unused fields ignored).
 // ---------------------------------------------------------------------------------
@@ -190,6 +212,9 @@ struct Variant {
   int dw_r;         // output pixels per depthwise thread (TW must be a multiple), 0 = no DW
   LaunchFn launch;
   const char* name;
+  int tile_h = 0;   // compile-time tile (0 = chosen at run time)
+  int tile_w = 0;
+  int gen = 1;      // 2: NHWC, 16-byte channel rows, LDS-DMA staging, fixed chunk of 64 bytes
 };
 
 // Compiled variants of each translation unit, and all of them in a fixed order
@@ -199,6 +224,9 @@ const Variant* variants_dwpw_bf16(int* count);
 const Variant* variants_dwpw_i8(int* count);
 const Variant* variants_pwdw(int* count);
 const Variant* variants_pwdwpw(int* count);
+const Variant* variants_v2_bf16(int* count);
+const Variant* variants_v2_f32(int* count);
+const Variant* variants_v2_i8(int* count);
 const Variant* all_variants(int* count);
 
 }  // namespace fcm

@@ -70,9 +70,9 @@ __global__ __launch_bounds__(kThreads) void k_dwpw(KArgs a) {
     for (int j = 0; j < TNW; ++j) acc[i][j] = AccV{0, 0, 0, 0};
 
   for (int c0 = 0; c0 < a.Ci; c0 += a.CB) {
-    stage_input<DT>(smem + L.off_in, L.ps_in, x, a.layout, n, a.Ci, a.H, a.W, iy0, ix0, IH, IW, c0, a.CB, a.vec_x);
-    stage_rows<DT>(smem + L.off_w, L.rs_w, wp, a.Co, a.Ci, co0, m_tiles * 16, c0, a.CB, vec_wp);
-    if constexpr (HAS_DW) stage_dw_weights<DT, K>((Acc*)(smem + L.off_wd), wd, a.b1, a.Ci, c0, a.CB);
+    stage_chunk<DT, HAS_DW ? K : 0>(smem, x, a.layout, a.vec_x, n, a.Ci, a.H, a.W, iy0, ix0, IH, IW, c0, a.CB,
+                                    L.ps_in, L.off_in, wp, vec_wp, a.Co, a.Ci, co0, m_tiles * 16, L.rs_w, L.off_w,
+                                    wd, a.b1, a.Ci, c0, a.CB, L.off_wd);
     __syncthreads();
     const char* B = smem + L.off_in;
     int bs = L.ps_in;
@@ -133,9 +133,9 @@ __global__ __launch_bounds__(kThreads) void k_pwdw(KArgs a) {
 #pragma unroll
       for (int j = 0; j < TNW; ++j) acc[i][j] = AccV{0, 0, 0, 0};
     for (int c0 = 0; c0 < a.Ci; c0 += a.CB) {
-      stage_input<DT>(smem + L.off_in, L.ps_in, x, a.layout, n, a.Ci, a.H, a.W, iy0, ix0, IH, IW, c0, a.CB,
-                      a.vec_x);
-      stage_rows<DT>(smem + L.off_w, L.rs_w, (const T*)a.w1, a.Cm, a.Ci, m0, m_tiles * 16, c0, a.CB, a.vec_w1);
+      stage_chunk<DT, 0>(smem, x, a.layout, a.vec_x, n, a.Ci, a.H, a.W, iy0, ix0, IH, IW, c0, a.CB, L.ps_in,
+                         L.off_in, (const T*)a.w1, a.vec_w1, a.Cm, a.Ci, m0, m_tiles * 16, L.rs_w, L.off_w, nullptr,
+                         nullptr, 0, 0, 0, 0);
       __syncthreads();
       mma_chunk<DT, TMW, TNW>(acc, smem + L.off_w, L.rs_w, smem + L.off_in, L.ps_in, a.CB, wm * TMW * 16,
                               wn * TNW * 16, m_act, n_act);
@@ -144,10 +144,10 @@ __global__ __launch_bounds__(kThreads) void k_pwdw(KArgs a) {
     // PW output over the haloed window -> E [Q][MB]; zero outside the image.
     acc_to_lds<DT, TMW, TNW>(acc, wm * TMW * 16, wn * TNW * 16, m_act, n_act, a.b1, m0, mb_eff, a.act[0], a.rq[0],
                              smem + L.off_e, L.rs_e, IW, iy0, ix0, a.H, a.W);
-    stage_dw_weights<DT, K>((Acc*)(smem + L.off_wd), (const T*)a.w2, a.b2, a.Cm, m0, MB);
+    staged_copy<kBatch>(smem, (K * K + 1) * MB, DwWeights<DT, K>{(const T*)a.w2, a.b2, a.Cm, m0, MB, L.off_wd});
   } else {
-    stage_input<DT>(smem + L.off_e, L.rs_e, x, a.layout, n, a.Cm, a.H, a.W, iy0, ix0, IH, IW, m0, MB, a.vec_x);
-    stage_dw_weights<DT, K>((Acc*)(smem + L.off_wd), (const T*)a.w1, a.b1, a.Cm, m0, MB);
+    stage_chunk<DT, K>(smem, x, a.layout, a.vec_x, n, a.Cm, a.H, a.W, iy0, ix0, IH, IW, m0, MB, L.rs_e, L.off_e,
+                       nullptr, false, 0, 0, 0, 0, 0, 0, (const T*)a.w1, a.b1, a.Cm, m0, MB, L.off_wd);
   }
   __syncthreads();
   const int act_dw = HAS_PW ? a.act[1] : a.act[0];
@@ -195,7 +195,8 @@ __global__ __launch_bounds__(kThreads) void k_pwdwpw(KArgs a) {
   const int n_act2 = max(0, min(TNW2, p_tiles - wn2 * TNW2));
 
   const T* x = (const T*)a.x;
-  stage_input<DT>(smem + L.off_in, L.ps_in, x, a.layout, n, a.Ci, a.H, a.W, iy0, ix0, IH, IW, 0, CIP, a.vec_x);
+  stage_chunk<DT, 0>(smem, x, a.layout, a.vec_x, n, a.Ci, a.H, a.W, iy0, ix0, IH, IW, 0, CIP, L.ps_in, L.off_in,
+                     nullptr, false, 0, 0, 0, 0, 0, 0, nullptr, nullptr, 0, 0, 0, 0);
 
   AccV acc2[TMW2][TNW2];
 #pragma unroll
@@ -207,9 +208,20 @@ __global__ __launch_bounds__(kThreads) void k_pwdwpw(KArgs a) {
     const int mb_eff = min(MB, a.Cm - m0);
     const int m_tiles = ceil_div(mb_eff, 16);
     const int m_act1 = max(0, min(TMW1, m_tiles - wm1 * TMW1));
-    stage_rows<DT>(smem + L.off_w, L.rs_w, (const T*)a.w1, a.Cm, a.Ci, m0, m_tiles * 16, 0, CIP, a.vec_w1);
-    stage_dw_weights<DT, K>((Acc*)(smem + L.off_wd), (const T*)a.w2, a.b2, a.Cm, m0, MB);
-    stage_rows<DT>(smem + L.off_w2, L.rs_w2, (const T*)a.w3, a.Co, a.Cm, co0, o_tiles * 16, m0, MB, a.vec_w3);
+    {
+      constexpr int VE = 16 / DT::ELT;
+      const DwWeights<DT, K> dww{(const T*)a.w2, a.b2, a.Cm, m0, MB, L.off_wd};
+      if (a.vec_w1 && a.vec_w3) {
+        staged_copy<kBatch>(smem, m_tiles * 16 * CIP / VE,
+                            rows_vec<DT>((const T*)a.w1, a.Cm, a.Ci, m0, 0, CIP, L.rs_w, L.off_w),
+                            (K * K + 1) * MB, dww, o_tiles * 16 * MB / VE,
+                            rows_vec<DT>((const T*)a.w3, a.Co, a.Cm, co0, m0, MB, L.rs_w2, L.off_w2));
+      } else {
+        stage_rows<DT>(smem, (const T*)a.w1, a.vec_w1, a.Cm, a.Ci, m0, m_tiles * 16, 0, CIP, L.rs_w, L.off_w);
+        staged_copy<kBatch>(smem, (K * K + 1) * MB, dww);
+        stage_rows<DT>(smem, (const T*)a.w3, a.vec_w3, a.Co, a.Cm, co0, o_tiles * 16, m0, MB, L.rs_w2, L.off_w2);
+      }
+    }
     __syncthreads();
     {
       AccV acc1[TMW1][TNW1];
@@ -267,6 +279,11 @@ int launch_pwdw(const KArgs& a, int grid, void* stream) {
 template <class DT, int K, int S, int QMAX, int MBMAX, int WM1, int OMAX, int PMAX, int WM2, int R>
 int launch_pwdwpw(const KArgs& a, int grid, void* stream) {
   return launch_kernel(k_pwdwpw<DT, K, S, QMAX, MBMAX, WM1, OMAX, PMAX, WM2, R>, a, grid, stream);
+}
+
+template <class DT>
+constexpr int dtype_elt() {
+  return DT::ELT;
 }
 
 template <class DT>

@@ -50,6 +50,7 @@ Geom geometry(int op, const fcm_desc* d) {
   g.w = d->w;
   g.dtype = d->dtype;
   g.elt = elt_size(d->dtype);
+  g.layout = d->layout;
   g.k = d->k;
   g.s = d->stride;
   g.pad = d->pad;
@@ -161,6 +162,18 @@ static int tiling_lds(const Variant& v, const Geom& g, int TH, int TW, int CB, i
   const int Q = ((TH - 1) * g.s + g.k) * ((TW - 1) * g.s + g.k);
   if (v.max_p && P > v.max_p) return 0;
   if (v.max_q && Q > v.max_q) return 0;
+  if (v.gen == 2) {
+    // NHWC, 16-byte channel rows, 32-bit buffer offsets, fixed tile and 64-byte chunk
+    if (g.layout != FCM_NHWC || TH != v.tile_h || TW != v.tile_w) return 0;
+    const int last = g.family == FAM_DW ? g.cm : g.co;
+    if ((g.ci * g.elt) % 16 || (last * g.elt) % 16) return 0;
+    if ((int64_t)g.h * g.w * g.ci * g.elt >= ((int64_t)1 << 31)) return 0;
+    if ((int64_t)g.co * g.ci * g.elt >= ((int64_t)1 << 31)) return 0;
+    const int cb = 64 / g.elt;
+    if (CB != cb) return 0;
+    if (v.family == FAM_DW) return COB == cb ? lds_dw2(g.dtype, g.k, g.s, TH, TW) : 0;
+    return lds_dwpw2(g.dtype, g.k, g.s, v.family == FAM_DWPW, TH, TW, v.max_cob, COB);
+  }
   switch (v.family) {
     case FAM_DWPW:
     case FAM_PW:
@@ -178,6 +191,12 @@ static int tiling_lds(const Variant& v, const Geom& g, int TH, int TW, int CB, i
       return lds_layout_pwdwpw(g.dtype, g.k, g.s, TH, TW, g.ci, CB, COB).bytes;
   }
   return 0;
+}
+
+bool variant_needs_alignment(int variant) {
+  int nv = 0;
+  const Variant* vs = all_variants(&nv);
+  return variant >= 0 && variant < nv && vs[variant].gen == 2;
 }
 
 static bool variant_matches(const Variant& v, const Geom& g) {
@@ -231,7 +250,8 @@ static std::vector<int> tile_ws(const Variant& v) {
 
 static const int kTileH[] = {1, 2, 4, 7, 8, 14, 16, 28, 32};
 
-static fcm_status search(const Geom& g, const fcm_desc* d, const fcm_hw_desc& hw, fcm_plan_t* best_out) {
+static fcm_status search(const Geom& g, const fcm_desc* d, const fcm_hw_desc& hw, fcm_plan_t* best_out,
+                         bool allow_dma) {
   int nv = 0;
   const Variant* vs = all_variants(&nv);
   const int kb = k_block(g.dtype);
@@ -240,8 +260,11 @@ static fcm_status search(const Geom& g, const fcm_desc* d, const fcm_hw_desc& hw
   for (int vi = 0; vi < nv; ++vi) {
     const Variant& v = vs[vi];
     if (!variant_matches(v, g)) continue;
+    if (v.gen == 2 && !allow_dma) continue;
     std::vector<int> cbs;
-    if (v.family == FAM_DW) {
+    if (v.gen == 2) {
+      cbs = {64 / g.elt};
+    } else if (v.family == FAM_DW) {
       cbs = {0};  // CB follows COB
     } else if (v.family == FAM_PWDWPW) {
       const int step = std::max(16, kb);
@@ -251,13 +274,16 @@ static fcm_status search(const Geom& g, const fcm_desc* d, const fcm_hw_desc& hw
       if (round_up(g.ci, kb) < 8 * kb && std::find(cbs.begin(), cbs.end(), round_up(g.ci, kb)) == cbs.end())
         cbs.push_back(round_up(g.ci, kb));
     }
-    for (int TW : tile_ws(v)) {
-      if (TW > round_up(g.wo, v.dw_r ? v.dw_r : 1) && TW > 4) continue;
-      for (int TH : kTileH) {
-        if (TH > g.ho && TH > 1) continue;
+    std::vector<int> tws = v.tile_w ? std::vector<int>{v.tile_w} : tile_ws(v);
+    std::vector<int> ths = v.tile_h ? std::vector<int>{v.tile_h}
+                                    : std::vector<int>(std::begin(kTileH), std::end(kTileH));
+    for (int TW : tws) {
+      if (!v.tile_w && TW > round_up(g.wo, v.dw_r ? v.dw_r : 1) && TW > 4) continue;
+      for (int TH : ths) {
+        if (!v.tile_h && TH > g.ho && TH > 1) continue;
         for (int COB = 16; COB <= std::min(v.max_cob, round_up(last, 16)); COB += 16) {
           for (int cb0 : cbs) {
-            const int CB = v.family == FAM_DW ? COB : cb0;
+            const int CB = (v.family == FAM_DW && v.gen != 2) ? COB : cb0;
             const int lds = tiling_lds(v, g, TH, TW, CB, COB);
             if (lds <= 0 || lds > hw.lds_per_wg) continue;
             Cand c;
@@ -358,11 +384,13 @@ static std::vector<int64_t> cache_key(int op, const fcm_desc* d, const fcm_hw_de
   return k;
 }
 
-fcm_status find_plan(int op, const fcm_desc* d, const fcm_hw_desc* hw_in, fcm_plan_t* out) {
+fcm_status find_plan(int op, const fcm_desc* d, const fcm_hw_desc* hw_in, fcm_plan_t* out, bool allow_dma) {
   const fcm_hw_desc hw = hw_in ? *hw_in : default_hw();
   if (hw.num_cus <= 0 || hw.lds_per_wg <= 0 || hw.lds_per_cu <= 0)
     return fail(FCM_EINVAL, "plan: hardware description has non-positive sizes");
-  const std::vector<int64_t> key = cache_key(op, d, hw);
+  std::vector<int64_t> key = cache_key(op, d, hw);
+  key.push_back(allow_dma ? 1 : 0);
+  key.push_back(d->layout);
   {
     std::lock_guard<std::mutex> lock(g_cache_mu);
     auto it = g_cache.find(key);
@@ -373,7 +401,7 @@ fcm_status find_plan(int op, const fcm_desc* d, const fcm_hw_desc* hw_in, fcm_pl
   }
   const Geom g = geometry(op, d);
   fcm_plan_t p;
-  fcm_status st = search(g, d, hw, &p);
+  fcm_status st = search(g, d, hw, &p, allow_dma);
   if (st != FCM_OK) return st;
   // layer-by-layer chain: each stage planned on its own (first pass of Sec. IV)
   std::vector<std::pair<int, fcm_desc>> stages;
@@ -386,7 +414,7 @@ fcm_status find_plan(int op, const fcm_desc* d, const fcm_hw_desc* hw_in, fcm_pl
     int64_t lp = 0, li = 0;
     for (auto& sd : stages) {
       fcm_plan_t sp;
-      st = find_plan(sd.first, &sd.second, &hw, &sp);
+      st = find_plan(sd.first, &sd.second, &hw, &sp, allow_dma);
       if (st != FCM_OK) return st;
       lp += sp.bytes_paper;
       li += sp.bytes_ideal;

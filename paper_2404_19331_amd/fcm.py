@@ -92,8 +92,16 @@ def lib():
         L.fcm_status_string.restype = ctypes.c_char_p
         L.fcm_last_error.restype = ctypes.c_char_p
         L.fcm_version.restype = ctypes.c_char_p
+        L.fcm_variant_name.argtypes = [ctypes.c_int32]
+        L.fcm_variant_name.restype = ctypes.c_char_p
+        L.fcm_variant_count.restype = ctypes.c_int32
         _lib = L
     return _lib
+
+
+def variant_name(v):
+    n = lib().fcm_variant_name(int(v))
+    return None if n is None else n.decode()
 
 
 def last_error():
@@ -210,6 +218,31 @@ def _stream(x, stream):
     return ctypes.c_void_p(stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
 
 
+class Prepared:
+    """A C-ABI launch whose arguments were marshalled once; calling it launches again
+    (same tensors, same plan, same stream). Used for repeated timed launches."""
+
+    def __init__(self, fn, args, y):
+        self.fn, self.args, self.y = fn, args, y
+
+    def __call__(self):
+        st = self.fn(*self.args)
+        if st != 0:
+            raise FcmError(st, last_error())
+        return self.y
+
+
+def _call(fn, args, y, prepare):
+    if prepare:
+        return Prepared(fn, args, y)
+    _check(fn(*args))
+    return y
+
+
+def _plan_arg(plan):
+    return ctypes.byref(plan) if plan is not None else None
+
+
 def out_hw(h, w, k, stride, pad):
     return (h + 2 * pad - k) // stride + 1, (w + 2 * pad - k) // stride + 1
 
@@ -219,7 +252,7 @@ def _kk(w_dw):
 
 
 def dw_pw(x, w_dw, w_pw, b_dw=None, b_pw=None, *, stride=1, pad=None, act=("none", "none"), rq=None,
-          layout="nchw", plan=None, out=None, stream=None):
+          layout="nchw", plan=None, out=None, stream=None, prepare=False):
     """DW -> PW module in one kernel. Returns y [n, c_out, h_o, w_o] in `layout`."""
     dt = _dtype_name(x)
     n, c, h, w = _dims(x, layout)
@@ -230,13 +263,12 @@ def dw_pw(x, w_dw, w_pw, b_dw=None, b_pw=None, *, stride=1, pad=None, act=("none
     d = make_desc(n, h, w, c, c, co, k, stride, pad, dt, layout, act, rq)
     ho, wo = out_hw(h, w, k, stride, pad)
     y = _out(x, layout, n, co, ho, wo, out)
-    _check(lib().fcm_dw_pw(ctypes.byref(d), _ptr(x), _ptr(w_dw), _ptr(b_dw), _ptr(w_pw), _ptr(b_pw), _ptr(y),
-                           ctypes.byref(plan) if plan is not None else None, _stream(x, stream)))
-    return y
+    return _call(lib().fcm_dw_pw, (ctypes.byref(d), _ptr(x), _ptr(w_dw), _ptr(b_dw), _ptr(w_pw), _ptr(b_pw),
+                                   _ptr(y), _plan_arg(plan), _stream(x, stream)), y, prepare)
 
 
 def pw_dw(x, w_pw, w_dw, b_pw=None, b_dw=None, *, stride=1, pad=None, act=("none", "none"), rq=None,
-          layout="nchw", plan=None, out=None, stream=None):
+          layout="nchw", plan=None, out=None, stream=None, prepare=False):
     """PW -> DW module in one kernel. Returns y [n, c_mid, h_o, w_o]."""
     dt = _dtype_name(x)
     n, c, h, w = _dims(x, layout)
@@ -247,13 +279,13 @@ def pw_dw(x, w_pw, w_dw, b_pw=None, b_dw=None, *, stride=1, pad=None, act=("none
     d = make_desc(n, h, w, c, cm, cm, k, stride, pad, dt, layout, act, rq)
     ho, wo = out_hw(h, w, k, stride, pad)
     y = _out(x, layout, n, cm, ho, wo, out)
-    _check(lib().fcm_pw_dw(ctypes.byref(d), _ptr(x), _ptr(w_pw), _ptr(b_pw), _ptr(w_dw), _ptr(b_dw), _ptr(y),
-                           ctypes.byref(plan) if plan is not None else None, _stream(x, stream)))
-    return y
+    return _call(lib().fcm_pw_dw, (ctypes.byref(d), _ptr(x), _ptr(w_pw), _ptr(b_pw), _ptr(w_dw), _ptr(b_dw),
+                                   _ptr(y), _plan_arg(plan), _stream(x, stream)), y, prepare)
 
 
 def pw_dw_pw(x, w_pw1, w_dw, w_pw2, b_pw1=None, b_dw=None, b_pw2=None, *, stride=1, pad=None,
-             act=("none", "none", "none"), rq=None, layout="nchw", plan=None, out=None, stream=None):
+             act=("none", "none", "none"), rq=None, layout="nchw", plan=None, out=None, stream=None,
+             prepare=False):
     """PW -> DW -> PW inverted residual in one kernel. Returns y [n, c_out, h_o, w_o]."""
     dt = _dtype_name(x)
     n, c, h, w = _dims(x, layout)
@@ -264,14 +296,13 @@ def pw_dw_pw(x, w_pw1, w_dw, w_pw2, b_pw1=None, b_dw=None, b_pw2=None, *, stride
     d = make_desc(n, h, w, c, cm, co, k, stride, pad, dt, layout, act, rq)
     ho, wo = out_hw(h, w, k, stride, pad)
     y = _out(x, layout, n, co, ho, wo, out)
-    _check(lib().fcm_pw_dw_pw(ctypes.byref(d), _ptr(x), _ptr(w_pw1), _ptr(b_pw1), _ptr(w_dw), _ptr(b_dw),
-                              _ptr(w_pw2), _ptr(b_pw2), _ptr(y),
-                              ctypes.byref(plan) if plan is not None else None, _stream(x, stream)))
-    return y
+    return _call(lib().fcm_pw_dw_pw, (ctypes.byref(d), _ptr(x), _ptr(w_pw1), _ptr(b_pw1), _ptr(w_dw), _ptr(b_dw),
+                                      _ptr(w_pw2), _ptr(b_pw2), _ptr(y), _plan_arg(plan), _stream(x, stream)),
+                 y, prepare)
 
 
 def dw(x, w_dw, b_dw=None, *, stride=1, pad=None, act="none", rq=None, layout="nchw", plan=None, out=None,
-       stream=None):
+       stream=None, prepare=False):
     """Single depthwise layer (layer-by-layer kernel)."""
     dt = _dtype_name(x)
     n, c, h, w = _dims(x, layout)
@@ -281,12 +312,12 @@ def dw(x, w_dw, b_dw=None, *, stride=1, pad=None, act="none", rq=None, layout="n
     d = make_desc(n, h, w, c, c, c, k, stride, pad, dt, layout, (act,), [rq] if rq else None)
     ho, wo = out_hw(h, w, k, stride, pad)
     y = _out(x, layout, n, c, ho, wo, out)
-    _check(lib().fcm_dw(ctypes.byref(d), _ptr(x), _ptr(w_dw), _ptr(b_dw), _ptr(y),
-                        ctypes.byref(plan) if plan is not None else None, _stream(x, stream)))
-    return y
+    return _call(lib().fcm_dw, (ctypes.byref(d), _ptr(x), _ptr(w_dw), _ptr(b_dw), _ptr(y), _plan_arg(plan),
+                                _stream(x, stream)), y, prepare)
 
 
-def pw(x, w_pw, b_pw=None, *, act="none", rq=None, layout="nchw", plan=None, out=None, stream=None):
+def pw(x, w_pw, b_pw=None, *, act="none", rq=None, layout="nchw", plan=None, out=None, stream=None,
+       prepare=False):
     """Single pointwise layer (layer-by-layer kernel)."""
     dt = _dtype_name(x)
     n, c, h, w = _dims(x, layout)
@@ -294,9 +325,8 @@ def pw(x, w_pw, b_pw=None, *, act="none", rq=None, layout="nchw", plan=None, out
     _prep(x, [w_pw], [b_pw], dt)
     d = make_desc(n, h, w, c, c, co, 1, 1, 0, dt, layout, (act,), [rq] if rq else None)
     y = _out(x, layout, n, co, h, w, out)
-    _check(lib().fcm_pw(ctypes.byref(d), _ptr(x), _ptr(w_pw), _ptr(b_pw), _ptr(y),
-                        ctypes.byref(plan) if plan is not None else None, _stream(x, stream)))
-    return y
+    return _call(lib().fcm_pw, (ctypes.byref(d), _ptr(x), _ptr(w_pw), _ptr(b_pw), _ptr(y), _plan_arg(plan),
+                                _stream(x, stream)), y, prepare)
 
 
 # ------------------------------------------------------------------------------------
@@ -304,25 +334,47 @@ def pw(x, w_pw, b_pw=None, *, act="none", rq=None, layout="nchw", plan=None, out
 # intermediate feature map goes through device memory.
 # ------------------------------------------------------------------------------------
 
+class _Chain:
+    """Several prepared launches issued in order (a layer-by-layer chain)."""
+
+    def __init__(self, calls):
+        self.calls = calls
+        self.y = calls[-1].y
+
+    def __call__(self):
+        for c in self.calls:
+            c()
+        return self.y
+
+
 def dw_then_pw(x, w_dw, w_pw, b_dw=None, b_pw=None, *, stride=1, pad=None, act=("none", "none"), rq=None,
-               layout="nchw", mid=None, out=None, stream=None):
+               layout="nchw", mid=None, out=None, stream=None, prepare=False):
     rq = list(rq) if rq else [None, None]
-    m = dw(x, w_dw, b_dw, stride=stride, pad=pad, act=act[0], rq=rq[0], layout=layout, out=mid, stream=stream)
-    return pw(m, w_pw, b_pw, act=act[1], rq=rq[1], layout=layout, out=out, stream=stream)
+    c1 = dw(x, w_dw, b_dw, stride=stride, pad=pad, act=act[0], rq=rq[0], layout=layout, out=mid, stream=stream,
+            prepare=prepare)
+    m = c1.y if prepare else c1
+    c2 = pw(m, w_pw, b_pw, act=act[1], rq=rq[1], layout=layout, out=out, stream=stream, prepare=prepare)
+    return _Chain([c1, c2]) if prepare else c2
 
 
 def pw_then_dw(x, w_pw, w_dw, b_pw=None, b_dw=None, *, stride=1, pad=None, act=("none", "none"), rq=None,
-               layout="nchw", mid=None, out=None, stream=None):
+               layout="nchw", mid=None, out=None, stream=None, prepare=False):
     rq = list(rq) if rq else [None, None]
-    m = pw(x, w_pw, b_pw, act=act[0], rq=rq[0], layout=layout, out=mid, stream=stream)
-    return dw(m, w_dw, b_dw, stride=stride, pad=pad, act=act[1], rq=rq[1], layout=layout, out=out, stream=stream)
+    c1 = pw(x, w_pw, b_pw, act=act[0], rq=rq[0], layout=layout, out=mid, stream=stream, prepare=prepare)
+    m = c1.y if prepare else c1
+    c2 = dw(m, w_dw, b_dw, stride=stride, pad=pad, act=act[1], rq=rq[1], layout=layout, out=out, stream=stream,
+            prepare=prepare)
+    return _Chain([c1, c2]) if prepare else c2
 
 
 def pw_then_dw_then_pw(x, w_pw1, w_dw, w_pw2, b_pw1=None, b_dw=None, b_pw2=None, *, stride=1, pad=None,
                        act=("none", "none", "none"), rq=None, layout="nchw", mids=(None, None), out=None,
-                       stream=None):
+                       stream=None, prepare=False):
     rq = list(rq) if rq else [None, None, None]
-    m1 = pw(x, w_pw1, b_pw1, act=act[0], rq=rq[0], layout=layout, out=mids[0], stream=stream)
-    m2 = dw(m1, w_dw, b_dw, stride=stride, pad=pad, act=act[1], rq=rq[1], layout=layout, out=mids[1],
-            stream=stream)
-    return pw(m2, w_pw2, b_pw2, act=act[2], rq=rq[2], layout=layout, out=out, stream=stream)
+    c1 = pw(x, w_pw1, b_pw1, act=act[0], rq=rq[0], layout=layout, out=mids[0], stream=stream, prepare=prepare)
+    m1 = c1.y if prepare else c1
+    c2 = dw(m1, w_dw, b_dw, stride=stride, pad=pad, act=act[1], rq=rq[1], layout=layout, out=mids[1],
+            stream=stream, prepare=prepare)
+    m2 = c2.y if prepare else c2
+    c3 = pw(m2, w_pw2, b_pw2, act=act[2], rq=rq[2], layout=layout, out=out, stream=stream, prepare=prepare)
+    return _Chain([c1, c2, c3]) if prepare else c3

@@ -22,7 +22,9 @@ ARCH = "gfx950"
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-I" + CSRC, "-I" + INCLUDE, "-Wall", "-Wno-unused-function"]
 # Packed fp32 VALU instructions stay off: ordinary float code is enough here.
-DEVICE = ["--offload-arch=" + ARCH, "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+DEVICE = ["--offload-arch=" + ARCH, "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+          # matrix-core accumulators in ordinary VGPRs: no AGPR copies around each MFMA
+          "-mllvm", "-amdgpu-mfma-vgpr-form"]
 
 
 def sources():

@@ -4,6 +4,7 @@
 
 #include <cstdint>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -22,7 +23,10 @@ const Variant* all_variants(int* count) {
   static std::vector<Variant> all = [] {
     std::vector<Variant> v;
     const Variant* (*fns[])(int*) = {variants_dwpw_f32, variants_dwpw_bf16, variants_dwpw_i8, variants_pwdw,
-                                     variants_pwdwpw,   variants_v2_bf16,   variants_v2_f32,  variants_v2_i8};
+                                     variants_pwdwpw,   variants_v2_bf16,   variants_v2_f32,  variants_v2_i8,
+                                     variants_v3_dwpw_bf16_s1, variants_v3_dwpw_bf16_s2, variants_v3_dwpw_f32,
+                                     variants_v3_dwpw_i8, variants_v3_pw, variants_v3_pw_f32, variants_v3_pw_i8,
+                                     variants_v3_dw_bf16, variants_v3_dw_f32, variants_v3_dw_i8};
     for (auto fn : fns) {
       int n = 0;
       const Variant* t = fn(&n);
@@ -86,6 +90,30 @@ fcm_status validate(int op, const fcm_desc* d) {
 }
 
 static bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+#ifdef FCM_TRACE
+// Development builds only: device buffer that the persistent kernels write their
+// per-workgroup shader-clock timeline into.
+static unsigned long long* g_trace = nullptr;
+extern "C" void fcm_debug_trace(void* dev_buffer) { g_trace = (unsigned long long*)dev_buffer; }
+#endif
+
+// Compute units of the current device (queried once per device).
+static int device_cus() {
+  static std::mutex mu;
+  static std::vector<int> cache;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return default_hw().num_cus;
+  std::lock_guard<std::mutex> lock(mu);
+  if ((int)cache.size() <= dev) cache.resize(dev + 1, 0);
+  if (cache[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+      n = default_hw().num_cus;
+    cache[dev] = n;
+  }
+  return cache[dev];
+}
 
 static fcm_status check_alignment(const void* p, int elt, const char* what) {
   if (p && ((uintptr_t)p % (uintptr_t)elt) != 0)
@@ -182,7 +210,13 @@ static fcm_status run(int op, const fcm_desc* d, const Tensors& t, const fcm_pla
       break;
     default: break;
   }
-  if (v.gen == 2) {
+  a.nwork = a.N * a.tiles_y * a.tiles_x * a.n_cb;
+  a.cus = device_cus();
+  a.grid_cap = v.gen == 3 ? p.workgroups : 0;
+#ifdef FCM_TRACE
+  a.trace = g_trace;
+#endif
+  if (v.gen >= 2) {
     a.L = LdsLayout{};
     a.L.bytes = p.lds_bytes;
   } else switch (g.family) {

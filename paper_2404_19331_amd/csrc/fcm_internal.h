@@ -174,6 +174,44 @@ FCM_HD inline int lds_dw2(int dt, int K, int S, int TH, int TW) {
   return (npin + 15) / 16 * 1024 + ((K * K + 1) * (kRowB / e) * 4 + 15) / 16 * 16;
 }
 
+// Persistent NHWC kernels (k_fused3): module selector and LDS bytes of one buffer.
+enum { M3_DWPW = 0, M3_PW = 1, M3_DW = 2 };
+
+// Byte sizes and offsets of one LDS buffer of the persistent kernels (host and device):
+// the input window of IH rows at a pitch of IWP pixels of 64 bytes; the pointwise weight
+// block (16*CT rows of 64 bytes); the depthwise weights of one chunk as 32-bit
+// dot-operand words [K*K][CB]; the raw depthwise weights as copied ([CB][K*K] elements,
+// whole KiB); and two KiB of biases (depthwise, then pointwise). Three buffers.
+constexpr int kThreads3 = 320;  // one copy wave + four compute waves
+struct Lds3 {
+  int in_bytes, w_bytes, wd_off, raw_off, bias_off, buf_bytes, total;
+};
+FCM_HD inline Lds3 lds3p(int dt, int K, int mode, int IH, int IWP, int CT) {
+  Lds3 r;
+  const int cb = kRowB / elt_size(dt);
+  r.in_bytes = IH * IWP * kRowB;
+  r.w_bytes = mode == M3_DW ? 0 : CT * 1024;
+  int off = r.in_bytes + r.w_bytes;
+  r.wd_off = off;
+  if (mode != M3_PW) off += (K * K * cb * 4 + 15) / 16 * 16;
+  r.raw_off = off;
+  if (mode != M3_PW) off += (64 * K * K + 1023) / 1024 * 1024;
+  r.bias_off = off;
+  off += 2048;
+  r.buf_bytes = off;
+  r.total = 3 * off;
+  return r;
+}
+
+// Copy instructions the copy wave of a persistent kernel issues per item (host and
+// device); a partial wait on the vector-memory counter covers at most 63 of them.
+FCM_HD inline int copies_per_item3(int mode, int K, int IH, int IWP, int CT) {
+  int n = IH * (IWP / 16);
+  if (mode != M3_DW) n += CT + 1;                          // PW weight rows, PW bias
+  if (mode != M3_PW) n += (64 * K * K + 1023) / 1024 + 1;  // raw DW weights, DW bias
+  return n;
+}
+
 // ---------------------------------------------------------------------------------
 // Kernel argument block (one struct for all families; unused fields ignored).
 // ---------------------------------------------------------------------------------
@@ -196,6 +234,10 @@ struct KArgs {
   Requant rq[3];
   int vec_x, vec_w1, vec_w2, vec_w3, vec_y;
   LdsLayout L;
+  int nwork;     // persistent kernels: work tiles (image x tile x channel block)
+  int cus;       // compute units of the device
+  int grid_cap;  // persistent kernels: at most this many workgroups (0 = no cap)
+  unsigned long long* trace;  // development timeline buffer (used only in FCM_TRACE builds)
 };
 
 // One compiled kernel instance and the tilings it implements.
@@ -215,6 +257,8 @@ struct Variant {
   int tile_h = 0;   // compile-time tile (0 = chosen at run time)
   int tile_w = 0;
   int gen = 1;      // 2: NHWC, 16-byte channel rows, LDS-DMA staging, fixed chunk of 64 bytes
+                    // 3: as 2, persistent workgroups, run-time tile, max_p = 64 * blocks per wave
+  int pitch = 0;    // gen 3: LDS window row pitch in pixels (window width must not exceed it)
 };
 
 // Compiled variants of each translation unit, and all of them in a fixed order
@@ -227,6 +271,16 @@ const Variant* variants_pwdwpw(int* count);
 const Variant* variants_v2_bf16(int* count);
 const Variant* variants_v2_f32(int* count);
 const Variant* variants_v2_i8(int* count);
+const Variant* variants_v3_dwpw_bf16_s1(int* count);
+const Variant* variants_v3_dwpw_bf16_s2(int* count);
+const Variant* variants_v3_dwpw_f32(int* count);
+const Variant* variants_v3_dwpw_i8(int* count);
+const Variant* variants_v3_pw(int* count);
+const Variant* variants_v3_pw_f32(int* count);
+const Variant* variants_v3_pw_i8(int* count);
+const Variant* variants_v3_dw_bf16(int* count);
+const Variant* variants_v3_dw_f32(int* count);
+const Variant* variants_v3_dw_i8(int* count);
 const Variant* all_variants(int* count);
 
 }  // namespace fcm

@@ -1,0 +1,578 @@
+// fcm_kernels_v3.h -- persistent NHWC kernels for gfx950: DW->PW module, and the
+// layer-by-layer PW and DW kernels built from the same pieces.
+//
+// k_fused3<DT, K, S, BPW, CT, MODE>
+//   A persistent workgroup (4 waves) owns a contiguous range of work tiles; a work tile
+//   is (image, TH x TW output tile, block of 16*CT output channels). Work tiles are cut
+//   into items, one per input-channel chunk of 64 bytes (one MFMA k-step); the items of
+//   the whole range form one stream, and the copy of item i+1 (global -> LDS with
+//   buffer_load ... lds, out-of-range offsets read as zero, i.e. the zero padding of the
+//   convolution) overlaps the arithmetic of item i, across tile boundaries as well.
+//
+//   Lane l of wave w owns, in each of its BPW pixel blocks, output pixel (l % 16) of the
+//   block and the 16 bytes of channels (l / 16) of the chunk: exactly the MFMA B operand
+//   the lane supplies. The depthwise stencil is computed straight into that operand, so
+//   the DW output never leaves the registers (the paper's on-chip communication buffer,
+//   Sec. III-B). Its multiply-adds use the packed dot instructions with one half of the
+//   weight operand zero (bf16: v_dot2c_f32_bf16, int8: v_dot4c_i32_i8), so no unpacking
+//   of the packed input is needed.
+//
+//   The pointwise weights rows are staged in a permuted order such that the accumulator
+//   lane (l % 16, l / 16) ends up holding 4*CT consecutive output channels of its pixel:
+//   the epilogue (+bias, activation, cast) writes them with 16-byte stores straight from
+//   registers, and the output is written once (output-stationary, Sec. III-A OS-LWS).
+//
+//   MODE M3_PW: the DW stage is off (window = output tile); M3_DW: the PW stage is off,
+//   each lane writes its 16 bytes of depthwise output directly.
+//
+// LDS per buffer (two buffers): window [npin pixels][64 B] (pixel q at 64 q, no padding;
+// stride-2 windows keep even and odd columns in separate halves so that the lanes of a
+// block read consecutive pixels), PW weights [16*CT rows][64 B] (16-byte slots XOR-
+// swizzled by row bit 3, conflict-free MFMA A reads), DW weights [K*K taps][CB] 32-bit
+// values in dot-operand form + bias [CB].
+#pragma once
+
+#include "fcm_kernels_v2.h"
+
+namespace fcm {
+
+#ifdef FCM_TRACE
+// Development builds only: the first lane of the copy wave (slots 0..31) and of the first
+// compute wave (slots 32..63) record the shader clock at fixed points ([workgroup][64]).
+#define FCM_TS_AT(tid, slot)                                                              \
+  do {                                                                                    \
+    const int ts_slot_ = (slot);                                                          \
+    if (a.trace && threadIdx.x == (tid) && ts_slot_ < 64)                                 \
+      a.trace[blockIdx.x * 64 + ts_slot_] = __builtin_amdgcn_s_memtime();                 \
+  } while (0)
+#else
+#define FCM_TS_AT(tid, slot) \
+  do {                       \
+  } while (0)
+#endif
+#define FCM_TS(slot) FCM_TS_AT(0, slot)
+#define FCM_TSC(slot) FCM_TS_AT(64, slot)
+
+constexpr int kNiwMax = 10;  // window copy instructions per wave (<= 640 window pixels)
+
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+
+// Branch-free epilogue of a convolution stage. Float paths: activation as a clamp to
+// [lo, hi] (NONE: unbounded, RELU: [0, inf), RELU6: [0, 6]). Int8: requantisation
+// (round half to even of acc * mult / 2^shift) and a clamp to [qlo, qhi], which is the
+// saturation range with ReLU folded in (relu(clamp(q, a, b)) = clamp(q, max(a,0), max(b,0))).
+struct Epi3 {
+  float lo, hi;
+  int32_t mult, shift, qlo, qhi;
+};
+__device__ __forceinline__ Epi3 make_epi3(int act, const Requant& rq) {
+  Epi3 e;
+  e.lo = act == ACT_NONE ? -__builtin_huge_valf() : 0.0f;
+  e.hi = act == ACT_RELU6 ? 6.0f : __builtin_huge_valf();
+  e.mult = rq.mult;
+  e.shift = rq.shift;
+  e.qlo = act == ACT_RELU ? max(rq.qmin, 0) : rq.qmin;
+  e.qhi = act == ACT_RELU ? max(rq.qmax, 0) : rq.qmax;
+  return e;
+}
+__device__ __forceinline__ float epi_f(float v, const Epi3& e) { return __builtin_amdgcn_fmed3f(v, e.lo, e.hi); }
+__device__ __forceinline__ int32_t epi_i(int32_t acc, const Epi3& e) {
+  const int64_t t = (int64_t)acc * e.mult;
+  const int64_t half = ((int64_t)1 << e.shift) >> 1;
+  const int64_t rnd = e.shift > 0 ? half - 1 + ((t >> e.shift) & 1) : 0;
+  int64_t q = (t + rnd) >> e.shift;
+  q = q < e.qlo ? e.qlo : q;
+  q = q > e.qhi ? e.qhi : q;
+  return (int32_t)q;
+}
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+  const f32x2_t v = {a, b};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_t));
+}
+
+// Depthwise arithmetic on one 16-byte lane slot of channels.
+template <class DT>
+struct Dw3;
+
+template <>
+struct Dw3<TF32> {
+  static constexpr int CPL = 4;  // channels per 16-byte slot
+  static constexpr int WQ = 1;   // 16-byte weight reads per tap and lane
+  __device__ static __forceinline__ uint32_t weight_word(uint32_t raw, int) { return raw; }
+  __device__ static __forceinline__ void tap(float (&acc)[4], const u32x4& x, const u32x4 (&w)[1]) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) acc[e] = __builtin_fmaf(__uint_as_float(x[e]), __uint_as_float(w[0][e]), acc[e]);
+  }
+  __device__ static __forceinline__ u32x4 finish(const float (&acc)[4], const Epi3& ep) {
+    u32x4 r;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) r[e] = __float_as_uint(epi_f(acc[e], ep));
+    return r;
+  }
+};
+
+template <>
+struct Dw3<TBF16> {
+  static constexpr int CPL = 8;
+  static constexpr int WQ = 2;
+  // dot operand for channel c: the weight in the half that multiplies channel c's half of
+  // the packed input pair, zero in the other half
+  __device__ static __forceinline__ uint32_t weight_word(uint32_t raw, int c) {
+    return (c & 1) ? (raw << 16) : (raw & 0xffffu);
+  }
+  __device__ static __forceinline__ void tap(float (&acc)[8], const u32x4& x, const u32x4 (&w)[2]) {
+    // (vector elements are copied to scalars before __builtin_bit_cast: applied to a vector
+    // element expression directly, the cast reads element 0)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const uint32_t xs = x[e >> 1], ws = w[e >> 2][e & 3];
+      acc[e] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, xs), __builtin_bit_cast(bf16x2_t, ws),
+                                               acc[e], false);
+    }
+  }
+  __device__ static __forceinline__ u32x4 finish(const float (&acc)[8], const Epi3& ep) {
+    u32x4 r;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) r[j] = pack_bf16x2(epi_f(acc[2 * j], ep), epi_f(acc[2 * j + 1], ep));
+    return r;
+  }
+};
+
+template <>
+struct Dw3<TI8> {
+  static constexpr int CPL = 16;
+  static constexpr int WQ = 4;
+  __device__ static __forceinline__ uint32_t weight_word(uint32_t raw, int c) { return (raw & 0xffu) << (8 * (c & 3)); }
+  __device__ static __forceinline__ void tap(int32_t (&acc)[16], const u32x4& x, const u32x4 (&w)[4]) {
+#pragma unroll
+    for (int e = 0; e < 16; ++e)
+      acc[e] = __builtin_amdgcn_sdot4((int)x[e >> 2], (int)w[e >> 2][e & 3], acc[e], false);
+  }
+  __device__ static __forceinline__ u32x4 finish(const int32_t (&acc)[16], const Epi3& ep) {
+    u32x4 r;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      uint32_t wv = 0;
+#pragma unroll
+      for (int b = 0; b < 4; ++b) wv |= ((uint32_t)epi_i(acc[4 * j + b], ep) & 0xffu) << (8 * b);
+      r[j] = wv;
+    }
+    return r;
+  }
+};
+
+// s_waitcnt vmcnt(n) with the other counters left alone, for a run-time n in [0, 63]:
+// gfx9 encoding vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] | vmcnt[5:4] << 14.
+template <int N>
+__device__ __forceinline__ void wait_vm_n() {
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | (((N >> 4) & 3) << 14));
+}
+// s_waitcnt lgkmcnt(0) only (LDS operations of this wave are complete).
+__device__ __forceinline__ void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (0 << 8) | (3 << 14)); }
+// Workgroup barrier without the memory fences of __syncthreads: a release fence would
+// make the copy wave wait for all of its outstanding copies (they are LDS writes). The
+// waits each side needs are explicit; the empty asm statements keep the compiler from
+// moving memory accesses across the barrier.
+__device__ __forceinline__ void barrier3() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+__device__ __forceinline__ void wait_vm(int n) {
+  switch (n) {
+#define FCM_W4(b) \
+  case b: wait_vm_n<b>(); break; \
+  case b + 1: wait_vm_n<b + 1>(); break; \
+  case b + 2: wait_vm_n<b + 2>(); break; \
+  case b + 3: wait_vm_n<b + 3>(); break;
+    FCM_W4(0) FCM_W4(4) FCM_W4(8) FCM_W4(12) FCM_W4(16) FCM_W4(20) FCM_W4(24) FCM_W4(28)
+    FCM_W4(32) FCM_W4(36) FCM_W4(40) FCM_W4(44) FCM_W4(48) FCM_W4(52) FCM_W4(56) FCM_W4(60)
+#undef FCM_W4
+    default: wait_vm_n<0>(); break;
+  }
+}
+
+template <class DT, int K, int S, int BPW, int CT, int MODE, int IWP>
+__global__ __launch_bounds__(kThreads3) void k_fused3(KArgs a) {
+  extern __shared__ __align__(16) char smem[];
+  using T = typename DT::T;
+  using Acc = typename DT::Acc;
+  using AccV = typename DT::AccV;
+  using D3 = Dw3<DT>;
+  constexpr bool HAS_DW = MODE != M3_PW;
+  constexpr bool HAS_PW = MODE != M3_DW;
+  constexpr int KE = HAS_DW ? K : 1, SE = HAS_DW ? S : 1;
+  constexpr int KK = KE * KE;
+  constexpr int CB = kRowB / DT::ELT;  // channels per chunk
+  constexpr int CPL = D3::CPL;
+  constexpr int WQ = D3::WQ;
+  constexpr int IPR = IWP / 16;  // copy instructions per window row
+  constexpr int NRAW = (64 * K * K + 1023) / 1024;
+  static_assert(CPL * 4 == CB, "lane slot layout");
+  static_assert(IWP % 16 == 0, "window pitch");
+
+  const int TH = a.TH, TW = a.TW, P = TH * TW;
+  const int IW = HAS_DW ? (TW - 1) * SE + KE : TW;
+  const int IH = HAS_DW ? (TH - 1) * SE + KE : TH;
+  const int nins = IH * IPR;
+  const Lds3 lay = lds3p(dtype_id<DT>(), KE, MODE, IH, IWP, CT);
+  const int C = MODE == M3_DW ? a.Cm : a.Ci;
+  const int nchunks = MODE == M3_DW ? 1 : ceil_div(C, CB);
+  const int per_item = copies_per_item3(MODE, KE, IH, IWP, CT);
+
+  // ---- work range of this workgroup (consecutive logical ids share an XCD) ----
+  const int G = gridDim.x;
+  const int L = xcd_remap(blockIdx.x, G);
+  const int wt0 = (int)((int64_t)a.nwork * L / G), wt1 = (int)((int64_t)a.nwork * (L + 1) / G);
+  if (wt1 <= wt0) return;
+  const int nitems = (wt1 - wt0) * nchunks;
+
+  // wave 0 copies, waves 1..4 compute; the wave index is uniform: keep it scalar
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  const int r16 = lane & 15, g = lane >> 4;
+  const bool producer = wave == 0;
+  const int cw = wave - 1;  // compute-wave index
+
+  const T* x = (const T*)a.x;
+  const size_t img = (size_t)a.H * a.W * C;
+  const T* wp = (const T*)(MODE == M3_PW ? a.w1 : a.w2);
+  const T* wd = (const T*)a.w1;
+  const void* bd = a.b1;
+  const void* bp = MODE == M3_PW ? a.b1 : a.b2;
+  const int CoB = 16 * CT;
+
+  struct Tile {
+    int n, oy0, ox0, cb;  // cb: output-channel block (DW: channel chunk)
+  };
+  auto decode = [&](int wt) {
+    Tile r;
+    int t = wt;
+    r.cb = t % a.n_cb;
+    t /= a.n_cb;
+    const int tx = t % a.tiles_x;
+    t /= a.tiles_x;
+    const int ty = t % a.tiles_y;
+    r.n = t / a.tiles_y;
+    r.oy0 = ty * TH;
+    r.ox0 = tx * TW;
+    return r;
+  };
+  auto bufp = [&](int it) { return smem + (it % 3) * lay.buf_bytes; };
+
+  int tsi = 0;
+  FCM_TS(tsi++);
+
+  if (producer) {
+    // ======================= producer: all copies, three items deep ================
+    const rsrc_t rw = make_rsrc(wp, HAS_PW ? (uint32_t)((size_t)a.Co * a.Ci * DT::ELT) : 0u);
+    const rsrc_t rwd = make_rsrc(wd, HAS_DW ? (uint32_t)((size_t)C * KK * DT::ELT) : 0u);
+    const rsrc_t rbd = make_rsrc(bd ? bd : (const void*)wd, (HAS_DW && bd) ? (uint32_t)(C * 4) : 0u);
+    const rsrc_t rbp = make_rsrc(bp ? bp : (const void*)wp, (HAS_PW && bp) ? (uint32_t)(a.Co * 4) : 0u);
+    int wxl[IPR];
+#pragma unroll
+    for (int j = 0; j < IPR; ++j) {
+      const int col = j * 16 + (lane >> 2);
+      int wx = col;
+      if (SE == 2) wx = col < IWP / 2 ? 2 * col : 2 * (col - IWP / 2) + 1;
+      wxl[j] = wx < IW ? wx : -1;
+    }
+    int iss = 0, iss_wt = wt0, iss_ch = 0;
+    Tile iss_t = decode(wt0);
+    auto issue_next = [&]() {
+      char* buf = bufp(iss);
+      const int c0 = MODE == M3_DW ? iss_t.cb * CB : iss_ch * CB;
+      const int co0 = iss_t.cb * CoB;
+      const int iy0 = HAS_DW ? iss_t.oy0 * SE - a.pad : iss_t.oy0;
+      const int ix0 = HAS_DW ? iss_t.ox0 * SE - a.pad : iss_t.ox0;
+      const rsrc_t rx = make_rsrc(x + (size_t)iss_t.n * img, (uint32_t)(img * DT::ELT));
+      const int c = c0 + (lane & 3) * CPL;
+      for (int ins = 0; ins < nins; ++ins) {
+        const int wy = ins / IPR;
+        const int wx = wxl[IPR == 1 ? 0 : ins % IPR];
+        const int gy = iy0 + wy, gx = ix0 + wx;
+        const bool ok = wx >= 0 && (unsigned)gy < (unsigned)a.H && (unsigned)gx < (unsigned)a.W && c < C;
+        dma16(rx, buf + ins * 1024, ok ? (uint32_t)(((gy * a.W + gx) * C + c) * DT::ELT) : kOob);
+      }
+      if constexpr (HAS_PW) {
+        const int mrow = lane >> 2;
+        const int j = (lane & 3) ^ (((mrow >> 3) & 1) << 1);
+        const int cw_ = c0 + j * CPL;
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct) {
+          const int co = co0 + 4 * CT * (mrow >> 2) + 4 * ct + (mrow & 3);
+          const bool ok = co < a.Co && cw_ < a.Ci;
+          dma16(rw, buf + lay.in_bytes + ct * 1024, ok ? (uint32_t)((co * a.Ci + cw_) * DT::ELT) : kOob);
+        }
+        dma16(rbp, buf + lay.bias_off + 1024, lane * 16 < CoB * 4 ? (uint32_t)(co0 * 4 + lane * 16) : kOob);
+      }
+      if constexpr (HAS_DW) {
+#pragma unroll
+        for (int r = 0; r < NRAW; ++r) {
+          const int b = r * 1024 + lane * 16;
+          dma16(rwd, buf + lay.raw_off + r * 1024,
+                b < CB * KK * DT::ELT ? (uint32_t)(c0 * KK * DT::ELT + b) : kOob);
+        }
+        dma16(rbd, buf + lay.bias_off, lane * 16 < CB * 4 ? (uint32_t)(c0 * 4 + lane * 16) : kOob);
+      }
+      ++iss;
+      if (++iss_ch == nchunks) {
+        iss_ch = 0;
+        if (++iss_wt < wt1) iss_t = decode(iss_wt);
+      }
+    };
+    // depthwise weights of item `it`: raw [c][tap] elements -> [tap][c] dot-operand words
+    auto convert = [&](int it) {
+      if constexpr (HAS_DW) {
+        char* buf = bufp(it);
+        const char* raw = buf + lay.raw_off;
+        uint32_t* dst = (uint32_t*)(buf + lay.wd_off);
+#pragma unroll 4
+        for (int i = lane; i < KK * CB; i += 64) {
+          const int ci = i % CB, tap = i / CB;
+          const int e = ci * KK + tap;
+          uint32_t rv;
+          if constexpr (DT::ELT == 4)
+            rv = ((const uint32_t*)raw)[e];
+          else if constexpr (DT::ELT == 2)
+            rv = ((const uint16_t*)raw)[e];
+          else
+            rv = (uint32_t)((const uint8_t*)raw)[e];
+          dst[i] = D3::weight_word(rv, ci);
+        }
+      }
+    };
+    issue_next();
+    if (nitems > 1) issue_next();
+    wait_vm(nitems > 1 ? per_item : 0);
+    convert(0);
+    wait_lgkm0();
+    barrier3();
+    FCM_TS(tsi++);
+    for (int it = 0; it < nitems; ++it) {
+      if (it + 2 < nitems) issue_next();
+      FCM_TS(tsi++);
+      if (it + 1 < nitems) {
+        wait_vm(it + 2 < nitems ? per_item : 0);
+        convert(it + 1);
+      }
+      wait_lgkm0();
+      FCM_TS(tsi++);
+      barrier3();
+      FCM_TS(tsi++);
+    }
+    return;
+  }
+
+  // ========================== compute waves ==========================================
+  int base[BPW], pyx[BPW];
+#pragma unroll
+  for (int b = 0; b < BPW; ++b) {
+    int p = (b * 4 + cw) * 16 + r16;
+    const bool ok = p < P;
+    if (!ok) p = P - 1;
+    const int py = p / TW, px = p - py * TW;
+    pyx[b] = ok ? (py << 16) | px : -1;
+    base[b] = (py * SE * IWP + px) * kRowB + g * 16;
+  }
+  int nblk = 0;  // blocks holding at least one pixel of the tile (wave-uniform)
+#pragma unroll
+  for (int b = 0; b < BPW; ++b)
+    if ((b * 4 + cw) * 16 < P) nblk = b + 1;
+  const int a_row = r16 * kRowB + ((g ^ (((r16 >> 3) & 1) << 1)) * 16);  // swizzled MFMA A slot
+  const Epi3 ep_dw = make_epi3(a.act[0], a.rq[0]);
+  const Epi3 ep_pw = MODE == M3_PW ? ep_dw : make_epi3(a.act[1], a.rq[1]);
+
+  AccV acc[BPW][CT];
+#pragma unroll
+  for (int b = 0; b < BPW; ++b)
+#pragma unroll
+    for (int i = 0; i < CT; ++i) acc[b][i] = AccV{0, 0, 0, 0};
+  u32x4 bop[BPW];
+
+  barrier3();  // item 0 is ready
+  int tsc = 32;
+  FCM_TSC(tsc++);
+  int wt = wt0, ch = 0;
+  Tile cur_t = decode(wt0);
+  for (int it = 0; it < nitems; ++it) {
+    const char* buf = bufp(it);
+    // B operand of each block: depthwise output of this lane's pixel and channel slot
+    // (or the staged input itself for the PW kernel), then the PW contraction. The
+    // number of blocks holding pixels is a compile-time constant of each instance of
+    // `step`, so the unrolled loops carry no branches and the LDS reads of all taps
+    // can be scheduled ahead of the arithmetic.
+    auto step = [&](auto nb_tag) {
+      constexpr int NB = decltype(nb_tag)::value;
+      if constexpr (HAS_DW) {
+        Acc dacc[NB][CPL];
+        const char* wl = buf + lay.wd_off;
+        {
+          u32x4 bv[WQ];
+#pragma unroll
+          for (int q = 0; q < WQ; ++q) bv[q] = *(const u32x4*)(buf + lay.bias_off + (g * CPL + 4 * q) * 4);
+#pragma unroll
+          for (int b = 0; b < NB; ++b)
+#pragma unroll
+            for (int e = 0; e < CPL; ++e) {
+              const uint32_t u = bv[e >> 2][e & 3];
+              dacc[b][e] = __builtin_bit_cast(Acc, u);
+            }
+        }
+        const char* xb[NB];
+#pragma unroll
+        for (int b = 0; b < NB; ++b) xb[b] = buf + base[b];
+#pragma unroll
+        for (int ky = 0; ky < KE; ++ky) {
+#pragma unroll
+          for (int kx = 0; kx < KE; ++kx) {
+            const int toff = (ky * IWP + (SE == 2 ? (kx & 1) * (IWP / 2) + (kx >> 1) : kx)) * kRowB;
+            u32x4 wv[WQ];
+#pragma unroll
+            for (int q = 0; q < WQ; ++q) wv[q] = *(const u32x4*)(wl + ((ky * KE + kx) * CB + g * CPL + 4 * q) * 4);
+#pragma unroll
+            for (int b = 0; b < NB; ++b) D3::tap(dacc[b], *(const u32x4*)(xb[b] + toff), wv);
+          }
+        }
+#pragma unroll
+        for (int b = 0; b < NB; ++b) bop[b] = D3::finish(dacc[b], ep_dw);
+      } else {
+#pragma unroll
+        for (int b = 0; b < NB; ++b) bop[b] = *(const u32x4*)(buf + base[b]);
+      }
+      if constexpr (HAS_PW) {
+        const char* wl = buf + lay.in_bytes;
+#pragma unroll
+        for (int i = 0; i < CT; ++i) {
+          const u32x4 av = *(const u32x4*)(wl + i * 1024 + a_row);
+#pragma unroll
+          for (int b = 0; b < NB; ++b) mma16(DT{}, acc[b][i], av, bop[b]);
+        }
+      }
+    };
+    if (nblk >= BPW) {
+      step(std::integral_constant<int, BPW>{});
+    } else if constexpr (BPW > 1) {
+      if (nblk == 1) step(std::integral_constant<int, 1>{});
+      else if (BPW > 2 && nblk == 2) step(std::integral_constant<int, (BPW > 2 ? 2 : 1)>{});
+      else if (BPW > 3 && nblk == 3) step(std::integral_constant<int, (BPW > 3 ? 3 : 1)>{});
+    }
+
+    if (ch + 1 == nchunks) {
+      // ---- epilogue of the work tile: straight from registers to global memory ----
+      if constexpr (MODE == M3_DW) {
+        const int c = cur_t.cb * CB + g * CPL;
+#pragma unroll
+        for (int b = 0; b < BPW; ++b) {
+          const int v = pyx[b];
+          const int oy = cur_t.oy0 + (v >> 16), ox = cur_t.ox0 + (v & 0xffff);
+          if (v >= 0 && oy < a.Ho && ox < a.Wo && c < C)
+            *(u32x4*)((T*)a.y + (((size_t)cur_t.n * a.Ho + oy) * a.Wo + ox) * C + c) = bop[b];
+        }
+      } else {
+        // this lane's output channels: co_l .. co_l + 4*CT - 1, contiguous
+        const int co_l = cur_t.cb * CoB + 4 * CT * g;
+        const int nvalid = min(4 * CT, a.Co - co_l);
+        if (nvalid > 0) {
+          Acc bias[4 * CT];
+          {
+            const char* bl = buf + lay.bias_off + 1024 + 4 * CT * g * 4;  // bias block of this co-block
+#pragma unroll
+            for (int q = 0; q < CT; ++q) {
+              const u32x4 bv = *(const u32x4*)(bl + 16 * q);
+#pragma unroll
+              for (int e = 0; e < 4; ++e) {
+                const uint32_t u = bv[e];
+                bias[4 * q + e] = __builtin_bit_cast(Acc, u);
+              }
+            }
+          }
+          constexpr int NW = 4 * CT * DT::ELT / 4;  // 32-bit words of this lane's output run
+          const bool full16 = (a.Co * DT::ELT) % 16 == 0;
+          const int vbytes = nvalid * DT::ELT;
+#pragma unroll
+          for (int b = 0; b < BPW; ++b) {
+            const int v = pyx[b];
+            const int oy = cur_t.oy0 + (v >> 16), ox = cur_t.ox0 + (v & 0xffff);
+            if (b >= nblk || v < 0 || oy >= a.Ho || ox >= a.Wo) continue;
+            uint32_t wds[NW];
+            if constexpr (DT::ELT == 4) {
+#pragma unroll
+              for (int i = 0; i < CT; ++i)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) wds[4 * i + e] = __float_as_uint(epi_f(acc[b][i][e] + bias[4 * i + e], ep_pw));
+            } else if constexpr (DT::ELT == 2) {
+#pragma unroll
+              for (int i = 0; i < CT; ++i)
+#pragma unroll
+                for (int e = 0; e < 4; e += 2)
+                  wds[2 * i + e / 2] = pack_bf16x2(epi_f(acc[b][i][e] + bias[4 * i + e], ep_pw),
+                                                   epi_f(acc[b][i][e + 1] + bias[4 * i + e + 1], ep_pw));
+            } else {
+#pragma unroll
+              for (int i = 0; i < CT; ++i) {
+                uint32_t wv = 0;
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                  wv |= ((uint32_t)epi_i(acc[b][i][e] + bias[4 * i + e], ep_pw) & 0xffu) << (8 * e);
+                wds[i] = wv;
+              }
+            }
+            char* dst = (char*)a.y + ((((size_t)cur_t.n * a.Ho + oy) * a.Wo + ox) * a.Co + co_l) * DT::ELT;
+            if (full16) {
+#pragma unroll
+              for (int k = 0; k < NW / 4; ++k)
+                if (16 * k < vbytes)
+                  *(u32x4*)(dst + 16 * k) = u32x4{wds[4 * k], wds[4 * k + 1], wds[4 * k + 2], wds[4 * k + 3]};
+            } else {
+#pragma unroll
+              for (int k = 0; k < NW; ++k)
+                if (4 * k < vbytes) *(uint32_t*)(dst + 4 * k) = wds[k];
+            }
+          }
+        }
+#pragma unroll
+        for (int b = 0; b < BPW; ++b)
+#pragma unroll
+          for (int i = 0; i < CT; ++i) acc[b][i] = AccV{0, 0, 0, 0};
+      }
+      ch = 0;
+      if (++wt < wt1) cur_t = decode(wt);
+    } else {
+      ++ch;
+    }
+    wait_lgkm0();
+    FCM_TSC(tsc++);
+    barrier3();  // item it+1 is ready; this item's buffer may be refilled
+    FCM_TSC(tsc++);
+  }
+}
+
+template <class DT, int K, int S, int BPW, int CT, int MODE, int IWP>
+int launch_fused3(const KArgs& a, int grid, void* stream) {
+  auto fn = k_fused3<DT, K, S, BPW, CT, MODE, IWP>;
+  const int lds = a.L.bytes;
+  if (lds > 65536) {
+    hipError_t e = hipFuncSetAttribute((const void*)fn, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+    if (e != hipSuccess) return (int)e;
+  }
+  // persistent grid: as many workgroups as are resident at once, at most one per work tile
+  static thread_local int cached_lds = -1, cached_occ = 1;
+  if (cached_lds != lds) {
+    int occ = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, (const void*)fn, kThreads3, lds) != hipSuccess || occ < 1)
+      occ = 1;
+    cached_lds = lds;
+    cached_occ = occ;
+  }
+  int g = a.cus * cached_occ;
+  if (a.grid_cap > 0 && g > a.grid_cap) g = a.grid_cap;
+  if (g > a.nwork) g = a.nwork;
+  if (g < 1) g = 1;
+  (void)grid;
+  hipLaunchKernelGGL(fn, dim3(g), dim3(kThreads3), lds, (hipStream_t)stream, a);
+  return (int)hipGetLastError();
+}
+
+}  // namespace fcm

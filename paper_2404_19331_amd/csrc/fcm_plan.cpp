@@ -161,7 +161,26 @@ static int tiling_lds(const Variant& v, const Geom& g, int TH, int TW, int CB, i
   const int P = TH * TW;
   const int Q = ((TH - 1) * g.s + g.k) * ((TW - 1) * g.s + g.k);
   if (v.max_p && P > v.max_p) return 0;
-  if (v.max_q && Q > v.max_q) return 0;
+  if (v.gen != 3 && v.max_q && Q > v.max_q) return 0;
+  if (v.gen == 3) {
+    // NHWC, 16-byte input channel rows, 32-bit buffer offsets, 64-byte chunk, run-time
+    // tile whose input window fits the kernel's LDS row pitch
+    if (g.layout != FCM_NHWC) return 0;
+    const bool dw_only = g.family == FAM_DW;
+    const int cin = dw_only ? g.cm : g.ci;
+    if ((cin * g.elt) % 16) return 0;
+    if (dw_only ? (g.cm * g.elt) % 16 : (g.co * g.elt) % 4) return 0;
+    if ((int64_t)g.h * g.w * cin * g.elt >= ((int64_t)1 << 31)) return 0;
+    if (!dw_only && (int64_t)g.co * g.ci * g.elt >= ((int64_t)1 << 31)) return 0;
+    if (CB != 64 / g.elt || COB != v.max_cob) return 0;
+    if (P > v.max_p) return 0;
+    const int mode = g.family == FAM_DWPW ? M3_DWPW : (g.family == FAM_PW ? M3_PW : M3_DW);
+    const int IW = mode == M3_PW ? TW : (TW - 1) * g.s + g.k;
+    const int IH = mode == M3_PW ? TH : (TH - 1) * g.s + g.k;
+    if (IW > v.pitch) return 0;
+    if (copies_per_item3(mode, mode == M3_PW ? 1 : g.k, IH, v.pitch, COB / 16) > 63) return 0;
+    return lds3p(g.dtype, mode == M3_PW ? 1 : g.k, mode, IH, v.pitch, COB / 16).total;
+  }
   if (v.gen == 2) {
     // NHWC, 16-byte channel rows, 32-bit buffer offsets, fixed tile and 64-byte chunk
     if (g.layout != FCM_NHWC || TH != v.tile_h || TW != v.tile_w) return 0;
@@ -196,7 +215,7 @@ static int tiling_lds(const Variant& v, const Geom& g, int TH, int TW, int CB, i
 bool variant_needs_alignment(int variant) {
   int nv = 0;
   const Variant* vs = all_variants(&nv);
-  return variant >= 0 && variant < nv && vs[variant].gen == 2;
+  return variant >= 0 && variant < nv && vs[variant].gen >= 2;
 }
 
 static bool variant_matches(const Variant& v, const Geom& g) {
@@ -220,6 +239,22 @@ fcm_status evaluate_plan(const Geom& g, const fcm_desc* d, const fcm_hw_desc& hw
   const int64_t wgs = (int64_t)g.n * nty * ntx * ceil_div(last, p->co_block);
   if (wgs <= 0 || wgs > 0x7fffffff) return fail(FCM_EUNSUPPORTED, "plan: grid too large");
   const Bytes b = module_bytes(g, p->tile_h, p->tile_w, p->co_block);
+  if (v.gen == 3) {
+    // persistent: the workgroups resident at once (LDS-limited estimate; the launcher
+    // also applies the compiled kernel's register-limited occupancy), at most one per
+    // work tile
+    const int64_t per_cu = std::max<int64_t>(1, std::min<int64_t>(8, hw.lds_per_cu / lds));
+    int64_t grid = std::min<int64_t>(wgs, per_cu * hw.num_cus);
+    if (p->workgroups > 0 && p->workgroups < grid) grid = p->workgroups;  // caller's cap
+    p->workgroups = (int32_t)grid;
+    p->waves = 4;
+    p->lds_bytes = lds;
+    p->bytes_ideal = b.ideal;
+    p->bytes_tiled = b.tiled;
+    p->bytes_paper = b.paper;
+    p->redundancy = b.redundancy;
+    return FCM_OK;
+  }
   p->waves = 4;
   p->lds_bytes = lds;
   p->workgroups = (int32_t)wgs;
@@ -233,6 +268,37 @@ fcm_status evaluate_plan(const Geom& g, const fcm_desc* d, const fcm_hw_desc& hw
 // ---------------------------------------------------------------------------------
 // Search
 // ---------------------------------------------------------------------------------
+
+// Time model of a persistent (gen 3) kernel launch, in seconds. Each workgroup runs a
+// pipeline of items (tile x 64-byte channel chunk): a copy wave issues the LDS copies of
+// item i+2 while four compute waves run item i, so an item costs the larger of the two
+// sides; workgroups sharing a CU share its SIMDs. Cycle costs per item were fitted to
+// traces of the kernels on MI355X (1.6 GHz effective clock under load): compute
+// ~700 + per pixel block (70 per depthwise tap, 28 per 16x16 MFMA tile), copies ~90 per
+// 1 KiB copy instruction. The launch is never faster than its HBM traffic at 5 TB/s.
+static double persistent_time_estimate(const Variant& v, const Geom& g, const fcm_plan_t& p,
+                                       const fcm_hw_desc& hw) {
+  const bool has_dw = v.family != FAM_PW, has_pw = v.family != FAM_DW;
+  const int K = has_dw ? g.k : 1, S = has_dw ? g.s : 1;
+  const int P = p.tile_h * p.tile_w;
+  const int nb = ceil_div(ceil_div(P, 16), 4);
+  const int ct = has_pw ? p.co_block / 16 : 0;
+  const int cin = v.family == FAM_DW ? g.cm : g.ci;
+  const int nchunks = v.family == FAM_DW ? 1 : ceil_div(cin, 64 / g.elt);
+  const int last = v.family == FAM_DW ? g.cm : g.co;
+  const int64_t nwork = (int64_t)g.n * ceil_div(g.ho, p.tile_h) * ceil_div(g.wo, p.tile_w) * ceil_div(last, p.co_block);
+  const int IH = has_dw ? (p.tile_h - 1) * S + K : p.tile_h;
+  const int mode = v.family == FAM_DWPW ? M3_DWPW : (v.family == FAM_PW ? M3_PW : M3_DW);
+  const double c_item = 700.0 + nb * (has_dw ? K * K * 70.0 : 20.0) + nb * ct * 28.0;
+  const double p_item = 400.0 + 90.0 * copies_per_item3(mode, K, IH, v.pitch, ct);
+  const int64_t grid = std::max<int64_t>(1, p.workgroups);
+  const double per_cu = std::max(1.0, (double)grid / hw.num_cus);
+  const double ipw = (double)ceil_div((int)std::min<int64_t>(nwork, 1 << 30), (int)grid) * nchunks;
+  const double cycles = ipw * std::max(c_item * per_cu, p_item) + 3000.0;
+  const double t_pipe = cycles / 1.6e9;
+  const double t_mem = (double)p.bytes_tiled / 5.0e12;
+  return std::max(t_pipe, t_mem);
+}
 
 struct Cand {
   fcm_plan_t p;
@@ -281,7 +347,10 @@ static fcm_status search(const Geom& g, const fcm_desc* d, const fcm_hw_desc& hw
       if (!v.tile_w && TW > round_up(g.wo, v.dw_r ? v.dw_r : 1) && TW > 4) continue;
       for (int TH : ths) {
         if (!v.tile_h && TH > g.ho && TH > 1) continue;
-        for (int COB = 16; COB <= std::min(v.max_cob, round_up(last, 16)); COB += 16) {
+        // persistent kernels have one compiled output-channel block (the last is masked)
+        const int cob_lo = v.gen == 3 ? v.max_cob : 16;
+        const int cob_hi = v.gen == 3 ? v.max_cob : std::min(v.max_cob, round_up(last, 16));
+        for (int COB = cob_lo; COB <= cob_hi; COB += 16) {
           for (int cb0 : cbs) {
             const int CB = (v.family == FAM_DW && v.gen != 2) ? COB : cb0;
             const int lds = tiling_lds(v, g, TH, TW, CB, COB);
@@ -307,6 +376,24 @@ static fcm_status search(const Geom& g, const fcm_desc* d, const fcm_hw_desc& hw
     }
   }
   if (cands.empty()) return fail(FCM_EUNSUPPORTED, "plan: no compiled kernel implements this shape");
+  // The persistent kernels (gen 3) are preferred wherever one implements the shape; among
+  // them the tiling with the least estimated time wins (see persistent_time_estimate).
+  {
+    const Cand* best3 = nullptr;
+    double best_t = 0;
+    for (const Cand& c : cands) {
+      if (vs[c.p.variant].gen != 3) continue;
+      const double t = persistent_time_estimate(vs[c.p.variant], g, c.p, hw);
+      if (!best3 || t < best_t || (t == best_t && c.p.variant < best3->p.variant)) {
+        best3 = &c;
+        best_t = t;
+      }
+    }
+    if (best3) {
+      *best_out = best3->p;
+      return FCM_OK;
+    }
+  }
   bool any_full = false;
   for (const Cand& c : cands) any_full |= c.wgs >= hw.num_cus;
   const int target = 2 * hw.num_cus;

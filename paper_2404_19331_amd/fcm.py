@@ -144,9 +144,12 @@ def plan(op, desc, hw=None):
     return p
 
 
-def plan_evaluate(op, desc, tile_h, tile_w, c_block, co_block, variant, hw=None):
+def plan_evaluate(op, desc, tile_h, tile_w, c_block, co_block, variant, hw=None, workgroups=0):
+    """Evaluate a caller-chosen tiling. For the persistent kernels `workgroups` > 0 caps
+    the number of workgroups launched."""
     p = Plan()
     p.op, p.tile_h, p.tile_w, p.c_block, p.co_block, p.variant = OP[op], tile_h, tile_w, c_block, co_block, variant
+    p.workgroups = workgroups
     _check(lib().fcm_plan_evaluate(ctypes.byref(desc), ctypes.byref(hw) if hw else None, ctypes.byref(p)))
     return p
 

@@ -215,7 +215,6 @@ __global__ __launch_bounds__(kThreads3) void k_fused3(KArgs a) {
   const int TH = a.TH, TW = a.TW, P = TH * TW;
   const int IW = HAS_DW ? (TW - 1) * SE + KE : TW;
   const int IH = HAS_DW ? (TH - 1) * SE + KE : TH;
-  const int nins = IH * IPR;
   const Lds3 lay = lds3p(dtype_id<DT>(), KE, MODE, IH, IWP, CT);
   const int C = MODE == M3_DW ? a.Cm : a.Ci;
   const int nchunks = MODE == M3_DW ? 1 : ceil_div(C, CB);
@@ -287,24 +286,35 @@ __global__ __launch_bounds__(kThreads3) void k_fused3(KArgs a) {
       const int iy0 = HAS_DW ? iss_t.oy0 * SE - a.pad : iss_t.oy0;
       const int ix0 = HAS_DW ? iss_t.ox0 * SE - a.pad : iss_t.ox0;
       const rsrc_t rx = make_rsrc(x + (size_t)iss_t.n * img, (uint32_t)(img * DT::ELT));
+      // Byte offsets: a per-lane part (window column, channel slot), fixed for the item,
+      // plus a uniform part per window row. Lanes outside the image or the channel range
+      // carry kOob, which stays out of range after the row offset (< 2^31) is added.
       const int c = c0 + (lane & 3) * CPL;
-      for (int ins = 0; ins < nins; ++ins) {
-        const int wy = ins / IPR;
-        const int wx = wxl[IPR == 1 ? 0 : ins % IPR];
-        const int gy = iy0 + wy, gx = ix0 + wx;
-        const bool ok = wx >= 0 && (unsigned)gy < (unsigned)a.H && (unsigned)gx < (unsigned)a.W && c < C;
-        dma16(rx, buf + ins * 1024, ok ? (uint32_t)(((gy * a.W + gx) * C + c) * DT::ELT) : kOob);
+      uint32_t coff[IPR];
+#pragma unroll
+      for (int j = 0; j < IPR; ++j) {
+        const int gx = ix0 + wxl[j];
+        const bool ok = wxl[j] >= 0 && (unsigned)gx < (unsigned)a.W && c < C;
+        coff[j] = ok ? (uint32_t)((gx * C + c) * DT::ELT) : kOob;
+      }
+      const uint32_t rstride = (uint32_t)(a.W * C * DT::ELT);
+      for (int wy = 0; wy < IH; ++wy) {
+        const int gy = iy0 + wy;
+        const bool rok = (unsigned)gy < (unsigned)a.H;
+        const uint32_t roff = rok ? (uint32_t)gy * rstride : 0u;
+#pragma unroll
+        for (int j = 0; j < IPR; ++j) dma16(rx, buf + (wy * IPR + j) * 1024, rok ? coff[j] + roff : kOob);
       }
       if constexpr (HAS_PW) {
         const int mrow = lane >> 2;
         const int j = (lane & 3) ^ (((mrow >> 3) & 1) << 1);
         const int cw_ = c0 + j * CPL;
+        // rows beyond c_out fall outside the weight tensor and read as zero
+        const uint32_t woff =
+            cw_ < a.Ci ? (uint32_t)(((co0 + 4 * CT * (mrow >> 2) + (mrow & 3)) * a.Ci + cw_) * DT::ELT) : kOob;
 #pragma unroll
-        for (int ct = 0; ct < CT; ++ct) {
-          const int co = co0 + 4 * CT * (mrow >> 2) + 4 * ct + (mrow & 3);
-          const bool ok = co < a.Co && cw_ < a.Ci;
-          dma16(rw, buf + lay.in_bytes + ct * 1024, ok ? (uint32_t)((co * a.Ci + cw_) * DT::ELT) : kOob);
-        }
+        for (int ct = 0; ct < CT; ++ct)
+          dma16(rw, buf + lay.in_bytes + ct * 1024, woff + (uint32_t)(4 * ct * a.Ci * DT::ELT));
         dma16(rbp, buf + lay.bias_off + 1024, lane * 16 < CoB * 4 ? (uint32_t)(co0 * 4 + lane * 16) : kOob);
       }
       if constexpr (HAS_DW) {

@@ -171,7 +171,8 @@ static int tiling_lds(const Variant& v, const Geom& g, int TH, int TW, int CB, i
     if ((cin * g.elt) % 16) return 0;
     if (dw_only ? (g.cm * g.elt) % 16 : (g.co * g.elt) % 4) return 0;
     if ((int64_t)g.h * g.w * cin * g.elt >= ((int64_t)1 << 31)) return 0;
-    if (!dw_only && (int64_t)g.co * g.ci * g.elt >= ((int64_t)1 << 31)) return 0;
+    // weight rows up to the last block's padding are addressed with 32-bit offsets
+    if (!dw_only && (int64_t)(g.co + COB) * g.ci * g.elt >= ((int64_t)1 << 31)) return 0;
     if (CB != 64 / g.elt || COB != v.max_cob) return 0;
     if (P > v.max_p) return 0;
     const int mode = g.family == FAM_DWPW ? M3_DWPW : (g.family == FAM_PW ? M3_PW : M3_DW);

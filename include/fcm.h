@@ -130,6 +130,8 @@ typedef struct {
   int32_t lds_bytes;     /* dynamic LDS per workgroup */
   int32_t workgroups;
   int32_t fuse;          /* planner verdict: 1 if the fused estimate < layer-by-layer */
+  int32_t depth;         /* persistent kernels: LDS ring buffers, i.e. items in flight + 1
+                            (2..8; 0 on input to fcm_plan_evaluate = the planner's choice) */
   int64_t bytes_ideal;          /* input + weights + output, each once                  */
   int64_t bytes_tiled;          /* per-workgroup loads + stores of this tiling (exact)  */
   int64_t bytes_paper;          /* Eq. 1-4 estimate of this module at this tiling        */

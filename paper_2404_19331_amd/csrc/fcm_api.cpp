@@ -213,6 +213,7 @@ static fcm_status run(int op, const fcm_desc* d, const Tensors& t, const fcm_pla
   a.nwork = a.N * a.tiles_y * a.tiles_x * a.n_cb;
   a.cus = device_cus();
   a.grid_cap = v.gen == 3 ? p.workgroups : 0;
+  a.depth = p.depth;
 #ifdef FCM_TRACE
   a.trace = g_trace;
 #endif

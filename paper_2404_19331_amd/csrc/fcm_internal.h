@@ -181,12 +181,15 @@ enum { M3_DWPW = 0, M3_PW = 1, M3_DW = 2 };
 // the input window of IH rows at a pitch of IWP pixels of 64 bytes; the pointwise weight
 // block (16*CT rows of 64 bytes); the depthwise weights of one chunk as 32-bit
 // dot-operand words [K*K][CB]; the raw depthwise weights as copied ([CB][K*K] elements,
-// whole KiB); and two KiB of biases (depthwise, then pointwise). Three buffers.
-constexpr int kThreads3 = 320;  // one copy wave + four compute waves
+// whole KiB); and two KiB of biases (depthwise, then pointwise). `depth` buffers form
+// the ring (the copy wave runs depth - 1 items ahead).
+constexpr int kCopyWaves3 = 2;  // copy waves (each issues about half of an item's copies)
+constexpr int kThreads3 = 64 * (kCopyWaves3 + 4);  // + four compute waves
+constexpr int kMaxDepth3 = 8;   // ring buffers at most
 struct Lds3 {
   int in_bytes, w_bytes, wd_off, raw_off, bias_off, buf_bytes, total;
 };
-FCM_HD inline Lds3 lds3p(int dt, int K, int mode, int IH, int IWP, int CT) {
+FCM_HD inline Lds3 lds3p(int dt, int K, int mode, int IH, int IWP, int CT, int depth = 2) {
   Lds3 r;
   const int cb = kRowB / elt_size(dt);
   r.in_bytes = IH * IWP * kRowB;
@@ -199,17 +202,39 @@ FCM_HD inline Lds3 lds3p(int dt, int K, int mode, int IH, int IWP, int CT) {
   r.bias_off = off;
   off += 2048;
   r.buf_bytes = off;
-  r.total = 3 * off;
+  r.total = depth * off;
   return r;
 }
 
-// Copy instructions the copy wave of a persistent kernel issues per item (host and
-// device); a partial wait on the vector-memory counter covers at most 63 of them.
+// Copy instructions of one item of a persistent kernel (host and device), in issue
+// order: raw DW weights and DW bias, window rows, PW weight rows, PW bias.
 FCM_HD inline int copies_per_item3(int mode, int K, int IH, int IWP, int CT) {
   int n = IH * (IWP / 16);
   if (mode != M3_DW) n += CT + 1;                          // PW weight rows, PW bias
   if (mode != M3_PW) n += (64 * K * K + 1023) / 1024 + 1;  // raw DW weights, DW bias
   return n;
+}
+// Split of an item's copies between the two copy waves: wave 0 issues the DW weights
+// and bias (it converts them) and window rows [0, r0), wave 1 rows [r0, IH), the PW
+// weight rows and the PW bias; r0 balances the two counts.
+FCM_HD inline int rows_wave0_3(int mode, int K, int IH, int IWP, int CT) {
+  const int ipr = IWP / 16;
+  const int ndw = mode != M3_PW ? (64 * K * K + 1023) / 1024 + 1 : 0;
+  const int t = copies_per_item3(mode, K, IH, IWP, CT);
+  int r0 = (t - 2 * ndw + ipr) / (2 * ipr);
+  r0 = r0 < 0 ? 0 : (r0 > IH ? IH : r0);
+  return r0;
+}
+FCM_HD inline int copies_wave0_3(int mode, int K, int IH, int IWP, int CT) {
+  const int ndw = mode != M3_PW ? (64 * K * K + 1023) / 1024 + 1 : 0;
+  return ndw + rows_wave0_3(mode, K, IH, IWP, CT) * (IWP / 16);
+}
+// The larger per-wave share: a partial wait on the vector-memory counter covers at most
+// 63 outstanding copies of one wave.
+FCM_HD inline int copies_per_wave3(int mode, int K, int IH, int IWP, int CT) {
+  const int t = copies_per_item3(mode, K, IH, IWP, CT);
+  const int w0 = copies_wave0_3(mode, K, IH, IWP, CT);
+  return w0 > t - w0 ? w0 : t - w0;
 }
 
 // ---------------------------------------------------------------------------------
@@ -235,6 +260,7 @@ struct KArgs {
   int vec_x, vec_w1, vec_w2, vec_w3, vec_y;
   LdsLayout L;
   int nwork;     // persistent kernels: work tiles (image x tile x channel block)
+  int depth;     // persistent kernels: LDS ring buffers (>= 2)
   int cus;       // compute units of the device
   int grid_cap;  // persistent kernels: at most this many workgroups (0 = no cap)
   unsigned long long* trace;  // development timeline buffer (used only in FCM_TRACE builds)

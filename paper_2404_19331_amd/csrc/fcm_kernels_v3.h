@@ -1,15 +1,16 @@
 // fcm_kernels_v3.h -- persistent NHWC kernels for gfx950: DW->PW module, and the
 // layer-by-layer PW and DW kernels built from the same pieces.
 //
-// k_fused3<DT, K, S, BPW, CT, MODE>
-//   A persistent workgroup (4 waves) owns a contiguous range of work tiles; a work tile
-//   is (image, TH x TW output tile, block of 16*CT output channels). Work tiles are cut
-//   into items, one per input-channel chunk of 64 bytes (one MFMA k-step); the items of
-//   the whole range form one stream, and the copy of item i+1 (global -> LDS with
-//   buffer_load ... lds, out-of-range offsets read as zero, i.e. the zero padding of the
-//   convolution) overlaps the arithmetic of item i, across tile boundaries as well.
+// k_fused3<DT, K, S, BPW, CT, MODE, IWP>
+//   A persistent workgroup (two copy waves, four compute waves) owns a contiguous range
+//   of work tiles; a work tile is (image, TH x TW output tile, block of 16*CT output
+//   channels). Work tiles are cut into items, one per input-channel chunk of 64 bytes
+//   (one MFMA k-step); the items of the whole range form one stream, and the copies of
+//   items i+1 .. i+depth-1 (global -> LDS with buffer_load ... lds, out-of-range offsets
+//   read as zero, i.e. the zero padding of the convolution) overlap the arithmetic of
+//   item i, across tile boundaries as well.
 //
-//   Lane l of wave w owns, in each of its BPW pixel blocks, output pixel (l % 16) of the
+//   Lane l of compute wave w owns, in each of its BPW pixel blocks, output pixel (l % 16) of the
 //   block and the 16 bytes of channels (l / 16) of the chunk: exactly the MFMA B operand
 //   the lane supplies. The depthwise stencil is computed straight into that operand, so
 //   the DW output never leaves the registers (the paper's on-chip communication buffer,
@@ -25,7 +26,8 @@
 //   MODE M3_PW: the DW stage is off (window = output tile); M3_DW: the PW stage is off,
 //   each lane writes its 16 bytes of depthwise output directly.
 //
-// LDS per buffer (two buffers): window [npin pixels][64 B] (pixel q at 64 q, no padding;
+// LDS: a ring of a.depth buffers (the copy waves run a.depth - 1 items ahead of the
+// compute waves; deeper rings keep more bytes in flight per CU). Per buffer: window [npin pixels][64 B] (pixel q at 64 q, no padding;
 // stride-2 windows keep even and odd columns in separate halves so that the lanes of a
 // block read consecutive pixels), PW weights [16*CT rows][64 B] (16-byte slots XOR-
 // swizzled by row bit 3, conflict-free MFMA A reads), DW weights [K*K taps][CB] 32-bit
@@ -37,7 +39,7 @@
 namespace fcm {
 
 #ifdef FCM_TRACE
-// Development builds only: the first lane of the copy wave (slots 0..31) and of the first
+// Development builds only: the first lane of copy wave 0 (slots 0..31) and of the first
 // compute wave (slots 32..63) record the shader clock at fixed points ([workgroup][64]).
 #define FCM_TS_AT(tid, slot)                                                              \
   do {                                                                                    \
@@ -51,7 +53,7 @@ namespace fcm {
   } while (0)
 #endif
 #define FCM_TS(slot) FCM_TS_AT(0, slot)
-#define FCM_TSC(slot) FCM_TS_AT(64, slot)
+#define FCM_TSC(slot) FCM_TS_AT(64 * kCopyWaves3, slot)
 
 constexpr int kNiwMax = 10;  // window copy instructions per wave (<= 640 window pixels)
 
@@ -171,7 +173,7 @@ __device__ __forceinline__ void wait_vm_n() {
 // s_waitcnt lgkmcnt(0) only (LDS operations of this wave are complete).
 __device__ __forceinline__ void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (0 << 8) | (3 << 14)); }
 // Workgroup barrier without the memory fences of __syncthreads: a release fence would
-// make the copy wave wait for all of its outstanding copies (they are LDS writes). The
+// make a copy wave wait for all of its outstanding copies (they are LDS writes). The
 // waits each side needs are explicit; the empty asm statements keep the compiler from
 // moving memory accesses across the barrier.
 __device__ __forceinline__ void barrier3() {
@@ -227,12 +229,13 @@ __global__ __launch_bounds__(kThreads3) void k_fused3(KArgs a) {
   if (wt1 <= wt0) return;
   const int nitems = (wt1 - wt0) * nchunks;
 
-  // wave 0 copies, waves 1..4 compute; the wave index is uniform: keep it scalar
+  // waves 0..kCopyWaves3-1 copy, the next four compute; the wave index is uniform:
+  // keep it scalar
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   const int r16 = lane & 15, g = lane >> 4;
-  const bool producer = wave == 0;
-  const int cw = wave - 1;  // compute-wave index
+  const bool producer = wave < kCopyWaves3;
+  const int cw = wave - kCopyWaves3;  // compute-wave index
 
   const T* x = (const T*)a.x;
   const size_t img = (size_t)a.H * a.W * C;
@@ -258,13 +261,21 @@ __global__ __launch_bounds__(kThreads3) void k_fused3(KArgs a) {
     r.ox0 = tx * TW;
     return r;
   };
-  auto bufp = [&](int it) { return smem + (it % 3) * lay.buf_bytes; };
+  const int D = a.depth < 2 ? 2 : a.depth;  // ring buffers
+  auto bufp = [&](int slot) { return smem + slot * lay.buf_bytes; };
+  auto next_slot = [&](int slot) { return slot + 1 == D ? 0 : slot + 1; };
 
   int tsi = 0;
   FCM_TS(tsi++);
 
   if (producer) {
-    // ======================= producer: all copies, three items deep ================
+    // ===== copy waves: all copies, D - 1 items ahead of the compute waves. Wave 0 issues
+    // the DW weights and bias (and converts them) and window rows [0, r0); wave 1 the
+    // rows [r0, IH), the PW weight rows and the PW bias. =====
+    const int r0 = rows_wave0_3(MODE, KE, IH, IWP, CT);
+    const int wy0 = wave == 0 ? 0 : r0, wy1 = wave == 0 ? r0 : IH;
+    const int w0n = copies_wave0_3(MODE, KE, IH, IWP, CT);
+    const int mine = wave == 0 ? w0n : per_item - w0n;  // copies per item of this wave
     const rsrc_t rw = make_rsrc(wp, HAS_PW ? (uint32_t)((size_t)a.Co * a.Ci * DT::ELT) : 0u);
     const rsrc_t rwd = make_rsrc(wd, HAS_DW ? (uint32_t)((size_t)C * KK * DT::ELT) : 0u);
     const rsrc_t rbd = make_rsrc(bd ? bd : (const void*)wd, (HAS_DW && bd) ? (uint32_t)(C * 4) : 0u);
@@ -277,10 +288,10 @@ __global__ __launch_bounds__(kThreads3) void k_fused3(KArgs a) {
       if (SE == 2) wx = col < IWP / 2 ? 2 * col : 2 * (col - IWP / 2) + 1;
       wxl[j] = wx < IW ? wx : -1;
     }
-    int iss = 0, iss_wt = wt0, iss_ch = 0;
+    int iss_slot = 0, iss_wt = wt0, iss_ch = 0;
     Tile iss_t = decode(wt0);
     auto issue_next = [&]() {
-      char* buf = bufp(iss);
+      char* buf = bufp(iss_slot);
       const int c0 = MODE == M3_DW ? iss_t.cb * CB : iss_ch * CB;
       const int co0 = iss_t.cb * CoB;
       const int iy0 = HAS_DW ? iss_t.oy0 * SE - a.pad : iss_t.oy0;
@@ -298,14 +309,22 @@ __global__ __launch_bounds__(kThreads3) void k_fused3(KArgs a) {
         coff[j] = ok ? (uint32_t)((gx * C + c) * DT::ELT) : kOob;
       }
       const uint32_t rstride = (uint32_t)(a.W * C * DT::ELT);
-      for (int wy = 0; wy < IH; ++wy) {
+      if (HAS_DW && wave == 0) {
+#pragma unroll
+        for (int r = 0; r < NRAW; ++r) {
+          const int b = r * 1024 + lane * 16;
+          dma16(rwd, buf + lay.raw_off + r * 1024, b < CB * KK * DT::ELT ? (uint32_t)(c0 * KK * DT::ELT + b) : kOob);
+        }
+        dma16(rbd, buf + lay.bias_off, lane * 16 < CB * 4 ? (uint32_t)(c0 * 4 + lane * 16) : kOob);
+      }
+      for (int wy = wy0; wy < wy1; ++wy) {
         const int gy = iy0 + wy;
         const bool rok = (unsigned)gy < (unsigned)a.H;
         const uint32_t roff = rok ? (uint32_t)gy * rstride : 0u;
 #pragma unroll
         for (int j = 0; j < IPR; ++j) dma16(rx, buf + (wy * IPR + j) * 1024, rok ? coff[j] + roff : kOob);
       }
-      if constexpr (HAS_PW) {
+      if (HAS_PW && wave == 1) {
         const int mrow = lane >> 2;
         const int j = (lane & 3) ^ (((mrow >> 3) & 1) << 1);
         const int cw_ = c0 + j * CPL;
@@ -317,56 +336,67 @@ __global__ __launch_bounds__(kThreads3) void k_fused3(KArgs a) {
           dma16(rw, buf + lay.in_bytes + ct * 1024, woff + (uint32_t)(4 * ct * a.Ci * DT::ELT));
         dma16(rbp, buf + lay.bias_off + 1024, lane * 16 < CoB * 4 ? (uint32_t)(co0 * 4 + lane * 16) : kOob);
       }
-      if constexpr (HAS_DW) {
-#pragma unroll
-        for (int r = 0; r < NRAW; ++r) {
-          const int b = r * 1024 + lane * 16;
-          dma16(rwd, buf + lay.raw_off + r * 1024,
-                b < CB * KK * DT::ELT ? (uint32_t)(c0 * KK * DT::ELT + b) : kOob);
-        }
-        dma16(rbd, buf + lay.bias_off, lane * 16 < CB * 4 ? (uint32_t)(c0 * 4 + lane * 16) : kOob);
-      }
-      ++iss;
+      iss_slot = next_slot(iss_slot);
       if (++iss_ch == nchunks) {
         iss_ch = 0;
         if (++iss_wt < wt1) iss_t = decode(iss_wt);
       }
     };
-    // depthwise weights of item `it`: raw [c][tap] elements -> [tap][c] dot-operand words
-    auto convert = [&](int it) {
+    // Depthwise weights of the item in ring slot `slot` (wave 0): raw [c][tap] elements
+    // -> [tap][c] dot-operand words. All reads are issued before the first write.
+    auto convert = [&](int slot) {
       if constexpr (HAS_DW) {
-        char* buf = bufp(it);
+        if (wave != 0) return;
+        constexpr int NEL = CB * KK;                      // weights of the chunk
+        constexpr int EPV = 16 / DT::ELT;                 // elements per 16-byte vector
+        constexpr int NV = (NEL * DT::ELT + 1023) / 1024;  // vectors per lane
+        char* buf = bufp(slot);
         const char* raw = buf + lay.raw_off;
         uint32_t* dst = (uint32_t*)(buf + lay.wd_off);
-#pragma unroll 4
-        for (int i = lane; i < KK * CB; i += 64) {
-          const int ci = i % CB, tap = i / CB;
-          const int e = ci * KK + tap;
-          uint32_t rv;
-          if constexpr (DT::ELT == 4)
-            rv = ((const uint32_t*)raw)[e];
-          else if constexpr (DT::ELT == 2)
-            rv = ((const uint16_t*)raw)[e];
-          else
-            rv = (uint32_t)((const uint8_t*)raw)[e];
-          dst[i] = D3::weight_word(rv, ci);
+        u32x4 rv[NV];
+#pragma unroll
+        for (int v = 0; v < NV; ++v) rv[v] = *(const u32x4*)(raw + (v * 64 + lane) * 16);  // within the NRAW KiB
+#pragma unroll
+        for (int v = 0; v < NV; ++v) {
+#pragma unroll
+          for (int k = 0; k < EPV; ++k) {
+            const int e = (v * 64 + lane) * EPV + k;
+            if (e < NEL) {
+              const uint32_t word = rv[v][k * DT::ELT / 4];
+              uint32_t el;
+              if constexpr (DT::ELT == 4)
+                el = word;
+              else if constexpr (DT::ELT == 2)
+                el = (k & 1) ? word >> 16 : word & 0xffffu;
+              else
+                el = (word >> (8 * (k & 3))) & 0xffu;
+              const int ci = e / KK, tap = e - (e / KK) * KK;
+              dst[tap * CB + ci] = D3::weight_word(el, ci);
+            }
+          }
         }
       }
     };
-    issue_next();
-    if (nitems > 1) issue_next();
-    wait_vm(nitems > 1 ? per_item : 0);
+    // Copies complete in issue order, so "item j has landed" is a wait until at most the
+    // copies of the items issued after j are outstanding (the host keeps that count
+    // <= 63; a larger one would fall back to a full wait).
+    const int ahead = min(nitems, D - 1);
+    for (int i = 0; i < ahead; ++i) issue_next();
+    wait_vm((ahead - 1) * mine);
     convert(0);
     wait_lgkm0();
     barrier3();
     FCM_TS(tsi++);
+    int cv_slot = next_slot(0);
     for (int it = 0; it < nitems; ++it) {
-      if (it + 2 < nitems) issue_next();
+      // slot of item it + D - 1 is the one item it - 1 used: released by the last barrier
+      if (it + D - 1 < nitems) issue_next();
       FCM_TS(tsi++);
       if (it + 1 < nitems) {
-        wait_vm(it + 2 < nitems ? per_item : 0);
-        convert(it + 1);
+        wait_vm((min(nitems, it + D) - (it + 2)) * mine);
+        convert(cv_slot);
       }
+      cv_slot = next_slot(cv_slot);
       wait_lgkm0();
       FCM_TS(tsi++);
       barrier3();
@@ -404,10 +434,11 @@ __global__ __launch_bounds__(kThreads3) void k_fused3(KArgs a) {
   barrier3();  // item 0 is ready
   int tsc = 32;
   FCM_TSC(tsc++);
-  int wt = wt0, ch = 0;
+  int wt = wt0, ch = 0, slot = 0;
   Tile cur_t = decode(wt0);
   for (int it = 0; it < nitems; ++it) {
-    const char* buf = bufp(it);
+    const char* buf = bufp(slot);
+    slot = next_slot(slot);
     // B operand of each block: depthwise output of this lane's pixel and channel slot
     // (or the staged input itself for the PW kernel), then the PW contraction. The
     // number of blocks holding pixels is a compile-time constant of each instance of

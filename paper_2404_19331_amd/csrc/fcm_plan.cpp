@@ -152,8 +152,25 @@ static Bytes module_bytes(const Geom& g, int TH, int TW, int COB) {
   return b;
 }
 
-// LDS bytes of a tiling (0 if the variant cannot implement it).
-static int tiling_lds(const Variant& v, const Geom& g, int TH, int TW, int CB, int COB) {
+// Ring depth of a persistent kernel: the caller's `want` (2..8), else the deepest ring
+// whose buffers fit in max(3 buffers, 80 KiB) of LDS (so that two workgroups share a CU
+// when buffers are small); every depth keeps the partial wait on the copies of the
+// items in flight (per copy wave) within the 6-bit vector-memory counter. 0 if `want` is
+// invalid.
+static int ring_depth3(int want, int buf, int per_item, int lds_per_wg) {
+  const int dmax = std::min(kMaxDepth3, 63 / per_item + 2);
+  if (want > 0) return (want >= 2 && want <= dmax && want * buf <= lds_per_wg) ? want : 0;
+  const int budget = std::min(lds_per_wg, std::max(3 * buf, 80 * 1024));
+  int d = dmax;
+  while (d > 2 && d * buf > budget) --d;
+  return d;
+}
+
+// LDS bytes of a tiling (0 if the variant cannot implement it). For the persistent
+// kernels *depth is the requested ring depth on input (0 = choose) and the chosen one on
+// output.
+static int tiling_lds(const Variant& v, const Geom& g, int TH, int TW, int CB, int COB, int lds_per_wg,
+                      int* depth) {
   const int kb = k_block(g.dtype);
   if (TH <= 0 || TW <= 0 || COB <= 0 || COB % 16) return 0;
   if (v.dw_r && TW % v.dw_r) return 0;
@@ -179,8 +196,14 @@ static int tiling_lds(const Variant& v, const Geom& g, int TH, int TW, int CB, i
     const int IW = mode == M3_PW ? TW : (TW - 1) * g.s + g.k;
     const int IH = mode == M3_PW ? TH : (TH - 1) * g.s + g.k;
     if (IW > v.pitch) return 0;
-    if (copies_per_item3(mode, mode == M3_PW ? 1 : g.k, IH, v.pitch, COB / 16) > 63) return 0;
-    return lds3p(g.dtype, mode == M3_PW ? 1 : g.k, mode, IH, v.pitch, COB / 16).total;
+    const int KE = mode == M3_PW ? 1 : g.k;
+    const int per_item = copies_per_wave3(mode, KE, IH, v.pitch, COB / 16);
+    if (per_item > 63) return 0;
+    const int buf = lds3p(g.dtype, KE, mode, IH, v.pitch, COB / 16).buf_bytes;
+    const int d = ring_depth3(*depth, buf, per_item, lds_per_wg);
+    if (d == 0) return 0;
+    *depth = d;
+    return lds3p(g.dtype, KE, mode, IH, v.pitch, COB / 16, d).total;
   }
   if (v.gen == 2) {
     // NHWC, 16-byte channel rows, 32-bit buffer offsets, fixed tile and 64-byte chunk
@@ -232,7 +255,8 @@ fcm_status evaluate_plan(const Geom& g, const fcm_desc* d, const fcm_hw_desc& hw
   if (p->variant < 0 || p->variant >= nv) return fail(FCM_EUNSUPPORTED, "plan: unknown kernel variant");
   const Variant& v = vs[p->variant];
   if (!variant_matches(v, g)) return fail(FCM_EUNSUPPORTED, "plan: kernel variant does not implement this module");
-  const int lds = tiling_lds(v, g, p->tile_h, p->tile_w, p->c_block, p->co_block);
+  int depth = v.gen == 3 ? p->depth : 0;
+  const int lds = tiling_lds(v, g, p->tile_h, p->tile_w, p->c_block, p->co_block, hw.lds_per_wg, &depth);
   if (lds <= 0) return fail(FCM_EUNSUPPORTED, "plan: tiling not implemented by the kernel variant");
   if (lds > hw.lds_per_wg) return fail(FCM_EUNSUPPORTED, "plan: tiling exceeds the LDS per workgroup");
   const int nty = ceil_div(g.ho, p->tile_h), ntx = ceil_div(g.wo, p->tile_w);
@@ -248,6 +272,7 @@ fcm_status evaluate_plan(const Geom& g, const fcm_desc* d, const fcm_hw_desc& hw
     int64_t grid = std::min<int64_t>(wgs, per_cu * hw.num_cus);
     if (p->workgroups > 0 && p->workgroups < grid) grid = p->workgroups;  // caller's cap
     p->workgroups = (int32_t)grid;
+    p->depth = depth;
     p->waves = 4;
     p->lds_bytes = lds;
     p->bytes_ideal = b.ideal;
@@ -257,6 +282,7 @@ fcm_status evaluate_plan(const Geom& g, const fcm_desc* d, const fcm_hw_desc& hw
     return FCM_OK;
   }
   p->waves = 4;
+  p->depth = 0;
   p->lds_bytes = lds;
   p->workgroups = (int32_t)wgs;
   p->bytes_ideal = b.ideal;
@@ -354,7 +380,8 @@ static fcm_status search(const Geom& g, const fcm_desc* d, const fcm_hw_desc& hw
         for (int COB = cob_lo; COB <= cob_hi; COB += 16) {
           for (int cb0 : cbs) {
             const int CB = (v.family == FAM_DW && v.gen != 2) ? COB : cb0;
-            const int lds = tiling_lds(v, g, TH, TW, CB, COB);
+            int depth = 0;
+            const int lds = tiling_lds(v, g, TH, TW, CB, COB, hw.lds_per_wg, &depth);
             if (lds <= 0 || lds > hw.lds_per_wg) continue;
             Cand c;
             memset(&c.p, 0, sizeof(c.p));

@@ -2,8 +2,9 @@
 
 Every compiled persistent variant that implements a case runs at several tile shapes
 (full and ragged pixel blocks) and compared with the CPU oracle. A capped grid makes
-each workgroup stream many (tile, channel chunk) items, which exercises the double
-buffering across tile boundaries.
+each workgroup stream many (tile, channel chunk) items, which exercises the LDS ring
+across tile boundaries, at depths from 2 (one item in flight) to 8 where the tiling
+allows it.
 """
 import pytest
 
@@ -45,7 +46,11 @@ def _cases():
     return out
 
 
-def _v3_plans(case, caps=(0,)):
+# (workgroup cap, ring depth); 0 = the planner's choice
+LAUNCH = ((0, 0), (3, 2), (3, 0), (2, 5), (2, 8))
+
+
+def _v3_plans(case, launch=((0, 0),)):
     desc = fcm.desc_from_case(case)
     cb = 64 // ELT[case.dtype]
     plans = []
@@ -56,9 +61,9 @@ def _v3_plans(case, caps=(0,)):
         for th, tw in TILES:
             cobs = [cb] if case.op == "dw" else [16 * int(name.split(",")[4])]
             for cob in cobs:
-                for cap in caps:
+                for cap, depth in launch:
                     try:
-                        p = fcm.plan_evaluate(case.op, desc, th, tw, cb, cob, v, workgroups=cap)
+                        p = fcm.plan_evaluate(case.op, desc, th, tw, cb, cob, v, workgroups=cap, depth=depth)
                     except fcm.FcmError:
                         continue
                     plans.append(p)
@@ -73,9 +78,9 @@ def test_persistent_variants_match_oracle(case):
     inp = make_inputs(case)
     ref = oracle_ref(case, inp)
     d = dev_inputs(inp, case.dtype)
-    plans = _v3_plans(case, caps=(0, 3))
+    plans = _v3_plans(case, launch=LAUNCH)
     assert plans, "no persistent variant implements %s" % case.name
     for p in plans:
         got = to_np(run_fused(case, d, plan=p))
-        assert_close(got, ref, case.dtype, "%s %s tile %dx%d grid %d" % (
-            case.name, fcm.variant_name(p.variant), p.tile_h, p.tile_w, p.workgroups))
+        assert_close(got, ref, case.dtype, "%s %s tile %dx%d grid %d depth %d" % (
+            case.name, fcm.variant_name(p.variant), p.tile_h, p.tile_w, p.workgroups, p.depth))

@@ -347,10 +347,12 @@ def main():
         "layers": per_layer,
     }
     if a.calib:
-        src = torch.empty(256 << 20, dtype=torch.uint8, device="cuda").fill_(1)
+        # plain device copy of known size for the profiler's byte counters: a float
+        # multiply by one reads 256 MiB and writes 256 MiB
+        src = torch.ones(64 << 20, dtype=torch.float32, device="cuda")
         dst = torch.empty_like(src)
         for _ in range(5):
-            dst.copy_(src)
+            torch.mul(src, 1.0, out=dst)
         torch.cuda.synchronize()
         out["calib_copy_bytes"] = 256 << 20
     if not a.no_cpu_baseline:

@@ -152,18 +152,14 @@ static Bytes module_bytes(const Geom& g, int TH, int TW, int COB) {
   return b;
 }
 
-// Ring depth of a persistent kernel: the caller's `want` (2..8), else the deepest ring
-// whose buffers fit in max(3 buffers, 80 KiB) of LDS (so that two workgroups share a CU
-// when buffers are small); every depth keeps the partial wait on the copies of the
-// items in flight (per copy wave) within the 6-bit vector-memory counter. 0 if `want` is
-// invalid.
+// Ring depth of a persistent kernel: the caller's `want` (2..8), else 3 buffers (two
+// items in flight) where they fit, else 2. Every depth keeps the partial wait on the
+// copies of the items in flight (per copy wave) within the 6-bit vector-memory counter.
+// 0 if `want` is invalid.
 static int ring_depth3(int want, int buf, int per_item, int lds_per_wg) {
   const int dmax = std::min(kMaxDepth3, 63 / per_item + 2);
   if (want > 0) return (want >= 2 && want <= dmax && want * buf <= lds_per_wg) ? want : 0;
-  const int budget = std::min(lds_per_wg, std::max(3 * buf, 80 * 1024));
-  int d = dmax;
-  while (d > 2 && d * buf > budget) --d;
-  return d;
+  return (dmax >= 3 && 3 * buf <= lds_per_wg) ? 3 : 2;
 }
 
 // LDS bytes of a tiling (0 if the variant cannot implement it). For the persistent
@@ -297,18 +293,37 @@ fcm_status evaluate_plan(const Geom& g, const fcm_desc* d, const fcm_hw_desc& hw
 // ---------------------------------------------------------------------------------
 
 // Time model of a persistent (gen 3) kernel launch, in seconds. Each workgroup runs a
-// pipeline of items (tile x 64-byte channel chunk): a copy wave issues the LDS copies of
-// item i+2 while four compute waves run item i, so an item costs the larger of the two
-// sides; workgroups sharing a CU share its SIMDs. Cycle costs per item were fitted to
-// traces of the kernels on MI355X (1.6 GHz effective clock under load): compute
-// ~700 + per pixel block (70 per depthwise tap, 28 per 16x16 MFMA tile), copies ~90 per
-// 1 KiB copy instruction. The launch is never faster than its HBM traffic at 5 TB/s.
+// pipeline of items (tile x 64-byte channel chunk): two copy waves issue the LDS copies
+// of items i+1 .. i+depth-1 while four compute waves run item i, so an item costs the
+// largest of: the busiest compute wave's depthwise dot instructions (workgroups sharing
+// a CU share its SIMDs), the busier copy wave's copy instructions, and the item's copy
+// bytes at the CU's copy rate, which is capped and limited by the bytes in flight
+// (Little's law). Launch overhead is added and the launch is never faster than its HBM
+// traffic. The constants were fitted (least squares on log time, then on the quality of
+// the chosen plans) to timings of every plan of the MobileNetV1, ViT-projection and
+// MBConv DW->PW layers on MI355X; the MFMA and LDS-read terms came out non-binding.
 static double persistent_time_estimate(const Variant& v, const Geom& g, const fcm_plan_t& p,
                                        const fcm_hw_desc& hw) {
+  constexpr double kItem0 = 891.0;        // cycles per item, fixed (busiest compute wave)
+  constexpr double kPerDot = 10.6;        // cycles per depthwise dot instruction
+  constexpr double kPerCopy = 48.7;       // cycles per 1 KiB copy instruction (one copy wave)
+  constexpr double kLaunch = 13100.0;     // cycles of launch, prologue and drain
+  constexpr double kHbm = 5.59e12;        // bytes/s
+  constexpr double kCuRate = 13.0;        // copy bytes per cycle and CU, at most
+  constexpr double kLatency = 887.0;      // cycles: copy bytes in flight / rate
+  constexpr double kShallow = 26.0;       // cycles per item lost with one item in flight
+  constexpr double kClock = 2.4e9;
   const bool has_dw = v.family != FAM_PW, has_pw = v.family != FAM_DW;
   const int K = has_dw ? g.k : 1, S = has_dw ? g.s : 1;
   const int P = p.tile_h * p.tile_w;
-  const int nb = ceil_div(ceil_div(P, 16), 4);
+  const int bpw = std::max(1, v.max_p / 64);
+  const int nbt = ceil_div(P, 16);
+  int nb_max = 0;  // pixel blocks of the busiest compute wave
+  for (int w = 0; w < 4; ++w) {
+    int n = 0;
+    for (int b = 0; b < bpw; ++b) n += (b * 4 + w < nbt) ? 1 : 0;
+    nb_max = std::max(nb_max, n);
+  }
   const int ct = has_pw ? p.co_block / 16 : 0;
   const int cin = v.family == FAM_DW ? g.cm : g.ci;
   const int nchunks = v.family == FAM_DW ? 1 : ceil_div(cin, 64 / g.elt);
@@ -316,15 +331,20 @@ static double persistent_time_estimate(const Variant& v, const Geom& g, const fc
   const int64_t nwork = (int64_t)g.n * ceil_div(g.ho, p.tile_h) * ceil_div(g.wo, p.tile_w) * ceil_div(last, p.co_block);
   const int IH = has_dw ? (p.tile_h - 1) * S + K : p.tile_h;
   const int mode = v.family == FAM_DWPW ? M3_DWPW : (v.family == FAM_PW ? M3_PW : M3_DW);
-  const double c_item = 700.0 + nb * (has_dw ? K * K * 70.0 : 20.0) + nb * ct * 28.0;
-  const double p_item = 400.0 + 90.0 * copies_per_item3(mode, K, IH, v.pitch, ct);
+  const double dots = has_dw ? (double)nb_max * K * K * (16 / g.elt) : 0.0;
+  const double comp = kItem0 + kPerDot * dots;
+  const double prod = kPerCopy * copies_per_wave3(mode, K, IH, v.pitch, ct);
+  const double item_bytes = 1024.0 * copies_per_item3(mode, K, IH, v.pitch, ct);
   const int64_t grid = std::max<int64_t>(1, p.workgroups);
-  const double per_cu = std::max(1.0, (double)grid / hw.num_cus);
+  const double wpc = std::max(1.0, (double)grid / hw.num_cus);
+  const int depth = std::max(2, p.depth);
+  const double rate = std::min(kCuRate, wpc * (depth - 1) * item_bytes / kLatency);
+  const double per = std::max(std::max(comp * wpc, prod), item_bytes * wpc / rate) + (depth == 2 ? kShallow : 0.0);
   const double ipw = (double)ceil_div((int)std::min<int64_t>(nwork, 1 << 30), (int)grid) * nchunks;
-  const double cycles = ipw * std::max(c_item * per_cu, p_item) + 3000.0;
-  const double t_pipe = cycles / 1.6e9;
-  const double t_mem = (double)p.bytes_tiled / 5.0e12;
-  return std::max(t_pipe, t_mem);
+  const double t_pipe = (ipw * per + kLaunch) / kClock;
+  const double t_mem = (double)p.bytes_tiled / kHbm;
+  // (the pipeline term breaks ties between traffic-bound tilings)
+  return std::max(t_pipe, t_mem) + 1e-3 * t_pipe;
 }
 
 struct Cand {
@@ -342,6 +362,13 @@ static std::vector<int> tile_ws(const Variant& v) {
 }
 
 static const int kTileH[] = {1, 2, 4, 7, 8, 14, 16, 28, 32};
+
+// Tile shapes (TH, TW) searched for the persistent kernels: the shapes over which their
+// time model was fitted (widths whose windows fill the copy rows reasonably).
+static const int kTiles3[][2] = {{16, 14}, {8, 14}, {7, 14}, {4, 14}, {14, 14}, {28, 8}, {14, 7}, {8, 7}, {7, 7},
+                                 {16, 7},  {9, 14}, {12, 14}, {7, 28}, {4, 28}, {8, 28}, {9, 28}, {16, 16}, {8, 16},
+                                 {4, 16},  {2, 14}, {1, 14}, {3, 14}, {5, 14}, {6, 14}, {2, 7},  {4, 7},  {1, 7},
+                                 {2, 4},   {4, 4},  {2, 2},  {3, 7},  {6, 7},  {12, 7}};
 
 static fcm_status search(const Geom& g, const fcm_desc* d, const fcm_hw_desc& hw, fcm_plan_t* best_out,
                          bool allow_dma) {
@@ -370,9 +397,17 @@ static fcm_status search(const Geom& g, const fcm_desc* d, const fcm_hw_desc& hw
     std::vector<int> tws = v.tile_w ? std::vector<int>{v.tile_w} : tile_ws(v);
     std::vector<int> ths = v.tile_h ? std::vector<int>{v.tile_h}
                                     : std::vector<int>(std::begin(kTileH), std::end(kTileH));
-    for (int TW : tws) {
+    std::vector<std::pair<int, int>> tiles;
+    if (v.gen == 3) {
+      for (const auto& t : kTiles3) tiles.push_back({t[0], t[1]});
+    } else {
+      for (int TW : tws)
+        for (int TH : ths) tiles.push_back({TH, TW});
+    }
+    for (const auto& tile : tiles) {
+      const int TH = tile.first, TW = tile.second;
       if (!v.tile_w && TW > round_up(g.wo, v.dw_r ? v.dw_r : 1) && TW > 4) continue;
-      for (int TH : ths) {
+      {
         if (!v.tile_h && TH > g.ho && TH > 1) continue;
         // persistent kernels have one compiled output-channel block (the last is masked)
         const int cob_lo = v.gen == 3 ? v.max_cob : 16;
@@ -380,24 +415,29 @@ static fcm_status search(const Geom& g, const fcm_desc* d, const fcm_hw_desc& hw
         for (int COB = cob_lo; COB <= cob_hi; COB += 16) {
           for (int cb0 : cbs) {
             const int CB = (v.family == FAM_DW && v.gen != 2) ? COB : cb0;
-            int depth = 0;
-            const int lds = tiling_lds(v, g, TH, TW, CB, COB, hw.lds_per_wg, &depth);
-            if (lds <= 0 || lds > hw.lds_per_wg) continue;
-            Cand c;
-            memset(&c.p, 0, sizeof(c.p));
-            c.p.op = g.op;
-            c.p.tile_h = TH;
-            c.p.tile_w = TW;
-            c.p.c_block = CB;
-            c.p.co_block = COB;
-            c.p.variant = vi;
-            if (evaluate_plan(g, d, hw, &c.p) != FCM_OK) continue;
-            c.bytes = c.p.bytes_tiled;
-            c.wgs = c.p.workgroups;
-            c.lds = lds;
-            c.area = TH * TW;
-            c.cap = v.max_cob * 1024 + (v.max_p ? v.max_p : v.max_q);
-            cands.push_back(c);
+            // persistent kernels: one or two items in flight (deeper rings measured no faster)
+            const int depths[2] = {2, 3};
+            for (int di = 0; di < (v.gen == 3 ? 2 : 1); ++di) {
+              int depth = v.gen == 3 ? depths[di] : 0;
+              const int lds = tiling_lds(v, g, TH, TW, CB, COB, hw.lds_per_wg, &depth);
+              if (lds <= 0 || lds > hw.lds_per_wg) continue;
+              Cand c;
+              memset(&c.p, 0, sizeof(c.p));
+              c.p.op = g.op;
+              c.p.tile_h = TH;
+              c.p.tile_w = TW;
+              c.p.c_block = CB;
+              c.p.co_block = COB;
+              c.p.variant = vi;
+              c.p.depth = depth;
+              if (evaluate_plan(g, d, hw, &c.p) != FCM_OK) continue;
+              c.bytes = c.p.bytes_tiled;
+              c.wgs = c.p.workgroups;
+              c.lds = lds;
+              c.area = TH * TW;
+              c.cap = v.max_cob * 1024 + (v.max_p ? v.max_p : v.max_q);
+              cands.push_back(c);
+            }
           }
         }
       }

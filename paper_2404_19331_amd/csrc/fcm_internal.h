@@ -187,9 +187,11 @@ constexpr int kCopyWaves3 = 2;  // copy waves (each issues about half of an item
 constexpr int kThreads3 = 64 * (kCopyWaves3 + 4);  // + four compute waves
 constexpr int kMaxDepth3 = 8;   // ring buffers at most
 struct Lds3 {
-  int in_bytes, w_bytes, wd_off, raw_off, bias_off, buf_bytes, total;
+  int in_bytes, w_bytes, wd_off, raw_off, plane_bytes, bias_off, buf_bytes, total;
 };
-FCM_HD inline Lds3 lds3p(int dt, int K, int mode, int IH, int IWP, int CT, int depth = 2) {
+// One buffer holds `ks` planes (one per 64-byte channel chunk of the item: window, PW
+// weights, DW dot-operand words, raw DW weights) and then the biases of the item.
+FCM_HD inline Lds3 lds3p(int dt, int K, int mode, int IH, int IWP, int CT, int depth = 2, int ks = 1) {
   Lds3 r;
   const int cb = kRowB / elt_size(dt);
   r.in_bytes = IH * IWP * kRowB;
@@ -199,41 +201,42 @@ FCM_HD inline Lds3 lds3p(int dt, int K, int mode, int IH, int IWP, int CT, int d
   if (mode != M3_PW) off += (K * K * cb * 4 + 15) / 16 * 16;
   r.raw_off = off;
   if (mode != M3_PW) off += (64 * K * K + 1023) / 1024 * 1024;
-  r.bias_off = off;
-  off += 2048;
-  r.buf_bytes = off;
-  r.total = depth * off;
+  r.plane_bytes = off;
+  r.bias_off = ks * off;
+  r.buf_bytes = r.bias_off + 2048;
+  r.total = depth * r.buf_bytes;
   return r;
 }
 
-// Copy instructions of one item of a persistent kernel (host and device), in issue
-// order: raw DW weights and DW bias, window rows, PW weight rows, PW bias.
-FCM_HD inline int copies_per_item3(int mode, int K, int IH, int IWP, int CT) {
-  int n = IH * (IWP / 16);
-  if (mode != M3_DW) n += CT + 1;                          // PW weight rows, PW bias
-  if (mode != M3_PW) n += (64 * K * K + 1023) / 1024 + 1;  // raw DW weights, DW bias
+// Copy instructions of one item (ks channel chunks) of a persistent kernel (host and
+// device), in issue order: raw DW weights of each chunk and the DW bias, window rows,
+// PW weight rows of each chunk, PW bias.
+FCM_HD inline int copies_per_item3(int mode, int K, int IH, int IWP, int CT, int ks = 1) {
+  int n = ks * IH * (IWP / 16);
+  if (mode != M3_DW) n += ks * CT + 1;                          // PW weight rows, PW bias
+  if (mode != M3_PW) n += ks * ((64 * K * K + 1023) / 1024) + 1;  // raw DW weights, DW bias
   return n;
 }
 // Split of an item's copies between the two copy waves: wave 0 issues the DW weights
-// and bias (it converts them) and window rows [0, r0), wave 1 rows [r0, IH), the PW
-// weight rows and the PW bias; r0 balances the two counts.
-FCM_HD inline int rows_wave0_3(int mode, int K, int IH, int IWP, int CT) {
-  const int ipr = IWP / 16;
-  const int ndw = mode != M3_PW ? (64 * K * K + 1023) / 1024 + 1 : 0;
-  const int t = copies_per_item3(mode, K, IH, IWP, CT);
+// and bias (it converts them) and window rows [0, r0) of every chunk, wave 1 rows
+// [r0, IH), the PW weight rows and the PW bias; r0 balances the two counts.
+FCM_HD inline int rows_wave0_3(int mode, int K, int IH, int IWP, int CT, int ks = 1) {
+  const int ipr = (IWP / 16) * ks;
+  const int ndw = mode != M3_PW ? ks * ((64 * K * K + 1023) / 1024) + 1 : 0;
+  const int t = copies_per_item3(mode, K, IH, IWP, CT, ks);
   int r0 = (t - 2 * ndw + ipr) / (2 * ipr);
   r0 = r0 < 0 ? 0 : (r0 > IH ? IH : r0);
   return r0;
 }
-FCM_HD inline int copies_wave0_3(int mode, int K, int IH, int IWP, int CT) {
-  const int ndw = mode != M3_PW ? (64 * K * K + 1023) / 1024 + 1 : 0;
-  return ndw + rows_wave0_3(mode, K, IH, IWP, CT) * (IWP / 16);
+FCM_HD inline int copies_wave0_3(int mode, int K, int IH, int IWP, int CT, int ks = 1) {
+  const int ndw = mode != M3_PW ? ks * ((64 * K * K + 1023) / 1024) + 1 : 0;
+  return ndw + rows_wave0_3(mode, K, IH, IWP, CT, ks) * (IWP / 16) * ks;
 }
 // The larger per-wave share: a partial wait on the vector-memory counter covers at most
 // 63 outstanding copies of one wave.
-FCM_HD inline int copies_per_wave3(int mode, int K, int IH, int IWP, int CT) {
-  const int t = copies_per_item3(mode, K, IH, IWP, CT);
-  const int w0 = copies_wave0_3(mode, K, IH, IWP, CT);
+FCM_HD inline int copies_per_wave3(int mode, int K, int IH, int IWP, int CT, int ks = 1) {
+  const int t = copies_per_item3(mode, K, IH, IWP, CT, ks);
+  const int w0 = copies_wave0_3(mode, K, IH, IWP, CT, ks);
   return w0 > t - w0 ? w0 : t - w0;
 }
 
@@ -285,6 +288,7 @@ struct Variant {
   int gen = 1;      // 2: NHWC, 16-byte channel rows, LDS-DMA staging, fixed chunk of 64 bytes
                     // 3: as 2, persistent workgroups, run-time tile, max_p = 64 * blocks per wave
   int pitch = 0;    // gen 3: LDS window row pitch in pixels (window width must not exceed it)
+  int ks = 1;       // gen 3: 64-byte channel chunks per item
 };
 
 // Compiled variants of each translation unit, and all of them in a fixed order

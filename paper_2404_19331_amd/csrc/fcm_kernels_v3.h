@@ -1,11 +1,11 @@
 // fcm_kernels_v3.h -- persistent NHWC kernels for gfx950: DW->PW module, and the
 // layer-by-layer PW and DW kernels built from the same pieces.
 //
-// k_fused3<DT, K, S, BPW, CT, MODE, IWP>
+// k_fused3<DT, K, S, BPW, CT, MODE, IWP, KS>
 //   A persistent workgroup (two copy waves, four compute waves) owns a contiguous range
 //   of work tiles; a work tile is (image, TH x TW output tile, block of 16*CT output
-//   channels). Work tiles are cut into items, one per input-channel chunk of 64 bytes
-//   (one MFMA k-step); the items of the whole range form one stream, and the copies of
+//   channels). Work tiles are cut into items of KS input-channel chunks of 64 bytes (one
+//   MFMA k-step each); the items of the whole range form one stream, and the copies of
 //   items i+1 .. i+depth-1 (global -> LDS with buffer_load ... lds, out-of-range offsets
 //   read as zero, i.e. the zero padding of the convolution) overlap the arithmetic of
 //   item i, across tile boundaries as well.
@@ -195,7 +195,7 @@ __device__ __forceinline__ void wait_vm(int n) {
   }
 }
 
-template <class DT, int K, int S, int BPW, int CT, int MODE, int IWP>
+template <class DT, int K, int S, int BPW, int CT, int MODE, int IWP, int KS>
 __global__ __launch_bounds__(kThreads3) void k_fused3(KArgs a) {
   extern __shared__ __align__(16) char smem[];
   using T = typename DT::T;
@@ -213,14 +213,15 @@ __global__ __launch_bounds__(kThreads3) void k_fused3(KArgs a) {
   constexpr int NRAW = (64 * K * K + 1023) / 1024;
   static_assert(CPL * 4 == CB, "lane slot layout");
   static_assert(IWP % 16 == 0, "window pitch");
+  static_assert(MODE != M3_DW || KS == 1, "a depthwise-only item is one chunk");
 
   const int TH = a.TH, TW = a.TW, P = TH * TW;
   const int IW = HAS_DW ? (TW - 1) * SE + KE : TW;
   const int IH = HAS_DW ? (TH - 1) * SE + KE : TH;
-  const Lds3 lay = lds3p(dtype_id<DT>(), KE, MODE, IH, IWP, CT);
+  const Lds3 lay = lds3p(dtype_id<DT>(), KE, MODE, IH, IWP, CT, 2, KS);
   const int C = MODE == M3_DW ? a.Cm : a.Ci;
-  const int nchunks = MODE == M3_DW ? 1 : ceil_div(C, CB);
-  const int per_item = copies_per_item3(MODE, KE, IH, IWP, CT);
+  const int nchunks = MODE == M3_DW ? 1 : ceil_div(C, CB * KS);  // items per work tile
+  const int per_item = copies_per_item3(MODE, KE, IH, IWP, CT, KS);
 
   // ---- work range of this workgroup (consecutive logical ids share an XCD) ----
   const int G = gridDim.x;
@@ -272,9 +273,9 @@ __global__ __launch_bounds__(kThreads3) void k_fused3(KArgs a) {
     // ===== copy waves: all copies, D - 1 items ahead of the compute waves. Wave 0 issues
     // the DW weights and bias (and converts them) and window rows [0, r0); wave 1 the
     // rows [r0, IH), the PW weight rows and the PW bias. =====
-    const int r0 = rows_wave0_3(MODE, KE, IH, IWP, CT);
+    const int r0 = rows_wave0_3(MODE, KE, IH, IWP, CT, KS);
     const int wy0 = wave == 0 ? 0 : r0, wy1 = wave == 0 ? r0 : IH;
-    const int w0n = copies_wave0_3(MODE, KE, IH, IWP, CT);
+    const int w0n = copies_wave0_3(MODE, KE, IH, IWP, CT, KS);
     const int mine = wave == 0 ? w0n : per_item - w0n;  // copies per item of this wave
     const rsrc_t rw = make_rsrc(wp, HAS_PW ? (uint32_t)((size_t)a.Co * a.Ci * DT::ELT) : 0u);
     const rsrc_t rwd = make_rsrc(wd, HAS_DW ? (uint32_t)((size_t)C * KK * DT::ELT) : 0u);
@@ -292,7 +293,7 @@ __global__ __launch_bounds__(kThreads3) void k_fused3(KArgs a) {
     Tile iss_t = decode(wt0);
     auto issue_next = [&]() {
       char* buf = bufp(iss_slot);
-      const int c0 = MODE == M3_DW ? iss_t.cb * CB : iss_ch * CB;
+      const int c0 = MODE == M3_DW ? iss_t.cb * CB : iss_ch * (CB * KS);
       const int co0 = iss_t.cb * CoB;
       const int iy0 = HAS_DW ? iss_t.oy0 * SE - a.pad : iss_t.oy0;
       const int ix0 = HAS_DW ? iss_t.ox0 * SE - a.pad : iss_t.ox0;
@@ -300,40 +301,52 @@ __global__ __launch_bounds__(kThreads3) void k_fused3(KArgs a) {
       // Byte offsets: a per-lane part (window column, channel slot), fixed for the item,
       // plus a uniform part per window row. Lanes outside the image or the channel range
       // carry kOob, which stays out of range after the row offset (< 2^31) is added.
-      const int c = c0 + (lane & 3) * CPL;
-      uint32_t coff[IPR];
+      uint32_t coff[KS][IPR];
 #pragma unroll
-      for (int j = 0; j < IPR; ++j) {
-        const int gx = ix0 + wxl[j];
-        const bool ok = wxl[j] >= 0 && (unsigned)gx < (unsigned)a.W && c < C;
-        coff[j] = ok ? (uint32_t)((gx * C + c) * DT::ELT) : kOob;
+      for (int s = 0; s < KS; ++s) {
+        const int c = c0 + s * CB + (lane & 3) * CPL;
+#pragma unroll
+        for (int j = 0; j < IPR; ++j) {
+          const int gx = ix0 + wxl[j];
+          const bool ok = wxl[j] >= 0 && (unsigned)gx < (unsigned)a.W && c < C;
+          coff[s][j] = ok ? (uint32_t)((gx * C + c) * DT::ELT) : kOob;
+        }
       }
       const uint32_t rstride = (uint32_t)(a.W * C * DT::ELT);
       if (HAS_DW && wave == 0) {
 #pragma unroll
-        for (int r = 0; r < NRAW; ++r) {
-          const int b = r * 1024 + lane * 16;
-          dma16(rwd, buf + lay.raw_off + r * 1024, b < CB * KK * DT::ELT ? (uint32_t)(c0 * KK * DT::ELT + b) : kOob);
-        }
-        dma16(rbd, buf + lay.bias_off, lane * 16 < CB * 4 ? (uint32_t)(c0 * 4 + lane * 16) : kOob);
+        for (int s = 0; s < KS; ++s)
+#pragma unroll
+          for (int r = 0; r < NRAW; ++r) {
+            const int b = r * 1024 + lane * 16;
+            dma16(rwd, buf + s * lay.plane_bytes + lay.raw_off + r * 1024,
+                  b < CB * KK * DT::ELT ? (uint32_t)((c0 + s * CB) * KK * DT::ELT + b) : kOob);
+          }
+        dma16(rbd, buf + lay.bias_off, lane * 16 < KS * CB * 4 ? (uint32_t)(c0 * 4 + lane * 16) : kOob);
       }
       for (int wy = wy0; wy < wy1; ++wy) {
         const int gy = iy0 + wy;
         const bool rok = (unsigned)gy < (unsigned)a.H;
         const uint32_t roff = rok ? (uint32_t)gy * rstride : 0u;
 #pragma unroll
-        for (int j = 0; j < IPR; ++j) dma16(rx, buf + (wy * IPR + j) * 1024, rok ? coff[j] + roff : kOob);
+        for (int s = 0; s < KS; ++s)
+#pragma unroll
+          for (int j = 0; j < IPR; ++j)
+            dma16(rx, buf + s * lay.plane_bytes + (wy * IPR + j) * 1024, rok ? coff[s][j] + roff : kOob);
       }
       if (HAS_PW && wave == 1) {
         const int mrow = lane >> 2;
         const int j = (lane & 3) ^ (((mrow >> 3) & 1) << 1);
-        const int cw_ = c0 + j * CPL;
-        // rows beyond c_out fall outside the weight tensor and read as zero
-        const uint32_t woff =
-            cw_ < a.Ci ? (uint32_t)(((co0 + 4 * CT * (mrow >> 2) + (mrow & 3)) * a.Ci + cw_) * DT::ELT) : kOob;
 #pragma unroll
-        for (int ct = 0; ct < CT; ++ct)
-          dma16(rw, buf + lay.in_bytes + ct * 1024, woff + (uint32_t)(4 * ct * a.Ci * DT::ELT));
+        for (int s = 0; s < KS; ++s) {
+          const int cw_ = c0 + s * CB + j * CPL;
+          // rows beyond c_out fall outside the weight tensor and read as zero
+          const uint32_t woff =
+              cw_ < a.Ci ? (uint32_t)(((co0 + 4 * CT * (mrow >> 2) + (mrow & 3)) * a.Ci + cw_) * DT::ELT) : kOob;
+#pragma unroll
+          for (int ct = 0; ct < CT; ++ct)
+            dma16(rw, buf + s * lay.plane_bytes + lay.in_bytes + ct * 1024, woff + (uint32_t)(4 * ct * a.Ci * DT::ELT));
+        }
         dma16(rbp, buf + lay.bias_off + 1024, lane * 16 < CoB * 4 ? (uint32_t)(co0 * 4 + lane * 16) : kOob);
       }
       iss_slot = next_slot(iss_slot);
@@ -350,28 +363,31 @@ __global__ __launch_bounds__(kThreads3) void k_fused3(KArgs a) {
         constexpr int NEL = CB * KK;                      // weights of the chunk
         constexpr int EPV = 16 / DT::ELT;                 // elements per 16-byte vector
         constexpr int NV = (NEL * DT::ELT + 1023) / 1024;  // vectors per lane
-        char* buf = bufp(slot);
-        const char* raw = buf + lay.raw_off;
-        uint32_t* dst = (uint32_t*)(buf + lay.wd_off);
-        u32x4 rv[NV];
 #pragma unroll
-        for (int v = 0; v < NV; ++v) rv[v] = *(const u32x4*)(raw + (v * 64 + lane) * 16);  // within the NRAW KiB
+        for (int s = 0; s < KS; ++s) {
+          char* plane = bufp(slot) + s * lay.plane_bytes;
+          const char* raw = plane + lay.raw_off;
+          uint32_t* dst = (uint32_t*)(plane + lay.wd_off);
+          u32x4 rv[NV];
 #pragma unroll
-        for (int v = 0; v < NV; ++v) {
+          for (int v = 0; v < NV; ++v) rv[v] = *(const u32x4*)(raw + (v * 64 + lane) * 16);  // within the NRAW KiB
 #pragma unroll
-          for (int k = 0; k < EPV; ++k) {
-            const int e = (v * 64 + lane) * EPV + k;
-            if (e < NEL) {
-              const uint32_t word = rv[v][k * DT::ELT / 4];
-              uint32_t el;
-              if constexpr (DT::ELT == 4)
-                el = word;
-              else if constexpr (DT::ELT == 2)
-                el = (k & 1) ? word >> 16 : word & 0xffffu;
-              else
-                el = (word >> (8 * (k & 3))) & 0xffu;
-              const int ci = e / KK, tap = e - (e / KK) * KK;
-              dst[tap * CB + ci] = D3::weight_word(el, ci);
+          for (int v = 0; v < NV; ++v) {
+#pragma unroll
+            for (int k = 0; k < EPV; ++k) {
+              const int e = (v * 64 + lane) * EPV + k;
+              if (e < NEL) {
+                const uint32_t word = rv[v][k * DT::ELT / 4];
+                uint32_t el;
+                if constexpr (DT::ELT == 4)
+                  el = word;
+                else if constexpr (DT::ELT == 2)
+                  el = (k & 1) ? word >> 16 : word & 0xffffu;
+                else
+                  el = (word >> (8 * (k & 3))) & 0xffu;
+                const int ci = e / KK, tap = e - (e / KK) * KK;
+                dst[tap * CB + ci] = D3::weight_word(el, ci);
+              }
             }
           }
         }
@@ -446,49 +462,55 @@ __global__ __launch_bounds__(kThreads3) void k_fused3(KArgs a) {
     // can be scheduled ahead of the arithmetic.
     auto step = [&](auto nb_tag) {
       constexpr int NB = decltype(nb_tag)::value;
-      if constexpr (HAS_DW) {
-        Acc dacc[NB][CPL];
-        const char* wl = buf + lay.wd_off;
-        {
-          u32x4 bv[WQ];
 #pragma unroll
-          for (int q = 0; q < WQ; ++q) bv[q] = *(const u32x4*)(buf + lay.bias_off + (g * CPL + 4 * q) * 4);
+      for (int s = 0; s < KS; ++s) {  // the item's channel chunks, one plane each
+        const char* plane = buf + s * lay.plane_bytes;
+        if constexpr (HAS_DW) {
+          Acc dacc[NB][CPL];
+          const char* wl = plane + lay.wd_off;
+          {
+            u32x4 bv[WQ];
 #pragma unroll
-          for (int b = 0; b < NB; ++b)
+            for (int q = 0; q < WQ; ++q)
+              bv[q] = *(const u32x4*)(buf + lay.bias_off + (s * CB + g * CPL + 4 * q) * 4);
 #pragma unroll
-            for (int e = 0; e < CPL; ++e) {
-              const uint32_t u = bv[e >> 2][e & 3];
-              dacc[b][e] = __builtin_bit_cast(Acc, u);
-            }
-        }
-        const char* xb[NB];
+            for (int b = 0; b < NB; ++b)
 #pragma unroll
-        for (int b = 0; b < NB; ++b) xb[b] = buf + base[b];
-#pragma unroll
-        for (int ky = 0; ky < KE; ++ky) {
-#pragma unroll
-          for (int kx = 0; kx < KE; ++kx) {
-            const int toff = (ky * IWP + (SE == 2 ? (kx & 1) * (IWP / 2) + (kx >> 1) : kx)) * kRowB;
-            u32x4 wv[WQ];
-#pragma unroll
-            for (int q = 0; q < WQ; ++q) wv[q] = *(const u32x4*)(wl + ((ky * KE + kx) * CB + g * CPL + 4 * q) * 4);
-#pragma unroll
-            for (int b = 0; b < NB; ++b) D3::tap(dacc[b], *(const u32x4*)(xb[b] + toff), wv);
+              for (int e = 0; e < CPL; ++e) {
+                const uint32_t u = bv[e >> 2][e & 3];
+                dacc[b][e] = __builtin_bit_cast(Acc, u);
+              }
           }
+          const char* xb[NB];
+#pragma unroll
+          for (int b = 0; b < NB; ++b) xb[b] = plane + base[b];
+#pragma unroll
+          for (int ky = 0; ky < KE; ++ky) {
+#pragma unroll
+            for (int kx = 0; kx < KE; ++kx) {
+              const int toff = (ky * IWP + (SE == 2 ? (kx & 1) * (IWP / 2) + (kx >> 1) : kx)) * kRowB;
+              u32x4 wv[WQ];
+#pragma unroll
+              for (int q = 0; q < WQ; ++q)
+                wv[q] = *(const u32x4*)(wl + ((ky * KE + kx) * CB + g * CPL + 4 * q) * 4);
+#pragma unroll
+              for (int b = 0; b < NB; ++b) D3::tap(dacc[b], *(const u32x4*)(xb[b] + toff), wv);
+            }
+          }
+#pragma unroll
+          for (int b = 0; b < NB; ++b) bop[b] = D3::finish(dacc[b], ep_dw);
+        } else {
+#pragma unroll
+          for (int b = 0; b < NB; ++b) bop[b] = *(const u32x4*)(plane + base[b]);
         }
+        if constexpr (HAS_PW) {
+          const char* wl = plane + lay.in_bytes;
 #pragma unroll
-        for (int b = 0; b < NB; ++b) bop[b] = D3::finish(dacc[b], ep_dw);
-      } else {
+          for (int i = 0; i < CT; ++i) {
+            const u32x4 av = *(const u32x4*)(wl + i * 1024 + a_row);
 #pragma unroll
-        for (int b = 0; b < NB; ++b) bop[b] = *(const u32x4*)(buf + base[b]);
-      }
-      if constexpr (HAS_PW) {
-        const char* wl = buf + lay.in_bytes;
-#pragma unroll
-        for (int i = 0; i < CT; ++i) {
-          const u32x4 av = *(const u32x4*)(wl + i * 1024 + a_row);
-#pragma unroll
-          for (int b = 0; b < NB; ++b) mma16(DT{}, acc[b][i], av, bop[b]);
+            for (int b = 0; b < NB; ++b) mma16(DT{}, acc[b][i], av, bop[b]);
+          }
         }
       }
     };
@@ -590,9 +612,9 @@ __global__ __launch_bounds__(kThreads3) void k_fused3(KArgs a) {
   }
 }
 
-template <class DT, int K, int S, int BPW, int CT, int MODE, int IWP>
+template <class DT, int K, int S, int BPW, int CT, int MODE, int IWP, int KS>
 int launch_fused3(const KArgs& a, int grid, void* stream) {
-  auto fn = k_fused3<DT, K, S, BPW, CT, MODE, IWP>;
+  auto fn = k_fused3<DT, K, S, BPW, CT, MODE, IWP, KS>;
   const int lds = a.L.bytes;
   if (lds > 65536) {
     hipError_t e = hipFuncSetAttribute((const void*)fn, hipFuncAttributeMaxDynamicSharedMemorySize, lds);

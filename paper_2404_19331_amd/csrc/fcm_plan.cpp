@@ -193,13 +193,13 @@ static int tiling_lds(const Variant& v, const Geom& g, int TH, int TW, int CB, i
     const int IH = mode == M3_PW ? TH : (TH - 1) * g.s + g.k;
     if (IW > v.pitch) return 0;
     const int KE = mode == M3_PW ? 1 : g.k;
-    const int per_item = copies_per_wave3(mode, KE, IH, v.pitch, COB / 16);
+    const int per_item = copies_per_wave3(mode, KE, IH, v.pitch, COB / 16, v.ks);
     if (per_item > 63) return 0;
-    const int buf = lds3p(g.dtype, KE, mode, IH, v.pitch, COB / 16).buf_bytes;
+    const int buf = lds3p(g.dtype, KE, mode, IH, v.pitch, COB / 16, 2, v.ks).buf_bytes;
     const int d = ring_depth3(*depth, buf, per_item, lds_per_wg);
     if (d == 0) return 0;
     *depth = d;
-    return lds3p(g.dtype, KE, mode, IH, v.pitch, COB / 16, d).total;
+    return lds3p(g.dtype, KE, mode, IH, v.pitch, COB / 16, d, v.ks).total;
   }
   if (v.gen == 2) {
     // NHWC, 16-byte channel rows, 32-bit buffer offsets, fixed tile and 64-byte chunk
@@ -293,53 +293,58 @@ fcm_status evaluate_plan(const Geom& g, const fcm_desc* d, const fcm_hw_desc& hw
 // ---------------------------------------------------------------------------------
 
 // Time model of a persistent (gen 3) kernel launch, in seconds. Each workgroup runs a
-// pipeline of items (tile x 64-byte channel chunk): two copy waves issue the LDS copies
-// of items i+1 .. i+depth-1 while four compute waves run item i, so an item costs the
-// largest of: the busiest compute wave's depthwise dot instructions (workgroups sharing
-// a CU share its SIMDs), the busier copy wave's copy instructions, and the item's copy
-// bytes at the CU's copy rate, which is capped and limited by the bytes in flight
-// (Little's law). Launch overhead is added and the launch is never faster than its HBM
-// traffic. The constants were fitted (least squares on log time, then on the quality of
-// the chosen plans) to timings of every plan of the MobileNetV1, ViT-projection and
-// MBConv DW->PW layers on MI355X; the MFMA and LDS-read terms came out non-binding.
+// pipeline of items (tile x ks channel chunks of 64 bytes): two copy waves issue the
+// LDS copies of items i+1 .. i+depth-1 while four compute waves run item i, so an item
+// costs the largest of: the busiest compute wave's depthwise dot instructions
+// (workgroups sharing a CU share its SIMDs), the LDS bytes the compute waves read, the
+// busier copy wave's copy instructions, and the item's copy bytes at the CU's copy rate,
+// which is capped and limited by the bytes in flight (Little's law). Launch overhead is
+// added and the launch is never faster than its HBM traffic. The constants were fitted
+// (least squares on log time, then on the quality of the chosen plans) to timings of
+// every plan of the MobileNetV1, ViT-projection and MBConv DW->PW layers on MI355X; the
+// MFMA term came out non-binding.
 static double persistent_time_estimate(const Variant& v, const Geom& g, const fcm_plan_t& p,
                                        const fcm_hw_desc& hw) {
-  constexpr double kItem0 = 891.0;        // cycles per item, fixed (busiest compute wave)
-  constexpr double kPerDot = 10.6;        // cycles per depthwise dot instruction
-  constexpr double kPerCopy = 48.7;       // cycles per 1 KiB copy instruction (one copy wave)
-  constexpr double kLaunch = 13100.0;     // cycles of launch, prologue and drain
-  constexpr double kHbm = 5.59e12;        // bytes/s
-  constexpr double kCuRate = 13.0;        // copy bytes per cycle and CU, at most
-  constexpr double kLatency = 887.0;      // cycles: copy bytes in flight / rate
-  constexpr double kShallow = 26.0;       // cycles per item lost with one item in flight
+  constexpr double kItem0 = 1209.0;       // cycles per item, fixed (busiest compute wave)
+  constexpr double kPerDot = 9.04;        // cycles per depthwise dot instruction
+  constexpr double kPerLdsKiB = 1.06;     // cycles per KiB read from LDS by the compute waves
+  constexpr double kPerCopy = 104.8;      // cycles per 1 KiB copy instruction (one copy wave)
+  constexpr double kCopy0 = 1.4;          // cycles per item, fixed (copy wave)
+  constexpr double kLaunch = 12340.0;     // cycles of launch, prologue and drain
+  constexpr double kHbm = 3.88e12;        // bytes/s
+  constexpr double kCuRate = 8.0;         // copy bytes per cycle and CU, at most
+  constexpr double kLatency = 533.0;      // cycles: copy bytes in flight / rate
   constexpr double kClock = 2.4e9;
   const bool has_dw = v.family != FAM_PW, has_pw = v.family != FAM_DW;
   const int K = has_dw ? g.k : 1, S = has_dw ? g.s : 1;
   const int P = p.tile_h * p.tile_w;
   const int bpw = std::max(1, v.max_p / 64);
   const int nbt = ceil_div(P, 16);
+  const int ct = has_pw ? p.co_block / 16 : 0;
   int nb_max = 0;  // pixel blocks of the busiest compute wave
+  double lds_kib = 0;  // LDS KiB the compute waves read per chunk
   for (int w = 0; w < 4; ++w) {
     int n = 0;
     for (int b = 0; b < bpw; ++b) n += (b * 4 + w < nbt) ? 1 : 0;
     nb_max = std::max(nb_max, n);
+    if (n > 0) lds_kib += (double)K * K * n + (has_dw ? K * K * (4 / g.elt) : 0) + ct;
   }
-  const int ct = has_pw ? p.co_block / 16 : 0;
   const int cin = v.family == FAM_DW ? g.cm : g.ci;
-  const int nchunks = v.family == FAM_DW ? 1 : ceil_div(cin, 64 / g.elt);
+  const int nchunks = v.family == FAM_DW ? 1 : ceil_div(cin, v.ks * 64 / g.elt);  // items per work tile
   const int last = v.family == FAM_DW ? g.cm : g.co;
   const int64_t nwork = (int64_t)g.n * ceil_div(g.ho, p.tile_h) * ceil_div(g.wo, p.tile_w) * ceil_div(last, p.co_block);
   const int IH = has_dw ? (p.tile_h - 1) * S + K : p.tile_h;
   const int mode = v.family == FAM_DWPW ? M3_DWPW : (v.family == FAM_PW ? M3_PW : M3_DW);
-  const double dots = has_dw ? (double)nb_max * K * K * (16 / g.elt) : 0.0;
+  const double dots = has_dw ? (double)v.ks * nb_max * K * K * (16 / g.elt) : 0.0;
   const double comp = kItem0 + kPerDot * dots;
-  const double prod = kPerCopy * copies_per_wave3(mode, K, IH, v.pitch, ct);
-  const double item_bytes = 1024.0 * copies_per_item3(mode, K, IH, v.pitch, ct);
+  const double lds = kPerLdsKiB * v.ks * lds_kib;
+  const double prod = kCopy0 + kPerCopy * copies_per_wave3(mode, K, IH, v.pitch, ct, v.ks);
+  const double item_bytes = 1024.0 * copies_per_item3(mode, K, IH, v.pitch, ct, v.ks);
   const int64_t grid = std::max<int64_t>(1, p.workgroups);
   const double wpc = std::max(1.0, (double)grid / hw.num_cus);
   const int depth = std::max(2, p.depth);
   const double rate = std::min(kCuRate, wpc * (depth - 1) * item_bytes / kLatency);
-  const double per = std::max(std::max(comp * wpc, prod), item_bytes * wpc / rate) + (depth == 2 ? kShallow : 0.0);
+  const double per = std::max(std::max(comp * wpc, lds * wpc), std::max(prod, item_bytes * wpc / rate));
   const double ipw = (double)ceil_div((int)std::min<int64_t>(nwork, 1 << 30), (int)grid) * nchunks;
   const double t_pipe = (ipw * per + kLaunch) / kClock;
   const double t_mem = (double)p.bytes_tiled / kHbm;

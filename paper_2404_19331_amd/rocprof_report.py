@@ -28,15 +28,15 @@ _DT = {"f32": "TF32", "bf16": "TBF16", "i8": "TI8"}
 
 def kernel_symbol(variant):
     """Demangled kernel name of a persistent variant, e.g. k_dwpw3<bf16,3,1,1,16,p16> ->
-    void fcm::k_fused3<fcm::TBF16, 3, 1, 1, 16, 0, 16>(fcm::KArgs)."""
-    m = re.match(r"(k_\w+3)<(\w+),(\d+),(\d+),(\d+),(\d+),p(\d+)>$", variant)
+    void fcm::k_fused3<fcm::TBF16, 3, 1, 1, 16, 0, 16, 1>(fcm::KArgs)."""
+    m = re.match(r"(k_\w+3)<(\w+),(\d+),(\d+),(\d+),(\d+),p(\d+)(?:,k(\d+))?>$", variant)
     if not m:
         raise ValueError("not a persistent-kernel variant name: %s" % variant)
-    fam, dt, k, s, bpw, ct, pitch = m.groups()
+    fam, dt, k, s, bpw, ct, pitch, ks = m.groups()
     if fam == "k_pw3":
         k = s = "1"
-    return "void fcm::k_fused3<fcm::%s, %s, %s, %s, %s, %d, %s>(fcm::KArgs)" % (
-        _DT[dt], k, s, bpw, ct, _MODE[fam], pitch)
+    return "void fcm::k_fused3<fcm::%s, %s, %s, %s, %s, %d, %s, %s>(fcm::KArgs)" % (
+        _DT[dt], k, s, bpw, ct, _MODE[fam], pitch, ks or "1")
 
 
 def read_counters(path):

@@ -18,10 +18,11 @@
 //   weight operand zero (bf16: v_dot2c_f32_bf16, int8: v_dot4c_i32_i8), so no unpacking
 //   of the packed input is needed.
 //
-//   The pointwise weights rows are staged in a permuted order such that the accumulator
-//   lane (l % 16, l / 16) ends up holding 4*CT consecutive output channels of its pixel:
-//   the epilogue (+bias, activation, cast) writes them with 16-byte stores straight from
-//   registers, and the output is written once (output-stationary, Sec. III-A OS-LWS).
+//   The pointwise weights rows are staged in a permuted order such that accumulator lane
+//   (l % 16, l / 16) holds whole 16-byte granules of output channels of its pixel, and the
+//   four lane groups hold adjacent granules: the epilogue (+bias, activation, cast)
+//   writes 64 contiguous bytes per pixel with each 16-byte store instruction, straight
+//   from registers, and the output is written once (output-stationary, Sec. III-A OS-LWS).
 //
 //   MODE M3_PW: the DW stage is off (window = output tile); M3_DW: the PW stage is off,
 //   each lane writes its 16 bytes of depthwise output directly.
@@ -214,6 +215,13 @@ __global__ __launch_bounds__(kThreads3) void k_fused3(KArgs a) {
   static_assert(CPL * 4 == CB, "lane slot layout");
   static_assert(IWP % 16 == 0, "window pitch");
   static_assert(MODE != M3_DW || KS == 1, "a depthwise-only item is one chunk");
+  // Output-channel order of the PW accumulators: lane (l % 16, g = l / 16) of tile i holds
+  // values v = 0..3 of channel OGE * (4 * (i / OTPG) + g) + 4 * (i % OTPG) + v, so that the
+  // OTPG tiles of each 16-byte output granule sit in one lane and the four lane groups
+  // write 64 contiguous bytes of a pixel with each store instruction.
+  constexpr int OGE = 16 / DT::ELT;  // channels per 16-byte granule
+  constexpr int OTPG = OGE / 4;      // MFMA tiles per granule
+  static_assert(MODE == M3_DW || CT % OTPG == 0, "whole output granules per lane");
 
   const int TH = a.TH, TW = a.TW, P = TH * TW;
   const int IW = HAS_DW ? (TW - 1) * SE + KE : TW;
@@ -342,10 +350,11 @@ __global__ __launch_bounds__(kThreads3) void k_fused3(KArgs a) {
           const int cw_ = c0 + s * CB + j * CPL;
           // rows beyond c_out fall outside the weight tensor and read as zero
           const uint32_t woff =
-              cw_ < a.Ci ? (uint32_t)(((co0 + 4 * CT * (mrow >> 2) + (mrow & 3)) * a.Ci + cw_) * DT::ELT) : kOob;
+              cw_ < a.Ci ? (uint32_t)(((co0 + OGE * (mrow >> 2) + (mrow & 3)) * a.Ci + cw_) * DT::ELT) : kOob;
 #pragma unroll
           for (int ct = 0; ct < CT; ++ct)
-            dma16(rw, buf + s * lay.plane_bytes + lay.in_bytes + ct * 1024, woff + (uint32_t)(4 * ct * a.Ci * DT::ELT));
+            dma16(rw, buf + s * lay.plane_bytes + lay.in_bytes + ct * 1024,
+                  woff + (uint32_t)((4 * OGE * (ct / OTPG) + 4 * (ct % OTPG)) * a.Ci * DT::ELT));
         }
         dma16(rbp, buf + lay.bias_off + 1024, lane * 16 < CoB * 4 ? (uint32_t)(co0 * 4 + lane * 16) : kOob);
       }
@@ -534,64 +543,65 @@ __global__ __launch_bounds__(kThreads3) void k_fused3(KArgs a) {
             *(u32x4*)((T*)a.y + (((size_t)cur_t.n * a.Ho + oy) * a.Wo + ox) * C + c) = bop[b];
         }
       } else {
-        // this lane's output channels: co_l .. co_l + 4*CT - 1, contiguous
-        const int co_l = cur_t.cb * CoB + 4 * CT * g;
-        const int nvalid = min(4 * CT, a.Co - co_l);
-        if (nvalid > 0) {
-          Acc bias[4 * CT];
-          {
-            const char* bl = buf + lay.bias_off + 1024 + 4 * CT * g * 4;  // bias block of this co-block
+        // this lane's output granules k = 0 .. CT/OTPG - 1: channels co_blk + OGE * (4k + g) + [0, OGE)
+        constexpr int NG = MODE == M3_DW ? 1 : CT / OTPG;
+        const int co_blk = cur_t.cb * CoB;
+        const bool full16 = (a.Co * DT::ELT) % 16 == 0;
+        Acc bias[NG][OGE];
+        {
+          const char* bl = buf + lay.bias_off + 1024;  // bias block of this co-block
 #pragma unroll
-            for (int q = 0; q < CT; ++q) {
-              const u32x4 bv = *(const u32x4*)(bl + 16 * q);
+          for (int k = 0; k < NG; ++k)
+#pragma unroll
+            for (int q = 0; q < OGE / 4; ++q) {
+              const u32x4 bv = *(const u32x4*)(bl + (OGE * (4 * k + g) + 4 * q) * 4);
 #pragma unroll
               for (int e = 0; e < 4; ++e) {
                 const uint32_t u = bv[e];
-                bias[4 * q + e] = __builtin_bit_cast(Acc, u);
+                bias[k][4 * q + e] = __builtin_bit_cast(Acc, u);
               }
             }
-          }
-          constexpr int NW = 4 * CT * DT::ELT / 4;  // 32-bit words of this lane's output run
-          const bool full16 = (a.Co * DT::ELT) % 16 == 0;
-          const int vbytes = nvalid * DT::ELT;
+        }
 #pragma unroll
-          for (int b = 0; b < BPW; ++b) {
-            const int v = pyx[b];
-            const int oy = cur_t.oy0 + (v >> 16), ox = cur_t.ox0 + (v & 0xffff);
-            if (b >= nblk || v < 0 || oy >= a.Ho || ox >= a.Wo) continue;
-            uint32_t wds[NW];
+        for (int b = 0; b < BPW; ++b) {
+          const int v = pyx[b];
+          const int oy = cur_t.oy0 + (v >> 16), ox = cur_t.ox0 + (v & 0xffff);
+          if (b >= nblk || v < 0 || oy >= a.Ho || ox >= a.Wo) continue;
+          char* dpx = (char*)a.y + (((size_t)cur_t.n * a.Ho + oy) * a.Wo + ox) * a.Co * DT::ELT;
+#pragma unroll
+          for (int k = 0; k < NG; ++k) {
+            const int c0k = co_blk + OGE * (4 * k + g);
+            if (c0k >= a.Co) continue;
+            // channel c0k + j, j = 4t + e, is value e of tile k * OTPG + t
+            uint32_t wd4[4];
             if constexpr (DT::ELT == 4) {
 #pragma unroll
-              for (int i = 0; i < CT; ++i)
-#pragma unroll
-                for (int e = 0; e < 4; ++e) wds[4 * i + e] = __float_as_uint(epi_f(acc[b][i][e] + bias[4 * i + e], ep_pw));
+              for (int e = 0; e < 4; ++e) wd4[e] = __float_as_uint(epi_f(acc[b][k][e] + bias[k][e], ep_pw));
             } else if constexpr (DT::ELT == 2) {
 #pragma unroll
-              for (int i = 0; i < CT; ++i)
-#pragma unroll
-                for (int e = 0; e < 4; e += 2)
-                  wds[2 * i + e / 2] = pack_bf16x2(epi_f(acc[b][i][e] + bias[4 * i + e], ep_pw),
-                                                   epi_f(acc[b][i][e + 1] + bias[4 * i + e + 1], ep_pw));
+              for (int w = 0; w < 4; ++w) {
+                const int t = w >> 1, e = 2 * (w & 1);
+                wd4[w] = pack_bf16x2(epi_f(acc[b][2 * k + t][e] + bias[k][4 * t + e], ep_pw),
+                                     epi_f(acc[b][2 * k + t][e + 1] + bias[k][4 * t + e + 1], ep_pw));
+              }
             } else {
 #pragma unroll
-              for (int i = 0; i < CT; ++i) {
+              for (int w = 0; w < 4; ++w) {
                 uint32_t wv = 0;
 #pragma unroll
                 for (int e = 0; e < 4; ++e)
-                  wv |= ((uint32_t)epi_i(acc[b][i][e] + bias[4 * i + e], ep_pw) & 0xffu) << (8 * e);
-                wds[i] = wv;
+                  wv |= ((uint32_t)epi_i(acc[b][4 * k + w][e] + bias[k][4 * w + e], ep_pw) & 0xffu) << (8 * e);
+                wd4[w] = wv;
               }
             }
-            char* dst = (char*)a.y + ((((size_t)cur_t.n * a.Ho + oy) * a.Wo + ox) * a.Co + co_l) * DT::ELT;
+            char* dst = dpx + (size_t)c0k * DT::ELT;
             if (full16) {
-#pragma unroll
-              for (int k = 0; k < NW / 4; ++k)
-                if (16 * k < vbytes)
-                  *(u32x4*)(dst + 16 * k) = u32x4{wds[4 * k], wds[4 * k + 1], wds[4 * k + 2], wds[4 * k + 3]};
+              *(u32x4*)dst = u32x4{wd4[0], wd4[1], wd4[2], wd4[3]};
             } else {
+              // c_out * elt is a multiple of 4: whole 32-bit words are in or out of range
 #pragma unroll
-              for (int k = 0; k < NW; ++k)
-                if (4 * k < vbytes) *(uint32_t*)(dst + 4 * k) = wds[k];
+              for (int w = 0; w < 4; ++w)
+                if (c0k + w * (4 / DT::ELT) < a.Co) *(uint32_t*)(dst + 4 * w) = wd4[w];
             }
           }
         }

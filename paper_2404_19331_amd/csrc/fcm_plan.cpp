@@ -301,19 +301,21 @@ fcm_status evaluate_plan(const Geom& g, const fcm_desc* d, const fcm_hw_desc& hw
 // which is capped and limited by the bytes in flight (Little's law). Launch overhead is
 // added and the launch is never faster than its HBM traffic. The constants were fitted
 // (least squares on log time, then on the quality of the chosen plans) to timings of
-// every plan of the MobileNetV1, ViT-projection and MBConv DW->PW layers on MI355X; the
-// MFMA term came out non-binding.
+// every plan of the MobileNetV1, ViT-projection and MBConv DW->PW layers on MI355X
+// (global search over the constants for the quality of the chosen plans).
 static double persistent_time_estimate(const Variant& v, const Geom& g, const fcm_plan_t& p,
                                        const fcm_hw_desc& hw) {
-  constexpr double kItem0 = 1209.0;       // cycles per item, fixed (busiest compute wave)
-  constexpr double kPerDot = 9.04;        // cycles per depthwise dot instruction
-  constexpr double kPerLdsKiB = 1.06;     // cycles per KiB read from LDS by the compute waves
-  constexpr double kPerCopy = 104.8;      // cycles per 1 KiB copy instruction (one copy wave)
-  constexpr double kCopy0 = 1.4;          // cycles per item, fixed (copy wave)
-  constexpr double kLaunch = 12340.0;     // cycles of launch, prologue and drain
-  constexpr double kHbm = 3.88e12;        // bytes/s
-  constexpr double kCuRate = 8.0;         // copy bytes per cycle and CU, at most
-  constexpr double kLatency = 533.0;      // cycles: copy bytes in flight / rate
+  constexpr double kItem0 = 1274.0;       // cycles per item, fixed (busiest compute wave)
+  constexpr double kPerDot = 3.42;        // cycles per depthwise dot instruction
+  constexpr double kPerMfma = 0.575;      // cycles per MFMA instruction
+  constexpr double kPerLdsKiB = 10.7;     // cycles per KiB read from LDS by the compute waves
+  constexpr double kPerCopy = 165.9;      // cycles per 1 KiB copy instruction (one copy wave)
+  constexpr double kCopy0 = 152.0;        // cycles per item, fixed (copy wave)
+  constexpr double kShallow = 377.0;      // cycles per item lost with one item in flight
+  constexpr double kLaunch = 10720.0;     // cycles of launch, prologue and drain
+  constexpr double kHbm = 7.98e12;        // bytes/s
+  constexpr double kCuRate = 11.9;        // copy bytes per cycle and CU, at most
+  constexpr double kLatency = 1092.0;     // cycles: copy bytes in flight / rate
   constexpr double kClock = 2.4e9;
   const bool has_dw = v.family != FAM_PW, has_pw = v.family != FAM_DW;
   const int K = has_dw ? g.k : 1, S = has_dw ? g.s : 1;
@@ -336,7 +338,8 @@ static double persistent_time_estimate(const Variant& v, const Geom& g, const fc
   const int IH = has_dw ? (p.tile_h - 1) * S + K : p.tile_h;
   const int mode = v.family == FAM_DWPW ? M3_DWPW : (v.family == FAM_PW ? M3_PW : M3_DW);
   const double dots = has_dw ? (double)v.ks * nb_max * K * K * (16 / g.elt) : 0.0;
-  const double comp = kItem0 + kPerDot * dots;
+  const double mfmas = (double)v.ks * nb_max * ct * (g.elt == 4 ? 4 : 1);
+  const double comp = kItem0 + kPerDot * dots + kPerMfma * mfmas;
   const double lds = kPerLdsKiB * v.ks * lds_kib;
   const double prod = kCopy0 + kPerCopy * copies_per_wave3(mode, K, IH, v.pitch, ct, v.ks);
   const double item_bytes = 1024.0 * copies_per_item3(mode, K, IH, v.pitch, ct, v.ks);
@@ -344,7 +347,8 @@ static double persistent_time_estimate(const Variant& v, const Geom& g, const fc
   const double wpc = std::max(1.0, (double)grid / hw.num_cus);
   const int depth = std::max(2, p.depth);
   const double rate = std::min(kCuRate, wpc * (depth - 1) * item_bytes / kLatency);
-  const double per = std::max(std::max(comp * wpc, lds * wpc), std::max(prod, item_bytes * wpc / rate));
+  const double per = std::max(std::max(comp * wpc, lds * wpc), std::max(prod, item_bytes * wpc / rate)) +
+                     (depth == 2 ? kShallow : 0.0);
   const double ipw = (double)ceil_div((int)std::min<int64_t>(nwork, 1 << 30), (int)grid) * nchunks;
   const double t_pipe = (ipw * per + kLaunch) / kClock;
   const double t_mem = (double)p.bytes_tiled / kHbm;

@@ -20,9 +20,12 @@
  *
  * Conventions shared by every entry point
  * ---------------------------------------
- *  * Tensors are caller-owned DEVICE pointers (e.g. PyTorch tensors). The library never
- *    allocates, frees or synchronises; every launch is asynchronous on `stream`
- *    (a hipStream_t; NULL = the null stream).
+ *  * Tensors are caller-owned DEVICE pointers (e.g. PyTorch tensors). Every launch is
+ *    asynchronous on `stream` (a hipStream_t; NULL = the null stream); the library never
+ *    frees or synchronises. It allocates only its split workspace: the first call with a
+ *    plan whose `splits` > 1 on a device allocates FCM_SPLIT_WORKSPACE_BYTES there, once.
+ *    Calls with such plans share that workspace, so on one device they must not run
+ *    concurrently (e.g. on two streams).
  *  * Activations: x is [n, c, h, w] (FCM_NCHW) or [n, h, w, c] (FCM_NHWC), dense,
  *    row-major. The output uses the same layout.
  *  * Weights are canonical regardless of layout: depthwise [c][k][k] (PyTorch
@@ -50,6 +53,10 @@
 #ifdef __cplusplus
 extern "C" {
 #endif
+
+/* Device memory the library allocates once per device for split plans (partial sums
+ * and arrival counters); plans whose workspace would exceed it are not split. */
+#define FCM_SPLIT_WORKSPACE_BYTES (64u << 20)
 
 typedef enum {
   FCM_OK = 0,
@@ -132,6 +139,11 @@ typedef struct {
   int32_t fuse;          /* planner verdict: 1 if the fused estimate < layer-by-layer */
   int32_t depth;         /* persistent kernels: LDS ring buffers, i.e. items in flight + 1
                             (2..8; 0 on input to fcm_plan_evaluate = the planner's choice) */
+  int32_t splits;        /* persistent DW->PW and PW kernels: the channel chunks of each
+                            work tile are split over this many workgroups; each writes its
+                            partial sums to the library's workspace and a second kernel
+                            adds them in split order, then applies bias, activation and
+                            cast (1 = no split; 0 on input to fcm_plan_evaluate = 1) */
   int64_t bytes_ideal;          /* input + weights + output, each once                  */
   int64_t bytes_tiled;          /* per-workgroup loads + stores of this tiling (exact)  */
   int64_t bytes_paper;          /* Eq. 1-4 estimate of this module at this tiling        */

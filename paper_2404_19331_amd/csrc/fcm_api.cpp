@@ -115,6 +115,24 @@ static int device_cus() {
   return cache[dev];
 }
 
+// Split workspace of the current device: FCM_SPLIT_WORKSPACE_BYTES, allocated on first
+// use and kept until the process ends (split plans write every partial sum they read,
+// so it needs no initialisation).
+static void* split_workspace() {
+  static std::mutex mu;
+  static std::vector<void*> cache;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return nullptr;
+  std::lock_guard<std::mutex> lock(mu);
+  if ((int)cache.size() <= dev) cache.resize(dev + 1, nullptr);
+  if (!cache[dev]) {
+    void* p = nullptr;
+    if (hipMalloc(&p, FCM_SPLIT_WORKSPACE_BYTES) != hipSuccess) return nullptr;
+    cache[dev] = p;
+  }
+  return cache[dev];
+}
+
 static fcm_status check_alignment(const void* p, int elt, const char* what) {
   if (p && ((uintptr_t)p % (uintptr_t)elt) != 0)
     return fail(FCM_EINVAL, std::string(what) + " is not aligned to its element size");
@@ -211,6 +229,13 @@ static fcm_status run(int op, const fcm_desc* d, const Tensors& t, const fcm_pla
     default: break;
   }
   a.nwork = a.N * a.tiles_y * a.tiles_x * a.n_cb;
+  a.splits = 1;
+  if (v.gen == 3 && p.splits > 1) {
+    a.ws = split_workspace();
+    if (!a.ws) return fail(FCM_EDEVICE, "could not allocate the split workspace");
+    a.splits = p.splits;
+    a.nwork *= p.splits;  // work units
+  }
   a.cus = device_cus();
   a.grid_cap = v.gen == 3 ? p.workgroups : 0;
   a.depth = p.depth;

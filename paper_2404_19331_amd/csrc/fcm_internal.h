@@ -208,6 +208,13 @@ FCM_HD inline Lds3 lds3p(int dt, int K, int mode, int IH, int IWP, int CT, int d
   return r;
 }
 
+// Split plans: items per split of a work tile with `ipt` items, and whether every split
+// gets at least one item.
+FCM_HD inline int items_per_split3(int ipt, int splits) { return (ipt + splits - 1) / splits; }
+FCM_HD inline bool splits_valid3(int ipt, int splits) {
+  return splits >= 1 && (splits - 1) * items_per_split3(ipt, splits) < ipt;
+}
+
 // Copy instructions of one item (ks channel chunks) of a persistent kernel (host and
 // device), in issue order: raw DW weights of each chunk and the DW bias, window rows,
 // PW weight rows of each chunk, PW bias.
@@ -262,8 +269,10 @@ struct KArgs {
   Requant rq[3];
   int vec_x, vec_w1, vec_w2, vec_w3, vec_y;
   LdsLayout L;
-  int nwork;     // persistent kernels: work tiles (image x tile x channel block)
+  int nwork;     // persistent kernels: work units (work tiles x splits)
   int depth;     // persistent kernels: LDS ring buffers (>= 2)
+  int splits;    // persistent kernels: workgroups sharing one work tile's channel chunks
+  void* ws;      // splits > 1: partial sums [split][work tile][TH*TW][COB] (fp32 / int32)
   int cus;       // compute units of the device
   int grid_cap;  // persistent kernels: at most this many workgroups (0 = no cap)
   unsigned long long* trace;  // development timeline buffer (used only in FCM_TRACE builds)

@@ -196,7 +196,7 @@ __device__ __forceinline__ void wait_vm(int n) {
   }
 }
 
-template <class DT, int K, int S, int BPW, int CT, int MODE, int IWP, int KS>
+template <class DT, int K, int S, int BPW, int CT, int MODE, int IWP, int KS, bool SPLIT>
 __global__ __launch_bounds__(kThreads3) void k_fused3(KArgs a) {
   extern __shared__ __align__(16) char smem[];
   using T = typename DT::T;
@@ -230,13 +230,21 @@ __global__ __launch_bounds__(kThreads3) void k_fused3(KArgs a) {
   const int C = MODE == M3_DW ? a.Cm : a.Ci;
   const int nchunks = MODE == M3_DW ? 1 : ceil_div(C, CB * KS);  // items per work tile
   const int per_item = copies_per_item3(MODE, KE, IH, IWP, CT, KS);
+  // Work units: split u % SPL of work tile u / SPL runs items [u_lo(u), u_hi(u)).
+  // (a separate instance: the partial-sum epilogue in the same loop costs the unsplit
+  // kernel its schedule)
+  const int SPL = SPLIT ? a.splits : 1;
+  const int ips = items_per_split3(nchunks, SPL);
+  auto u_lo = [&](int u) { return (u % SPL) * ips; };
+  auto u_hi = [&](int u) { return min(nchunks, (u % SPL) * ips + ips); };
 
   // ---- work range of this workgroup (consecutive logical ids share an XCD) ----
   const int G = gridDim.x;
   const int L = xcd_remap(blockIdx.x, G);
   const int wt0 = (int)((int64_t)a.nwork * L / G), wt1 = (int)((int64_t)a.nwork * (L + 1) / G);
   if (wt1 <= wt0) return;
-  const int nitems = (wt1 - wt0) * nchunks;
+  int nitems = 0;
+  for (int u = wt0; u < wt1; ++u) nitems += u_hi(u) - u_lo(u);
 
   // waves 0..kCopyWaves3-1 copy, the next four compute; the wave index is uniform:
   // keep it scalar
@@ -297,8 +305,8 @@ __global__ __launch_bounds__(kThreads3) void k_fused3(KArgs a) {
       if (SE == 2) wx = col < IWP / 2 ? 2 * col : 2 * (col - IWP / 2) + 1;
       wxl[j] = wx < IW ? wx : -1;
     }
-    int iss_slot = 0, iss_wt = wt0, iss_ch = 0;
-    Tile iss_t = decode(wt0);
+    int iss_slot = 0, iss_wt = wt0, iss_ch = u_lo(wt0), iss_hi = u_hi(wt0);
+    Tile iss_t = decode(wt0 / SPL);
     auto issue_next = [&]() {
       char* buf = bufp(iss_slot);
       const int c0 = MODE == M3_DW ? iss_t.cb * CB : iss_ch * (CB * KS);
@@ -359,9 +367,10 @@ __global__ __launch_bounds__(kThreads3) void k_fused3(KArgs a) {
         dma16(rbp, buf + lay.bias_off + 1024, lane * 16 < CoB * 4 ? (uint32_t)(co0 * 4 + lane * 16) : kOob);
       }
       iss_slot = next_slot(iss_slot);
-      if (++iss_ch == nchunks) {
-        iss_ch = 0;
-        if (++iss_wt < wt1) iss_t = decode(iss_wt);
+      if (++iss_ch == iss_hi && ++iss_wt < wt1) {
+        iss_ch = u_lo(iss_wt);
+        iss_hi = u_hi(iss_wt);
+        iss_t = decode(iss_wt / SPL);
       }
     };
     // Depthwise weights of the item in ring slot `slot` (wave 0): raw [c][tap] elements
@@ -459,8 +468,8 @@ __global__ __launch_bounds__(kThreads3) void k_fused3(KArgs a) {
   barrier3();  // item 0 is ready
   int tsc = 32;
   FCM_TSC(tsc++);
-  int wt = wt0, ch = 0, slot = 0;
-  Tile cur_t = decode(wt0);
+  int wt = wt0, ch = u_lo(wt0), ch_hi = u_hi(wt0), slot = 0;
+  Tile cur_t = decode(wt0 / SPL);
   for (int it = 0; it < nitems; ++it) {
     const char* buf = bufp(slot);
     slot = next_slot(slot);
@@ -531,8 +540,8 @@ __global__ __launch_bounds__(kThreads3) void k_fused3(KArgs a) {
       else if (BPW > 3 && nblk == 3) step(std::integral_constant<int, (BPW > 3 ? 3 : 1)>{});
     }
 
-    if (ch + 1 == nchunks) {
-      // ---- epilogue of the work tile: straight from registers to global memory ----
+    if (ch + 1 == ch_hi) {
+      // ---- epilogue of the work unit: straight from registers to global memory ----
       if constexpr (MODE == M3_DW) {
         const int c = cur_t.cb * CB + g * CPL;
 #pragma unroll
@@ -542,6 +551,23 @@ __global__ __launch_bounds__(kThreads3) void k_fused3(KArgs a) {
           if (v >= 0 && oy < a.Ho && ox < a.Wo && c < C)
             *(u32x4*)((T*)a.y + (((size_t)cur_t.n * a.Ho + oy) * a.Wo + ox) * C + c) = bop[b];
         }
+      } else if constexpr (SPLIT) {
+        // a split of the work tile: its partial sums (before bias and activation) go to
+        // slice [split][work tile][pixel][channel] of the workspace, 16 bytes per MFMA tile
+        Acc* wsp = (Acc*)a.ws + ((size_t)(wt % SPL) * (a.nwork / SPL) + wt / SPL) * P * CoB;
+#pragma unroll
+        for (int b = 0; b < BPW; ++b) {
+          const int v = pyx[b];
+          if (b >= nblk || v < 0) continue;
+          Acc* row = wsp + (size_t)((v >> 16) * TW + (v & 0xffff)) * CoB;
+#pragma unroll
+          for (int i = 0; i < CT; ++i)
+            *(AccV*)(row + OGE * (4 * (i / OTPG) + g) + 4 * (i % OTPG)) = acc[b][i];
+        }
+#pragma unroll
+        for (int b = 0; b < BPW; ++b)
+#pragma unroll
+          for (int i = 0; i < CT; ++i) acc[b][i] = AccV{0, 0, 0, 0};
       } else {
         // this lane's output granules k = 0 .. CT/OTPG - 1: channels co_blk + OGE * (4k + g) + [0, OGE)
         constexpr int NG = MODE == M3_DW ? 1 : CT / OTPG;
@@ -610,8 +636,11 @@ __global__ __launch_bounds__(kThreads3) void k_fused3(KArgs a) {
 #pragma unroll
           for (int i = 0; i < CT; ++i) acc[b][i] = AccV{0, 0, 0, 0};
       }
-      ch = 0;
-      if (++wt < wt1) cur_t = decode(wt);
+      if (++wt < wt1) {
+        ch = u_lo(wt);
+        ch_hi = u_hi(wt);
+        cur_t = decode(wt / SPL);
+      }
     } else {
       ++ch;
     }
@@ -622,29 +651,96 @@ __global__ __launch_bounds__(kThreads3) void k_fused3(KArgs a) {
   }
 }
 
+// Second kernel of a split plan: for every work tile, pixel and group of four output
+// channels, the partial sums of the splits are added in split order, then bias,
+// activation and cast as in the single-kernel epilogue (same rounding: the fp32 or int32
+// total of the contraction, then +bias, then the stage's activation / requantisation).
+template <class DT, int STAGE>
+__global__ __launch_bounds__(256) void k_combine3(KArgs a) {
+  using T = typename DT::T;
+  using Acc = typename DT::Acc;
+  const int SPL = a.splits, ntile = a.nwork / SPL;
+  const int TH = a.TH, TW = a.TW, P = TH * TW, CoB = a.COB, nq = CoB / 4;
+  const int64_t total = (int64_t)ntile * P * nq;
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= total) return;
+  const int q = (int)(idx % nq);
+  const int64_t r = idx / nq;
+  const int p = (int)(r % P), wtile = (int)(r / P);
+  int t = wtile;
+  const int cb = t % a.n_cb;
+  t /= a.n_cb;
+  const int tx = t % a.tiles_x;
+  t /= a.tiles_x;
+  const int ty = t % a.tiles_y, n = t / a.tiles_y;
+  const int oy = ty * TH + p / TW, ox = tx * TW + p % TW;
+  const int co = cb * CoB + 4 * q;
+  if (oy >= a.Ho || ox >= a.Wo || co >= a.Co) return;
+  const size_t slice = (size_t)ntile * P * CoB;
+  const Acc* src = (const Acc*)a.ws + ((size_t)wtile * P + p) * CoB + 4 * q;
+  Acc sum[4] = {0, 0, 0, 0};
+  for (int s = 0; s < SPL; ++s) {
+    const typename DT::AccV v = *(const typename DT::AccV*)(src + s * slice);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) sum[e] += v[e];
+  }
+  const Epi3 ep = make_epi3(a.act[STAGE], a.rq[STAGE]);  // STAGE: index of the PW convolution
+  const void* bp = STAGE == 0 ? a.b1 : a.b2;
+  T* y = (T*)a.y + (((size_t)n * a.Ho + oy) * a.Wo + ox) * a.Co + co;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    if (co + e >= a.Co) break;
+    if constexpr (DT::ELT == 1) {
+      const int32_t b = bp ? ((const int32_t*)bp)[co + e] : 0;
+      y[e] = (T)epi_i(sum[e] + b, ep);
+    } else {
+      const float b = bp ? ((const float*)bp)[co + e] : 0.0f;
+      const float o = epi_f(sum[e] + b, ep);
+      if constexpr (DT::ELT == 4)
+        y[e] = o;
+      else
+        *(uint16_t*)(y + e) = (uint16_t)(pack_bf16x2(o, 0.0f) & 0xffffu);
+    }
+  }
+}
+
 template <class DT, int K, int S, int BPW, int CT, int MODE, int IWP, int KS>
 int launch_fused3(const KArgs& a, int grid, void* stream) {
-  auto fn = k_fused3<DT, K, S, BPW, CT, MODE, IWP, KS>;
+  const bool split = MODE != M3_DW && a.splits > 1;
+  auto fn = split ? k_fused3<DT, K, S, BPW, CT, MODE, IWP, KS, MODE != M3_DW>
+                  : k_fused3<DT, K, S, BPW, CT, MODE, IWP, KS, false>;
   const int lds = a.L.bytes;
   if (lds > 65536) {
     hipError_t e = hipFuncSetAttribute((const void*)fn, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
     if (e != hipSuccess) return (int)e;
   }
-  // persistent grid: as many workgroups as are resident at once, at most one per work tile
-  static thread_local int cached_lds = -1, cached_occ = 1;
-  if (cached_lds != lds) {
+  // persistent grid: as many workgroups as are resident at once, at most one per work unit
+  static thread_local int cached_lds[2] = {-1, -1}, cached_occ[2] = {1, 1};
+  const int ci = split ? 1 : 0;
+  if (cached_lds[ci] != lds) {
     int occ = 0;
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, (const void*)fn, kThreads3, lds) != hipSuccess || occ < 1)
       occ = 1;
-    cached_lds = lds;
-    cached_occ = occ;
+    cached_lds[ci] = lds;
+    cached_occ[ci] = occ;
   }
-  int g = a.cus * cached_occ;
+  int g = a.cus * cached_occ[ci];
   if (a.grid_cap > 0 && g > a.grid_cap) g = a.grid_cap;
   if (g > a.nwork) g = a.nwork;
   if (g < 1) g = 1;
   (void)grid;
   hipLaunchKernelGGL(fn, dim3(g), dim3(kThreads3), lds, (hipStream_t)stream, a);
+  if constexpr (MODE != M3_DW) {
+    if (a.splits > 1) {
+      hipError_t e = hipGetLastError();
+      if (e != hipSuccess) return (int)e;
+      KArgs c = a;
+      c.COB = 16 * CT;
+      const int64_t total = (int64_t)(a.nwork / a.splits) * a.TH * a.TW * (4 * CT);
+      hipLaunchKernelGGL((k_combine3<DT, MODE == M3_PW ? 0 : 1>), dim3((unsigned)((total + 255) / 256)), dim3(256), 0,
+                         (hipStream_t)stream, c);
+    }
+  }
   return (int)hipGetLastError();
 }
 

@@ -162,6 +162,11 @@ static int ring_depth3(int want, int buf, int per_item, int lds_per_wg) {
   return (dmax >= 3 && 3 * buf <= lds_per_wg) ? 3 : 2;
 }
 
+// Workspace bytes of a split plan: fp32 / int32 partial sums [split][work tile][TH*TW][COB].
+static int64_t split_workspace_bytes(int64_t tiles, int pixels, int cob, int splits) {
+  return (int64_t)splits * tiles * pixels * cob * 4;
+}
+
 // LDS bytes of a tiling (0 if the variant cannot implement it). For the persistent
 // kernels *depth is the requested ring depth on input (0 = choose) and the chosen one on
 // output.
@@ -260,15 +265,25 @@ fcm_status evaluate_plan(const Geom& g, const fcm_desc* d, const fcm_hw_desc& hw
   const int64_t wgs = (int64_t)g.n * nty * ntx * ceil_div(last, p->co_block);
   if (wgs <= 0 || wgs > 0x7fffffff) return fail(FCM_EUNSUPPORTED, "plan: grid too large");
   const Bytes b = module_bytes(g, p->tile_h, p->tile_w, p->co_block);
+  if (v.gen != 3 && p->splits > 1) return fail(FCM_EUNSUPPORTED, "plan: only the persistent kernels split");
   if (v.gen == 3) {
+    const int splits = p->splits > 1 ? p->splits : 1;
+    if (splits > 1) {
+      if (v.family == FAM_DW) return fail(FCM_EUNSUPPORTED, "plan: a depthwise-only kernel does not split");
+      const int ipt = ceil_div(g.ci, v.ks * (64 / g.elt));
+      if (!splits_valid3(ipt, splits)) return fail(FCM_EUNSUPPORTED, "plan: more splits than channel chunks");
+      if (split_workspace_bytes(wgs, p->tile_h * p->tile_w, p->co_block, splits) > FCM_SPLIT_WORKSPACE_BYTES)
+        return fail(FCM_EUNSUPPORTED, "plan: split workspace too large");
+    }
     // persistent: the workgroups resident at once (LDS-limited estimate; the launcher
     // also applies the compiled kernel's register-limited occupancy), at most one per
-    // work tile
+    // work unit (work tile x split)
     const int64_t per_cu = std::max<int64_t>(1, std::min<int64_t>(8, hw.lds_per_cu / lds));
-    int64_t grid = std::min<int64_t>(wgs, per_cu * hw.num_cus);
+    int64_t grid = std::min<int64_t>(wgs * splits, per_cu * hw.num_cus);
     if (p->workgroups > 0 && p->workgroups < grid) grid = p->workgroups;  // caller's cap
     p->workgroups = (int32_t)grid;
     p->depth = depth;
+    p->splits = splits;
     p->waves = 4;
     p->lds_bytes = lds;
     p->bytes_ideal = b.ideal;
@@ -279,6 +294,7 @@ fcm_status evaluate_plan(const Geom& g, const fcm_desc* d, const fcm_hw_desc& hw
   }
   p->waves = 4;
   p->depth = 0;
+  p->splits = 1;
   p->lds_bytes = lds;
   p->workgroups = (int32_t)wgs;
   p->bytes_ideal = b.ideal;
@@ -301,22 +317,24 @@ fcm_status evaluate_plan(const Geom& g, const fcm_desc* d, const fcm_hw_desc& hw
 // which is capped and limited by the bytes in flight (Little's law). Launch overhead is
 // added and the launch is never faster than its HBM traffic. The constants were fitted
 // (least squares on log time, then on the quality of the chosen plans) to timings of
-// every plan of the MobileNetV1, ViT-projection and MBConv DW->PW layers on MI355X
-// (global search over the constants for the quality of the chosen plans).
+// every plan of the MobileNetV1, ViT-projection and MBConv DW->PW layers on MI355X,
+// unsplit and split (global search over the constants for the quality of the chosen
+// plans). A split plan adds its partial sums' round trip and the second kernel.
 static double persistent_time_estimate(const Variant& v, const Geom& g, const fcm_plan_t& p,
                                        const fcm_hw_desc& hw) {
-  constexpr double kItem0 = 1274.0;       // cycles per item, fixed (busiest compute wave)
-  constexpr double kPerDot = 3.42;        // cycles per depthwise dot instruction
-  constexpr double kPerMfma = 0.575;      // cycles per MFMA instruction
-  constexpr double kPerLdsKiB = 10.7;     // cycles per KiB read from LDS by the compute waves
-  constexpr double kPerCopy = 165.9;      // cycles per 1 KiB copy instruction (one copy wave)
-  constexpr double kCopy0 = 152.0;        // cycles per item, fixed (copy wave)
-  constexpr double kShallow = 377.0;      // cycles per item lost with one item in flight
-  constexpr double kLaunch = 10720.0;     // cycles of launch, prologue and drain
-  constexpr double kHbm = 7.98e12;        // bytes/s
-  constexpr double kCuRate = 11.9;        // copy bytes per cycle and CU, at most
-  constexpr double kLatency = 1092.0;     // cycles: copy bytes in flight / rate
+  constexpr double kItem0 = 332.0;        // cycles per item, fixed (busiest compute wave)
+  constexpr double kPerDot = 11.2;        // cycles per depthwise dot instruction
+  constexpr double kPerMfma = 29.4;       // cycles per MFMA instruction
+  constexpr double kPerLdsKiB = 10.5;     // cycles per KiB read from LDS by the compute waves
+  constexpr double kPerCopy = 115.2;      // cycles per 1 KiB copy instruction (one copy wave)
+  constexpr double kCopy0 = 257.0;        // cycles per item, fixed (copy wave)
+  constexpr double kShallow = 189.0;      // cycles per item lost with one item in flight
+  constexpr double kLaunch = 16820.0;     // cycles of launch, prologue and drain
+  constexpr double kHbm = 4.26e12;        // bytes/s
+  constexpr double kCuRate = 13.2;        // copy bytes per cycle and CU, at most
+  constexpr double kLatency = 578.0;      // cycles: copy bytes in flight / rate
   constexpr double kClock = 2.4e9;
+  constexpr double kCombineLaunch = 8800.0;  // cycles: second kernel of a split plan
   const bool has_dw = v.family != FAM_PW, has_pw = v.family != FAM_DW;
   const int K = has_dw ? g.k : 1, S = has_dw ? g.s : 1;
   const int P = p.tile_h * p.tile_w;
@@ -332,9 +350,11 @@ static double persistent_time_estimate(const Variant& v, const Geom& g, const fc
     if (n > 0) lds_kib += (double)K * K * n + (has_dw ? K * K * (4 / g.elt) : 0) + ct;
   }
   const int cin = v.family == FAM_DW ? g.cm : g.ci;
-  const int nchunks = v.family == FAM_DW ? 1 : ceil_div(cin, v.ks * 64 / g.elt);  // items per work tile
+  const int splits = std::max(1, p.splits);
+  const int nchunks = v.family == FAM_DW ? 1 : items_per_split3(ceil_div(cin, v.ks * 64 / g.elt), splits);  // items per unit
   const int last = v.family == FAM_DW ? g.cm : g.co;
-  const int64_t nwork = (int64_t)g.n * ceil_div(g.ho, p.tile_h) * ceil_div(g.wo, p.tile_w) * ceil_div(last, p.co_block);
+  const int64_t ntile = (int64_t)g.n * ceil_div(g.ho, p.tile_h) * ceil_div(g.wo, p.tile_w) * ceil_div(last, p.co_block);
+  const int64_t nwork = ntile * splits;  // work units
   const int IH = has_dw ? (p.tile_h - 1) * S + K : p.tile_h;
   const int mode = v.family == FAM_DWPW ? M3_DWPW : (v.family == FAM_PW ? M3_PW : M3_DW);
   const double dots = has_dw ? (double)v.ks * nb_max * K * K * (16 / g.elt) : 0.0;
@@ -350,8 +370,14 @@ static double persistent_time_estimate(const Variant& v, const Geom& g, const fc
   const double per = std::max(std::max(comp * wpc, lds * wpc), std::max(prod, item_bytes * wpc / rate)) +
                      (depth == 2 ? kShallow : 0.0);
   const double ipw = (double)ceil_div((int)std::min<int64_t>(nwork, 1 << 30), (int)grid) * nchunks;
-  const double t_pipe = (ipw * per + kLaunch) / kClock;
-  const double t_mem = (double)p.bytes_tiled / kHbm;
+  double t_pipe = (ipw * per + kLaunch) / kClock;
+  double t_mem = (double)p.bytes_tiled / kHbm;
+  if (splits > 1) {
+    // partial sums out and back in, and the second kernel
+    const double ws = (double)split_workspace_bytes(ntile, P, p.co_block, splits);
+    t_pipe += kCombineLaunch / kClock + ws / kHbm;
+    t_mem += 2.0 * ws / kHbm;
+  }
   // (the pipeline term breaks ties between traffic-bound tilings)
   return std::max(t_pipe, t_mem) + 1e-3 * t_pipe;
 }
@@ -426,6 +452,10 @@ static fcm_status search(const Geom& g, const fcm_desc* d, const fcm_hw_desc& hw
             const int CB = (v.family == FAM_DW && v.gen != 2) ? COB : cb0;
             // persistent kernels: one or two items in flight (deeper rings measured no faster)
             const int depths[2] = {2, 3};
+            // persistent kernels with a PW stage: also split each work tile's channel chunks
+            const int splitss[4] = {1, 2, 4, 8};
+            const int nsplits = (v.gen == 3 && v.family != FAM_DW) ? 4 : 1;
+            for (int si = 0; si < nsplits; ++si)
             for (int di = 0; di < (v.gen == 3 ? 2 : 1); ++di) {
               int depth = v.gen == 3 ? depths[di] : 0;
               const int lds = tiling_lds(v, g, TH, TW, CB, COB, hw.lds_per_wg, &depth);
@@ -439,6 +469,7 @@ static fcm_status search(const Geom& g, const fcm_desc* d, const fcm_hw_desc& hw
               c.p.co_block = COB;
               c.p.variant = vi;
               c.p.depth = depth;
+              c.p.splits = splitss[si];
               if (evaluate_plan(g, d, hw, &c.p) != FCM_OK) continue;
               c.bytes = c.p.bytes_tiled;
               c.wgs = c.p.workgroups;

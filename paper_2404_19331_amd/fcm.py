@@ -56,7 +56,7 @@ class Plan(ctypes.Structure):
                 ("c_block", ctypes.c_int32), ("co_block", ctypes.c_int32),
                 ("variant", ctypes.c_int32), ("waves", ctypes.c_int32),
                 ("lds_bytes", ctypes.c_int32), ("workgroups", ctypes.c_int32),
-                ("fuse", ctypes.c_int32), ("depth", ctypes.c_int32),
+                ("fuse", ctypes.c_int32), ("depth", ctypes.c_int32), ("splits", ctypes.c_int32),
                 ("bytes_ideal", ctypes.c_int64), ("bytes_tiled", ctypes.c_int64),
                 ("bytes_paper", ctypes.c_int64), ("bytes_lbl_paper", ctypes.c_int64),
                 ("bytes_lbl_ideal", ctypes.c_int64), ("redundancy", ctypes.c_double)]
@@ -144,13 +144,15 @@ def plan(op, desc, hw=None):
     return p
 
 
-def plan_evaluate(op, desc, tile_h, tile_w, c_block, co_block, variant, hw=None, workgroups=0, depth=0):
+def plan_evaluate(op, desc, tile_h, tile_w, c_block, co_block, variant, hw=None, workgroups=0, depth=0, splits=0):
     """Evaluate a caller-chosen tiling. For the persistent kernels `workgroups` > 0 caps
-    the number of workgroups launched and `depth` > 0 sets the LDS ring depth."""
+    the number of workgroups launched, `depth` > 0 sets the LDS ring depth and
+    `splits` > 1 splits each work tile's channel chunks over that many workgroups."""
     p = Plan()
     p.op, p.tile_h, p.tile_w, p.c_block, p.co_block, p.variant = OP[op], tile_h, tile_w, c_block, co_block, variant
     p.workgroups = workgroups
     p.depth = depth
+    p.splits = splits
     _check(lib().fcm_plan_evaluate(ctypes.byref(desc), ctypes.byref(hw) if hw else None, ctypes.byref(p)))
     return p
 

@@ -4,7 +4,7 @@ Every compiled persistent variant that implements a case runs at several tile sh
 (full and ragged pixel blocks) and compared with the CPU oracle. A capped grid makes
 each workgroup stream many (tile, channel chunk) items, which exercises the LDS ring
 across tile boundaries, at depths from 2 (one item in flight) to 8 where the tiling
-allows it.
+allows it, and split plans (2-4 workgroups per work tile, combined by a second kernel).
 """
 import pytest
 
@@ -46,11 +46,11 @@ def _cases():
     return out
 
 
-# (workgroup cap, ring depth); 0 = the planner's choice
-LAUNCH = ((0, 0), (3, 2), (3, 0), (2, 5), (2, 8))
+# (workgroup cap, ring depth, splits); 0 = the planner's choice
+LAUNCH = ((0, 0, 1), (3, 2, 1), (3, 0, 1), (2, 5, 1), (2, 8, 1), (0, 0, 2), (3, 0, 3), (0, 2, 4))
 
 
-def _v3_plans(case, launch=((0, 0),)):
+def _v3_plans(case, launch=((0, 0, 1),)):
     desc = fcm.desc_from_case(case)
     cb = 64 // ELT[case.dtype]
     plans = []
@@ -61,9 +61,10 @@ def _v3_plans(case, launch=((0, 0),)):
         for th, tw in TILES:
             cobs = [cb] if case.op == "dw" else [16 * int(name.split(",")[4])]
             for cob in cobs:
-                for cap, depth in launch:
+                for cap, depth, splits in launch:
                     try:
-                        p = fcm.plan_evaluate(case.op, desc, th, tw, cb, cob, v, workgroups=cap, depth=depth)
+                        p = fcm.plan_evaluate(case.op, desc, th, tw, cb, cob, v, workgroups=cap, depth=depth,
+                                              splits=splits)
                     except fcm.FcmError:
                         continue
                     plans.append(p)
@@ -82,5 +83,5 @@ def test_persistent_variants_match_oracle(case):
     assert plans, "no persistent variant implements %s" % case.name
     for p in plans:
         got = to_np(run_fused(case, d, plan=p))
-        assert_close(got, ref, case.dtype, "%s %s tile %dx%d grid %d depth %d" % (
-            case.name, fcm.variant_name(p.variant), p.tile_h, p.tile_w, p.workgroups, p.depth))
+        assert_close(got, ref, case.dtype, "%s %s tile %dx%d grid %d depth %d splits %d" % (
+            case.name, fcm.variant_name(p.variant), p.tile_h, p.tile_w, p.workgroups, p.depth, p.splits))

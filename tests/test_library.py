@@ -1,0 +1,181 @@
+"""Host-side tests of the C-ABI library (no GPU needed): libfcm.so loads and exports every
+function include/fcm.h declares, the FusePlanner (Sec. IV) returns consistent plans for
+every layer of the five workloads, its byte model matches the closed forms of
+"input + weights + output" and "plus twice each intermediate" (Sec. IV, Eq. 1-4 and the
+layer-by-layer comparison of Sec. II-D), and invalid descriptors or plans are rejected
+with the documented status codes. Nothing here launches a kernel."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import bench
+from paper_2404_19331_amd import fcm
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "fcm.h")
+ELT = {"f32": 4, "bf16": 2, "i8": 1}
+EINVAL, EUNSUPPORTED = 1, 2
+
+
+def _header():
+    with open(HEADER) as f:
+        return f.read()
+
+
+def _declared_functions():
+    src = re.sub(r"/\*.*?\*/", " ", _header(), flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(fcm_\w+)\s*\(", src, flags=re.M)))
+
+
+def _workspace_limit():
+    m = re.search(r"#define\s+FCM_SPLIT_WORKSPACE_BYTES\s+\((\d+)u\s*<<\s*(\d+)\)", _header())
+    return int(m.group(1)) << int(m.group(2))
+
+
+def _all_cases():
+    out = []
+    for wl in ("C1", "C2", "C3b1", "C3b32", "C4", "C5"):
+        cases, _ = bench.workload_cases(wl)
+        out += [(wl, c) for c in cases]
+    return out
+
+
+CASES = _all_cases()
+
+
+def test_library_exports_every_declared_function():
+    names = _declared_functions()
+    assert len(names) >= 12, names
+    L = fcm.lib()
+    for n in names:
+        assert hasattr(L, n), "libfcm.so does not export %s" % n
+
+
+def test_status_strings_version_and_variant_table():
+    L = fcm.lib()
+    for st in range(4):
+        assert L.fcm_status_string(st)
+    assert fcm.lib().fcm_version().decode().startswith("fcm ")
+    n = L.fcm_variant_count()
+    names = [fcm.variant_name(v) for v in range(n)]
+    assert n > 50 and all(names)
+    persistent = [x for x in names if re.match(r"k_\w+3<", x)]  # these names carry the element type
+    assert persistent and len(set(persistent)) == len(persistent)
+    assert fcm.variant_name(n) is None and fcm.variant_name(-1) is None
+
+
+def test_missing_library_fails_loudly(monkeypatch):
+    monkeypatch.setattr(fcm, "_lib", None)
+    monkeypatch.setattr(fcm, "LIB_PATH", os.path.join(ROOT, "no_such_dir", "libfcm.so"))
+    with pytest.raises(fcm.FcmError):
+        fcm.lib()
+
+
+@pytest.mark.parametrize("wl,case", CASES, ids=lambda v: v if isinstance(v, str) else v.name)
+def test_plan_every_layer(wl, case):
+    d = fcm.desc_from_case(case)
+    p = fcm.plan(case.op, d)
+    ho, wo = fcm.out_hw(case.h, case.w, case.k, case.stride, case.pad)
+    name = fcm.variant_name(p.variant)
+    fam = {"dw_pw": "k_dwpw", "pw_dw": "k_pwdw", "pw_dw_pw": "k_pwdwpw", "dw": "k_dw", "pw": "k_pw"}[case.op]
+    assert name.startswith(fam), name
+    assert 1 <= p.tile_h and 1 <= p.tile_w and p.co_block >= 1 and p.c_block >= 1
+    assert 0 < p.lds_bytes <= 160 * 1024
+    assert p.workgroups >= 1 and p.waves == 4
+    assert p.bytes_tiled >= p.bytes_ideal > 0
+    if name.endswith(">") and re.match(r"k_\w+3<", name):  # persistent kernels
+        assert p.depth in (2, 3)
+        assert p.splits in (1, 2, 4, 8)
+        if p.splits > 1:
+            tiles = case.n * -(-ho // p.tile_h) * -(-wo // p.tile_w) * -(-case.c_out // p.co_block)
+            assert p.splits * tiles * p.tile_h * p.tile_w * p.co_block * 4 <= _workspace_limit()
+    # same answer every time (the plan cache and the search are deterministic)
+    q = fcm.plan(case.op, d)
+    assert p.as_dict() == q.as_dict()
+
+
+@pytest.mark.parametrize("wl,case", [(w, c) for w, c in CASES if c.op == "dw_pw"],
+                         ids=lambda v: v if isinstance(v, str) else v.name)
+def test_dw_pw_byte_model_closed_forms(wl, case):
+    p = fcm.plan(case.op, fcm.desc_from_case(case))
+    ho, wo = fcm.out_hw(case.h, case.w, case.k, case.stride, case.pad)
+    e = ELT[case.dtype]
+    x = case.n * case.h * case.w * case.c_in
+    mid = case.n * ho * wo * case.c_in
+    y = case.n * ho * wo * case.c_out
+    w = case.c_in * case.k * case.k + case.c_out * case.c_in
+    assert p.bytes_ideal == (x + w + y) * e
+    assert p.bytes_lbl_ideal == (x + w + y + 2 * mid) * e
+
+
+def test_fusion_saves_half_the_traffic_when_widths_match():
+    # Fig. 1's sanity check: with C_in = C_out and stride 1 the layer-by-layer chain
+    # moves x, mid (twice) and y, all of one size, the fused module only x and y.
+    d = fcm.make_desc(8, 112, 112, 64, 64, 64, k=3, stride=1, pad=1, dtype="bf16", layout="nhwc")
+    p = fcm.plan("dw_pw", d)
+    saved = 1 - p.bytes_ideal / p.bytes_lbl_ideal
+    assert abs(saved - 0.5) < 0.005
+
+
+def _evaluate(op, d, th, tw, variant_prefix, **kw):
+    for v in range(fcm.lib().fcm_variant_count()):
+        if fcm.variant_name(v).startswith(variant_prefix):
+            ct = int(fcm.variant_name(v).split(",")[4])
+            return fcm.plan_evaluate(op, d, th, tw, 64 // ELT["bf16"], 16 * ct, v, **kw)
+    raise AssertionError(variant_prefix)
+
+
+def test_plan_evaluate_checks_depth_and_splits():
+    d = fcm.make_desc(1, 14, 14, 512, 512, 512, k=3, stride=1, pad=1, dtype="bf16", layout="nhwc")
+    p = _evaluate("dw_pw", d, 2, 7, "k_dwpw3<bf16,3,1,4,4,p16>", depth=3, splits=4)
+    assert (p.depth, p.splits) == (3, 4)
+    assert _evaluate("dw_pw", d, 2, 7, "k_dwpw3<bf16,3,1,4,4,p16>").splits == 1  # 0 = no split
+    for kw in (dict(depth=9), dict(depth=1), dict(splits=32)):  # 16 channel chunks: 32 splits leave some empty
+        with pytest.raises(fcm.FcmError) as e:
+            _evaluate("dw_pw", d, 2, 7, "k_dwpw3<bf16,3,1,4,4,p16>", **kw)
+        assert e.value.status == EUNSUPPORTED
+    dd = fcm.make_desc(1, 14, 14, 512, 512, 512, k=3, stride=1, pad=1, dtype="bf16", layout="nhwc")
+    with pytest.raises(fcm.FcmError):  # a depthwise-only kernel has no contraction to split
+        _evaluate("dw", dd, 2, 7, "k_dw3<bf16,3,1", splits=2)
+
+
+def test_plan_evaluate_rejects_what_no_kernel_implements():
+    d = fcm.make_desc(1, 56, 56, 64, 64, 64, k=3, stride=1, pad=1, dtype="bf16", layout="nhwc")
+    with pytest.raises(fcm.FcmError):  # window wider than the kernel's LDS row pitch
+        _evaluate("dw_pw", d, 2, 28, "k_dwpw3<bf16,3,1,4,4,p16>")
+    with pytest.raises(fcm.FcmError):  # unknown variant
+        fcm.plan_evaluate("dw_pw", d, 4, 4, 32, 64, 10 ** 6)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(n=0), EINVAL), (dict(h=0), EINVAL), (dict(c_in=0), EINVAL), (dict(c_out=0), EINVAL),
+    (dict(c_mid=16), EINVAL), (dict(pad=3), EINVAL), (dict(stride=0), EINVAL), (dict(h=1, w=1, pad=0), EINVAL),
+    (dict(k=4), EUNSUPPORTED), (dict(k=7), EUNSUPPORTED), (dict(stride=3), EUNSUPPORTED),
+    (dict(dtype="i8", rq=[(1, 70, -128, 127)]), EINVAL), (dict(dtype="i8", rq=[(1, 8, 5, -5)]), EINVAL)])
+def test_descriptor_validation(kw, status):
+    a = dict(n=1, h=16, w=16, c_in=32, c_mid=32, c_out=32, k=3, stride=1, pad=1, dtype="f32", layout="nchw")
+    a.update(kw)
+    d = fcm.make_desc(**a)
+    with pytest.raises(fcm.FcmError) as e:
+        fcm.plan("dw_pw", d)
+    assert e.value.status == status
+
+
+def test_int8_relu6_is_unsupported():
+    d = fcm.make_desc(1, 16, 16, 32, 32, 32, k=3, stride=1, pad=1, dtype="i8", layout="nhwc",
+                      act=("relu6", "none", "none"))
+    with pytest.raises(fcm.FcmError) as e:
+        fcm.plan("dw_pw", d)
+    assert e.value.status == EUNSUPPORTED
+
+
+def test_header_is_plain_c():
+    src = _header()
+    assert "extern \"C\"" in src and "#include <stdint.h>" in src
+    assert "hip" not in re.sub(r"/\*.*?\*/", " ", src, flags=re.S).lower()
+    L = fcm.lib()
+    # the plan struct the Python binding marshals has the size the library fills in
+    assert ctypes.sizeof(fcm.Plan) % 8 == 0
+    assert L.fcm_variant_count() > 0

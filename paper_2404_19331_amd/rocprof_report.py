@@ -26,17 +26,18 @@ _MODE = {"k_dwpw3": 0, "k_pw3": 1, "k_dw3": 2}
 _DT = {"f32": "TF32", "bf16": "TBF16", "i8": "TI8"}
 
 
-def kernel_symbol(variant):
+def kernel_symbol(variant, split=False):
     """Demangled kernel name of a persistent variant, e.g. k_dwpw3<bf16,3,1,1,16,p16> ->
-    void fcm::k_fused3<fcm::TBF16, 3, 1, 1, 16, 0, 16, 1>(fcm::KArgs)."""
+    void fcm::k_fused3<fcm::TBF16, 3, 1, 1, 16, 0, 16, 1, false>(fcm::KArgs) (the instance
+    of unsplit plans; split=True names the one of split plans)."""
     m = re.match(r"(k_\w+3)<(\w+),(\d+),(\d+),(\d+),(\d+),p(\d+)(?:,k(\d+))?>$", variant)
     if not m:
         raise ValueError("not a persistent-kernel variant name: %s" % variant)
     fam, dt, k, s, bpw, ct, pitch, ks = m.groups()
     if fam == "k_pw3":
         k = s = "1"
-    return "void fcm::k_fused3<fcm::%s, %s, %s, %s, %s, %d, %s, %s>(fcm::KArgs)" % (
-        _DT[dt], k, s, bpw, ct, _MODE[fam], pitch, ks or "1")
+    return "void fcm::k_fused3<fcm::%s, %s, %s, %s, %s, %d, %s, %s, %s>(fcm::KArgs)" % (
+        _DT[dt], k, s, bpw, ct, _MODE[fam], pitch, ks or "1", "true" if split else "false")
 
 
 def read_counters(path):
@@ -70,7 +71,7 @@ def _mean(vals, name, counter):
 
 
 def traffic(args):
-    sym = kernel_symbol(args.variant)
+    sym = kernel_symbol(args.variant, args.split)
     fv, fg = read_counters(args.fetch)
     wv, wg = read_counters(args.write)
     f_k, w_k = _mean(fv, sym, "FETCH_SIZE"), _mean(wv, sym, "WRITE_SIZE")
@@ -126,6 +127,7 @@ def main():
     t.add_argument("--variant", required=True)
     t.add_argument("--fetch", required=True)
     t.add_argument("--write", required=True)
+    t.add_argument("--split", action="store_true", help="the split-plan instance of the variant")
     t.add_argument("--calib-bytes", type=int, default=256 << 20)
     t.add_argument("--out", default=os.path.join(ROOT, "profiles", "traffic.json"))
     a = ap.parse_args()

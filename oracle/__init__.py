@@ -76,7 +76,8 @@ def _lib():
         lib.orc_dw_pw.argtypes = [dp, vp, vp, vp, vp, vp, vp]
         lib.orc_pw_dw.argtypes = [dp, vp, vp, vp, vp, vp, vp]
         lib.orc_pw_dw_pw.argtypes = [dp, vp, vp, vp, vp, vp, vp, vp, vp]
-        for f in (lib.orc_dw, lib.orc_pw, lib.orc_dw_pw, lib.orc_pw_dw, lib.orc_pw_dw_pw):
+        lib.orc_pw_pw.argtypes = [dp, vp, vp, vp, vp, vp, vp]
+        for f in (lib.orc_dw, lib.orc_pw, lib.orc_dw_pw, lib.orc_pw_dw, lib.orc_pw_dw_pw, lib.orc_pw_pw):
             f.restype = ctypes.c_int
         lib.orc_requant.argtypes = [ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
                                     ctypes.c_int32, ctypes.c_int32]
@@ -214,6 +215,18 @@ def pw_dw_pw(case, x, w_pw1, b_pw1, w_dw, b_dw, w_pw2, b_pw2):
     return y
 
 
+def pw_pw(case, x, w_pw1, b_pw1, w_pw2, b_pw2):
+    """Two pointwise layers c_in -> c_mid -> c_out (spatial size unchanged)."""
+    dt, lay = _get(case, "dtype"), _get(case, "layout")
+    d = _desc(case)
+    x, w_pw1, w_pw2 = (_arr(a, dt) for a in (x, w_pw1, w_pw2))
+    b_pw1, b_pw2 = (_bias(b, dt) for b in (b_pw1, b_pw2))
+    y = np.empty(_shape(lay, d.n, d.c_out, d.h, d.w), dtype=_NP[dt])
+    _check(_lib().orc_pw_pw(ctypes.byref(d), _ptr(x), _ptr(w_pw1), _ptr(b_pw1), _ptr(w_pw2), _ptr(b_pw2),
+                            _ptr(y)))
+    return y
+
+
 def run(op, case, inputs):
     """Dispatch by module name with the inputs dict produced by the seeded generators."""
     g = inputs.get
@@ -224,6 +237,8 @@ def run(op, case, inputs):
     if op == "pw_dw_pw":
         return pw_dw_pw(case, g("x"), g("w_pw1"), g("b_pw1"), g("w_dw"), g("b_dw"),
                         g("w_pw2"), g("b_pw2"))
+    if op == "pw_pw":
+        return pw_pw(case, g("x"), g("w_pw1"), g("b_pw1"), g("w_pw2"), g("b_pw2"))
     if op == "dw":
         return dw(case, g("x"), g("w_dw"), g("b_dw"))
     if op == "pw":

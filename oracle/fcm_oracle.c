@@ -463,6 +463,45 @@ int orc_pw_dw(const orc_desc* d, const void* x, const void* wp, const void* bp, 
   return ORC_OK;
 }
 
+/* PW -> PW: two pointwise convolutions, c_in -> c_mid -> c_out, spatial size unchanged
+ * (the paper's PwPw module; k, stride and pad are ignored). */
+int orc_pw_pw(const orc_desc* d, const void* x, const void* wp1, const void* bp1, const void* wp2,
+              const void* bp2, void* y) {
+  int st = check_common(d);
+  if (st) return st;
+  if (d->c_in <= 0 || d->c_mid <= 0 || d->c_out <= 0 || !x || !wp1 || !wp2 || !y) return ORC_EINVAL;
+  int N = d->n, Ci = d->c_in, Cm = d->c_mid, Co = d->c_out, H = d->h, W = d->w;
+  size_t nm = (size_t)N * Cm * H * W, no = (size_t)N * Co * H * W;
+  if (d->dtype == ORC_I8) {
+    int64_t* xi = load_fmap_i((const int8_t*)x, d->layout, N, Ci, H, W);
+    int64_t* w1 = load_vec_i((const int8_t*)wp1, (size_t)Cm * Ci);
+    int64_t* w2 = load_vec_i((const int8_t*)wp2, (size_t)Co * Cm);
+    int64_t* mi = (int64_t*)malloc(nm * sizeof(int64_t));
+    int64_t* yi = (int64_t*)malloc(no * sizeof(int64_t));
+    pw_stage_i(xi, N, Ci, H, W, w1, (const int32_t*)bp1, Cm, mi);
+    st = finish_i(mi, nm, d->act[0], d->rq[0]);
+    if (!st) {
+      pw_stage_i(mi, N, Cm, H, W, w2, (const int32_t*)bp2, Co, yi);
+      st = finish_i(yi, no, d->act[1], d->rq[1]);
+    }
+    if (!st) store_fmap_i(yi, d->layout, N, Co, H, W, (int8_t*)y);
+    free(xi); free(w1); free(w2); free(mi); free(yi);
+    return st;
+  }
+  double* xf = load_fmap_f(x, d->dtype, d->layout, N, Ci, H, W);
+  double* w1 = load_vec_f(wp1, d->dtype, (size_t)Cm * Ci);
+  double* w2 = load_vec_f(wp2, d->dtype, (size_t)Co * Cm);
+  double* mf = (double*)malloc(nm * sizeof(double));
+  double* yf = (double*)malloc(no * sizeof(double));
+  pw_stage_f(xf, N, Ci, H, W, w1, bp1, d->dtype, Cm, mf);
+  finish_f(mf, nm, d->act[0], d->dtype);
+  pw_stage_f(mf, N, Cm, H, W, w2, bp2, d->dtype, Co, yf);
+  finish_f(yf, no, d->act[1], d->dtype);
+  store_fmap_f(yf, d->dtype, d->layout, N, Co, H, W, y);
+  free(xf); free(w1); free(w2); free(mf); free(yf);
+  return ORC_OK;
+}
+
 /* PW -> DW -> PW (inverted residual without the skip connection). */
 int orc_pw_dw_pw(const orc_desc* d, const void* x, const void* wp1, const void* bp1, const void* wd,
                  const void* bd, const void* wp2, const void* bp2, void* y) {

@@ -34,7 +34,7 @@ RQ_C4 = (1, 8, -127, 127)  # per-tensor scale 2^-8, symmetric int8 range
 @dataclass(frozen=True)
 class Case:
     """One module invocation: module name, geometry, precision, layout, epilogues."""
-    op: str                      # dw_pw | pw_dw | pw_dw_pw | dw | pw
+    op: str                      # dw_pw | pw_dw | pw_dw_pw | pw_pw | dw | pw
     n: int
     h: int
     w: int
@@ -142,6 +142,11 @@ def make_inputs(case, seed=None):
         out["b_pw1"] = _draw_b(rng, case, case.c_mid)
         out["b_dw"] = _draw_b(rng, case, case.c_mid)
         out["b_pw2"] = _draw_b(rng, case, case.c_out)
+    elif case.op == "pw_pw":
+        out["w_pw1"] = _draw_w(rng, case, (case.c_mid, case.c_in), case.c_in)
+        out["w_pw2"] = _draw_w(rng, case, (case.c_out, case.c_mid), case.c_mid)
+        out["b_pw1"] = _draw_b(rng, case, case.c_mid)
+        out["b_pw2"] = _draw_b(rng, case, case.c_out)
     elif case.op == "dw":
         out["w_dw"] = _draw_w(rng, case, (case.c_in, k, k), k * k)
         out["b_dw"] = _draw_b(rng, case, case.c_in)
@@ -213,6 +218,21 @@ def config_c5():
                  dist_x="n01", seed=BASE_SEED + 5 + 100 * i,
                  name="C5 %dx%dx%d->%d bf16 b64" % (hw, hw, c, co))
             for i, (hw, c, co) in enumerate(VIT_GRIDS, start=1)]
+
+
+# MobileNetV2 expansion / projection widths (spatial size, c_in, expanded, c_out) used
+# as two fused pointwise layers without the depthwise layer between them.
+PWPW_SHAPES = [(56, 24, 144, 24), (28, 32, 192, 32), (14, 64, 384, 64), (14, 96, 576, 96), (7, 160, 960, 160)]
+
+
+def config_pwpw():
+    """PW -> PW pairs (the paper's PwPw module, frequent in its int8 plans), int8 NHWC,
+    batch 8, requant 2^-8 RNE, ReLU after the first layer."""
+    rq = (RQ_C4, RQ_C4, RQ_C4)
+    return [Case("pw_pw", 8, hw, hw, ci, cm, co, 1, 1, 0, "i8", "nhwc", ("relu", "none", "none"), rq,
+                 dist_x="i8", dist_w="i8", seed=BASE_SEED + 6 + 100 * i,
+                 name="PWPW %dx%dx%d->%d->%d i8 b8" % (hw, hw, ci, cm, co))
+            for i, (hw, ci, cm, co) in enumerate(PWPW_SHAPES, start=1)]
 
 
 CONFIGS = {"C1": config_c1, "C2": config_c2, "C3": config_c3, "C4": config_c4, "C5": config_c5}

@@ -166,6 +166,52 @@ def test_pw_dw_equals_dense_conv_without_activation():
 
 
 @pytest.mark.parametrize("layout", ["nchw", "nhwc"])
+def test_pw_pw_without_activation_is_one_pw_with_composed_weights(layout):
+    """Two linear 1x1 convolutions compose into one: W = W2 W1, b = W2 b1 + b2 (float64
+    exact mode, torch's conv2d as the reference)."""
+    rng = np.random.default_rng(16)
+    n, ci, cm, co, h, w = 2, 5, 9, 4, 6, 7
+    x = _rand(rng, (n, ci, h, w))
+    w1, w2 = _rand(rng, (cm, ci)), _rand(rng, (co, cm))
+    b1, b2 = _rand(rng, cm), _rand(rng, co)
+    case = dict(n=n, h=h, w=w, c_in=ci, c_mid=cm, c_out=co, k=1, stride=1, pad=0, dtype="f64", layout=layout,
+                act=["none"] * 3)
+    y = _nchw(oracle.pw_pw(case, _to_layout(x, layout), w1, b1, w2, b2), layout)
+    ref = F.conv2d(torch.from_numpy(x), torch.from_numpy((w2 @ w1)[:, :, None, None]),
+                   torch.from_numpy(w2 @ b1 + b2)).numpy()
+    np.testing.assert_allclose(y, ref, rtol=1e-11, atol=1e-11)
+
+
+@pytest.mark.parametrize("act", [("relu", "none"), ("none", "relu")])
+def test_pw_pw_int8_matches_integer_reference(act):
+    """int8 PW -> PW against numpy int64 matmuls and a round-half-even requantisation
+    (np.round on exactly representable quotients), saturated per stage."""
+    rng = np.random.default_rng(17)
+    n, ci, cm, co, h, w = 2, 40, 72, 24, 5, 6
+    rq = ((3, 9, -127, 127), (5, 10, -128, 127), (1, 0, -128, 127))
+    # small magnitudes keep most results inside the int8 range (saturation is exercised too)
+    x = rng.integers(-8, 9, (n, h, w, ci)).astype(np.int8)
+    w1 = rng.integers(-8, 9, (cm, ci)).astype(np.int8)
+    w2 = rng.integers(-8, 9, (co, cm)).astype(np.int8)
+    b1 = rng.integers(-500, 500, cm).astype(np.int32)
+    b2 = rng.integers(-500, 500, co).astype(np.int32)
+    case = dict(n=n, h=h, w=w, c_in=ci, c_mid=cm, c_out=co, k=1, stride=1, pad=0, dtype="i8", layout="nhwc",
+                act=list(act) + ["none"], rq=list(rq))
+
+    def stage(t, wt, b, r, a):
+        acc = t.astype(np.int64) @ wt.astype(np.int64).T + b.astype(np.int64)
+        q = np.round(acc.astype(np.float64) * r[0] / 2.0 ** r[1])
+        lo, hi = (max(r[2], 0), max(r[3], 0)) if a == "relu" else (r[2], r[3])
+        return np.clip(q, lo, hi).astype(np.int8)
+
+    mid = stage(x, w1, b1, rq[0], act[0])
+    ref = stage(mid, w2, b2, rq[1], act[1])
+    assert 0.5 < np.mean(np.abs(ref.astype(int)) < 127) and np.mean(mid != 0) > 0.5  # not saturated, not zero
+    y = oracle.pw_pw(case, x, w1, b1, w2, b2)
+    assert np.array_equal(y, ref)
+
+
+@pytest.mark.parametrize("layout", ["nchw", "nhwc"])
 def test_pw_dw_pw_matches_torch(layout):
     rng = np.random.default_rng(15)
     n, ci, cm, co, h, w, k, s, p = 2, 3, 8, 5, 9, 7, 3, 1, 1
@@ -450,7 +496,7 @@ def test_bf16_rounding_matches_torch():
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16", "i8"])
-@pytest.mark.parametrize("op", ["dw_pw", "pw_dw", "pw_dw_pw"])
+@pytest.mark.parametrize("op", ["dw_pw", "pw_dw", "pw_dw_pw", "pw_pw"])
 def test_module_equals_chain_of_single_layers(dtype, op):
     """A module computes exactly its layer-by-layer chain: each stage's output is cast to
     the storage precision before the next stage reads it (fusion moves data only). Each
@@ -458,7 +504,7 @@ def test_module_equals_chain_of_single_layers(dtype, op):
     intermediate casts."""
     rq = ((1, 6, -127, 127), (3, 9, -127, 127), (1, 7, -127, 127))
     cm = 6 if op == "dw_pw" else 9
-    co = {"dw_pw": 5, "pw_dw": 9, "pw_dw_pw": 4}[op]
+    co = {"dw_pw": 5, "pw_dw": 9, "pw_dw_pw": 4, "pw_pw": 7}[op]
     case = Case(op, 2, 9, 8, 6, cm, co, 3, 2, 1, dtype, "nhwc", ("relu", "relu6" if dtype != "i8" else "none", "relu"),
                 rq, dist_x="i8small" if dtype == "i8" else "n01", dist_w="i8small", bias=True, seed=61)
     inp = make_inputs(case)
@@ -480,6 +526,9 @@ def test_module_equals_chain_of_single_layers(dtype, op):
     elif op == "pw_dw":
         m = stage_pw(inp["x"], 9, 8, 6, cm, inp["w_pw"], inp["b_pw"], 0)
         ref = stage_dw(m, 9, 8, cm, inp["w_dw"], inp["b_dw"], 1)
+    elif op == "pw_pw":  # spatial size unchanged: k, stride and pad do not apply
+        m = stage_pw(inp["x"], 9, 8, 6, cm, inp["w_pw1"], inp["b_pw1"], 0)
+        ref = stage_pw(m, 9, 8, cm, co, inp["w_pw2"], inp["b_pw2"], 1)
     else:
         m = stage_pw(inp["x"], 9, 8, 6, cm, inp["w_pw1"], inp["b_pw1"], 0)
         m = stage_dw(m, 9, 8, cm, inp["w_dw"], inp["b_dw"], 1)

@@ -188,7 +188,7 @@ def test_pw_pw_int8_matches_integer_reference(act):
     (np.round on exactly representable quotients), saturated per stage."""
     rng = np.random.default_rng(17)
     n, ci, cm, co, h, w = 2, 40, 72, 24, 5, 6
-    rq = ((3, 9, -127, 127), (5, 10, -128, 127), (1, 0, -128, 127))
+    rq = ((3, 4, -127, 127), (5, 7, -128, 127), (1, 0, -128, 127))
     # small magnitudes keep most results inside the int8 range (saturation is exercised too)
     x = rng.integers(-8, 9, (n, h, w, ci)).astype(np.int8)
     w1 = rng.integers(-8, 9, (cm, ci)).astype(np.int8)
@@ -206,7 +206,8 @@ def test_pw_pw_int8_matches_integer_reference(act):
 
     mid = stage(x, w1, b1, rq[0], act[0])
     ref = stage(mid, w2, b2, rq[1], act[1])
-    assert 0.5 < np.mean(np.abs(ref.astype(int)) < 127) and np.mean(mid != 0) > 0.5  # not saturated, not zero
+    # spread results: mostly inside the int8 range, some saturated, few zeros beyond ReLU's
+    assert 0.5 < np.mean(np.abs(ref.astype(int)) < 127) < 1 and np.mean(mid != 0) > 0.4 and np.mean(ref != 0) > 0.4
     y = oracle.pw_pw(case, x, w1, b1, w2, b2)
     assert np.array_equal(y, ref)
 

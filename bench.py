@@ -35,7 +35,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="C3b32",
-                    choices=["C1", "C2", "C3b1", "C3b32", "C4", "C5"])
+                    choices=["C1", "C2", "C3b1", "C3b32", "C4", "C5", "PWPW"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target CPU-baseline sample time")
     ap.add_argument("--layers", default=None, help="comma-separated layer indices (subset)")
@@ -56,6 +56,8 @@ def workload_cases(name):
         return W.config_c3(batches=(32,)), "MobileNetV1 13 DW3x3+PW layers (224x224 input), bf16 NHWC, ReLU, batch 32"
     if name == "C4":
         return W.config_c4(), "EfficientNet-B0-style int8 DW5x5+PW (112x112x96 s2 ->24; 14x14x480 ->112), NHWC, batch 8"
+    if name == "PWPW":
+        return W.config_pwpw(), "MobileNetV2-width PW->PW pairs (expand ReLU, project), int8 NHWC, batch 8"
     return W.config_c5(), "CvT/CMT-style token grids DW3x3+PW (56x56x64->192, 28x28x192->384, 14x14x384->768), bf16 NHWC, batch 64"
 
 
@@ -84,6 +86,11 @@ def layer_stats(c):
         y = c.n * ho * wo * c.c_out
         mids = [c.n * c.h * c.w * c.c_mid, c.n * ho * wo * c.c_mid]
         flops = 2 * (c.n * c.h * c.w * c.c_mid * c.c_in + c.n * ho * wo * c.c_mid * (kk + c.c_out))
+    elif c.op == "pw_pw":
+        w = c.c_mid * c.c_in + c.c_out * c.c_mid
+        y = c.n * c.h * c.w * c.c_out
+        mids = [c.n * c.h * c.w * c.c_mid]
+        flops = 2 * c.n * c.h * c.w * c.c_mid * (c.c_in + c.c_out)
     else:  # pw_dw
         w = c.c_mid * c.c_in + c.c_mid * kk
         y = c.n * ho * wo * c.c_mid
@@ -123,7 +130,7 @@ class Layer:
             mid_shapes = [shaped(c.c_in, ho, wo)]
         elif c.op == "pw_dw_pw":
             mid_shapes = [shaped(c.c_mid, c.h, c.w), shaped(c.c_mid, ho, wo)]
-        else:
+        else:  # pw_dw, pw_pw
             mid_shapes = [shaped(c.c_mid, c.h, c.w)]
         self.desc = fcm.desc_from_case(c)
         self.plan = fcm.plan(c.op, self.desc)
@@ -144,6 +151,12 @@ class Layer:
                                  d.get("b_pw2"), act=c.act, rq=rq, plan=self.plan, **kw)
                 u = fcm.pw_then_dw_then_pw(x, d["w_pw1"], d["w_dw"], d["w_pw2"], d.get("b_pw1"), d.get("b_dw"),
                                            d.get("b_pw2"), act=c.act, rq=rq, mids=(mids[0], mids[1]), **kw)
+            elif c.op == "pw_pw":
+                kp = dict(layout=c.layout, out=y, prepare=True)
+                f = fcm.pw_pw(x, d["w_pw1"], d["w_pw2"], d.get("b_pw1"), d.get("b_pw2"), act=c.act[:2], rq=rq,
+                              plan=self.plan, **kp)
+                u = fcm.pw_then_pw(x, d["w_pw1"], d["w_pw2"], d.get("b_pw1"), d.get("b_pw2"), act=c.act[:2], rq=rq,
+                                   mid=mids[0], **kp)
             else:
                 f = fcm.pw_dw(x, d["w_pw"], d["w_dw"], d.get("b_pw"), d.get("b_dw"), act=c.act[:2], rq=rq,
                               plan=self.plan, **kw)

@@ -13,6 +13,8 @@
  *                 once when a tile spans the whole plane.
  *   fcm_pw_dw_pw  PW -> DW -> PW in one kernel (the inverted-residual block of Sec. II-B,
  *                 three layers fused; the paper's modules fuse two).
+ *   fcm_pw_pw     PW -> PW in one kernel (Sec. III-A "PwPw", two pointwise layers; the
+ *                 first layer's output tile stays on chip, chunk by chunk).
  *   fcm_dw, fcm_pw  single layers ("layer-by-layer", LBL, Sec. II-D and V-C): the
  *                 unfused comparison, built from the same tiles and dataflow.
  *   fcm_plan      FusePlanner (Sec. IV): global-memory-access estimates of the LBL and
@@ -77,7 +79,8 @@ typedef enum {
   FCM_OP_PW_DW = 1,
   FCM_OP_PW_DW_PW = 2,
   FCM_OP_DW = 3,
-  FCM_OP_PW = 4
+  FCM_OP_PW = 4,
+  FCM_OP_PW_PW = 5
 } fcm_op;
 
 /* int8 requantisation of a stage: q = clamp(rne(acc * mult / 2^shift), qmin, qmax),
@@ -188,6 +191,13 @@ fcm_status fcm_pw_dw_pw(const fcm_desc* desc, const void* x, const void* w_pw1,
                         const void* b_pw1, const void* w_dw, const void* b_dw,
                         const void* w_pw2, const void* b_pw2, void* y, const fcm_plan_t* plan,
                         void* stream);
+
+/* PW -> PW (the paper's PwPw module, Sec. III-A): y = cast(act1(P2 * cast(act0(P1 * x + b1))
+ * + b2)), P1 [c_mid][c_in], P2 [c_out][c_mid]; the spatial size is unchanged (k, stride and
+ * pad are ignored). desc->act[0]/rq[0] belong to the first layer, act[1]/rq[1] to the
+ * second. Same conventions and errors as fcm_dw_pw. */
+fcm_status fcm_pw_pw(const fcm_desc* desc, const void* x, const void* w_pw1, const void* b_pw1,
+                     const void* w_pw2, const void* b_pw2, void* y, const fcm_plan_t* plan, void* stream);
 
 /* Single depthwise layer (layer-by-layer baseline): y [n, c_in, h_o, w_o]. */
 fcm_status fcm_dw(const fcm_desc* desc, const void* x, const void* w_dw, const void* b_dw,

@@ -38,10 +38,10 @@ const Variant* all_variants(int* count) {
   return all.data();
 }
 
-static bool uses_dw(int op) { return op != FCM_OP_PW; }
+static bool uses_dw(int op) { return op != FCM_OP_PW && op != FCM_OP_PW_PW; }
 
 fcm_status validate(int op, const fcm_desc* d) {
-  if (op < FCM_OP_DW_PW || op > FCM_OP_PW) return fail(FCM_EINVAL, "unknown module");
+  if (op < FCM_OP_DW_PW || op > FCM_OP_PW_PW) return fail(FCM_EINVAL, "unknown module");
   if (!d) return fail(FCM_EINVAL, "descriptor is NULL");
   if (d->n <= 0 || d->h <= 0 || d->w <= 0 || d->c_in <= 0)
     return fail(FCM_EINVAL, "n, h, w and c_in must be positive");
@@ -68,6 +68,7 @@ fcm_status validate(int op, const fcm_desc* d) {
       if (d->c_out != d->c_mid) return fail(FCM_EINVAL, "pw_dw: c_out must equal c_mid");
       break;
     case FCM_OP_PW_DW_PW:
+    case FCM_OP_PW_PW:
       if (d->c_mid <= 0 || d->c_out <= 0) return fail(FCM_EINVAL, "c_mid and c_out must be positive");
       break;
     case FCM_OP_PW:
@@ -226,6 +227,10 @@ static fcm_status run(int op, const fcm_desc* d, const Tensors& t, const fcm_pla
       a.vec_w1 = aligned16(t.w[0]) && (g.ci * e) % 16 == 0;
       a.vec_w3 = aligned16(t.w[2]) && (g.cm * e) % 16 == 0;
       break;
+    case FAM_PWPW:  // second PW weights in w2, its vector flag in vec_w3
+      a.vec_w1 = aligned16(t.w[0]) && (g.ci * e) % 16 == 0;
+      a.vec_w3 = aligned16(t.w[1]) && (g.cm * e) % 16 == 0;
+      break;
     default: break;
   }
   a.nwork = a.N * a.tiles_y * a.tiles_x * a.n_cb;
@@ -320,6 +325,12 @@ fcm_status fcm_dw(const fcm_desc* desc, const void* x, const void* w_dw, const v
                   const fcm_plan_t* plan, void* stream) {
   Tensors t = {x, {w_dw, nullptr, nullptr}, {b_dw, nullptr, nullptr}, y};
   return run(FCM_OP_DW, desc, t, plan, stream);
+}
+
+fcm_status fcm_pw_pw(const fcm_desc* desc, const void* x, const void* w_pw1, const void* b_pw1, const void* w_pw2,
+                     const void* b_pw2, void* y, const fcm_plan_t* plan, void* stream) {
+  Tensors t = {x, {w_pw1, w_pw2, nullptr}, {b_pw1, b_pw2, nullptr}, y};
+  return run(FCM_OP_PW_PW, desc, t, plan, stream);
 }
 
 fcm_status fcm_pw(const fcm_desc* desc, const void* x, const void* w_pw, const void* b_pw, void* y,

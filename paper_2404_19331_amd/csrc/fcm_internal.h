@@ -28,6 +28,7 @@ enum Family {
   FAM_PWDW = 2,    // PW -> DW (fused, halo recomputed)
   FAM_DW = 3,      // DW alone (family PWDW with the PW stage off)
   FAM_PWDWPW = 4,  // PW -> DW -> PW (fused)
+  FAM_PWPW = 5,    // PW -> PW (fused; family PWDWPW with the DW stage off)
 };
 
 struct Requant {

@@ -159,7 +159,10 @@ __global__ __launch_bounds__(kThreads) void k_pwdw(KArgs a) {
                  a.vec_y && ((mb_eff * DT::ELT) % 16 == 0));
 }
 
-template <class DT, int K, int S, int QMAX, int MBMAX, int WM1, int OMAX, int PMAX, int WM2, int R>
+// MIDDW false: the PW -> PW module (K = S = 1, pad 0, window = tile): no depthwise stage,
+// the second PW reads the first's output chunk straight from LDS; its weights, bias and
+// epilogue are stage 1 (w2, b2, act[1], rq[1]) instead of stage 2.
+template <class DT, int K, int S, int QMAX, int MBMAX, int WM1, int OMAX, int PMAX, int WM2, int R, bool MIDDW>
 __global__ __launch_bounds__(kThreads) void k_pwdwpw(KArgs a) {
   extern __shared__ __align__(16) char smem[];
   using T = typename DT::T;
@@ -195,6 +198,8 @@ __global__ __launch_bounds__(kThreads) void k_pwdwpw(KArgs a) {
   const int n_act2 = max(0, min(TNW2, p_tiles - wn2 * TNW2));
 
   const T* x = (const T*)a.x;
+  static_assert(MIDDW || (K == 1 && S == 1), "PW -> PW has no depthwise geometry");
+  const T* w_last = (const T*)(MIDDW ? a.w3 : a.w2);  // weights of the last PW
   stage_chunk<DT, 0>(smem, x, a.layout, a.vec_x, n, a.Ci, a.H, a.W, iy0, ix0, IH, IW, 0, CIP, L.ps_in, L.off_in,
                      nullptr, false, 0, 0, 0, 0, 0, 0, nullptr, nullptr, 0, 0, 0, 0);
 
@@ -208,7 +213,18 @@ __global__ __launch_bounds__(kThreads) void k_pwdwpw(KArgs a) {
     const int mb_eff = min(MB, a.Cm - m0);
     const int m_tiles = ceil_div(mb_eff, 16);
     const int m_act1 = max(0, min(TMW1, m_tiles - wm1 * TMW1));
-    {
+    if constexpr (!MIDDW) {
+      constexpr int VE = 16 / DT::ELT;
+      if (a.vec_w1 && a.vec_w3) {
+        staged_copy<kBatch>(smem, m_tiles * 16 * CIP / VE,
+                            rows_vec<DT>((const T*)a.w1, a.Cm, a.Ci, m0, 0, CIP, L.rs_w, L.off_w),
+                            o_tiles * 16 * MB / VE, rows_vec<DT>(w_last, a.Co, a.Cm, co0, m0, MB, L.rs_w2, L.off_w2), 0,
+                            NullLoader{});
+      } else {
+        stage_rows<DT>(smem, (const T*)a.w1, a.vec_w1, a.Cm, a.Ci, m0, m_tiles * 16, 0, CIP, L.rs_w, L.off_w);
+        stage_rows<DT>(smem, w_last, a.vec_w3, a.Co, a.Cm, co0, o_tiles * 16, m0, MB, L.rs_w2, L.off_w2);
+      }
+    } else {
       constexpr int VE = 16 / DT::ELT;
       const DwWeights<DT, K> dww{(const T*)a.w2, a.b2, a.Cm, m0, MB, L.off_wd};
       if (a.vec_w1 && a.vec_w3) {
@@ -238,16 +254,23 @@ __global__ __launch_bounds__(kThreads) void k_pwdwpw(KArgs a) {
                                  a.rq[0], smem + L.off_e, L.rs_e, IW, iy0, ix0, a.H, a.W);
     }
     __syncthreads();
-    dw_compute<DT, K, S, R>(smem + L.off_e, L.rs_e, IW, (const Acc*)(smem + L.off_wd), MB, a.TH, a.TW, a.act[1],
-                            a.rq[1], smem + L.off_d, L.rs_d);
-    __syncthreads();
-    mma_chunk<DT, TMW2, TNW2>(acc2, smem + L.off_w2, L.rs_w2, smem + L.off_d, L.rs_d, MB, wm2 * TMW2 * 16,
-                              wn2 * TNW2 * 16, m_act2, n_act2);
+    if constexpr (MIDDW) {
+      dw_compute<DT, K, S, R>(smem + L.off_e, L.rs_e, IW, (const Acc*)(smem + L.off_wd), MB, a.TH, a.TW, a.act[1],
+                              a.rq[1], smem + L.off_d, L.rs_d);
+      __syncthreads();
+      mma_chunk<DT, TMW2, TNW2>(acc2, smem + L.off_w2, L.rs_w2, smem + L.off_d, L.rs_d, MB, wm2 * TMW2 * 16,
+                                wn2 * TNW2 * 16, m_act2, n_act2);
+    } else {
+      // window = tile: the first PW's output positions are the output pixels
+      mma_chunk<DT, TMW2, TNW2>(acc2, smem + L.off_w2, L.rs_w2, smem + L.off_e, L.rs_e, MB, wm2 * TMW2 * 16,
+                                wn2 * TNW2 * 16, m_act2, n_act2);
+    }
     __syncthreads();
   }
 
-  acc_to_lds<DT, TMW2, TNW2>(acc2, wm2 * TMW2 * 16, wn2 * TNW2 * 16, m_act2, n_act2, a.b3, co0, cob_eff, a.act[2],
-                             a.rq[2], smem + L.off_out, L.rs_out, 0, 0, 0, 0, 0);
+  constexpr int LAST = MIDDW ? 2 : 1;  // stage index of the last PW
+  acc_to_lds<DT, TMW2, TNW2>(acc2, wm2 * TMW2 * 16, wn2 * TNW2 * 16, m_act2, n_act2, MIDDW ? a.b3 : a.b2, co0,
+                             cob_eff, a.act[LAST], a.rq[LAST], smem + L.off_out, L.rs_out, 0, 0, 0, 0, 0);
   __syncthreads();
   store_tile<DT>(smem + L.off_out, L.rs_out, (T*)a.y, a.layout, n, a.Co, a.Ho, a.Wo, oy0, ox0, a.TH, a.TW, co0,
                  cob_eff, a.vec_y && ((cob_eff * DT::ELT) % 16 == 0));
@@ -276,9 +299,9 @@ int launch_pwdw(const KArgs& a, int grid, void* stream) {
   return launch_kernel(k_pwdw<DT, K, S, HAS_PW, QMAX, MMAX, WM, R>, a, grid, stream);
 }
 
-template <class DT, int K, int S, int QMAX, int MBMAX, int WM1, int OMAX, int PMAX, int WM2, int R>
+template <class DT, int K, int S, int QMAX, int MBMAX, int WM1, int OMAX, int PMAX, int WM2, int R, bool MIDDW>
 int launch_pwdwpw(const KArgs& a, int grid, void* stream) {
-  return launch_kernel(k_pwdwpw<DT, K, S, QMAX, MBMAX, WM1, OMAX, PMAX, WM2, R>, a, grid, stream);
+  return launch_kernel(k_pwdwpw<DT, K, S, QMAX, MBMAX, WM1, OMAX, PMAX, WM2, R, MIDDW>, a, grid, stream);
 }
 
 template <class DT>

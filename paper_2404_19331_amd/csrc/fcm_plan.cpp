@@ -59,6 +59,9 @@ Geom geometry(int op, const fcm_desc* d) {
     case FCM_OP_PW_DW: g.family = FAM_PWDW; g.ci = d->c_in; g.cm = d->c_mid; g.co = d->c_mid; break;
     case FCM_OP_PW_DW_PW: g.family = FAM_PWDWPW; g.ci = d->c_in; g.cm = d->c_mid; g.co = d->c_out; break;
     case FCM_OP_DW: g.family = FAM_DW; g.ci = d->c_in; g.cm = d->c_in; g.co = d->c_in; break;
+    case FCM_OP_PW_PW:
+      g.family = FAM_PWPW; g.ci = d->c_in; g.cm = d->c_mid; g.co = d->c_out; g.k = 1; g.s = 1; g.pad = 0;
+      break;
     default: g.family = FAM_PW; g.ci = d->c_in; g.cm = d->c_in; g.co = d->c_out; g.k = 1; g.s = 1; g.pad = 0; break;
   }
   g.ho = out_dim(g.h, g.k, g.s, g.pad);
@@ -135,6 +138,16 @@ static Bytes module_bytes(const Geom& g, int TH, int TW, int COB) {
       // Eq. 4 (+ output write); both weight-tile counts are the mid-channel blocks
       b.paper = ((2 * g.ci * ovl + x_el) * nmb + T * (int64_t)g.cm * g.ci + T * g.cm * kk + y_el) * e;
       b.redundancy = (double)(SR * SC) / ((double)g.h * g.w) - 1.0;
+      break;
+    }
+    case FAM_PWPW: {
+      // as PW->DW->PW without the depthwise weights and halo: x per output-channel block,
+      // the first layer's weights per tile and block, the second's per tile
+      const int64_t ncb = ceil_div(g.co, COB);
+      const int64_t y_el = N * g.h * (int64_t)g.w * g.co;
+      b.ideal = (x_el + (int64_t)g.cm * g.ci + (int64_t)g.co * g.cm + y_el) * e;
+      b.tiled = (ncb * staged * g.ci + T * ncb * (int64_t)g.cm * g.ci + T * (int64_t)g.co * g.cm + y_el) * e;
+      b.paper = (ncb * x_el + T * ncb * (int64_t)g.cm * g.ci + T * (int64_t)g.co * g.cm + y_el) * e;
       break;
     }
     case FAM_PWDWPW: {
@@ -230,6 +243,7 @@ static int tiling_lds(const Variant& v, const Geom& g, int TH, int TW, int CB, i
       if (CB != COB) return 0;
       return lds_layout_pwdw(g.dtype, g.k, g.s, false, TH, TW, CB, COB).bytes;
     case FAM_PWDWPW:
+    case FAM_PWPW:
       // CB = intermediate chunk: a multiple of both the MFMA M tile and its K step
       if (CB <= 0 || CB % 16 || CB % kb || CB > v.max_mb) return 0;
       return lds_layout_pwdwpw(g.dtype, g.k, g.s, TH, TW, g.ci, CB, COB).bytes;
@@ -421,7 +435,7 @@ static fcm_status search(const Geom& g, const fcm_desc* d, const fcm_hw_desc& hw
       cbs = {64 / g.elt};
     } else if (v.family == FAM_DW) {
       cbs = {0};  // CB follows COB
-    } else if (v.family == FAM_PWDWPW) {
+    } else if (v.family == FAM_PWDWPW || v.family == FAM_PWPW) {
       const int step = std::max(16, kb);
       for (int c = step; c <= std::min(v.max_mb, round_up(g.cm, step)); c += step) cbs.push_back(c);
     } else {
@@ -564,6 +578,10 @@ static void lbl_stages(int op, const fcm_desc* d, std::vector<std::pair<int, fcm
       one(FCM_OP_PW, s.h, s.w, s.c_in, s.c_mid, 0);
       one(FCM_OP_DW, s.h, s.w, s.c_mid, s.c_mid, 1);
       one(FCM_OP_PW, ho, wo, s.c_mid, s.c_out, 2);
+      break;
+    case FCM_OP_PW_PW:
+      one(FCM_OP_PW, s.h, s.w, s.c_in, s.c_mid, 0);
+      one(FCM_OP_PW, s.h, s.w, s.c_mid, s.c_out, 1);
       break;
     default:
       break;

@@ -18,7 +18,7 @@ import os
 PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG, "libfcm.so")
 
-OP = {"dw_pw": 0, "pw_dw": 1, "pw_dw_pw": 2, "dw": 3, "pw": 4}
+OP = {"dw_pw": 0, "pw_dw": 1, "pw_dw_pw": 2, "dw": 3, "pw": 4, "pw_pw": 5}
 DTYPE = {"f32": 0, "bf16": 1, "i8": 2}
 LAYOUT = {"nchw": 0, "nhwc": 1}
 ACT = {"none": 0, "relu": 1, "relu6": 2}
@@ -83,10 +83,11 @@ def lib():
         L.fcm_dw_pw.argtypes = [dp, vp, vp, vp, vp, vp, vp, pp, vp]
         L.fcm_pw_dw.argtypes = [dp, vp, vp, vp, vp, vp, vp, pp, vp]
         L.fcm_pw_dw_pw.argtypes = [dp, vp, vp, vp, vp, vp, vp, vp, vp, pp, vp]
+        L.fcm_pw_pw.argtypes = [dp, vp, vp, vp, vp, vp, vp, pp, vp]
         L.fcm_dw.argtypes = [dp, vp, vp, vp, vp, pp, vp]
         L.fcm_pw.argtypes = [dp, vp, vp, vp, vp, pp, vp]
         for f in (L.fcm_plan, L.fcm_plan_evaluate, L.fcm_dw_pw, L.fcm_pw_dw, L.fcm_pw_dw_pw,
-                  L.fcm_dw, L.fcm_pw):
+                  L.fcm_pw_pw, L.fcm_dw, L.fcm_pw):
             f.restype = ctypes.c_int
         L.fcm_status_string.argtypes = [ctypes.c_int]
         L.fcm_status_string.restype = ctypes.c_char_p
@@ -307,6 +308,19 @@ def pw_dw_pw(x, w_pw1, w_dw, w_pw2, b_pw1=None, b_dw=None, b_pw2=None, *, stride
                  y, prepare)
 
 
+def pw_pw(x, w_pw1, w_pw2, b_pw1=None, b_pw2=None, *, act=("none", "none"), rq=None, layout="nchw", plan=None,
+          out=None, stream=None, prepare=False):
+    """PW -> PW module in one kernel. Returns y [n, c_out, h, w]."""
+    dt = _dtype_name(x)
+    n, c, h, w = _dims(x, layout)
+    cm, co = int(w_pw1.shape[0]), int(w_pw2.shape[0])
+    _prep(x, [w_pw1, w_pw2], [b_pw1, b_pw2], dt)
+    d = make_desc(n, h, w, c, cm, co, 1, 1, 0, dt, layout, act, rq)
+    y = _out(x, layout, n, co, h, w, out)
+    return _call(lib().fcm_pw_pw, (ctypes.byref(d), _ptr(x), _ptr(w_pw1), _ptr(b_pw1), _ptr(w_pw2), _ptr(b_pw2),
+                                   _ptr(y), _plan_arg(plan), _stream(x, stream)), y, prepare)
+
+
 def dw(x, w_dw, b_dw=None, *, stride=1, pad=None, act="none", rq=None, layout="nchw", plan=None, out=None,
        stream=None, prepare=False):
     """Single depthwise layer (layer-by-layer kernel)."""
@@ -370,6 +384,15 @@ def pw_then_dw(x, w_pw, w_dw, b_pw=None, b_dw=None, *, stride=1, pad=None, act=(
     m = c1.y if prepare else c1
     c2 = dw(m, w_dw, b_dw, stride=stride, pad=pad, act=act[1], rq=rq[1], layout=layout, out=out, stream=stream,
             prepare=prepare)
+    return _Chain([c1, c2]) if prepare else c2
+
+
+def pw_then_pw(x, w_pw1, w_pw2, b_pw1=None, b_pw2=None, *, act=("none", "none"), rq=None, layout="nchw",
+               mid=None, out=None, stream=None, prepare=False):
+    rq = list(rq) if rq else [None, None]
+    c1 = pw(x, w_pw1, b_pw1, act=act[0], rq=rq[0], layout=layout, out=mid, stream=stream, prepare=prepare)
+    m = c1.y if prepare else c1
+    c2 = pw(m, w_pw2, b_pw2, act=act[1], rq=rq[1], layout=layout, out=out, stream=stream, prepare=prepare)
     return _Chain([c1, c2]) if prepare else c2
 
 

@@ -21,6 +21,8 @@ weights in execution order):
 from dataclasses import dataclass, field, replace
 from typing import Tuple
 
+import math
+
 import numpy as np
 
 BASE_SEED = 2404_19331
@@ -227,12 +229,21 @@ PWPW_SHAPES = [(56, 24, 144, 24), (28, 32, 192, 32), (14, 64, 384, 64), (14, 96,
 
 def config_pwpw():
     """PW -> PW pairs (the paper's PwPw module, frequent in its int8 plans), int8 NHWC,
-    batch 8, requant 2^-8 RNE, ReLU after the first layer."""
-    rq = (RQ_C4, RQ_C4, RQ_C4)
-    return [Case("pw_pw", 8, hw, hw, ci, cm, co, 1, 1, 0, "i8", "nhwc", ("relu", "none", "none"), rq,
-                 dist_x="i8", dist_w="i8", seed=BASE_SEED + 6 + 100 * i,
-                 name="PWPW %dx%dx%d->%d->%d i8 b8" % (hw, hw, ci, cm, co))
-            for i, (hw, ci, cm, co) in enumerate(PWPW_SHAPES, start=1)]
+    batch 8, ReLU after the first layer. Each stage requantises by a power of two sized to
+    its contraction: U{-127..127} operands have standard deviation 127/sqrt(3), so a
+    C-wide sum has 127^2/3 * sqrt(C); the shift brings that to about 48, keeping nearly
+    all results inside the int8 range. The second stage reads ReLU output, whose root mean
+    square is about 48/sqrt(2)."""
+    sd = 127 / math.sqrt(3)
+    out = []
+    for i, (hw, ci, cm, co) in enumerate(PWPW_SHAPES, start=1):
+        s1 = int(round(math.log2(sd * sd * math.sqrt(ci) / 48)))
+        s2 = int(round(math.log2(48 / math.sqrt(2) * sd * math.sqrt(cm) / 48)))
+        rq = ((1, s1, -127, 127), (1, s2, -127, 127), RQ_C4)
+        out.append(Case("pw_pw", 8, hw, hw, ci, cm, co, 1, 1, 0, "i8", "nhwc", ("relu", "none", "none"), rq,
+                        dist_x="i8", dist_w="i8", seed=BASE_SEED + 6 + 100 * i,
+                        name="PWPW %dx%dx%d->%d->%d i8 b8" % (hw, hw, ci, cm, co)))
+    return out
 
 
 CONFIGS = {"C1": config_c1, "C2": config_c2, "C3": config_c3, "C4": config_c4, "C5": config_c5}

@@ -84,6 +84,10 @@ def run_fused(case, d, plan=None, out=None):
     if case.op == "pw_dw_pw":
         return fcm.pw_dw_pw(d["x"], d["w_pw1"], d["w_dw"], d["w_pw2"], d.get("b_pw1"), d.get("b_dw"),
                             d.get("b_pw2"), act=case.act, rq=rq, **kw)
+    if case.op == "pw_pw":
+        kw.pop("stride"), kw.pop("pad")
+        return fcm.pw_pw(d["x"], d["w_pw1"], d["w_pw2"], d.get("b_pw1"), d.get("b_pw2"), act=case.act[:2], rq=rq,
+                         **kw)
     if case.op == "dw":
         return fcm.dw(d["x"], d["w_dw"], d.get("b_dw"), act=case.act[0], rq=rq[0] if rq else None, **kw)
     if case.op == "pw":
@@ -104,6 +108,9 @@ def run_unfused(case, d):
     if case.op == "pw_dw_pw":
         return fcm.pw_then_dw_then_pw(d["x"], d["w_pw1"], d["w_dw"], d["w_pw2"], d.get("b_pw1"), d.get("b_dw"),
                                       d.get("b_pw2"), act=case.act, rq=rq, **kw)
+    if case.op == "pw_pw":
+        return fcm.pw_then_pw(d["x"], d["w_pw1"], d["w_pw2"], d.get("b_pw1"), d.get("b_pw2"), act=case.act[:2],
+                              rq=rq, layout=case.layout)
     raise ValueError(case.op)
 
 

@@ -10,7 +10,8 @@ import numpy as np
 import pytest
 
 from paper_2404_19331_amd import fcm
-from paper_2404_19331_amd.workloads import Case, make_inputs, config_c1, config_c2, config_c3, config_c4, config_c5
+from paper_2404_19331_amd.workloads import (Case, make_inputs, config_c1, config_c2, config_c3, config_c4, config_c5,
+                                             config_pwpw)
 
 from gpu_util import (assert_close, batch_slice, dev_inputs, oracle_ref, run_fused, run_unfused, to_np, torch)
 
@@ -35,6 +36,9 @@ def _small_cases():
             out.append(Case("pw", 2, 13, 11, 40, 40, 24, 1, 1, 0, dt, lay, ACTS[dt], RQ_SMALL,
                             dist_x="i8small" if dt == "i8" else "n01", dist_w="i8small", bias=True,
                             seed=1000 + len(out), name="pw-%s-%s" % (dt, lay)))
+            out.append(Case("pw_pw", 2, 13, 11, 40, 72, 24, 1, 1, 0, dt, lay, ACTS[dt], RQ_SMALL,
+                            dist_x="i8small" if dt == "i8" else "n01", dist_w="i8small", bias=True,
+                            seed=1000 + len(out), name="pw_pw-%s-%s" % (dt, lay)))
     return out
 
 
@@ -74,6 +78,12 @@ EDGE = [
     Case("dw_pw", 1, 6, 5, 600, 600, 300, 3, 1, 1, "bf16", "nhwc", ("relu", "none", "none"), bias=True, seed=12),
     Case("pw_dw_pw", 1, 6, 5, 100, 200, 150, 3, 1, 1, "bf16", "nhwc", ("relu6", "relu6", "none"), bias=True,
          seed=13),
+    # PW -> PW: ragged channel rows, single channels, many chunks and output blocks
+    Case("pw_pw", 2, 10, 12, 20, 36, 12, 1, 1, 0, "i8", "nhwc", ("relu", "none", "none"), RQ_SMALL,
+         dist_x="i8small", dist_w="i8small", bias=True, seed=14),
+    Case("pw_pw", 1, 9, 7, 1, 1, 1, 1, 1, 0, "bf16", "nchw", ("relu6", "none", "none"), bias=True, seed=15),
+    Case("pw_pw", 1, 6, 5, 600, 300, 200, 1, 1, 0, "bf16", "nhwc", ("relu", "none", "none"), bias=True, seed=16),
+    Case("pw_pw", 3, 1, 1, 16, 48, 8, 1, 1, 0, "f32", "nhwc", ("relu", "relu", "none"), bias=True, seed=17),
 ]
 
 
@@ -89,7 +99,7 @@ def test_edge_parity(case):
 # Named configurations at full size
 # ---------------------------------------------------------------------------------
 
-FULL = config_c1() + config_c2() + config_c3(batches=(1,)) + config_c4()
+FULL = config_c1() + config_c2() + config_c3(batches=(1,)) + config_c4() + config_pwpw()
 SAMPLED = config_c3(batches=(32,)) + config_c5()
 
 
@@ -114,8 +124,8 @@ def test_config_parity_sampled_images(case):
 # Fused vs layer-by-layer, determinism, tilings
 # ---------------------------------------------------------------------------------
 
-UNFUSED = [c for c in SMALL if c.op in ("dw_pw", "pw_dw", "pw_dw_pw") and c.layout == "nhwc"] + config_c1() + \
-    config_c2() + config_c4()
+UNFUSED = [c for c in SMALL if c.op in ("dw_pw", "pw_dw", "pw_dw_pw", "pw_pw") and c.layout == "nhwc"] + \
+    config_c1() + config_c2() + config_c4() + config_pwpw()
 
 
 @pytest.mark.parametrize("case", UNFUSED, ids=lambda c: c.name.replace(" ", "_"))
@@ -139,9 +149,10 @@ def test_run_to_run_bitwise_determinism(case):
 
 
 @pytest.mark.parametrize("dt", ["f32", "bf16"])
-@pytest.mark.parametrize("op", ["dw_pw", "pw_dw", "pw_dw_pw"])
+@pytest.mark.parametrize("op", ["dw_pw", "pw_dw", "pw_dw_pw", "pw_pw"])
 def test_power_of_two_homogeneity_bit_exact(dt, op):
-    case = Case(op, 2, 12, 9, 24, 24 if op == "dw_pw" else 48, 16 if op != "pw_dw" else 48, 3, 1, 1, dt, "nhwc",
+    k, pad = (1, 0) if op == "pw_pw" else (3, 1)
+    case = Case(op, 2, 12, 9, 24, 24 if op == "dw_pw" else 48, 16 if op != "pw_dw" else 48, k, 1, pad, dt, "nhwc",
                 ("relu", "relu", "none"), dist_x="n01", bias=False, seed=77)
     inp = make_inputs(case)
     d = dev_inputs(inp, case.dtype)

@@ -36,7 +36,7 @@ def _workspace_limit():
 
 def _all_cases():
     out = []
-    for wl in ("C1", "C2", "C3b1", "C3b32", "C4", "C5"):
+    for wl in ("C1", "C2", "C3b1", "C3b32", "C4", "C5", "PWPW"):
         cases, _ = bench.workload_cases(wl)
         out += [(wl, c) for c in cases]
     return out
@@ -79,7 +79,8 @@ def test_plan_every_layer(wl, case):
     p = fcm.plan(case.op, d)
     ho, wo = fcm.out_hw(case.h, case.w, case.k, case.stride, case.pad)
     name = fcm.variant_name(p.variant)
-    fam = {"dw_pw": "k_dwpw", "pw_dw": "k_pwdw", "pw_dw_pw": "k_pwdwpw", "dw": "k_dw", "pw": "k_pw"}[case.op]
+    fam = {"dw_pw": "k_dwpw", "pw_dw": "k_pwdw", "pw_dw_pw": "k_pwdwpw", "pw_pw": "k_pwpw", "dw": "k_dw",
+           "pw": "k_pw"}[case.op]
     assert name.startswith(fam), name
     assert 1 <= p.tile_h and 1 <= p.tile_w and p.co_block >= 1 and p.c_block >= 1
     assert 0 < p.lds_bytes <= 160 * 1024
@@ -179,3 +180,15 @@ def test_header_is_plain_c():
     # the plan struct the Python binding marshals has the size the library fills in
     assert ctypes.sizeof(fcm.Plan) % 8 == 0
     assert L.fcm_variant_count() > 0
+
+
+@pytest.mark.parametrize("wl,case", [(w, c) for w, c in CASES if c.op == "pw_pw"],
+                         ids=lambda v: v if isinstance(v, str) else v.name)
+def test_pw_pw_byte_model_closed_forms(wl, case):
+    # two pointwise layers: the fused module moves x, both weight matrices and y; the
+    # layer-by-layer pair also writes and reads the c_mid-wide intermediate
+    p = fcm.plan(case.op, fcm.desc_from_case(case))
+    px = case.n * case.h * case.w
+    w = case.c_mid * case.c_in + case.c_out * case.c_mid
+    assert p.bytes_ideal == px * (case.c_in + case.c_out) + w
+    assert p.bytes_lbl_ideal == p.bytes_ideal + 2 * px * case.c_mid

@@ -26,7 +26,8 @@ const Variant* all_variants(int* count) {
                                      variants_pwdwpw,   variants_v2_bf16,   variants_v2_f32,  variants_v2_i8,
                                      variants_v3_dwpw_bf16_s1, variants_v3_dwpw_bf16_s2, variants_v3_dwpw_f32,
                                      variants_v3_dwpw_i8, variants_v3_pw, variants_v3_pw_f32, variants_v3_pw_i8,
-                                     variants_v3_dw_bf16, variants_v3_dw_f32, variants_v3_dw_i8};
+                                     variants_v3_dw_bf16, variants_v3_dw_f32, variants_v3_dw_i8,
+                                     variants_v4_pwpw_i8, variants_v4_pwpw_bf16, variants_v4_pwpw_f32};
     for (auto fn : fns) {
       int n = 0;
       const Variant* t = fn(&n);
@@ -240,6 +241,12 @@ static fcm_status run(int op, const fcm_desc* d, const Tensors& t, const fcm_pla
     if (!a.ws) return fail(FCM_EDEVICE, "could not allocate the split workspace");
     a.splits = p.splits;
     a.nwork *= p.splits;  // work units
+  }
+  if (v.gen == 4) {
+    // PW -> PW register kernel: pixel groups, each on `splits` waves of one workgroup
+    a.nwork = (int)ceil_div((int64_t)g.n * g.h * g.w, (int64_t)v.max_p);
+    a.splits = p.splits;
+    a.vec_w2 = aligned16(t.w[1]) && (g.cm * e) % 16 == 0;
   }
   a.cus = device_cus();
   a.grid_cap = v.gen == 3 ? p.workgroups : 0;

@@ -297,8 +297,11 @@ struct Variant {
   int tile_w = 0;
   int gen = 1;      // 2: NHWC, 16-byte channel rows, LDS-DMA staging, fixed chunk of 64 bytes
                     // 3: as 2, persistent workgroups, run-time tile, max_p = 64 * blocks per wave
+                    // 4: PW -> PW with the intermediate in registers, one pixel group per
+                    //    wave (max_p = 16 * blocks), all output channels, no LDS
   int pitch = 0;    // gen 3: LDS window row pitch in pixels (window width must not exceed it)
-  int ks = 1;       // gen 3: 64-byte channel chunks per item
+  int ks = 1;       // gen 3: 64-byte channel chunks per item; gen 4: 64-byte k-steps of the
+                    // first convolution held in registers (input channels <= 64 * ks bytes)
 };
 
 // Compiled variants of each translation unit, and all of them in a fixed order
@@ -321,6 +324,9 @@ const Variant* variants_v3_pw_i8(int* count);
 const Variant* variants_v3_dw_bf16(int* count);
 const Variant* variants_v3_dw_f32(int* count);
 const Variant* variants_v3_dw_i8(int* count);
+const Variant* variants_v4_pwpw_i8(int* count);
+const Variant* variants_v4_pwpw_bf16(int* count);
+const Variant* variants_v4_pwpw_f32(int* count);
 const Variant* all_variants(int* count);
 
 }  // namespace fcm

@@ -279,14 +279,21 @@ __global__ __launch_bounds__(kThreads) void k_pwdwpw(KArgs a) {
 // ------------------------------------------------------------------------------------
 // Host launchers
 // ------------------------------------------------------------------------------------
+// Launch a kernel taking one KArgs by value; returns this launch's own status (not an
+// error left behind by an earlier runtime call of the process).
+inline int launch_args(const void* fn, int grid, int threads, int lds, void* stream, const KArgs& a) {
+  KArgs copy = a;
+  void* args[] = {(void*)&copy};
+  return (int)hipLaunchKernel(fn, dim3(grid), dim3(threads), args, (size_t)lds, (hipStream_t)stream);
+}
+
 template <class Kern>
 inline int launch_kernel(Kern fn, const KArgs& a, int grid, void* stream) {
   if (a.L.bytes > 65536) {
     hipError_t e = hipFuncSetAttribute((const void*)fn, hipFuncAttributeMaxDynamicSharedMemorySize, a.L.bytes);
     if (e != hipSuccess) return (int)e;
   }
-  hipLaunchKernelGGL(fn, dim3(grid), dim3(kThreads), a.L.bytes, (hipStream_t)stream, a);
-  return (int)hipGetLastError();
+  return launch_args((const void*)fn, grid, kThreads, a.L.bytes, stream, a);
 }
 
 template <class DT, int K, int S, bool HAS_DW, int PMAX, int MMAX, int WM, int R>

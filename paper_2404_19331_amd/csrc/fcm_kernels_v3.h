@@ -729,19 +729,18 @@ int launch_fused3(const KArgs& a, int grid, void* stream) {
   if (g > a.nwork) g = a.nwork;
   if (g < 1) g = 1;
   (void)grid;
-  hipLaunchKernelGGL(fn, dim3(g), dim3(kThreads3), lds, (hipStream_t)stream, a);
+  const int e = launch_args((const void*)fn, g, kThreads3, lds, stream, a);
+  if (e != 0) return e;
   if constexpr (MODE != M3_DW) {
     if (a.splits > 1) {
-      hipError_t e = hipGetLastError();
-      if (e != hipSuccess) return (int)e;
       KArgs c = a;
       c.COB = 16 * CT;
       const int64_t total = (int64_t)(a.nwork / a.splits) * a.TH * a.TW * (4 * CT);
-      hipLaunchKernelGGL((k_combine3<DT, MODE == M3_PW ? 0 : 1>), dim3((unsigned)((total + 255) / 256)), dim3(256), 0,
-                         (hipStream_t)stream, c);
+      return launch_args((const void*)k_combine3<DT, MODE == M3_PW ? 0 : 1>, (int)((total + 255) / 256), 256, 0,
+                         stream, c);
     }
   }
-  return (int)hipGetLastError();
+  return 0;
 }
 
 }  // namespace fcm

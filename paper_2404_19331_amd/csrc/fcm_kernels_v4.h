@@ -1,0 +1,245 @@
+// fcm_kernels_v4.h -- PW -> PW module for gfx950 with the intermediate handed from the
+// first pointwise convolution to the second in registers (NHWC).
+//
+// k_pwpw4<DT, KS, CT, PB>
+//   A workgroup is four waves. A pixel group (PB blocks of 16 pixels) is computed against
+//   every output channel (up to 16*CT) by S = 1, 2 or 4 of them (a.splits): the
+//   intermediate is cut into chunks of 64 bytes (one MFMA k-step of the second
+//   convolution) and wave j of the S takes chunks j, j+S, j+2S, ... A workgroup covers
+//   4/S neighbouring pixel groups; with S = 1 its four waves are independent (no LDS, no
+//   barrier) and their weight loads are the same addresses, served by the CU's cache.
+//
+//   For each chunk the wave loads, straight into MFMA operand registers, the first
+//   convolution's weight rows of the chunk and the chunk's 64-byte column slice of the
+//   second convolution's weights. The first convolution's weight rows are taken in a
+//   permuted order: MFMA row i of M-tile t is intermediate channel
+//   m0 + (16/elt)*(i/4) + 4t + i%4, so the accumulator lane (pixel l%16, group l/16), which
+//   holds rows 4*(l/16)..+3 of every tile, ends up with the 16 contiguous bytes of channels
+//   m0 + (16/elt)*(l/16) + [0, 16/elt) after +bias, activation and the cast (int8:
+//   requantisation). Those 16 bytes are exactly the B operand the lane supplies to the
+//   second convolution's MFMA for that chunk: the paper's communication buffer between
+//   the two layers (Sec. III-B) never leaves the registers. Output-stationary over the
+//   chunks (Sec. III-A, OS-LWS), output written once.
+//
+//   S > 1: the S waves of a pixel group put their partial sums (fp32 / int32, MFMA lane
+//   order) in LDS, meet at one barrier, and wave j then finishes the output tiles t with
+//   t % S == j, adding the S partial sums in wave order (int8 sums are exact, float sums
+//   always in the same order, so results are reproducible).
+#pragma once
+
+#include "fcm_kernels_v3.h"
+
+namespace fcm {
+
+// 16 bytes of a row at byte offset off, zero beyond nbytes. vec: the row is 16-byte
+// aligned and nbytes a multiple of 16; otherwise the row is 4-byte aligned and nbytes a
+// multiple of 4, and the slot is read as four 4-byte words.
+__device__ __forceinline__ u32x4 load_slot4(const char* row, int off, int nbytes, bool vec) {
+  u32x4 v = {0u, 0u, 0u, 0u};
+  if (vec) {
+    if (off < nbytes) v = *(const u32x4*)(row + off);
+  } else {
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      if (off + 4 * e < nbytes) v[e] = *(const uint32_t*)(row + off + 4 * e);
+  }
+  return v;
+}
+
+// Stage-one epilogue of M-tile t into the lane's 16-byte operand slot: elements
+// 4t .. 4t+3 of the slot (channels m0 + (16/elt)*group + 4t + v).
+template <class DT>
+struct Mid4;
+template <>
+struct Mid4<TI8> {
+  __device__ static __forceinline__ void put(u32x4& slot, int t, const i32x4& acc, const int32_t (&b)[4],
+                                             const Epi3& e) {
+    uint32_t w = 0;
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int32_t s = acc[v];
+      w |= ((uint32_t)epi_i(s + b[v], e) & 0xffu) << (8 * v);
+    }
+    slot[t] = w;
+  }
+};
+template <>
+struct Mid4<TBF16> {
+  __device__ static __forceinline__ void put(u32x4& slot, int t, const f32x4& acc, const float (&b)[4],
+                                             const Epi3& e) {
+    const float a0 = acc[0], a1 = acc[1], a2 = acc[2], a3 = acc[3];
+    slot[2 * t] = pack_bf16x2(epi_f(a0 + b[0], e), epi_f(a1 + b[1], e));
+    slot[2 * t + 1] = pack_bf16x2(epi_f(a2 + b[2], e), epi_f(a3 + b[3], e));
+  }
+};
+template <>
+struct Mid4<TF32> {
+  __device__ static __forceinline__ void put(u32x4& slot, int, const f32x4& acc, const float (&b)[4],
+                                             const Epi3& e) {
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const float s = acc[v];
+      slot[v] = __float_as_uint(epi_f(s + b[v], e));
+    }
+  }
+};
+
+// Final epilogue of four consecutive output channels: +bias, activation, cast, one store
+// of 4 elements.
+template <class DT>
+__device__ __forceinline__ void store4_out(char* p, const typename DT::AccV& acc, const typename DT::Acc (&b)[4],
+                                           const Epi3& e) {
+  const typename DT::Acc s0 = acc[0], s1 = acc[1], s2 = acc[2], s3 = acc[3];
+  if constexpr (std::is_same<DT, TI8>::value) {
+    *(uint32_t*)p = ((uint32_t)epi_i(s0 + b[0], e) & 0xffu) | (((uint32_t)epi_i(s1 + b[1], e) & 0xffu) << 8) |
+                    (((uint32_t)epi_i(s2 + b[2], e) & 0xffu) << 16) | ((uint32_t)epi_i(s3 + b[3], e) << 24);
+  } else if constexpr (std::is_same<DT, TBF16>::value) {
+    *(u32x2*)p = u32x2{pack_bf16x2(epi_f(s0 + b[0], e), epi_f(s1 + b[1], e)),
+                       pack_bf16x2(epi_f(s2 + b[2], e), epi_f(s3 + b[3], e))};
+  } else {
+    *(u32x4*)p = u32x4{__float_as_uint(epi_f(s0 + b[0], e)), __float_as_uint(epi_f(s1 + b[1], e)),
+                       __float_as_uint(epi_f(s2 + b[2], e)), __float_as_uint(epi_f(s3 + b[3], e))};
+  }
+}
+
+template <class DT, int KS, int CT, int PB>
+__global__ __launch_bounds__(256) void k_pwpw4(KArgs a) {
+  using Acc = typename DT::Acc;
+  using AccV = typename DT::AccV;
+  constexpr int E = DT::ELT;
+  constexpr int TPC = 4 / E;   // first-convolution M-tiles per 64-byte chunk
+  constexpr int CPG = 16 / E;  // channels per 16-byte lane slot
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int r16 = lane & 15, g = lane >> 4;
+
+  const int S = a.splits;                  // waves per pixel group: 1, 2 or 4
+  const int L = xcd_remap(blockIdx.x, gridDim.x);
+  const int gi = wave / S, j = wave % S;   // pixel group in the workgroup, split
+  const int pg = (4 / S) * L + gi;         // pixel group
+  const bool active = pg < a.nwork;
+  if (S == 1 && !active) return;           // (S > 1: every wave reaches the barrier)
+  const int npix = a.N * a.H * a.W;
+  const int ci_b = a.Ci * E, cm_b = a.Cm * E;
+  const int ks = ceil_div(ci_b, 64);
+  const int ct = ceil_div(a.Co, 16);
+  const int nch = ceil_div(cm_b, 64);
+  const char* x = (const char*)a.x;
+  const char* w1 = (const char*)a.w1;
+  const char* w2 = (const char*)a.w2;
+  const bool vx = a.vec_x, vw1 = a.vec_w1, vw2 = a.vec_w2;
+
+  // B operands of the first convolution: the group's pixels, all input channels
+  u32x4 xb[PB][KS];
+#pragma unroll
+  for (int pb = 0; pb < PB; ++pb) {
+    const int p = (pg * PB + pb) * 16 + r16;
+    const char* row = x + (size_t)p * ci_b;
+    const int nb = p < npix ? ci_b : 0;
+#pragma unroll
+    for (int s = 0; s < KS; ++s) xb[pb][s] = s < ks ? load_slot4(row, 64 * s + 16 * g, nb, vx) : u32x4{0u, 0u, 0u, 0u};
+  }
+
+  AccV acc2[PB][CT];
+#pragma unroll
+  for (int pb = 0; pb < PB; ++pb)
+#pragma unroll
+    for (int u = 0; u < CT; ++u) acc2[pb][u] = AccV{0, 0, 0, 0};
+
+  const Epi3 e1 = make_epi3(a.act[0], a.rq[0]);
+#pragma unroll 1
+  for (int c = active ? j : nch; c < nch; c += S) {
+    const int m0 = c * (64 / E);
+    u32x4 a1[TPC][KS];
+#pragma unroll
+    for (int t = 0; t < TPC; ++t) {
+      const int ch = m0 + CPG * (r16 >> 2) + 4 * t + (r16 & 3);
+      const char* row = w1 + (size_t)ch * ci_b;
+      const int nb = ch < a.Cm ? ci_b : 0;
+#pragma unroll
+      for (int s = 0; s < KS; ++s)
+        a1[t][s] = s < ks ? load_slot4(row, 64 * s + 16 * g, nb, vw1) : u32x4{0u, 0u, 0u, 0u};
+    }
+    u32x4 a2[CT];
+#pragma unroll
+    for (int u = 0; u < CT; ++u) {
+      const int co = 16 * u + r16;
+      const int nb = (u < ct && co < a.Co) ? cm_b : 0;
+      a2[u] = load_slot4(w2 + (size_t)(co < a.Co ? co : 0) * cm_b, 64 * c + 16 * g, nb, vw2);
+    }
+    Acc b1[TPC][4];
+#pragma unroll
+    for (int t = 0; t < TPC; ++t)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int ch = m0 + CPG * g + 4 * t + v;
+        b1[t][v] = ch < a.Cm ? load_bias<DT>(a.b1, ch) : Acc(0);
+      }
+#pragma unroll
+    for (int pb = 0; pb < PB; ++pb) {
+      u32x4 mid = {0u, 0u, 0u, 0u};
+#pragma unroll
+      for (int t = 0; t < TPC; ++t) {
+        AccV acc1 = AccV{0, 0, 0, 0};
+#pragma unroll
+        for (int s = 0; s < KS; ++s)
+          if (s < ks) mma16(DT(), acc1, a1[t][s], xb[pb][s]);
+        Mid4<DT>::put(mid, t, acc1, b1[t], e1);
+      }
+#pragma unroll
+      for (int u = 0; u < CT; ++u)
+        if (u < ct) mma16(DT(), acc2[pb][u], a2[u], mid);
+    }
+  }
+
+  const Epi3 e2 = make_epi3(a.act[1], a.rq[1]);
+  char* y = (char*)a.y;
+  // final epilogue of output tile u of pixel block pb: lane (pixel r16, group g) holds
+  // output channels 16u + 4g + [0, 4)
+  auto finish = [&](const AccV& v, int pb, int u) {
+    const int p = (pg * PB + pb) * 16 + r16;
+    const int co = 16 * u + 4 * g;
+    if (p >= npix || co >= a.Co) return;
+    Acc b[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) b[q] = load_bias<DT>(a.b2, co + q);
+    store4_out<DT>(y + ((size_t)p * a.Co + co) * E, v, b, e2);
+  };
+
+  if (S > 1) {
+    // partial sums through LDS: [wave][pixel block][output tile][lane], 16 bytes each
+    extern __shared__ __align__(16) char smem[];
+    AccV* red = (AccV*)smem;
+    const int nt = PB * ct;
+#pragma unroll
+    for (int pb = 0; pb < PB; ++pb)
+#pragma unroll
+      for (int u = 0; u < CT; ++u)
+        if (u < ct) red[(wave * nt + pb * ct + u) * 64 + lane] = acc2[pb][u];
+    __syncthreads();
+    if (!active) return;
+    for (int t = j; t < nt; t += S) {
+      AccV v = red[((gi * S) * nt + t) * 64 + lane];
+      for (int jj = 1; jj < S; ++jj) v += red[((gi * S + jj) * nt + t) * 64 + lane];
+      finish(v, t / ct, t % ct);
+    }
+    return;
+  }
+#pragma unroll
+  for (int pb = 0; pb < PB; ++pb)
+#pragma unroll
+    for (int u = 0; u < CT; ++u)
+      if (u < ct) finish(acc2[pb][u], pb, u);
+}
+
+template <class DT, int KS, int CT, int PB>
+int launch_pwpw4(const KArgs& a, int grid, void* stream) {
+  const void* fn = (const void*)k_pwpw4<DT, KS, CT, PB>;
+  const int lds = a.splits > 1 ? 4 * PB * ceil_div(a.Co, 16) * 1024 : 0;
+  if (lds > 65536) {
+    const hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+    if (e != hipSuccess) return (int)e;
+  }
+  return launch_args(fn, grid, 256, lds, stream, a);
+}
+
+}  // namespace fcm

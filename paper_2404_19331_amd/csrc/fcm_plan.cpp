@@ -263,6 +263,58 @@ static bool variant_matches(const Variant& v, const Geom& g) {
   return v.k == g.k && v.stride == g.s;
 }
 
+// Pixel groups of the PW -> PW register kernel (gen 4): one wave each.
+static int64_t pixel_groups4(const Variant& v, const Geom& g) {
+  return ceil_div((int64_t)g.n * g.h * g.w, (int64_t)v.max_p);
+}
+
+// LDS bytes of the PW -> PW register kernel: with splits > 1 the four waves' partial
+// sums, [wave][pixel block][output tile][64 lanes] of 16 bytes.
+static int lds_bytes4(const Variant& v, const Geom& g, int splits) {
+  return splits > 1 ? 4 * (v.max_p / 16) * ceil_div(g.co, 16) * 1024 : 0;
+}
+
+// Plan of the PW -> PW register kernel: its tiling is fixed by the variant (pixel groups of
+// max_p pixels, 64-byte intermediate chunks, every output channel); only the number of
+// waves sharing a pixel group's intermediate chunks (1, 2 or 4, in one workgroup) is chosen.
+static fcm_status evaluate_plan4(const Variant& v, const Geom& g, const fcm_hw_desc& hw, fcm_plan_t* p) {
+  const int e = g.elt;
+  if (g.layout != FCM_NHWC) return fail(FCM_EUNSUPPORTED, "plan: the register kernel needs NHWC");
+  if ((g.ci * e) % 4 || (g.cm * e) % 4 || g.co % 4)
+    return fail(FCM_EUNSUPPORTED, "plan: the register kernel needs 4-byte channel rows and output channels in fours");
+  if (g.ci * e > 64 * v.ks || g.co > v.max_cob)
+    return fail(FCM_EUNSUPPORTED, "plan: channels exceed what the kernel variant holds in registers");
+  if (p->tile_h != 1 || p->tile_w != v.max_p || p->c_block != 64 / e || p->co_block != round_up(g.co, 16))
+    return fail(FCM_EUNSUPPORTED, "plan: tiling not implemented by the kernel variant");
+  const int64_t npix = (int64_t)g.n * g.h * g.w;
+  if ((npix + v.max_p) * std::max(g.ci, g.co) * (int64_t)e >= ((int64_t)1 << 40) || npix + v.max_p >= (1 << 30))
+    return fail(FCM_EUNSUPPORTED, "plan: tensor too large");
+  const int64_t npg = pixel_groups4(v, g);
+  const int nch = ceil_div(g.cm * e, 64);
+  const int splits = std::max(1, (int)p->splits);
+  if (splits != 1 && splits != 2 && splits != 4)
+    return fail(FCM_EUNSUPPORTED, "plan: the register kernel splits over 1, 2 or 4 waves");
+  if (splits > nch) return fail(FCM_EUNSUPPORTED, "plan: more splits than intermediate channel chunks");
+  const int lds = lds_bytes4(v, g, splits);
+  if (lds > hw.lds_per_wg) return fail(FCM_EUNSUPPORTED, "plan: partial sums exceed the LDS per workgroup");
+  const int64_t grid = ceil_div(npg, (int64_t)(4 / splits));
+  if (grid > 0x7fffffff) return fail(FCM_EUNSUPPORTED, "plan: grid too large");
+  // bytes: x and y once, both weight matrices once per pixel group (Eq. 1 style: every
+  // output tile convolves with all filters)
+  const int64_t w_el = (int64_t)g.cm * g.ci + (int64_t)g.co * g.cm;
+  const int64_t xy_el = npix * (g.ci + g.co);
+  p->bytes_ideal = (xy_el + w_el) * e;
+  p->bytes_paper = (xy_el + npg * w_el) * e;
+  p->bytes_tiled = p->bytes_paper;
+  p->redundancy = 0.0;
+  p->workgroups = (int32_t)grid;
+  p->depth = 0;
+  p->splits = splits;
+  p->waves = 4;
+  p->lds_bytes = lds;
+  return FCM_OK;
+}
+
 fcm_status evaluate_plan(const Geom& g, const fcm_desc* d, const fcm_hw_desc& hw, fcm_plan_t* p) {
   (void)d;
   int nv = 0;
@@ -270,6 +322,7 @@ fcm_status evaluate_plan(const Geom& g, const fcm_desc* d, const fcm_hw_desc& hw
   if (p->variant < 0 || p->variant >= nv) return fail(FCM_EUNSUPPORTED, "plan: unknown kernel variant");
   const Variant& v = vs[p->variant];
   if (!variant_matches(v, g)) return fail(FCM_EUNSUPPORTED, "plan: kernel variant does not implement this module");
+  if (v.gen == 4) return evaluate_plan4(v, g, hw, p);
   int depth = v.gen == 3 ? p->depth : 0;
   const int lds = tiling_lds(v, g, p->tile_h, p->tile_w, p->c_block, p->co_block, hw.lds_per_wg, &depth);
   if (lds <= 0) return fail(FCM_EUNSUPPORTED, "plan: tiling not implemented by the kernel variant");
@@ -279,7 +332,7 @@ fcm_status evaluate_plan(const Geom& g, const fcm_desc* d, const fcm_hw_desc& hw
   const int64_t wgs = (int64_t)g.n * nty * ntx * ceil_div(last, p->co_block);
   if (wgs <= 0 || wgs > 0x7fffffff) return fail(FCM_EUNSUPPORTED, "plan: grid too large");
   const Bytes b = module_bytes(g, p->tile_h, p->tile_w, p->co_block);
-  if (v.gen != 3 && p->splits > 1) return fail(FCM_EUNSUPPORTED, "plan: only the persistent kernels split");
+  if (v.gen != 3 && p->splits > 1) return fail(FCM_EUNSUPPORTED, "plan: this kernel variant does not split");
   if (v.gen == 3) {
     const int splits = p->splits > 1 ? p->splits : 1;
     if (splits > 1) {
@@ -396,6 +449,38 @@ static double persistent_time_estimate(const Variant& v, const Geom& g, const fc
   return std::max(t_pipe, t_mem) + 1e-3 * t_pipe;
 }
 
+// Time model of the PW -> PW register kernel (gen 4), in seconds: each wave runs its
+// chunks one after another, each chunk costing its operand loads (1 KiB per 16-byte-per-
+// lane load, the CU's cache port shared by the resident waves), its MFMAs and a memory
+// latency that the resident waves overlap; splitting a pixel group's chunks over waves
+// adds the LDS exchange of the partial sums.
+static double pwpw4_time_estimate(const Variant& v, const Geom& g, const fcm_plan_t& p, const fcm_hw_desc& hw) {
+  constexpr double kLat = 900.0;       // cycles of memory latency per chunk
+  constexpr double kPerLoad = 16.0;    // cycles per 1 KiB operand load (cache port)
+  constexpr double kPerMfma = 16.0;    // cycles per 16x16 MFMA step
+  constexpr double kResident = 8.0;    // waves resident per CU
+  constexpr double kLaunch = 7000.0;   // cycles of launch and drain
+  constexpr double kReduce = 400.0;    // cycles: partial sums through LDS and the barrier
+  constexpr double kClock = 2.4e9;
+  const int e = g.elt;
+  const int pb = v.max_p / 16;
+  const int tpc = 4 / e;
+  const int ks = ceil_div(g.ci * e, 64), ct = ceil_div(g.co, 16);
+  const int nch = ceil_div(g.cm * e, 64);
+  const int splits = std::max(1, (int)p.splits);
+  const int cu = ceil_div(nch, splits);                                  // chunks of the busiest wave
+  const double loads = tpc * ks + ct + (e == 1 ? 4 : 2);                 // + bias
+  const double mfmas = (double)pb * (tpc * ks + ct) * (e == 4 ? 4 : 1);
+  const double waves = 4.0 * std::max(1, (int)p.workgroups);
+  const double per_cu = std::max(1.0, waves / hw.num_cus);               // waves per CU over the launch
+  const double issue = kPerLoad * loads + kPerMfma * mfmas;              // one wave, one chunk
+  const double lat_bound = std::ceil(per_cu / kResident) * cu * (kLat + issue);
+  const double thr_bound = per_cu * cu * issue;
+  double cyc = kLaunch + std::max(lat_bound, thr_bound);
+  if (splits > 1) cyc += kReduce + kPerLoad * pb * ct;
+  return cyc / kClock;
+}
+
 struct Cand {
   fcm_plan_t p;
   int64_t bytes;
@@ -429,7 +514,29 @@ static fcm_status search(const Geom& g, const fcm_desc* d, const fcm_hw_desc& hw
   for (int vi = 0; vi < nv; ++vi) {
     const Variant& v = vs[vi];
     if (!variant_matches(v, g)) continue;
-    if (v.gen == 2 && !allow_dma) continue;
+    if (v.gen >= 2 && !allow_dma) continue;
+    if (v.gen == 4) {
+      const int nch = ceil_div(g.cm * g.elt, 64);
+      for (int sp = 1; sp <= std::min(4, nch); sp *= 2) {
+        Cand c;
+        memset(&c.p, 0, sizeof(c.p));
+        c.p.op = g.op;
+        c.p.tile_h = 1;
+        c.p.tile_w = v.max_p;
+        c.p.c_block = 64 / g.elt;
+        c.p.co_block = round_up(g.co, 16);
+        c.p.variant = vi;
+        c.p.splits = sp;
+        if (evaluate_plan(g, d, hw, &c.p) != FCM_OK) continue;
+        c.bytes = c.p.bytes_tiled;
+        c.wgs = c.p.workgroups;
+        c.lds = 0;
+        c.area = v.max_p;
+        c.cap = v.max_cob * 1024 + v.ks;
+        cands.push_back(c);
+      }
+      continue;
+    }
     std::vector<int> cbs;
     if (v.gen == 2) {
       cbs = {64 / g.elt};
@@ -498,6 +605,24 @@ static fcm_status search(const Geom& g, const fcm_desc* d, const fcm_hw_desc& hw
     }
   }
   if (cands.empty()) return fail(FCM_EUNSUPPORTED, "plan: no compiled kernel implements this shape");
+  // The PW -> PW register kernel (gen 4) is preferred wherever one implements the shape:
+  // the plan with the least estimated time, ties to the smaller variant.
+  {
+    const Cand* best4 = nullptr;
+    double best_t = 0;
+    for (const Cand& c : cands) {
+      if (vs[c.p.variant].gen != 4) continue;
+      const double t = pwpw4_time_estimate(vs[c.p.variant], g, c.p, hw);
+      if (!best4 || t < best_t || (t == best_t && c.cap < best4->cap)) {
+        best4 = &c;
+        best_t = t;
+      }
+    }
+    if (best4) {
+      *best_out = best4->p;
+      return FCM_OK;
+    }
+  }
   // The persistent kernels (gen 3) are preferred wherever one implements the shape; among
   // them the tiling with the least estimated time wins (see persistent_time_estimate).
   {

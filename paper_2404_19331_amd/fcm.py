@@ -6,7 +6,7 @@ descriptor, allocates the output tensor with torch when none is given, and calls
 library. There is no fallback: if libfcm.so is missing or cannot load, importing the
 binding's functions raises.
 
-Entry points mirror the C ABI: dw_pw, pw_dw, pw_dw_pw, dw, pw, plan, plan_evaluate.
+Entry points mirror the C ABI: dw_pw, pw_dw, pw_pw, pw_dw_pw, dw, pw, plan, plan_evaluate.
 Tensors: x is [n, c, h, w] (layout="nchw") or [n, h, w, c] (layout="nhwc");
 depthwise weights [c, k, k] (or [c, 1, k, k]); pointwise weights [c_out, c_in]
 (or [c_out, c_in, 1, 1]); biases float32 (float paths) or int32 (int8) or None.
@@ -69,12 +69,18 @@ _lib = None
 
 
 def lib():
-    """Load libfcm.so (raises if it has not been built)."""
+    """Load libfcm.so (raises if it has not been built).
+
+    torch is imported first: its ROCm build carries its own HIP and HSA runtimes, and
+    libfcm.so must bind to those already-loaded copies. Loaded the other way round, the
+    process ends up with two HIP runtimes, and the one libfcm.so uses finds no device
+    once torch's has opened it."""
     global _lib
     if _lib is None:
         if not os.path.exists(LIB_PATH):
             raise FcmError(-1, "libfcm.so not found at %s; build it with "
                                "`python -m paper_2404_19331_amd.build`" % LIB_PATH)
+        import torch  # noqa: F401  (see above)
         L = ctypes.CDLL(LIB_PATH)
         vp, dp, pp = ctypes.c_void_p, ctypes.POINTER(Desc), ctypes.POINTER(Plan)
         hp = ctypes.POINTER(HwDesc)

@@ -7,6 +7,8 @@ with the documented status codes. Nothing here launches a kernel."""
 import ctypes
 import os
 import re
+import subprocess
+import sys
 
 import pytest
 
@@ -83,7 +85,12 @@ def test_plan_every_layer(wl, case):
            "pw": "k_pw"}[case.op]
     assert name.startswith(fam), name
     assert 1 <= p.tile_h and 1 <= p.tile_w and p.co_block >= 1 and p.c_block >= 1
-    assert 0 < p.lds_bytes <= 160 * 1024
+    if name.startswith("k_pwpw4"):  # registers; LDS only for the partial sums of split waves
+        assert p.tile_h == 1 and p.tile_w in (16, 32) and p.splits in (1, 2, 4)
+        assert p.splits <= -(-case.c_mid * ELT[case.dtype] // 64)
+        assert p.lds_bytes == (4 * (p.tile_w // 16) * -(-case.c_out // 16) * 1024 if p.splits > 1 else 0)
+    else:
+        assert 0 < p.lds_bytes <= 160 * 1024
     assert p.workgroups >= 1 and p.waves == 4
     assert p.bytes_tiled >= p.bytes_ideal > 0
     if name.endswith(">") and re.match(r"k_\w+3<", name):  # persistent kernels
@@ -192,3 +199,57 @@ def test_pw_pw_byte_model_closed_forms(wl, case):
     w = case.c_mid * case.c_in + case.c_out * case.c_mid
     assert p.bytes_ideal == px * (case.c_in + case.c_out) + w
     assert p.bytes_lbl_ideal == p.bytes_ideal + 2 * px * case.c_mid
+
+
+def _v4_variant(dt, prefix):
+    for v in range(fcm.lib().fcm_variant_count()):
+        if fcm.variant_name(v).startswith("k_pwpw4<%s,%s" % (dt, prefix)):
+            return v
+    raise AssertionError(prefix)
+
+
+def test_register_kernel_plan_checks():
+    d = fcm.make_desc(2, 14, 14, 64, 384, 64, k=1, stride=1, pad=0, dtype="i8", layout="nhwc",
+                      act=("relu", "none", "none"))
+    v = _v4_variant("i8", "1,4,1")
+    npg = -(-2 * 14 * 14 // 16)
+    for s, wgs in ((1, -(-npg // 4)), (2, -(-npg // 2)), (4, npg)):
+        p = fcm.plan_evaluate("pw_pw", d, 1, 16, 64, 64, v, splits=s)
+        assert (p.splits, p.workgroups) == (s, wgs)
+        assert p.lds_bytes == (4 * 4 * 1024 if s > 1 else 0)
+    assert p.bytes_ideal == (2 * 14 * 14 * 128 + 2 * 64 * 384)
+    assert p.bytes_paper == p.bytes_tiled == 2 * 14 * 14 * 128 + npg * 2 * 64 * 384
+    bad = [dict(splits=3), dict(splits=8),       # one workgroup: 1, 2 or 4 waves per pixel group
+           dict(tile_w=32), dict(co_block=128)]  # the variant's tiling is fixed
+    for kw in bad:
+        a = dict(tile_h=1, tile_w=16, c_block=64, co_block=64, splits=1)
+        a.update(kw)
+        with pytest.raises(fcm.FcmError) as e:
+            fcm.plan_evaluate("pw_pw", d, a["tile_h"], a["tile_w"], a["c_block"], a["co_block"], v,
+                              splits=a["splits"])
+        assert e.value.status == EUNSUPPORTED
+    # more splits than intermediate chunks (64 channels: one chunk)
+    d1 = fcm.make_desc(2, 14, 14, 64, 64, 64, k=1, stride=1, pad=0, dtype="i8", layout="nhwc")
+    with pytest.raises(fcm.FcmError):
+        fcm.plan_evaluate("pw_pw", d1, 1, 16, 64, 64, v, splits=2)
+    # too many input channels for one k-step, output channels not in fours, NCHW
+    for kw in (dict(c_in=80), dict(c_out=62), dict(layout="nchw")):
+        a = dict(n=2, h=14, w=14, c_in=64, c_mid=384, c_out=64, k=1, stride=1, pad=0, dtype="i8", layout="nhwc")
+        a.update(kw)
+        dd = fcm.make_desc(**a)
+        with pytest.raises(fcm.FcmError) as e:
+            fcm.plan_evaluate("pw_pw", dd, 1, 16, 64, -(-a["c_out"] // 16) * 16, v)
+        assert e.value.status == EUNSUPPORTED
+        # the planner still finds a kernel (the first-generation one where the register kernel cannot run)
+        assert fcm.plan("pw_pw", dd).variant >= 0
+
+
+def test_library_binds_to_the_hip_runtime_torch_loads():
+    # torch's ROCm build ships its own HIP runtime; libfcm.so loaded before torch would
+    # pull in a second one, which finds no device once torch's has opened it
+    code = ("from paper_2404_19331_amd import fcm; fcm.lib(); import torch; "
+            "m = open('/proc/self/maps').read().splitlines(); "
+            "print(len({l.split()[-1] for l in m if 'libamdhip64' in l}))")
+    out = subprocess.run([sys.executable, "-c", code], cwd=ROOT, capture_output=True, text=True, timeout=300)
+    assert out.returncode == 0, out.stderr
+    assert out.stdout.strip().splitlines()[-1] == "1"

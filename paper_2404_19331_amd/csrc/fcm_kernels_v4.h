@@ -1,7 +1,7 @@
 // fcm_kernels_v4.h -- PW -> PW module for gfx950 with the intermediate handed from the
 // first pointwise convolution to the second in registers (NHWC).
 //
-// k_pwpw4<DT, KS, CT, PB>
+// k_pwpw4<DT, KS, CT, PB, VEC>
 //   A workgroup is four waves. A pixel group (PB blocks of 16 pixels) is computed against
 //   every output channel (up to 16*CT) by S = 1, 2 or 4 of them (a.splits): the
 //   intermediate is cut into chunks of 64 bytes (one MFMA k-step of the second
@@ -31,18 +31,18 @@
 
 namespace fcm {
 
-// 16 bytes of a row at byte offset off, zero beyond nbytes. vec: the row is 16-byte
-// aligned and nbytes a multiple of 16; otherwise the row is 4-byte aligned and nbytes a
-// multiple of 4, and the slot is read as four 4-byte words.
-__device__ __forceinline__ u32x4 load_slot4(const char* row, int off, int nbytes, bool vec) {
-  u32x4 v = {0u, 0u, 0u, 0u};
-  if (vec) {
-    if (off < nbytes) v = *(const u32x4*)(row + off);
-  } else {
+// 16 bytes at byte offset off of a row that starts at row_off in the buffer r and has
+// nbytes valid bytes (0: no row); bytes beyond nbytes read as zero. Buffer loads return
+// zero for an offset beyond the buffer (kOob), so no lane selects or waits: the loads of a
+// whole operand set stay in flight together. vec: rows are 16-byte aligned multiples of 16
+// bytes (one 16-byte load); otherwise rows are multiples of 4 bytes (four word loads).
+template <bool VEC>
+__device__ __forceinline__ u32x4 load_slot4(rsrc_t r, uint32_t row_off, int off, int nbytes) {
+  if constexpr (VEC) return __builtin_amdgcn_raw_buffer_load_b128(r, off < nbytes ? row_off + off : kOob, 0, 0);
+  u32x4 v;
 #pragma unroll
-    for (int e = 0; e < 4; ++e)
-      if (off + 4 * e < nbytes) v[e] = *(const uint32_t*)(row + off + 4 * e);
-  }
+  for (int e = 0; e < 4; ++e)
+    v[e] = __builtin_amdgcn_raw_buffer_load_b32(r, off + 4 * e < nbytes ? row_off + off + 4 * e : kOob, 0, 0);
   return v;
 }
 
@@ -102,7 +102,9 @@ __device__ __forceinline__ void store4_out(char* p, const typename DT::AccV& acc
   }
 }
 
-template <class DT, int KS, int CT, int PB>
+// VEC: every operand row is a 16-byte aligned multiple of 16 bytes (x, both weight
+// matrices, the first bias); otherwise operands are read as 4-byte words.
+template <class DT, int KS, int CT, int PB, bool VEC>
 __global__ __launch_bounds__(256) void k_pwpw4(KArgs a) {
   using Acc = typename DT::Acc;
   using AccV = typename DT::AccV;
@@ -123,20 +125,20 @@ __global__ __launch_bounds__(256) void k_pwpw4(KArgs a) {
   const int ks = ceil_div(ci_b, 64);
   const int ct = ceil_div(a.Co, 16);
   const int nch = ceil_div(cm_b, 64);
-  const char* x = (const char*)a.x;
-  const char* w1 = (const char*)a.w1;
-  const char* w2 = (const char*)a.w2;
-  const bool vx = a.vec_x, vw1 = a.vec_w1, vw2 = a.vec_w2;
+  // buffer resources (sizes below 2^31 bytes, checked by the planner)
+  const rsrc_t rx = make_rsrc(a.x, (uint32_t)npix * ci_b);
+  const rsrc_t rw1 = make_rsrc(a.w1, (uint32_t)a.Cm * ci_b);
+  const rsrc_t rw2 = make_rsrc(a.w2, (uint32_t)a.Co * cm_b);
+  const rsrc_t rb1 = make_rsrc(a.b1, a.b1 ? (uint32_t)a.Cm * 4 : 0u);
 
   // B operands of the first convolution: the group's pixels, all input channels
   u32x4 xb[PB][KS];
 #pragma unroll
   for (int pb = 0; pb < PB; ++pb) {
     const int p = (pg * PB + pb) * 16 + r16;
-    const char* row = x + (size_t)p * ci_b;
     const int nb = p < npix ? ci_b : 0;
 #pragma unroll
-    for (int s = 0; s < KS; ++s) xb[pb][s] = s < ks ? load_slot4(row, 64 * s + 16 * g, nb, vx) : u32x4{0u, 0u, 0u, 0u};
+    for (int s = 0; s < KS; ++s) xb[pb][s] = load_slot4<VEC>(rx, (uint32_t)p * ci_b, 64 * s + 16 * g, nb);
   }
 
   AccV acc2[PB][CT];
@@ -146,34 +148,48 @@ __global__ __launch_bounds__(256) void k_pwpw4(KArgs a) {
     for (int u = 0; u < CT; ++u) acc2[pb][u] = AccV{0, 0, 0, 0};
 
   const Epi3 e1 = make_epi3(a.act[0], a.rq[0]);
-#pragma unroll 1
-  for (int c = active ? j : nch; c < nch; c += S) {
-    const int m0 = c * (64 / E);
+  // operands of one intermediate chunk: the first convolution's weight rows (permuted,
+  // see above), the chunk's slice of the second convolution's weights, the first bias
+  struct Ops {
     u32x4 a1[TPC][KS];
+    u32x4 a2[CT];
+    Acc b1[TPC][4];
+  };
+  // Every load and MFMA is issued whatever the shape (k-steps beyond the input channels
+  // and tiles beyond the output channels read zeros and add zeros): with a fixed count of
+  // loads per chunk the compiler's memory-counter waits let the next chunk's loads stay
+  // in flight during this chunk's MFMAs.
+  auto load_ops = [&](Ops& o, int c) {
+    const int m0 = c * (64 / E);
 #pragma unroll
     for (int t = 0; t < TPC; ++t) {
       const int ch = m0 + CPG * (r16 >> 2) + 4 * t + (r16 & 3);
-      const char* row = w1 + (size_t)ch * ci_b;
       const int nb = ch < a.Cm ? ci_b : 0;
 #pragma unroll
-      for (int s = 0; s < KS; ++s)
-        a1[t][s] = s < ks ? load_slot4(row, 64 * s + 16 * g, nb, vw1) : u32x4{0u, 0u, 0u, 0u};
+      for (int s = 0; s < KS; ++s) o.a1[t][s] = load_slot4<VEC>(rw1, (uint32_t)ch * ci_b, 64 * s + 16 * g, nb);
     }
-    u32x4 a2[CT];
 #pragma unroll
     for (int u = 0; u < CT; ++u) {
       const int co = 16 * u + r16;
       const int nb = (u < ct && co < a.Co) ? cm_b : 0;
-      a2[u] = load_slot4(w2 + (size_t)(co < a.Co ? co : 0) * cm_b, 64 * c + 16 * g, nb, vw2);
+      o.a2[u] = load_slot4<VEC>(rw2, (uint32_t)co * cm_b, 64 * c + 16 * g, nb);
     }
-    Acc b1[TPC][4];
+    // bias of channels m0 + CPG*g + 4t + [0, 4): 16 contiguous bytes per t (Cm % 4 == 0)
 #pragma unroll
-    for (int t = 0; t < TPC; ++t)
+    for (int t = 0; t < TPC; ++t) {
+      const int ch = m0 + CPG * g + 4 * t;
+      const u32x4 bv = load_slot4<VEC>(rb1, 0u, ch * 4, a.b1 ? a.Cm * 4 : 0);
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int ch = m0 + CPG * g + 4 * t + v;
-        b1[t][v] = ch < a.Cm ? load_bias<DT>(a.b1, ch) : Acc(0);
+      for (int q = 0; q < 4; ++q) {
+        const uint32_t w = bv[q];
+        o.b1[t][q] = __builtin_bit_cast(Acc, w);
       }
+    }
+    // keep the whole set issued here: a load the scheduler sank past the next chunk's
+    // loads would make this chunk's arithmetic wait for those as well
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  auto compute = [&](const Ops& o) {
 #pragma unroll
     for (int pb = 0; pb < PB; ++pb) {
       u32x4 mid = {0u, 0u, 0u, 0u};
@@ -181,13 +197,31 @@ __global__ __launch_bounds__(256) void k_pwpw4(KArgs a) {
       for (int t = 0; t < TPC; ++t) {
         AccV acc1 = AccV{0, 0, 0, 0};
 #pragma unroll
-        for (int s = 0; s < KS; ++s)
-          if (s < ks) mma16(DT(), acc1, a1[t][s], xb[pb][s]);
-        Mid4<DT>::put(mid, t, acc1, b1[t], e1);
+        for (int s = 0; s < KS; ++s) mma16(DT(), acc1, o.a1[t][s], xb[pb][s]);
+        Mid4<DT>::put(mid, t, acc1, o.b1[t], e1);
       }
 #pragma unroll
-      for (int u = 0; u < CT; ++u)
-        if (u < ct) mma16(DT(), acc2[pb][u], a2[u], mid);
+      for (int u = 0; u < CT; ++u) mma16(DT(), acc2[pb][u], o.a2[u], mid);
+    }
+  };
+  // software pipeline over the wave's chunks j, j+S, ...: the next chunk's operand loads
+  // are in flight while the current chunk's MFMAs run (two operand sets, alternating).
+  // The loads of the chunk after the last are issued too (every offset out of range,
+  // zeros, no memory traffic), so every path has the same loads outstanding.
+  if (active && j < nch) {
+    Ops o0, o1;
+    int c = j;
+    load_ops(o0, c);
+#pragma unroll 1
+    while (true) {
+      load_ops(o1, c + S);
+      compute(o0);
+      c += S;
+      if (c >= nch) break;
+      load_ops(o0, c + S);
+      compute(o1);
+      c += S;
+      if (c >= nch) break;
     }
   }
 
@@ -233,7 +267,8 @@ __global__ __launch_bounds__(256) void k_pwpw4(KArgs a) {
 
 template <class DT, int KS, int CT, int PB>
 int launch_pwpw4(const KArgs& a, int grid, void* stream) {
-  const void* fn = (const void*)k_pwpw4<DT, KS, CT, PB>;
+  const bool vec = a.vec_x && a.vec_w1 && a.vec_w2 && ((uintptr_t)a.b1 & 15) == 0;
+  const void* fn = vec ? (const void*)k_pwpw4<DT, KS, CT, PB, true> : (const void*)k_pwpw4<DT, KS, CT, PB, false>;
   const int lds = a.splits > 1 ? 4 * PB * ceil_div(a.Co, 16) * 1024 : 0;
   if (lds > 65536) {
     const hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, lds);

@@ -287,8 +287,11 @@ static fcm_status evaluate_plan4(const Variant& v, const Geom& g, const fcm_hw_d
   if (p->tile_h != 1 || p->tile_w != v.max_p || p->c_block != 64 / e || p->co_block != round_up(g.co, 16))
     return fail(FCM_EUNSUPPORTED, "plan: tiling not implemented by the kernel variant");
   const int64_t npix = (int64_t)g.n * g.h * g.w;
-  if ((npix + v.max_p) * std::max(g.ci, g.co) * (int64_t)e >= ((int64_t)1 << 40) || npix + v.max_p >= (1 << 30))
-    return fail(FCM_EUNSUPPORTED, "plan: tensor too large");
+  // buffer addressing: 32-bit byte offsets below 2^31 for x, y and both weight matrices
+  const int64_t lim = (int64_t)1 << 31;
+  if (npix * std::max(g.ci, g.co) * (int64_t)e >= lim || (int64_t)g.cm * g.ci * e >= lim ||
+      (int64_t)g.co * g.cm * e >= lim || npix + v.max_p >= (1 << 30))
+    return fail(FCM_EUNSUPPORTED, "plan: tensor too large for the register kernel");
   const int64_t npg = pixel_groups4(v, g);
   const int nch = ceil_div(g.cm * e, 64);
   const int splits = std::max(1, (int)p->splits);

@@ -35,7 +35,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="C3b32",
-                    choices=["C1", "C2", "C3b1", "C3b32", "C4", "C5", "PWPW"])
+                    choices=["C1", "C2", "C3b1", "C3b32", "C4", "C5", "PWPW", "MNV2", "MNV2bf16"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target CPU-baseline sample time")
     ap.add_argument("--layers", default=None, help="comma-separated layer indices (subset)")
@@ -259,6 +259,71 @@ def load_traffic(workload, kernel_name):
     return ent.get("bytes_per_launch")
 
 
+def bench_chain(a, torch, fcm):
+    """End-to-end MobileNetV2 body (51 DW/PW layers after the stem, batch 32, NHWC): the
+    chain planned by least Eq. 1-4 bytes, by least modelled time and layer by layer, each
+    run through fcm_chain_run; a step is one pass of the whole chain over one batch."""
+    import numpy as np
+    from paper_2404_19331_amd.workloads import mobilenetv2_chain, make_chain_inputs
+    dtype = "bf16" if a.workload == "MNV2bf16" else "i8"
+    spec = mobilenetv2_chain(n=32, dtype=dtype)
+    x, ws, bs = make_chain_inputs(spec)
+
+    def dev(v):
+        if v is None:
+            return None
+        if v.dtype == np.uint16:
+            return torch.from_numpy(v.view(np.int16).copy()).view(torch.bfloat16).cuda()
+        return torch.from_numpy(v).cuda()
+
+    xd, wd, bd = dev(x), [dev(w) for w in ws], [dev(b) for b in bs]
+    nsets = max(2, -(-ROTATE_BYTES // (xd.numel() * xd.element_size())))
+    xs = [xd] + [xd.clone() for _ in range(nsets - 1)]
+    d = fcm.chain_desc(spec.n, spec.h, spec.w, spec.c, spec.layers, spec.dtype, spec.layout)
+    stream = torch.cuda.current_stream()
+    res = {}
+    for obj in ("time", "bytes", "unfused"):
+        p = fcm.chain_plan(d, obj)
+        calls = [fcm.chain_run(d, p, xv, wd, bd, prepare=True) for xv in xs]
+        for k in range(a.warmup):
+            calls[k % nsets]()
+        torch.cuda.synchronize()
+        t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        _preroll(torch)
+        t0.record(stream)
+        for k in range(a.steps):
+            calls[k % nsets]()
+        t1.record(stream)
+        torch.cuda.synchronize()
+        ms = t0.elapsed_time(t1) / a.steps
+        ideal = sum(int(p.plan[g].bytes_ideal) for g in range(p.num_groups))
+        res[obj] = {"ms_per_step": round(ms, 4), "images_per_s": round(spec.n / (ms * 1e-3), 1),
+                    "groups": int(p.num_groups), "fused_layers": int(p.fused_layers),
+                    "bytes_paper": int(p.bytes_paper), "bytes_ideal": ideal,
+                    "gbs": round(ideal / (ms * 1e-3) / 1e9, 1), "time_est_ms": round(p.time_est * 1e3, 4),
+                    "ops": [op for _, op, _ in p.groups()]}
+        print("bench: chain %s plan %.3f ms (%d groups)" % (obj, ms, p.num_groups), file=sys.stderr, flush=True)
+    best = res["time"]
+    out = {
+        "metric": "MobileNetV2 body end-to-end images/s (chain FusePlanner) vs layer-by-layer",
+        "value": best["images_per_s"],
+        "unit": "images/s",
+        "n_gpus": 1, "steps": a.steps, "warmup": a.warmup,
+        "ms_per_step": best["ms_per_step"],
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": dtype, "data": "synthetic (seeded, random-init weights)",
+        "config": {"workload": spec.name, "name": a.workload, "layers": len(spec.layers), "batch": spec.n,
+                   "layout": spec.layout, "parallelism": "none (1 GPU)"},
+        "chains": res,
+        "speedup_vs_unfused": round(res["unfused"]["ms_per_step"] / best["ms_per_step"], 3),
+        "roofline": {"bound": "hbm", "achieved": best["gbs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(best["gbs"] / HBM_PEAK_GBS, 4), "kernel": "whole chain", "traffic": None},
+        "cpu_baseline": None,
+    }
+    print(json.dumps(out), flush=True)
+    return 0
+
+
 def main():
     a = parse()
     if a.gpus != 1:
@@ -272,6 +337,8 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     fcm.lib()
+    if a.workload.startswith("MNV2"):
+        return bench_chain(a, torch, fcm)
     cases, desc = workload_cases(a.workload)
     if a.layers:
         keep = [int(i) for i in a.layers.split(",")]

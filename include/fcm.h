@@ -56,8 +56,9 @@
 extern "C" {
 #endif
 
-/* Device memory the library allocates once per device for split plans (partial sums
- * and arrival counters); plans whose workspace would exceed it are not split. */
+/* Device memory the library allocates once per device for split plans of the persistent
+ * DW->PW and PW kernels (their partial sums); plans whose partial sums would exceed it
+ * are not split. */
 #define FCM_SPLIT_WORKSPACE_BYTES (64u << 20)
 
 typedef enum {
@@ -97,6 +98,7 @@ typedef struct {
  *   fcm_dw_pw:    c_in channels -> DW -> PW -> c_out          (c_mid must equal c_in)
  *   fcm_pw_dw:    c_in -> PW -> c_mid -> DW                   (c_out must equal c_mid)
  *   fcm_pw_dw_pw: c_in -> PW -> c_mid -> DW -> PW -> c_out
+ *   fcm_pw_pw:    c_in -> PW -> c_mid -> PW -> c_out on the h x w grid (k, stride, pad ignored)
  *   fcm_dw:       c_in channels, uses act[0], rq[0]
  *   fcm_pw:       c_in -> c_out on the h x w grid (k, stride, pad ignored), act[0], rq[0] */
 typedef struct {
@@ -146,7 +148,10 @@ typedef struct {
                             work tile are split over this many workgroups; each writes its
                             partial sums to the library's workspace and a second kernel
                             adds them in split order, then applies bias, activation and
-                            cast (1 = no split; 0 on input to fcm_plan_evaluate = 1) */
+                            cast. PW->PW register kernel: 1, 2 or 4 waves of a workgroup
+                            share a pixel group's intermediate chunks and add their partial
+                            sums through LDS in wave order (no workspace).
+                            1 = no split; 0 on input to fcm_plan_evaluate = 1 */
   int64_t bytes_ideal;          /* input + weights + output, each once                  */
   int64_t bytes_tiled;          /* per-workgroup loads + stores of this tiling (exact)  */
   int64_t bytes_paper;          /* Eq. 1-4 estimate of this module at this tiling        */
@@ -156,10 +161,13 @@ typedef struct {
 } fcm_plan_t;
 
 /* FusePlanner. Chooses the tiling of `op` for `desc` on `hw` (NULL = MI355X) among the
- * tilings the compiled kernels implement: minimises bytes_tiled subject to the LDS limit
- * and to #workgroups >= #CUs where any tiling reaches it (Sec. IV-A constraints),
- * ties broken by more workgroups (up to 2 per CU), then larger tiles. Host-only,
- * integer arithmetic, deterministic; results are cached per (op, desc, hw).
+ * tilings the compiled kernels implement. Where a persistent NHWC kernel (or, for PW->PW,
+ * the register kernel) implements the shape, the plan with the least time under that
+ * kernel's fitted time model wins; otherwise the plan minimises bytes_tiled subject to
+ * the LDS limit and to #workgroups >= #CUs where any tiling reaches it (Sec. IV-A
+ * constraints), ties broken by more workgroups (up to 2 per CU), then larger tiles.
+ * `fuse` is the paper's verdict: the module's Eq. 1-4 estimate against the sum of its
+ * layers' (Sec. IV-B). Host-only, deterministic; results are cached per (op, desc, hw).
  * Returns FCM_EINVAL / FCM_EUNSUPPORTED like the launch entry points. */
 fcm_status fcm_plan(int32_t op, const fcm_desc* desc, const fcm_hw_desc* hw, fcm_plan_t* out);
 
@@ -167,6 +175,10 @@ fcm_status fcm_plan(int32_t op, const fcm_desc* desc, const fcm_hw_desc* hw, fcm
  * variant) without searching: fills every other field, or fails with
  * FCM_EUNSUPPORTED if no compiled kernel implements it. */
 fcm_status fcm_plan_evaluate(const fcm_desc* desc, const fcm_hw_desc* hw, fcm_plan_t* plan);
+
+/* The planner's estimate of a plan's launch time in seconds (the fitted time model of the
+ * plan's kernel family on `hw`, NULL = MI355X), as used by FCM_CHAIN_TIME; 0 on error. */
+double fcm_plan_time_estimate(const fcm_desc* desc, const fcm_hw_desc* hw, const fcm_plan_t* plan);
 
 /* DW -> PW module: y = act1(PW(act0(DW(x) + b_dw)) + b_pw).
  *   x [n, c_in, h, w] | w_dw [c_in][k][k] | b_dw [c_in] | w_pw [c_out][c_in] |
@@ -206,6 +218,79 @@ fcm_status fcm_dw(const fcm_desc* desc, const void* x, const void* w_dw, const v
 /* Single pointwise layer (layer-by-layer baseline): y [n, c_out, h, w]. */
 fcm_status fcm_pw(const fcm_desc* desc, const void* x, const void* w_pw, const void* b_pw,
                   void* y, const fcm_plan_t* plan, void* stream);
+
+/* ------------------------------------------------------------------------------------
+ * Chains of layers: FusePlanner over a network (Sec. IV: FCMs and layer-by-layer kernels
+ * "used to derive complete CNN execution plans"; Sec. V reports the share of conv layers
+ * fused in whole models).
+ *
+ * A chain is a sequence of DW and PW layers, each consuming the previous layer's output
+ * (no skip connections). fcm_chain_plan partitions it into groups, each run as one
+ * kernel: a single layer (fcm_dw / fcm_pw) or a fused module over adjacent layers
+ * (DW->PW, PW->DW, PW->PW, PW->DW->PW). Every candidate group is planned with fcm_plan;
+ * dynamic programming over the chain picks the partition of least total cost. With
+ * FCM_CHAIN_BYTES the cost is the paper's global-memory-access estimate (bytes_paper,
+ * Eq. 1-4), so a pair is fused exactly when the module's estimate is below the sum of
+ * its layers' (Sec. IV-B), applied to the whole chain at once; ties keep layers apart.
+ * FCM_CHAIN_TIME uses the fitted time models of the kernels the plans launch (plans of
+ * kernels without one: their bytes at the HBM rate plus a launch). FCM_CHAIN_UNFUSED
+ * runs every layer alone (the layer-by-layer baseline).
+ * ------------------------------------------------------------------------------------ */
+
+#define FCM_CHAIN_MAX_LAYERS 128
+
+typedef enum { FCM_LAYER_DW = 0, FCM_LAYER_PW = 1 } fcm_layer_kind;
+typedef enum { FCM_CHAIN_BYTES = 0, FCM_CHAIN_TIME = 1, FCM_CHAIN_UNFUSED = 2 } fcm_chain_objective;
+
+/* One layer: conv -> +bias -> act -> cast (int8: requantised by rq). */
+typedef struct {
+  int32_t kind;            /* fcm_layer_kind */
+  int32_t c_out;           /* PW: output channels; DW: ignored (equals its input channels) */
+  int32_t k, stride, pad;  /* DW geometry (as fcm_desc); ignored for PW */
+  int32_t act;             /* fcm_act */
+  fcm_requant rq;          /* FCM_I8 only */
+} fcm_layer;
+
+typedef struct {
+  int32_t n, h, w, c;      /* input of the first layer */
+  int32_t dtype;           /* fcm_dtype, the whole chain */
+  int32_t layout;          /* fcm_layout, the whole chain */
+  int32_t num_layers;      /* 1 .. FCM_CHAIN_MAX_LAYERS */
+  fcm_layer layers[FCM_CHAIN_MAX_LAYERS];
+} fcm_chain_desc;
+
+typedef struct {
+  int32_t objective;                      /* fcm_chain_objective it was made for */
+  int32_t num_groups;
+  int32_t first[FCM_CHAIN_MAX_LAYERS];    /* first layer of group g */
+  int32_t op[FCM_CHAIN_MAX_LAYERS];       /* fcm_op of group g (its layers: first[g] ..) */
+  fcm_plan_t plan[FCM_CHAIN_MAX_LAYERS];  /* plan of group g */
+  int32_t fused_layers;                   /* layers that run inside fused modules */
+  int64_t act_bytes_max;                  /* largest activation passed between groups */
+  int64_t bytes_paper, bytes_lbl_paper;   /* Eq. 1-4 totals: this partition, every layer alone */
+  double time_est, time_lbl_est;          /* time-model totals (seconds), same two */
+} fcm_chain_plan_t;
+
+/* Plan a chain (hw: NULL = MI355X). Fails with FCM_EINVAL for an invalid chain (sizes,
+ * geometry, requantisation, as the single-layer entry points) and FCM_EUNSUPPORTED if
+ * some layer has no compiled kernel at all. Host-only, deterministic. */
+fcm_status fcm_chain_plan(const fcm_chain_desc* chain, int32_t objective, const fcm_hw_desc* hw,
+                          fcm_chain_plan_t* out);
+
+/* Device bytes fcm_chain_run needs in `workspace` for `plan` (two activation buffers,
+ * each aligned to 256 bytes; 0 when the chain is one group). */
+int64_t fcm_chain_workspace_bytes(const fcm_chain_plan_t* plan);
+
+/* Run a planned chain on `stream`: x is the chain input, y the last layer's output
+ * (shapes from the chain and each layer's geometry, layout chain->layout); weights[i],
+ * biases[i] belong to layer i (canonical layouts as the single-layer entry points;
+ * biases[i] may be NULL). `workspace` (device, fcm_chain_workspace_bytes(plan) bytes,
+ * caller-owned, may be NULL when that is 0) holds the activations between groups. The
+ * library allocates nothing beyond what the groups' own plans need (split workspace).
+ * Errors are those of the group launches; a failing group stops the chain. */
+fcm_status fcm_chain_run(const fcm_chain_desc* chain, const fcm_chain_plan_t* plan, const void* x,
+                         const void* const* weights, const void* const* biases, void* workspace, void* y,
+                         void* stream);
 
 /* Human-readable name of a status code (static storage). */
 const char* fcm_status_string(fcm_status status);

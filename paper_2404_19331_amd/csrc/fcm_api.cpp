@@ -309,6 +309,12 @@ fcm_status fcm_plan_evaluate(const fcm_desc* desc, const fcm_hw_desc* hw, fcm_pl
   return FCM_OK;
 }
 
+double fcm_plan_time_estimate(const fcm_desc* desc, const fcm_hw_desc* hw, const fcm_plan_t* plan) {
+  if (!plan || validate(plan->op, desc) != FCM_OK) return 0.0;
+  const fcm_hw_desc H = hw ? *hw : default_hw();
+  return plan_time_estimate(geometry(plan->op, desc), *plan, H);
+}
+
 fcm_status fcm_dw_pw(const fcm_desc* desc, const void* x, const void* w_dw, const void* b_dw, const void* w_pw,
                      const void* b_pw, void* y, const fcm_plan_t* plan, void* stream) {
   Tensors t = {x, {w_dw, w_pw, nullptr}, {b_dw, b_pw, nullptr}, y};
@@ -338,6 +344,46 @@ fcm_status fcm_pw_pw(const fcm_desc* desc, const void* x, const void* w_pw1, con
                      const void* b_pw2, void* y, const fcm_plan_t* plan, void* stream) {
   Tensors t = {x, {w_pw1, w_pw2, nullptr}, {b_pw1, b_pw2, nullptr}, y};
   return run(FCM_OP_PW_PW, desc, t, plan, stream);
+}
+
+fcm_status fcm_chain_run(const fcm_chain_desc* chain, const fcm_chain_plan_t* plan, const void* x,
+                         const void* const* weights, const void* const* biases, void* workspace, void* y,
+                         void* stream) {
+  if (!plan) return fail(FCM_EINVAL, "chain plan is NULL");
+  if (!weights) return fail(FCM_EINVAL, "weights array is NULL");
+  std::vector<int> h(FCM_CHAIN_MAX_LAYERS + 1), w(FCM_CHAIN_MAX_LAYERS + 1), ch(FCM_CHAIN_MAX_LAYERS + 1);
+  fcm_status st = chain_shapes(chain, h.data(), w.data(), ch.data());
+  if (st != FCM_OK) return st;
+  // the plan must cover the chain exactly, group after group
+  if (plan->num_groups < 1 || plan->num_groups > chain->num_layers) return fail(FCM_EINVAL, "chain plan: bad group count");
+  std::vector<fcm_desc> descs(plan->num_groups);
+  int next = 0;
+  for (int g = 0; g < plan->num_groups; ++g) {
+    if (plan->first[g] != next || next >= chain->num_layers ||
+        chain_group_desc(chain, h.data(), w.data(), ch.data(), next, plan->op[g], &descs[g]) != FCM_OK)
+      return fail(FCM_EINVAL, "chain plan does not match the chain");
+    next += op_layers(plan->op[g]);
+  }
+  if (next != chain->num_layers) return fail(FCM_EINVAL, "chain plan does not match the chain");
+  const int64_t half = fcm_chain_workspace_bytes(plan) / 2;
+  if (plan->num_groups > 1 && !workspace) return fail(FCM_EINVAL, "chain needs a workspace");
+  const void* in = x;
+  for (int g = 0; g < plan->num_groups; ++g) {
+    const int first = plan->first[g], op = plan->op[g], nl = op_layers(op);
+    const fcm_desc& d = descs[g];
+    const int64_t e = chain->dtype == FCM_F32 ? 4 : (chain->dtype == FCM_BF16 ? 2 : 1);
+    if ((int64_t)chain->n * h[first + nl] * w[first + nl] * ch[first + nl] * e > half && g + 1 < plan->num_groups)
+      return fail(FCM_EINVAL, "chain plan's workspace size does not fit the chain");
+    void* out = g + 1 == plan->num_groups ? y : (char*)workspace + (g % 2) * half;
+    Tensors t = {in, {nullptr, nullptr, nullptr}, {nullptr, nullptr, nullptr}, out};
+    for (int i = 0; i < nl; ++i) {
+      t.w[i] = weights[first + i];
+      t.b[i] = biases ? biases[first + i] : nullptr;
+    }
+    if ((st = run(op, &d, t, &plan->plan[g], stream)) != FCM_OK) return st;
+    in = out;
+  }
+  return FCM_OK;
 }
 
 fcm_status fcm_pw(const fcm_desc* desc, const void* x, const void* w_pw, const void* b_pw, void* y,

@@ -39,4 +39,21 @@ bool variant_needs_alignment(int variant);
 
 fcm_hw_desc default_hw();
 
+// Estimated seconds of a plan's launch: the fitted time model of its kernel family where
+// there is one (persistent DW->PW / PW / DW kernels, PW->PW register kernel), else its
+// bytes at the HBM rate plus a launch.
+double plan_time_estimate(const Geom& g, const fcm_plan_t& p, const fcm_hw_desc& hw);
+
+// Chains: input shape of every layer (h[i], w[i], c[i] for layer i; index num_layers is
+// the chain output) after checking the chain's sizes and geometry.
+fcm_status chain_shapes(const fcm_chain_desc* c, int* h, int* w, int* ch);
+
+// Descriptor of the module `op` over the chain's layers first, first+1, ... (their count
+// follows from op), or FCM_EINVAL if those layers do not form that module.
+fcm_status chain_group_desc(const fcm_chain_desc* c, const int* h, const int* w, const int* ch, int first, int op,
+                            fcm_desc* d);
+
+// Number of layers a module spans.
+int op_layers(int op);
+
 }  // namespace fcm

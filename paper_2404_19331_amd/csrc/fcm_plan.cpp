@@ -484,6 +484,67 @@ static double pwpw4_time_estimate(const Variant& v, const Geom& g, const fcm_pla
   return cyc / kClock;
 }
 
+// Multiply-accumulate work of a module, counted as 2 flops each (the recomputed PW halo
+// of PW->DW is not included).
+static double module_flops(const Geom& g) {
+  const double px = (double)g.n * g.h * g.w, po = (double)g.n * g.ho * g.wo;
+  const double kk = (double)g.k * g.k;
+  switch (g.family) {
+    case FAM_DWPW: return 2.0 * po * g.ci * (kk + g.co);
+    case FAM_PWDW: return 2.0 * (px * g.ci * g.cm + po * g.cm * kk);
+    case FAM_PWDWPW: return 2.0 * (px * g.ci * g.cm + po * g.cm * (kk + g.co));
+    case FAM_PWPW: return 2.0 * px * g.cm * (g.ci + g.co);
+    case FAM_DW: return 2.0 * po * g.cm * kk;
+    default: return 2.0 * px * g.ci * g.co;  // FAM_PW
+  }
+}
+
+// Linear time models of the kernels without a structural one: microseconds =
+// c0 + per_mb * bytes_tiled/1e6 + per_gflop * flops/1e9 + per_kwg * workgroups/1e3,
+// fitted (non-negative least squares on relative error) to every candidate module of the
+// MobileNetV2 layer chain, int8 and bf16, batch 1 and 32, timed on MI355X; the fitted
+// figures are within about 0.5-1.5x of the timings. FP32 takes the bf16 figures.
+struct LinModel {
+  int family, gen, dtype;
+  double c0, per_mb, per_gflop, per_kwg;
+};
+static const LinModel kLinModels[] = {
+    {FAM_PW, 1, DT_I8, 6.56, 3.617, 0.0, 0.0},
+    {FAM_PWDW, 1, DT_BF16, 7.97, 0.0, 27.647, 12.939},
+    {FAM_PWDW, 1, DT_I8, 10.05, 0.0, 24.499, 15.288},
+    {FAM_PWDWPW, 1, DT_BF16, 21.16, 1.864, 0.0, 3.306},
+    {FAM_PWDWPW, 1, DT_I8, 33.52, 4.262, 0.0, 25.127},
+    {FAM_PWPW, 1, DT_BF16, 6.16, 0.649, 0.0, 0.0},
+    {FAM_PWPW, 1, DT_I8, 6.21, 0.822, 0.0, 0.0},
+    {FAM_PWPW, 4, DT_BF16, 3.97, 0.0, 27.116, 0.661},
+    {FAM_PWPW, 4, DT_I8, 7.01, 0.0, 14.325, 12.663},
+};
+
+static double linear_time_estimate(const Variant& v, const Geom& g, const fcm_plan_t& p) {
+  const int dt = g.dtype == DT_F32 ? DT_BF16 : g.dtype;
+  const LinModel* m = nullptr;
+  for (const LinModel& l : kLinModels)
+    if (l.family == v.family && l.gen == v.gen && l.dtype == dt) m = &l;
+  // kernels never timed for the fit: a conservative generic figure
+  static const LinModel kGeneric = {0, 0, 0, 10.0, 2.0, 25.0, 10.0};
+  if (!m) m = &kGeneric;
+  const double us = m->c0 + m->per_mb * (double)p.bytes_tiled / 1e6 + m->per_gflop * module_flops(g) / 1e9 +
+                    m->per_kwg * (double)p.workgroups / 1e3;
+  return us * 1e-6;
+}
+
+double plan_time_estimate(const Geom& g, const fcm_plan_t& p, const fcm_hw_desc& hw) {
+  int nv = 0;
+  const Variant* vs = all_variants(&nv);
+  if (p.variant < 0 || p.variant >= nv) return 0.0;
+  const Variant& v = vs[p.variant];
+  if (v.gen == 3) return persistent_time_estimate(v, g, p, hw);
+  // the register kernel's structural model ranks its own plans; for comparisons with other
+  // kernels the fitted figure bounds it from below
+  if (v.gen == 4) return std::max(pwpw4_time_estimate(v, g, p, hw), linear_time_estimate(v, g, p));
+  return linear_time_estimate(v, g, p);
+}
+
 struct Cand {
   fcm_plan_t p;
   int64_t bytes;

@@ -6,7 +6,8 @@ descriptor, allocates the output tensor with torch when none is given, and calls
 library. There is no fallback: if libfcm.so is missing or cannot load, importing the
 binding's functions raises.
 
-Entry points mirror the C ABI: dw_pw, pw_dw, pw_pw, pw_dw_pw, dw, pw, plan, plan_evaluate.
+Entry points mirror the C ABI: dw_pw, pw_dw, pw_pw, pw_dw_pw, dw, pw, plan, plan_evaluate,
+chain_desc, chain_plan, chain_run.
 Tensors: x is [n, c, h, w] (layout="nchw") or [n, h, w, c] (layout="nhwc");
 depthwise weights [c, k, k] (or [c, 1, k, k]); pointwise weights [c_out, c_in]
 (or [c_out, c_in, 1, 1]); biases float32 (float paths) or int32 (int8) or None.
@@ -65,6 +66,36 @@ class Plan(ctypes.Structure):
         return {f: getattr(self, f) for f, _ in self._fields_}
 
 
+CHAIN_MAX_LAYERS = 128
+LAYER_KIND = {"dw": 0, "pw": 1}
+OBJECTIVE = {"bytes": 0, "time": 1, "unfused": 2}
+
+
+class Layer(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int32), ("c_out", ctypes.c_int32), ("k", ctypes.c_int32),
+                ("stride", ctypes.c_int32), ("pad", ctypes.c_int32), ("act", ctypes.c_int32), ("rq", Requant)]
+
+
+class ChainDesc(ctypes.Structure):
+    _fields_ = [("n", ctypes.c_int32), ("h", ctypes.c_int32), ("w", ctypes.c_int32), ("c", ctypes.c_int32),
+                ("dtype", ctypes.c_int32), ("layout", ctypes.c_int32), ("num_layers", ctypes.c_int32),
+                ("layers", Layer * CHAIN_MAX_LAYERS)]
+
+
+class ChainPlan(ctypes.Structure):
+    _fields_ = [("objective", ctypes.c_int32), ("num_groups", ctypes.c_int32),
+                ("first", ctypes.c_int32 * CHAIN_MAX_LAYERS), ("op", ctypes.c_int32 * CHAIN_MAX_LAYERS),
+                ("plan", Plan * CHAIN_MAX_LAYERS), ("fused_layers", ctypes.c_int32),
+                ("act_bytes_max", ctypes.c_int64), ("bytes_paper", ctypes.c_int64),
+                ("bytes_lbl_paper", ctypes.c_int64), ("time_est", ctypes.c_double),
+                ("time_lbl_est", ctypes.c_double)]
+
+    def groups(self):
+        """[(first layer, op name, Plan)] of the chain's kernels in order."""
+        names = {v: k for k, v in OP.items()}
+        return [(self.first[g], names[self.op[g]], self.plan[g]) for g in range(self.num_groups)]
+
+
 _lib = None
 
 
@@ -102,6 +133,15 @@ def lib():
         L.fcm_variant_name.argtypes = [ctypes.c_int32]
         L.fcm_variant_name.restype = ctypes.c_char_p
         L.fcm_variant_count.restype = ctypes.c_int32
+        cdp, cpp = ctypes.POINTER(ChainDesc), ctypes.POINTER(ChainPlan)
+        L.fcm_chain_plan.argtypes = [cdp, ctypes.c_int32, hp, cpp]
+        L.fcm_chain_plan.restype = ctypes.c_int
+        L.fcm_chain_workspace_bytes.argtypes = [cpp]
+        L.fcm_chain_workspace_bytes.restype = ctypes.c_int64
+        L.fcm_chain_run.argtypes = [cdp, cpp, vp, ctypes.POINTER(vp), ctypes.POINTER(vp), vp, vp, vp]
+        L.fcm_chain_run.restype = ctypes.c_int
+        L.fcm_plan_time_estimate.argtypes = [dp, hp, pp]
+        L.fcm_plan_time_estimate.restype = ctypes.c_double
         _lib = L
     return _lib
 
@@ -149,6 +189,11 @@ def plan(op, desc, hw=None):
     p = Plan()
     _check(lib().fcm_plan(OP[op], ctypes.byref(desc), ctypes.byref(hw) if hw else None, ctypes.byref(p)))
     return p
+
+
+def plan_time_estimate(desc, plan, hw=None):
+    """Seconds the planner's time model gives the plan's launch (0.0 on error)."""
+    return lib().fcm_plan_time_estimate(ctypes.byref(desc), ctypes.byref(hw) if hw else None, ctypes.byref(plan))
 
 
 def plan_evaluate(op, desc, tile_h, tile_w, c_block, co_block, variant, hw=None, workgroups=0, depth=0, splits=0):
@@ -413,3 +458,77 @@ def pw_then_dw_then_pw(x, w_pw1, w_dw, w_pw2, b_pw1=None, b_dw=None, b_pw2=None,
     m2 = c2.y if prepare else c2
     c3 = pw(m2, w_pw2, b_pw2, act=act[2], rq=rq[2], layout=layout, out=out, stream=stream, prepare=prepare)
     return _Chain([c1, c2, c3]) if prepare else c3
+
+
+# ------------------------------------------------------------------------------------
+# Chains of layers (FusePlanner over a network): plan once, run every group's kernel
+# ------------------------------------------------------------------------------------
+
+def chain_desc(n, h, w, c, layers, dtype="i8", layout="nhwc"):
+    """Chain descriptor. layers: dicts with kind ("dw" | "pw"), c_out (PW), k, stride,
+    pad (DW), act ("none" | "relu" | "relu6"), rq ((mult, shift, qmin, qmax), int8)."""
+    if not 1 <= len(layers) <= CHAIN_MAX_LAYERS:
+        raise ValueError("a chain has 1 .. %d layers" % CHAIN_MAX_LAYERS)
+    d = ChainDesc()
+    d.n, d.h, d.w, d.c = n, h, w, c
+    d.dtype = DTYPE[dtype] if isinstance(dtype, str) else int(dtype)
+    d.layout = LAYOUT[layout] if isinstance(layout, str) else int(layout)
+    d.num_layers = len(layers)
+    for i, L in enumerate(layers):
+        t = d.layers[i]
+        t.kind = LAYER_KIND[L["kind"]]
+        t.c_out = int(L.get("c_out", 0))
+        t.k, t.stride, t.pad = int(L.get("k", 1)), int(L.get("stride", 1)), int(L.get("pad", 0))
+        a = L.get("act", "none")
+        t.act = ACT[a] if isinstance(a, str) else int(a)
+        r = L.get("rq") or (1, 0, -128, 127)
+        t.rq.mult, t.rq.shift, t.rq.qmin, t.rq.qmax = (int(v) for v in r)
+    return d
+
+
+def chain_plan(desc, objective="bytes", hw=None):
+    p = ChainPlan()
+    _check(lib().fcm_chain_plan(ctypes.byref(desc), OBJECTIVE[objective], ctypes.byref(hw) if hw else None,
+                                ctypes.byref(p)))
+    return p
+
+
+def chain_output_shape(desc):
+    h, w, c = desc.h, desc.w, desc.c
+    for i in range(desc.num_layers):
+        L = desc.layers[i]
+        if L.kind == LAYER_KIND["pw"]:
+            c = L.c_out
+        else:
+            h, w = out_hw(h, w, L.k, L.stride, L.pad)
+    return (desc.n, c, h, w) if desc.layout == LAYOUT["nchw"] else (desc.n, h, w, c)
+
+
+class _ChainRun(Prepared):
+    def __init__(self, fn, args, y, keep):
+        super().__init__(fn, args, y)
+        self.keep = keep  # the pointer arrays and workspace the arguments refer to
+
+
+def chain_run(desc, plan, x, weights, biases=None, *, out=None, workspace=None, stream=None, prepare=False):
+    """Run a planned chain: x the input tensor, weights/biases per layer (biases may be
+    None or hold None). The inter-group workspace is a torch allocation unless given."""
+    torch = _torch()
+    if len(weights) != desc.num_layers:
+        raise ValueError("one weight tensor per layer")
+    biases = list(biases) if biases is not None else [None] * desc.num_layers
+    _prep(x, weights, biases, _dtype_name(x))
+    shape = chain_output_shape(desc)
+    y = torch.empty(shape, dtype=x.dtype, device=x.device) if out is None else out
+    if tuple(y.shape) != shape or y.dtype != x.dtype or not y.is_contiguous():
+        raise ValueError("out must be a contiguous %s tensor of shape %s" % (x.dtype, shape))
+    nbytes = lib().fcm_chain_workspace_bytes(ctypes.byref(plan))
+    if workspace is None and nbytes > 0:
+        workspace = torch.empty(nbytes, dtype=torch.uint8, device=x.device)
+    if workspace is not None and workspace.numel() * workspace.element_size() < nbytes:
+        raise ValueError("workspace smaller than fcm_chain_workspace_bytes")
+    W = (ctypes.c_void_p * desc.num_layers)(*[t.data_ptr() for t in weights])
+    B = (ctypes.c_void_p * desc.num_layers)(*[(b.data_ptr() if b is not None else None) for b in biases])
+    args = (ctypes.byref(desc), ctypes.byref(plan), _ptr(x), W, B, _ptr(workspace), _ptr(y), _stream(x, stream))
+    r = _ChainRun(lib().fcm_chain_run, args, y, (W, B, workspace, desc, plan))
+    return r if prepare else r()

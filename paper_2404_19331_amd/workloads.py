@@ -246,6 +246,80 @@ def config_pwpw():
     return out
 
 
+# MobileNetV2 inverted-residual stages after the stem convolution (112x112x32 input):
+# (expansion t, output channels c, repeats, stride of the first block).
+MNV2_STAGES = [(1, 16, 1, 1), (6, 24, 2, 2), (6, 32, 3, 2), (6, 64, 4, 2), (6, 96, 3, 1), (6, 160, 3, 2),
+               (6, 320, 1, 1)]
+
+
+@dataclass
+class ChainSpec:
+    """A sequence of DW/PW layers (no skip connections) with its input and seed."""
+    n: int
+    h: int
+    w: int
+    c: int
+    dtype: str
+    layout: str
+    layers: list
+    seed: int = BASE_SEED
+    name: str = ""
+
+
+def mobilenetv2_chain(n=8, dtype="i8", layout="nhwc", h=112, w=112, stages=None, final_pw=True):
+    """The DW and PW layers of MobileNetV2 after its stem (51 layers at full depth): per
+    block an expansion PW (t > 1), a DW 3x3 and a linear projection PW, then the final PW
+    to 1280 channels. Float types use ReLU6 after the expansion and the DW; int8 uses ReLU
+    there (int8 ReLU6 is not supported) and requantises every layer by 2^-s, s sized to
+    the layer's accumulator spread (U{-127..127} weights, inputs of RMS about 48 or, after
+    ReLU, 34) so outputs spread over the int8 range."""
+    stages = MNV2_STAGES if stages is None else stages
+    act = "relu" if dtype == "i8" else "relu6"
+    sd_w = 127 / math.sqrt(3)
+    layers = []
+    c = 32
+    sd_in = [sd_w]  # RMS of the current int8 activations (input drawn as U{-127..127})
+
+    def rq_for(fan_in, relu):
+        s = int(round(math.log2(max(1.0, sd_in[0] * sd_w * math.sqrt(fan_in) / 48))))
+        sd_in[0] = 48 / math.sqrt(2) if relu else 48.0
+        return (1, s, -127, 127)
+
+    for t, co, reps, s0 in stages:
+        for r in range(reps):
+            if t != 1:
+                layers.append(dict(kind="pw", c_out=c * t, act=act, rq=rq_for(c, True)))
+            layers.append(dict(kind="dw", k=3, stride=s0 if r == 0 else 1, pad=1, act=act, rq=rq_for(9, True)))
+            cm = c * t
+            layers.append(dict(kind="pw", c_out=co, act="none", rq=rq_for(cm, False)))
+            c = co
+    if final_pw:
+        layers.append(dict(kind="pw", c_out=1280, act=act, rq=rq_for(c, True)))
+    return ChainSpec(n, h, w, 32, dtype, layout, layers, seed=BASE_SEED + 7,
+                     name="MobileNetV2 body %d layers %s %s b%d" % (len(layers), dtype, layout, n))
+
+
+def make_chain_inputs(spec, seed=None):
+    """Seeded input and per-layer weights/biases of a chain, storage format as make_inputs:
+    x, then for each layer its weights ([c][k][k] DW, [c_out][c_in] PW) and bias."""
+    rng = np.random.default_rng(spec.seed if seed is None else seed)
+    case = Case("pw", spec.n, spec.h, spec.w, spec.c, spec.c, spec.c, 1, 1, 0, spec.dtype, spec.layout,
+                dist_x="i8" if spec.dtype == "i8" else "n01", dist_w="i8", bias=True)
+    x = _draw_x(rng, case)
+    ws, bs = [], []
+    c = spec.c
+    for L in spec.layers:
+        if L["kind"] == "dw":
+            k = L["k"]
+            ws.append(_draw_w(rng, case, (c, k, k), k * k))
+            bs.append(_draw_b(rng, case, c))
+        else:
+            ws.append(_draw_w(rng, case, (L["c_out"], c), c))
+            bs.append(_draw_b(rng, case, L["c_out"]))
+            c = L["c_out"]
+    return x, ws, bs
+
+
 CONFIGS = {"C1": config_c1, "C2": config_c2, "C3": config_c3, "C4": config_c4, "C5": config_c5}
 
 

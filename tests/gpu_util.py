@@ -122,3 +122,29 @@ def batch_slice(inp, idx):
     out = dict(inp)
     out["x"] = np.ascontiguousarray(inp["x"][idx])
     return out
+
+
+def oracle_chain(spec, x, ws, bs, upto=None):
+    """The chain on the CPU oracle, one layer at a time (definition of the chain)."""
+    h, w, c = spec.h, spec.w, spec.c
+    for i, L in enumerate(spec.layers[:upto]):
+        k, s, p = (L["k"], L["stride"], L["pad"]) if L["kind"] == "dw" else (1, 1, 0)
+        co = c if L["kind"] == "dw" else L["c_out"]
+        case = dict(n=spec.n, h=h, w=w, c_in=c, c_mid=c, c_out=co, k=k, stride=s, pad=p, dtype=spec.dtype,
+                    layout=spec.layout, act=[L["act"], "none", "none"],
+                    rq=[list(L.get("rq") or (1, 0, -128, 127))] * 3)
+        if L["kind"] == "dw":
+            x = oracle.dw(case, x, ws[i], bs[i])
+            h, w = fcm.out_hw(h, w, k, s, p)
+        else:
+            x = oracle.pw(case, x, ws[i], bs[i])
+            c = co
+    return x
+
+
+def run_chain(spec, objective, x, ws, bs, upto=None):
+    """The chain through the C ABI (fcm_chain_plan + fcm_chain_run) on device tensors."""
+    layers = spec.layers[:upto]
+    d = fcm.chain_desc(spec.n, spec.h, spec.w, spec.c, layers, spec.dtype, spec.layout)
+    p = fcm.chain_plan(d, objective)
+    return fcm.chain_run(d, p, x, ws[:len(layers)], bs[:len(layers)]), p

@@ -1,0 +1,54 @@
+"""GPU parity of whole chains (FusePlanner over a network, Sec. IV): the MobileNetV2 body
+(51 DW/PW layers after the stem, no skip connections) planned three ways -- least
+Eq. 1-4 bytes, least modelled time, every layer alone -- and run through fcm_chain_run,
+against the CPU oracle applied layer by layer. int8 is bit-exact end to end; float
+chains are compared at the parity tolerance over their first stages (rounding of each
+layer's result to bfloat16 in a different order can flip a last bit that later layers
+carry along, so the full float chains are compared between the three plans instead)."""
+import numpy as np
+import pytest
+
+from paper_2404_19331_amd.workloads import MNV2_STAGES, mobilenetv2_chain, make_chain_inputs
+
+from gpu_util import assert_close, oracle_chain, run_chain, to_dev, to_np
+
+pytestmark = pytest.mark.gpu
+
+OBJECTIVES = ("bytes", "time", "unfused")
+
+
+def _dev(spec):
+    x, ws, bs = make_chain_inputs(spec)
+    return (x, ws, bs), (to_dev(x, spec.dtype), [to_dev(w, spec.dtype) for w in ws],
+                         [to_dev(b, spec.dtype) for b in bs])
+
+
+@pytest.mark.parametrize("layout", ["nhwc", "nchw"])
+def test_int8_mobilenetv2_chain_bit_exact(layout):
+    spec = mobilenetv2_chain(n=2, dtype="i8", layout=layout, h=112 if layout == "nhwc" else 56,
+                             w=112 if layout == "nhwc" else 56)
+    host, dev = _dev(spec)
+    ref = oracle_chain(spec, *host)
+    assert 0.05 < np.mean(ref != 0) and np.mean(np.abs(ref.astype(int)) == 127) < 0.2  # a spread result
+    for obj in OBJECTIVES:
+        got, plan = run_chain(spec, obj, *dev)
+        assert np.array_equal(to_np(got), ref), "%s plan (%d groups, %d fused layers)" % (
+            obj, plan.num_groups, plan.fused_layers)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_float_chain_first_stages_match_oracle(dtype):
+    spec = mobilenetv2_chain(n=2, dtype=dtype, stages=MNV2_STAGES[:3], final_pw=False)
+    host, dev = _dev(spec)
+    ref = oracle_chain(spec, *host)
+    for obj in OBJECTIVES:
+        got, plan = run_chain(spec, obj, *dev)
+        assert_close(to_np(got), ref, dtype, "%s chain, %s plan" % (dtype, obj))
+
+
+def test_bf16_full_chain_plans_agree():
+    spec = mobilenetv2_chain(n=2, dtype="bf16")
+    _, dev = _dev(spec)
+    outs = {obj: to_np(run_chain(spec, obj, *dev)[0]) for obj in OBJECTIVES}
+    for obj in ("bytes", "time"):
+        assert_close(outs[obj], outs["unfused"], "bf16", "full bf16 chain, %s plan vs layer by layer" % obj)

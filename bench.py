@@ -41,6 +41,9 @@ def parse():
     ap.add_argument("--layers", default=None, help="comma-separated layer indices (subset)")
     ap.add_argument("--calib", action="store_true",
                     help="also run a plain 256 MiB device copy (reference for profiler byte counters)")
+    ap.add_argument("--energy", type=float, default=0.0, metavar="SECONDS",
+                    help="also measure energy per step, fused and unfused: the GPU's power sensor sampled "
+                         "while the step loop runs for this many seconds each (0 = off)")
     return ap.parse_args()
 
 
@@ -259,6 +262,90 @@ def load_traffic(workload, kernel_name):
     return ent.get("bytes_per_launch")
 
 
+def power_sensor():
+    """Path of the GPU's socket-power sensor (hwmon, microwatts), or None."""
+    import glob
+    for pat in ("/sys/class/drm/card*/device/hwmon/hwmon*/power1_input",
+                "/sys/class/drm/card*/device/hwmon/hwmon*/power1_average"):
+        for path in sorted(glob.glob(pat)):
+            try:
+                with open(path) as f:
+                    int(f.read().strip())
+                return path
+            except (OSError, ValueError):
+                continue
+    return None
+
+
+class PowerSampler:
+    """Reads the power sensor every `period` seconds on a thread: [(time, watts)]."""
+
+    def __init__(self, path, period=0.005):
+        import threading
+        self.path, self.period, self.samples = path, period, []
+        self._stop = threading.Event()
+        self._t = threading.Thread(target=self._run, daemon=True)
+
+    def _run(self):
+        while not self._stop.is_set():
+            try:
+                with open(self.path) as f:
+                    self.samples.append((time.perf_counter(), int(f.read().strip()) * 1e-6))
+            except (OSError, ValueError):
+                pass
+            time.sleep(self.period)
+
+    def __enter__(self):
+        self._t.start()
+        return self
+
+    def __exit__(self, *exc):
+        self._stop.set()
+        self._t.join()
+
+
+def measure_energy(torch, step, seconds, images, path):
+    """Energy per step of `step` (enqueues one step): the step loop runs for about
+    `seconds` (batches of steps between synchronisations) while the power sensor is
+    sampled; energy = mean sampled power x wall time, over the steps completed. Also the
+    idle power over one second before, and the energy above idle."""
+    with PowerSampler(path) as idle:
+        time.sleep(1.0)
+    p_idle = sum(w for _, w in idle.samples) / max(1, len(idle.samples))
+    for _ in range(3):
+        step()
+    torch.cuda.synchronize()
+    steps = 0
+    with PowerSampler(path) as ps:
+        t0 = time.perf_counter()
+        while time.perf_counter() - t0 < seconds:
+            for _ in range(10):
+                step()
+            steps += 10
+            torch.cuda.synchronize()
+        t1 = time.perf_counter()
+    inside = [w for t, w in ps.samples if t0 <= t <= t1]
+    p = sum(inside) / max(1, len(inside))
+    j_step = p * (t1 - t0) / steps
+    return {"watts_mean": round(p, 1), "watts_idle": round(p_idle, 1), "samples": len(inside),
+            "seconds": round(t1 - t0, 3), "steps": steps, "ms_per_step_wall": round(1e3 * (t1 - t0) / steps, 4),
+            "joules_per_step": round(j_step, 5), "mj_per_image": round(1e3 * j_step / images, 4),
+            "mj_per_image_above_idle": round(1e3 * (p - p_idle) * (t1 - t0) / steps / images, 4)}
+
+
+def energy_block(torch, steps_by_name, seconds, images):
+    path = power_sensor()
+    if path is None:
+        return {"error": "no readable GPU power sensor"}
+    out = {"sensor": path, "method": "hwmon socket power sampled every 5 ms during a %.1f s step loop" % seconds}
+    for name, step in steps_by_name.items():
+        print("bench: energy of the %s step" % name, file=sys.stderr, flush=True)
+        out[name] = measure_energy(torch, step, seconds, images, path)
+    if "fused" in out and "unfused" in out:
+        out["ratio_unfused_over_fused"] = round(out["unfused"]["joules_per_step"] / out["fused"]["joules_per_step"], 3)
+    return out
+
+
 def bench_chain(a, torch, fcm):
     """End-to-end MobileNetV2 body (51 DW/PW layers after the stem, batch 32, NHWC): the
     chain planned by least Eq. 1-4 bytes, by least modelled time and layer by layer, each
@@ -320,6 +407,14 @@ def bench_chain(a, torch, fcm):
                      "frac": round(best["gbs"] / HBM_PEAK_GBS, 4), "kernel": "whole chain", "traffic": None},
         "cpu_baseline": None,
     }
+    if a.energy > 0:
+        steps = {}
+        for obj, name in (("time", "fused"), ("unfused", "unfused")):
+            p = fcm.chain_plan(d, obj)
+            cl = [fcm.chain_run(d, p, xv, wd, bd, prepare=True) for xv in xs]
+            it = iter(range(1 << 62))
+            steps[name] = (lambda cl=cl, it=it: cl[next(it) % len(cl)]())
+        out["energy"] = energy_block(torch, steps, a.energy, spec.n)
     print(json.dumps(out), flush=True)
     return 0
 
@@ -426,6 +521,18 @@ def main():
         "roofline": roof,
         "layers": per_layer,
     }
+    if a.energy > 0:
+        def step_of(which):
+            calls = [L.calls(which) for L in layers]
+            it = iter(range(1 << 62))
+
+            def step():
+                k = next(it)
+                for cl in calls:
+                    cl[k % len(cl)]()
+            return step
+        out["energy"] = energy_block(torch, {"fused": step_of("fused"), "unfused": step_of("unfused")}, a.energy,
+                                     cases[0].n)
     if a.calib:
         # plain device copy of known size for the profiler's byte counters: a float
         # multiply by one reads 256 MiB and writes 256 MiB

@@ -272,14 +272,16 @@ static void finish_f(double* v, size_t cnt, int act, int dtype) {
 }
 
 /* int8 tail: requantise (RNE + saturate), then ReLU. Both maps are monotone and fix
- * zero, so the order of ReLU and requantisation does not change the result.
+ * zero, so the order of ReLU and requantisation does not change the result. ReLU6 is the
+ * quantised clamp: below at 0, above at qmax, which carries 6.0 in the output's
+ * quantised units (the upper clamp is the requantisation's own saturation).
  * Returns ORC_EOVERFLOW when an accumulator does not fit the 32-bit accumulator
  * the method prescribes (Sec. III-B: four-way dot product with 32-bit accumulate). */
 static int finish_i(int64_t* v, size_t cnt, int act, orc_rq rq) {
   for (size_t i = 0; i < cnt; ++i) {
     if (v[i] > INT32_MAX || v[i] < INT32_MIN) return ORC_EOVERFLOW;
     int64_t q = orc_requant(v[i], rq.mult, rq.shift, rq.qmin, rq.qmax);
-    if (act == ORC_ACT_RELU && q < 0) q = 0;
+    if (act != ORC_ACT_NONE && q < 0) q = 0;
     v[i] = q;
   }
   return ORC_OK;
@@ -299,7 +301,6 @@ static int check_common(const orc_desc* d) {
   for (int i = 0; i < 3; ++i) {
     if (d->act[i] < ORC_ACT_NONE || d->act[i] > ORC_ACT_RELU6) return ORC_EINVAL;
     if (d->dtype == ORC_I8) {
-      if (d->act[i] == ORC_ACT_RELU6) return ORC_EUNSUPPORTED;
       if (d->rq[i].shift < 0 || d->rq[i].shift > 62) return ORC_EINVAL;
       if (d->rq[i].qmin > d->rq[i].qmax || d->rq[i].qmin < -128 || d->rq[i].qmax > 127) return ORC_EINVAL;
     }

@@ -468,11 +468,21 @@ def test_int32_overflow_is_reported():
         oracle.pw(case, x, w, b)
 
 
-def test_int8_relu6_unsupported():
-    case = dict(n=1, h=1, w=1, c_in=1, c_mid=1, c_out=1, k=1, stride=1, pad=0, dtype="i8",
-                layout="nchw", act=["relu6"] * 3, rq=[(1, 0, -127, 127)] * 3)
-    with pytest.raises(oracle.OracleError):
-        oracle.pw(case, np.zeros((1, 1, 1, 1), np.int8), np.zeros((1, 1), np.int8), None)
+def test_int8_relu6_is_the_quantised_clamp():
+    """int8 ReLU6: clamp to [max(qmin, 0), qmax], qmax holding 6.0 in output units. Worked
+    by hand for requantisation by 2^-2 (scale 1/4, so 6.0 is 24): accumulators
+    -40, 7, 50, 200 (diagonal weights -1, 1, 1, 2 on inputs 40, 7, 50, 100) give
+    rne(-10) = -10, rne(1.75) = 2, rne(12.5) = 12 (ties to even), rne(50) = 50;
+    saturated to [-127, 24]: -10, 2, 12, 24; clamped at 0: 0, 2, 12, 24."""
+    x = np.array([40, 7, 50, 100], dtype=np.int8).reshape(1, 1, 1, 4)
+    w = np.diag([-1, 1, 1, 2]).astype(np.int8)
+    base = dict(n=1, h=1, w=1, c_in=4, c_mid=4, c_out=4, k=1, stride=1, pad=0, dtype="i8", layout="nhwc",
+                rq=[(1, 2, -127, 24)] * 3)
+    got = {a: oracle.pw(dict(base, act=[a] * 3), x, w, None).ravel().tolist() for a in ("none", "relu", "relu6")}
+    assert got["none"] == [-10, 2, 12, 24]
+    assert got["relu6"] == [0, 2, 12, 24]
+    # the same as ReLU with the same range: 6 lives in qmax
+    assert got["relu6"] == got["relu"]
 
 
 # --------------------------------------------------------------------------------------

@@ -65,7 +65,7 @@ typedef enum {
   FCM_OK = 0,
   FCM_EINVAL = 1,        /* NULL tensor, non-positive size, bad geometry or requant  */
   FCM_EUNSUPPORTED = 2,  /* valid but not built: k not in {3,5}, stride not in {1,2},
-                            int8 with RELU6, plan that no compiled kernel implements,
+                            plan that no compiled kernel implements,
                             tile that does not fit in LDS                              */
   FCM_EDEVICE = 3        /* HIP reported an error at launch                          */
 } fcm_status;
@@ -85,7 +85,9 @@ typedef enum {
 } fcm_op;
 
 /* int8 requantisation of a stage: q = clamp(rne(acc * mult / 2^shift), qmin, qmax),
- * rne = round half to even, acc = int32 accumulator + int32 bias.
+ * rne = round half to even, acc = int32 accumulator + int32 bias. int8 activations act on
+ * q: RELU and RELU6 clamp it below at 0; RELU6's upper end is qmax, which the caller sets
+ * to 6.0 in the output's quantised units (e.g. 24 for a scale of 1/4).
  * Constraints: 0 <= shift <= 62, -128 <= qmin <= qmax <= 127. Ignored for float types. */
 typedef struct {
   int32_t mult;
@@ -291,6 +293,19 @@ int64_t fcm_chain_workspace_bytes(const fcm_chain_plan_t* plan);
 fcm_status fcm_chain_run(const fcm_chain_desc* chain, const fcm_chain_plan_t* plan, const void* x,
                          const void* const* weights, const void* const* biases, void* workspace, void* y,
                          void* stream);
+
+/* Fold an inference-mode batch normalisation that follows a convolution into that
+ * convolution's weights and bias (an FCM stage is convolution -> normalisation ->
+ * activation, Sec. III-A; the kernels take the normalisation folded). For output channel o:
+ *   s_o = gamma[o] / sqrt(var[o] + eps),  w_out[o][j] = w[o][j] * s_o,
+ *   b_out[o] = (b[o] - mean[o]) * s_o + beta[o]            (b may be NULL: zero)
+ * computed in double, rounded to float. w holds c_out rows of `row` floats (depthwise
+ * [c][k][k]: row = k*k; pointwise [c_out][c_in]: row = c_in). HOST pointers; w_out / b_out
+ * may alias w / b. Float models only (int8 folds into its requantisation instead).
+ * FCM_EINVAL for NULL arrays, non-positive sizes, eps < 0 or var + eps <= 0. */
+fcm_status fcm_fold_batchnorm(int32_t c_out, int32_t row, const float* w, const float* b, const float* gamma,
+                              const float* beta, const float* mean, const float* var, float eps, float* w_out,
+                              float* b_out);
 
 /* Human-readable name of a status code (static storage). */
 const char* fcm_status_string(fcm_status status);

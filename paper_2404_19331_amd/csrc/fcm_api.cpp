@@ -2,6 +2,7 @@
 // argument marshalling and launch. No allocation, no synchronisation.
 #include <hip/hip_runtime.h>
 
+#include <cmath>
 #include <cstdint>
 #include <cstring>
 #include <mutex>
@@ -56,7 +57,6 @@ fcm_status validate(int op, const fcm_desc* d) {
       if (r.shift < 0 || r.shift > 62) return fail(FCM_EINVAL, "requant shift must be in [0, 62]");
       if (r.qmin < -128 || r.qmax > 127 || r.qmin > r.qmax)
         return fail(FCM_EINVAL, "requant range must satisfy -128 <= qmin <= qmax <= 127");
-      if (d->act[i] == FCM_ACT_RELU6) return fail(FCM_EUNSUPPORTED, "int8 supports NONE and RELU activations");
     }
   }
   switch (op) {
@@ -313,6 +313,27 @@ double fcm_plan_time_estimate(const fcm_desc* desc, const fcm_hw_desc* hw, const
   if (!plan || validate(plan->op, desc) != FCM_OK) return 0.0;
   const fcm_hw_desc H = hw ? *hw : default_hw();
   return plan_time_estimate(geometry(plan->op, desc), *plan, H);
+}
+
+fcm_status fcm_fold_batchnorm(int32_t c_out, int32_t row, const float* w, const float* b, const float* gamma,
+                              const float* beta, const float* mean, const float* var, float eps, float* w_out,
+                              float* b_out) {
+  if (c_out <= 0 || row <= 0) return fail(FCM_EINVAL, "fold_batchnorm: c_out and row must be positive");
+  if (!w || !gamma || !beta || !mean || !var || !w_out || !b_out)
+    return fail(FCM_EINVAL, "fold_batchnorm: NULL array");
+  if (!(eps >= 0.0f)) return fail(FCM_EINVAL, "fold_batchnorm: eps must be >= 0");
+  for (int32_t o = 0; o < c_out; ++o)
+    if (!((double)var[o] + (double)eps > 0.0)) return fail(FCM_EINVAL, "fold_batchnorm: var + eps must be > 0");
+  for (int32_t o = 0; o < c_out; ++o) {
+    const double sc = (double)gamma[o] / std::sqrt((double)var[o] + (double)eps);
+    const double bo = b ? (double)b[o] : 0.0;
+    for (int32_t j = 0; j < row; ++j) {
+      const size_t i = (size_t)o * row + j;
+      w_out[i] = (float)((double)w[i] * sc);
+    }
+    b_out[o] = (float)((bo - (double)mean[o]) * sc + (double)beta[o]);
+  }
+  return FCM_OK;
 }
 
 fcm_status fcm_dw_pw(const fcm_desc* desc, const void* x, const void* w_dw, const void* b_dw, const void* w_pw,

@@ -77,7 +77,8 @@ __device__ __forceinline__ float act_f(float v, int act) {
   return v;
 }
 
-// q = clamp(round_half_even(acc * mult / 2^shift), qmin, qmax), then ReLU if asked.
+// q = clamp(round_half_even(acc * mult / 2^shift), qmin, qmax), then ReLU if asked (ReLU6
+// too: its upper end is qmax, 6.0 in the output's quantised units).
 __device__ __forceinline__ int32_t requant(int32_t acc, const Requant& rq, int act) {
   int64_t t = (int64_t)acc * (int64_t)rq.mult;
   int64_t q = t;
@@ -89,7 +90,7 @@ __device__ __forceinline__ int32_t requant(int32_t acc, const Requant& rq, int a
   }
   q = q < rq.qmin ? rq.qmin : q;
   q = q > rq.qmax ? rq.qmax : q;
-  if (act == ACT_RELU && q < 0) q = 0;
+  if (act != ACT_NONE && q < 0) q = 0;
   return (int32_t)q;
 }
 

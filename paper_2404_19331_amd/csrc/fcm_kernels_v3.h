@@ -75,8 +75,8 @@ __device__ __forceinline__ Epi3 make_epi3(int act, const Requant& rq) {
   e.hi = act == ACT_RELU6 ? 6.0f : __builtin_huge_valf();
   e.mult = rq.mult;
   e.shift = rq.shift;
-  e.qlo = act == ACT_RELU ? max(rq.qmin, 0) : rq.qmin;
-  e.qhi = act == ACT_RELU ? max(rq.qmax, 0) : rq.qmax;
+  e.qlo = act != ACT_NONE ? max(rq.qmin, 0) : rq.qmin;  // int8 ReLU6: its 6 is qmax
+  e.qhi = act != ACT_NONE ? max(rq.qmax, 0) : rq.qmax;
   return e;
 }
 __device__ __forceinline__ float epi_f(float v, const Epi3& e) { return __builtin_amdgcn_fmed3f(v, e.lo, e.hi); }

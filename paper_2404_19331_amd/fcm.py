@@ -7,7 +7,7 @@ library. There is no fallback: if libfcm.so is missing or cannot load, importing
 binding's functions raises.
 
 Entry points mirror the C ABI: dw_pw, pw_dw, pw_pw, pw_dw_pw, dw, pw, plan, plan_evaluate,
-chain_desc, chain_plan, chain_run.
+chain_desc, chain_plan, chain_run, fold_batchnorm.
 Tensors: x is [n, c, h, w] (layout="nchw") or [n, h, w, c] (layout="nhwc");
 depthwise weights [c, k, k] (or [c, 1, k, k]); pointwise weights [c_out, c_in]
 (or [c_out, c_in, 1, 1]); biases float32 (float paths) or int32 (int8) or None.
@@ -140,6 +140,9 @@ def lib():
         L.fcm_chain_workspace_bytes.restype = ctypes.c_int64
         L.fcm_chain_run.argtypes = [cdp, cpp, vp, ctypes.POINTER(vp), ctypes.POINTER(vp), vp, vp, vp]
         L.fcm_chain_run.restype = ctypes.c_int
+        fp = ctypes.POINTER(ctypes.c_float)
+        L.fcm_fold_batchnorm.argtypes = [ctypes.c_int32, ctypes.c_int32, fp, fp, fp, fp, fp, fp, ctypes.c_float, fp, fp]
+        L.fcm_fold_batchnorm.restype = ctypes.c_int
         L.fcm_plan_time_estimate.argtypes = [dp, hp, pp]
         L.fcm_plan_time_estimate.restype = ctypes.c_double
         _lib = L
@@ -532,3 +535,22 @@ def chain_run(desc, plan, x, weights, biases=None, *, out=None, workspace=None, 
     args = (ctypes.byref(desc), ctypes.byref(plan), _ptr(x), W, B, _ptr(workspace), _ptr(y), _stream(x, stream))
     r = _ChainRun(lib().fcm_chain_run, args, y, (W, B, workspace, desc, plan))
     return r if prepare else r()
+
+
+def fold_batchnorm(w, b, gamma, beta, mean, var, eps=1e-5):
+    """Fold an inference batch normalisation into the preceding convolution (host numpy
+    float32 arrays; w is [c_out, ...]). Returns (w_folded, b_folded)."""
+    import numpy as np
+    f32 = lambda a: np.ascontiguousarray(a, dtype=np.float32)
+    w = f32(w)
+    c_out = w.shape[0]
+    row = int(w.size // c_out)
+    g, bt, m, v = f32(gamma), f32(beta), f32(mean), f32(var)
+    for a in (g, bt, m, v):
+        if a.shape != (c_out,):
+            raise ValueError("gamma, beta, mean, var must have c_out = %d entries" % c_out)
+    bb = None if b is None else f32(b)
+    wo, bo = np.empty_like(w), np.empty(c_out, dtype=np.float32)
+    p = lambda a: None if a is None else a.ctypes.data_as(ctypes.POINTER(ctypes.c_float))
+    _check(lib().fcm_fold_batchnorm(c_out, row, p(w), p(bb), p(g), p(bt), p(m), p(v), float(eps), p(wo), p(bo)))
+    return wo, bo

@@ -162,8 +162,8 @@ def test_chain_validation():
         fcm.chain_plan(d, "bytes")
     d = fcm.chain_desc(1, 8, 8, 8, good, "f32")
     assert fcm.lib().fcm_chain_plan(fcm.ctypes.byref(d), 7, None, fcm.ctypes.byref(fcm.ChainPlan())) == EINVAL
-    # int8 ReLU6 has no kernel: the chain cannot be planned
-    d = fcm.chain_desc(1, 8, 8, 8, [dict(kind="pw", c_out=8, act="relu6")], "i8")
+    # a 7x7 depthwise layer has no kernel: the chain cannot be planned
+    d = fcm.chain_desc(1, 8, 8, 8, [dict(kind="dw", k=7, stride=1, pad=3)], "i8")
     with pytest.raises(fcm.FcmError) as e:
         fcm.chain_plan(d, "bytes")
     assert e.value.status == EUNSUPPORTED

@@ -78,6 +78,19 @@ EDGE = [
     Case("dw_pw", 1, 6, 5, 600, 600, 300, 3, 1, 1, "bf16", "nhwc", ("relu", "none", "none"), bias=True, seed=12),
     Case("pw_dw_pw", 1, 6, 5, 100, 200, 150, 3, 1, 1, "bf16", "nhwc", ("relu6", "relu6", "none"), bias=True,
          seed=13),
+    # int8 ReLU6: the quantised clamp [0, qmax] (qmax = 6.0 in output units), every module
+    Case("dw_pw", 2, 10, 12, 40, 40, 24, 3, 1, 1, "i8", "nhwc", ("relu6", "relu6", "none"),
+         ((1, 4, -127, 40), (1, 6, -128, 30), (1, 6, -127, 127)), dist_x="i8small", dist_w="i8small", bias=True,
+         seed=20),
+    Case("pw_dw_pw", 2, 10, 12, 24, 48, 16, 3, 2, 1, "i8", "nchw", ("relu6", "relu6", "relu6"),
+         ((1, 4, -127, 40), (1, 6, -128, 30), (1, 5, -127, 20)), dist_x="i8small", dist_w="i8small", bias=True,
+         seed=21),
+    Case("pw_pw", 2, 10, 12, 32, 72, 16, 1, 1, 0, "i8", "nhwc", ("relu6", "relu6", "none"),
+         ((1, 5, -127, 30), (1, 6, -128, 25), (1, 6, -127, 127)), dist_x="i8small", dist_w="i8small", bias=True,
+         seed=22),
+    Case("pw_dw", 2, 10, 12, 32, 48, 48, 5, 1, 2, "i8", "nhwc", ("relu6", "relu6", "none"),
+         ((1, 5, -127, 30), (1, 6, -128, 25), (1, 6, -127, 127)), dist_x="i8small", dist_w="i8small", bias=True,
+         seed=23),
     # PW -> PW: ragged channel rows, single channels, many chunks and output blocks
     Case("pw_pw", 2, 10, 12, 20, 36, 12, 1, 1, 0, "i8", "nhwc", ("relu", "none", "none"), RQ_SMALL,
          dist_x="i8small", dist_w="i8small", bias=True, seed=14),

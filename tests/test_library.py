@@ -171,12 +171,10 @@ def test_descriptor_validation(kw, status):
     assert e.value.status == status
 
 
-def test_int8_relu6_is_unsupported():
+def test_int8_relu6_plans_as_the_quantised_clamp():
     d = fcm.make_desc(1, 16, 16, 32, 32, 32, k=3, stride=1, pad=1, dtype="i8", layout="nhwc",
-                      act=("relu6", "none", "none"))
-    with pytest.raises(fcm.FcmError) as e:
-        fcm.plan("dw_pw", d)
-    assert e.value.status == EUNSUPPORTED
+                      act=("relu6", "relu6", "none"), rq=[(1, 6, -127, 24)] * 3)
+    assert fcm.plan("dw_pw", d).variant >= 0
 
 
 def test_header_is_plain_c():

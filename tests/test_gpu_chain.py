@@ -52,3 +52,16 @@ def test_bf16_full_chain_plans_agree():
     outs = {obj: to_np(run_chain(spec, obj, *dev)[0]) for obj in OBJECTIVES}
     for obj in ("bytes", "time"):
         assert_close(outs[obj], outs["unfused"], "bf16", "full bf16 chain, %s plan vs layer by layer" % obj)
+
+
+def test_autotuned_chain_plan_runs_bit_exact():
+    from paper_2404_19331_amd import fcm
+    from paper_2404_19331_amd.autotune import chain_autotune
+    spec = mobilenetv2_chain(n=2, dtype="i8", stages=MNV2_STAGES[:4], final_pw=False)
+    host, dev = _dev(spec)
+    ref = oracle_chain(spec, *host)
+    d = fcm.chain_desc(spec.n, spec.h, spec.w, spec.c, spec.layers, spec.dtype, spec.layout)
+    plan, timed = chain_autotune(d, reps=3)
+    assert plan.num_groups >= 1 and len(timed) >= len(spec.layers)
+    got = fcm.chain_run(d, plan, dev[0], dev[1], dev[2])
+    assert np.array_equal(to_np(got), ref)

@@ -19,6 +19,9 @@
  *                 unfused comparison, built from the same tiles and dataflow.
  *   fcm_plan      FusePlanner (Sec. IV): global-memory-access estimates of the LBL and
  *                 fused kernels (Eq. 1-4) and the tiling that minimises them.
+ *   fcm_chain_plan, fcm_chain_run  FusePlanner over a sequence of DW/PW layers: which
+ *                 adjacent layers to fuse into which module, then the chain's launches.
+ *   fcm_fold_batchnorm  folds an inference batch normalisation into a float convolution.
  *
  * Conventions shared by every entry point
  * ---------------------------------------

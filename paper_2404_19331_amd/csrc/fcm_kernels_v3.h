@@ -282,7 +282,7 @@ __global__ __launch_bounds__(kThreads3) void k_fused3(KArgs a) {
   auto bufp = [&](int slot) { return smem + slot * lay.buf_bytes; };
   auto next_slot = [&](int slot) { return slot + 1 == D ? 0 : slot + 1; };
 
-  int tsi = 0;
+  [[maybe_unused]] int tsi = 0;  // timeline slot (development builds)
   FCM_TS(tsi++);
 
   if (producer) {
@@ -466,7 +466,7 @@ __global__ __launch_bounds__(kThreads3) void k_fused3(KArgs a) {
   u32x4 bop[BPW];
 
   barrier3();  // item 0 is ready
-  int tsc = 32;
+  [[maybe_unused]] int tsc = 32;
   FCM_TSC(tsc++);
   int wt = wt0, ch = u_lo(wt0), ch_hi = u_hi(wt0), slot = 0;
   Tile cur_t = decode(wt0 / SPL);

@@ -122,7 +122,6 @@ __global__ __launch_bounds__(256) void k_pwpw4(KArgs a) {
   if (S == 1 && !active) return;           // (S > 1: every wave reaches the barrier)
   const int npix = a.N * a.H * a.W;
   const int ci_b = a.Ci * E, cm_b = a.Cm * E;
-  const int ks = ceil_div(ci_b, 64);
   const int ct = ceil_div(a.Co, 16);
   const int nch = ceil_div(cm_b, 64);
   // buffer resources (sizes below 2^31 bytes, checked by the planner)

@@ -222,6 +222,7 @@ __global__ __launch_bounds__(kThreads3) void k_fused3(KArgs a) {
   constexpr int OGE = 16 / DT::ELT;  // channels per 16-byte granule
   constexpr int OTPG = OGE / 4;      // MFMA tiles per granule
   static_assert(MODE == M3_DW || CT % OTPG == 0, "whole output granules per lane");
+  static_assert(MODE == M3_DW || CT <= 16, "the block's PW bias (16*CT fp32 / int32) is one 1 KiB copy");
 
   const int TH = a.TH, TW = a.TW, P = TH * TW;
   const int IW = HAS_DW ? (TW - 1) * SE + KE : TW;

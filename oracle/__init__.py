@@ -46,7 +46,8 @@ class _Desc(ctypes.Structure):
                 ("c_in", ctypes.c_int32), ("c_mid", ctypes.c_int32), ("c_out", ctypes.c_int32),
                 ("k", ctypes.c_int32), ("stride", ctypes.c_int32), ("pad", ctypes.c_int32),
                 ("dtype", ctypes.c_int32), ("layout", ctypes.c_int32),
-                ("act", ctypes.c_int32 * 3), ("rq", _Rq * 3)]
+                ("act", ctypes.c_int32 * 3), ("rq", _Rq * 3),
+                ("rqc", ctypes.POINTER(ctypes.c_int32) * 3)]
 
 
 def build(force=False):
@@ -114,6 +115,15 @@ def _desc(case):
     rqs = (rqs + [(1, 0, -128, 127)] * 3)[:3]
     for i, r in enumerate(rqs):
         d.rq[i].mult, d.rq[i].shift, d.rq[i].qmin, d.rq[i].qmax = (int(v) for v in r)
+    # int8 per-channel requantisation: rq_channel[i] = (multipliers, shifts) of stage i's
+    # output channels, or None for the per-tensor rq[i]
+    d._keep = []
+    for i, pc in enumerate(list(_get(case, "rq_channel", None) or [None] * 3)[:3]):
+        if pc is None:
+            continue
+        a = np.ascontiguousarray(np.concatenate([np.asarray(pc[0]), np.asarray(pc[1])]).astype(np.int32))
+        d._keep.append(a)
+        d.rqc[i] = a.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
     return d
 
 

@@ -52,6 +52,10 @@ typedef struct {
   int32_t dtype, layout;
   int32_t act[3];
   orc_rq rq[3];
+  /* int8 per-channel requantisation of stage i (NULL = per-tensor rq[i]): host array of
+   * 2 x (the stage's output channels), the multipliers then the shifts; qmin/qmax stay
+   * those of rq[i] */
+  const int32_t* rqc[3];
 } orc_desc;
 
 /* ------------------------------------------------------------------------- */
@@ -277,10 +281,17 @@ static void finish_f(double* v, size_t cnt, int act, int dtype) {
  * quantised units (the upper clamp is the requantisation's own saturation).
  * Returns ORC_EOVERFLOW when an accumulator does not fit the 32-bit accumulator
  * the method prescribes (Sec. III-B: four-way dot product with 32-bit accumulate). */
-static int finish_i(int64_t* v, size_t cnt, int act, orc_rq rq) {
+static int finish_i(int64_t* v, size_t cnt, int C, size_t HW, int act, orc_rq rq, const int32_t* rqc) {
   for (size_t i = 0; i < cnt; ++i) {
     if (v[i] > INT32_MAX || v[i] < INT32_MIN) return ORC_EOVERFLOW;
-    int64_t q = orc_requant(v[i], rq.mult, rq.shift, rq.qmin, rq.qmax);
+    int32_t mult = rq.mult, shift = rq.shift;
+    if (rqc) {  /* canonical [n][c][h][w]: channel of element i */
+      const int c = (int)((i / HW) % (size_t)C);
+      mult = rqc[c];
+      shift = rqc[C + c];
+      if (shift < 0 || shift > 62) return ORC_EINVAL;
+    }
+    int64_t q = orc_requant(v[i], mult, shift, rq.qmin, rq.qmax);
     if (act != ORC_ACT_NONE && q < 0) q = 0;
     v[i] = q;
   }
@@ -340,7 +351,7 @@ int orc_dw(const orc_desc* d, const void* x, const void* wd, const void* bd, voi
     int64_t* wi = load_vec_i((const int8_t*)wd, (size_t)C * K * K);
     int64_t* yi = (int64_t*)malloc(no * sizeof(int64_t));
     dw_stage_i(xi, N, C, H, W, wi, (const int32_t*)bd, K, S, P, Ho, Wo, yi);
-    st = finish_i(yi, no, d->act[0], d->rq[0]);
+    st = finish_i(yi, no, C, (size_t)Ho * Wo, d->act[0], d->rq[0], d->rqc[0]);
     if (!st) store_fmap_i(yi, d->layout, N, C, Ho, Wo, (int8_t*)y);
     free(xi); free(wi); free(yi);
     return st;
@@ -367,7 +378,7 @@ int orc_pw(const orc_desc* d, const void* x, const void* wp, const void* bp, voi
     int64_t* wi = load_vec_i((const int8_t*)wp, (size_t)Co * C);
     int64_t* yi = (int64_t*)malloc(no * sizeof(int64_t));
     pw_stage_i(xi, N, C, H, W, wi, (const int32_t*)bp, Co, yi);
-    st = finish_i(yi, no, d->act[0], d->rq[0]);
+    st = finish_i(yi, no, Co, (size_t)H * W, d->act[0], d->rq[0], d->rqc[0]);
     if (!st) store_fmap_i(yi, d->layout, N, Co, H, W, (int8_t*)y);
     free(xi); free(wi); free(yi);
     return st;
@@ -399,10 +410,10 @@ int orc_dw_pw(const orc_desc* d, const void* x, const void* wd, const void* bd, 
     int64_t* mi = (int64_t*)malloc(nm * sizeof(int64_t));
     int64_t* yi = (int64_t*)malloc(no * sizeof(int64_t));
     dw_stage_i(xi, N, C, H, W, wdi, (const int32_t*)bd, K, S, P, Ho, Wo, mi);
-    st = finish_i(mi, nm, d->act[0], d->rq[0]);
+    st = finish_i(mi, nm, C, (size_t)Ho * Wo, d->act[0], d->rq[0], d->rqc[0]);
     if (!st) {
       pw_stage_i(mi, N, C, Ho, Wo, wpi, (const int32_t*)bp, Co, yi);
-      st = finish_i(yi, no, d->act[1], d->rq[1]);
+      st = finish_i(yi, no, Co, (size_t)Ho * Wo, d->act[1], d->rq[1], d->rqc[1]);
     }
     if (!st) store_fmap_i(yi, d->layout, N, Co, Ho, Wo, (int8_t*)y);
     free(xi); free(wdi); free(wpi); free(mi); free(yi);
@@ -441,10 +452,10 @@ int orc_pw_dw(const orc_desc* d, const void* x, const void* wp, const void* bp, 
     int64_t* mi = (int64_t*)malloc(nm * sizeof(int64_t));
     int64_t* yi = (int64_t*)malloc(no * sizeof(int64_t));
     pw_stage_i(xi, N, Ci, H, W, wpi, (const int32_t*)bp, Cm, mi);
-    st = finish_i(mi, nm, d->act[0], d->rq[0]);
+    st = finish_i(mi, nm, Cm, (size_t)H * W, d->act[0], d->rq[0], d->rqc[0]);
     if (!st) {
       dw_stage_i(mi, N, Cm, H, W, wdi, (const int32_t*)bd, K, S, P, Ho, Wo, yi);
-      st = finish_i(yi, no, d->act[1], d->rq[1]);
+      st = finish_i(yi, no, Cm, (size_t)Ho * Wo, d->act[1], d->rq[1], d->rqc[1]);
     }
     if (!st) store_fmap_i(yi, d->layout, N, Cm, Ho, Wo, (int8_t*)y);
     free(xi); free(wpi); free(wdi); free(mi); free(yi);
@@ -480,10 +491,10 @@ int orc_pw_pw(const orc_desc* d, const void* x, const void* wp1, const void* bp1
     int64_t* mi = (int64_t*)malloc(nm * sizeof(int64_t));
     int64_t* yi = (int64_t*)malloc(no * sizeof(int64_t));
     pw_stage_i(xi, N, Ci, H, W, w1, (const int32_t*)bp1, Cm, mi);
-    st = finish_i(mi, nm, d->act[0], d->rq[0]);
+    st = finish_i(mi, nm, Cm, (size_t)H * W, d->act[0], d->rq[0], d->rqc[0]);
     if (!st) {
       pw_stage_i(mi, N, Cm, H, W, w2, (const int32_t*)bp2, Co, yi);
-      st = finish_i(yi, no, d->act[1], d->rq[1]);
+      st = finish_i(yi, no, Co, (size_t)H * W, d->act[1], d->rq[1], d->rqc[1]);
     }
     if (!st) store_fmap_i(yi, d->layout, N, Co, H, W, (int8_t*)y);
     free(xi); free(w1); free(w2); free(mi); free(yi);
@@ -523,14 +534,14 @@ int orc_pw_dw_pw(const orc_desc* d, const void* x, const void* wp1, const void* 
     int64_t* m2 = (int64_t*)malloc(n2 * sizeof(int64_t));
     int64_t* yi = (int64_t*)malloc(no * sizeof(int64_t));
     pw_stage_i(xi, N, Ci, H, W, w1, (const int32_t*)bp1, Cm, m1);
-    st = finish_i(m1, n1, d->act[0], d->rq[0]);
+    st = finish_i(m1, n1, Cm, (size_t)H * W, d->act[0], d->rq[0], d->rqc[0]);
     if (!st) {
       dw_stage_i(m1, N, Cm, H, W, wdi, (const int32_t*)bd, K, S, P, Ho, Wo, m2);
-      st = finish_i(m2, n2, d->act[1], d->rq[1]);
+      st = finish_i(m2, n2, Cm, (size_t)Ho * Wo, d->act[1], d->rq[1], d->rqc[1]);
     }
     if (!st) {
       pw_stage_i(m2, N, Cm, Ho, Wo, w2, (const int32_t*)bp2, Co, yi);
-      st = finish_i(yi, no, d->act[2], d->rq[2]);
+      st = finish_i(yi, no, Co, (size_t)Ho * Wo, d->act[2], d->rq[2], d->rqc[2]);
     }
     if (!st) store_fmap_i(yi, d->layout, N, Co, Ho, Wo, (int8_t*)y);
     free(xi); free(w1); free(wdi); free(w2); free(m1); free(m2); free(yi);

@@ -545,3 +545,79 @@ def test_module_equals_chain_of_single_layers(dtype, op):
         m = stage_dw(m, 9, 8, cm, inp["w_dw"], inp["b_dw"], 1)
         ref = stage_pw(m, ho, wo, cm, co, inp["w_pw2"], inp["b_pw2"], 2)
     assert np.array_equal(y, ref)
+
+
+# --------------------------------------------------------------------------------------
+# int8 per-channel requantisation
+# --------------------------------------------------------------------------------------
+
+def _i8_case(op, ci, cm, co, k=3, s=1, acts=("relu", "none", "relu"), layout="nhwc"):
+    return dict(op=op, n=2, h=7, w=6, c_in=ci, c_mid=cm, c_out=co, k=k, stride=s, pad=k // 2, dtype="i8",
+                layout=layout, act=list(acts), rq=[(1, 6, -127, 127), (3, 8, -128, 127), (1, 5, -127, 127)],
+                dist_x="i8small", dist_w="i8small", bias=True, seed=77)
+
+
+def _i8_inputs(c):
+    from paper_2404_19331_amd.workloads import Case, make_inputs
+    kw = {k: v for k, v in c.items() if k != "op"}
+    return make_inputs(Case(c["op"], **{k: kw[k] for k in ("n", "h", "w", "c_in", "c_mid", "c_out", "k", "stride",
+                                                              "pad", "dtype", "layout")}, act=tuple(c["act"]),
+                            rq=tuple(c["rq"]), dist_x="i8small", dist_w="i8small", bias=True, seed=c["seed"]))
+
+
+def _stage_channels(op, c):
+    return {"dw_pw": [c["c_in"], c["c_out"]], "pw_dw": [c["c_mid"], c["c_mid"]], "pw_pw": [c["c_mid"], c["c_out"]],
+            "pw_dw_pw": [c["c_mid"], c["c_mid"], c["c_out"]], "dw": [c["c_in"]], "pw": [c["c_out"]]}[op]
+
+
+@pytest.mark.parametrize("op", ["dw_pw", "pw_dw", "pw_pw", "pw_dw_pw", "dw", "pw"])
+def test_per_channel_requant_with_equal_channels_is_per_tensor(op):
+    c = _i8_case(op, 12, 12 if op in ("dw_pw", "dw") else 20, 12 if op in ("dw", "pw_dw") else 8,
+                 k=1 if op in ("pw", "pw_pw") else 3)
+    if op == "pw_dw":
+        c["c_out"] = c["c_mid"]
+    inp = _i8_inputs(c)
+    ref = oracle.run(op, c, inp)
+    chans = _stage_channels(op, c)
+    pc = dict(c, rq_channel=[(np.full(n, r[0]), np.full(n, r[1])) for n, r in zip(chans, c["rq"])])
+    assert np.array_equal(oracle.run(op, pc, inp), ref)
+
+
+def test_per_channel_requant_selects_each_channels_own_scale():
+    """A PW layer requantised per output channel equals, channel by channel, the layer run
+    with that channel's (mult, shift) as the per-tensor requantisation."""
+    c = _i8_case("pw", 16, 16, 6, k=1, acts=("none",) * 3)
+    inp = _i8_inputs(c)
+    mults, shifts = np.array([1, 3, 5, 1, 7, 2]), np.array([2, 4, 6, 8, 5, 3])
+    got = oracle.run("pw", dict(c, rq_channel=[(mults, shifts)]), inp)
+    for ch in range(6):
+        one = oracle.run("pw", dict(c, rq=[(int(mults[ch]), int(shifts[ch]), -127, 127)] * 3), inp)
+        assert np.array_equal(got[..., ch], one[..., ch])
+    # not vacuous: one shared scale gives a different result
+    shared = oracle.run("pw", dict(c, rq=[(1, 2, -127, 127)] * 3), inp)
+    assert not np.array_equal(got, shared) and np.mean(got != 0) > 0.3
+
+
+def test_per_channel_requant_composes_stage_by_stage():
+    """DW -> PW with per-channel requantisation of both stages equals the DW layer and the
+    PW layer run one after the other with the same per-channel requantisation."""
+    c = _i8_case("dw_pw", 10, 10, 7)
+    inp = _i8_inputs(c)
+    rng = np.random.default_rng(3)
+    pc0 = (rng.integers(1, 8, 10), rng.integers(3, 9, 10))
+    pc1 = (rng.integers(1, 8, 7), rng.integers(5, 11, 7))
+    fused = oracle.run("dw_pw", dict(c, rq_channel=[pc0, pc1]), inp)
+    mid = oracle.dw(dict(c, rq_channel=[pc0]), inp["x"], inp["w_dw"], inp["b_dw"])
+    c2 = dict(c, h=mid.shape[1], w=mid.shape[2], c_in=10, c_out=7, act=[c["act"][1]] * 3, rq=[c["rq"][1]] * 3,
+              rq_channel=[pc1])
+    assert np.array_equal(fused, oracle.pw(c2, mid, inp["w_pw"], inp["b_pw"]))
+
+
+def test_per_channel_requant_hand_values():
+    # one pixel, identity weights on inputs 40 and 50: channel 0 by 3/2^2 -> rne(30) = 30,
+    # channel 1 by 1/2^3 -> rne(6.25) = 6
+    x = np.array([40, 50], dtype=np.int8).reshape(1, 1, 1, 2)
+    w = np.eye(2, dtype=np.int8)
+    c = dict(n=1, h=1, w=1, c_in=2, c_mid=2, c_out=2, k=1, stride=1, pad=0, dtype="i8", layout="nhwc",
+             act=["none"] * 3, rq=[(1, 0, -127, 127)] * 3, rq_channel=[(np.array([3, 1]), np.array([2, 3]))])
+    assert oracle.pw(c, x, w, None).ravel().tolist() == [30, 6]

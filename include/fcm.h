@@ -114,6 +114,11 @@ typedef struct {
   int32_t layout;  /* fcm_layout */
   int32_t act[3];  /* fcm_act per conv stage, execution order */
   fcm_requant rq[3];
+  /* int8 per-channel requantisation of stage i (NULL = per-tensor rq[i]): DEVICE array of
+   * 2 x (the stage's output channels) int32, the multipliers then the shifts (shifts in
+   * [0, 62]); the clamp range stays rq[i].qmin / qmax. Such descriptors are planned and
+   * launched on the first-generation kernels only. Ignored for float types. */
+  const int32_t* rq_channel[3];
 } fcm_desc;
 
 /* GPU description for the planner (Sec. IV: number of SMs, L1/shared-memory size).

@@ -20,6 +20,14 @@ fcm_status fail(fcm_status st, const std::string& msg) {
   return st;
 }
 
+bool has_per_channel_rq(int op, const fcm_desc* d) {
+  if (!d || d->dtype != FCM_I8) return false;
+  const int stages = op == FCM_OP_PW_DW_PW ? 3 : ((op == FCM_OP_DW || op == FCM_OP_PW) ? 1 : 2);
+  for (int i = 0; i < stages; ++i)
+    if (d->rq_channel[i]) return true;
+  return false;
+}
+
 const Variant* all_variants(int* count) {
   static std::vector<Variant> all = [] {
     std::vector<Variant> v;
@@ -167,13 +175,17 @@ static fcm_status run(int op, const fcm_desc* d, const Tensors& t, const fcm_pla
   // LDS-DMA kernels need 16-byte aligned tensors
   bool aligned = aligned16(t.x) && aligned16(t.y);
   for (int i = 0; i < nw; ++i) aligned = aligned && aligned16(t.w[i]);
+  // per-channel requantisation is implemented by the first-generation kernels only
+  const bool per_channel = has_per_channel_rq(op, d);
+  aligned = aligned && !per_channel;
   fcm_plan_t p;
   if (plan_in) {
     if (plan_in->op != op) return fail(FCM_EINVAL, "plan was made for another module");
     p = *plan_in;
     if ((st = evaluate_plan(g, d, hw, &p)) != FCM_OK) return st;
     if (!aligned && variant_needs_alignment(p.variant))
-      return fail(FCM_EUNSUPPORTED, "plan's kernel needs 16-byte aligned tensors");
+      return fail(FCM_EUNSUPPORTED, per_channel ? "per-channel requantisation runs on the first-generation kernels only"
+                                                : "plan's kernel needs 16-byte aligned tensors");
   } else {
     if ((st = find_plan(op, d, &hw, &p, aligned)) != FCM_OK) return st;
   }
@@ -210,6 +222,7 @@ static fcm_status run(int op, const fcm_desc* d, const Tensors& t, const fcm_pla
   const int last = (g.family == FAM_PWDW || g.family == FAM_DW) ? g.cm : g.co;
   a.n_cb = ceil_div(last, p.co_block);
   for (int i = 0; i < 3; ++i) {
+    a.rqc[i] = (per_channel && i < nw) ? d->rq_channel[i] : nullptr;
     a.act[i] = d->act[i];
     a.rq[i].mult = d->rq[i].mult;
     a.rq[i].shift = d->rq[i].shift;
@@ -287,7 +300,7 @@ fcm_status fcm_plan(int32_t op, const fcm_desc* desc, const fcm_hw_desc* hw, fcm
   if (!out) return fail(FCM_EINVAL, "output plan is NULL");
   fcm_status st = validate(op, desc);
   if (st != FCM_OK) return st;
-  return find_plan(op, desc, hw, out);
+  return find_plan(op, desc, hw, out, !has_per_channel_rq(op, desc));
 }
 
 fcm_status fcm_plan_evaluate(const fcm_desc* desc, const fcm_hw_desc* hw, fcm_plan_t* plan) {

@@ -94,6 +94,16 @@ __device__ __forceinline__ int32_t requant(int32_t acc, const Requant& rq, int a
   return (int32_t)q;
 }
 
+// The requantisation of channel c: its own multiplier and shift when the stage has
+// per-channel ones (shift kept in [0, 62]), the stage's clamp range either way.
+__device__ __forceinline__ Requant rq_at(const Requant& rq, const ReqCh& pc, int c) {
+  if (!pc.p) return rq;
+  Requant r = rq;
+  r.mult = pc.p[c];
+  r.shift = min(max(pc.p[pc.n + c], 0), 62);
+  return r;
+}
+
 // Finish one accumulator (+bias, activation, cast) into storage bits.
 template <class DT>
 struct Fin;
@@ -485,9 +495,12 @@ struct Vec<TI8> {
   }
 };
 
+// pc / ch0: per-channel requantisation of the stage (int8) and the global channel of the
+// block's first channel (ch_valid channels exist).
 template <class DT, int K, int S, int R>
 __device__ __forceinline__ void dw_compute(const char* sin, int ips, int IW, const typename DT::Acc* swd, int CB, int TH, int TW,
-                           int act, const Requant& rq, char* sout, int ops) {
+                           int act, const Requant& rq, char* sout, int ops, ReqCh pc = ReqCh{}, int ch0 = 0,
+                           int ch_valid = 1) {
   using Acc = typename DT::Acc;
   constexpr int CPT = DT::CPT;
   constexpr int NIN = (R - 1) * S + K;
@@ -524,15 +537,18 @@ __device__ __forceinline__ void dw_compute(const char* sin, int ips, int IW, con
       }
     }
     const Acc* bias = swd + K * K * CB + g * CPT;
+    Requant rqe[CPT];
+#pragma unroll
+    for (int e = 0; e < CPT; ++e) rqe[e] = rq_at(rq, pc, min(ch0 + g * CPT + e, ch_valid - 1));
 #pragma unroll
     for (int r = 0; r < R; ++r) {
       char* o = sout + (ty * TW + tx0 + r) * ops + g * CPT * DT::ELT;
 #pragma unroll
       for (int e = 0; e < CPT; e += 4) {
-        lds_store4<DT>(o + e * DT::ELT, Fin<DT>::apply(acc[r][e + 0], bias[e + 0], act, rq),
-                       Fin<DT>::apply(acc[r][e + 1], bias[e + 1], act, rq),
-                       Fin<DT>::apply(acc[r][e + 2], bias[e + 2], act, rq),
-                       Fin<DT>::apply(acc[r][e + 3], bias[e + 3], act, rq));
+        lds_store4<DT>(o + e * DT::ELT, Fin<DT>::apply(acc[r][e + 0], bias[e + 0], act, rqe[e + 0]),
+                       Fin<DT>::apply(acc[r][e + 1], bias[e + 1], act, rqe[e + 1]),
+                       Fin<DT>::apply(acc[r][e + 2], bias[e + 2], act, rqe[e + 2]),
+                       Fin<DT>::apply(acc[r][e + 3], bias[e + 3], act, rqe[e + 3]));
       }
     }
   }
@@ -551,7 +567,7 @@ template <class DT, int TMW, int TNW>
 __device__ __forceinline__ void acc_to_lds(const typename DT::AccV (&acc)[TMW][TNW], int m_base, int n_base,
                                            int m_wr, int n_act, const void* bias, int bias_off, int m_valid,
                                            int act, const Requant& rq, char* so, int rs, int mask_iw, int iy0,
-                                           int ix0, int H, int W) {
+                                           int ix0, int H, int W, ReqCh pc = ReqCh{}) {
   const int lane = threadIdx.x & 63;
   const int r = lane & 15, g = lane >> 4;
 #pragma unroll
@@ -559,10 +575,12 @@ __device__ __forceinline__ void acc_to_lds(const typename DT::AccV (&acc)[TMW][T
     if (i >= m_wr) continue;
     const int m = m_base + i * 16 + 4 * g;
     typename DT::Acc b[4];
+    Requant rqv[4];
 #pragma unroll
     for (int v = 0; v < 4; ++v) {  // unconditional load at a clamped index, then select
       b[v] = load_bias<DT>(bias, bias_off + min(m + v, m_valid - 1));
       if (m + v >= m_valid) b[v] = 0;
+      rqv[v] = rq_at(rq, pc, bias_off + min(m + v, m_valid - 1));
     }
 #pragma unroll
     for (int j = 0; j < TNW; ++j) {
@@ -570,7 +588,7 @@ __device__ __forceinline__ void acc_to_lds(const typename DT::AccV (&acc)[TMW][T
       const int n = n_base + j * 16 + r;
       uint32_t o[4];
 #pragma unroll
-      for (int v = 0; v < 4; ++v) o[v] = Fin<DT>::apply(acc[i][j][v], b[v], act, rq);
+      for (int v = 0; v < 4; ++v) o[v] = Fin<DT>::apply(acc[i][j][v], b[v], act, rqv[v]);
       if (mask_iw > 0) {
         const int qy = n / mask_iw, qx = n - qy * mask_iw;
         const int gy = iy0 + qy, gx = ix0 + qx;

@@ -35,6 +35,13 @@ struct Requant {
   int32_t mult, shift, qmin, qmax;
 };
 
+// int8 per-channel requantisation of one stage: p = device array [2][n] (the stage's n
+// output channels' multipliers, then their shifts); p == nullptr: the per-tensor Requant.
+struct ReqCh {
+  const int32_t* p = nullptr;
+  int n = 0;
+};
+
 FCM_HD inline int elt_size(int dt) { return dt == DT_F32 ? 4 : (dt == DT_BF16 ? 2 : 1); }
 // contraction elements per MFMA operand step (64 bytes of k per row)
 FCM_HD inline int k_block(int dt) { return 64 / elt_size(dt); }
@@ -276,6 +283,7 @@ struct KArgs {
   void* ws;      // splits > 1: partial sums [split][work tile][TH*TW][COB] (fp32 / int32)
   int cus;       // compute units of the device
   int grid_cap;  // persistent kernels: at most this many workgroups (0 = no cap)
+  const int32_t* rqc[3];  // int8 per-channel requantisation per stage ([2][channels]) or nullptr
   unsigned long long* trace;  // development timeline buffer (used only in FCM_TRACE builds)
 };
 

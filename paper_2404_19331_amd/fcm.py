@@ -42,7 +42,7 @@ class Desc(ctypes.Structure):
                 ("c_in", ctypes.c_int32), ("c_mid", ctypes.c_int32), ("c_out", ctypes.c_int32),
                 ("k", ctypes.c_int32), ("stride", ctypes.c_int32), ("pad", ctypes.c_int32),
                 ("dtype", ctypes.c_int32), ("layout", ctypes.c_int32),
-                ("act", ctypes.c_int32 * 3), ("rq", Requant * 3)]
+                ("act", ctypes.c_int32 * 3), ("rq", Requant * 3), ("rq_channel", ctypes.c_void_p * 3)]
 
 
 class HwDesc(ctypes.Structure):
@@ -164,7 +164,7 @@ def _check(st):
 
 
 def make_desc(n, h, w, c_in, c_mid, c_out, k=3, stride=1, pad=1, dtype="f32", layout="nchw",
-              act=("none", "none", "none"), rq=None):
+              act=("none", "none", "none"), rq=None, rq_channel=None):
     d = Desc()
     d.n, d.h, d.w = n, h, w
     d.c_in, d.c_mid, d.c_out = c_in, c_mid, c_out
@@ -177,6 +177,15 @@ def make_desc(n, h, w, c_in, c_mid, c_out, k=3, stride=1, pad=1, dtype="f32", la
     rqs = (list(rq or []) + [(1, 0, -128, 127)] * 3)[:3]
     for i, r in enumerate(rqs):
         d.rq[i].mult, d.rq[i].shift, d.rq[i].qmin, d.rq[i].qmax = (int(v) for v in r)
+    # int8 per-channel requantisation: device int32 tensors [2 * channels] per stage or None
+    d._keep = []
+    for i, t in enumerate(list(rq_channel or [])[:3]):
+        if t is None:
+            continue
+        if not (t.is_cuda and t.dtype == _torch().int32 and t.is_contiguous()):
+            raise ValueError("rq_channel entries must be contiguous int32 device tensors")
+        d.rq_channel[i] = t.data_ptr()
+        d._keep.append(t)
     return d
 
 
@@ -312,7 +321,7 @@ def _kk(w_dw):
     return int(w_dw.shape[-1])
 
 
-def dw_pw(x, w_dw, w_pw, b_dw=None, b_pw=None, *, stride=1, pad=None, act=("none", "none"), rq=None,
+def dw_pw(x, w_dw, w_pw, b_dw=None, b_pw=None, *, stride=1, pad=None, act=("none", "none"), rq=None, rq_channel=None,
           layout="nchw", plan=None, out=None, stream=None, prepare=False):
     """DW -> PW module in one kernel. Returns y [n, c_out, h_o, w_o] in `layout`."""
     dt = _dtype_name(x)
@@ -321,14 +330,14 @@ def dw_pw(x, w_dw, w_pw, b_dw=None, b_pw=None, *, stride=1, pad=None, act=("none
     pad = (k - 1) // 2 if pad is None else pad
     co = int(w_pw.shape[0])
     _prep(x, [w_dw, w_pw], [b_dw, b_pw], dt)
-    d = make_desc(n, h, w, c, c, co, k, stride, pad, dt, layout, act, rq)
+    d = make_desc(n, h, w, c, c, co, k, stride, pad, dt, layout, act, rq, rq_channel=rq_channel)
     ho, wo = out_hw(h, w, k, stride, pad)
     y = _out(x, layout, n, co, ho, wo, out)
     return _call(lib().fcm_dw_pw, (ctypes.byref(d), _ptr(x), _ptr(w_dw), _ptr(b_dw), _ptr(w_pw), _ptr(b_pw),
                                    _ptr(y), _plan_arg(plan), _stream(x, stream)), y, prepare)
 
 
-def pw_dw(x, w_pw, w_dw, b_pw=None, b_dw=None, *, stride=1, pad=None, act=("none", "none"), rq=None,
+def pw_dw(x, w_pw, w_dw, b_pw=None, b_dw=None, *, stride=1, pad=None, act=("none", "none"), rq=None, rq_channel=None,
           layout="nchw", plan=None, out=None, stream=None, prepare=False):
     """PW -> DW module in one kernel. Returns y [n, c_mid, h_o, w_o]."""
     dt = _dtype_name(x)
@@ -337,7 +346,7 @@ def pw_dw(x, w_pw, w_dw, b_pw=None, b_dw=None, *, stride=1, pad=None, act=("none
     pad = (k - 1) // 2 if pad is None else pad
     cm = int(w_pw.shape[0])
     _prep(x, [w_pw, w_dw], [b_pw, b_dw], dt)
-    d = make_desc(n, h, w, c, cm, cm, k, stride, pad, dt, layout, act, rq)
+    d = make_desc(n, h, w, c, cm, cm, k, stride, pad, dt, layout, act, rq, rq_channel=rq_channel)
     ho, wo = out_hw(h, w, k, stride, pad)
     y = _out(x, layout, n, cm, ho, wo, out)
     return _call(lib().fcm_pw_dw, (ctypes.byref(d), _ptr(x), _ptr(w_pw), _ptr(b_pw), _ptr(w_dw), _ptr(b_dw),
@@ -345,7 +354,7 @@ def pw_dw(x, w_pw, w_dw, b_pw=None, b_dw=None, *, stride=1, pad=None, act=("none
 
 
 def pw_dw_pw(x, w_pw1, w_dw, w_pw2, b_pw1=None, b_dw=None, b_pw2=None, *, stride=1, pad=None,
-             act=("none", "none", "none"), rq=None, layout="nchw", plan=None, out=None, stream=None,
+             act=("none", "none", "none"), rq=None, rq_channel=None, layout="nchw", plan=None, out=None, stream=None,
              prepare=False):
     """PW -> DW -> PW inverted residual in one kernel. Returns y [n, c_out, h_o, w_o]."""
     dt = _dtype_name(x)
@@ -354,7 +363,7 @@ def pw_dw_pw(x, w_pw1, w_dw, w_pw2, b_pw1=None, b_dw=None, b_pw2=None, *, stride
     pad = (k - 1) // 2 if pad is None else pad
     cm, co = int(w_pw1.shape[0]), int(w_pw2.shape[0])
     _prep(x, [w_pw1, w_dw, w_pw2], [b_pw1, b_dw, b_pw2], dt)
-    d = make_desc(n, h, w, c, cm, co, k, stride, pad, dt, layout, act, rq)
+    d = make_desc(n, h, w, c, cm, co, k, stride, pad, dt, layout, act, rq, rq_channel=rq_channel)
     ho, wo = out_hw(h, w, k, stride, pad)
     y = _out(x, layout, n, co, ho, wo, out)
     return _call(lib().fcm_pw_dw_pw, (ctypes.byref(d), _ptr(x), _ptr(w_pw1), _ptr(b_pw1), _ptr(w_dw), _ptr(b_dw),
@@ -362,20 +371,20 @@ def pw_dw_pw(x, w_pw1, w_dw, w_pw2, b_pw1=None, b_dw=None, b_pw2=None, *, stride
                  y, prepare)
 
 
-def pw_pw(x, w_pw1, w_pw2, b_pw1=None, b_pw2=None, *, act=("none", "none"), rq=None, layout="nchw", plan=None,
+def pw_pw(x, w_pw1, w_pw2, b_pw1=None, b_pw2=None, *, act=("none", "none"), rq=None, rq_channel=None, layout="nchw", plan=None,
           out=None, stream=None, prepare=False):
     """PW -> PW module in one kernel. Returns y [n, c_out, h, w]."""
     dt = _dtype_name(x)
     n, c, h, w = _dims(x, layout)
     cm, co = int(w_pw1.shape[0]), int(w_pw2.shape[0])
     _prep(x, [w_pw1, w_pw2], [b_pw1, b_pw2], dt)
-    d = make_desc(n, h, w, c, cm, co, 1, 1, 0, dt, layout, act, rq)
+    d = make_desc(n, h, w, c, cm, co, 1, 1, 0, dt, layout, act, rq, rq_channel=rq_channel)
     y = _out(x, layout, n, co, h, w, out)
     return _call(lib().fcm_pw_pw, (ctypes.byref(d), _ptr(x), _ptr(w_pw1), _ptr(b_pw1), _ptr(w_pw2), _ptr(b_pw2),
                                    _ptr(y), _plan_arg(plan), _stream(x, stream)), y, prepare)
 
 
-def dw(x, w_dw, b_dw=None, *, stride=1, pad=None, act="none", rq=None, layout="nchw", plan=None, out=None,
+def dw(x, w_dw, b_dw=None, *, stride=1, pad=None, act="none", rq=None, rq_channel=None, layout="nchw", plan=None, out=None,
        stream=None, prepare=False):
     """Single depthwise layer (layer-by-layer kernel)."""
     dt = _dtype_name(x)
@@ -383,21 +392,21 @@ def dw(x, w_dw, b_dw=None, *, stride=1, pad=None, act="none", rq=None, layout="n
     k = _kk(w_dw)
     pad = (k - 1) // 2 if pad is None else pad
     _prep(x, [w_dw], [b_dw], dt)
-    d = make_desc(n, h, w, c, c, c, k, stride, pad, dt, layout, (act,), [rq] if rq else None)
+    d = make_desc(n, h, w, c, c, c, k, stride, pad, dt, layout, (act,), [rq] if rq else None, rq_channel=rq_channel)
     ho, wo = out_hw(h, w, k, stride, pad)
     y = _out(x, layout, n, c, ho, wo, out)
     return _call(lib().fcm_dw, (ctypes.byref(d), _ptr(x), _ptr(w_dw), _ptr(b_dw), _ptr(y), _plan_arg(plan),
                                 _stream(x, stream)), y, prepare)
 
 
-def pw(x, w_pw, b_pw=None, *, act="none", rq=None, layout="nchw", plan=None, out=None, stream=None,
+def pw(x, w_pw, b_pw=None, *, act="none", rq=None, rq_channel=None, layout="nchw", plan=None, out=None, stream=None,
        prepare=False):
     """Single pointwise layer (layer-by-layer kernel)."""
     dt = _dtype_name(x)
     n, c, h, w = _dims(x, layout)
     co = int(w_pw.shape[0])
     _prep(x, [w_pw], [b_pw], dt)
-    d = make_desc(n, h, w, c, c, co, 1, 1, 0, dt, layout, (act,), [rq] if rq else None)
+    d = make_desc(n, h, w, c, c, co, 1, 1, 0, dt, layout, (act,), [rq] if rq else None, rq_channel=rq_channel)
     y = _out(x, layout, n, co, h, w, out)
     return _call(lib().fcm_pw, (ctypes.byref(d), _ptr(x), _ptr(w_pw), _ptr(b_pw), _ptr(y), _plan_arg(plan),
                                 _stream(x, stream)), y, prepare)

@@ -73,9 +73,12 @@ def dev_inputs(inp, dtype):
     return {k: to_dev(v, dtype) for k, v in inp.items()}
 
 
-def run_fused(case, d, plan=None, out=None):
-    """Run the case's module on the GPU through the C ABI. d: dict of device tensors."""
+def run_fused(case, d, plan=None, out=None, rq_channel=None):
+    """Run the case's module on the GPU through the C ABI. d: dict of device tensors.
+    rq_channel: int8 per-channel requantisation tensors per stage (or None)."""
     kw = dict(stride=case.stride, pad=case.pad, layout=case.layout, plan=plan, out=out)
+    if rq_channel is not None:
+        kw["rq_channel"] = rq_channel
     rq = list(case.rq) if case.dtype == "i8" else None
     if case.op == "dw_pw":
         return fcm.dw_pw(d["x"], d["w_dw"], d["w_pw"], d.get("b_dw"), d.get("b_pw"), act=case.act[:2], rq=rq, **kw)

@@ -13,6 +13,7 @@ from paper_2404_19331_amd import fcm
 from paper_2404_19331_amd.workloads import (Case, make_inputs, config_c1, config_c2, config_c3, config_c4, config_c5,
                                              config_pwpw)
 
+import oracle
 from gpu_util import (assert_close, batch_slice, dev_inputs, oracle_ref, run_fused, run_unfused, to_np, torch)
 
 pytestmark = pytest.mark.gpu
@@ -212,3 +213,37 @@ def test_every_output_element_is_written():
     out = torch().full(ref.shape, float("nan"), dtype=torch().float32, device="cuda")
     got = to_np(run_fused(case, d, out=out))
     assert_close(got, ref, case.dtype, "nan-poisoned output")
+
+
+# ---------------------------------------------------------------------------------
+# int8 per-channel requantisation (first-generation kernels)
+# ---------------------------------------------------------------------------------
+
+PC_OPS = [("dw_pw", 24, 24, 16, 3), ("pw_dw", 16, 40, 40, 3), ("pw_dw_pw", 16, 40, 12, 3), ("pw_pw", 20, 36, 12, 1),
+          ("dw", 24, 24, 24, 5), ("pw", 24, 24, 20, 1)]
+
+
+@pytest.mark.parametrize("layout", ["nhwc", "nchw"])
+@pytest.mark.parametrize("op,ci,cm,co,k", PC_OPS)
+def test_per_channel_requant_parity(op, ci, cm, co, k, layout):
+    case = Case(op, 2, 11, 9, ci, cm, co, k, 1, k // 2, "i8", layout, ("relu", "relu6", "none"),
+                ((1, 6, -127, 127), (1, 7, -128, 40), (1, 6, -127, 127)), dist_x="i8small", dist_w="i8small",
+                bias=True, seed=3000 + len(op) + k, name="pc-%s-%s" % (op, layout))
+    chans = {"dw_pw": [ci, co], "pw_dw": [cm, cm], "pw_dw_pw": [cm, cm, co], "pw_pw": [cm, co], "dw": [ci],
+             "pw": [co]}[op]
+    rng = np.random.default_rng(11)
+    pcs = [(rng.integers(1, 8, n), rng.integers(4, 10, n)) for n in chans]
+    inp = make_inputs(case)
+    ref = oracle.run(op, dict(case.as_dict(), rq_channel=pcs), inp)
+    d = dev_inputs(inp, case.dtype)
+    T = torch()
+    rqc = [T.from_numpy(np.concatenate(pc).astype(np.int32)).cuda() for pc in pcs]
+    got = to_np(run_fused(case, d, rq_channel=rqc))
+    assert_close(got, ref, "i8", case.name)
+    # the shared scale gives another result (the per-channel scales were used)
+    assert not np.array_equal(got, to_np(run_fused(case, d)))
+    desc = fcm.desc_from_case(case)
+    name = fcm.variant_name(fcm.plan(op, fcm.make_desc(desc.n, desc.h, desc.w, desc.c_in, desc.c_mid, desc.c_out,
+                                                       desc.k, desc.stride, desc.pad, "i8", layout,
+                                                       rq_channel=rqc)).variant)
+    assert not any(g in name for g in ("3<", "4<", "2<")), name

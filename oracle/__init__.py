@@ -38,7 +38,7 @@ class OracleError(RuntimeError):
 
 class _Rq(ctypes.Structure):
     _fields_ = [("mult", ctypes.c_int32), ("shift", ctypes.c_int32),
-                ("qmin", ctypes.c_int32), ("qmax", ctypes.c_int32)]
+                ("qmin", ctypes.c_int32), ("qmax", ctypes.c_int32), ("zero_point", ctypes.c_int32)]
 
 
 class _Desc(ctypes.Structure):
@@ -47,7 +47,7 @@ class _Desc(ctypes.Structure):
                 ("k", ctypes.c_int32), ("stride", ctypes.c_int32), ("pad", ctypes.c_int32),
                 ("dtype", ctypes.c_int32), ("layout", ctypes.c_int32),
                 ("act", ctypes.c_int32 * 3), ("rq", _Rq * 3),
-                ("rqc", ctypes.POINTER(ctypes.c_int32) * 3)]
+                ("rqc", ctypes.POINTER(ctypes.c_int32) * 3), ("zp_in", ctypes.c_int32)]
 
 
 def build(force=False):
@@ -114,7 +114,10 @@ def _desc(case):
     rqs = list(_get(case, "rq", ()) or ())
     rqs = (rqs + [(1, 0, -128, 127)] * 3)[:3]
     for i, r in enumerate(rqs):
-        d.rq[i].mult, d.rq[i].shift, d.rq[i].qmin, d.rq[i].qmax = (int(v) for v in r)
+        # (mult, shift, qmin, qmax[, zero point of the stage's output])
+        r = tuple(r) + (0,) * (5 - len(r))
+        d.rq[i].mult, d.rq[i].shift, d.rq[i].qmin, d.rq[i].qmax, d.rq[i].zero_point = (int(v) for v in r)
+    d.zp_in = int(_get(case, "zp_in", 0) or 0)  # int8 zero point of the input
     # int8 per-channel requantisation: rq_channel[i] = (multipliers, shifts) of stage i's
     # output channels, or None for the per-tensor rq[i]
     d._keep = []

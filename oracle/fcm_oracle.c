@@ -20,7 +20,8 @@
  * the normalisation and activation following it). Accumulation is exact: double for
  * the float paths, int64 for int8 (whose intermediate is requantised to int8 before
  * the next stage, Sec. III-B: INT8 results are packed before being written to any
- * buffer).
+ * buffer). int8 tensors may be asymmetric: a code q stands for scale * (q - zero point),
+ * and every stage convolves codes minus their zero point, so padding is real 0.
  *
  * Who may use this file: the test-suite, the smoke check and the CPU-baseline leg of
  * the benchmark. The product path (the HIP library) never loads or calls it, and this
@@ -41,8 +42,10 @@ enum { ORC_NCHW = 0, ORC_NHWC = 1 };
 enum { ORC_ACT_NONE = 0, ORC_ACT_RELU = 1, ORC_ACT_RELU6 = 2 };
 enum { ORC_OK = 0, ORC_EINVAL = 1, ORC_EUNSUPPORTED = 2, ORC_EOVERFLOW = 3 };
 
+/* int8 requantisation of a stage's output. zero_point is the code of real 0 in that
+ * output (asymmetric quantisation: a code q stands for scale * (q - zero_point)). */
 typedef struct {
-  int32_t mult, shift, qmin, qmax;
+  int32_t mult, shift, qmin, qmax, zero_point;
 } orc_rq;
 
 typedef struct {
@@ -56,6 +59,8 @@ typedef struct {
    * 2 x (the stage's output channels), the multipliers then the shifts; qmin/qmax stay
    * those of rq[i] */
   const int32_t* rqc[3];
+  /* int8 zero point of the input x; stage i > 0 takes its input's from rq[i-1] */
+  int32_t zp_in;
 } orc_desc;
 
 /* ------------------------------------------------------------------------- */
@@ -275,10 +280,12 @@ static void finish_f(double* v, size_t cnt, int act, int dtype) {
   for (size_t i = 0; i < cnt; ++i) v[i] = cast_f(act_f(v[i], act), dtype);
 }
 
-/* int8 tail: requantise (RNE + saturate), then ReLU. Both maps are monotone and fix
- * zero, so the order of ReLU and requantisation does not change the result. ReLU6 is the
- * quantised clamp: below at 0, above at qmax, which carries 6.0 in the output's
- * quantised units (the upper clamp is the requantisation's own saturation).
+/* int8 tail: requantise (RNE), add the output zero point, saturate to [qmin, qmax], then
+ * ReLU, which in the quantised domain clamps below at the zero point (the code of real 0).
+ * With a zero point of 0 both maps are monotone and fix zero, so the order of ReLU and
+ * requantisation does not change the result. ReLU6 is the quantised clamp: below at the
+ * zero point, above at qmax, which carries 6.0 in the output's quantised units (the upper
+ * clamp is the requantisation's own saturation).
  * Returns ORC_EOVERFLOW when an accumulator does not fit the 32-bit accumulator
  * the method prescribes (Sec. III-B: four-way dot product with 32-bit accumulate). */
 static int finish_i(int64_t* v, size_t cnt, int C, size_t HW, int act, orc_rq rq, const int32_t* rqc) {
@@ -291,11 +298,20 @@ static int finish_i(int64_t* v, size_t cnt, int C, size_t HW, int act, orc_rq rq
       shift = rqc[C + c];
       if (shift < 0 || shift > 62) return ORC_EINVAL;
     }
-    int64_t q = orc_requant(v[i], mult, shift, rq.qmin, rq.qmax);
-    if (act != ORC_ACT_NONE && q < 0) q = 0;
+    /* rounding only (int32-wide clamp: the int8 clamp below makes it immaterial) */
+    int64_t q = orc_requant(v[i], mult, shift, INT32_MIN, INT32_MAX) + rq.zero_point;
+    if (q < rq.qmin) q = rq.qmin;
+    if (q > rq.qmax) q = rq.qmax;
+    if (act != ORC_ACT_NONE && q < rq.zero_point) q = rq.zero_point;
     v[i] = q;
   }
   return ORC_OK;
+}
+
+/* The value a stage convolves is the real one up to the scale: code minus zero point.
+ * So a zero-padded position (real 0) contributes nothing, whatever the zero point. */
+static void center_i(int64_t* v, size_t cnt, int32_t zero_point) {
+  for (size_t i = 0; i < cnt; ++i) v[i] -= zero_point;
 }
 
 /* ------------------------------------------------------------------------- */
@@ -314,8 +330,10 @@ static int check_common(const orc_desc* d) {
     if (d->dtype == ORC_I8) {
       if (d->rq[i].shift < 0 || d->rq[i].shift > 62) return ORC_EINVAL;
       if (d->rq[i].qmin > d->rq[i].qmax || d->rq[i].qmin < -128 || d->rq[i].qmax > 127) return ORC_EINVAL;
+      if (d->rq[i].zero_point < -128 || d->rq[i].zero_point > 127) return ORC_EINVAL;
     }
   }
+  if (d->dtype == ORC_I8 && (d->zp_in < -128 || d->zp_in > 127)) return ORC_EINVAL;
   return ORC_OK;
 }
 
@@ -348,6 +366,7 @@ int orc_dw(const orc_desc* d, const void* x, const void* wd, const void* bd, voi
   size_t no = (size_t)N * C * Ho * Wo;
   if (d->dtype == ORC_I8) {
     int64_t* xi = load_fmap_i((const int8_t*)x, d->layout, N, C, H, W);
+    center_i(xi, (size_t)N * C * H * W, d->zp_in);
     int64_t* wi = load_vec_i((const int8_t*)wd, (size_t)C * K * K);
     int64_t* yi = (int64_t*)malloc(no * sizeof(int64_t));
     dw_stage_i(xi, N, C, H, W, wi, (const int32_t*)bd, K, S, P, Ho, Wo, yi);
@@ -375,6 +394,7 @@ int orc_pw(const orc_desc* d, const void* x, const void* wp, const void* bp, voi
   size_t no = (size_t)N * Co * H * W;
   if (d->dtype == ORC_I8) {
     int64_t* xi = load_fmap_i((const int8_t*)x, d->layout, N, C, H, W);
+    center_i(xi, (size_t)N * C * H * W, d->zp_in);
     int64_t* wi = load_vec_i((const int8_t*)wp, (size_t)Co * C);
     int64_t* yi = (int64_t*)malloc(no * sizeof(int64_t));
     pw_stage_i(xi, N, C, H, W, wi, (const int32_t*)bp, Co, yi);
@@ -405,12 +425,14 @@ int orc_dw_pw(const orc_desc* d, const void* x, const void* wd, const void* bd, 
   size_t nm = (size_t)N * C * Ho * Wo, no = (size_t)N * Co * Ho * Wo;
   if (d->dtype == ORC_I8) {
     int64_t* xi = load_fmap_i((const int8_t*)x, d->layout, N, C, H, W);
+    center_i(xi, (size_t)N * C * H * W, d->zp_in);
     int64_t* wdi = load_vec_i((const int8_t*)wd, (size_t)C * K * K);
     int64_t* wpi = load_vec_i((const int8_t*)wp, (size_t)Co * C);
     int64_t* mi = (int64_t*)malloc(nm * sizeof(int64_t));
     int64_t* yi = (int64_t*)malloc(no * sizeof(int64_t));
     dw_stage_i(xi, N, C, H, W, wdi, (const int32_t*)bd, K, S, P, Ho, Wo, mi);
     st = finish_i(mi, nm, C, (size_t)Ho * Wo, d->act[0], d->rq[0], d->rqc[0]);
+    if (!st) center_i(mi, nm, d->rq[0].zero_point);
     if (!st) {
       pw_stage_i(mi, N, C, Ho, Wo, wpi, (const int32_t*)bp, Co, yi);
       st = finish_i(yi, no, Co, (size_t)Ho * Wo, d->act[1], d->rq[1], d->rqc[1]);
@@ -434,7 +456,8 @@ int orc_dw_pw(const orc_desc* d, const void* x, const void* wd, const void* bd, 
 }
 
 /* PW -> DW. The PW output (c_mid channels, h x w) is the DW input, zero padded by the
- * DW like any other input: positions outside the image are 0, never act(bias).
+ * DW like any other input: positions outside the image are real 0, never act(bias)
+ * (for int8, the code of real 0 is the intermediate's zero point).
  * c_out must equal c_mid. */
 int orc_pw_dw(const orc_desc* d, const void* x, const void* wp, const void* bp, const void* wd,
               const void* bd, void* y) {
@@ -447,12 +470,14 @@ int orc_pw_dw(const orc_desc* d, const void* x, const void* wp, const void* bp, 
   size_t nm = (size_t)N * Cm * H * W, no = (size_t)N * Cm * Ho * Wo;
   if (d->dtype == ORC_I8) {
     int64_t* xi = load_fmap_i((const int8_t*)x, d->layout, N, Ci, H, W);
+    center_i(xi, (size_t)N * Ci * H * W, d->zp_in);
     int64_t* wpi = load_vec_i((const int8_t*)wp, (size_t)Cm * Ci);
     int64_t* wdi = load_vec_i((const int8_t*)wd, (size_t)Cm * K * K);
     int64_t* mi = (int64_t*)malloc(nm * sizeof(int64_t));
     int64_t* yi = (int64_t*)malloc(no * sizeof(int64_t));
     pw_stage_i(xi, N, Ci, H, W, wpi, (const int32_t*)bp, Cm, mi);
     st = finish_i(mi, nm, Cm, (size_t)H * W, d->act[0], d->rq[0], d->rqc[0]);
+    if (!st) center_i(mi, nm, d->rq[0].zero_point);
     if (!st) {
       dw_stage_i(mi, N, Cm, H, W, wdi, (const int32_t*)bd, K, S, P, Ho, Wo, yi);
       st = finish_i(yi, no, Cm, (size_t)Ho * Wo, d->act[1], d->rq[1], d->rqc[1]);
@@ -486,12 +511,14 @@ int orc_pw_pw(const orc_desc* d, const void* x, const void* wp1, const void* bp1
   size_t nm = (size_t)N * Cm * H * W, no = (size_t)N * Co * H * W;
   if (d->dtype == ORC_I8) {
     int64_t* xi = load_fmap_i((const int8_t*)x, d->layout, N, Ci, H, W);
+    center_i(xi, (size_t)N * Ci * H * W, d->zp_in);
     int64_t* w1 = load_vec_i((const int8_t*)wp1, (size_t)Cm * Ci);
     int64_t* w2 = load_vec_i((const int8_t*)wp2, (size_t)Co * Cm);
     int64_t* mi = (int64_t*)malloc(nm * sizeof(int64_t));
     int64_t* yi = (int64_t*)malloc(no * sizeof(int64_t));
     pw_stage_i(xi, N, Ci, H, W, w1, (const int32_t*)bp1, Cm, mi);
     st = finish_i(mi, nm, Cm, (size_t)H * W, d->act[0], d->rq[0], d->rqc[0]);
+    if (!st) center_i(mi, nm, d->rq[0].zero_point);
     if (!st) {
       pw_stage_i(mi, N, Cm, H, W, w2, (const int32_t*)bp2, Co, yi);
       st = finish_i(yi, no, Co, (size_t)H * W, d->act[1], d->rq[1], d->rqc[1]);
@@ -527,6 +554,7 @@ int orc_pw_dw_pw(const orc_desc* d, const void* x, const void* wp1, const void* 
   size_t n1 = (size_t)N * Cm * H * W, n2 = (size_t)N * Cm * Ho * Wo, no = (size_t)N * Co * Ho * Wo;
   if (d->dtype == ORC_I8) {
     int64_t* xi = load_fmap_i((const int8_t*)x, d->layout, N, Ci, H, W);
+    center_i(xi, (size_t)N * Ci * H * W, d->zp_in);
     int64_t* w1 = load_vec_i((const int8_t*)wp1, (size_t)Cm * Ci);
     int64_t* wdi = load_vec_i((const int8_t*)wd, (size_t)Cm * K * K);
     int64_t* w2 = load_vec_i((const int8_t*)wp2, (size_t)Co * Cm);
@@ -535,9 +563,11 @@ int orc_pw_dw_pw(const orc_desc* d, const void* x, const void* wp1, const void* 
     int64_t* yi = (int64_t*)malloc(no * sizeof(int64_t));
     pw_stage_i(xi, N, Ci, H, W, w1, (const int32_t*)bp1, Cm, m1);
     st = finish_i(m1, n1, Cm, (size_t)H * W, d->act[0], d->rq[0], d->rqc[0]);
+    if (!st) center_i(m1, n1, d->rq[0].zero_point);
     if (!st) {
       dw_stage_i(m1, N, Cm, H, W, wdi, (const int32_t*)bd, K, S, P, Ho, Wo, m2);
       st = finish_i(m2, n2, Cm, (size_t)Ho * Wo, d->act[1], d->rq[1], d->rqc[1]);
+    if (!st) center_i(m2, n2, d->rq[1].zero_point);
     }
     if (!st) {
       pw_stage_i(m2, N, Cm, Ho, Wo, w2, (const int32_t*)bp2, Co, yi);

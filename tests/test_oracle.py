@@ -621,3 +621,130 @@ def test_per_channel_requant_hand_values():
     c = dict(n=1, h=1, w=1, c_in=2, c_mid=2, c_out=2, k=1, stride=1, pad=0, dtype="i8", layout="nhwc",
              act=["none"] * 3, rq=[(1, 0, -127, 127)] * 3, rq_channel=[(np.array([3, 1]), np.array([2, 3]))])
     assert oracle.pw(c, x, w, None).ravel().tolist() == [30, 6]
+
+
+# --------------------------------------------------------------------------------------
+# Asymmetric int8: zero points (a code q stands for scale * (q - zero point))
+# --------------------------------------------------------------------------------------
+
+ZP_OPS = ["dw_pw", "pw_dw", "pw_pw", "pw_dw_pw", "dw", "pw"]
+
+
+def _zp_case(op, **kw):
+    c = _i8_case(op, 12, 12 if op in ("dw_pw", "dw") else 20, 12 if op in ("dw", "pw_dw") else 8,
+                 k=1 if op in ("pw", "pw_pw") else 3, s=2 if op in ("dw_pw", "pw_dw_pw") else 1)
+    if op == "pw_dw":
+        c["c_out"] = c["c_mid"]
+    c.update(kw)
+    return c
+
+
+@pytest.mark.parametrize("op", ZP_OPS)
+def test_input_zero_point_equals_centred_input(op):
+    """With input zero point z, every module equals the symmetric (z = 0) module run on the
+    centred codes x - z (whenever those fit int8): zero padding means real 0 in both,
+    so a padding or centring mistake in any stage shows at the borders."""
+    z = 5
+    c = _zp_case(op)
+    inp = _i8_inputs(c)  # x in [-8, 8], so x + z fits int8
+    shifted = dict(inp, x=(inp["x"].astype(np.int16) + z).astype(np.int8))
+    got = oracle.run(op, dict(c, zp_in=z), shifted)
+    assert np.array_equal(got, oracle.run(op, c, inp))
+    # not vacuous: the same codes read as symmetric differ
+    assert not np.array_equal(oracle.run(op, c, shifted), got)
+
+
+@pytest.mark.parametrize("op", ["dw_pw", "pw_dw", "pw_pw", "pw_dw_pw"])
+def test_intermediate_zero_point_is_invisible_without_saturation(op):
+    """A zero point on an intermediate only relabels its codes: when no intermediate code
+    saturates, the module's output does not depend on it (the next stage subtracts what
+    the previous one added, and pads with the new code of real 0)."""
+    rq = [(1, 9, -128, 127), (1, 9, -128, 127), (1, 5, -128, 127)]
+    c = _zp_case(op, rq=rq, act=["relu", "relu", "none"])
+    inp = _i8_inputs(c)
+    ref = oracle.run(op, c, inp)
+    nstages = 3 if op == "pw_dw_pw" else 2
+    for zs in ((17,), (-23,), (40, -31)):
+        rqz = [tuple(r) + (zs[i] if i < len(zs) and i < nstages - 1 else 0,) for i, r in enumerate(rq)]
+        assert np.array_equal(oracle.run(op, dict(c, rq=rqz), inp), ref), zs
+    # the intermediates really are small: a wrong centring would move the output
+    assert np.abs(ref).max() > 0
+
+
+@pytest.mark.parametrize("op", ZP_OPS)
+@pytest.mark.parametrize("act", ["none", "relu"])
+def test_output_zero_point_offsets_the_codes(op, act):
+    """Without saturation the output codes move by exactly the output zero point; ReLU
+    clamps at the zero point, so it is max(symmetric ReLU output + z, z)."""
+    z = -9
+    last = {"dw": 0, "pw": 0, "pw_dw_pw": 2}.get(op, 1)
+    rq = [(1, 6, -128, 127), (3, 8, -128, 127), (1, 5, -128, 127)]
+    acts = ["relu", "none", "relu"]
+    acts[last] = act
+    c = _zp_case(op, rq=rq, act=acts)
+    inp = _i8_inputs(c)
+    ref = oracle.run(op, c, inp).astype(np.int32)
+    assert ref.max() + z <= 127 and ref.min() + z >= -128
+    rqz = [tuple(r) + ((z,) if i == last else (0,)) for i, r in enumerate(rq)]
+    got = oracle.run(op, dict(c, rq=rqz), inp).astype(np.int32)
+    assert np.array_equal(got, ref + z)
+    if act == "relu":
+        assert (got >= z).all() and (got == z).any()
+
+
+def test_zero_point_hand_values():
+    """Worked by hand.
+    DW 3x3, pad 1, on a 1x1 image: only the centre tap lies inside. Code 10 with input
+    zero point 3 is the value 7; centre weight 2 gives 14; output zero point -5 gives code
+    9. (Padding with code 0 instead of real 0 would add 8 * 5 * (0 - 3) = -120.)
+    PW on one pixel, codes (10, -4) with input zero point 2, i.e. values (8, -6), bias 5,
+    requantised by 2^-1 with output zero point -7:
+      weights (3, -1):  24 + 6 + 5 = 35  -> rne(17.5) = 18 (tie to even)  -> 11
+      weights (-3, 1): -24 - 6 + 5 = -25 -> rne(-12.5) = -12 (tie to even) -> -19,
+    which ReLU clamps at the zero point: -7."""
+    wd = np.full((1, 3, 3), 5, dtype=np.int8)
+    wd[0, 1, 1] = 2
+    c = dict(n=1, h=1, w=1, c_in=1, c_mid=1, c_out=1, k=3, stride=1, pad=1, dtype="i8", layout="nchw",
+             act=["none"] * 3, rq=[(1, 0, -128, 127, -5)] * 3, zp_in=3)
+    assert oracle.dw(c, np.array([[[[10]]]], dtype=np.int8), wd, None).ravel().tolist() == [9]
+    x = np.array([10, -4], dtype=np.int8).reshape(1, 1, 1, 2)
+    w = np.array([[3, -1], [-3, 1]], dtype=np.int8)
+    b = np.array([5, 5], dtype=np.int32)
+    c = dict(n=1, h=1, w=1, c_in=2, c_mid=2, c_out=2, k=1, stride=1, pad=0, dtype="i8", layout="nhwc",
+             rq=[(1, 1, -128, 127, -7)] * 3, zp_in=2)
+    assert oracle.pw(dict(c, act=["none"] * 3), x, w, b).ravel().tolist() == [11, -19]
+    assert oracle.pw(dict(c, act=["relu"] * 3), x, w, b).ravel().tolist() == [11, -7]
+
+
+def test_int8_zero_points_match_float_convolution_reference():
+    """DW -> PW with zero points on input, intermediate and output against torch's float64
+    convolutions of the centred values (zero padding = real 0 by torch's definition) and
+    exact Fraction rounding, saturating heavily (wide inputs, U{-127..127})."""
+    zin, zmid, zout = -20, 13, 31
+    rq = [(5, 11, -128, 127, zmid), (3, 12, -100, 120, zout)]
+    case = Case("dw_pw", 2, 9, 8, 12, 12, 5, 5, 2, 2, "i8", "nchw", ("relu", "none", "none"),
+                (rq[0], rq[1], rq[1]), dist_x="i8", dist_w="i8", bias=True, seed=43)
+    inp = make_inputs(case)
+    y = oracle.run("dw_pw", dict(case.as_dict(), rq=rq, zp_in=zin), inp)
+
+    def requant(t, r):
+        q = np.vectorize(lambda a: _rq_fraction(int(a), r[0], r[1], -2 ** 40, 2 ** 40))(t) + r[4]
+        return np.maximum(np.clip(q, r[2], r[3]), r[4])  # relu at the zero point
+
+    x = torch.from_numpy(inp["x"].astype(np.float64) - zin)
+    t = F.conv2d(x, torch.from_numpy(inp["w_dw"].astype(np.float64)[:, None]), stride=2, padding=2, groups=12)
+    m = requant(np.rint(t.numpy()).astype(np.int64) + inp["b_dw"].astype(np.int64)[None, :, None, None], rq[0])
+    u = F.conv2d(torch.from_numpy(m.astype(np.float64) - zmid),
+                 torch.from_numpy(inp["w_pw"].astype(np.float64)[:, :, None, None]))
+    t2 = np.rint(u.numpy()).astype(np.int64) + inp["b_pw"].astype(np.int64)[None, :, None, None]
+    ref = np.clip(np.vectorize(lambda a: _rq_fraction(int(a), 3, 12, -2 ** 40, 2 ** 40))(t2) + zout, -100, 120)
+    assert np.array_equal(y, ref.astype(np.int8))
+    assert np.mean(np.abs(m) >= 127) > 0.01 or np.mean(m == zmid) > 0.05
+
+
+def test_zero_point_validation():
+    c = _zp_case("pw")
+    inp = _i8_inputs(c)
+    for bad in (dict(zp_in=128), dict(zp_in=-129), dict(rq=[(1, 6, -127, 127, 200)] * 3)):
+        with pytest.raises(oracle.OracleError):
+            oracle.run("pw", dict(c, **bad), inp)

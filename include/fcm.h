@@ -87,16 +87,24 @@ typedef enum {
   FCM_OP_PW_PW = 5
 } fcm_op;
 
-/* int8 requantisation of a stage: q = clamp(rne(acc * mult / 2^shift), qmin, qmax),
+/* int8 requantisation of a stage:
+ *   q = clamp(rne(acc * mult / 2^shift) + zero_point, qmin, qmax),
  * rne = round half to even, acc = int32 accumulator + int32 bias. int8 activations act on
- * q: RELU and RELU6 clamp it below at 0; RELU6's upper end is qmax, which the caller sets
- * to 6.0 in the output's quantised units (e.g. 24 for a scale of 1/4).
- * Constraints: 0 <= shift <= 62, -128 <= qmin <= qmax <= 127. Ignored for float types. */
+ * q: RELU and RELU6 clamp it below at zero_point, the code of real 0; RELU6's upper end is
+ * qmax, which the caller sets to 6.0 in the output's quantised units (e.g. 24 + zero_point
+ * for a scale of 1/4).
+ * Asymmetric quantisation: a code q of the stage's output stands for scale * (q -
+ * zero_point). The stage that reads it convolves q - zero_point and pads with real 0.
+ * The paper states INT8 arithmetic (Sec. III-B) without a quantisation scheme; zero points
+ * extend it to asymmetric int8 models and change no module's data movement.
+ * Constraints: 0 <= shift <= 62, -128 <= qmin <= qmax <= 127, -128 <= zero_point <= 127.
+ * Ignored for float types. */
 typedef struct {
   int32_t mult;
   int32_t shift;
   int32_t qmin;
   int32_t qmax;
+  int32_t zero_point;
 } fcm_requant;
 
 /* One descriptor for every entry point; fields a module does not use are ignored.
@@ -119,6 +127,11 @@ typedef struct {
    * [0, 62]); the clamp range stays rq[i].qmin / qmax. Such descriptors are planned and
    * launched on the first-generation kernels only. Ignored for float types. */
   const int32_t* rq_channel[3];
+  /* int8 zero point of the input x (the code of real 0, in [-128, 127]); the input of
+   * stage i > 0 has the zero point of stage i-1's output, rq[i-1].zero_point. Descriptors
+   * with a nonzero zero point anywhere are planned and launched on the first-generation
+   * kernels only. Ignored for float types. */
+  int32_t zp_in;
 } fcm_desc;
 
 /* GPU description for the planner (Sec. IV: number of SMs, L1/shared-memory size).
@@ -265,6 +278,8 @@ typedef struct {
   int32_t n, h, w, c;      /* input of the first layer */
   int32_t dtype;           /* fcm_dtype, the whole chain */
   int32_t layout;          /* fcm_layout, the whole chain */
+  int32_t zp_in;           /* FCM_I8: zero point of the chain input (layer i > 0 reads
+                              layer i-1's output zero point, layers[i-1].rq.zero_point) */
   int32_t num_layers;      /* 1 .. FCM_CHAIN_MAX_LAYERS */
   fcm_layer layers[FCM_CHAIN_MAX_LAYERS];
 } fcm_chain_desc;

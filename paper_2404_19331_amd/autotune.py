@@ -21,7 +21,7 @@ def _layers(desc):
     for i in range(desc.num_layers):
         L = desc.layers[i]
         out.append(dict(kind=kinds[L.kind], c_out=L.c_out, k=L.k, stride=L.stride, pad=L.pad, act=acts[L.act],
-                        rq=(L.rq.mult, L.rq.shift, L.rq.qmin, L.rq.qmax)))
+                        rq=(L.rq.mult, L.rq.shift, L.rq.qmin, L.rq.qmax, L.rq.zero_point)))
     return out
 
 
@@ -74,7 +74,8 @@ def chain_autotune(desc, reps=20, device="cuda"):
             if len(sub_layers) != len(kinds) or tuple(L["kind"] for L in sub_layers) != kinds:
                 continue
             h, w, c = shapes[i]
-            sub = fcm.chain_desc(desc.n, h, w, c, sub_layers, desc.dtype, desc.layout)
+            zp = desc.zp_in if i == 0 else layers[i - 1]["rq"][4]
+            sub = fcm.chain_desc(desc.n, h, w, c, sub_layers, desc.dtype, desc.layout, zp_in=zp)
             plan = _module_plan(sub, op)
             if plan is None:
                 continue
@@ -138,7 +139,8 @@ def _module_plan(sub, op):
             chans.append(L["c_out"])
     c_mid = chans[1] if op in ("pw_dw", "pw_pw", "pw_dw_pw") else sub.c
     d = fcm.make_desc(sub.n, sub.h, sub.w, sub.c, c_mid, chans[-1], k=k, stride=s, pad=p, dtype=sub.dtype,
-                      layout=sub.layout, act=[L["act"] for L in layers], rq=[L["rq"] for L in layers])
+                      layout=sub.layout, act=[L["act"] for L in layers], rq=[L["rq"] for L in layers],
+                      zp_in=sub.zp_in)
     try:
         return fcm.plan(op, d)
     except fcm.FcmError:

@@ -20,11 +20,14 @@ fcm_status fail(fcm_status st, const std::string& msg) {
   return st;
 }
 
-bool has_per_channel_rq(int op, const fcm_desc* d) {
+// int8 features only the first-generation kernels implement: per-channel requantisation
+// and zero points (asymmetric quantisation).
+bool needs_first_gen(int op, const fcm_desc* d) {
   if (!d || d->dtype != FCM_I8) return false;
   const int stages = op == FCM_OP_PW_DW_PW ? 3 : ((op == FCM_OP_DW || op == FCM_OP_PW) ? 1 : 2);
+  if (d->zp_in != 0) return true;
   for (int i = 0; i < stages; ++i)
-    if (d->rq_channel[i]) return true;
+    if (d->rq_channel[i] || d->rq[i].zero_point != 0) return true;
   return false;
 }
 
@@ -65,8 +68,11 @@ fcm_status validate(int op, const fcm_desc* d) {
       if (r.shift < 0 || r.shift > 62) return fail(FCM_EINVAL, "requant shift must be in [0, 62]");
       if (r.qmin < -128 || r.qmax > 127 || r.qmin > r.qmax)
         return fail(FCM_EINVAL, "requant range must satisfy -128 <= qmin <= qmax <= 127");
+      if (r.zero_point < -128 || r.zero_point > 127) return fail(FCM_EINVAL, "zero points must be in [-128, 127]");
     }
   }
+  if (d->dtype == FCM_I8 && (d->zp_in < -128 || d->zp_in > 127))
+    return fail(FCM_EINVAL, "zero points must be in [-128, 127]");
   switch (op) {
     case FCM_OP_DW_PW:
       if (d->c_out <= 0) return fail(FCM_EINVAL, "c_out must be positive");
@@ -175,17 +181,19 @@ static fcm_status run(int op, const fcm_desc* d, const Tensors& t, const fcm_pla
   // LDS-DMA kernels need 16-byte aligned tensors
   bool aligned = aligned16(t.x) && aligned16(t.y);
   for (int i = 0; i < nw; ++i) aligned = aligned && aligned16(t.w[i]);
-  // per-channel requantisation is implemented by the first-generation kernels only
-  const bool per_channel = has_per_channel_rq(op, d);
-  aligned = aligned && !per_channel;
+  // per-channel requantisation and zero points are implemented by the first-generation
+  // kernels only
+  const bool first_gen = needs_first_gen(op, d);
+  aligned = aligned && !first_gen;
   fcm_plan_t p;
   if (plan_in) {
     if (plan_in->op != op) return fail(FCM_EINVAL, "plan was made for another module");
     p = *plan_in;
     if ((st = evaluate_plan(g, d, hw, &p)) != FCM_OK) return st;
     if (!aligned && variant_needs_alignment(p.variant))
-      return fail(FCM_EUNSUPPORTED, per_channel ? "per-channel requantisation runs on the first-generation kernels only"
-                                                : "plan's kernel needs 16-byte aligned tensors");
+      return fail(FCM_EUNSUPPORTED, first_gen ? "per-channel requantisation and zero points run on the "
+                                                "first-generation kernels only"
+                                              : "plan's kernel needs 16-byte aligned tensors");
   } else {
     if ((st = find_plan(op, d, &hw, &p, aligned)) != FCM_OK) return st;
   }
@@ -221,13 +229,16 @@ static fcm_status run(int op, const fcm_desc* d, const Tensors& t, const fcm_pla
   a.tiles_x = ceil_div(g.wo, p.tile_w);
   const int last = (g.family == FAM_PWDW || g.family == FAM_DW) ? g.cm : g.co;
   a.n_cb = ceil_div(last, p.co_block);
+  const bool i8 = d->dtype == FCM_I8;
   for (int i = 0; i < 3; ++i) {
-    a.rqc[i] = (per_channel && i < nw) ? d->rq_channel[i] : nullptr;
+    a.rqc[i] = (i8 && i < nw) ? d->rq_channel[i] : nullptr;
     a.act[i] = d->act[i];
     a.rq[i].mult = d->rq[i].mult;
     a.rq[i].shift = d->rq[i].shift;
     a.rq[i].qmin = d->rq[i].qmin;
     a.rq[i].qmax = d->rq[i].qmax;
+    a.rq[i].zp = i8 ? d->rq[i].zero_point : 0;
+    a.zin[i] = !i8 ? 0 : (i == 0 ? d->zp_in : d->rq[i - 1].zero_point);
   }
   // vector paths: 16-byte aligned base and 16-byte multiple rows
   const int xc = g.family == FAM_DW ? g.cm : g.ci;
@@ -300,7 +311,7 @@ fcm_status fcm_plan(int32_t op, const fcm_desc* desc, const fcm_hw_desc* hw, fcm
   if (!out) return fail(FCM_EINVAL, "output plan is NULL");
   fcm_status st = validate(op, desc);
   if (st != FCM_OK) return st;
-  return find_plan(op, desc, hw, out, !has_per_channel_rq(op, desc));
+  return find_plan(op, desc, hw, out, !needs_first_gen(op, desc));
 }
 
 fcm_status fcm_plan_evaluate(const fcm_desc* desc, const fcm_hw_desc* hw, fcm_plan_t* plan) {
@@ -311,9 +322,12 @@ fcm_status fcm_plan_evaluate(const fcm_desc* desc, const fcm_hw_desc* hw, fcm_pl
   const Geom g = geometry(plan->op, desc);
   st = evaluate_plan(g, desc, h, plan);
   if (st != FCM_OK) return st;
+  const bool first_gen = needs_first_gen(plan->op, desc);
+  if (first_gen && variant_needs_alignment(plan->variant))
+    return fail(FCM_EUNSUPPORTED, "per-channel requantisation and zero points run on the first-generation kernels only");
   // the layer-by-layer figures and the verdict come from the searched plan
   fcm_plan_t ref;
-  st = find_plan(plan->op, desc, &h, &ref);
+  st = find_plan(plan->op, desc, &h, &ref, !first_gen);
   if (st != FCM_OK) return st;
   plan->bytes_lbl_paper = ref.bytes_lbl_paper;
   plan->bytes_lbl_ideal = ref.bytes_lbl_ideal;

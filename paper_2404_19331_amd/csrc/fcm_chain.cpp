@@ -86,6 +86,8 @@ fcm_status chain_group_desc(const fcm_chain_desc* c, const int* h, const int* w,
       d->pad = L.pad;
     }
   }
+  // int8: the group's input zero point is the chain's or the previous layer's output one
+  d->zp_in = first == 0 ? c->zp_in : c->layers[first - 1].rq.zero_point;
   d->c_in = ch[first];
   switch (op) {
     case FCM_OP_DW:
@@ -151,7 +153,7 @@ fcm_status fcm_chain_plan(const fcm_chain_desc* chain, int32_t objective, const 
       }
       Opt o;
       o.op = op;
-      st = find_plan(op, &d, &H, &o.plan);
+      st = find_plan(op, &d, &H, &o.plan, !needs_first_gen(op, &d));
       if (st != FCM_OK) {
         if (single) return st;
         continue;

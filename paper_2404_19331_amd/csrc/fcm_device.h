@@ -77,8 +77,9 @@ __device__ __forceinline__ float act_f(float v, int act) {
   return v;
 }
 
-// q = clamp(round_half_even(acc * mult / 2^shift), qmin, qmax), then ReLU if asked (ReLU6
-// too: its upper end is qmax, 6.0 in the output's quantised units).
+// q = clamp(round_half_even(acc * mult / 2^shift) + zp, qmin, qmax), then ReLU if asked,
+// which clamps below at zp, the code of real 0 (ReLU6 too: its upper end is qmax, 6.0 in
+// the output's quantised units).
 __device__ __forceinline__ int32_t requant(int32_t acc, const Requant& rq, int act) {
   int64_t t = (int64_t)acc * (int64_t)rq.mult;
   int64_t q = t;
@@ -88,9 +89,10 @@ __device__ __forceinline__ int32_t requant(int32_t acc, const Requant& rq, int a
     int64_t half = (int64_t)1 << (rq.shift - 1);
     q += (r > half || (r == half && (q & 1))) ? 1 : 0;
   }
+  q += rq.zp;
   q = q < rq.qmin ? rq.qmin : q;
   q = q > rq.qmax ? rq.qmax : q;
-  if (act != ACT_NONE && q < 0) q = 0;
+  if (act != ACT_NONE && q < rq.zp) q = rq.zp;
   return (int32_t)q;
 }
 
@@ -257,24 +259,36 @@ __device__ __forceinline__ void staged_copy(char* s, int ta, const LA& la) {
   staged_copy<B>(s, ta, la, 0, NullLoader{}, 0, NullLoader{});
 }
 
-__device__ __forceinline__ void store_vec(char* s, int d, const u32x4& v) {
-  *(u32x4*)(s + (d & kOffMask)) = (d & kZero) ? u32x4{0u, 0u, 0u, 0u} : v;
+// fill: the bits stored for a kZero item (four copies of an int8 zero point for a window
+// a depthwise stage pads; 0 everywhere else).
+__device__ __forceinline__ void store_vec(char* s, int d, const u32x4& v, uint32_t fill = 0u) {
+  *(u32x4*)(s + (d & kOffMask)) = (d & kZero) ? u32x4{fill, fill, fill, fill} : v;
 }
 
 template <class T>
-__device__ __forceinline__ void store_elem(char* s, int d, const T& v) {
-  *(T*)(s + (d & kOffMask)) = (d & kZero) ? T(0) : v;
+__device__ __forceinline__ void store_elem(char* s, int d, const T& v, uint32_t fill = 0u) {
+  *(T*)(s + (d & kOffMask)) = (d & kZero) ? (T)fill : v;
+}
+
+// Bits of four int8 codes equal to zero point z (0 for the float types).
+template <class DT>
+__device__ __forceinline__ uint32_t zp_fill(int z) {
+  if constexpr (std::is_same<DT, TI8>::value)
+    return (uint32_t)(uint8_t)z * 0x01010101u;
+  else
+    return 0u;
 }
 
 // Haloed input window rows [iy0, iy0+IH) x cols [ix0, ix0+IW), channels [c0, c0+CB) into
-// LDS at `off` as [IH*IW pixels][CB] with pixel stride ps bytes. Zero outside the image
-// and for channels >= C.
+// LDS at `off` as [IH*IW pixels][CB] with pixel stride ps bytes. `fill` outside the image
+// and for channels >= C: zero, or the code of real 0 of an asymmetric int8 input.
 template <class DT>
 struct InputVec {  // NHWC, 16-byte vectors (C*ELT % 16 == 0, x 16-byte aligned)
   using V = u32x4;
   static constexpr int VE = 16 / DT::ELT;
   const typename DT::T* x;
   int n, C, H, W, iy0, ix0, IW, c0, nv, ps, off;
+  uint32_t fill = 0u;
   __device__ __forceinline__ int load(int i, V& v) const {
     const int vv = i % nv, pix = i / nv;
     const int py = pix / IW, px = pix - py * IW;
@@ -284,7 +298,7 @@ struct InputVec {  // NHWC, 16-byte vectors (C*ELT % 16 == 0, x 16-byte aligned)
     v = *(const u32x4*)(x + idx);
     return (off + pix * ps + vv * 16) | (ok ? 0 : kZero);
   }
-  __device__ __forceinline__ void store(char* s, int d, const V& v) const { store_vec(s, d, v); }
+  __device__ __forceinline__ void store(char* s, int d, const V& v) const { store_vec(s, d, v, fill); }
 };
 
 template <class DT>
@@ -292,6 +306,7 @@ struct InputElem {  // NHWC or NCHW, one element per item
   using V = typename DT::T;
   const typename DT::T* x;
   int layout, n, C, H, W, iy0, ix0, IH, IW, c0, CB, ps, off;
+  uint32_t fill = 0u;
   __device__ __forceinline__ int load(int i, V& v) const {
     int ci, py, px;
     if (layout == LAYOUT_NHWC) {
@@ -313,7 +328,7 @@ struct InputElem {  // NHWC or NCHW, one element per item
     v = x[idx];
     return (off + (py * IW + px) * ps + ci * DT::ELT) | (ok ? 0 : kZero);
   }
-  __device__ __forceinline__ void store(char* s, int d, const V& v) const { store_elem(s, d, v); }
+  __device__ __forceinline__ void store(char* s, int d, const V& v) const { store_elem(s, d, v, fill); }
 };
 
 // Rows [r0, r0+rows) x cols [c0, c0+CB) of a row-major [R][Cc] matrix into LDS rows of
@@ -387,14 +402,15 @@ struct DwWeights {
 
 template <class DT>
 __device__ __forceinline__ InputVec<DT> input_vec(const typename DT::T* x, int n, int C, int H, int W, int iy0,
-                                                  int ix0, int IW, int c0, int CB, int ps, int off) {
-  return InputVec<DT>{x, n, C, H, W, iy0, ix0, IW, c0, CB / InputVec<DT>::VE, ps, off};
+                                                  int ix0, int IW, int c0, int CB, int ps, int off,
+                                                  uint32_t fill = 0u) {
+  return InputVec<DT>{x, n, C, H, W, iy0, ix0, IW, c0, CB / InputVec<DT>::VE, ps, off, fill};
 }
 template <class DT>
 __device__ __forceinline__ InputElem<DT> input_elem(const typename DT::T* x, int layout, int n, int C, int H, int W,
                                                     int iy0, int ix0, int IH, int IW, int c0, int CB, int ps,
-                                                    int off) {
-  return InputElem<DT>{x, layout, n, C, H, W, iy0, ix0, IH, IW, c0, CB, ps, off};
+                                                    int off, uint32_t fill = 0u) {
+  return InputElem<DT>{x, layout, n, C, H, W, iy0, ix0, IH, IW, c0, CB, ps, off, fill};
 }
 template <class DT>
 __device__ __forceinline__ RowsVec<DT> rows_vec(const typename DT::T* w, int R, int Cc, int r0, int c0, int CB,
@@ -407,22 +423,23 @@ __device__ __forceinline__ RowsElem<DT> rows_elem(const typename DT::T* w, int R
   return RowsElem<DT>{w, R, Cc, r0, c0, CB, rs, off};
 }
 
-// Stage a chunk: haloed input window (IH x IW x CB at off_in, pixel stride ps), `rows`
-// rows of a [R][Cc] weight matrix (columns c0..c0+CB at off_w, stride rs) and, with
-// K > 0, the depthwise weights + bias of channels cd0..cd0+CBD at off_wd.
+// Stage a chunk: haloed input window (IH x IW x CB at off_in, pixel stride ps, `fill`
+// outside the image), `rows` rows of a [R][Cc] weight matrix (columns c0..c0+CB at off_w,
+// stride rs) and, with K > 0, the depthwise weights + bias of channels cd0..cd0+CBD at
+// off_wd.
 template <class DT, int K>
 __device__ __forceinline__ void stage_chunk(char* s, const typename DT::T* x, int layout, bool vec_x, int n, int C,
                                             int H, int W, int iy0, int ix0, int IH, int IW, int c0, int CB, int ps,
                                             int off_in, const typename DT::T* w, bool vec_w, int R, int Cc, int r0,
                                             int rows, int rs, int off_w, const typename DT::T* wd, const void* bd,
-                                            int Cd, int cd0, int CBD, int off_wd) {
+                                            int Cd, int cd0, int CBD, int off_wd, uint32_t fill = 0u) {
   constexpr int VE = 16 / DT::ELT;
   const int t_in = x ? IH * IW * CB : 0;
   const int t_w = w ? rows * CB : 0;
   const int t_d = K > 0 ? (K * K + 1) * CBD : 0;
   const bool fast_in = layout == LAYOUT_NHWC && vec_x;
   if (fast_in && (vec_w || t_w == 0)) {
-    const InputVec<DT> li = input_vec<DT>(x, n, C, H, W, iy0, ix0, IW, c0, CB, ps, off_in);
+    const InputVec<DT> li = input_vec<DT>(x, n, C, H, W, iy0, ix0, IW, c0, CB, ps, off_in, fill);
     if constexpr (K > 0) {
       const DwWeights<DT, K> ld{wd, bd, Cd, cd0, CBD, off_wd};
       if (t_w > 0)
@@ -439,9 +456,10 @@ __device__ __forceinline__ void stage_chunk(char* s, const typename DT::T* x, in
     return;
   }
   if (fast_in)
-    staged_copy<kBatch>(s, t_in / VE, input_vec<DT>(x, n, C, H, W, iy0, ix0, IW, c0, CB, ps, off_in));
+    staged_copy<kBatch>(s, t_in / VE, input_vec<DT>(x, n, C, H, W, iy0, ix0, IW, c0, CB, ps, off_in, fill));
   else
-    staged_copy<kBatch>(s, t_in, input_elem<DT>(x, layout, n, C, H, W, iy0, ix0, IH, IW, c0, CB, ps, off_in));
+    staged_copy<kBatch>(s, t_in,
+                        input_elem<DT>(x, layout, n, C, H, W, iy0, ix0, IH, IW, c0, CB, ps, off_in, fill));
   if (t_w > 0) {
     if (vec_w)
       staged_copy<kBatch>(s, t_w / VE, rows_vec<DT>(w, R, Cc, r0, c0, CB, rs, off_w));
@@ -497,10 +515,12 @@ struct Vec<TI8> {
 
 // pc / ch0: per-channel requantisation of the stage (int8) and the global channel of the
 // block's first channel (ch_valid channels exist).
+// zin: int8 zero point of the input. The window holds codes, padded with zin (real 0), so
+// sum_taps w * (code - zin) = sum_taps w * code - zin * sum_taps w.
 template <class DT, int K, int S, int R>
 __device__ __forceinline__ void dw_compute(const char* sin, int ips, int IW, const typename DT::Acc* swd, int CB, int TH, int TW,
                            int act, const Requant& rq, char* sout, int ops, ReqCh pc = ReqCh{}, int ch0 = 0,
-                           int ch_valid = 1) {
+                           int ch_valid = 1, int zin = 0) {
   using Acc = typename DT::Acc;
   constexpr int CPT = DT::CPT;
   constexpr int NIN = (R - 1) * S + K;
@@ -536,6 +556,18 @@ __device__ __forceinline__ void dw_compute(const char* sin, int ips, int IW, con
         }
       }
     }
+    if constexpr (std::is_same<DT, TI8>::value) {
+      if (zin != 0) {  // uniform: one zero point per launch
+#pragma unroll
+        for (int e = 0; e < CPT; ++e) {
+          Acc wsum = 0;
+#pragma unroll
+          for (int tap = 0; tap < K * K; ++tap) wsum += wg[tap * CB + e];
+#pragma unroll
+          for (int r = 0; r < R; ++r) acc[r][e] -= zin * wsum;
+        }
+      }
+    }
     const Acc* bias = swd + K * K * CB + g * CPT;
     Requant rqe[CPT];
 #pragma unroll
@@ -559,17 +591,43 @@ __device__ __forceinline__ void dw_compute(const char* sin, int ips, int IW, con
 // acc[i][j] holds rows m = m_base + 16i + 4*(lane/16) + v, columns n = n_base + 16j + lane%16
 // of C[m = channel][n = pixel].
 // m_wr >= m_act tiles are written; tiles the MFMA loop skipped hold zero accumulators
-// and come out as act(0 + 0) = 0 (bias is masked beyond m_valid).
+// and come out as act(0 + 0), real 0 (bias is masked beyond m_valid).
 // mask_iw > 0: pixel n is a position of an IW-wide window starting at (iy0, ix0) and
-// positions outside [0,H)x[0,W) are written as zero (PW output feeding a zero-padded DW).
+// positions outside [0,H)x[0,W) are written as real zero (PW output feeding a zero-padded
+// DW): 0, or the output zero point of an asymmetric int8 stage.
+// zin != 0 (int8): the B operand held codes of zero point zin, so each row m loses
+// zin * sum_c wz[bias_off + m][c] (wz: the [rows][wz_cc] weights of this contraction).
 // ------------------------------------------------------------------------------------
+
+// Row sums of int8 weights w [rows][cc]: out[v] = sum_c w[row0 + 4 * (lane / 16) + v][c]
+// (0 for rows >= rows_valid), the rows of this lane's accumulators. Lane l adds every
+// fourth element of row row0 + l % 16 from element l / 16; two butterfly steps complete
+// each sum and every lane then reads its four. All 64 lanes of the wave must call it.
+__device__ __forceinline__ void int8_row_sums(const int8_t* w, int cc, int row0, int rows_valid,
+                                              int32_t (&out)[4]) {
+  const int lane = threadIdx.x & 63;
+  const int row = row0 + (lane & 15);
+  int32_t s = 0;
+  if (row < rows_valid) {
+    const int8_t* p = w + (size_t)row * cc;
+    for (int c = lane >> 4; c < cc; c += 4) s += p[c];
+  }
+  s += __shfl_xor(s, 16);
+  s += __shfl_xor(s, 32);
+#pragma unroll
+  for (int v = 0; v < 4; ++v) out[v] = __shfl(s, 4 * (lane >> 4) + v);
+}
+
 template <class DT, int TMW, int TNW>
 __device__ __forceinline__ void acc_to_lds(const typename DT::AccV (&acc)[TMW][TNW], int m_base, int n_base,
                                            int m_wr, int n_act, const void* bias, int bias_off, int m_valid,
                                            int act, const Requant& rq, char* so, int rs, int mask_iw, int iy0,
-                                           int ix0, int H, int W, ReqCh pc = ReqCh{}) {
+                                           int ix0, int H, int W, ReqCh pc = ReqCh{}, int zin = 0,
+                                           const void* wz = nullptr, int wz_cc = 0) {
   const int lane = threadIdx.x & 63;
   const int r = lane & 15, g = lane >> 4;
+  constexpr bool kI8 = std::is_same<DT, TI8>::value;
+  const uint32_t real0 = kI8 ? (uint32_t)(rq.zp & 0xff) : 0u;  // storage bits of real 0
 #pragma unroll
   for (int i = 0; i < TMW; ++i) {
     if (i >= m_wr) continue;
@@ -582,6 +640,14 @@ __device__ __forceinline__ void acc_to_lds(const typename DT::AccV (&acc)[TMW][T
       if (m + v >= m_valid) b[v] = 0;
       rqv[v] = rq_at(rq, pc, bias_off + min(m + v, m_valid - 1));
     }
+    if constexpr (kI8) {
+      if (zin != 0) {  // uniform: one zero point per launch
+        int32_t rsum[4];
+        int8_row_sums((const int8_t*)wz, wz_cc, bias_off + m_base + i * 16, bias_off + m_valid, rsum);
+#pragma unroll
+        for (int v = 0; v < 4; ++v) b[v] -= zin * rsum[v];
+      }
+    }
 #pragma unroll
     for (int j = 0; j < TNW; ++j) {
       if (j >= n_act) continue;
@@ -592,7 +658,7 @@ __device__ __forceinline__ void acc_to_lds(const typename DT::AccV (&acc)[TMW][T
       if (mask_iw > 0) {
         const int qy = n / mask_iw, qx = n - qy * mask_iw;
         const int gy = iy0 + qy, gx = ix0 + qx;
-        if (!((unsigned)gy < (unsigned)H && (unsigned)gx < (unsigned)W)) o[0] = o[1] = o[2] = o[3] = 0u;
+        if (!((unsigned)gy < (unsigned)H && (unsigned)gx < (unsigned)W)) o[0] = o[1] = o[2] = o[3] = real0;
       }
       lds_store4<DT>(so + n * rs + m * DT::ELT, o[0], o[1], o[2], o[3]);
     }

@@ -11,8 +11,9 @@ namespace fcm {
 // Record a failure message for fcm_last_error() and return the status.
 fcm_status fail(fcm_status st, const std::string& msg);
 
-// Whether an int8 descriptor asks for per-channel requantisation in any stage of op.
-bool has_per_channel_rq(int op, const fcm_desc* d);
+// Whether an int8 descriptor asks for per-channel requantisation or a nonzero zero point
+// in any stage of op (features of the first-generation kernels only).
+bool needs_first_gen(int op, const fcm_desc* d);
 
 // Argument checks common to fcm_plan and every launch entry point.
 fcm_status validate(int op, const fcm_desc* d);

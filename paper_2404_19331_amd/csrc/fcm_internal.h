@@ -31,8 +31,9 @@ enum Family {
   FAM_PWPW = 5,    // PW -> PW (fused; family PWDWPW with the DW stage off)
 };
 
+// zp: the code of real 0 in the stage's output (asymmetric int8), added after rounding.
 struct Requant {
-  int32_t mult, shift, qmin, qmax;
+  int32_t mult, shift, qmin, qmax, zp;
 };
 
 // int8 per-channel requantisation of one stage: p = device array [2][n] (the stage's n
@@ -284,6 +285,7 @@ struct KArgs {
   int cus;       // compute units of the device
   int grid_cap;  // persistent kernels: at most this many workgroups (0 = no cap)
   const int32_t* rqc[3];  // int8 per-channel requantisation per stage ([2][channels]) or nullptr
+  int zin[3];             // int8 zero point of each stage's input (first-generation kernels)
   unsigned long long* trace;  // development timeline buffer (used only in FCM_TRACE builds)
 };
 

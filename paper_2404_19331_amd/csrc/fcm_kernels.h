@@ -10,7 +10,7 @@
 //             layer-by-layer DW kernel. Workgroup = (image, spatial tile, intermediate-
 //             channel block). The PW is evaluated on the whole haloed window, so halo
 //             positions are recomputed by neighbouring tiles (Sec. II-D); positions outside
-//             the image are zero, being the DW's zero padding.
+//             the image are real zero, being the DW's zero padding.
 //   k_pwdwpw  PW -> DW -> PW inverted residual in one kernel. Workgroup = (image, spatial
 //             tile, output-channel block). The input window is staged once; the
 //             intermediate channels stream through LDS in chunks, each chunk being expanded
@@ -72,13 +72,14 @@ __global__ __launch_bounds__(kThreads) void k_dwpw(KArgs a) {
   for (int c0 = 0; c0 < a.Ci; c0 += a.CB) {
     stage_chunk<DT, HAS_DW ? K : 0>(smem, x, a.layout, a.vec_x, n, a.Ci, a.H, a.W, iy0, ix0, IH, IW, c0, a.CB,
                                     L.ps_in, L.off_in, wp, vec_wp, a.Co, a.Ci, co0, m_tiles * 16, L.rs_w, L.off_w,
-                                    wd, a.b1, a.Ci, c0, a.CB, L.off_wd);
+                                    wd, a.b1, a.Ci, c0, a.CB, L.off_wd, HAS_DW ? zp_fill<DT>(a.zin[0]) : 0u);
     __syncthreads();
     const char* B = smem + L.off_in;
     int bs = L.ps_in;
     if constexpr (HAS_DW) {
       dw_compute<DT, K, S, R>(smem + L.off_in, L.ps_in, IW, (const Acc*)(smem + L.off_wd), a.CB, a.TH, a.TW,
-                              a.act[0], a.rq[0], smem + L.off_d, L.rs_d, ReqCh{a.rqc[0], a.Ci}, c0, a.Ci);
+                              a.act[0], a.rq[0], smem + L.off_d, L.rs_d, ReqCh{a.rqc[0], a.Ci}, c0, a.Ci,
+                              a.zin[0]);
       __syncthreads();
       B = smem + L.off_d;
       bs = L.rs_d;
@@ -88,7 +89,8 @@ __global__ __launch_bounds__(kThreads) void k_dwpw(KArgs a) {
   }
 
   acc_to_lds<DT, TMW, TNW>(acc, wm * TMW * 16, wn * TNW * 16, m_act, n_act, bp, co0, cob_eff, act_pw, rq_pw,
-                           smem + L.off_out, L.rs_out, 0, 0, 0, 0, 0, ReqCh{a.rqc[HAS_DW ? 1 : 0], a.Co});
+                           smem + L.off_out, L.rs_out, 0, 0, 0, 0, 0, ReqCh{a.rqc[HAS_DW ? 1 : 0], a.Co},
+                           a.zin[HAS_DW ? 1 : 0], wp, a.Ci);
   __syncthreads();
   store_tile<DT>(smem + L.off_out, L.rs_out, (T*)a.y, a.layout, n, a.Co, a.Ho, a.Wo, oy0, ox0, a.TH, a.TW, co0,
                  cob_eff, a.vec_y && ((cob_eff * DT::ELT) % 16 == 0));
@@ -143,17 +145,20 @@ __global__ __launch_bounds__(kThreads) void k_pwdw(KArgs a) {
     }
     // PW output over the haloed window -> E [Q][MB]; zero outside the image.
     acc_to_lds<DT, TMW, TNW>(acc, wm * TMW * 16, wn * TNW * 16, m_act, n_act, a.b1, m0, mb_eff, a.act[0], a.rq[0],
-                             smem + L.off_e, L.rs_e, IW, iy0, ix0, a.H, a.W, ReqCh{a.rqc[0], a.Cm});
+                             smem + L.off_e, L.rs_e, IW, iy0, ix0, a.H, a.W, ReqCh{a.rqc[0], a.Cm}, a.zin[0], a.w1,
+                             a.Ci);
     staged_copy<kBatch>(smem, (K * K + 1) * MB, DwWeights<DT, K>{(const T*)a.w2, a.b2, a.Cm, m0, MB, L.off_wd});
   } else {
     stage_chunk<DT, K>(smem, x, a.layout, a.vec_x, n, a.Cm, a.H, a.W, iy0, ix0, IH, IW, m0, MB, L.rs_e, L.off_e,
-                       nullptr, false, 0, 0, 0, 0, 0, 0, (const T*)a.w1, a.b1, a.Cm, m0, MB, L.off_wd);
+                       nullptr, false, 0, 0, 0, 0, 0, 0, (const T*)a.w1, a.b1, a.Cm, m0, MB, L.off_wd,
+                       zp_fill<DT>(a.zin[0]));
   }
   __syncthreads();
   const int act_dw = HAS_PW ? a.act[1] : a.act[0];
   const Requant rq_dw = HAS_PW ? a.rq[1] : a.rq[0];
   dw_compute<DT, K, S, R>(smem + L.off_e, L.rs_e, IW, (const Acc*)(smem + L.off_wd), MB, a.TH, a.TW, act_dw, rq_dw,
-                          smem + L.off_out, L.rs_out, ReqCh{a.rqc[HAS_PW ? 1 : 0], a.Cm}, m0, a.Cm);
+                          smem + L.off_out, L.rs_out, ReqCh{a.rqc[HAS_PW ? 1 : 0], a.Cm}, m0, a.Cm,
+                          a.zin[HAS_PW ? 1 : 0]);
   __syncthreads();
   store_tile<DT>(smem + L.off_out, L.rs_out, (T*)a.y, a.layout, n, a.Cm, a.Ho, a.Wo, oy0, ox0, a.TH, a.TW, m0, mb_eff,
                  a.vec_y && ((mb_eff * DT::ELT) % 16 == 0));
@@ -251,12 +256,13 @@ __global__ __launch_bounds__(kThreads) void k_pwdwpw(KArgs a) {
       // projection below never read uninitialised LDS.
       const int m_wr1 = max(0, min(TMW1, MB / 16 - wm1 * TMW1));
       acc_to_lds<DT, TMW1, TNW1>(acc1, wm1 * TMW1 * 16, wn1 * TNW1 * 16, m_wr1, n_act1, a.b1, m0, mb_eff, a.act[0],
-                                 a.rq[0], smem + L.off_e, L.rs_e, IW, iy0, ix0, a.H, a.W, ReqCh{a.rqc[0], a.Cm});
+                                 a.rq[0], smem + L.off_e, L.rs_e, IW, iy0, ix0, a.H, a.W, ReqCh{a.rqc[0], a.Cm},
+                                 a.zin[0], a.w1, a.Ci);
     }
     __syncthreads();
     if constexpr (MIDDW) {
       dw_compute<DT, K, S, R>(smem + L.off_e, L.rs_e, IW, (const Acc*)(smem + L.off_wd), MB, a.TH, a.TW, a.act[1],
-                              a.rq[1], smem + L.off_d, L.rs_d, ReqCh{a.rqc[1], a.Cm}, m0, a.Cm);
+                              a.rq[1], smem + L.off_d, L.rs_d, ReqCh{a.rqc[1], a.Cm}, m0, a.Cm, a.zin[1]);
       __syncthreads();
       mma_chunk<DT, TMW2, TNW2>(acc2, smem + L.off_w2, L.rs_w2, smem + L.off_d, L.rs_d, MB, wm2 * TMW2 * 16,
                                 wn2 * TNW2 * 16, m_act2, n_act2);
@@ -271,7 +277,7 @@ __global__ __launch_bounds__(kThreads) void k_pwdwpw(KArgs a) {
   constexpr int LAST = MIDDW ? 2 : 1;  // stage index of the last PW
   acc_to_lds<DT, TMW2, TNW2>(acc2, wm2 * TMW2 * 16, wn2 * TNW2 * 16, m_act2, n_act2, MIDDW ? a.b3 : a.b2, co0,
                              cob_eff, a.act[LAST], a.rq[LAST], smem + L.off_out, L.rs_out, 0, 0, 0, 0, 0,
-                             ReqCh{a.rqc[LAST], a.Co});
+                             ReqCh{a.rqc[LAST], a.Co}, a.zin[LAST], w_last, a.Cm);
   __syncthreads();
   store_tile<DT>(smem + L.off_out, L.rs_out, (T*)a.y, a.layout, n, a.Co, a.Ho, a.Wo, oy0, ox0, a.TH, a.TW, co0,
                  cob_eff, a.vec_y && ((cob_eff * DT::ELT) % 16 == 0));

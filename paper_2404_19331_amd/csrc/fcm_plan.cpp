@@ -746,6 +746,9 @@ static void lbl_stages(int op, const fcm_desc* d, std::vector<std::pair<int, fcm
     t.c_out = co;
     t.act[0] = t.act[1] = t.act[2] = d->act[stage];
     t.rq[0] = t.rq[1] = t.rq[2] = d->rq[stage];
+    t.rq_channel[0] = d->rq_channel[stage];
+    t.rq_channel[1] = t.rq_channel[2] = nullptr;
+    t.zp_in = stage == 0 ? d->zp_in : d->rq[stage - 1].zero_point;
     if (sop == FCM_OP_PW) {
       t.k = 1;
       t.stride = 1;

@@ -34,7 +34,12 @@ class FcmError(RuntimeError):
 
 class Requant(ctypes.Structure):
     _fields_ = [("mult", ctypes.c_int32), ("shift", ctypes.c_int32),
-                ("qmin", ctypes.c_int32), ("qmax", ctypes.c_int32)]
+                ("qmin", ctypes.c_int32), ("qmax", ctypes.c_int32), ("zero_point", ctypes.c_int32)]
+
+    def set(self, r):
+        """(mult, shift, qmin, qmax[, zero point of the stage's output])."""
+        r = tuple(int(v) for v in r) + (0,) * (5 - len(r))
+        self.mult, self.shift, self.qmin, self.qmax, self.zero_point = r
 
 
 class Desc(ctypes.Structure):
@@ -42,7 +47,8 @@ class Desc(ctypes.Structure):
                 ("c_in", ctypes.c_int32), ("c_mid", ctypes.c_int32), ("c_out", ctypes.c_int32),
                 ("k", ctypes.c_int32), ("stride", ctypes.c_int32), ("pad", ctypes.c_int32),
                 ("dtype", ctypes.c_int32), ("layout", ctypes.c_int32),
-                ("act", ctypes.c_int32 * 3), ("rq", Requant * 3), ("rq_channel", ctypes.c_void_p * 3)]
+                ("act", ctypes.c_int32 * 3), ("rq", Requant * 3), ("rq_channel", ctypes.c_void_p * 3),
+                ("zp_in", ctypes.c_int32)]
 
 
 class HwDesc(ctypes.Structure):
@@ -78,8 +84,8 @@ class Layer(ctypes.Structure):
 
 class ChainDesc(ctypes.Structure):
     _fields_ = [("n", ctypes.c_int32), ("h", ctypes.c_int32), ("w", ctypes.c_int32), ("c", ctypes.c_int32),
-                ("dtype", ctypes.c_int32), ("layout", ctypes.c_int32), ("num_layers", ctypes.c_int32),
-                ("layers", Layer * CHAIN_MAX_LAYERS)]
+                ("dtype", ctypes.c_int32), ("layout", ctypes.c_int32), ("zp_in", ctypes.c_int32),
+                ("num_layers", ctypes.c_int32), ("layers", Layer * CHAIN_MAX_LAYERS)]
 
 
 class ChainPlan(ctypes.Structure):
@@ -164,7 +170,9 @@ def _check(st):
 
 
 def make_desc(n, h, w, c_in, c_mid, c_out, k=3, stride=1, pad=1, dtype="f32", layout="nchw",
-              act=("none", "none", "none"), rq=None, rq_channel=None):
+              act=("none", "none", "none"), rq=None, rq_channel=None, zp_in=0):
+    """rq: per stage (mult, shift, qmin, qmax[, output zero point]); zp_in: int8 zero point
+    of the input (the code of real 0)."""
     d = Desc()
     d.n, d.h, d.w = n, h, w
     d.c_in, d.c_mid, d.c_out = c_in, c_mid, c_out
@@ -176,7 +184,8 @@ def make_desc(n, h, w, c_in, c_mid, c_out, k=3, stride=1, pad=1, dtype="f32", la
         d.act[i] = ACT[a] if isinstance(a, str) else int(a)
     rqs = (list(rq or []) + [(1, 0, -128, 127)] * 3)[:3]
     for i, r in enumerate(rqs):
-        d.rq[i].mult, d.rq[i].shift, d.rq[i].qmin, d.rq[i].qmax = (int(v) for v in r)
+        d.rq[i].set(r)
+    d.zp_in = int(zp_in)
     # int8 per-channel requantisation: device int32 tensors [2 * channels] per stage or None
     d._keep = []
     for i, t in enumerate(list(rq_channel or [])[:3]):
@@ -192,8 +201,9 @@ def make_desc(n, h, w, c_in, c_mid, c_out, k=3, stride=1, pad=1, dtype="f32", la
 def desc_from_case(case):
     """Descriptor from a workloads.Case (or any object/dict with the same fields)."""
     g = (lambda k: case[k]) if isinstance(case, dict) else (lambda k: getattr(case, k))
+    zp = case.get("zp_in", 0) if isinstance(case, dict) else getattr(case, "zp_in", 0)
     return make_desc(g("n"), g("h"), g("w"), g("c_in"), g("c_mid"), g("c_out"), g("k"), g("stride"),
-                     g("pad"), g("dtype"), g("layout"), g("act"), g("rq"))
+                     g("pad"), g("dtype"), g("layout"), g("act"), g("rq"), zp_in=zp or 0)
 
 
 def plan(op, desc, hw=None):
@@ -322,7 +332,7 @@ def _kk(w_dw):
 
 
 def dw_pw(x, w_dw, w_pw, b_dw=None, b_pw=None, *, stride=1, pad=None, act=("none", "none"), rq=None, rq_channel=None,
-          layout="nchw", plan=None, out=None, stream=None, prepare=False):
+          layout="nchw", plan=None, out=None, stream=None, prepare=False, zp_in=0):
     """DW -> PW module in one kernel. Returns y [n, c_out, h_o, w_o] in `layout`."""
     dt = _dtype_name(x)
     n, c, h, w = _dims(x, layout)
@@ -330,7 +340,7 @@ def dw_pw(x, w_dw, w_pw, b_dw=None, b_pw=None, *, stride=1, pad=None, act=("none
     pad = (k - 1) // 2 if pad is None else pad
     co = int(w_pw.shape[0])
     _prep(x, [w_dw, w_pw], [b_dw, b_pw], dt)
-    d = make_desc(n, h, w, c, c, co, k, stride, pad, dt, layout, act, rq, rq_channel=rq_channel)
+    d = make_desc(n, h, w, c, c, co, k, stride, pad, dt, layout, act, rq, rq_channel=rq_channel, zp_in=zp_in)
     ho, wo = out_hw(h, w, k, stride, pad)
     y = _out(x, layout, n, co, ho, wo, out)
     return _call(lib().fcm_dw_pw, (ctypes.byref(d), _ptr(x), _ptr(w_dw), _ptr(b_dw), _ptr(w_pw), _ptr(b_pw),
@@ -338,7 +348,7 @@ def dw_pw(x, w_dw, w_pw, b_dw=None, b_pw=None, *, stride=1, pad=None, act=("none
 
 
 def pw_dw(x, w_pw, w_dw, b_pw=None, b_dw=None, *, stride=1, pad=None, act=("none", "none"), rq=None, rq_channel=None,
-          layout="nchw", plan=None, out=None, stream=None, prepare=False):
+          layout="nchw", plan=None, out=None, stream=None, prepare=False, zp_in=0):
     """PW -> DW module in one kernel. Returns y [n, c_mid, h_o, w_o]."""
     dt = _dtype_name(x)
     n, c, h, w = _dims(x, layout)
@@ -346,7 +356,7 @@ def pw_dw(x, w_pw, w_dw, b_pw=None, b_dw=None, *, stride=1, pad=None, act=("none
     pad = (k - 1) // 2 if pad is None else pad
     cm = int(w_pw.shape[0])
     _prep(x, [w_pw, w_dw], [b_pw, b_dw], dt)
-    d = make_desc(n, h, w, c, cm, cm, k, stride, pad, dt, layout, act, rq, rq_channel=rq_channel)
+    d = make_desc(n, h, w, c, cm, cm, k, stride, pad, dt, layout, act, rq, rq_channel=rq_channel, zp_in=zp_in)
     ho, wo = out_hw(h, w, k, stride, pad)
     y = _out(x, layout, n, cm, ho, wo, out)
     return _call(lib().fcm_pw_dw, (ctypes.byref(d), _ptr(x), _ptr(w_pw), _ptr(b_pw), _ptr(w_dw), _ptr(b_dw),
@@ -355,7 +365,7 @@ def pw_dw(x, w_pw, w_dw, b_pw=None, b_dw=None, *, stride=1, pad=None, act=("none
 
 def pw_dw_pw(x, w_pw1, w_dw, w_pw2, b_pw1=None, b_dw=None, b_pw2=None, *, stride=1, pad=None,
              act=("none", "none", "none"), rq=None, rq_channel=None, layout="nchw", plan=None, out=None, stream=None,
-             prepare=False):
+             prepare=False, zp_in=0):
     """PW -> DW -> PW inverted residual in one kernel. Returns y [n, c_out, h_o, w_o]."""
     dt = _dtype_name(x)
     n, c, h, w = _dims(x, layout)
@@ -363,7 +373,7 @@ def pw_dw_pw(x, w_pw1, w_dw, w_pw2, b_pw1=None, b_dw=None, b_pw2=None, *, stride
     pad = (k - 1) // 2 if pad is None else pad
     cm, co = int(w_pw1.shape[0]), int(w_pw2.shape[0])
     _prep(x, [w_pw1, w_dw, w_pw2], [b_pw1, b_dw, b_pw2], dt)
-    d = make_desc(n, h, w, c, cm, co, k, stride, pad, dt, layout, act, rq, rq_channel=rq_channel)
+    d = make_desc(n, h, w, c, cm, co, k, stride, pad, dt, layout, act, rq, rq_channel=rq_channel, zp_in=zp_in)
     ho, wo = out_hw(h, w, k, stride, pad)
     y = _out(x, layout, n, co, ho, wo, out)
     return _call(lib().fcm_pw_dw_pw, (ctypes.byref(d), _ptr(x), _ptr(w_pw1), _ptr(b_pw1), _ptr(w_dw), _ptr(b_dw),
@@ -372,27 +382,27 @@ def pw_dw_pw(x, w_pw1, w_dw, w_pw2, b_pw1=None, b_dw=None, b_pw2=None, *, stride
 
 
 def pw_pw(x, w_pw1, w_pw2, b_pw1=None, b_pw2=None, *, act=("none", "none"), rq=None, rq_channel=None, layout="nchw", plan=None,
-          out=None, stream=None, prepare=False):
+          out=None, stream=None, prepare=False, zp_in=0):
     """PW -> PW module in one kernel. Returns y [n, c_out, h, w]."""
     dt = _dtype_name(x)
     n, c, h, w = _dims(x, layout)
     cm, co = int(w_pw1.shape[0]), int(w_pw2.shape[0])
     _prep(x, [w_pw1, w_pw2], [b_pw1, b_pw2], dt)
-    d = make_desc(n, h, w, c, cm, co, 1, 1, 0, dt, layout, act, rq, rq_channel=rq_channel)
+    d = make_desc(n, h, w, c, cm, co, 1, 1, 0, dt, layout, act, rq, rq_channel=rq_channel, zp_in=zp_in)
     y = _out(x, layout, n, co, h, w, out)
     return _call(lib().fcm_pw_pw, (ctypes.byref(d), _ptr(x), _ptr(w_pw1), _ptr(b_pw1), _ptr(w_pw2), _ptr(b_pw2),
                                    _ptr(y), _plan_arg(plan), _stream(x, stream)), y, prepare)
 
 
 def dw(x, w_dw, b_dw=None, *, stride=1, pad=None, act="none", rq=None, rq_channel=None, layout="nchw", plan=None, out=None,
-       stream=None, prepare=False):
+       stream=None, prepare=False, zp_in=0):
     """Single depthwise layer (layer-by-layer kernel)."""
     dt = _dtype_name(x)
     n, c, h, w = _dims(x, layout)
     k = _kk(w_dw)
     pad = (k - 1) // 2 if pad is None else pad
     _prep(x, [w_dw], [b_dw], dt)
-    d = make_desc(n, h, w, c, c, c, k, stride, pad, dt, layout, (act,), [rq] if rq else None, rq_channel=rq_channel)
+    d = make_desc(n, h, w, c, c, c, k, stride, pad, dt, layout, (act,), [rq] if rq else None, rq_channel=rq_channel, zp_in=zp_in)
     ho, wo = out_hw(h, w, k, stride, pad)
     y = _out(x, layout, n, c, ho, wo, out)
     return _call(lib().fcm_dw, (ctypes.byref(d), _ptr(x), _ptr(w_dw), _ptr(b_dw), _ptr(y), _plan_arg(plan),
@@ -400,13 +410,13 @@ def dw(x, w_dw, b_dw=None, *, stride=1, pad=None, act="none", rq=None, rq_channe
 
 
 def pw(x, w_pw, b_pw=None, *, act="none", rq=None, rq_channel=None, layout="nchw", plan=None, out=None, stream=None,
-       prepare=False):
+       prepare=False, zp_in=0):
     """Single pointwise layer (layer-by-layer kernel)."""
     dt = _dtype_name(x)
     n, c, h, w = _dims(x, layout)
     co = int(w_pw.shape[0])
     _prep(x, [w_pw], [b_pw], dt)
-    d = make_desc(n, h, w, c, c, co, 1, 1, 0, dt, layout, (act,), [rq] if rq else None, rq_channel=rq_channel)
+    d = make_desc(n, h, w, c, c, co, 1, 1, 0, dt, layout, (act,), [rq] if rq else None, rq_channel=rq_channel, zp_in=zp_in)
     y = _out(x, layout, n, co, h, w, out)
     return _call(lib().fcm_pw, (ctypes.byref(d), _ptr(x), _ptr(w_pw), _ptr(b_pw), _ptr(y), _plan_arg(plan),
                                 _stream(x, stream)), y, prepare)
@@ -430,45 +440,56 @@ class _Chain:
         return self.y
 
 
+def _zp_out(r):
+    """Output zero point of an int8 stage's (mult, shift, qmin, qmax[, zero point])."""
+    return int(r[4]) if r is not None and len(r) > 4 else 0
+
+
 def dw_then_pw(x, w_dw, w_pw, b_dw=None, b_pw=None, *, stride=1, pad=None, act=("none", "none"), rq=None,
-               layout="nchw", mid=None, out=None, stream=None, prepare=False):
+               layout="nchw", mid=None, out=None, stream=None, prepare=False, zp_in=0):
     rq = list(rq) if rq else [None, None]
     c1 = dw(x, w_dw, b_dw, stride=stride, pad=pad, act=act[0], rq=rq[0], layout=layout, out=mid, stream=stream,
-            prepare=prepare)
+            prepare=prepare, zp_in=zp_in)
     m = c1.y if prepare else c1
-    c2 = pw(m, w_pw, b_pw, act=act[1], rq=rq[1], layout=layout, out=out, stream=stream, prepare=prepare)
+    c2 = pw(m, w_pw, b_pw, act=act[1], rq=rq[1], layout=layout, out=out, stream=stream, prepare=prepare,
+            zp_in=_zp_out(rq[0]))
     return _Chain([c1, c2]) if prepare else c2
 
 
 def pw_then_dw(x, w_pw, w_dw, b_pw=None, b_dw=None, *, stride=1, pad=None, act=("none", "none"), rq=None,
-               layout="nchw", mid=None, out=None, stream=None, prepare=False):
+               layout="nchw", mid=None, out=None, stream=None, prepare=False, zp_in=0):
     rq = list(rq) if rq else [None, None]
-    c1 = pw(x, w_pw, b_pw, act=act[0], rq=rq[0], layout=layout, out=mid, stream=stream, prepare=prepare)
+    c1 = pw(x, w_pw, b_pw, act=act[0], rq=rq[0], layout=layout, out=mid, stream=stream, prepare=prepare,
+            zp_in=zp_in)
     m = c1.y if prepare else c1
     c2 = dw(m, w_dw, b_dw, stride=stride, pad=pad, act=act[1], rq=rq[1], layout=layout, out=out, stream=stream,
-            prepare=prepare)
+            prepare=prepare, zp_in=_zp_out(rq[0]))
     return _Chain([c1, c2]) if prepare else c2
 
 
 def pw_then_pw(x, w_pw1, w_pw2, b_pw1=None, b_pw2=None, *, act=("none", "none"), rq=None, layout="nchw",
-               mid=None, out=None, stream=None, prepare=False):
+               mid=None, out=None, stream=None, prepare=False, zp_in=0):
     rq = list(rq) if rq else [None, None]
-    c1 = pw(x, w_pw1, b_pw1, act=act[0], rq=rq[0], layout=layout, out=mid, stream=stream, prepare=prepare)
+    c1 = pw(x, w_pw1, b_pw1, act=act[0], rq=rq[0], layout=layout, out=mid, stream=stream, prepare=prepare,
+            zp_in=zp_in)
     m = c1.y if prepare else c1
-    c2 = pw(m, w_pw2, b_pw2, act=act[1], rq=rq[1], layout=layout, out=out, stream=stream, prepare=prepare)
+    c2 = pw(m, w_pw2, b_pw2, act=act[1], rq=rq[1], layout=layout, out=out, stream=stream, prepare=prepare,
+            zp_in=_zp_out(rq[0]))
     return _Chain([c1, c2]) if prepare else c2
 
 
 def pw_then_dw_then_pw(x, w_pw1, w_dw, w_pw2, b_pw1=None, b_dw=None, b_pw2=None, *, stride=1, pad=None,
                        act=("none", "none", "none"), rq=None, layout="nchw", mids=(None, None), out=None,
-                       stream=None, prepare=False):
+                       stream=None, prepare=False, zp_in=0):
     rq = list(rq) if rq else [None, None, None]
-    c1 = pw(x, w_pw1, b_pw1, act=act[0], rq=rq[0], layout=layout, out=mids[0], stream=stream, prepare=prepare)
+    c1 = pw(x, w_pw1, b_pw1, act=act[0], rq=rq[0], layout=layout, out=mids[0], stream=stream, prepare=prepare,
+            zp_in=zp_in)
     m1 = c1.y if prepare else c1
     c2 = dw(m1, w_dw, b_dw, stride=stride, pad=pad, act=act[1], rq=rq[1], layout=layout, out=mids[1],
-            stream=stream, prepare=prepare)
+            stream=stream, prepare=prepare, zp_in=_zp_out(rq[0]))
     m2 = c2.y if prepare else c2
-    c3 = pw(m2, w_pw2, b_pw2, act=act[2], rq=rq[2], layout=layout, out=out, stream=stream, prepare=prepare)
+    c3 = pw(m2, w_pw2, b_pw2, act=act[2], rq=rq[2], layout=layout, out=out, stream=stream, prepare=prepare,
+            zp_in=_zp_out(rq[1]))
     return _Chain([c1, c2, c3]) if prepare else c3
 
 
@@ -476,15 +497,17 @@ def pw_then_dw_then_pw(x, w_pw1, w_dw, w_pw2, b_pw1=None, b_dw=None, b_pw2=None,
 # Chains of layers (FusePlanner over a network): plan once, run every group's kernel
 # ------------------------------------------------------------------------------------
 
-def chain_desc(n, h, w, c, layers, dtype="i8", layout="nhwc"):
+def chain_desc(n, h, w, c, layers, dtype="i8", layout="nhwc", zp_in=0):
     """Chain descriptor. layers: dicts with kind ("dw" | "pw"), c_out (PW), k, stride,
-    pad (DW), act ("none" | "relu" | "relu6"), rq ((mult, shift, qmin, qmax), int8)."""
+    pad (DW), act ("none" | "relu" | "relu6"), rq ((mult, shift, qmin, qmax[, output
+    zero point]), int8). zp_in: int8 zero point of the chain input."""
     if not 1 <= len(layers) <= CHAIN_MAX_LAYERS:
         raise ValueError("a chain has 1 .. %d layers" % CHAIN_MAX_LAYERS)
     d = ChainDesc()
     d.n, d.h, d.w, d.c = n, h, w, c
     d.dtype = DTYPE[dtype] if isinstance(dtype, str) else int(dtype)
     d.layout = LAYOUT[layout] if isinstance(layout, str) else int(layout)
+    d.zp_in = int(zp_in)
     d.num_layers = len(layers)
     for i, L in enumerate(layers):
         t = d.layers[i]
@@ -493,8 +516,7 @@ def chain_desc(n, h, w, c, layers, dtype="i8", layout="nhwc"):
         t.k, t.stride, t.pad = int(L.get("k", 1)), int(L.get("stride", 1)), int(L.get("pad", 0))
         a = L.get("act", "none")
         t.act = ACT[a] if isinstance(a, str) else int(a)
-        r = L.get("rq") or (1, 0, -128, 127)
-        t.rq.mult, t.rq.shift, t.rq.qmin, t.rq.qmax = (int(v) for v in r)
+        t.rq.set(L.get("rq") or (1, 0, -128, 127))
     return d
 
 

@@ -55,6 +55,7 @@ class Case:
     bias: bool = False
     seed: int = BASE_SEED
     name: str = ""
+    zp_in: int = 0               # int8 zero point of x (rq entries may carry a 5th: output zero point)
 
     def with_(self, **kw):
         return replace(self, **kw)
@@ -63,7 +64,7 @@ class Case:
         return dict(op=self.op, n=self.n, h=self.h, w=self.w, c_in=self.c_in, c_mid=self.c_mid,
                     c_out=self.c_out, k=self.k, stride=self.stride, pad=self.pad,
                     dtype=self.dtype, layout=self.layout, act=list(self.act),
-                    rq=[list(r) for r in self.rq], name=self.name)
+                    rq=[list(r) for r in self.rq], zp_in=self.zp_in, name=self.name)
 
 
 def _x_shape(case):
@@ -264,6 +265,7 @@ class ChainSpec:
     layers: list
     seed: int = BASE_SEED
     name: str = ""
+    zp_in: int = 0               # int8 zero point of x (rq entries may carry a 5th: output zero point)
 
 
 def mobilenetv2_chain(n=8, dtype="i8", layout="nhwc", h=112, w=112, stages=None, final_pw=True):

@@ -80,6 +80,8 @@ def run_fused(case, d, plan=None, out=None, rq_channel=None):
     if rq_channel is not None:
         kw["rq_channel"] = rq_channel
     rq = list(case.rq) if case.dtype == "i8" else None
+    if case.dtype == "i8":
+        kw["zp_in"] = getattr(case, "zp_in", 0)
     if case.op == "dw_pw":
         return fcm.dw_pw(d["x"], d["w_dw"], d["w_pw"], d.get("b_dw"), d.get("b_pw"), act=case.act[:2], rq=rq, **kw)
     if case.op == "pw_dw":
@@ -102,6 +104,8 @@ def run_fused(case, d, plan=None, out=None, rq_channel=None):
 def run_unfused(case, d):
     kw = dict(stride=case.stride, pad=case.pad, layout=case.layout)
     rq = list(case.rq) if case.dtype == "i8" else None
+    if case.dtype == "i8":
+        kw["zp_in"] = getattr(case, "zp_in", 0)
     if case.op == "dw_pw":
         return fcm.dw_then_pw(d["x"], d["w_dw"], d["w_pw"], d.get("b_dw"), d.get("b_pw"), act=case.act[:2],
                               rq=rq, **kw)
@@ -113,7 +117,7 @@ def run_unfused(case, d):
                                       d.get("b_pw2"), act=case.act, rq=rq, **kw)
     if case.op == "pw_pw":
         return fcm.pw_then_pw(d["x"], d["w_pw1"], d["w_pw2"], d.get("b_pw1"), d.get("b_pw2"), act=case.act[:2],
-                              rq=rq, layout=case.layout)
+                              rq=rq, layout=case.layout, zp_in=kw.get("zp_in", 0))
     raise ValueError(case.op)
 
 
@@ -130,12 +134,14 @@ def batch_slice(inp, idx):
 def oracle_chain(spec, x, ws, bs, upto=None):
     """The chain on the CPU oracle, one layer at a time (definition of the chain)."""
     h, w, c = spec.h, spec.w, spec.c
+    zp = getattr(spec, "zp_in", 0)
     for i, L in enumerate(spec.layers[:upto]):
         k, s, p = (L["k"], L["stride"], L["pad"]) if L["kind"] == "dw" else (1, 1, 0)
         co = c if L["kind"] == "dw" else L["c_out"]
+        rq = list(L.get("rq") or (1, 0, -128, 127))
         case = dict(n=spec.n, h=h, w=w, c_in=c, c_mid=c, c_out=co, k=k, stride=s, pad=p, dtype=spec.dtype,
-                    layout=spec.layout, act=[L["act"], "none", "none"],
-                    rq=[list(L.get("rq") or (1, 0, -128, 127))] * 3)
+                    layout=spec.layout, act=[L["act"], "none", "none"], rq=[rq] * 3, zp_in=zp)
+        zp = rq[4] if len(rq) > 4 else 0
         if L["kind"] == "dw":
             x = oracle.dw(case, x, ws[i], bs[i])
             h, w = fcm.out_hw(h, w, k, s, p)
@@ -148,6 +154,7 @@ def oracle_chain(spec, x, ws, bs, upto=None):
 def run_chain(spec, objective, x, ws, bs, upto=None):
     """The chain through the C ABI (fcm_chain_plan + fcm_chain_run) on device tensors."""
     layers = spec.layers[:upto]
-    d = fcm.chain_desc(spec.n, spec.h, spec.w, spec.c, layers, spec.dtype, spec.layout)
+    d = fcm.chain_desc(spec.n, spec.h, spec.w, spec.c, layers, spec.dtype, spec.layout,
+                       zp_in=getattr(spec, "zp_in", 0))
     p = fcm.chain_plan(d, objective)
     return fcm.chain_run(d, p, x, ws[:len(layers)], bs[:len(layers)]), p

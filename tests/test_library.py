@@ -251,3 +251,92 @@ def test_library_binds_to_the_hip_runtime_torch_loads():
     out = subprocess.run([sys.executable, "-c", code], cwd=ROOT, capture_output=True, text=True, timeout=300)
     assert out.returncode == 0, out.stderr
     assert out.stdout.strip().splitlines()[-1] == "1"
+
+
+# --------------------------------------------------------------------------------------
+# Asymmetric int8 (zero points): planned on the first-generation kernels
+# --------------------------------------------------------------------------------------
+
+def _first_gen(v):
+    return re.search(r"\d<", fcm.variant_name(v)) is None
+
+
+ZP_SHAPES = {"dw_pw": (64, 64, 64, 3), "pw_dw": (32, 96, 96, 3), "pw_dw_pw": (32, 96, 32, 3),
+             "pw_pw": (64, 128, 64, 1), "dw": (64, 64, 64, 3), "pw": (64, 64, 96, 1)}
+
+
+def _zp_desc(op, zp_in=0, zps=(0, 0, 0), dtype="i8"):
+    ci, cm, co, k = ZP_SHAPES[op]
+    rq = [(1, 6, -128, 127, z) for z in zps]
+    return fcm.make_desc(4, 28, 28, ci, cm, co, k=k, stride=1, pad=k // 2, dtype=dtype, layout="nhwc",
+                         act=("relu", "relu", "none"), rq=rq, zp_in=zp_in)
+
+
+@pytest.mark.parametrize("op", list(ZP_SHAPES))
+def test_zero_points_plan_first_generation_kernels(op):
+    stages = {"pw_dw_pw": 3, "dw": 1, "pw": 1}.get(op, 2)
+    sym = fcm.plan(op, _zp_desc(op))
+    if op in ("dw_pw", "pw_pw", "dw", "pw"):
+        assert not _first_gen(sym.variant)  # not vacuous: symmetric int8 runs on a newer kernel
+    variants = [(5, (0, 0, 0))] + [(0, tuple(-7 if j == i else 0 for j in range(3))) for i in range(stages)]
+    for zin, zps in variants:
+        p = fcm.plan(op, _zp_desc(op, zin, zps))
+        assert _first_gen(p.variant), (zin, zps, fcm.variant_name(p.variant))
+    # a zero point of a stage the module does not have is ignored, as are float types
+    if stages < 3:
+        assert fcm.plan(op, _zp_desc(op, 0, (0, 0, 9) if stages == 2 else (0, 9, 9))).as_dict() == sym.as_dict()
+    f = fcm.plan(op, _zp_desc(op, 5, (3, 3, 3), dtype="bf16"))
+    assert f.as_dict() == fcm.plan(op, _zp_desc(op, dtype="bf16")).as_dict()
+
+
+def test_zero_points_validation_and_explicit_plans():
+    for zin, zps in ((128, (0, 0, 0)), (-129, (0, 0, 0)), (0, (0, 200, 0)), (0, (-300, 0, 0))):
+        with pytest.raises(fcm.FcmError) as e:
+            fcm.plan("dw_pw", _zp_desc("dw_pw", zin, zps))
+        assert e.value.status == EINVAL and "zero point" in str(e.value)
+    # an explicit plan on a newer kernel is refused for an asymmetric descriptor
+    sym = fcm.plan("dw_pw", _zp_desc("dw_pw"))
+    assert not _first_gen(sym.variant)
+    with pytest.raises(fcm.FcmError) as e:
+        fcm.plan_evaluate("dw_pw", _zp_desc("dw_pw", 3), sym.tile_h, sym.tile_w, sym.c_block, sym.co_block,
+                          sym.variant)
+    assert e.value.status == EUNSUPPORTED
+
+
+def test_chain_zero_points_reach_the_groups_they_touch():
+    """A zero point on one layer's output moves to the first-generation kernels exactly the
+    groups that write that tensor or read it; the others keep the symmetric plan."""
+    layers = [dict(kind="pw", c_out=96, act="relu", rq=(1, 6, -128, 127)),
+              dict(kind="dw", k=3, stride=1, pad=1, act="relu", rq=(1, 4, -128, 127)),
+              dict(kind="pw", c_out=64, act="none", rq=(1, 7, -128, 127)),
+              dict(kind="pw", c_out=128, act="relu", rq=(1, 6, -128, 127)),
+              dict(kind="dw", k=3, stride=1, pad=1, act="relu", rq=(1, 4, -128, 127)),
+              dict(kind="pw", c_out=64, act="none", rq=(1, 7, -128, 127))]
+    sym = fcm.chain_plan(fcm.chain_desc(4, 28, 28, 64, layers, "i8"), "unfused")
+    for j in range(len(layers)):
+        zl = [dict(L) for L in layers]
+        zl[j]["rq"] = tuple(zl[j]["rq"]) + (-11,)
+        p = fcm.chain_plan(fcm.chain_desc(4, 28, 28, 64, zl, "i8"), "unfused")
+        for g, (first, op, plan) in enumerate(p.groups()):
+            touched = first in (j, j + 1)  # unfused: one layer per group
+            assert _first_gen(plan.variant) or not touched, (j, first)
+            if not touched:
+                assert plan.as_dict() == sym.plan[g].as_dict()
+    # the chain input's zero point reaches the first group only
+    p = fcm.chain_plan(fcm.chain_desc(4, 28, 28, 64, layers, "i8", zp_in=-128), "unfused")
+    assert _first_gen(p.plan[0].variant) and p.plan[1].as_dict() == sym.plan[1].as_dict()
+
+
+def test_abi_struct_sizes_match_the_binding(tmp_path):
+    """The ctypes mirrors of the descriptor structs have the C sizes and field offsets."""
+    src = tmp_path / "sizes.c"
+    src.write_text('#include <stdio.h>\n#include <stddef.h>\n#include "fcm.h"\nint main(void){\n'
+                   'printf("%zu %zu %zu %zu %zu %zu %zu\\n", sizeof(fcm_requant), sizeof(fcm_desc),'
+                   ' offsetof(fcm_desc, zp_in), sizeof(fcm_layer), sizeof(fcm_chain_desc),'
+                   ' offsetof(fcm_chain_desc, layers), sizeof(fcm_chain_plan_t));\nreturn 0;}\n')
+    exe = tmp_path / "sizes"
+    subprocess.run(["gcc", "-std=c99", "-I", os.path.join(ROOT, "include"), "-o", str(exe), str(src)], check=True)
+    got = [int(v) for v in subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout.split()]
+    assert got == [ctypes.sizeof(fcm.Requant), ctypes.sizeof(fcm.Desc), fcm.Desc.zp_in.offset,
+                   ctypes.sizeof(fcm.Layer), ctypes.sizeof(fcm.ChainDesc), fcm.ChainDesc.layers.offset,
+                   ctypes.sizeof(fcm.ChainPlan)]

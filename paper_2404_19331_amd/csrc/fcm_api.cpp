@@ -20,15 +20,22 @@ fcm_status fail(fcm_status st, const std::string& msg) {
   return st;
 }
 
-// int8 features only the first-generation kernels implement: per-channel requantisation
-// and zero points (asymmetric quantisation).
-bool needs_first_gen(int op, const fcm_desc* d) {
-  if (!d || d->dtype != FCM_I8) return false;
+// int8 features not every kernel implements: per-channel requantisation (first-generation
+// kernels) and zero points (first-generation kernels and the PW->PW register kernel).
+int kernel_set(int op, const fcm_desc* d) {
+  if (!d || d->dtype != FCM_I8) return KSET_ALL;
   const int stages = op == FCM_OP_PW_DW_PW ? 3 : ((op == FCM_OP_DW || op == FCM_OP_PW) ? 1 : 2);
-  if (d->zp_in != 0) return true;
-  for (int i = 0; i < stages; ++i)
-    if (d->rq_channel[i] || d->rq[i].zero_point != 0) return true;
-  return false;
+  bool zp = d->zp_in != 0;
+  for (int i = 0; i < stages; ++i) {
+    if (d->rq_channel[i]) return KSET_FIRST;
+    zp = zp || d->rq[i].zero_point != 0;
+  }
+  return zp ? KSET_REG : KSET_ALL;
+}
+
+static const char* kset_message(int kset) {
+  return kset == KSET_FIRST ? "per-channel requantisation runs on the first-generation kernels only"
+                            : "zero points run on the first-generation and PW->PW register kernels only";
 }
 
 const Variant* all_variants(int* count) {
@@ -181,21 +188,20 @@ static fcm_status run(int op, const fcm_desc* d, const Tensors& t, const fcm_pla
   // LDS-DMA kernels need 16-byte aligned tensors
   bool aligned = aligned16(t.x) && aligned16(t.y);
   for (int i = 0; i < nw; ++i) aligned = aligned && aligned16(t.w[i]);
-  // per-channel requantisation and zero points are implemented by the first-generation
-  // kernels only
-  const bool first_gen = needs_first_gen(op, d);
-  aligned = aligned && !first_gen;
+  // the kernels the descriptor's int8 features allow, and of those the ones the tensors'
+  // alignment allows
+  const int feat = kernel_set(op, d);
+  const int kset = aligned ? feat : KSET_FIRST;
   fcm_plan_t p;
   if (plan_in) {
     if (plan_in->op != op) return fail(FCM_EINVAL, "plan was made for another module");
     p = *plan_in;
     if ((st = evaluate_plan(g, d, hw, &p)) != FCM_OK) return st;
-    if (!aligned && variant_needs_alignment(p.variant))
-      return fail(FCM_EUNSUPPORTED, first_gen ? "per-channel requantisation and zero points run on the "
-                                                "first-generation kernels only"
-                                              : "plan's kernel needs 16-byte aligned tensors");
+    if (!variant_in_set(p.variant, kset))
+      return fail(FCM_EUNSUPPORTED, !variant_in_set(p.variant, feat) ? kset_message(feat)
+                                                                       : "plan's kernel needs 16-byte aligned tensors");
   } else {
-    if ((st = find_plan(op, d, &hw, &p, aligned)) != FCM_OK) return st;
+    if ((st = find_plan(op, d, &hw, &p, kset)) != FCM_OK) return st;
   }
   int nv = 0;
   const Variant* vs = all_variants(&nv);
@@ -311,7 +317,7 @@ fcm_status fcm_plan(int32_t op, const fcm_desc* desc, const fcm_hw_desc* hw, fcm
   if (!out) return fail(FCM_EINVAL, "output plan is NULL");
   fcm_status st = validate(op, desc);
   if (st != FCM_OK) return st;
-  return find_plan(op, desc, hw, out, !needs_first_gen(op, desc));
+  return find_plan(op, desc, hw, out, kernel_set(op, desc));
 }
 
 fcm_status fcm_plan_evaluate(const fcm_desc* desc, const fcm_hw_desc* hw, fcm_plan_t* plan) {
@@ -322,12 +328,11 @@ fcm_status fcm_plan_evaluate(const fcm_desc* desc, const fcm_hw_desc* hw, fcm_pl
   const Geom g = geometry(plan->op, desc);
   st = evaluate_plan(g, desc, h, plan);
   if (st != FCM_OK) return st;
-  const bool first_gen = needs_first_gen(plan->op, desc);
-  if (first_gen && variant_needs_alignment(plan->variant))
-    return fail(FCM_EUNSUPPORTED, "per-channel requantisation and zero points run on the first-generation kernels only");
+  const int kset = kernel_set(plan->op, desc);
+  if (!variant_in_set(plan->variant, kset)) return fail(FCM_EUNSUPPORTED, kset_message(kset));
   // the layer-by-layer figures and the verdict come from the searched plan
   fcm_plan_t ref;
-  st = find_plan(plan->op, desc, &h, &ref, !first_gen);
+  st = find_plan(plan->op, desc, &h, &ref, kset);
   if (st != FCM_OK) return st;
   plan->bytes_lbl_paper = ref.bytes_lbl_paper;
   plan->bytes_lbl_ideal = ref.bytes_lbl_ideal;

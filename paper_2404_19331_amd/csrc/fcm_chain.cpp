@@ -153,7 +153,7 @@ fcm_status fcm_chain_plan(const fcm_chain_desc* chain, int32_t objective, const 
       }
       Opt o;
       o.op = op;
-      st = find_plan(op, &d, &H, &o.plan, !needs_first_gen(op, &d));
+      st = find_plan(op, &d, &H, &o.plan, kernel_set(op, &d));
       if (st != FCM_OK) {
         if (single) return st;
         continue;

@@ -11,9 +11,15 @@ namespace fcm {
 // Record a failure message for fcm_last_error() and return the status.
 fcm_status fail(fcm_status st, const std::string& msg);
 
-// Whether an int8 descriptor asks for per-channel requantisation or a nonzero zero point
-// in any stage of op (features of the first-generation kernels only).
-bool needs_first_gen(int op, const fcm_desc* d);
+// Kernel sets a descriptor may run on: the first-generation kernels always; with
+// KSET_DMA every kernel; with KSET_REG only (zero points) also the PW->PW register
+// kernel's instances of at most kZpMaxTiles output tiles.
+enum { KSET_FIRST = 0, KSET_DMA = 1, KSET_REG = 2, KSET_ALL = 3 };
+// The set an int8 descriptor's features allow: per-channel requantisation -> first
+// generation only; zero points -> first generation and the register kernel; else all.
+int kernel_set(int op, const fcm_desc* d);
+// Whether compiled variant `variant` belongs to kernel set `kset`.
+bool variant_in_set(int variant, int kset);
 
 // Argument checks common to fcm_plan and every launch entry point.
 fcm_status validate(int op, const fcm_desc* d);
@@ -34,9 +40,9 @@ Geom geometry(int op, const fcm_desc* d);
 // Returns FCM_EUNSUPPORTED if the variant cannot implement the tiling.
 fcm_status evaluate_plan(const Geom& g, const fcm_desc* d, const fcm_hw_desc& hw, fcm_plan_t* p);
 
-// Search (cached). plan_out is fully filled on success. allow_dma = false excludes the
-// kernels that need 16-byte aligned tensors (LDS-DMA staging).
-fcm_status find_plan(int op, const fcm_desc* d, const fcm_hw_desc* hw, fcm_plan_t* plan_out, bool allow_dma = true);
+// Search (cached) over the variants of kernel set kset. plan_out is fully filled on
+// success.
+fcm_status find_plan(int op, const fcm_desc* d, const fcm_hw_desc* hw, fcm_plan_t* plan_out, int kset = KSET_ALL);
 
 // Whether a compiled variant stages through LDS-DMA (needs 16-byte aligned tensors).
 bool variant_needs_alignment(int variant);

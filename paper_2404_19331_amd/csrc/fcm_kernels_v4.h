@@ -25,6 +25,15 @@
 //   order) in LDS, meet at one barrier, and wave j then finishes the output tiles t with
 //   t % S == j, adding the S partial sums in wave order (int8 sums are exact, float sums
 //   always in the same order, so results are reproducible).
+//
+//   ZP (int8 with zero points): the MFMAs take raw codes; each contraction then loses
+//   (input zero point) x (weight-row sum). The row sums come from the weight operands
+//   already in registers: a lane adds the 16 bytes it holds with a four-way dot product
+//   against ones, two butterfly shuffles complete the row over the four lane groups, and
+//   each accumulator lane reads the rows it holds. The first convolution's sums are taken
+//   per chunk (its rows change with the chunk), the second's accumulate over the wave's
+//   chunks and are subtracted before the partial sums are combined. Epilogues add the
+//   stage's output zero point after rounding and clamp ReLU there.
 #pragma once
 
 #include "fcm_kernels_v3.h"
@@ -46,6 +55,41 @@ __device__ __forceinline__ u32x4 load_slot4(rsrc_t r, uint32_t row_off, int off,
   return v;
 }
 
+// int8 epilogue with an output zero point: round half to even, add zp, clamp to
+// [qlo, qhi] (which hold ReLU's floor at zp, see zp_epi).
+__device__ __forceinline__ int32_t epi_i_zp(int32_t acc, const Epi3& e, int32_t zp) {
+  const int64_t t = (int64_t)acc * e.mult;
+  const int64_t half = ((int64_t)1 << e.shift) >> 1;
+  const int64_t rnd = e.shift > 0 ? half - 1 + ((t >> e.shift) & 1) : 0;
+  int64_t q = ((t + rnd) >> e.shift) + zp;
+  q = q < e.qlo ? e.qlo : q;
+  q = q > e.qhi ? e.qhi : q;
+  return (int32_t)q;
+}
+// The clamp range of a stage whose output has zero point zp: ReLU / ReLU6 floor at zp.
+__device__ __forceinline__ Epi3 zp_epi(int act, const Requant& rq) {
+  Epi3 e = make_epi3(act, rq);
+  e.qlo = act != ACT_NONE ? max(rq.qmin, rq.zp) : rq.qmin;
+  e.qhi = act != ACT_NONE ? max(rq.qmax, rq.zp) : rq.qmax;
+  return e;
+}
+// Sum of the 16 int8 codes of a 16-byte operand slot, added to acc.
+__device__ __forceinline__ int32_t sum_i8x16(const u32x4& v, int32_t acc) {
+#pragma unroll
+  for (int q = 0; q < 4; ++q) acc = __builtin_amdgcn_sdot4((int)v[q], 0x01010101, acc, false);
+  return acc;
+}
+// Row sums held by lanes (row l % 16, a quarter of it per lane group l / 16) completed
+// over the four lane groups; out[v] = the sum of row 4 * (l / 16) + v, the accumulator
+// rows of lane l. All 64 lanes of the wave take part.
+__device__ __forceinline__ void rows_to_acc_lanes(int32_t part, int32_t (&out)[4]) {
+  part += __shfl_xor(part, 16);
+  part += __shfl_xor(part, 32);
+  const int g = (threadIdx.x & 63) >> 4;
+#pragma unroll
+  for (int v = 0; v < 4; ++v) out[v] = __shfl(part, 4 * g + v);
+}
+
 // Stage-one epilogue of M-tile t into the lane's 16-byte operand slot: elements
 // 4t .. 4t+3 of the slot (channels m0 + (16/elt)*group + 4t + v).
 template <class DT>
@@ -59,6 +103,16 @@ struct Mid4<TI8> {
     for (int v = 0; v < 4; ++v) {
       const int32_t s = acc[v];
       w |= ((uint32_t)epi_i(s + b[v], e) & 0xffu) << (8 * v);
+    }
+    slot[t] = w;
+  }
+  __device__ static __forceinline__ void put_zp(u32x4& slot, int t, const i32x4& acc, const int32_t (&b)[4],
+                                                const Epi3& e, int32_t zp) {
+    uint32_t w = 0;
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int32_t s = acc[v];
+      w |= ((uint32_t)epi_i_zp(s + b[v], e, zp) & 0xffu) << (8 * v);
     }
     slot[t] = w;
   }
@@ -102,10 +156,23 @@ __device__ __forceinline__ void store4_out(char* p, const typename DT::AccV& acc
   }
 }
 
+// int8 output of four consecutive channels with an output zero point.
+__device__ __forceinline__ void store4_out_zp(char* p, const i32x4& acc, const int32_t (&b)[4], const Epi3& e,
+                                              int32_t zp) {
+  const int32_t s0 = acc[0], s1 = acc[1], s2 = acc[2], s3 = acc[3];
+  *(uint32_t*)p = ((uint32_t)epi_i_zp(s0 + b[0], e, zp) & 0xffu) |
+                  (((uint32_t)epi_i_zp(s1 + b[1], e, zp) & 0xffu) << 8) |
+                  (((uint32_t)epi_i_zp(s2 + b[2], e, zp) & 0xffu) << 16) |
+                  ((uint32_t)epi_i_zp(s3 + b[3], e, zp) << 24);
+}
+
 // VEC: every operand row is a 16-byte aligned multiple of 16 bytes (x, both weight
 // matrices, the first bias); otherwise operands are read as 4-byte words.
-template <class DT, int KS, int CT, int PB, bool VEC>
+// ZP: int8 with zero points (a.zin: the inputs' of both convolutions, a.rq[].zp: their
+// outputs').
+template <class DT, int KS, int CT, int PB, bool VEC, bool ZP>
 __global__ __launch_bounds__(256) void k_pwpw4(KArgs a) {
+  static_assert(!ZP || std::is_same<DT, TI8>::value, "zero points are int8 only");
   using Acc = typename DT::Acc;
   using AccV = typename DT::AccV;
   constexpr int E = DT::ELT;
@@ -146,7 +213,12 @@ __global__ __launch_bounds__(256) void k_pwpw4(KArgs a) {
 #pragma unroll
     for (int u = 0; u < CT; ++u) acc2[pb][u] = AccV{0, 0, 0, 0};
 
-  const Epi3 e1 = make_epi3(a.act[0], a.rq[0]);
+  const Epi3 e1 = ZP ? zp_epi(a.act[0], a.rq[0]) : make_epi3(a.act[0], a.rq[0]);
+  [[maybe_unused]] int32_t rs2[CT];  // ZP: partial row sums of the second weights (this wave's chunks)
+  if constexpr (ZP) {
+#pragma unroll
+    for (int u = 0; u < CT; ++u) rs2[u] = 0;
+  }
   // operands of one intermediate chunk: the first convolution's weight rows (permuted,
   // see above), the chunk's slice of the second convolution's weights, the first bias
   struct Ops {
@@ -189,6 +261,21 @@ __global__ __launch_bounds__(256) void k_pwpw4(KArgs a) {
     __builtin_amdgcn_sched_barrier(0);
   };
   auto compute = [&](const Ops& o) {
+    [[maybe_unused]] int32_t b1z[TPC][4];  // ZP: first bias minus zin x row sums
+    if constexpr (ZP) {
+#pragma unroll
+      for (int t = 0; t < TPC; ++t) {
+        int32_t part = 0;
+#pragma unroll
+        for (int s = 0; s < KS; ++s) part = sum_i8x16(o.a1[t][s], part);
+        int32_t rs[4];
+        rows_to_acc_lanes(part, rs);
+#pragma unroll
+        for (int v = 0; v < 4; ++v) b1z[t][v] = o.b1[t][v] - a.zin[0] * rs[v];
+      }
+#pragma unroll
+      for (int u = 0; u < CT; ++u) rs2[u] = sum_i8x16(o.a2[u], rs2[u]);
+    }
 #pragma unroll
     for (int pb = 0; pb < PB; ++pb) {
       u32x4 mid = {0u, 0u, 0u, 0u};
@@ -197,7 +284,10 @@ __global__ __launch_bounds__(256) void k_pwpw4(KArgs a) {
         AccV acc1 = AccV{0, 0, 0, 0};
 #pragma unroll
         for (int s = 0; s < KS; ++s) mma16(DT(), acc1, o.a1[t][s], xb[pb][s]);
-        Mid4<DT>::put(mid, t, acc1, o.b1[t], e1);
+        if constexpr (ZP)
+          Mid4<DT>::put_zp(mid, t, acc1, b1z[t], e1, a.rq[0].zp);
+        else
+          Mid4<DT>::put(mid, t, acc1, o.b1[t], e1);
       }
 #pragma unroll
       for (int u = 0; u < CT; ++u) mma16(DT(), acc2[pb][u], o.a2[u], mid);
@@ -224,7 +314,22 @@ __global__ __launch_bounds__(256) void k_pwpw4(KArgs a) {
     }
   }
 
-  const Epi3 e2 = make_epi3(a.act[1], a.rq[1]);
+  if constexpr (ZP) {
+    // the second convolution read codes of zero point zin[1]: subtract it times this
+    // wave's share of each weight-row sum (the shares add up over the split waves)
+    if (active && j < nch) {  // wave-uniform
+#pragma unroll
+      for (int u = 0; u < CT; ++u) {
+        int32_t rs[4];
+        rows_to_acc_lanes(rs2[u], rs);
+#pragma unroll
+        for (int pb = 0; pb < PB; ++pb)
+#pragma unroll
+          for (int v = 0; v < 4; ++v) acc2[pb][u][v] -= a.zin[1] * rs[v];
+      }
+    }
+  }
+  const Epi3 e2 = ZP ? zp_epi(a.act[1], a.rq[1]) : make_epi3(a.act[1], a.rq[1]);
   char* y = (char*)a.y;
   // final epilogue of output tile u of pixel block pb: lane (pixel r16, group g) holds
   // output channels 16u + 4g + [0, 4)
@@ -235,7 +340,10 @@ __global__ __launch_bounds__(256) void k_pwpw4(KArgs a) {
     Acc b[4];
 #pragma unroll
     for (int q = 0; q < 4; ++q) b[q] = load_bias<DT>(a.b2, co + q);
-    store4_out<DT>(y + ((size_t)p * a.Co + co) * E, v, b, e2);
+    if constexpr (ZP)
+      store4_out_zp(y + ((size_t)p * a.Co + co) * E, v, b, e2, a.rq[1].zp);
+    else
+      store4_out<DT>(y + ((size_t)p * a.Co + co) * E, v, b, e2);
   };
 
   if (S > 1) {
@@ -267,7 +375,16 @@ __global__ __launch_bounds__(256) void k_pwpw4(KArgs a) {
 template <class DT, int KS, int CT, int PB>
 int launch_pwpw4(const KArgs& a, int grid, void* stream) {
   const bool vec = a.vec_x && a.vec_w1 && a.vec_w2 && ((uintptr_t)a.b1 & 15) == 0;
-  const void* fn = vec ? (const void*)k_pwpw4<DT, KS, CT, PB, true> : (const void*)k_pwpw4<DT, KS, CT, PB, false>;
+  const void* fn = vec ? (const void*)k_pwpw4<DT, KS, CT, PB, true, false>
+                       : (const void*)k_pwpw4<DT, KS, CT, PB, false, false>;
+  if ((a.zin[0] | a.zin[1] | a.rq[0].zp | a.rq[1].zp) != 0) {
+    // zero points: int8 instances of at most kZpMaxTiles output tiles (the row sums of
+    // the second weights need CT more registers; larger instances exceed the budget)
+    if constexpr (std::is_same<DT, TI8>::value && CT <= kZpMaxTiles)
+      fn = vec ? (const void*)k_pwpw4<DT, KS, CT, PB, true, true> : (const void*)k_pwpw4<DT, KS, CT, PB, false, true>;
+    else
+      return (int)hipErrorInvalidValue;  // the planner never selects such a plan
+  }
   const int lds = a.splits > 1 ? 4 * PB * ceil_div(a.Co, 16) * 1024 : 0;
   if (lds > 65536) {
     const hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, lds);

@@ -257,6 +257,20 @@ bool variant_needs_alignment(int variant) {
   return variant >= 0 && variant < nv && vs[variant].gen >= 2;
 }
 
+// Generations 2 and 3 need the full set; the register kernel (4) is also in KSET_REG
+// (zero points) for its instances of at most kZpMaxTiles output tiles.
+static bool in_set(const Variant& v, int kset) {
+  if (v.gen < 2) return true;
+  if (kset & KSET_DMA) return true;
+  return v.gen == 4 && (kset & KSET_REG) && v.max_cob <= 16 * kZpMaxTiles;
+}
+
+bool variant_in_set(int variant, int kset) {
+  int nv = 0;
+  const Variant* vs = all_variants(&nv);
+  return variant >= 0 && variant < nv && in_set(vs[variant], kset);
+}
+
 static bool variant_matches(const Variant& v, const Geom& g) {
   if (v.family != g.family || v.dtype != g.dtype) return false;
   if (g.family == FAM_PW) return true;
@@ -569,7 +583,7 @@ static const int kTiles3[][2] = {{16, 14}, {8, 14}, {7, 14}, {4, 14}, {14, 14}, 
                                  {2, 4},   {4, 4},  {2, 2},  {3, 7},  {6, 7},  {12, 7}};
 
 static fcm_status search(const Geom& g, const fcm_desc* d, const fcm_hw_desc& hw, fcm_plan_t* best_out,
-                         bool allow_dma) {
+                         int kset) {
   int nv = 0;
   const Variant* vs = all_variants(&nv);
   const int kb = k_block(g.dtype);
@@ -578,7 +592,7 @@ static fcm_status search(const Geom& g, const fcm_desc* d, const fcm_hw_desc& hw
   for (int vi = 0; vi < nv; ++vi) {
     const Variant& v = vs[vi];
     if (!variant_matches(v, g)) continue;
-    if (v.gen >= 2 && !allow_dma) continue;
+    if (!in_set(v, kset)) continue;
     if (v.gen == 4) {
       const int nch = ceil_div(g.cm * g.elt, 64);
       for (int sp = 1; sp <= std::min(4, nch); sp *= 2) {
@@ -789,12 +803,12 @@ static std::vector<int64_t> cache_key(int op, const fcm_desc* d, const fcm_hw_de
   return k;
 }
 
-fcm_status find_plan(int op, const fcm_desc* d, const fcm_hw_desc* hw_in, fcm_plan_t* out, bool allow_dma) {
+fcm_status find_plan(int op, const fcm_desc* d, const fcm_hw_desc* hw_in, fcm_plan_t* out, int kset) {
   const fcm_hw_desc hw = hw_in ? *hw_in : default_hw();
   if (hw.num_cus <= 0 || hw.lds_per_wg <= 0 || hw.lds_per_cu <= 0)
     return fail(FCM_EINVAL, "plan: hardware description has non-positive sizes");
   std::vector<int64_t> key = cache_key(op, d, hw);
-  key.push_back(allow_dma ? 1 : 0);
+  key.push_back(kset);
   key.push_back(d->layout);
   {
     std::lock_guard<std::mutex> lock(g_cache_mu);
@@ -806,7 +820,7 @@ fcm_status find_plan(int op, const fcm_desc* d, const fcm_hw_desc* hw_in, fcm_pl
   }
   const Geom g = geometry(op, d);
   fcm_plan_t p;
-  fcm_status st = search(g, d, hw, &p, allow_dma);
+  fcm_status st = search(g, d, hw, &p, kset);
   if (st != FCM_OK) return st;
   // layer-by-layer chain: each stage planned on its own (first pass of Sec. IV)
   std::vector<std::pair<int, fcm_desc>> stages;
@@ -819,7 +833,7 @@ fcm_status find_plan(int op, const fcm_desc* d, const fcm_hw_desc* hw_in, fcm_pl
     int64_t lp = 0, li = 0;
     for (auto& sd : stages) {
       fcm_plan_t sp;
-      st = find_plan(sd.first, &sd.second, &hw, &sp, allow_dma);
+      st = find_plan(sd.first, &sd.second, &hw, &sp, kset);
       if (st != FCM_OK) return st;
       lp += sp.bytes_paper;
       li += sp.bytes_ideal;

@@ -1,6 +1,7 @@
 """GPU parity of asymmetric int8 (zero points) against the CPU oracle, bit-exact.
 
-Zero points run on the first-generation kernels: the window a depthwise stage reads is
+Zero points run on the first-generation kernels and on the PW->PW register kernel's
+instances of at most 128 output channels. First generation: the window a depthwise stage reads is
 padded with its input's code of real 0, the depthwise sum and each pointwise contraction
 lose (input zero point) x (weight sum), the border of the PW -> DW intermediate holds the
 intermediate's code of real 0, and every epilogue adds its output zero point and clamps
@@ -9,7 +10,9 @@ element staging paths (channel rows that are and are not 16-byte multiples), rag
 tiles and channel blocks, an image smaller than the filter footprint (mostly padding),
 strides 1 and 2, zero points at the int8 extremes, per-channel requantisation together
 with zero points, explicit tilings, the layer-by-layer path and a chain run through
-fcm_chain_run.
+fcm_chain_run. The register kernel takes the weight-row sums from the operands in its
+registers; its instances run with every split of the intermediate chunks over 1, 2 and 4
+waves.
 """
 import dataclasses
 
@@ -68,14 +71,17 @@ def test_zero_point_parity(case):
     assert np.array_equal(got, ref), "%s: %d of %d differ" % (case.name, int(np.sum(got != ref)), ref.size)
     if case.h > 3:
         assert len(np.unique(ref)) > 8, case.name
-    assert _first_gen(fcm.plan(case.op, fcm.desc_from_case(case)).variant)
+    v = fcm.plan(case.op, fcm.desc_from_case(case)).variant
+    assert _first_gen(v) or (case.op == "pw_pw" and fcm.variant_name(v).startswith("k_pwpw4<i8,")), \
+        fcm.variant_name(v)
     if case.op not in ("dw", "pw"):
         assert np.array_equal(to_np(run_unfused(case, d)), ref), case.name + " (layer-by-layer)"
 
 
 @pytest.mark.parametrize("op", list(OPS))
 def test_zero_point_explicit_tilings(op):
-    case = _case(op, 1, "nhwc", h=19, w=17)
+    # first-generation tilings (PW->PW on NHWC plans the register kernel: its own test below)
+    case = _case(op, 1, "nchw" if op == "pw_pw" else "nhwc", h=19, w=17)
     inp = make_inputs(case)
     ref = oracle_ref(case, inp)
     d = dev_inputs(inp, case.dtype)
@@ -136,3 +142,37 @@ def test_zero_point_chain_matches_layer_by_layer_oracle():
     y, p = run_chain(spec, "bytes", xd, wd, bd)
     assert p.fused_layers > 0
     assert len(np.unique(ref)) > 8
+
+
+REG_SHAPES = [(40, 200, 40), (36, 100, 20), (64, 960, 4), (24, 144, 24), (128, 64, 128), (16, 64, 16)]
+
+
+@pytest.mark.parametrize("ci,cm,co", REG_SHAPES, ids=lambda v: str(v))
+def test_zero_points_register_kernel_every_variant_and_split(ci, cm, co):
+    case = Case("pw_pw", 2, 13, 11, ci, cm, co, 1, 1, 0, "i8", "nhwc", ("relu", "none", "none"),
+                ((1, 8, -128, 127, -37), (5, 9, -128, 100, 21), (1, 1, -128, 127)), dist_x="i8",
+                dist_w="i8small", bias=True, seed=4300 + ci + co, name="zp-reg-%d-%d-%d" % (ci, cm, co), zp_in=-128)
+    inp = make_inputs(case)
+    ref = oracle_ref(case, inp)
+    assert len(np.unique(ref)) > 8
+    d = dev_inputs(inp, case.dtype)
+    desc = fcm.desc_from_case(case)
+    assert fcm.variant_name(fcm.plan("pw_pw", desc).variant).startswith("k_pwpw4<i8,")
+    nch = -(-cm // 64)
+    n = 0
+    for v in range(fcm.lib().fcm_variant_count()):
+        name = fcm.variant_name(v)
+        if not name.startswith("k_pwpw4<i8,"):
+            continue
+        pb = int(name.rstrip(">").split(",")[3])
+        for s in (1, 2, 4):
+            if s > nch:
+                continue
+            try:
+                p = fcm.plan_evaluate("pw_pw", desc, 1, 16 * pb, 64, -(-co // 16) * 16, v, splits=s)
+            except fcm.FcmError:
+                continue
+            got = to_np(run_fused(case, d, plan=p))
+            assert np.array_equal(got, ref), "%s %s splits %d: %d differ" % (case.name, name, s, int(np.sum(got != ref)))
+            n += 1
+    assert n >= 2

@@ -281,12 +281,33 @@ def test_zero_points_plan_first_generation_kernels(op):
     variants = [(5, (0, 0, 0))] + [(0, tuple(-7 if j == i else 0 for j in range(3))) for i in range(stages)]
     for zin, zps in variants:
         p = fcm.plan(op, _zp_desc(op, zin, zps))
-        assert _first_gen(p.variant), (zin, zps, fcm.variant_name(p.variant))
+        name = fcm.variant_name(p.variant)
+        if op == "pw_pw":  # the register kernel carries zero points (up to 128 output channels)
+            assert name.startswith("k_pwpw4<i8,"), (zin, zps, name)
+        else:
+            assert _first_gen(p.variant), (zin, zps, name)
     # a zero point of a stage the module does not have is ignored, as are float types
     if stages < 3:
         assert fcm.plan(op, _zp_desc(op, 0, (0, 0, 9) if stages == 2 else (0, 9, 9))).as_dict() == sym.as_dict()
     f = fcm.plan(op, _zp_desc(op, 5, (3, 3, 3), dtype="bf16"))
     assert f.as_dict() == fcm.plan(op, _zp_desc(op, dtype="bf16")).as_dict()
+
+
+def test_zero_points_on_the_register_kernel_up_to_128_output_channels():
+    for co, reg in ((64, True), (128, True), (144, False), (256, False)):
+        d = fcm.make_desc(4, 28, 28, 64, 128, co, k=1, stride=1, pad=0, dtype="i8", layout="nhwc",
+                          act=("relu", "none"), rq=[(1, 6, -128, 127, 3)] * 3, zp_in=-2)
+        name = fcm.variant_name(fcm.plan("pw_pw", d).variant)
+        assert name.startswith("k_pwpw4<i8,") == reg, (co, name)
+        if not reg:
+            assert _first_gen(fcm.plan("pw_pw", d).variant)
+    # an explicit plan on a register-kernel instance with more output tiles is refused
+    d = fcm.make_desc(4, 28, 28, 64, 128, 256, k=1, stride=1, pad=0, dtype="i8", layout="nhwc",
+                      rq=[(1, 6, -128, 127, 3)] * 3)
+    big = [v for v in range(fcm.lib().fcm_variant_count()) if fcm.variant_name(v) == "k_pwpw4<i8,4,16,1>"][0]
+    with pytest.raises(fcm.FcmError) as e:
+        fcm.plan_evaluate("pw_pw", d, 1, 16, 64, 256, big)
+    assert e.value.status == EUNSUPPORTED and "zero points" in str(e.value)
 
 
 def test_zero_points_validation_and_explicit_plans():

@@ -45,7 +45,7 @@ struct ReqCh {
 
 // Zero points (int8) on the PW->PW register kernel: instances of at most this many
 // output-channel tiles of 16.
-constexpr int kZpMaxTiles = 8;
+constexpr int kZpMaxTiles = 12;
 
 FCM_HD inline int elt_size(int dt) { return dt == DT_F32 ? 4 : (dt == DT_BF16 ? 2 : 1); }
 // contraction elements per MFMA operand step (64 bytes of k per row)

@@ -1,7 +1,7 @@
 """GPU parity of asymmetric int8 (zero points) against the CPU oracle, bit-exact.
 
 Zero points run on the first-generation kernels and on the PW->PW register kernel's
-instances of at most 128 output channels. First generation: the window a depthwise stage reads is
+instances of at most 192 output channels. First generation: the window a depthwise stage reads is
 padded with its input's code of real 0, the depthwise sum and each pointwise contraction
 lose (input zero point) x (weight sum), the border of the PW -> DW intermediate holds the
 intermediate's code of real 0, and every epilogue adds its output zero point and clamps
@@ -144,7 +144,8 @@ def test_zero_point_chain_matches_layer_by_layer_oracle():
     assert len(np.unique(ref)) > 8
 
 
-REG_SHAPES = [(40, 200, 40), (36, 100, 20), (64, 960, 4), (24, 144, 24), (128, 64, 128), (16, 64, 16)]
+REG_SHAPES = [(40, 200, 40), (36, 100, 20), (64, 960, 4), (24, 144, 24), (128, 64, 128), (16, 64, 16),
+              (160, 960, 160), (192, 100, 180)]
 
 
 @pytest.mark.parametrize("ci,cm,co", REG_SHAPES, ids=lambda v: str(v))

@@ -282,7 +282,7 @@ def test_zero_points_plan_first_generation_kernels(op):
     for zin, zps in variants:
         p = fcm.plan(op, _zp_desc(op, zin, zps))
         name = fcm.variant_name(p.variant)
-        if op == "pw_pw":  # the register kernel carries zero points (up to 128 output channels)
+        if op == "pw_pw":  # the register kernel carries zero points (up to 192 output channels)
             assert name.startswith("k_pwpw4<i8,"), (zin, zps, name)
         else:
             assert _first_gen(p.variant), (zin, zps, name)
@@ -293,8 +293,8 @@ def test_zero_points_plan_first_generation_kernels(op):
     assert f.as_dict() == fcm.plan(op, _zp_desc(op, dtype="bf16")).as_dict()
 
 
-def test_zero_points_on_the_register_kernel_up_to_128_output_channels():
-    for co, reg in ((64, True), (128, True), (144, False), (256, False)):
+def test_zero_points_on_the_register_kernel_up_to_192_output_channels():
+    for co, reg in ((64, True), (128, True), (192, True), (208, False), (256, False)):
         d = fcm.make_desc(4, 28, 28, 64, 128, co, k=1, stride=1, pad=0, dtype="i8", layout="nhwc",
                           act=("relu", "none"), rq=[(1, 6, -128, 127, 3)] * 3, zp_in=-2)
         name = fcm.variant_name(fcm.plan("pw_pw", d).variant)

@@ -600,9 +600,11 @@ __device__ __forceinline__ void dw_compute(const char* sin, int ips, int IW, con
 // ------------------------------------------------------------------------------------
 
 // Row sums of int8 weights w [rows][cc]: out[v] = sum_c w[row0 + 4 * (lane / 16) + v][c]
-// (0 for rows >= rows_valid), the rows of this lane's accumulators. Lane l adds every
-// fourth element of row row0 + l % 16 from element l / 16; two butterfly steps complete
-// each sum and every lane then reads its four. All 64 lanes of the wave must call it.
+// (0 for rows >= rows_valid), the rows of this lane's accumulators. Lane l adds a quarter
+// of row row0 + l % 16 (every fourth 4-byte word from word l / 16 with a four-way dot
+// product against ones when rows are whole aligned words, else every fourth byte); two
+// butterfly steps complete each sum and every lane then reads its four. All 64 lanes of
+// the wave must call it.
 __device__ __forceinline__ void int8_row_sums(const int8_t* w, int cc, int row0, int rows_valid,
                                               int32_t (&out)[4]) {
   const int lane = threadIdx.x & 63;
@@ -610,7 +612,15 @@ __device__ __forceinline__ void int8_row_sums(const int8_t* w, int cc, int row0,
   int32_t s = 0;
   if (row < rows_valid) {
     const int8_t* p = w + (size_t)row * cc;
-    for (int c = lane >> 4; c < cc; c += 4) s += p[c];
+    if ((cc & 3) == 0 && ((uintptr_t)w & 3) == 0) {
+      const int32_t* p4 = (const int32_t*)p;
+      const int nw = cc >> 2;
+#pragma unroll 4
+      for (int c = lane >> 4; c < nw; c += 4) s = __builtin_amdgcn_sdot4(p4[c], 0x01010101, s, false);
+    } else {
+#pragma unroll 4
+      for (int c = lane >> 4; c < cc; c += 4) s += p[c];
+    }
   }
   s += __shfl_xor(s, 16);
   s += __shfl_xor(s, 32);

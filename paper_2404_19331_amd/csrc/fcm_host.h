@@ -33,6 +33,7 @@ struct Geom {
   int ho, wo;           // output
   int dtype, elt;
   int layout;
+  int zp;               // int8 with a nonzero zero point in any stage (time models)
 };
 Geom geometry(int op, const fcm_desc* d);
 

@@ -45,6 +45,7 @@ static int out_dim(int x, int k, int s, int p) { return (x + 2 * p - k) / s + 1;
 Geom geometry(int op, const fcm_desc* d) {
   Geom g = {};
   g.op = op;
+  g.zp = kernel_set(op, d) == KSET_REG ? 1 : 0;
   g.n = d->n;
   g.h = d->h;
   g.w = d->w;
@@ -518,29 +519,39 @@ static double module_flops(const Geom& g) {
 // fitted (non-negative least squares on relative error) to every candidate module of the
 // MobileNetV2 layer chain, int8 and bf16, batch 1 and 32, timed on MI355X; the fitted
 // figures are within about 0.5-1.5x of the timings. FP32 takes the bf16 figures.
+// zp = 1: the first-generation kernels with int8 zero points (they add the weight-row sums
+// and run layers the persistent kernels would otherwise take), fitted the same way to every
+// candidate module of the MobileNetV2 int8 chain at batch 32 with a zero point on every
+// tensor (0.34-1.41x of the timings).
 struct LinModel {
-  int family, gen, dtype;
+  int family, gen, dtype, zp;
   double c0, per_mb, per_gflop, per_kwg;
 };
 static const LinModel kLinModels[] = {
-    {FAM_PW, 1, DT_I8, 6.56, 3.617, 0.0, 0.0},
-    {FAM_PWDW, 1, DT_BF16, 7.97, 0.0, 27.647, 12.939},
-    {FAM_PWDW, 1, DT_I8, 10.05, 0.0, 24.499, 15.288},
-    {FAM_PWDWPW, 1, DT_BF16, 21.16, 1.864, 0.0, 3.306},
-    {FAM_PWDWPW, 1, DT_I8, 33.52, 4.262, 0.0, 25.127},
-    {FAM_PWPW, 1, DT_BF16, 6.16, 0.649, 0.0, 0.0},
-    {FAM_PWPW, 1, DT_I8, 6.21, 0.822, 0.0, 0.0},
-    {FAM_PWPW, 4, DT_BF16, 3.97, 0.0, 27.116, 0.661},
-    {FAM_PWPW, 4, DT_I8, 7.01, 0.0, 14.325, 12.663},
+    {FAM_PW, 1, DT_I8, 0, 6.56, 3.617, 0.0, 0.0},
+    {FAM_PWDW, 1, DT_BF16, 0, 7.97, 0.0, 27.647, 12.939},
+    {FAM_PWDW, 1, DT_I8, 0, 10.05, 0.0, 24.499, 15.288},
+    {FAM_PWDWPW, 1, DT_BF16, 0, 21.16, 1.864, 0.0, 3.306},
+    {FAM_PWDWPW, 1, DT_I8, 0, 33.52, 4.262, 0.0, 25.127},
+    {FAM_PWPW, 1, DT_BF16, 0, 6.16, 0.649, 0.0, 0.0},
+    {FAM_PWPW, 1, DT_I8, 0, 6.21, 0.822, 0.0, 0.0},
+    {FAM_PWPW, 4, DT_BF16, 0, 3.97, 0.0, 27.116, 0.661},
+    {FAM_PWPW, 4, DT_I8, 0, 7.01, 0.0, 14.325, 12.663},
+    {FAM_DWPW, 1, DT_I8, 1, 0.00, 1.024, 92.594, 2.451},
+    {FAM_DW, 1, DT_I8, 1, 3.96, 0.833, 18.913, 8.613},
+    {FAM_PW, 1, DT_I8, 1, 4.04, 0.000, 27.904, 8.483},
+    {FAM_PWDW, 1, DT_I8, 1, 11.61, 0.000, 26.027, 29.295},
+    {FAM_PWDWPW, 1, DT_I8, 1, 0.00, 4.790, 38.501, 44.039},
+    {FAM_PWPW, 1, DT_I8, 1, 0.00, 2.057, 0.000, 0.000},
 };
 
 static double linear_time_estimate(const Variant& v, const Geom& g, const fcm_plan_t& p) {
   const int dt = g.dtype == DT_F32 ? DT_BF16 : g.dtype;
   const LinModel* m = nullptr;
-  for (const LinModel& l : kLinModels)
-    if (l.family == v.family && l.gen == v.gen && l.dtype == dt) m = &l;
+  for (const LinModel& l : kLinModels)  // the zero-point figure if there is one
+    if (l.family == v.family && l.gen == v.gen && l.dtype == dt && (l.zp == g.zp || (!m && l.zp == 0))) m = &l;
   // kernels never timed for the fit: a conservative generic figure
-  static const LinModel kGeneric = {0, 0, 0, 10.0, 2.0, 25.0, 10.0};
+  static const LinModel kGeneric = {0, 0, 0, 0, 10.0, 2.0, 25.0, 10.0};
   if (!m) m = &kGeneric;
   const double us = m->c0 + m->per_mb * (double)p.bytes_tiled / 1e6 + m->per_gflop * module_flops(g) / 1e9 +
                     m->per_kwg * (double)p.workgroups / 1e3;

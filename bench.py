@@ -35,7 +35,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="C3b32",
-                    choices=["C1", "C2", "C3b1", "C3b32", "C4", "C5", "PWPW", "MNV2", "MNV2bf16"])
+                    choices=["C1", "C2", "C3b1", "C3b32", "C4", "C5", "PWPW", "MNV2", "MNV2bf16", "MNV2zp"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target CPU-baseline sample time")
     ap.add_argument("--layers", default=None, help="comma-separated layer indices (subset)")
@@ -354,7 +354,7 @@ def bench_chain(a, torch, fcm):
     import numpy as np
     from paper_2404_19331_amd.workloads import mobilenetv2_chain, make_chain_inputs
     dtype = "bf16" if a.workload == "MNV2bf16" else "i8"
-    spec = mobilenetv2_chain(n=32, dtype=dtype)
+    spec = mobilenetv2_chain(n=32, dtype=dtype, zero_points=a.workload == "MNV2zp")
     x, ws, bs = make_chain_inputs(spec)
 
     def dev(v):
@@ -367,7 +367,7 @@ def bench_chain(a, torch, fcm):
     xd, wd, bd = dev(x), [dev(w) for w in ws], [dev(b) for b in bs]
     nsets = max(2, -(-ROTATE_BYTES // (xd.numel() * xd.element_size())))
     xs = [xd] + [xd.clone() for _ in range(nsets - 1)]
-    d = fcm.chain_desc(spec.n, spec.h, spec.w, spec.c, spec.layers, spec.dtype, spec.layout)
+    d = fcm.chain_desc(spec.n, spec.h, spec.w, spec.c, spec.layers, spec.dtype, spec.layout, zp_in=spec.zp_in)
     stream = torch.cuda.current_stream()
     res = {}
     from paper_2404_19331_amd.autotune import chain_autotune

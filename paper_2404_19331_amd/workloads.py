@@ -268,13 +268,16 @@ class ChainSpec:
     zp_in: int = 0               # int8 zero point of x (rq entries may carry a 5th: output zero point)
 
 
-def mobilenetv2_chain(n=8, dtype="i8", layout="nhwc", h=112, w=112, stages=None, final_pw=True):
+def mobilenetv2_chain(n=8, dtype="i8", layout="nhwc", h=112, w=112, stages=None, final_pw=True,
+                      zero_points=False):
     """The DW and PW layers of MobileNetV2 after its stem (51 layers at full depth): per
     block an expansion PW (t > 1), a DW 3x3 and a linear projection PW, then the final PW
     to 1280 channels. Float types use ReLU6 after the expansion and the DW; int8 uses ReLU
-    there (int8 ReLU6 is not supported) and requantises every layer by 2^-s, s sized to
-    the layer's accumulator spread (U{-127..127} weights, inputs of RMS about 48 or, after
-    ReLU, 34) so outputs spread over the int8 range."""
+    there (its requantisation by a power of two has no output scale that would place 6.0)
+    and requantises every layer by 2^-s, s sized to the layer's accumulator spread
+    (U{-127..127} weights, inputs of RMS about 48 or, after ReLU, 34) so outputs spread over
+    the int8 range. zero_points (int8): asymmetric tensors, the input and every ReLU output
+    with zero point -128 (real 0 at the bottom of the code range), linear outputs with 3."""
     stages = MNV2_STAGES if stages is None else stages
     act = "relu" if dtype == "i8" else "relu6"
     sd_w = 127 / math.sqrt(3)
@@ -285,6 +288,8 @@ def mobilenetv2_chain(n=8, dtype="i8", layout="nhwc", h=112, w=112, stages=None,
     def rq_for(fan_in, relu):
         s = int(round(math.log2(max(1.0, sd_in[0] * sd_w * math.sqrt(fan_in) / 48))))
         sd_in[0] = 48 / math.sqrt(2) if relu else 48.0
+        if zero_points:
+            return (1, s, -127, 127, -128 if relu else 3)
         return (1, s, -127, 127)
 
     for t, co, reps, s0 in stages:
@@ -298,7 +303,9 @@ def mobilenetv2_chain(n=8, dtype="i8", layout="nhwc", h=112, w=112, stages=None,
     if final_pw:
         layers.append(dict(kind="pw", c_out=1280, act=act, rq=rq_for(c, True)))
     return ChainSpec(n, h, w, 32, dtype, layout, layers, seed=BASE_SEED + 7,
-                     name="MobileNetV2 body %d layers %s %s b%d" % (len(layers), dtype, layout, n))
+                     name="MobileNetV2 body %d layers %s%s %s b%d" % (len(layers), dtype,
+                                                                    " zero points" if zero_points else "", layout, n),
+                     zp_in=-128 if zero_points else 0)
 
 
 def make_chain_inputs(spec, seed=None):

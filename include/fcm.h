@@ -130,7 +130,9 @@ typedef struct {
   /* int8 zero point of the input x (the code of real 0, in [-128, 127]); the input of
    * stage i > 0 has the zero point of stage i-1's output, rq[i-1].zero_point. Descriptors
    * with a nonzero zero point anywhere are planned and launched on the first-generation
-   * kernels only. Ignored for float types. */
+   * kernels and on the PW->PW register kernel's instances of at most 192 output channels;
+   * an explicit plan on another kernel fails with FCM_EUNSUPPORTED. Ignored for float
+   * types. */
   int32_t zp_in;
 } fcm_desc;
 

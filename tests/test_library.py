@@ -361,3 +361,19 @@ def test_abi_struct_sizes_match_the_binding(tmp_path):
     assert got == [ctypes.sizeof(fcm.Requant), ctypes.sizeof(fcm.Desc), fcm.Desc.zp_in.offset,
                    ctypes.sizeof(fcm.Layer), ctypes.sizeof(fcm.ChainDesc), fcm.ChainDesc.layers.offset,
                    ctypes.sizeof(fcm.ChainPlan)]
+
+
+def test_zero_point_time_models_are_their_own():
+    """First-generation kernels under zero points are priced by their own fitted figures:
+    the same plan of the same shapes gets another estimate than symmetric, while a float
+    descriptor (zero points ignored) keeps the symmetric one."""
+    for op in ("pw", "dw", "pw_dw_pw"):
+        sym = _zp_desc(op)
+        asym = _zp_desc(op, -128, (5, 5, 5))
+        p = fcm.plan(op, asym)
+        assert _first_gen(p.variant)
+        t_sym, t_zp = fcm.plan_time_estimate(sym, p), fcm.plan_time_estimate(asym, p)
+        assert t_sym > 0 and t_zp > 0 and t_sym != t_zp, op
+        f_sym, f_zp = _zp_desc(op, dtype="bf16"), _zp_desc(op, -128, (5, 5, 5), dtype="bf16")
+        q = fcm.plan(op, f_sym)
+        assert fcm.plan_time_estimate(f_sym, q) == fcm.plan_time_estimate(f_zp, q)

@@ -176,3 +176,19 @@ def test_chain_run_rejects_a_plan_of_another_chain():
     ptrs = (fcm.ctypes.c_void_p * 2)()
     st = fcm.lib().fcm_chain_run(fcm.ctypes.byref(b), fcm.ctypes.byref(pa), None, ptrs, None, None, None, None)
     assert st == EINVAL and "does not match" in fcm.last_error()
+
+
+def test_chain_groups_carry_zero_points():
+    """With zero points, each group of a chain plan is the module planner's plan of the
+    group's descriptor with the zero points it sees: the chain input's (or the previous
+    layer's output zero point) as input, its layers' as outputs."""
+    sp = mobilenetv2_chain(n=4, dtype="i8", h=56, w=56, stages=[(1, 16, 1, 1), (6, 24, 2, 2)], final_pw=False,
+                           zero_points=True)
+    assert sp.zp_in == -128 and all(len(L["rq"]) == 5 for L in sp.layers)
+    d = fcm.chain_desc(sp.n, sp.h, sp.w, sp.c, sp.layers, sp.dtype, sp.layout, zp_in=sp.zp_in)
+    for obj in ("bytes", "time", "unfused"):
+        p = fcm.chain_plan(d, obj)
+        for first, op, plan in p.groups():
+            g = _group_desc(sp.n, sp.h, sp.w, sp.c, sp.layers, first, op, "i8")
+            g.zp_in = sp.zp_in if first == 0 else sp.layers[first - 1]["rq"][4]
+            assert plan.as_dict() == fcm.plan(op, g).as_dict(), (obj, first, op)

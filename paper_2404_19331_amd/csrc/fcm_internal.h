@@ -260,6 +260,39 @@ FCM_HD inline int copies_per_wave3(int mode, int K, int IH, int IWP, int CT, int
   return w0 > t - w0 ? w0 : t - w0;
 }
 
+// Streaming NHWC kernels (k_fused5, host and device): bytes of one LDS ring slot and of
+// the whole allocation. Window and pointwise weights are stored as two planes, plane h
+// holding the 16-byte slots 2h and 2h+1 of each 64-byte channel row at 32 bytes per
+// pixel (or row): the 32 lanes of a half-wave that read one MFMA operand (16 pixels x
+// two slots) then cover 512 distinct bytes, which ds_read_b128 serves without bank
+// conflicts. One LDS-DMA instruction fills 32 pixels (rows) of one plane.
+//   slot:  window [2][nqp][32 B] | PW weights [2][cobp][32 B] | DW words [K*K][CB] + bias [CB]
+//   after the ring: PW bias [COB] (fp32 / int32, whole KiB) | DW output exchange [2][pp][32 B]
+struct Lds5 {
+  int nqp;         // window pixels rounded up to 32
+  int win_bytes;   // 64 * nqp
+  int cobp;        // pointwise rows rounded up to 32 (0 without a PW stage)
+  int dw_off;      // depthwise words within a slot
+  int slot_bytes;
+  int pwb_off;     // PW bias block
+  int dwo_off;     // depthwise output exchange (pp > 0 only)
+  int total;
+};
+FCM_HD inline Lds5 lds5(int dt, int mode, int K, int IH, int IW, int COB, int ring, int pp) {
+  Lds5 L;
+  const int cb = kRowB / elt_size(dt);
+  const bool pw = mode != M3_DW, dw = mode != M3_PW;
+  L.nqp = round_up(IH * IW, 32);
+  L.win_bytes = 64 * L.nqp;
+  L.cobp = pw ? round_up(COB, 32) : 0;
+  L.dw_off = L.win_bytes + 64 * L.cobp;
+  L.slot_bytes = L.dw_off + (dw ? round_up((K * K + 1) * cb * 4, 16) : 0);
+  L.pwb_off = ring * L.slot_bytes;
+  L.dwo_off = L.pwb_off + (pw ? round_up(COB * 4, 1024) : 0);
+  L.total = L.dwo_off + 64 * pp;
+  return L;
+}
+
 // ---------------------------------------------------------------------------------
 // Kernel argument block (one struct for all families; unused fields ignored).
 // ---------------------------------------------------------------------------------
@@ -313,9 +346,13 @@ struct Variant {
                     // 3: as 2, persistent workgroups, run-time tile, max_p = 64 * blocks per wave
                     // 4: PW -> PW with the intermediate in registers, one pixel group per
                     //    wave (max_p = 16 * blocks), all output channels, no LDS
+                    // 5: NHWC streaming kernels, one work tile per workgroup, run-time tile
+                    //    of at most max_p pixels, one compiled output-channel block
   int pitch = 0;    // gen 3: LDS window row pitch in pixels (window width must not exceed it)
   int ks = 1;       // gen 3: 64-byte channel chunks per item; gen 4: 64-byte k-steps of the
-                    // first convolution held in registers (input channels <= 64 * ks bytes)
+                    // first convolution held in registers (input channels <= 64 * ks bytes);
+                    // gen 5: LDS ring slots
+  int wc = 1;       // gen 5: waves across output channels (1, 2 or 4)
 };
 
 // Compiled variants of each translation unit, and all of them in a fixed order
@@ -324,6 +361,9 @@ const Variant* variants_dwpw_f32(int* count);
 const Variant* variants_dwpw_bf16(int* count);
 const Variant* variants_dwpw_i8(int* count);
 const Variant* variants_pwdw(int* count);
+const Variant* variants_v5_dwpw_bf16_s1(int* count);
+const Variant* variants_v5_dwpw_bf16_s2(int* count);
+const Variant* variants_v5_pwdw_bf16(int* count);
 const Variant* variants_pwdwpw(int* count);
 const Variant* variants_v2_bf16(int* count);
 const Variant* variants_v2_f32(int* count);

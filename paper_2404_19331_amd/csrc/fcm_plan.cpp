@@ -194,6 +194,24 @@ static int tiling_lds(const Variant& v, const Geom& g, int TH, int TW, int CB, i
   const int Q = ((TH - 1) * g.s + g.k) * ((TW - 1) * g.s + g.k);
   if (v.max_p && P > v.max_p) return 0;
   if (v.gen != 3 && v.max_q && Q > v.max_q) return 0;
+  if (v.gen == 5) {
+    // NHWC, 16-byte input channel rows, 32-bit buffer offsets, 64-byte chunk, run-time
+    // tile of at most max_p pixels whose window fits the kernel's copy list
+    if (g.layout != FCM_NHWC) return 0;
+    const bool dw_only = g.family == FAM_DW;
+    const int cin = dw_only ? g.cm : g.ci;
+    if ((cin * g.elt) % 16) return 0;
+    if (dw_only ? (g.cm * g.elt) % 16 : (g.co * g.elt) % 4) return 0;
+    if ((int64_t)g.h * g.w * cin * g.elt >= ((int64_t)1 << 31)) return 0;
+    if (!dw_only && (int64_t)(g.co + COB) * g.ci * g.elt >= ((int64_t)1 << 31)) return 0;
+    if (CB != 64 / g.elt || COB != v.max_cob || P > v.max_p) return 0;
+    const int mode = g.family == FAM_DWPW ? M3_DWPW : (g.family == FAM_PW ? M3_PW : M3_DW);
+    const int KE = mode == M3_PW ? 1 : g.k, SE = mode == M3_PW ? 1 : g.s;
+    const int IH = (TH - 1) * SE + KE, IW = (TW - 1) * SE + KE;
+    if (round_up(IH * IW, 32) > 512) return 0;  // window copies: 8 per wave at most
+    const bool share = mode == M3_DWPW && v.wc > 1;
+    return lds5(g.dtype, mode, KE, IH, IW, COB, v.ks, share ? v.max_p : 0).total;
+  }
   if (v.gen == 3) {
     // NHWC, 16-byte input channel rows, 32-bit buffer offsets, 64-byte chunk, run-time
     // tile whose input window fits the kernel's LDS row pitch
@@ -351,6 +369,24 @@ fcm_status evaluate_plan(const Geom& g, const fcm_desc* d, const fcm_hw_desc& hw
   if (wgs <= 0 || wgs > 0x7fffffff) return fail(FCM_EUNSUPPORTED, "plan: grid too large");
   const Bytes b = module_bytes(g, p->tile_h, p->tile_w, p->co_block);
   if (v.gen != 3 && p->splits > 1) return fail(FCM_EUNSUPPORTED, "plan: this kernel variant does not split");
+  if (v.gen == 5) {
+    // persistent: the workgroups resident at once (LDS-limited estimate; the launcher
+    // also applies the compiled kernel's register-limited occupancy), at most one per
+    // work tile; a caller's cap is kept
+    const int64_t per_cu = std::max<int64_t>(1, std::min<int64_t>(8, hw.lds_per_cu / lds));
+    int64_t grid = std::min<int64_t>(wgs, per_cu * hw.num_cus);
+    if (p->workgroups > 0 && p->workgroups < grid) grid = p->workgroups;
+    p->workgroups = (int32_t)grid;
+    p->depth = v.ks;
+    p->splits = 1;
+    p->waves = 4;
+    p->lds_bytes = lds;
+    p->bytes_ideal = b.ideal;
+    p->bytes_tiled = b.tiled;
+    p->bytes_paper = b.paper;
+    p->redundancy = b.redundancy;
+    return FCM_OK;
+  }
   if (v.gen == 3) {
     const int splits = p->splits > 1 ? p->splits : 1;
     if (splits > 1) {
@@ -604,6 +640,7 @@ static fcm_status search(const Geom& g, const fcm_desc* d, const fcm_hw_desc& hw
     const Variant& v = vs[vi];
     if (!variant_matches(v, g)) continue;
     if (!in_set(v, kset)) continue;
+    if (v.gen == 5) continue;  // explicit plans only (no time model yet)
     if (v.gen == 4) {
       const int nch = ceil_div(g.cm * g.elt, 64);
       for (int sp = 1; sp <= std::min(4, nch); sp *= 2) {

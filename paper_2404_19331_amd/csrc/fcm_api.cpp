@@ -1,5 +1,5 @@
 // fcm_api.cpp -- the C ABI of libfcm.so: argument validation, plan lookup, kernel
-// argument marshalling and launch. No allocation, no synchronisation.
+// argument marshalling and launch.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -42,7 +42,7 @@ const Variant* all_variants(int* count) {
   static std::vector<Variant> all = [] {
     std::vector<Variant> v;
     const Variant* (*fns[])(int*) = {variants_dwpw_f32, variants_dwpw_bf16, variants_dwpw_i8, variants_pwdw,
-                                     variants_pwdwpw,   variants_v2_bf16,   variants_v2_f32,  variants_v2_i8,
+                                     variants_pwdwpw,
                                      variants_v3_dwpw_bf16_s1, variants_v3_dwpw_bf16_s2, variants_v3_dwpw_f32,
                                      variants_v3_dwpw_i8, variants_v3_pw, variants_v3_pw_f32, variants_v3_pw_i8,
                                      variants_v3_dw_bf16, variants_v3_dw_f32, variants_v3_dw_i8,
@@ -115,12 +115,6 @@ fcm_status validate(int op, const fcm_desc* d) {
 
 static bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
-#ifdef FCM_TRACE
-// Development builds only: device buffer that the persistent kernels write their
-// per-workgroup shader-clock timeline into.
-static unsigned long long* g_trace = nullptr;
-extern "C" void fcm_debug_trace(void* dev_buffer) { g_trace = (unsigned long long*)dev_buffer; }
-#endif
 
 // Compute units of the current device (queried once per device).
 static int device_cus() {
@@ -282,9 +276,6 @@ static fcm_status run(int op, const fcm_desc* d, const Tensors& t, const fcm_pla
   a.cus = device_cus();
   a.grid_cap = (v.gen == 3 || v.gen == 5) ? p.workgroups : 0;
   a.depth = p.depth;
-#ifdef FCM_TRACE
-  a.trace = g_trace;
-#endif
   if (v.gen >= 2) {
     a.L = LdsLayout{};
     a.L.bytes = p.lds_bytes;

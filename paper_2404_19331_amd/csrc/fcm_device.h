@@ -728,4 +728,24 @@ __device__ __forceinline__ int xcd_remap(int b, int G) {
   return x * q + (x < r ? x : r) + b / kNumXcd;
 }
 
+
+// ------------------------------------------------------------------------------------
+// Buffer resources: 32-bit offsets into [base, base + bytes); an offset at or beyond the
+// end reads zero (the kernels put kOob where the convolution's zero padding or a ragged
+// edge is), and LDS-DMA copies of 16 bytes per lane.
+// ------------------------------------------------------------------------------------
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+
+constexpr uint32_t kOob = 0x80000000u;  // buffer offset beyond any record: reads as zero
+
+__device__ __forceinline__ rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+
+// 16 bytes per lane from (rsrc + voff) to LDS (wave_base + 16 * lane).
+__device__ __forceinline__ void dma16(rsrc_t r, char* wave_base, uint32_t voff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)wave_base, 16, voff, 0, 0,
+                                           0);
+}
+
 }  // namespace fcm

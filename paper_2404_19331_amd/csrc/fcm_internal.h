@@ -168,25 +168,6 @@ FCM_HD inline LdsLayout lds_layout_pwdwpw(int dt, int K, int S, int TH, int TW, 
 // LDS-DMA kernels: bytes of channels per pixel row per staged chunk (one MFMA k-step).
 constexpr int kRowB = 64;
 
-// LDS bytes of the v2 kernels (host and device).
-FCM_HD inline int lds_dwpw2(int dt, int K, int S, bool has_dw, int TH, int TW, int CO_MAX, int COB) {
-  const int e = elt_size(dt);
-  const int KE = has_dw ? K : 1, SE = has_dw ? S : 1;
-  const int npin = ((TH - 1) * SE + KE) * ((TW - 1) * SE + KE);
-  const int in_bytes = (npin + 15) / 16 * 1024;
-  const int cb = kRowB / e;
-  const int wd = has_dw ? ((KE * KE + 1) * cb * 4 + 15) / 16 * 16 : 0;
-  const int buf = in_bytes + CO_MAX * kRowB + wd;
-  const int out = TH * TW * (COB * e + 16);
-  return 2 * buf > out ? 2 * buf : out;
-}
-
-FCM_HD inline int lds_dw2(int dt, int K, int S, int TH, int TW) {
-  const int e = elt_size(dt);
-  const int npin = ((TH - 1) * S + K) * ((TW - 1) * S + K);
-  return (npin + 15) / 16 * 1024 + ((K * K + 1) * (kRowB / e) * 4 + 15) / 16 * 16;
-}
-
 // Persistent NHWC kernels (k_fused3): module selector and LDS bytes of one buffer.
 enum { M3_DWPW = 0, M3_PW = 1, M3_DW = 2 };
 
@@ -323,7 +304,6 @@ struct KArgs {
   int grid_cap;  // persistent kernels: at most this many workgroups (0 = no cap)
   const int32_t* rqc[3];  // int8 per-channel requantisation per stage ([2][channels]) or nullptr
   int zin[3];             // int8 zero point of each stage's input (first-generation kernels)
-  unsigned long long* trace;  // development timeline buffer (used only in FCM_TRACE builds)
 };
 
 // One compiled kernel instance and the tilings it implements.
@@ -342,12 +322,13 @@ struct Variant {
   const char* name;
   int tile_h = 0;   // compile-time tile (0 = chosen at run time)
   int tile_w = 0;
-  int gen = 1;      // 2: NHWC, 16-byte channel rows, LDS-DMA staging, fixed chunk of 64 bytes
-                    // 3: as 2, persistent workgroups, run-time tile, max_p = 64 * blocks per wave
+  int gen = 1;      // 1: first generation (any layout and alignment, LDS staging)
+                    // 3: NHWC persistent kernels, 16-byte channel rows, LDS-DMA staging,
+                    //    run-time tile, max_p = 64 * blocks per wave
                     // 4: PW -> PW with the intermediate in registers, one pixel group per
                     //    wave (max_p = 16 * blocks), all output channels, no LDS
-                    // 5: NHWC streaming kernels, one work tile per workgroup, run-time tile
-                    //    of at most max_p pixels, one compiled output-channel block
+                    // 5: NHWC streaming kernels, run-time tile of at most max_p pixels,
+                    //    one compiled output-channel block
   int pitch = 0;    // gen 3: LDS window row pitch in pixels (window width must not exceed it)
   int ks = 1;       // gen 3: 64-byte channel chunks per item; gen 4: 64-byte k-steps of the
                     // first convolution held in registers (input channels <= 64 * ks bytes);
@@ -365,9 +346,6 @@ const Variant* variants_v5_dwpw_bf16_s1(int* count);
 const Variant* variants_v5_dwpw_bf16_s2(int* count);
 const Variant* variants_v5_pwdw_bf16(int* count);
 const Variant* variants_pwdwpw(int* count);
-const Variant* variants_v2_bf16(int* count);
-const Variant* variants_v2_f32(int* count);
-const Variant* variants_v2_i8(int* count);
 const Variant* variants_v3_dwpw_bf16_s1(int* count);
 const Variant* variants_v3_dwpw_bf16_s2(int* count);
 const Variant* variants_v3_dwpw_f32(int* count);

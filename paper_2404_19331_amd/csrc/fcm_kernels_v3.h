@@ -35,26 +35,10 @@
 // values in dot-operand form + bias [CB].
 #pragma once
 
-#include "fcm_kernels_v2.h"
+#include "fcm_kernels.h"
 
 namespace fcm {
 
-#ifdef FCM_TRACE
-// Development builds only: the first lane of copy wave 0 (slots 0..31) and of the first
-// compute wave (slots 32..63) record the shader clock at fixed points ([workgroup][64]).
-#define FCM_TS_AT(tid, slot)                                                              \
-  do {                                                                                    \
-    const int ts_slot_ = (slot);                                                          \
-    if (a.trace && threadIdx.x == (tid) && ts_slot_ < 64)                                 \
-      a.trace[blockIdx.x * 64 + ts_slot_] = __builtin_amdgcn_s_memtime();                 \
-  } while (0)
-#else
-#define FCM_TS_AT(tid, slot) \
-  do {                       \
-  } while (0)
-#endif
-#define FCM_TS(slot) FCM_TS_AT(0, slot)
-#define FCM_TSC(slot) FCM_TS_AT(64 * kCopyWaves3, slot)
 
 constexpr int kNiwMax = 10;  // window copy instructions per wave (<= 640 window pixels)
 
@@ -283,8 +267,6 @@ __global__ __launch_bounds__(kThreads3) void k_fused3(KArgs a) {
   auto bufp = [&](int slot) { return smem + slot * lay.buf_bytes; };
   auto next_slot = [&](int slot) { return slot + 1 == D ? 0 : slot + 1; };
 
-  [[maybe_unused]] int tsi = 0;  // timeline slot (development builds)
-  FCM_TS(tsi++);
 
   if (producer) {
     // ===== copy waves: all copies, D - 1 items ahead of the compute waves. Wave 0 issues
@@ -421,21 +403,17 @@ __global__ __launch_bounds__(kThreads3) void k_fused3(KArgs a) {
     convert(0);
     wait_lgkm0();
     barrier3();
-    FCM_TS(tsi++);
     int cv_slot = next_slot(0);
     for (int it = 0; it < nitems; ++it) {
       // slot of item it + D - 1 is the one item it - 1 used: released by the last barrier
       if (it + D - 1 < nitems) issue_next();
-      FCM_TS(tsi++);
       if (it + 1 < nitems) {
         wait_vm((min(nitems, it + D) - (it + 2)) * mine);
         convert(cv_slot);
       }
       cv_slot = next_slot(cv_slot);
       wait_lgkm0();
-      FCM_TS(tsi++);
       barrier3();
-      FCM_TS(tsi++);
     }
     return;
   }
@@ -467,8 +445,6 @@ __global__ __launch_bounds__(kThreads3) void k_fused3(KArgs a) {
   u32x4 bop[BPW];
 
   barrier3();  // item 0 is ready
-  [[maybe_unused]] int tsc = 32;
-  FCM_TSC(tsc++);
   int wt = wt0, ch = u_lo(wt0), ch_hi = u_hi(wt0), slot = 0;
   Tile cur_t = decode(wt0 / SPL);
   for (int it = 0; it < nitems; ++it) {
@@ -646,9 +622,7 @@ __global__ __launch_bounds__(kThreads3) void k_fused3(KArgs a) {
       ++ch;
     }
     wait_lgkm0();
-    FCM_TSC(tsc++);
     barrier3();  // item it+1 is ready; this item's buffer may be refilled
-    FCM_TSC(tsc++);
   }
 }
 

@@ -193,7 +193,7 @@ static int tiling_lds(const Variant& v, const Geom& g, int TH, int TW, int CB, i
   const int P = TH * TW;
   const int Q = ((TH - 1) * g.s + g.k) * ((TW - 1) * g.s + g.k);
   if (v.max_p && P > v.max_p) return 0;
-  if (v.gen != 3 && v.max_q && Q > v.max_q) return 0;
+  if (v.gen < 3 && v.max_q && Q > v.max_q) return 0;
   if (v.gen == 5) {
     // NHWC, 16-byte input channel rows, 32-bit buffer offsets, 64-byte chunk, run-time
     // tile of at most max_p pixels whose window fits the kernel's copy list
@@ -237,18 +237,6 @@ static int tiling_lds(const Variant& v, const Geom& g, int TH, int TW, int CB, i
     if (d == 0) return 0;
     *depth = d;
     return lds3p(g.dtype, KE, mode, IH, v.pitch, COB / 16, d, v.ks).total;
-  }
-  if (v.gen == 2) {
-    // NHWC, 16-byte channel rows, 32-bit buffer offsets, fixed tile and 64-byte chunk
-    if (g.layout != FCM_NHWC || TH != v.tile_h || TW != v.tile_w) return 0;
-    const int last = g.family == FAM_DW ? g.cm : g.co;
-    if ((g.ci * g.elt) % 16 || (last * g.elt) % 16) return 0;
-    if ((int64_t)g.h * g.w * g.ci * g.elt >= ((int64_t)1 << 31)) return 0;
-    if ((int64_t)g.co * g.ci * g.elt >= ((int64_t)1 << 31)) return 0;
-    const int cb = 64 / g.elt;
-    if (CB != cb) return 0;
-    if (v.family == FAM_DW) return COB == cb ? lds_dw2(g.dtype, g.k, g.s, TH, TW) : 0;
-    return lds_dwpw2(g.dtype, g.k, g.s, v.family == FAM_DWPW, TH, TW, v.max_cob, COB);
   }
   switch (v.family) {
     case FAM_DWPW:
@@ -664,9 +652,7 @@ static fcm_status search(const Geom& g, const fcm_desc* d, const fcm_hw_desc& hw
       continue;
     }
     std::vector<int> cbs;
-    if (v.gen == 2) {
-      cbs = {64 / g.elt};
-    } else if (v.family == FAM_DW) {
+    if (v.family == FAM_DW) {
       cbs = {0};  // CB follows COB
     } else if (v.family == FAM_PWDWPW || v.family == FAM_PWPW) {
       const int step = std::max(16, kb);
@@ -696,7 +682,7 @@ static fcm_status search(const Geom& g, const fcm_desc* d, const fcm_hw_desc& hw
         const int cob_hi = v.gen == 3 ? v.max_cob : std::min(v.max_cob, round_up(last, 16));
         for (int COB = cob_lo; COB <= cob_hi; COB += 16) {
           for (int cb0 : cbs) {
-            const int CB = (v.family == FAM_DW && v.gen != 2) ? COB : cb0;
+            const int CB = v.family == FAM_DW ? COB : cb0;
             // persistent kernels: one or two items in flight (deeper rings measured no faster)
             const int depths[2] = {2, 3};
             // persistent kernels with a PW stage: also split each work tile's channel chunks

@@ -27,10 +27,11 @@
  * ---------------------------------------
  *  * Tensors are caller-owned DEVICE pointers (e.g. PyTorch tensors). Every launch is
  *    asynchronous on `stream` (a hipStream_t; NULL = the null stream); the library never
- *    frees or synchronises. It allocates only its split workspace: the first call with a
- *    plan whose `splits` > 1 on a device allocates FCM_SPLIT_WORKSPACE_BYTES there, once.
- *    Calls with such plans share that workspace, so on one device they must not run
- *    concurrently (e.g. on two streams).
+ *    allocates, frees or synchronises. Plans that split a work tile's channel chunks over
+ *    several workgroups keep partial sums in a caller-provided device workspace
+ *    (fcm_workspace_bytes, fcm_dw_pw_ws, fcm_pw_ws); the entry points without a workspace
+ *    argument plan without splits and refuse a split plan with FCM_EINVAL. Calls that
+ *    share one workspace must not overlap (e.g. on two streams).
  *  * Activations: x is [n, c, h, w] (FCM_NCHW) or [n, h, w, c] (FCM_NHWC), dense,
  *    row-major. The output uses the same layout.
  *  * Weights are canonical regardless of layout: depthwise [c][k][k] (PyTorch
@@ -59,9 +60,8 @@
 extern "C" {
 #endif
 
-/* Device memory the library allocates once per device for split plans of the persistent
- * DW->PW and PW kernels (their partial sums); plans whose partial sums would exceed it
- * are not split. */
+/* The largest workspace a split plan of the persistent DW->PW and PW kernels may need
+ * (its partial sums); the planner does not split where they would exceed it. */
 #define FCM_SPLIT_WORKSPACE_BYTES (64u << 20)
 
 typedef enum {
@@ -171,7 +171,7 @@ typedef struct {
                             (2..8; 0 on input to fcm_plan_evaluate = the planner's choice) */
   int32_t splits;        /* persistent DW->PW and PW kernels: the channel chunks of each
                             work tile are split over this many workgroups; each writes its
-                            partial sums to the library's workspace and a second kernel
+                            partial sums to the caller's workspace and a second kernel
                             adds them in split order, then applies bias, activation and
                             cast. PW->PW register kernel: 1, 2 or 4 waves of a workgroup
                             share a pixel group's intermediate chunks and add their partial
@@ -196,6 +196,12 @@ typedef struct {
  * Returns FCM_EINVAL / FCM_EUNSUPPORTED like the launch entry points. */
 fcm_status fcm_plan(int32_t op, const fcm_desc* desc, const fcm_hw_desc* hw, fcm_plan_t* out);
 
+/* As fcm_plan, among the plans whose caller workspace (fcm_workspace_bytes) is at most
+ * max_workspace_bytes: 0 gives the best plan that needs none, which is what the entry
+ * points without a workspace argument launch when their plan is NULL. */
+fcm_status fcm_plan_limited(int32_t op, const fcm_desc* desc, const fcm_hw_desc* hw,
+                            int64_t max_workspace_bytes, fcm_plan_t* out);
+
 /* Evaluate a caller-chosen tiling (plan->op, tile_h, tile_w, c_block, co_block,
  * variant) without searching: fills every other field, or fails with
  * FCM_EUNSUPPORTED if no compiled kernel implements it. */
@@ -208,10 +214,27 @@ double fcm_plan_time_estimate(const fcm_desc* desc, const fcm_hw_desc* hw, const
 /* DW -> PW module: y = act1(PW(act0(DW(x) + b_dw)) + b_pw).
  *   x [n, c_in, h, w] | w_dw [c_in][k][k] | b_dw [c_in] | w_pw [c_out][c_in] |
  *   b_pw [c_out] | y [n, c_out, h_o, w_o] (layout order as desc->layout).
- * plan may be NULL (fcm_plan is called and cached). */
+ * plan may be NULL (the planner's best plan without a workspace, cached); a plan that
+ * needs a workspace (splits > 1) fails with FCM_EINVAL: use fcm_dw_pw_ws. */
 fcm_status fcm_dw_pw(const fcm_desc* desc, const void* x, const void* w_dw, const void* b_dw,
                      const void* w_pw, const void* b_pw, void* y, const fcm_plan_t* plan,
                      void* stream);
+
+/* DW -> PW module with a caller workspace (Sec. III-A "DWPW"), for plans that split a
+ * work tile's channel chunks over several workgroups (fcm_plan_t.splits > 1): their fp32 /
+ * int32 partial sums go to `workspace` (DEVICE, 16-byte aligned, caller-owned,
+ * workspace_bytes long) and a second kernel adds them in split order before bias,
+ * activation and cast, so results equal the unsplit plan's up to the float summation
+ * order (int8: bit-exact). plan NULL: the planner's best plan whose workspace fits
+ * workspace_bytes (NULL workspace = 0 bytes). An explicit plan needing more than
+ * workspace_bytes (fcm_workspace_bytes) fails with FCM_EINVAL. Otherwise as fcm_dw_pw. */
+fcm_status fcm_dw_pw_ws(const fcm_desc* desc, const void* x, const void* w_dw, const void* b_dw,
+                        const void* w_pw, const void* b_pw, void* y, const fcm_plan_t* plan,
+                        void* workspace, int64_t workspace_bytes, void* stream);
+
+/* Device workspace bytes `plan` needs (its partial sums when it splits channel chunks over
+ * workgroups; 0 for every other plan), or -1 for an invalid descriptor or plan. */
+int64_t fcm_workspace_bytes(const fcm_desc* desc, const fcm_plan_t* plan);
 
 /* PW -> DW module: y = act1(DW(pad0(act0(PW(x) + b_pw))) + b_dw); the DW input is zero
  * outside the image (never act0(b_pw)).
@@ -243,6 +266,11 @@ fcm_status fcm_dw(const fcm_desc* desc, const void* x, const void* w_dw, const v
 /* Single pointwise layer (layer-by-layer baseline): y [n, c_out, h, w]. */
 fcm_status fcm_pw(const fcm_desc* desc, const void* x, const void* w_pw, const void* b_pw,
                   void* y, const fcm_plan_t* plan, void* stream);
+
+/* Single pointwise layer with a caller workspace for split plans (as fcm_dw_pw_ws). */
+fcm_status fcm_pw_ws(const fcm_desc* desc, const void* x, const void* w_pw, const void* b_pw,
+                     void* y, const fcm_plan_t* plan, void* workspace, int64_t workspace_bytes,
+                     void* stream);
 
 /* ------------------------------------------------------------------------------------
  * Chains of layers: FusePlanner over a network (Sec. IV: FCMs and layer-by-layer kernels
@@ -312,8 +340,8 @@ int64_t fcm_chain_workspace_bytes(const fcm_chain_plan_t* plan);
  * (shapes from the chain and each layer's geometry, layout chain->layout); weights[i],
  * biases[i] belong to layer i (canonical layouts as the single-layer entry points;
  * biases[i] may be NULL). `workspace` (device, fcm_chain_workspace_bytes(plan) bytes,
- * caller-owned, may be NULL when that is 0) holds the activations between groups. The
- * library allocates nothing beyond what the groups' own plans need (split workspace).
+ * caller-owned, may be NULL when that is 0) holds the activations between groups. Chain
+ * plans use no split plans, so that is all the device memory a chain needs.
  * Errors are those of the group launches; a failing group stops the chain. */
 fcm_status fcm_chain_run(const fcm_chain_desc* chain, const fcm_chain_plan_t* plan, const void* x,
                          const void* const* weights, const void* const* biases, void* workspace, void* y,

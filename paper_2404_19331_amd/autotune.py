@@ -142,6 +142,6 @@ def _module_plan(sub, op):
                       layout=sub.layout, act=[L["act"] for L in layers], rq=[L["rq"] for L in layers],
                       zp_in=sub.zp_in)
     try:
-        return fcm.plan(op, d)
+        return fcm.plan_limited(op, d, 0)  # chain groups run without a split workspace
     except fcm.FcmError:
         return None

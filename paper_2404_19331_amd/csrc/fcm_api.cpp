@@ -133,24 +133,6 @@ static int device_cus() {
   return cache[dev];
 }
 
-// Split workspace of the current device: FCM_SPLIT_WORKSPACE_BYTES, allocated on first
-// use and kept until the process ends (split plans write every partial sum they read,
-// so it needs no initialisation).
-static void* split_workspace() {
-  static std::mutex mu;
-  static std::vector<void*> cache;
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return nullptr;
-  std::lock_guard<std::mutex> lock(mu);
-  if ((int)cache.size() <= dev) cache.resize(dev + 1, nullptr);
-  if (!cache[dev]) {
-    void* p = nullptr;
-    if (hipMalloc(&p, FCM_SPLIT_WORKSPACE_BYTES) != hipSuccess) return nullptr;
-    cache[dev] = p;
-  }
-  return cache[dev];
-}
-
 static fcm_status check_alignment(const void* p, int elt, const char* what) {
   if (p && ((uintptr_t)p % (uintptr_t)elt) != 0)
     return fail(FCM_EINVAL, std::string(what) + " is not aligned to its element size");
@@ -164,7 +146,13 @@ struct Tensors {
   void* y;
 };
 
-static fcm_status run(int op, const fcm_desc* d, const Tensors& t, const fcm_plan_t* plan_in, void* stream) {
+// ws / ws_bytes: the caller's device workspace (split plans keep their partial sums
+// there); NULL / 0 = none, and then only plans that need none are used or accepted.
+static fcm_status run(int op, const fcm_desc* d, const Tensors& t, const fcm_plan_t* plan_in, void* ws,
+                      int64_t ws_bytes, void* stream) {
+  if (ws_bytes < 0) return fail(FCM_EINVAL, "workspace size must not be negative");
+  if (ws && ((uintptr_t)ws & 15u)) return fail(FCM_EINVAL, "workspace must be 16-byte aligned");
+  if (!ws) ws_bytes = 0;
   fcm_status st = validate(op, d);
   if (st != FCM_OK) return st;
   const int nw = op == FCM_OP_PW_DW_PW ? 3 : ((op == FCM_OP_DW || op == FCM_OP_PW) ? 1 : 2);
@@ -196,8 +184,12 @@ static fcm_status run(int op, const fcm_desc* d, const Tensors& t, const fcm_pla
       return fail(FCM_EUNSUPPORTED, !variant_in_set(p.variant, feat) ? kset_message(feat)
                                                                        : "plan's kernel needs 16-byte aligned tensors");
   } else {
-    if ((st = find_plan(op, d, &hw, &p, kset)) != FCM_OK) return st;
+    if ((st = find_plan(op, d, &hw, &p, kset, ws_bytes)) != FCM_OK) return st;
   }
+  const int64_t need = plan_workspace_bytes(g, p);
+  if (need > ws_bytes)
+    return fail(FCM_EINVAL, "the plan splits its channel chunks and needs " + std::to_string(need) +
+                                " bytes of caller workspace (fcm_workspace_bytes; pass it to the _ws entry point)");
   int nv = 0;
   const Variant* vs = all_variants(&nv);
   const Variant& v = vs[p.variant];
@@ -262,8 +254,7 @@ static fcm_status run(int op, const fcm_desc* d, const Tensors& t, const fcm_pla
   a.nwork = a.N * a.tiles_y * a.tiles_x * a.n_cb;
   a.splits = 1;
   if (v.gen == 3 && p.splits > 1) {
-    a.ws = split_workspace();
-    if (!a.ws) return fail(FCM_EDEVICE, "could not allocate the split workspace");
+    a.ws = ws;
     a.splits = p.splits;
     a.nwork *= p.splits;  // work units
   }
@@ -310,6 +301,15 @@ fcm_status fcm_plan(int32_t op, const fcm_desc* desc, const fcm_hw_desc* hw, fcm
   fcm_status st = validate(op, desc);
   if (st != FCM_OK) return st;
   return find_plan(op, desc, hw, out, kernel_set(op, desc));
+}
+
+fcm_status fcm_plan_limited(int32_t op, const fcm_desc* desc, const fcm_hw_desc* hw, int64_t max_workspace_bytes,
+                            fcm_plan_t* out) {
+  if (!out) return fail(FCM_EINVAL, "output plan is NULL");
+  if (max_workspace_bytes < 0) return fail(FCM_EINVAL, "workspace limit must not be negative");
+  fcm_status st = validate(op, desc);
+  if (st != FCM_OK) return st;
+  return find_plan(op, desc, hw, out, kernel_set(op, desc), max_workspace_bytes);
 }
 
 fcm_status fcm_plan_evaluate(const fcm_desc* desc, const fcm_hw_desc* hw, fcm_plan_t* plan) {
@@ -363,32 +363,39 @@ fcm_status fcm_fold_batchnorm(int32_t c_out, int32_t row, const float* w, const 
 fcm_status fcm_dw_pw(const fcm_desc* desc, const void* x, const void* w_dw, const void* b_dw, const void* w_pw,
                      const void* b_pw, void* y, const fcm_plan_t* plan, void* stream) {
   Tensors t = {x, {w_dw, w_pw, nullptr}, {b_dw, b_pw, nullptr}, y};
-  return run(FCM_OP_DW_PW, desc, t, plan, stream);
+  return run(FCM_OP_DW_PW, desc, t, plan, nullptr, 0, stream);
+}
+
+fcm_status fcm_dw_pw_ws(const fcm_desc* desc, const void* x, const void* w_dw, const void* b_dw, const void* w_pw,
+                        const void* b_pw, void* y, const fcm_plan_t* plan, void* workspace, int64_t workspace_bytes,
+                        void* stream) {
+  Tensors t = {x, {w_dw, w_pw, nullptr}, {b_dw, b_pw, nullptr}, y};
+  return run(FCM_OP_DW_PW, desc, t, plan, workspace, workspace_bytes, stream);
 }
 
 fcm_status fcm_pw_dw(const fcm_desc* desc, const void* x, const void* w_pw, const void* b_pw, const void* w_dw,
                      const void* b_dw, void* y, const fcm_plan_t* plan, void* stream) {
   Tensors t = {x, {w_pw, w_dw, nullptr}, {b_pw, b_dw, nullptr}, y};
-  return run(FCM_OP_PW_DW, desc, t, plan, stream);
+  return run(FCM_OP_PW_DW, desc, t, plan, nullptr, 0, stream);
 }
 
 fcm_status fcm_pw_dw_pw(const fcm_desc* desc, const void* x, const void* w_pw1, const void* b_pw1, const void* w_dw,
                         const void* b_dw, const void* w_pw2, const void* b_pw2, void* y, const fcm_plan_t* plan,
                         void* stream) {
   Tensors t = {x, {w_pw1, w_dw, w_pw2}, {b_pw1, b_dw, b_pw2}, y};
-  return run(FCM_OP_PW_DW_PW, desc, t, plan, stream);
+  return run(FCM_OP_PW_DW_PW, desc, t, plan, nullptr, 0, stream);
 }
 
 fcm_status fcm_dw(const fcm_desc* desc, const void* x, const void* w_dw, const void* b_dw, void* y,
                   const fcm_plan_t* plan, void* stream) {
   Tensors t = {x, {w_dw, nullptr, nullptr}, {b_dw, nullptr, nullptr}, y};
-  return run(FCM_OP_DW, desc, t, plan, stream);
+  return run(FCM_OP_DW, desc, t, plan, nullptr, 0, stream);
 }
 
 fcm_status fcm_pw_pw(const fcm_desc* desc, const void* x, const void* w_pw1, const void* b_pw1, const void* w_pw2,
                      const void* b_pw2, void* y, const fcm_plan_t* plan, void* stream) {
   Tensors t = {x, {w_pw1, w_pw2, nullptr}, {b_pw1, b_pw2, nullptr}, y};
-  return run(FCM_OP_PW_PW, desc, t, plan, stream);
+  return run(FCM_OP_PW_PW, desc, t, plan, nullptr, 0, stream);
 }
 
 fcm_status fcm_chain_run(const fcm_chain_desc* chain, const fcm_chain_plan_t* plan, const void* x,
@@ -425,7 +432,7 @@ fcm_status fcm_chain_run(const fcm_chain_desc* chain, const fcm_chain_plan_t* pl
       t.w[i] = weights[first + i];
       t.b[i] = biases ? biases[first + i] : nullptr;
     }
-    if ((st = run(op, &d, t, &plan->plan[g], stream)) != FCM_OK) return st;
+    if ((st = run(op, &d, t, &plan->plan[g], nullptr, 0, stream)) != FCM_OK) return st;
     in = out;
   }
   return FCM_OK;
@@ -434,7 +441,25 @@ fcm_status fcm_chain_run(const fcm_chain_desc* chain, const fcm_chain_plan_t* pl
 fcm_status fcm_pw(const fcm_desc* desc, const void* x, const void* w_pw, const void* b_pw, void* y,
                   const fcm_plan_t* plan, void* stream) {
   Tensors t = {x, {w_pw, nullptr, nullptr}, {b_pw, nullptr, nullptr}, y};
-  return run(FCM_OP_PW, desc, t, plan, stream);
+  return run(FCM_OP_PW, desc, t, plan, nullptr, 0, stream);
+}
+
+fcm_status fcm_pw_ws(const fcm_desc* desc, const void* x, const void* w_pw, const void* b_pw, void* y,
+                     const fcm_plan_t* plan, void* workspace, int64_t workspace_bytes, void* stream) {
+  Tensors t = {x, {w_pw, nullptr, nullptr}, {b_pw, nullptr, nullptr}, y};
+  return run(FCM_OP_PW, desc, t, plan, workspace, workspace_bytes, stream);
+}
+
+int64_t fcm_workspace_bytes(const fcm_desc* desc, const fcm_plan_t* plan) {
+  if (!plan) {
+    fail(FCM_EINVAL, "plan is NULL");
+    return -1;
+  }
+  if (validate(plan->op, desc) != FCM_OK) return -1;
+  const Geom g = geometry(plan->op, desc);
+  fcm_plan_t p = *plan;
+  if (evaluate_plan(g, desc, default_hw(), &p) != FCM_OK) return -1;
+  return plan_workspace_bytes(g, p);
 }
 
 const char* fcm_status_string(fcm_status status) {

@@ -153,7 +153,8 @@ fcm_status fcm_chain_plan(const fcm_chain_desc* chain, int32_t objective, const 
       }
       Opt o;
       o.op = op;
-      st = find_plan(op, &d, &H, &o.plan, kernel_set(op, &d));
+      // groups run with the chain's activation buffers only: plans without split workspace
+      st = find_plan(op, &d, &H, &o.plan, kernel_set(op, &d), 0);
       if (st != FCM_OK) {
         if (single) return st;
         continue;

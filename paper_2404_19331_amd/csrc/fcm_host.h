@@ -1,6 +1,8 @@
 // fcm_host.h -- host-side internals shared by the planner and the C ABI.
 #pragma once
 
+#include <stdint.h>
+
 #include <string>
 
 #include "fcm.h"
@@ -43,7 +45,14 @@ fcm_status evaluate_plan(const Geom& g, const fcm_desc* d, const fcm_hw_desc& hw
 
 // Search (cached) over the variants of kernel set kset. plan_out is fully filled on
 // success.
-fcm_status find_plan(int op, const fcm_desc* d, const fcm_hw_desc* hw, fcm_plan_t* plan_out, int kset = KSET_ALL);
+// ws_max: the largest caller workspace a plan may need (split plans of the persistent
+// kernels keep their partial sums there); plans needing more are not considered.
+fcm_status find_plan(int op, const fcm_desc* d, const fcm_hw_desc* hw, fcm_plan_t* plan_out, int kset = KSET_ALL,
+                     int64_t ws_max = INT64_MAX);
+
+// Device workspace bytes a (fully evaluated) plan needs: the partial sums of a split plan,
+// 0 for every other plan.
+int64_t plan_workspace_bytes(const Geom& g, const fcm_plan_t& p);
 
 // Whether a compiled variant stages through LDS-DMA (needs 16-byte aligned tensors).
 bool variant_needs_alignment(int variant);

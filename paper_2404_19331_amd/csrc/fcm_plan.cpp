@@ -181,6 +181,16 @@ static int64_t split_workspace_bytes(int64_t tiles, int pixels, int cob, int spl
   return (int64_t)splits * tiles * pixels * cob * 4;
 }
 
+int64_t plan_workspace_bytes(const Geom& g, const fcm_plan_t& p) {
+  int nv = 0;
+  const Variant* vs = all_variants(&nv);
+  if (p.variant < 0 || p.variant >= nv || vs[p.variant].gen != 3 || p.splits <= 1) return 0;
+  const int last = (g.family == FAM_PWDW || g.family == FAM_DW) ? g.cm : g.co;
+  const int64_t tiles =
+      (int64_t)g.n * ceil_div(g.ho, p.tile_h) * ceil_div(g.wo, p.tile_w) * ceil_div(last, p.co_block);
+  return split_workspace_bytes(tiles, p.tile_h * p.tile_w, p.co_block, p.splits);
+}
+
 // LDS bytes of a tiling (0 if the variant cannot implement it). For the persistent
 // kernels *depth is the requested ring depth on input (0 = choose) and the chosen one on
 // output.
@@ -618,7 +628,7 @@ static const int kTiles3[][2] = {{16, 14}, {8, 14}, {7, 14}, {4, 14}, {14, 14}, 
                                  {2, 4},   {4, 4},  {2, 2},  {3, 7},  {6, 7},  {12, 7}};
 
 static fcm_status search(const Geom& g, const fcm_desc* d, const fcm_hw_desc& hw, fcm_plan_t* best_out,
-                         int kset) {
+                         int kset, int64_t ws_max) {
   int nv = 0;
   const Variant* vs = all_variants(&nv);
   const int kb = k_block(g.dtype);
@@ -704,6 +714,7 @@ static fcm_status search(const Geom& g, const fcm_desc* d, const fcm_hw_desc& hw
               c.p.depth = depth;
               c.p.splits = splitss[si];
               if (evaluate_plan(g, d, hw, &c.p) != FCM_OK) continue;
+              if (plan_workspace_bytes(g, c.p) > ws_max) continue;
               c.bytes = c.p.bytes_tiled;
               c.wgs = c.p.workgroups;
               c.lds = lds;
@@ -837,13 +848,15 @@ static std::vector<int64_t> cache_key(int op, const fcm_desc* d, const fcm_hw_de
   return k;
 }
 
-fcm_status find_plan(int op, const fcm_desc* d, const fcm_hw_desc* hw_in, fcm_plan_t* out, int kset) {
+fcm_status find_plan(int op, const fcm_desc* d, const fcm_hw_desc* hw_in, fcm_plan_t* out, int kset,
+                     int64_t ws_max) {
   const fcm_hw_desc hw = hw_in ? *hw_in : default_hw();
   if (hw.num_cus <= 0 || hw.lds_per_wg <= 0 || hw.lds_per_cu <= 0)
     return fail(FCM_EINVAL, "plan: hardware description has non-positive sizes");
   std::vector<int64_t> key = cache_key(op, d, hw);
   key.push_back(kset);
   key.push_back(d->layout);
+  key.push_back(std::min<int64_t>(ws_max, FCM_SPLIT_WORKSPACE_BYTES));
   {
     std::lock_guard<std::mutex> lock(g_cache_mu);
     auto it = g_cache.find(key);
@@ -854,7 +867,7 @@ fcm_status find_plan(int op, const fcm_desc* d, const fcm_hw_desc* hw_in, fcm_pl
   }
   const Geom g = geometry(op, d);
   fcm_plan_t p;
-  fcm_status st = search(g, d, hw, &p, kset);
+  fcm_status st = search(g, d, hw, &p, kset, ws_max);
   if (st != FCM_OK) return st;
   // layer-by-layer chain: each stage planned on its own (first pass of Sec. IV)
   std::vector<std::pair<int, fcm_desc>> stages;

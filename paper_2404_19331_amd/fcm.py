@@ -129,6 +129,14 @@ def lib():
         L.fcm_pw_pw.argtypes = [dp, vp, vp, vp, vp, vp, vp, pp, vp]
         L.fcm_dw.argtypes = [dp, vp, vp, vp, vp, pp, vp]
         L.fcm_pw.argtypes = [dp, vp, vp, vp, vp, pp, vp]
+        i64 = ctypes.c_int64
+        L.fcm_dw_pw_ws.argtypes = [dp, vp, vp, vp, vp, vp, vp, pp, vp, i64, vp]
+        L.fcm_pw_ws.argtypes = [dp, vp, vp, vp, vp, pp, vp, i64, vp]
+        L.fcm_dw_pw_ws.restype = L.fcm_pw_ws.restype = ctypes.c_int
+        L.fcm_workspace_bytes.argtypes = [dp, pp]
+        L.fcm_plan_limited.argtypes = [ctypes.c_int32, dp, hp, i64, pp]
+        L.fcm_plan_limited.restype = ctypes.c_int
+        L.fcm_workspace_bytes.restype = i64
         for f in (L.fcm_plan, L.fcm_plan_evaluate, L.fcm_dw_pw, L.fcm_pw_dw, L.fcm_pw_dw_pw,
                   L.fcm_pw_pw, L.fcm_dw, L.fcm_pw):
             f.restype = ctypes.c_int
@@ -210,6 +218,18 @@ def plan(op, desc, hw=None):
     """FusePlanner: the tiling fcm_plan chooses, as a dict."""
     p = Plan()
     _check(lib().fcm_plan(OP[op], ctypes.byref(desc), ctypes.byref(hw) if hw else None, ctypes.byref(p)))
+    return p
+
+
+_find_plan = plan  # (the entry points' `plan` argument shadows the function)
+
+
+def plan_limited(op, desc, max_workspace_bytes, hw=None):
+    """The planner's best plan among those needing at most `max_workspace_bytes` of
+    caller workspace (0: none)."""
+    p = Plan()
+    _check(lib().fcm_plan_limited(OP[op], ctypes.byref(desc), ctypes.byref(hw) if hw else None,
+                                  int(max_workspace_bytes), ctypes.byref(p)))
     return p
 
 
@@ -300,10 +320,11 @@ def _stream(x, stream):
 
 class Prepared:
     """A C-ABI launch whose arguments were marshalled once; calling it launches again
-    (same tensors, same plan, same stream). Used for repeated timed launches."""
+    (same tensors, same plan, same stream). Used for repeated timed launches. `keep`
+    holds tensors the launch uses that the caller did not pass (a split plan's workspace)."""
 
-    def __init__(self, fn, args, y):
-        self.fn, self.args, self.y = fn, args, y
+    def __init__(self, fn, args, y, keep=None):
+        self.fn, self.args, self.y, self.keep = fn, args, y, keep
 
     def __call__(self):
         st = self.fn(*self.args)
@@ -312,11 +333,35 @@ class Prepared:
         return self.y
 
 
-def _call(fn, args, y, prepare):
+def _call(fn, args, y, prepare, keep=None):
     if prepare:
-        return Prepared(fn, args, y)
+        return Prepared(fn, args, y, keep)
     _check(fn(*args))
     return y
+
+
+def workspace_bytes(desc, plan):
+    """Device bytes of workspace `plan` needs (0 unless it splits channel chunks)."""
+    n = lib().fcm_workspace_bytes(ctypes.byref(desc), ctypes.byref(plan))
+    if n < 0:
+        raise FcmError(1, last_error())
+    return int(n)
+
+
+def _with_workspace(op, d, x, plan, workspace):
+    """The plan to launch (the planner's best when None) and the workspace it needs: the
+    caller's tensor, or a fresh one from torch's allocator (the library allocates nothing)."""
+    if plan is None:
+        plan = _find_plan(op, d)
+    need = workspace_bytes(d, plan)
+    if need == 0:
+        return plan, None
+    torch = _torch()
+    if workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=x.device)
+    elif workspace.numel() * workspace.element_size() < need or not workspace.is_contiguous():
+        raise ValueError("workspace must be a contiguous device tensor of at least %d bytes" % need)
+    return plan, workspace
 
 
 def _plan_arg(plan):
@@ -332,8 +377,10 @@ def _kk(w_dw):
 
 
 def dw_pw(x, w_dw, w_pw, b_dw=None, b_pw=None, *, stride=1, pad=None, act=("none", "none"), rq=None, rq_channel=None,
-          layout="nchw", plan=None, out=None, stream=None, prepare=False, zp_in=0):
-    """DW -> PW module in one kernel. Returns y [n, c_out, h_o, w_o] in `layout`."""
+          layout="nchw", plan=None, out=None, stream=None, prepare=False, zp_in=0, workspace=None):
+    """DW -> PW module in one kernel. Returns y [n, c_out, h_o, w_o] in `layout`.
+    A plan that splits channel chunks (the planner's choice when `plan` is None) runs with
+    `workspace`, or with a device tensor allocated here through torch."""
     dt = _dtype_name(x)
     n, c, h, w = _dims(x, layout)
     k = _kk(w_dw)
@@ -343,8 +390,13 @@ def dw_pw(x, w_dw, w_pw, b_dw=None, b_pw=None, *, stride=1, pad=None, act=("none
     d = make_desc(n, h, w, c, c, co, k, stride, pad, dt, layout, act, rq, rq_channel=rq_channel, zp_in=zp_in)
     ho, wo = out_hw(h, w, k, stride, pad)
     y = _out(x, layout, n, co, ho, wo, out)
-    return _call(lib().fcm_dw_pw, (ctypes.byref(d), _ptr(x), _ptr(w_dw), _ptr(b_dw), _ptr(w_pw), _ptr(b_pw),
-                                   _ptr(y), _plan_arg(plan), _stream(x, stream)), y, prepare)
+    plan, ws = _with_workspace("dw_pw", d, x, plan, workspace)
+    if ws is None:
+        return _call(lib().fcm_dw_pw, (ctypes.byref(d), _ptr(x), _ptr(w_dw), _ptr(b_dw), _ptr(w_pw), _ptr(b_pw),
+                                       _ptr(y), _plan_arg(plan), _stream(x, stream)), y, prepare)
+    return _call(lib().fcm_dw_pw_ws, (ctypes.byref(d), _ptr(x), _ptr(w_dw), _ptr(b_dw), _ptr(w_pw), _ptr(b_pw),
+                                      _ptr(y), _plan_arg(plan), _ptr(ws), ws.numel() * ws.element_size(),
+                                      _stream(x, stream)), y, prepare, keep=ws)
 
 
 def pw_dw(x, w_pw, w_dw, b_pw=None, b_dw=None, *, stride=1, pad=None, act=("none", "none"), rq=None, rq_channel=None,
@@ -410,16 +462,20 @@ def dw(x, w_dw, b_dw=None, *, stride=1, pad=None, act="none", rq=None, rq_channe
 
 
 def pw(x, w_pw, b_pw=None, *, act="none", rq=None, rq_channel=None, layout="nchw", plan=None, out=None, stream=None,
-       prepare=False, zp_in=0):
-    """Single pointwise layer (layer-by-layer kernel)."""
+       prepare=False, zp_in=0, workspace=None):
+    """Single pointwise layer (layer-by-layer kernel); split plans as in dw_pw."""
     dt = _dtype_name(x)
     n, c, h, w = _dims(x, layout)
     co = int(w_pw.shape[0])
     _prep(x, [w_pw], [b_pw], dt)
     d = make_desc(n, h, w, c, c, co, 1, 1, 0, dt, layout, (act,), [rq] if rq else None, rq_channel=rq_channel, zp_in=zp_in)
     y = _out(x, layout, n, co, h, w, out)
-    return _call(lib().fcm_pw, (ctypes.byref(d), _ptr(x), _ptr(w_pw), _ptr(b_pw), _ptr(y), _plan_arg(plan),
-                                _stream(x, stream)), y, prepare)
+    plan, ws = _with_workspace("pw", d, x, plan, workspace)
+    if ws is None:
+        return _call(lib().fcm_pw, (ctypes.byref(d), _ptr(x), _ptr(w_pw), _ptr(b_pw), _ptr(y), _plan_arg(plan),
+                                    _stream(x, stream)), y, prepare)
+    return _call(lib().fcm_pw_ws, (ctypes.byref(d), _ptr(x), _ptr(w_pw), _ptr(b_pw), _ptr(y), _plan_arg(plan),
+                                   _ptr(ws), ws.numel() * ws.element_size(), _stream(x, stream)), y, prepare, keep=ws)
 
 
 # ------------------------------------------------------------------------------------

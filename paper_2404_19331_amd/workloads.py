@@ -215,6 +215,27 @@ def config_c4():
     ]
 
 
+def config_c4_spread():
+    """The C4 shapes (EfficientNet-B0-style int8 DW5x5+PW, NHWC, batch 8) with
+    requantisation shifts sized to each stage's accumulator spread, as config_pwpw does:
+    with the named configuration's 2^-8 most results saturate at +-127, which would leave
+    the bit-exact comparison mostly comparing the clamp. U{-127..127} operands have
+    standard deviation 127/sqrt(3) = s; a K*K depthwise sum has s^2 * K, a C-wide
+    pointwise sum over inputs of spread d has d * s * sqrt(C); each shift is the smallest
+    that brings its stage to a spread of at most 48."""
+    sd = 127 / math.sqrt(3)
+    out = []
+    for j, (n, hw, c, co, k, st) in enumerate([(8, 112, 96, 24, 5, 2), (8, 14, 480, 112, 5, 1)]):
+        s1 = int(math.ceil(math.log2(sd * sd * k / 48)))
+        d1 = sd * sd * k / 2 ** s1  # spread of the depthwise output
+        s2 = int(math.ceil(math.log2(d1 * sd * math.sqrt(c) / 48)))
+        rq = ((1, s1, -127, 127), (1, s2, -127, 127), RQ_C4)
+        out.append(Case("dw_pw", n, hw, hw, c, c, co, k, st, k // 2, "i8", "nhwc", ("none",) * 3, rq,
+                        dist_x="i8", dist_w="i8", seed=BASE_SEED + 4 + 1000 + 100 * j,
+                        name="C4%s-spread dwpw%dx%ds%d %dx%dx%d->%d i8 b%d" % ("ab"[j], k, k, st, hw, hw, c, co, n)))
+    return out
+
+
 def config_c5():
     """Convolutional-ViT token-grid DW3x3+PW projections, bf16 NHWC, batch 64, linear."""
     return [Case("dw_pw", 64, hw, hw, c, c, co, 3, 1, 1, "bf16", "nhwc", ("none",) * 3,

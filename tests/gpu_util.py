@@ -7,8 +7,9 @@ from paper_2404_19331_amd import fcm
 
 # Tolerances (written once, used by every parity test):
 #   f32:  |g - r| <= 1e-4 + 1e-5 |r|                       (elementwise)
-#   bf16: |g - r| <= 2e-2 (|r| + rms(r))                   (relative, floor at the RMS of
-#         the reference so that outputs near zero are not held to a pure relative bound)
+#   bf16: |g - r| <= 2e-2 max(|r|, rms(r))                 (2e-2 relative, with a floor at
+#         2e-2 of the reference's RMS so that outputs near zero are not held to a pure
+#         relative bound that rounding of the bf16 intermediate cannot meet)
 #   i8:   bit-exact
 F32_ATOL, F32_RTOL = 1e-4, 1e-5
 BF16_RTOL = 2e-2
@@ -60,9 +61,11 @@ def assert_close(got, ref, dtype, what=""):
         tol = F32_ATOL + F32_RTOL * np.abs(r)
     else:
         rms = np.sqrt(np.mean(r * r)) if r.size else 0.0
-        tol = BF16_RTOL * (np.abs(r) + rms)
+        tol = BF16_RTOL * np.maximum(np.abs(r), rms)
     err = np.abs(g - r)
     bad = err > tol
+    if err.size:
+        print("%s: max |err| / tolerance = %.3f" % (what, float(np.max(err / np.maximum(tol, 1e-300)))))
     if np.any(bad):
         i = tuple(np.argwhere(bad)[0])
         raise AssertionError("%s: %d/%d outside tolerance; first at %s got %r ref %r (max err %.3g)" % (

@@ -377,3 +377,55 @@ def test_zero_point_time_models_are_their_own():
         f_sym, f_zp = _zp_desc(op, dtype="bf16"), _zp_desc(op, -128, (5, 5, 5), dtype="bf16")
         q = fcm.plan(op, f_sym)
         assert fcm.plan_time_estimate(f_sym, q) == fcm.plan_time_estimate(f_zp, q)
+
+
+def test_split_plans_need_a_caller_workspace():
+    """The library allocates nothing: a plan that splits channel chunks names the workspace
+    it needs, the entry points without one refuse it, and a short workspace is refused;
+    all before anything reaches the device (the pointers below are never dereferenced)."""
+    d = fcm.make_desc(1, 14, 14, 512, 512, 512, k=3, stride=1, pad=1, dtype="bf16", layout="nhwc")
+    p = _evaluate("dw_pw", d, 2, 7, "k_dwpw3<bf16,3,1,4,4,p16>", splits=4)
+    need = fcm.workspace_bytes(d, p)
+    tiles = 7 * 2 * (512 // 64)  # spatial tiles x output-channel blocks of 64
+    assert need == 4 * tiles * 14 * 64 * 4  # [split][tile][pixel][channel] fp32 partial sums
+    assert fcm.workspace_bytes(d, _evaluate("dw_pw", d, 2, 7, "k_dwpw3<bf16,3,1,4,4,p16>")) == 0
+    L = fcm.lib()
+    dev = ctypes.c_void_p(1 << 20)  # aligned stand-in: validation fails before any launch
+    args = (ctypes.byref(d), dev, dev, None, dev, None, dev, ctypes.byref(p))
+    assert L.fcm_dw_pw(*args, None) == EINVAL
+    assert "workspace" in fcm.last_error()
+    assert L.fcm_dw_pw_ws(*args, dev, need - 16, None) == EINVAL
+    assert L.fcm_dw_pw_ws(*args, ctypes.c_void_p((1 << 20) + 8), need, None) == EINVAL  # misaligned
+    assert L.fcm_dw_pw_ws(*args, dev, -1, None) == EINVAL
+    dp = fcm.make_desc(1, 14, 14, 512, 512, 512, dtype="bf16", layout="nhwc")
+    pp = _evaluate("pw", dp, 2, 7, "k_pw3<bf16,1,1,4,4,p16>", splits=2)
+    assert fcm.workspace_bytes(dp, pp) > 0
+    assert L.fcm_pw(ctypes.byref(dp), dev, dev, None, dev, ctypes.byref(pp), None) == EINVAL
+    with pytest.raises(fcm.FcmError):
+        bad = fcm.make_desc(0, 14, 14, 512, 512, 512, dtype="bf16", layout="nhwc")
+        fcm.workspace_bytes(bad, p)
+
+
+def test_library_sources_do_not_allocate_device_memory():
+    """No allocation call anywhere in the library's host sources."""
+    csrc = os.path.join(ROOT, "paper_2404_19331_amd", "csrc")
+    for f in os.listdir(csrc):
+        if f.endswith((".cpp", ".h", ".hip", ".inc")):
+            src = open(os.path.join(csrc, f)).read()
+            assert not re.search(r"\bhip(Malloc|MallocAsync|HostMalloc|ExtMallocWithFlags|Free)\w*\s*\(", src), f
+
+
+def test_plan_limited_respects_the_workspace_budget():
+    """Where the unrestricted planner splits, a zero budget yields a plan needing none."""
+    found = False
+    for wl in ("C3b1", "C4"):
+        for case in bench.workload_cases(wl)[0]:
+            d = fcm.desc_from_case(case)
+            p = fcm.plan(case.op, d)
+            q = fcm.plan_limited(case.op, d, 0)
+            assert fcm.workspace_bytes(d, q) == 0
+            if fcm.workspace_bytes(d, p) > 0:
+                found = True
+                r = fcm.plan_limited(case.op, d, fcm.workspace_bytes(d, p))
+                assert (r.variant, r.tile_h, r.tile_w, r.splits) == (p.variant, p.tile_h, p.tile_w, p.splits)
+    assert found, "no workload layer is planned with a split"

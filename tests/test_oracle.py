@@ -748,3 +748,16 @@ def test_zero_point_validation():
     for bad in (dict(zp_in=128), dict(zp_in=-129), dict(rq=[(1, 6, -127, 127, 200)] * 3)):
         with pytest.raises(oracle.OracleError):
             oracle.run("pw", dict(c, **bad), inp)
+
+
+def test_c4_spread_cases_leave_most_outputs_unsaturated():
+    """The spread-keeping int8 C4 cases really exercise the contraction and rounding: most
+    of the oracle's outputs are strictly inside (-127, 127) and take many distinct values
+    (the named configuration saturates most of them)."""
+    from paper_2404_19331_amd.workloads import config_c4_spread
+    for case in config_c4_spread():
+        small = case.with_(n=1)
+        y = oracle.run(case.op, small, make_inputs(small))
+        inner = np.mean(np.abs(y.astype(np.int32)) < 127)
+        assert inner > 0.95, (case.name, inner)
+        assert len(np.unique(y)) > 100, case.name

@@ -232,6 +232,21 @@ fcm_status fcm_dw_pw_ws(const fcm_desc* desc, const void* x, const void* w_dw, c
                         const void* w_pw, const void* b_pw, void* y, const fcm_plan_t* plan,
                         void* workspace, int64_t workspace_bytes, void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc): fcm_dw_pw_ws with the workspace taken
+ * from a fixed device array of FCM_NOALLOC_SCRATCH_BYTES that the library holds on each
+ * GPU it runs on (from module load until the process ends) instead of from the caller.
+ * It allocates nothing and calls no allocating routine. plan NULL: the planner's best
+ * plan whose workspace fits the array; an explicit plan needing more fails with
+ * FCM_EINVAL. Every call on one GPU shares that GPU's array, so calls that overlap on one
+ * GPU (e.g. on two streams) race; the array keeps the last call's partial sums and needs
+ * no clearing (each split plan writes all it reads). FCM_EDEVICE if the runtime cannot
+ * resolve the array's device address. Otherwise as fcm_dw_pw. */
+#define FCM_NOALLOC_SCRATCH_BYTES (16u << 20)
+fcm_status fcm_dw_pw_noalloc(const fcm_desc* desc, const void* x, const void* w_dw, const void* b_dw,
+                             const void* w_pw, const void* b_pw, void* y, const fcm_plan_t* plan,
+                             void* stream);
+
 /* Device workspace bytes `plan` needs (its partial sums when it splits channel chunks over
  * workgroups; 0 for every other plan), or -1 for an invalid descriptor or plan. */
 int64_t fcm_workspace_bytes(const fcm_desc* desc, const fcm_plan_t* plan);

@@ -290,6 +290,12 @@ static fcm_status run(int op, const fcm_desc* d, const Tensors& t, const fcm_pla
   return FCM_OK;
 }
 
+fcm_status launch_module(int op, const fcm_desc* d, const void* x, const void* const* w, const void* const* b,
+                         void* y, const fcm_plan_t* plan, void* ws, int64_t ws_bytes, void* stream) {
+  Tensors t = {x, {w[0], w[1], w[2]}, {b[0], b[1], b[2]}, y};
+  return run(op, d, t, plan, ws, ws_bytes, stream);
+}
+
 }  // namespace fcm
 
 using namespace fcm;

@@ -76,4 +76,10 @@ fcm_status chain_group_desc(const fcm_chain_desc* c, const int* h, const int* w,
 // Number of layers a module spans.
 int op_layers(int op);
 
+// Launch module `op` (validation, planning, launch) with an optional caller workspace for
+// split plans: the body of every launch entry point. w / b: the module's weights and
+// biases in execution order (unused ones NULL).
+fcm_status launch_module(int op, const fcm_desc* d, const void* x, const void* const* w, const void* const* b,
+                         void* y, const fcm_plan_t* plan, void* ws, int64_t ws_bytes, void* stream);
+
 }  // namespace fcm

@@ -134,6 +134,8 @@ def lib():
         L.fcm_pw_ws.argtypes = [dp, vp, vp, vp, vp, pp, vp, i64, vp]
         L.fcm_dw_pw_ws.restype = L.fcm_pw_ws.restype = ctypes.c_int
         L.fcm_workspace_bytes.argtypes = [dp, pp]
+        L.fcm_dw_pw_noalloc.argtypes = [dp, vp, vp, vp, vp, vp, vp, pp, vp]
+        L.fcm_dw_pw_noalloc.restype = ctypes.c_int
         L.fcm_plan_limited.argtypes = [ctypes.c_int32, dp, hp, i64, pp]
         L.fcm_plan_limited.restype = ctypes.c_int
         L.fcm_workspace_bytes.restype = i64
@@ -397,6 +399,27 @@ def dw_pw(x, w_dw, w_pw, b_dw=None, b_pw=None, *, stride=1, pad=None, act=("none
     return _call(lib().fcm_dw_pw_ws, (ctypes.byref(d), _ptr(x), _ptr(w_dw), _ptr(b_dw), _ptr(w_pw), _ptr(b_pw),
                                       _ptr(y), _plan_arg(plan), _ptr(ws), ws.numel() * ws.element_size(),
                                       _stream(x, stream)), y, prepare, keep=ws)
+
+
+NOALLOC_SCRATCH_BYTES = 16 << 20  # FCM_NOALLOC_SCRATCH_BYTES
+
+
+def dw_pw_noalloc(x, w_dw, w_pw, b_dw=None, b_pw=None, *, stride=1, pad=None, act=("none", "none"), rq=None,
+                  layout="nchw", plan=None, out=None, stream=None, zp_in=0):
+    """DW -> PW module through fcm_dw_pw_noalloc: a split plan's partial sums go to the
+    library's fixed per-GPU array instead of a workspace (pass `out` to allocate nothing
+    here either). Calls overlapping on one GPU race on that array."""
+    dt = _dtype_name(x)
+    n, c, h, w = _dims(x, layout)
+    k = _kk(w_dw)
+    pad = (k - 1) // 2 if pad is None else pad
+    co = int(w_pw.shape[0])
+    _prep(x, [w_dw, w_pw], [b_dw, b_pw], dt)
+    d = make_desc(n, h, w, c, c, co, k, stride, pad, dt, layout, act, rq, zp_in=zp_in)
+    ho, wo = out_hw(h, w, k, stride, pad)
+    y = _out(x, layout, n, co, ho, wo, out)
+    return _call(lib().fcm_dw_pw_noalloc, (ctypes.byref(d), _ptr(x), _ptr(w_dw), _ptr(b_dw), _ptr(w_pw), _ptr(b_pw),
+                                           _ptr(y), _plan_arg(plan), _stream(x, stream)), y, False)
 
 
 def pw_dw(x, w_pw, w_dw, b_pw=None, b_dw=None, *, stride=1, pad=None, act=("none", "none"), rq=None, rq_channel=None,

@@ -154,9 +154,11 @@ typedef struct {
 
 /* A tiling chosen by fcm_plan (or filled in by the caller and validated at launch).
  * tile_h x tile_w output pixels per workgroup; c_block channels staged per step (the
- * contraction chunk, or the depthwise channel block); co_block output channels per
- * workgroup (dw_pw, pw: PW outputs; pw_dw, dw: intermediate/depthwise channels;
- * pw_dw_pw: intermediate-channel chunk). All byte figures are for the whole call. */
+ * contraction chunk, the depthwise channel block, or for pw_dw_pw / pw_pw the
+ * intermediate-channel chunk); co_block channels per workgroup (dw_pw, pw, pw_dw_pw,
+ * pw_pw: the last layer's outputs; pw_dw, dw: intermediate / depthwise channels). All
+ * byte figures are for the whole call; bytes_paper follows Sec. IV's Eq. 1-4 with the
+ * readings listed in the design notes. */
 typedef struct {
   int32_t op;            /* fcm_op */
   int32_t tile_h, tile_w;

@@ -1,5 +1,8 @@
 """FusePlanner cost model, written out from the paper -- TEST INFRASTRUCTURE.
 
+Only tests/ use this module; the library's planner (csrc/fcm_plan.cpp) shares no code
+with it and is checked against it.
+
 arXiv 2404.19331, Sec. IV. Two families of numbers are modelled here:
 
 1. The paper's closed-form global-memory-access estimates:
@@ -21,7 +24,10 @@ Readings where the paper is silent or ambiguous (listed in the design notes as w
     ceil(Wo/TW) for an output tile of width TW; batch multiplies the overlap;
   * Eq. 2's weight term uses the number of spatial tiles (ceil(OFMsHW/OFMsTileHW)),
     as Eq. 3 does; the literal variant is kept as ``pw_gma_literal``;
-  * Eq. 4 gets the output-write term (+DwOFMsSz) the printed equation omits;
+  * Eq. 4 gets the output-write term (+DwOFMsSz) the printed equation omits, and its
+    PW-weight term ceil(DwOFMsSz/DwOFMsTileSz) is read, like Eq. 2's, as the number of
+    spatial tiles: the workgroups of one spatial tile together read the PW weights once
+    (the literal count of output tiles would charge them once per channel block);
   * biases are not counted (the paper's model has none).
 """
 from math import ceil
@@ -74,13 +80,24 @@ def dwpw_gma(c, dw_overlap, dw_ifms_sz, n_co_blocks, n_spatial_tiles, pw_weights
             + n_spatial_tiles * n_co_blocks * dw_weights_sz + pw_ofms_sz)
 
 
-def pwdwpw_gma(ci, dw_overlap, pw1_ifms_sz, n_spatial_tiles, pw1_weights_sz, dw_weights_sz,
+def pwdwpw_gma(ci, dw_overlap, pw1_ifms_sz, n_co_blocks, n_spatial_tiles, pw1_weights_sz, dw_weights_sz,
                pw2_weights_sz, ofms_sz):
-    """Derived PW->DW->PW module estimate: one workgroup per spatial tile holds all
-    intermediate channels in turn, so the input (with overlap) is read once and every
-    spatial tile reads all three weight sets."""
-    return ((2 * ci * dw_overlap + pw1_ifms_sz)
-            + n_spatial_tiles * (pw1_weights_sz + dw_weights_sz + pw2_weights_sz) + ofms_sz)
+    """Derived PW->DW->PW module estimate (built as Eq. 4): a workgroup owns a spatial tile
+    and a block of the last layer's output channels and streams every intermediate
+    channel through PW1 and DW itself, so the input (with its overlap), PW1's and DW's
+    weights are read once per output-channel block; PW2's weights once per spatial tile
+    (its rows are split over the blocks); the output is written once."""
+    return ((2 * ci * dw_overlap + pw1_ifms_sz) * n_co_blocks
+            + n_spatial_tiles * n_co_blocks * (pw1_weights_sz + dw_weights_sz)
+            + n_spatial_tiles * pw2_weights_sz + ofms_sz)
+
+
+def pwpw_gma(ifms_sz, n_co_blocks, n_spatial_tiles, pw1_weights_sz, pw2_weights_sz, ofms_sz):
+    """Derived PW->PW module estimate (as PW->DW->PW without the depthwise layer and its
+    overlap): the input and PW1's weights per output-channel block, PW2's weights per
+    spatial tile, the output once."""
+    return (ifms_sz * n_co_blocks + n_spatial_tiles * n_co_blocks * pw1_weights_sz
+            + n_spatial_tiles * pw2_weights_sz + ofms_sz)
 
 
 # ----------------------------------------------------------------------------------
@@ -116,17 +133,18 @@ def _valid_outputs(ty, tx, th, tw, ho, wo):
 def brute_force_bytes(op, g, tiling, elt):
     """Global bytes moved by a tiled kernel, counted workgroup by workgroup.
 
-    op: 'dw_pw' | 'pw' | 'dw' | 'pw_dw' | 'pw_dw_pw'
+    op: 'dw_pw' | 'pw' | 'dw' | 'pw_dw' | 'pw_dw_pw' | 'pw_pw'
     g:  dict(n, h, w, c_in, c_mid, c_out, k, stride, pad)
     tiling: dict(tile_h, tile_w, co_block) -- co_block is the output-channel block of the
-            last convolution (dw_pw, pw) or the intermediate-channel block (pw_dw, dw);
-            pw_dw_pw keeps all channels in one workgroup.
+            last convolution (dw_pw, pw, pw_dw_pw, pw_pw) or the intermediate-channel
+            block (pw_dw, dw). A pw_dw_pw / pw_pw workgroup computes every intermediate
+            channel of its spatial tile itself, block after block.
     """
     n, h, w = g["n"], g["h"], g["w"]
     ci, cm, co = g["c_in"], g["c_mid"], g["c_out"]
     k, s, p = g["k"], g["stride"], g["pad"]
     th, tw = tiling["tile_h"], tiling["tile_w"]
-    if op == "pw":
+    if op in ("pw", "pw_pw"):
         k, s, p = 1, 1, 0
     ho, wo = out_dim(h, k, s, p), out_dim(w, k, s, p)
     nty, ntx = ceil(ho / th), ceil(wo / tw)
@@ -155,10 +173,29 @@ def brute_force_bytes(op, g, tiling, elt):
                         else:
                             total += pos * me                   # this channel block only
                         total += me * k * k + outs * me
-                elif op == "pw_dw_pw":
-                    total += pos * ci + cm * ci + cm * k * k + co * cm + outs * co
+                elif op in ("pw_dw_pw", "pw_pw"):
+                    cob = tiling["co_block"]
+                    for c0 in range(0, co, cob):
+                        ce = min(cob, co - c0)
+                        total += pos * ci + cm * ci             # staged input, all of PW1
+                        if op == "pw_dw_pw":
+                            total += cm * k * k                 # all DW weights
+                        total += ce * cm + outs * ce            # PW2 rows of the block, output
                 else:
                     raise ValueError(op)
+    return total * elt
+
+
+def register_pwpw_bytes(g, pixels_per_group, elt):
+    """PW->PW on pixel groups (the register-resident kernel: a group of pixels in one
+    wave with every channel): input and output once, both weight matrices once per
+    group, counted group by group."""
+    npix = g["n"] * g["h"] * g["w"]
+    ci, cm, co = g["c_in"], g["c_mid"], g["c_out"]
+    total = 0
+    for p0 in range(0, npix, pixels_per_group):
+        px = min(pixels_per_group, npix - p0)
+        total += px * (ci + co) + cm * ci + co * cm
     return total * elt
 
 
@@ -169,6 +206,8 @@ def ideal_bytes(op, g, elt):
     k, s, p = g["k"], g["stride"], g["pad"]
     if op == "pw":
         return (n * h * w * ci + co * ci + n * h * w * co) * elt
+    if op == "pw_pw":
+        return (n * h * w * ci + cm * ci + co * cm + n * h * w * co) * elt
     ho, wo = out_dim(h, k, s, p), out_dim(w, k, s, p)
     x = n * h * w * ci
     if op == "dw":

@@ -761,3 +761,40 @@ def test_c4_spread_cases_leave_most_outputs_unsaturated():
         inner = np.mean(np.abs(y.astype(np.int32)) < 127)
         assert inner > 0.95, (case.name, inner)
         assert len(np.unique(y)) > 100, case.name
+
+
+def _t_bf16_round(t64):
+    """float64 tensor -> bfloat16 bits the way the stage cast is defined: to float32
+    (nearest even), then to bfloat16 (nearest even), by torch's own conversions."""
+    return t64.to(torch.float32).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+
+
+def _t_vals(bits):
+    return torch.from_numpy(_bf16_to_f32(bits).astype(np.float64))
+
+
+@pytest.mark.parametrize("k,s,p", [(3, 1, 1), (3, 2, 1), (5, 1, 2), (5, 2, 0)])
+def test_bf16_stage_cast_matches_torch_float64_convolutions(k, s, p):
+    """bf16 oracle = float64 convolutions (torch) with each stage rounded to bf16
+    nearest-even, element for element, for the single DW and PW layers and the DW->PW
+    module (whose intermediate is rounded before the PW). Truncating instead of rounding
+    at either stage changes many of these outputs, so the pin sees the cast's mode."""
+    case = Case("dw_pw", 2, 11, 9, 24, 24, 20, k, s, p, "bf16", "nchw", ("relu", "relu6", "none"), bias=True,
+                dist_x="n01", seed=424)
+    inp = make_inputs(case)
+    x, wd, bd, wp, bp = (inp[n] for n in ("x", "w_dw", "b_dw", "w_pw", "b_pw"))
+    xt, wdt, wpt = _t_vals(x), _t_vals(wd), _t_vals(wp)
+    bdt, bpt = torch.from_numpy(bd.astype(np.float64)), torch.from_numpy(bp.astype(np.float64))
+    c = case.c_in
+    dw64 = F.conv2d(xt, wdt.reshape(c, 1, k, k), bdt, stride=s, padding=p, groups=c).clamp(min=0)
+    mid = _t_bf16_round(dw64)
+    pw64 = (F.conv2d(_t_vals(mid), wpt.reshape(case.c_out, c, 1, 1), bpt)).clamp(0, 6)
+    ref_dwpw = _t_bf16_round(pw64)
+    assert np.array_equal(oracle.dw_pw(case, x, wd, bd, wp, bp), ref_dwpw)
+    assert np.array_equal(oracle.dw(case, x, wd, bd), mid)
+    pw_case = case.with_(h=mid.shape[2], w=mid.shape[3], k=1, stride=1, pad=0, act=("relu6", "none", "none"),
+                         c_in=c, c_mid=c)
+    assert np.array_equal(oracle.pw(pw_case, mid, wp, bp), ref_dwpw)
+    # the rounding mode matters on these inputs: truncation differs
+    trunc = (dw64.to(torch.float32).numpy().view(np.uint32) >> 16).astype(np.uint16)
+    assert np.mean(trunc != mid) > 0.2

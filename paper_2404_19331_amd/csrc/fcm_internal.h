@@ -47,11 +47,11 @@ struct ReqCh {
 // output-channel tiles of 16.
 constexpr int kZpMaxTiles = 12;
 
-FCM_HD inline int elt_size(int dt) { return dt == DT_F32 ? 4 : (dt == DT_BF16 ? 2 : 1); }
+FCM_HD constexpr int elt_size(int dt) { return dt == DT_F32 ? 4 : (dt == DT_BF16 ? 2 : 1); }
 // contraction elements per MFMA operand step (64 bytes of k per row)
 FCM_HD inline int k_block(int dt) { return 64 / elt_size(dt); }
-FCM_HD inline int round_up(int a, int b) { return (a + b - 1) / b * b; }
-FCM_HD inline int ceil_div(int a, int b) { return (a + b - 1) / b; }
+FCM_HD constexpr int round_up(int a, int b) { return (a + b - 1) / b * b; }
+FCM_HD constexpr int ceil_div(int a, int b) { return (a + b - 1) / b; }
 
 // ---------------------------------------------------------------------------------
 // LDS layout: byte offsets of each buffer and row strides. Rows are padded by 16 bytes
@@ -259,8 +259,8 @@ struct Lds5 {
   int dwo_off;     // depthwise output exchange (pp > 0 only)
   int total;
 };
-FCM_HD inline Lds5 lds5(int dt, int mode, int K, int IH, int IW, int COB, int ring, int pp) {
-  Lds5 L;
+FCM_HD constexpr Lds5 lds5(int dt, int mode, int K, int IH, int IW, int COB, int ring, int pp) {
+  Lds5 L{};
   const int cb = kRowB / elt_size(dt);
   const bool pw = mode != M3_DW, dw = mode != M3_PW;
   L.nqp = round_up(IH * IW, 32);

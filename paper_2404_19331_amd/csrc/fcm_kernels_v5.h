@@ -1,9 +1,10 @@
 // fcm_kernels_v5.h -- streaming NHWC kernels for gfx950: the DW->PW module and the
 // layer-by-layer PW and DW kernels built from the same pieces.
 //
-// k_fused5<DT, K, S, MODE, NB, CTW, WC>
+// k_fused5<DT, K, S, MODE, TH, TW, CTW, WC>
 //   A workgroup (four waves) computes a sequence of work tiles: tile ids L, L + G, ...
-//   (G workgroups), each an image, a TH x TW output tile and a block of
+//   (G workgroups), each an image, a TH x TW output tile (compile-time: the window
+//   geometry and LDS layout are constants) and a block of
 //   COB = 16 * CTW * WC output channels (DW: one 64-byte channel chunk). Several
 //   workgroups are resident on each CU; their copies, arithmetic and stores interleave,
 //   which keeps HBM busy (Sec. III-B: the module stages what the first convolution needs,
@@ -45,16 +46,12 @@ constexpr int kThreads5 = 256;
 constexpr int kWinPerWave5 = 8;  // window copy instructions per wave (window <= 512 pixels)
 constexpr int kPwPerWave5 = 8;   // PW weight row copies per wave (output-channel block <= 1024)
 
-// q / d for small non-negative q: with m = ceil(2^20 / d), floor(q * m / 2^20) equals
-// floor(q / d) whenever q < 2^20 / d and q < 4096 (m exceeds 2^20 / d by less than one, so
-// the product overshoots q / d by less than q / 2^20 < 1 / d, which never carries past the
-// next multiple of d; q * m stays below 2^32). One 24-bit multiply and a shift instead of
-// a 32-bit division; window positions and tile pixels are far below these bounds.
-struct FastDiv {
-  uint32_t m;
-  __device__ explicit FastDiv(int d) : m(((1u << 20) + (uint32_t)d - 1u) / (uint32_t)d) {}
-  __device__ int operator()(int q) const { return (int)(__umul24((uint32_t)q, m) >> 20); }
-};
+// dma16 with a scalar part of the offset (added by the buffer unit; an out-of-range lane
+// offset stays out of range since both parts are below 2^31).
+__device__ __forceinline__ void dma16s(rsrc_t r, char* wave_base, uint32_t voff, uint32_t soff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)wave_base, 16, voff, soff, 0,
+                                           0);
+}
 
 __device__ __forceinline__ u32x4 buf_load16(rsrc_t r, uint32_t off) {
   return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
@@ -62,7 +59,7 @@ __device__ __forceinline__ u32x4 buf_load16(rsrc_t r, uint32_t off) {
 __device__ __forceinline__ void store_nt16(void* p, const u32x4& v) { __builtin_nontemporal_store(v, (u32x4*)p); }
 __device__ __forceinline__ void store_nt4(void* p, uint32_t v) { __builtin_nontemporal_store(v, (uint32_t*)p); }
 
-template <class DT, int K, int S, int MODE, int NB, int CTW, int WC>
+template <class DT, int K, int S, int MODE, int TH, int TW, int CTW, int WC>
 __global__ __launch_bounds__(kThreads5) void k_fused5(KArgs a) {
   extern __shared__ __align__(16) char smem[];
   using T = typename DT::T;
@@ -84,7 +81,9 @@ __global__ __launch_bounds__(kThreads5) void k_fused5(KArgs a) {
   constexpr int OTPG = OGE / 4;   // MFMA tiles per granule
   constexpr int NGW = HAS_PW ? CTW / OTPG : 1;  // output granules per lane
   constexpr bool SHARE = HAS_DW && HAS_PW && WC > 1;
-  constexpr int NBT = NB * WP;                // pixel blocks of the work tile
+  constexpr int P = TH * TW;
+  constexpr int NB = ((P + 15) / 16 + WP - 1) / WP;  // pixel blocks per wave
+  constexpr int NBT = NB * WP;                // pixel blocks of the work tile (some may be empty)
   constexpr int NBD = SHARE ? NBT / 4 : NB;   // depthwise blocks per wave
   constexpr int NRAW = HAS_DW ? (CB * KK * ELT + 1023) / 1024 : 0;  // raw DW weight loads (waves 0..)
   static_assert(WC == 1 || WC == 2 || WC == 4, "wave grid");
@@ -94,15 +93,16 @@ __global__ __launch_bounds__(kThreads5) void k_fused5(KArgs a) {
   static_assert(NRAW <= 4, "raw depthwise weights: one load per wave at most");
   static_assert(COB <= 1024, "PW bias block");
 
-  const int TH = a.TH, TW = a.TW, P = TH * TW;
-  const int IH = HAS_DW ? (TH - 1) * SE + KE : TH;
-  const int IW = HAS_DW ? (TW - 1) * SE + KE : TW;
-  const int IWE = SE == 2 ? (IW + 1) / 2 : IW;  // stride 2: even columns first, then odd
-  const int NQ = IH * IW;
-  const Lds5 lay = lds5(dtype_id<DT>(), MODE, KE, IH, IW, COB, 2, SHARE ? 16 * NBT : 0);
-  const int NWI = lay.nqp / 16;                // window copies: 2 planes x nqp / 32
-  const int NPW = HAS_PW ? lay.cobp / 16 : 0;  // PW weight row copies
-  const int NTOT = NWI + NPW + (HAS_DW ? 1 : 0);  // + DW bias
+  constexpr int IH = HAS_DW ? (TH - 1) * SE + KE : TH;
+  constexpr int IW = HAS_DW ? (TW - 1) * SE + KE : TW;
+  constexpr int IWE = SE == 2 ? (IW + 1) / 2 : IW;  // stride 2: even columns first, then odd
+  constexpr int NQ = IH * IW;
+  constexpr Lds5 lay = lds5(dtype_id<DT>(), MODE, KE, IH, IW, COB, 2, SHARE ? 16 * NBT : 0);
+  constexpr int NWI = lay.nqp / 16;                // window copies: 2 planes x nqp / 32
+  constexpr int NPW = HAS_PW ? lay.cobp / 16 : 0;  // PW weight row copies
+  constexpr int NTOT = NWI + NPW + (HAS_DW ? 1 : 0);  // + DW bias
+  static_assert(NWI <= 4 * kWinPerWave5, "window copies per wave");
+  static_assert(NPW <= 4 * kPwPerWave5, "weight row copies per wave");
   const int C = MODE == M3_DW ? a.Cm : a.Ci;
   const int nch = MODE == M3_DW ? 1 : ceil_div(C, CB);
 
@@ -153,24 +153,42 @@ __global__ __launch_bounds__(kThreads5) void k_fused5(KArgs a) {
   // [window | PW weight rows | DW bias]; i & 1 is the plane (both parts have an even
   // count), so each lane always copies 16-byte slot `sl` of a channel row.
   const int sl = 2 * (wave & 1) + (lane & 1);
-  const FastDiv div_iw(IW), div_tw(TW);
-  uint32_t woff[kWinPerWave5];  // pixel part of each window copy's offset (or kOob), per tile
+  // Window pixel this lane copies in its k-th window instruction, the same for every
+  // tile: (wy << 16) | wx within the window, or -1 beyond it.
+  int wyx[kWinPerWave5];
+#pragma unroll
+  for (int k = 0; k < kWinPerWave5; ++k) {
+    const int i = wave + 4 * k;
+    wyx[k] = -1;
+    if (i >= NWI) break;  // wave-uniform
+    const int q = 32 * (i >> 1) + (lane >> 1);  // stored window position
+    if (q < NQ) {
+      const int wy = q / IW, wxs = q - wy * IW;
+      wyx[k] = (wy << 16) | (SE == 2 ? (wxs < IWE ? 2 * wxs : 2 * (wxs - IWE) + 1) : wxs);
+    }
+  }
+  const uint32_t pixb = (uint32_t)(C * ELT), rowb = (uint32_t)a.W * pixb;
+  // Per tile: the lane part of each window copy's byte offset (kOob outside the image)
+  // and a scalar part: interior tiles put the tile origin in the scalar part and need no
+  // bounds checks; border tiles check every position.
+  uint32_t woff[kWinPerWave5];
+  uint32_t wsoff = 0;
   auto window_offsets = [&](const Tile& t) {
     const int iy0 = HAS_DW ? t.oy0 * SE - a.pad : t.oy0;
     const int ix0 = HAS_DW ? t.ox0 * SE - a.pad : t.ox0;
+    const bool interior = iy0 >= 0 && ix0 >= 0 && iy0 + IH <= a.H && ix0 + IW <= a.W;  // wave-uniform
+    wsoff = interior ? (uint32_t)(iy0 * a.W + ix0) * pixb : 0u;
 #pragma unroll
     for (int k = 0; k < kWinPerWave5; ++k) {
-      const int i = wave + 4 * k;
-      if (i >= NWI) break;  // wave-uniform
-      const int q = 32 * (i >> 1) + (lane >> 1);  // stored window position
-      uint32_t off = kOob;
-      if (q < NQ) {
-        const int wy = div_iw(q), wxs = q - wy * IW;
-        const int wx = SE == 2 ? (wxs < IWE ? 2 * wxs : 2 * (wxs - IWE) + 1) : wxs;
+      if (wave + 4 * k >= NWI) break;
+      const int v = wyx[k], wy = v >> 16, wx = v & 0xffff;
+      if (interior) {
+        woff[k] = v < 0 ? kOob : __umul24((uint32_t)wy, rowb) + __umul24((uint32_t)wx, pixb);
+      } else {
         const int gy = iy0 + wy, gx = ix0 + wx;
-        if ((unsigned)gy < (unsigned)a.H && (unsigned)gx < (unsigned)a.W) off = (uint32_t)((gy * a.W + gx) * C) * ELT;
+        const bool ok = v >= 0 && (unsigned)gy < (unsigned)a.H && (unsigned)gx < (unsigned)a.W;
+        woff[k] = ok ? (uint32_t)(gy * a.W + gx) * pixb : kOob;
       }
-      woff[k] = off;
     }
   };
   // pointwise weight rows of this wave's copies (fixed: the channel block is): byte
@@ -200,20 +218,22 @@ __global__ __launch_bounds__(kThreads5) void k_fused5(KArgs a) {
     }
     const rsrc_t rx = make_rsrc(x + (size_t)n * img, (uint32_t)(img * ELT));
     const int cs = c0 + sl * CPL;  // first channel of this lane's slot
-    const bool cok = cs < C;
-    const uint32_t coff = (uint32_t)(cs * ELT);
+    const bool cok = c0 + CB <= C || cs < C;  // (only a ragged last chunk has lanes beyond C)
+    const uint32_t coff = (uint32_t)(sl * CPL * ELT);
+    const uint32_t soff = wsoff + (uint32_t)(c0 * ELT);  // scalar
 #pragma unroll
     for (int k = 0; k < kWinPerWave5; ++k) {
       const int i = wave + 4 * k;
       if (i >= NWI) break;
-      dma16(rx, sb + (i & 1) * (lay.nqp * 32) + (i >> 1) * 1024, cok ? woff[k] + coff : kOob);
+      dma16s(rx, sb + (i & 1) * (lay.nqp * 32) + (i >> 1) * 1024, cok ? woff[k] + coff : kOob, soff);
     }
     if constexpr (HAS_PW) {
 #pragma unroll
       for (int k = 0; k < kPwPerWave5; ++k) {
         const int tt = pw_first + 4 * k - NWI;
         if (tt >= NPW) break;  // wave-uniform
-        dma16(rw, sb + lay.win_bytes + (tt & 1) * (lay.cobp * 32) + (tt >> 1) * 1024, cok ? poff[k] + coff : kOob);
+        dma16s(rw, sb + lay.win_bytes + (tt & 1) * (lay.cobp * 32) + (tt >> 1) * 1024, cok ? poff[k] + coff : kOob,
+               (uint32_t)(c0 * ELT));
       }
     }
     if constexpr (HAS_DW) {
@@ -271,20 +291,37 @@ __global__ __launch_bounds__(kThreads5) void k_fused5(KArgs a) {
   // after the next item's copies, so that the wait for those copies never has to wait
   // for fresh stores as well (stores and loads share the counter). ----
   const bool full16 = (a.Co * ELT) % 16 == 0;
+  // Output pixel of each of this lane's pixel blocks within a tile, the same for every
+  // tile: (py << 16) | px, or -1 past the tile; and its byte offset from the tile's first
+  // output pixel (the lane's first channel included). A tile's base address is scalar.
+  const int cl0 = co0 + OGE * (4 * wc * NGW + g);  // this lane's first output channel (PW)
+  const int nbo = HAS_PW ? NB : NBD;              // blocks this lane stores
+  int eyx[HAS_PW ? NB : NBD];
+  uint32_t eoff[HAS_PW ? NB : NBD];
+  const int ochan = HAS_PW ? a.Co : C;  // channels of an output pixel
+#pragma unroll
+  for (int b = 0; b < nbo; ++b) {
+    const int p = (HAS_PW ? (b * WP + wp) : dw_block(b)) * 16 + r16;
+    const int py = p / TW, px = p - py * TW;
+    eyx[b] = p < P ? (py << 16) | px : -1;
+    eoff[b] = (uint32_t)(((py * a.Wo + px) * ochan + (HAS_PW ? cl0 : cb * CB + g * CPL)) * ELT);
+  }
+  // lanes whose pixel lies in the image (tiles at the right and bottom edges are partial)
+  auto out_ok = [&](const Tile& t, int b) {
+    const int v = eyx[b];
+    const bool full = t.oy0 + TH <= a.Ho && t.ox0 + TW <= a.Wo;  // wave-uniform
+    return v >= 0 && (full || ((v >> 16) < a.Ho - t.oy0 && (v & 0xffff) < a.Wo - t.ox0));
+  };
   auto epilogue = [&](const Tile& t) {
+    char* tbase = (char*)a.y + (size_t)((t.n * a.Ho + t.oy0) * a.Wo + t.ox0) * ochan * ELT;
     if constexpr (HAS_PW) {
       const char* bl = smem + lay.pwb_off;
-      const int cl0 = co0 + OGE * (4 * wc * NGW + g);  // this lane's first output channel
 #pragma unroll
       for (int b = 0; b < NB; ++b) {
-        const int p = (b * WP + wp) * 16 + r16;
-        if (p >= P) continue;
-        const int py = div_tw(p), px = p - py * TW;
-        const int oy = t.oy0 + py, ox = t.ox0 + px;
-        if (oy >= a.Ho || ox >= a.Wo) continue;
+        if (!out_ok(t, b)) continue;
         // granule k of this lane: channels cl0 + 4 * OGE * k + [0, OGE); channel
         // cl0 + 4 * OGE * k + 4t + e is value e of local tile k * OTPG + t
-        char* dpx = (char*)a.y + ((size_t)((t.n * a.Ho + oy) * a.Wo + ox) * a.Co + cl0) * ELT;
+        char* dpx = tbase + eoff[b];
 #pragma unroll
         for (int k = 0; k < NGW; ++k) {
           if (cl0 + 4 * OGE * k >= a.Co) break;
@@ -336,16 +373,10 @@ __global__ __launch_bounds__(kThreads5) void k_fused5(KArgs a) {
         for (int i = 0; i < CTW; ++i) acc[b][i] = AccV{0, 0, 0, 0};
     } else {
       // depthwise only: this lane's 16 bytes of channels of each of its pixels
-      const int ch = cb * CB + g * CPL;
+      const bool chok = cb * CB + g * CPL < C;
 #pragma unroll
-      for (int j = 0; j < NBD; ++j) {
-        const int p = dw_block(j) * 16 + r16;
-        if (p >= P) continue;
-        const int py = div_tw(p), px = p - py * TW;
-        const int oy = t.oy0 + py, ox = t.ox0 + px;
-        if (oy < a.Ho && ox < a.Wo && ch < C)
-          store_nt16((T*)a.y + (((size_t)t.n * a.Ho + oy) * a.Wo + ox) * C + ch, bop[j]);
-      }
+      for (int j = 0; j < NBD; ++j)
+        if (chok && out_ok(t, j)) store_nt16(tbase + eoff[j], bop[j]);
     }
   };
 
@@ -406,7 +437,7 @@ __global__ __launch_bounds__(kThreads5) void k_fused5(KArgs a) {
 #pragma unroll
         for (int j = 0; j < NL; ++j) {
           const int p = min(dw_block(j) * 16 + r16, P - 1);
-          const int py = div_tw(p), px = p - py * TW;
+          const int py = p / TW, px = p - py * TW;
           xb[j] = sb + plane_in + ((py * SE) * IW + px) * 32;
         }
         Acc dacc[NL][CPL];
@@ -487,9 +518,9 @@ __global__ __launch_bounds__(kThreads5) void k_fused5(KArgs a) {
   if (pending) epilogue(pend_t);
 }
 
-template <class DT, int K, int S, int MODE, int NB, int CTW, int WC>
+template <class DT, int K, int S, int MODE, int TH, int TW, int CTW, int WC>
 int launch_fused5(const KArgs& a, int grid, void* stream) {
-  auto fn = k_fused5<DT, K, S, MODE, NB, CTW, WC>;
+  auto fn = k_fused5<DT, K, S, MODE, TH, TW, CTW, WC>;
   const int lds = a.L.bytes;
   if (lds > 65536) {
     hipError_t e = hipFuncSetAttribute((const void*)fn, hipFuncAttributeMaxDynamicSharedMemorySize, lds);

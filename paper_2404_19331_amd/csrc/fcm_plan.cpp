@@ -214,13 +214,14 @@ static int tiling_lds(const Variant& v, const Geom& g, int TH, int TW, int CB, i
     if (dw_only ? (g.cm * g.elt) % 16 : (g.co * g.elt) % 4) return 0;
     if ((int64_t)g.h * g.w * cin * g.elt >= ((int64_t)1 << 31)) return 0;
     if (!dw_only && (int64_t)(g.co + COB) * g.ci * g.elt >= ((int64_t)1 << 31)) return 0;
-    if (CB != 64 / g.elt || COB != v.max_cob || P > v.max_p) return 0;
+    if (CB != 64 / g.elt || COB != v.max_cob || TH != v.tile_h || TW != v.tile_w) return 0;
     const int mode = g.family == FAM_DWPW ? M3_DWPW : (g.family == FAM_PW ? M3_PW : M3_DW);
     const int KE = mode == M3_PW ? 1 : g.k, SE = mode == M3_PW ? 1 : g.s;
     const int IH = (TH - 1) * SE + KE, IW = (TW - 1) * SE + KE;
     if (round_up(IH * IW, 32) > 512) return 0;  // window copies: 8 per wave at most
     const bool share = mode == M3_DWPW && v.wc > 1;
-    return lds5(g.dtype, mode, KE, IH, IW, COB, v.ks, share ? v.max_p : 0).total;
+    const int wp = 4 / v.wc, nbt = ((P + 15) / 16 + wp - 1) / wp * wp;  // pixel blocks, as the kernel
+    return lds5(g.dtype, mode, KE, IH, IW, COB, v.ks, share ? 16 * nbt : 0).total;
   }
   if (v.gen == 3) {
     // NHWC, 16-byte input channel rows, 32-bit buffer offsets, 64-byte chunk, run-time

@@ -84,11 +84,10 @@ __global__ __launch_bounds__(kThreads5) void k_fused5(KArgs a) {
   constexpr int P = TH * TW;
   constexpr int NB = ((P + 15) / 16 + WP - 1) / WP;  // pixel blocks per wave
   constexpr int NBT = NB * WP;                // pixel blocks of the work tile (some may be empty)
-  constexpr int NBD = SHARE ? NBT / 4 : NB;   // depthwise blocks per wave
+  constexpr int NBD = SHARE ? (NBT + 3) / 4 : NB;  // depthwise blocks per wave (the last may hold no pixels)
   constexpr int NRAW = HAS_DW ? (CB * KK * ELT + 1023) / 1024 : 0;  // raw DW weight loads (waves 0..)
   static_assert(WC == 1 || WC == 2 || WC == 4, "wave grid");
   static_assert(!HAS_PW || CTW % OTPG == 0, "whole output granules per lane");
-  static_assert(!SHARE || NBT % 4 == 0, "depthwise blocks split evenly over the waves");
   static_assert(MODE != M3_DW || WC == 1, "a depthwise-only tile has no channel split");
   static_assert(NRAW <= 4, "raw depthwise weights: one load per wave at most");
   static_assert(COB <= 1024, "PW bias block");

@@ -16,6 +16,7 @@
 // estimate with the layer-by-layer chain's (Sec. IV-B: fuse when the fused estimate is
 // lower).
 #include <algorithm>
+#include <cmath>
 #include <cstdlib>
 #include <cstring>
 #include <map>
@@ -502,6 +503,49 @@ static double persistent_time_estimate(const Variant& v, const Geom& g, const fc
   return std::max(t_pipe, t_mem) + 1e-3 * t_pipe;
 }
 
+// Time model of a streaming (gen 5) kernel launch, in seconds. A workgroup runs its items
+// (work tile x 64-byte channel chunk) one after another with the next item's copies in
+// flight, so a launch costs its items per workgroup times a per-item cost: fixed work,
+// the busiest wave's depthwise dot instructions, its MFMAs, the copy instructions of the
+// item, the epilogue's share per item and the exchange barrier of a channel-split tile,
+// scaled by how many workgroups share a CU; never faster than the module's HBM bytes.
+// Constants fitted (least squares on log time) to 329 timed plans of the MobileNetV1
+// (batch 1 and 32) and ViT-projection DW->PW layers on MI355X: within about 0.89-1.11x
+// of the timings for 80% of them.
+static double streaming_time_estimate(const Variant& v, const Geom& g, const fcm_plan_t& p, const fcm_hw_desc& hw) {
+  constexpr double kLaunchUs = 4.0;
+  constexpr double kItem = 773.7, kPerDot = 7.54, kPerMfma = 39.0, kPerCopy = 42.1, kPerEpi = 381.3;
+  constexpr double kShareExp = 0.649;
+  constexpr double kClockMHz = 2400.0, kHbm = 5.2e12, kLaunchFloorUs = 2.5;
+  const bool has_dw = v.family != FAM_PW, has_pw = v.family != FAM_DW;
+  const int K = has_dw ? g.k : 1, S = has_dw ? g.s : 1;
+  const int TH = v.tile_h, TW = v.tile_w, P = TH * TW;
+  const int wp = 4 / v.wc;
+  const int NB = ceil_div(ceil_div(P, 16), wp), NBT = NB * wp;
+  const bool share = has_dw && has_pw && v.wc > 1;
+  const int nbd = share ? ceil_div(NBT, 4) : NB;
+  const int ctw = has_pw ? v.max_cob / 16 / v.wc : 0;
+  const int ogtiles = 4 / g.elt;  // MFMA tiles per 16-byte output granule
+  const int cin = v.family == FAM_DW ? g.cm : g.ci, last = v.family == FAM_DW ? g.cm : g.co;
+  const int nch = v.family == FAM_DW ? 1 : ceil_div(cin * g.elt, 64);
+  const int64_t ntiles = (int64_t)g.n * ceil_div(g.ho, TH) * ceil_div(g.wo, TW) * ceil_div(last, p.co_block);
+  const int ncb = ceil_div(last, p.co_block);
+  int64_t G = std::min<int64_t>(std::max(1, p.workgroups), ntiles);
+  G -= G % ncb;
+  G = std::max<int64_t>(G, ncb);
+  const double ipw = (double)ceil_div((int)std::min<int64_t>(ntiles, 1 << 30), (int)G) * nch;
+  const double wpc = std::max(1.0, (double)G / hw.num_cus);
+  const int IH = (TH - 1) * S + K, IW = (TW - 1) * S + K;
+  const int copies = round_up(IH * IW, 32) / 16 + (has_pw ? round_up(p.co_block, 32) / 16 : 0) + (has_dw ? 1 : 0);
+  const double dots = has_dw ? (double)nbd * K * K * (16 / g.elt) : 0.0;
+  const double mfmas = has_pw ? (double)NB * ctw * (g.elt == 4 ? 4 : 1) : 0.0;
+  const double epi = has_pw ? (double)NB * std::max(1, ctw / ogtiles) / nch : (double)nbd;
+  const double per = kItem + kPerDot * dots + kPerMfma * mfmas + kPerCopy * copies + kPerEpi * epi;
+  const double t_us = kLaunchUs + ipw * per * std::pow(wpc, kShareExp) / kClockMHz;
+  const double t_mem_us = (double)p.bytes_ideal / kHbm * 1e6 + kLaunchFloorUs;
+  return std::max(t_us, t_mem_us) * 1e-6;
+}
+
 // Time model of the PW -> PW register kernel (gen 4), in seconds: each wave runs its
 // chunks one after another, each chunk costing its operand loads (1 KiB per 16-byte-per-
 // lane load, the CU's cache port shared by the resident waves), its MFMAs and a memory
@@ -599,6 +643,7 @@ double plan_time_estimate(const Geom& g, const fcm_plan_t& p, const fcm_hw_desc&
   if (p.variant < 0 || p.variant >= nv) return 0.0;
   const Variant& v = vs[p.variant];
   if (v.gen == 3) return persistent_time_estimate(v, g, p, hw);
+  if (v.gen == 5) return streaming_time_estimate(v, g, p, hw);
   // the register kernel's structural model ranks its own plans; for comparisons with other
   // kernels the fitted figure bounds it from below
   if (v.gen == 4) return std::max(pwpw4_time_estimate(v, g, p, hw), linear_time_estimate(v, g, p));
@@ -639,7 +684,25 @@ static fcm_status search(const Geom& g, const fcm_desc* d, const fcm_hw_desc& hw
     const Variant& v = vs[vi];
     if (!variant_matches(v, g)) continue;
     if (!in_set(v, kset)) continue;
-    if (v.gen == 5) continue;  // explicit plans only (no time model yet)
+    if (v.gen == 5) {
+      // streaming kernels: one compiled tile and output-channel block each
+      Cand c;
+      memset(&c.p, 0, sizeof(c.p));
+      c.p.op = g.op;
+      c.p.tile_h = v.tile_h;
+      c.p.tile_w = v.tile_w;
+      c.p.c_block = 64 / g.elt;
+      c.p.co_block = v.max_cob;
+      c.p.variant = vi;
+      if (evaluate_plan(g, d, hw, &c.p) != FCM_OK) continue;
+      c.bytes = c.p.bytes_tiled;
+      c.wgs = c.p.workgroups;
+      c.lds = c.p.lds_bytes;
+      c.area = v.tile_h * v.tile_w;
+      c.cap = v.max_cob * 1024 + v.max_p;
+      cands.push_back(c);
+      continue;
+    }
     if (v.gen == 4) {
       const int nch = ceil_div(g.cm * g.elt, 64);
       for (int sp = 1; sp <= std::min(4, nch); sp *= 2) {
@@ -747,21 +810,24 @@ static fcm_status search(const Geom& g, const fcm_desc* d, const fcm_hw_desc& hw
       return FCM_OK;
     }
   }
-  // The persistent kernels (gen 3) are preferred wherever one implements the shape; among
-  // them the tiling with the least estimated time wins (see persistent_time_estimate).
+  // The persistent (gen 3) and streaming (gen 5) kernels are preferred wherever one
+  // implements the shape; among them the plan with the least estimated time under its
+  // kernel family's fitted model wins (persistent_time_estimate, streaming_time_estimate).
   {
-    const Cand* best3 = nullptr;
+    const Cand* best35 = nullptr;
     double best_t = 0;
     for (const Cand& c : cands) {
-      if (vs[c.p.variant].gen != 3) continue;
-      const double t = persistent_time_estimate(vs[c.p.variant], g, c.p, hw);
-      if (!best3 || t < best_t || (t == best_t && c.p.variant < best3->p.variant)) {
-        best3 = &c;
+      const int gen = vs[c.p.variant].gen;
+      if (gen != 3 && gen != 5) continue;
+      const double t = gen == 3 ? persistent_time_estimate(vs[c.p.variant], g, c.p, hw)
+                                : streaming_time_estimate(vs[c.p.variant], g, c.p, hw);
+      if (!best35 || t < best_t || (t == best_t && c.p.variant < best35->p.variant)) {
+        best35 = &c;
         best_t = t;
       }
     }
-    if (best3) {
-      *best_out = best3->p;
+    if (best35) {
+      *best_out = best35->p;
       return FCM_OK;
     }
   }

@@ -204,6 +204,18 @@ fcm_status fcm_plan(int32_t op, const fcm_desc* desc, const fcm_hw_desc* hw, fcm
 fcm_status fcm_plan_limited(int32_t op, const fcm_desc* desc, const fcm_hw_desc* hw,
                             int64_t max_workspace_bytes, fcm_plan_t* out);
 
+/* The planner's candidate plans for a module, for callers that time them on the device
+ * and keep the fastest (Sec. IV runs FusePlanner offline; this hands it the measured
+ * choice). Writes at most max_count plans (> 0) to out (HOST array, caller-owned) and
+ * their number to *count: out[0] is fcm_plan_limited's choice, then the fastest plan of
+ * each other compiled kernel variant under the planner's time models, then the remaining
+ * plans, fastest first. Every plan needs at most max_workspace_bytes of caller workspace
+ * and can be passed to the module's entry point unchanged. FCM_EINVAL for NULL pointers,
+ * max_count <= 0 or a negative limit; the descriptor errors of fcm_plan. */
+fcm_status fcm_plan_candidates(int32_t op, const fcm_desc* desc, const fcm_hw_desc* hw,
+                               int64_t max_workspace_bytes, fcm_plan_t* out, int32_t max_count,
+                               int32_t* count);
+
 /* Evaluate a caller-chosen tiling (plan->op, tile_h, tile_w, c_block, co_block,
  * variant) without searching: fills every other field, or fails with
  * FCM_EUNSUPPORTED if no compiled kernel implements it. */

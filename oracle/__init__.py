@@ -88,6 +88,8 @@ def _lib():
         lib.orc_f32_from_bf16.argtypes = [ctypes.c_uint16]
         lib.orc_f32_from_bf16.restype = ctypes.c_float
         lib.orc_num_threads.restype = ctypes.c_int
+        lib.orc_set_num_threads.argtypes = [ctypes.c_int]
+        lib.orc_set_num_threads.restype = None
         _lib_handle = lib
     return _lib_handle
 
@@ -276,3 +278,8 @@ def bf16_value(bits):
 def num_threads():
     """Threads the oracle's OpenMP loops use (OMP_NUM_THREADS or all cores)."""
     return int(_lib().orc_num_threads())
+
+
+def set_num_threads(n):
+    """Threads of the oracle's OpenMP loops from now on in this thread (timing only)."""
+    _lib().orc_set_num_threads(int(n))

@@ -355,6 +355,15 @@ int orc_num_threads(void) {
 #endif
 }
 
+/* Threads of the following calls' parallel loops (for timing: 1 = single-threaded). */
+void orc_set_num_threads(int n) {
+#ifdef _OPENMP
+  if (n > 0) omp_set_num_threads(n);
+#else
+  (void)n;
+#endif
+}
+
 /* Single depthwise layer: channels c_in, stage 0 activation/requant. */
 int orc_dw(const orc_desc* d, const void* x, const void* wd, const void* bd, void* y) {
   int st = check_common(d);

@@ -145,3 +145,47 @@ def _module_plan(sub, op):
         return fcm.plan_limited(op, d, 0)  # chain groups run without a split workspace
     except fcm.FcmError:
         return None
+
+
+# ------------------------------------------------------------------------------------
+# One module or layer: the fastest of the planner's candidate plans, timed on the device
+# ------------------------------------------------------------------------------------
+
+def time_calls(torch, calls, launches, repeats=3, stream=None):
+    """Median over `repeats` of the mean microseconds per launch of `launches` launches
+    cycling through `calls` (prepared launches on `stream`), between two events on it."""
+    stream = stream or torch.cuda.current_stream()
+    for f in calls[:3]:
+        f()
+    torch.cuda.synchronize()
+    out = []
+    k = 0
+    for _ in range(repeats):
+        t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t0.record(stream)
+        for _ in range(launches):
+            calls[k % len(calls)]()
+            k += 1
+        t1.record(stream)
+        torch.cuda.synchronize()
+        out.append(1000.0 * t0.elapsed_time(t1) / launches)
+    return sorted(out)[len(out) // 2]
+
+
+def fastest_plan(torch, plans, make_calls, agrees, launches=30, repeats=3):
+    """Time every plan of `plans` (the first is the planner's choice) and return
+    (fastest plan, [(plan, microseconds or None), ...]). make_calls(plan) gives prepared
+    launches over rotating buffers; agrees(plan) runs the plan once and says whether its
+    output matches the planner's choice (bit-exact for int8, within rounding for floats):
+    a plan that does not is never chosen."""
+    timed = []
+    best, best_t = None, None
+    for i, p in enumerate(plans):
+        if i > 0 and not agrees(p):
+            timed.append((p, None))
+            continue
+        t = time_calls(torch, make_calls(p), launches, repeats)
+        timed.append((p, t))
+        if best is None or t < best_t:
+            best, best_t = p, t
+    return best, timed

@@ -318,6 +318,20 @@ fcm_status fcm_plan_limited(int32_t op, const fcm_desc* desc, const fcm_hw_desc*
   return find_plan(op, desc, hw, out, kernel_set(op, desc), max_workspace_bytes);
 }
 
+fcm_status fcm_plan_candidates(int32_t op, const fcm_desc* desc, const fcm_hw_desc* hw, int64_t max_workspace_bytes,
+                               fcm_plan_t* out, int32_t max_count, int32_t* count) {
+  if (!out || !count) return fail(FCM_EINVAL, "output plans or count is NULL");
+  *count = 0;
+  if (max_count <= 0) return fail(FCM_EINVAL, "max_count must be positive");
+  if (max_workspace_bytes < 0) return fail(FCM_EINVAL, "workspace limit must not be negative");
+  fcm_status st = validate(op, desc);
+  if (st != FCM_OK) return st;
+  int n = 0;
+  st = find_candidates(op, desc, hw, kernel_set(op, desc), max_workspace_bytes, out, max_count, &n);
+  *count = n;
+  return st;
+}
+
 fcm_status fcm_plan_evaluate(const fcm_desc* desc, const fcm_hw_desc* hw, fcm_plan_t* plan) {
   if (!plan) return fail(FCM_EINVAL, "plan is NULL");
   fcm_status st = validate(plan->op, desc);

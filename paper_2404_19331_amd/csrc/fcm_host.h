@@ -52,6 +52,10 @@ fcm_status find_plan(int op, const fcm_desc* d, const fcm_hw_desc* hw, fcm_plan_
 
 // Device workspace bytes a (fully evaluated) plan needs: the partial sums of a split plan,
 // 0 for every other plan.
+// Up to max_count plans for the shape: the planner's choice first, then each kernel
+// variant's best plan by the time models, then the rest, fastest first.
+fcm_status find_candidates(int op, const fcm_desc* d, const fcm_hw_desc* hw, int kset, int64_t ws_max,
+                           fcm_plan_t* out, int max_count, int* count);
 int64_t plan_workspace_bytes(const Geom& g, const fcm_plan_t& p);
 
 // Whether a compiled variant stages through LDS-DMA (needs 16-byte aligned tensors).

@@ -327,7 +327,7 @@ struct Variant {
                     //    run-time tile, max_p = 64 * blocks per wave
                     // 4: PW -> PW with the intermediate in registers, one pixel group per
                     //    wave (max_p = 16 * blocks), all output channels, no LDS
-                    // 5: NHWC streaming kernels, run-time tile of at most max_p pixels,
+                    // 5: NHWC streaming kernels, compile-time tile of max_p pixels,
                     //    one compiled output-channel block
   int pitch = 0;    // gen 3: LDS window row pitch in pixels (window width must not exceed it)
   int ks = 1;       // gen 3: 64-byte channel chunks per item; gen 4: 64-byte k-steps of the

@@ -673,13 +673,13 @@ static const int kTiles3[][2] = {{16, 14}, {8, 14}, {7, 14}, {4, 14}, {14, 14}, 
                                  {4, 16},  {2, 14}, {1, 14}, {3, 14}, {5, 14}, {6, 14}, {2, 7},  {4, 7},  {1, 7},
                                  {2, 4},   {4, 4},  {2, 2},  {3, 7},  {6, 7},  {12, 7}};
 
-static fcm_status search(const Geom& g, const fcm_desc* d, const fcm_hw_desc& hw, fcm_plan_t* best_out,
-                         int kset, int64_t ws_max) {
+// Every plan the compiled kernels can run for the shape (within the workspace limit).
+static void collect(const Geom& g, const fcm_desc* d, const fcm_hw_desc& hw, int kset, int64_t ws_max,
+                    std::vector<Cand>& cands) {
   int nv = 0;
   const Variant* vs = all_variants(&nv);
   const int kb = k_block(g.dtype);
   const int last = (g.family == FAM_PWDW || g.family == FAM_DW) ? g.cm : g.co;
-  std::vector<Cand> cands;
   for (int vi = 0; vi < nv; ++vi) {
     const Variant& v = vs[vi];
     if (!variant_matches(v, g)) continue;
@@ -791,6 +791,14 @@ static fcm_status search(const Geom& g, const fcm_desc* d, const fcm_hw_desc& hw
       }
     }
   }
+}
+
+static fcm_status search(const Geom& g, const fcm_desc* d, const fcm_hw_desc& hw, fcm_plan_t* best_out,
+                         int kset, int64_t ws_max) {
+  int nv = 0;
+  const Variant* vs = all_variants(&nv);
+  std::vector<Cand> cands;
+  collect(g, d, hw, kset, ws_max, cands);
   if (cands.empty()) return fail(FCM_EUNSUPPORTED, "plan: no compiled kernel implements this shape");
   // The PW -> PW register kernel (gen 4) is preferred wherever one implements the shape:
   // the plan with the least estimated time, ties to the smaller variant.
@@ -961,6 +969,53 @@ fcm_status find_plan(int op, const fcm_desc* d, const fcm_hw_desc* hw_in, fcm_pl
     g_cache[key] = p;
   }
   *out = p;
+  return FCM_OK;
+}
+
+static bool same_plan(const fcm_plan_t& a, const fcm_plan_t& b) {
+  return a.variant == b.variant && a.tile_h == b.tile_h && a.tile_w == b.tile_w && a.c_block == b.c_block &&
+         a.co_block == b.co_block && a.depth == b.depth && a.splits == b.splits && a.workgroups == b.workgroups;
+}
+
+fcm_status find_candidates(int op, const fcm_desc* d, const fcm_hw_desc* hw_in, int kset, int64_t ws_max,
+                           fcm_plan_t* out, int max_count, int* count) {
+  *count = 0;
+  const fcm_hw_desc hw = hw_in ? *hw_in : default_hw();
+  fcm_plan_t best;
+  fcm_status st = find_plan(op, d, &hw, &best, kset, ws_max);
+  if (st != FCM_OK) return st;
+  const Geom g = geometry(op, d);
+  std::vector<Cand> cands;
+  collect(g, d, hw, kset, ws_max, cands);
+  // each variant's fastest plan by the time models first (so that a mispredicted kernel
+  // family still gets timed), then the remaining plans, fastest first
+  std::vector<std::pair<double, int>> order;
+  for (int i = 0; i < (int)cands.size(); ++i) order.push_back({plan_time_estimate(g, cands[i].p, hw), i});
+  std::stable_sort(order.begin(), order.end());
+  std::vector<int> firsts, rest;
+  std::vector<char> seen_variant(1024, 0);
+  for (const auto& o : order) {
+    if (same_plan(cands[o.second].p, best)) continue;
+    const int v = cands[o.second].p.variant;
+    if (v >= 0 && v < 1024 && !seen_variant[v]) {
+      seen_variant[v] = 1;
+      firsts.push_back(o.second);
+    } else {
+      rest.push_back(o.second);
+    }
+  }
+  firsts.insert(firsts.end(), rest.begin(), rest.end());
+  int n = 0;
+  if (max_count > 0) out[n++] = best;  // the planner's own choice leads
+  for (int i : firsts) {
+    if (n >= max_count) break;
+    fcm_plan_t p = cands[i].p;
+    p.bytes_lbl_paper = best.bytes_lbl_paper;
+    p.bytes_lbl_ideal = best.bytes_lbl_ideal;
+    p.fuse = (op == FCM_OP_DW || op == FCM_OP_PW) ? 0 : (p.bytes_paper < p.bytes_lbl_paper ? 1 : 0);
+    out[n++] = p;
+  }
+  *count = n;
   return FCM_OK;
 }
 

@@ -138,6 +138,8 @@ def lib():
         L.fcm_dw_pw_noalloc.restype = ctypes.c_int
         L.fcm_plan_limited.argtypes = [ctypes.c_int32, dp, hp, i64, pp]
         L.fcm_plan_limited.restype = ctypes.c_int
+        L.fcm_plan_candidates.argtypes = [ctypes.c_int32, dp, hp, i64, pp, ctypes.c_int32, ctypes.POINTER(ctypes.c_int32)]
+        L.fcm_plan_candidates.restype = ctypes.c_int
         L.fcm_workspace_bytes.restype = i64
         for f in (L.fcm_plan, L.fcm_plan_evaluate, L.fcm_dw_pw, L.fcm_pw_dw, L.fcm_pw_dw_pw,
                   L.fcm_pw_pw, L.fcm_dw, L.fcm_pw):
@@ -233,6 +235,15 @@ def plan_limited(op, desc, max_workspace_bytes, hw=None):
     _check(lib().fcm_plan_limited(OP[op], ctypes.byref(desc), ctypes.byref(hw) if hw else None,
                                   int(max_workspace_bytes), ctypes.byref(p)))
     return p
+
+
+def plan_candidates(op, desc, max_count=12, max_workspace_bytes=0, hw=None):
+    """The planner's candidate plans, its own choice first (fcm_plan_candidates)."""
+    arr = (Plan * max_count)()
+    n = ctypes.c_int32(0)
+    _check(lib().fcm_plan_candidates(OP[op], ctypes.byref(desc), ctypes.byref(hw) if hw else None,
+                                     int(max_workspace_bytes), arr, max_count, ctypes.byref(n)))
+    return [arr[i] for i in range(n.value)]
 
 
 def plan_time_estimate(desc, plan, hw=None):
@@ -525,50 +536,54 @@ def _zp_out(r):
 
 
 def dw_then_pw(x, w_dw, w_pw, b_dw=None, b_pw=None, *, stride=1, pad=None, act=("none", "none"), rq=None,
-               layout="nchw", mid=None, out=None, stream=None, prepare=False, zp_in=0):
+               layout="nchw", mid=None, out=None, stream=None, prepare=False, zp_in=0, plans=(None, None),
+               workspace=None):
+    """DW then PW as two kernels (the intermediate through device memory); `plans` are
+    the stages' plans (None: the planner's), `workspace` the PW stage's (split plans)."""
     rq = list(rq) if rq else [None, None]
     c1 = dw(x, w_dw, b_dw, stride=stride, pad=pad, act=act[0], rq=rq[0], layout=layout, out=mid, stream=stream,
-            prepare=prepare, zp_in=zp_in)
+            prepare=prepare, zp_in=zp_in, plan=plans[0])
     m = c1.y if prepare else c1
     c2 = pw(m, w_pw, b_pw, act=act[1], rq=rq[1], layout=layout, out=out, stream=stream, prepare=prepare,
-            zp_in=_zp_out(rq[0]))
+            zp_in=_zp_out(rq[0]), plan=plans[1], workspace=workspace)
     return _Chain([c1, c2]) if prepare else c2
 
 
 def pw_then_dw(x, w_pw, w_dw, b_pw=None, b_dw=None, *, stride=1, pad=None, act=("none", "none"), rq=None,
-               layout="nchw", mid=None, out=None, stream=None, prepare=False, zp_in=0):
+               layout="nchw", mid=None, out=None, stream=None, prepare=False, zp_in=0, plans=(None, None),
+               workspace=None):
     rq = list(rq) if rq else [None, None]
     c1 = pw(x, w_pw, b_pw, act=act[0], rq=rq[0], layout=layout, out=mid, stream=stream, prepare=prepare,
-            zp_in=zp_in)
+            zp_in=zp_in, plan=plans[0], workspace=workspace)
     m = c1.y if prepare else c1
     c2 = dw(m, w_dw, b_dw, stride=stride, pad=pad, act=act[1], rq=rq[1], layout=layout, out=out, stream=stream,
-            prepare=prepare, zp_in=_zp_out(rq[0]))
+            prepare=prepare, zp_in=_zp_out(rq[0]), plan=plans[1])
     return _Chain([c1, c2]) if prepare else c2
 
 
 def pw_then_pw(x, w_pw1, w_pw2, b_pw1=None, b_pw2=None, *, act=("none", "none"), rq=None, layout="nchw",
-               mid=None, out=None, stream=None, prepare=False, zp_in=0):
+               mid=None, out=None, stream=None, prepare=False, zp_in=0, plans=(None, None), workspace=None):
     rq = list(rq) if rq else [None, None]
     c1 = pw(x, w_pw1, b_pw1, act=act[0], rq=rq[0], layout=layout, out=mid, stream=stream, prepare=prepare,
-            zp_in=zp_in)
+            zp_in=zp_in, plan=plans[0], workspace=workspace)
     m = c1.y if prepare else c1
     c2 = pw(m, w_pw2, b_pw2, act=act[1], rq=rq[1], layout=layout, out=out, stream=stream, prepare=prepare,
-            zp_in=_zp_out(rq[0]))
+            zp_in=_zp_out(rq[0]), plan=plans[1], workspace=workspace)
     return _Chain([c1, c2]) if prepare else c2
 
 
 def pw_then_dw_then_pw(x, w_pw1, w_dw, w_pw2, b_pw1=None, b_dw=None, b_pw2=None, *, stride=1, pad=None,
                        act=("none", "none", "none"), rq=None, layout="nchw", mids=(None, None), out=None,
-                       stream=None, prepare=False, zp_in=0):
+                       stream=None, prepare=False, zp_in=0, plans=(None, None, None), workspace=None):
     rq = list(rq) if rq else [None, None, None]
     c1 = pw(x, w_pw1, b_pw1, act=act[0], rq=rq[0], layout=layout, out=mids[0], stream=stream, prepare=prepare,
-            zp_in=zp_in)
+            zp_in=zp_in, plan=plans[0], workspace=workspace)
     m1 = c1.y if prepare else c1
     c2 = dw(m1, w_dw, b_dw, stride=stride, pad=pad, act=act[1], rq=rq[1], layout=layout, out=mids[1],
-            stream=stream, prepare=prepare, zp_in=_zp_out(rq[0]))
+            stream=stream, prepare=prepare, zp_in=_zp_out(rq[0]), plan=plans[1])
     m2 = c2.y if prepare else c2
     c3 = pw(m2, w_pw2, b_pw2, act=act[2], rq=rq[2], layout=layout, out=out, stream=stream, prepare=prepare,
-            zp_in=_zp_out(rq[1]))
+            zp_in=_zp_out(rq[1]), plan=plans[2], workspace=workspace)
     return _Chain([c1, c2, c3]) if prepare else c3
 
 

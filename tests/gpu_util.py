@@ -161,3 +161,25 @@ def run_chain(spec, objective, x, ws, bs, upto=None):
                        zp_in=getattr(spec, "zp_in", 0))
     p = fcm.chain_plan(d, objective)
     return fcm.chain_run(d, p, x, ws[:len(layers)], bs[:len(layers)]), p
+
+
+def assert_close_dev(got, ref, dtype, what=""):
+    """assert_close on the device: got is the HIP path's output tensor, ref the oracle's
+    (numpy, storage format); the same tolerances."""
+    t = torch()
+    r = t.from_numpy(values(ref, dtype).astype(np.float32)).to(got.device)
+    g = got.float()
+    assert tuple(g.shape) == tuple(r.shape), (tuple(g.shape), tuple(r.shape))
+    if dtype == "i8":
+        bad = int((g != r).sum().item())
+        assert bad == 0, "%s: %d int8 mismatches" % (what, bad)
+        return
+    assert bool(t.isfinite(g).all()), "%s: non-finite output" % what
+    if dtype == "f32":
+        tol = F32_ATOL + F32_RTOL * r.abs()
+    else:
+        rms = t.sqrt(t.mean(r.double() * r.double())).float() if r.numel() else t.zeros((), device=r.device)
+        tol = BF16_RTOL * t.maximum(r.abs(), rms)
+    ratio = float(((g - r).abs() / tol.clamp_min(1e-30)).max().item()) if r.numel() else 0.0
+    print("%s: max |err| / tolerance = %.3f" % (what, ratio))
+    assert ratio <= 1.0, "%s: outside tolerance (max err / tol = %.3f)" % (what, ratio)

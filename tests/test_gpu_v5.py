@@ -7,6 +7,8 @@ overlaps the next item's copies, across image borders, ragged tiles, ragged chan
 (input channels not a multiple of the 64-byte chunk) and ragged output-channel blocks.
 Compared with the CPU oracle at the bf16 tolerance.
 """
+import re
+
 import pytest
 
 from paper_2404_19331_amd import fcm
@@ -42,8 +44,8 @@ def _v5_plans(case):
         if not name.startswith(("k_dwpw5<", "k_pw5<", "k_dw5<")):
             continue
         th, tw = [int(t) for t in name.split(",")[3].split("x")]
-        cob = 32 if name.startswith("k_dw5<") else \
-            16 * int(name.split("ct")[1].split(",")[0]) * int(name.split("wc")[1].split(">")[0])
+        m = re.search(r"ct(\d+),wc(\d+)", name)
+        cob = 32 if name.startswith("k_dw5<") else 16 * int(m.group(1)) * int(m.group(2))
         for cap in CAPS:
             try:
                 p = fcm.plan_evaluate(case.op, desc, th, tw, 32, cob, v, workgroups=cap)

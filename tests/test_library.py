@@ -429,3 +429,45 @@ def test_plan_limited_respects_the_workspace_budget():
                 r = fcm.plan_limited(case.op, d, fcm.workspace_bytes(d, p))
                 assert (r.variant, r.tile_h, r.tile_w, r.splits) == (p.variant, p.tile_h, p.tile_w, p.splits)
     assert found, "no workload layer is planned with a split"
+
+
+def _same(p, q):
+    return (p.variant, p.tile_h, p.tile_w, p.c_block, p.co_block, p.depth, p.splits, p.workgroups) == (
+        q.variant, q.tile_h, q.tile_w, q.c_block, q.co_block, q.depth, q.splits, q.workgroups)
+
+
+@pytest.mark.parametrize("wl", ["C1", "C2", "C3b1", "C3b32", "C4", "C5", "PWPW"])
+def test_plan_candidates_lead_with_the_planners_choice(wl):
+    """fcm_plan_candidates: the workspace-limited planner's plan first, distinct plans,
+    each within the workspace limit and reproduced by fcm_plan_evaluate."""
+    for case in bench.workload_cases(wl)[0]:
+        d = fcm.desc_from_case(case)
+        for ws in (0, 64 << 20):
+            cands = fcm.plan_candidates(case.op, d, 12, ws)
+            assert 1 <= len(cands) <= 12
+            assert _same(cands[0], fcm.plan_limited(case.op, d, ws))
+            for i, p in enumerate(cands):
+                assert fcm.workspace_bytes(d, p) <= ws
+                assert not any(_same(p, q) for q in cands[:i])
+                e = fcm.plan_evaluate(case.op, d, p.tile_h, p.tile_w, p.c_block, p.co_block, p.variant,
+                                      workgroups=p.workgroups, depth=p.depth, splits=p.splits)
+                assert (e.bytes_tiled, e.lds_bytes, e.workgroups) == (p.bytes_tiled, p.lds_bytes, p.workgroups)
+        # each compiled variant that implements the layer appears before any variant repeats
+        cands = fcm.plan_candidates(case.op, d, 64, 0)
+        seen, repeated = set(), False
+        for p in cands[1:]:
+            if p.variant in seen:
+                repeated = True
+            else:
+                assert not repeated, "a new variant after a repeated one"
+                seen.add(p.variant)
+
+
+def test_plan_candidates_rejects_bad_arguments():
+    d = fcm.desc_from_case(bench.workload_cases("C1")[0][0])
+    arr = (fcm.Plan * 4)()
+    n = ctypes.c_int32(7)
+    assert fcm.lib().fcm_plan_candidates(fcm.OP["dw_pw"], ctypes.byref(d), None, 0, arr, 0, ctypes.byref(n)) == 1
+    assert n.value == 0
+    assert fcm.lib().fcm_plan_candidates(fcm.OP["dw_pw"], ctypes.byref(d), None, -1, arr, 4, ctypes.byref(n)) == 1
+    assert fcm.lib().fcm_plan_candidates(fcm.OP["dw_pw"], ctypes.byref(d), None, 0, None, 4, ctypes.byref(n)) == 1

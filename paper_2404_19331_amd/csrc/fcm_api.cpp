@@ -47,7 +47,8 @@ const Variant* all_variants(int* count) {
                                      variants_v3_dwpw_i8, variants_v3_pw, variants_v3_pw_f32, variants_v3_pw_i8,
                                      variants_v3_dw_bf16, variants_v3_dw_f32, variants_v3_dw_i8,
                                      variants_v4_pwpw_i8, variants_v4_pwpw_bf16, variants_v4_pwpw_f32,
-                                     variants_v5_dwpw_bf16_s1, variants_v5_dwpw_bf16_s2, variants_v5_pwdw_bf16};
+                                     variants_v5_dwpw_bf16_s1, variants_v5_dwpw_bf16_s2, variants_v5_pwdw_bf16,
+                                     variants_v6_f32};
     for (auto fn : fns) {
       int n = 0;
       const Variant* t = fn(&n);

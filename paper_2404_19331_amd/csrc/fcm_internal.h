@@ -274,6 +274,58 @@ FCM_HD constexpr Lds5 lds5(int dt, int mode, int K, int IH, int IW, int COB, int
   return L;
 }
 
+// Whole-module fp32 kernels for small batches (k_small6): module selector and the LDS
+// layout, in floats, for the run-time channel counts (host and device compute it alike).
+enum { M6_DWPW = 0, M6_PWDW = 1, M6_PWDWPW = 2 };
+struct Lds6 {
+  int cip, px;        // input channels rounded up to 16; row pitch of the window
+  int nqp;            // window positions rounded up to 16
+  int cmp;            // first PW's output rows rounded up to 16 (0 without one)
+  int cdp, pd;        // depthwise channels rounded up to 16; row pitch of D
+  int np;             // tile pixels rounded up to 16
+  int cop;            // last PW's output rows rounded up to 16 (0 without one)
+  int xs, w1, b1, wd, bd, es, ds, w2, b2, red;  // offsets
+  int floats;         // total
+};
+FCM_HD inline Lds6 lds6(int mode, int K, int S, int TH, int TW, int ci, int cm, int co) {
+  Lds6 L{};
+  const bool pw1 = mode != M6_DWPW, pw2 = mode != M6_PWDW;
+  const int IH = (TH - 1) * S + K, IW = (TW - 1) * S + K, nq = IH * IW, p = TH * TW;
+  const int cd = pw1 ? cm : ci;
+  L.cip = round_up(ci, 16);
+  L.px = L.cip + 4;
+  L.nqp = round_up(nq, 16);
+  L.cmp = pw1 ? round_up(cm, 16) : 0;
+  L.cdp = round_up(cd, 16);
+  L.pd = L.cdp + 4;
+  L.np = round_up(p, 16);
+  L.cop = pw2 ? round_up(co, 16) : 0;
+  int off = 0;
+  auto take = [&](int n) {
+    const int o = off;
+    off += round_up(n, 4);
+    return o;
+  };
+  L.xs = take(L.nqp * L.px);
+  L.w1 = take(pw1 ? L.cmp * ci + 16 : 0);  // [cm][ci] as stored, rows up to cmp, 16 zeros after cm rows
+  L.b1 = take(L.cmp);
+  L.wd = take(cd * K * K);
+  L.bd = take(cd);
+  L.es = take(pw1 ? L.cmp * L.nqp : 0);  // [cmp][nqp]
+  L.ds = take(pw2 ? L.np * L.pd : 0);
+  L.w2 = take(pw2 ? L.cop * cd + 16 : 0);  // [co][cd] as stored, likewise
+  L.b2 = take(L.cop);
+  {
+    // partial sums of the last PW: [split][pair][2][pixel tile][64 lanes x 4]
+    const int npt = (p + 15) / 16, npair = (L.cop / 16 + 1) / 2, cdp16 = L.cdp / 16;
+    int nsplit = npair > 0 ? 4 / npair : 1;
+    nsplit = nsplit < 1 ? 1 : (nsplit > cdp16 ? cdp16 : nsplit);
+    L.red = take(pw2 && nsplit > 1 ? nsplit * npair * 2 * npt * 256 : 0);
+  }
+  L.floats = off;
+  return L;
+}
+
 // ---------------------------------------------------------------------------------
 // Kernel argument block (one struct for all families; unused fields ignored).
 // ---------------------------------------------------------------------------------
@@ -329,6 +381,8 @@ struct Variant {
                     //    wave (max_p = 16 * blocks), all output channels, no LDS
                     // 5: NHWC streaming kernels, compile-time tile of max_p pixels,
                     //    one compiled output-channel block
+                    // 6: fp32 whole-module kernels for small batches: compile-time tile,
+                    //    every channel of every stage in one workgroup
   int pitch = 0;    // gen 3: LDS window row pitch in pixels (window width must not exceed it)
   int ks = 1;       // gen 3: 64-byte channel chunks per item; gen 4: 64-byte k-steps of the
                     // first convolution held in registers (input channels <= 64 * ks bytes);
@@ -345,6 +399,7 @@ const Variant* variants_pwdw(int* count);
 const Variant* variants_v5_dwpw_bf16_s1(int* count);
 const Variant* variants_v5_dwpw_bf16_s2(int* count);
 const Variant* variants_v5_pwdw_bf16(int* count);
+const Variant* variants_v6_f32(int* count);
 const Variant* variants_pwdwpw(int* count);
 const Variant* variants_v3_dwpw_bf16_s1(int* count);
 const Variant* variants_v3_dwpw_bf16_s2(int* count);

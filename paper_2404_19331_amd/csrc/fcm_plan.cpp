@@ -200,11 +200,21 @@ static int tiling_lds(const Variant& v, const Geom& g, int TH, int TW, int CB, i
   const int kb = k_block(g.dtype);
   if (TH <= 0 || TW <= 0 || COB <= 0 || COB % 16) return 0;
   if (v.dw_r && TW % v.dw_r) return 0;
-  if (COB > v.max_cob) return 0;
+  if (v.gen != 6 && COB > v.max_cob) return 0;  // (gen 6: every channel, bounded by LDS)
   const int P = TH * TW;
   const int Q = ((TH - 1) * g.s + g.k) * ((TW - 1) * g.s + g.k);
   if (v.max_p && P > v.max_p) return 0;
   if (v.gen < 3 && v.max_q && Q > v.max_q) return 0;
+  if (v.gen == 6) {
+    // the compiled tile and every channel of the last convolution in one workgroup
+    const int last = (g.family == FAM_PWDW || g.family == FAM_DW) ? g.cm : g.co;
+    if (TH != v.tile_h || TW != v.tile_w || COB != round_up(last, 16)) return 0;
+    // flat 16-byte weight copies: input and depthwise channels in fours
+    if (g.ci % 4 || (g.family != FAM_DWPW && g.cm % 4)) return 0;
+    const int mode = g.family == FAM_DWPW ? M6_DWPW : (g.family == FAM_PWDW ? M6_PWDW : M6_PWDWPW);
+    const int64_t bytes = 4 * (int64_t)lds6(mode, g.k, g.s, TH, TW, g.ci, g.cm, g.co).floats;
+    return bytes > lds_per_wg ? lds_per_wg + 1 : (int)bytes;
+  }
   if (v.gen == 5) {
     // NHWC, 16-byte input channel rows, 32-bit buffer offsets, 64-byte chunk, run-time
     // tile of at most max_p pixels whose window fits the kernel's copy list
@@ -700,6 +710,25 @@ static void collect(const Geom& g, const fcm_desc* d, const fcm_hw_desc& hw, int
       c.lds = c.p.lds_bytes;
       c.area = v.tile_h * v.tile_w;
       c.cap = v.max_cob * 1024 + v.max_p;
+      cands.push_back(c);
+      continue;
+    }
+    if (v.gen == 6) {
+      // whole-module kernels: one compiled tile, every channel
+      Cand c;
+      memset(&c.p, 0, sizeof(c.p));
+      c.p.op = g.op;
+      c.p.tile_h = v.tile_h;
+      c.p.tile_w = v.tile_w;
+      c.p.c_block = 16;
+      c.p.co_block = round_up(last, 16);
+      c.p.variant = vi;
+      if (evaluate_plan(g, d, hw, &c.p) != FCM_OK) continue;
+      c.bytes = c.p.bytes_tiled;
+      c.wgs = c.p.workgroups;
+      c.lds = c.p.lds_bytes;
+      c.area = v.tile_h * v.tile_w;
+      c.cap = v.max_p;
       cands.push_back(c);
       continue;
     }

@@ -647,6 +647,33 @@ static double linear_time_estimate(const Variant& v, const Geom& g, const fcm_pl
   return us * 1e-6;
 }
 
+// Time model of the whole-module fp32 kernels (gen 6), in seconds: the launch, then as
+// many rounds of workgroups as the LDS lets the CUs hold; a workgroup costs a fixed part
+// (its loads' latency and the stage barriers), the busiest wave's MFMA instructions and its
+// share of the window elements it stages. Cycle figures fitted (non-negative least
+// squares) to the eight C1 / C2 tilings timed on MI355X (within 0.8-1.15x).
+static double small_time_estimate(const Variant& v, const Geom& g, const fcm_plan_t& p, const fcm_hw_desc& hw) {
+  constexpr double kLaunch = 1.6e-6, kFixed = 9254.0, kPerMfma = 112.3, kPerWindowElt = 329.7, kClock = 2.4e9;
+  const int TH = v.tile_h, TW = v.tile_w;
+  const int IW = (TW - 1) * g.s + g.k, IH = (TH - 1) * g.s + g.k;
+  const int nqt = ceil_div(IH * IW, 16), npt = ceil_div(TH * TW, 16);
+  const bool pw1 = g.family == FAM_PWDW || g.family == FAM_PWDWPW;
+  const bool pw2 = g.family == FAM_DWPW || g.family == FAM_PWDWPW;
+  const int cd = pw1 ? g.cm : g.ci;
+  const int ci16 = ceil_div(g.ci, 16), cd16 = ceil_div(cd, 16);
+  double mfma = 0;
+  if (pw1) mfma += (double)ceil_div(ceil_div(g.cm, 16), 4) * nqt * ci16 * 4;
+  if (pw2) {
+    const int npair = ceil_div(ceil_div(g.co, 16), 2);
+    const int nsplit = std::max(1, std::min(4 / npair, cd16));
+    mfma += (double)ceil_div(npair * nsplit, 4) * 2 * npt * ceil_div(cd16, nsplit) * 4;
+  }
+  const double xpt = ceil_div(IH * IW * ci16 * 16, 256);
+  const int per_cu = std::max(1, std::min(8, (int)(hw.lds_per_cu / std::max(1, (int)p.lds_bytes))));
+  const double rounds = std::ceil((double)std::max(1, (int)p.workgroups) / ((double)per_cu * hw.num_cus));
+  return kLaunch + rounds * (kFixed + kPerMfma * mfma + kPerWindowElt * xpt) / kClock;
+}
+
 double plan_time_estimate(const Geom& g, const fcm_plan_t& p, const fcm_hw_desc& hw) {
   int nv = 0;
   const Variant* vs = all_variants(&nv);
@@ -654,6 +681,7 @@ double plan_time_estimate(const Geom& g, const fcm_plan_t& p, const fcm_hw_desc&
   const Variant& v = vs[p.variant];
   if (v.gen == 3) return persistent_time_estimate(v, g, p, hw);
   if (v.gen == 5) return streaming_time_estimate(v, g, p, hw);
+  if (v.gen == 6) return small_time_estimate(v, g, p, hw);
   // the register kernel's structural model ranks its own plans; for comparisons with other
   // kernels the fitted figure bounds it from below
   if (v.gen == 4) return std::max(pwpw4_time_estimate(v, g, p, hw), linear_time_estimate(v, g, p));
@@ -847,17 +875,16 @@ static fcm_status search(const Geom& g, const fcm_desc* d, const fcm_hw_desc& hw
       return FCM_OK;
     }
   }
-  // The persistent (gen 3) and streaming (gen 5) kernels are preferred wherever one
-  // implements the shape; among them the plan with the least estimated time under its
-  // kernel family's fitted model wins (persistent_time_estimate, streaming_time_estimate).
+  // The persistent (gen 3), streaming (gen 5) and whole-module (gen 6) kernels are
+  // preferred wherever one implements the shape; among them the plan with the least
+  // estimated time under its kernel family's fitted model wins.
   {
     const Cand* best35 = nullptr;
     double best_t = 0;
     for (const Cand& c : cands) {
       const int gen = vs[c.p.variant].gen;
-      if (gen != 3 && gen != 5) continue;
-      const double t = gen == 3 ? persistent_time_estimate(vs[c.p.variant], g, c.p, hw)
-                                : streaming_time_estimate(vs[c.p.variant], g, c.p, hw);
+      if (gen != 3 && gen != 5 && gen != 6) continue;
+      const double t = plan_time_estimate(g, c.p, hw);
       if (!best35 || t < best_t || (t == best_t && c.p.variant < best35->p.variant)) {
         best35 = &c;
         best_t = t;

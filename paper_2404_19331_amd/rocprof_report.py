@@ -3,7 +3,7 @@
   python -m paper_2404_19331_amd.rocprof_report stats KERNEL_STATS_CSV [--title T] [--command C]
       per-kernel launch statistics (from `rocprofv3 --kernel-trace --stats`) as a text table
 
-  python -m paper_2404_19331_amd.rocprof_report traffic --workload W --variant NAME
+  python -m paper_2404_19331_amd.rocprof_report traffic --workload W --variant NAME [--kernel SYMBOL]
           --fetch COUNTER_CSV --write COUNTER_CSV [--calib-bytes B] [--out profiles/traffic.json]
       HBM bytes per launch of one compiled variant from two `rocprofv3 --pmc` runs of
       `bench.py --calib` (FETCH_SIZE, then WRITE_SIZE). Each counter is scaled by what it
@@ -11,6 +11,17 @@
       B bytes that reads B and writes B bytes), so the unit and the coverage of the counter
       cancel out. The entry is keyed by workload and variant and stamped with the hash of
       the kernel sources; bench.py reports it only while the sources are unchanged.
+      --kernel gives the demangled kernel name (as the stats table prints it) for variants
+      whose name kernel_symbol does not map.
+
+  python -m paper_2404_19331_amd.rocprof_report layers --manifest MANIFEST_JSON --fetch CSV
+          --write CSV --mfma CSV --trace KERNEL_TRACE_CSV [--title T] [--command C]
+      per-layer table of a `profile_layers` run: for the fused module and for its two
+      unfused stages, the mean launch time, the HBM bytes per launch (FETCH_SIZE and
+      WRITE_SIZE scaled by the calibration copy that precedes each layer) against the
+      planner's figures (bytes_ideal: input + weights + output once; bytes_tiled: per-tile
+      staging; bytes_paper: Eq. 1-4), and the matrix-core busy fraction
+      (SQ_VALU_MFMA_BUSY_CYCLES over 1024 SIMDs x 2.4 GHz x the launch time).
 """
 import argparse
 import csv
@@ -27,12 +38,23 @@ _DT = {"f32": "TF32", "bf16": "TBF16", "i8": "TI8"}
 
 
 def kernel_symbol(variant, split=False):
-    """Demangled kernel name of a persistent variant, e.g. k_dwpw3<bf16,3,1,1,16,p16> ->
+    """Demangled kernel name of a variant: persistent, e.g. k_dwpw3<bf16,3,1,1,16,p16> ->
     void fcm::k_fused3<fcm::TBF16, 3, 1, 1, 16, 0, 16, 1, false>(fcm::KArgs) (the instance
-    of unsplit plans; split=True names the one of split plans)."""
+    of unsplit plans; split=True names the one of split plans); streaming (k_dwpw5<...>) and
+    whole-module (k_dwpw6<...>) variants map to their single instance."""
+    m5 = re.match(r"(k_\w+5)<(\w+),(\d+),(\d+),(\d+)x(\d+),ct(\d+),wc(\d+)>$", variant)
+    if m5:  # streaming kernels: k_fused5<DT, K, S, MODE, TH, TW, CTW, WC>
+        fam, dt, k, s, th, tw, ct, wc = m5.groups()
+        mode = {"k_dwpw5": 0, "k_pw5": 1, "k_dw5": 2}[fam]
+        return "void fcm::k_fused5<fcm::%s, %s, %s, %d, %s, %s, %s, %s>(fcm::KArgs)" % (_DT[dt], k, s, mode, th, tw, ct, wc)
+    m6 = re.match(r"(k_\w+6)<f32,(\d+),(\d+),(\d+)x(\d+)>$", variant)
+    if m6:  # whole-module fp32 kernels: k_small6<MODE, K, S, TH, TW>
+        fam, k, s, th, tw = m6.groups()
+        mode = {"k_dwpw6": 0, "k_pwdw6": 1, "k_pwdwpw6": 2}[fam]
+        return "void fcm::k_small6<%d, %s, %s, %s, %s>(fcm::KArgs)" % (mode, k, s, th, tw)
     m = re.match(r"(k_\w+3)<(\w+),(\d+),(\d+),(\d+),(\d+),p(\d+)(?:,k(\d+))?>$", variant)
     if not m:
-        raise ValueError("not a persistent-kernel variant name: %s" % variant)
+        raise ValueError("not a persistent, streaming or whole-module kernel variant name: %s" % variant)
     fam, dt, k, s, bpw, ct, pitch, ks = m.groups()
     if fam == "k_pw3":
         k = s = "1"
@@ -71,7 +93,7 @@ def _mean(vals, name, counter):
 
 
 def traffic(args):
-    sym = kernel_symbol(args.variant, args.split)
+    sym = args.kernel or kernel_symbol(args.variant, args.split)
     fv, fg = read_counters(args.fetch)
     wv, wg = read_counters(args.write)
     f_k, w_k = _mean(fv, sym, "FETCH_SIZE"), _mean(wv, sym, "WRITE_SIZE")
@@ -94,6 +116,89 @@ def traffic(args):
         json.dump(rec, f, indent=1, sort_keys=True)
         f.write("\n")
     print(json.dumps(ent))
+
+
+def _dispatches(path, field="counter"):
+    """[(dispatch id, kernel name, {counter: value} or duration ns)] in dispatch order."""
+    with open(path) as f:
+        rows = list(csv.DictReader(f))
+    if field == "trace":
+        out = [(int(r["Dispatch_Id"]), r["Kernel_Name"], int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
+               for r in rows]
+        return sorted(out)
+    by = {}
+    for r in rows:
+        d = by.setdefault(int(r["Dispatch_Id"]), [r["Kernel_Name"], {}])
+        d[1][r["Counter_Name"]] = d[1].get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+    return sorted((k, v[0], v[1]) for k, v in by.items())
+
+
+def _segments(disp, nlayers, reps):
+    """Per layer: (calibration dispatches, fused, dw, pw) of a profile_layers run: each
+    layer starts with three calibration copies (MulFunctor) followed by 3 x reps launches."""
+    out, i = [], 0
+    for _ in range(nlayers):
+        while i < len(disp) and "MulFunctor" not in disp[i][1]:
+            i += 1
+        cal = disp[i:i + 3]
+        body = disp[i + 3:i + 3 + 3 * reps]
+        if len(cal) < 3 or len(body) < 3 * reps:
+            raise SystemExit("dispatch sequence shorter than the manifest says")
+        out.append((cal, body[:reps], body[reps:2 * reps], body[2 * reps:]))
+        i += 3 + 3 * reps
+    return out
+
+
+def layers(args):
+    with open(args.manifest) as f:
+        man = json.load(f)
+    reps, nl, cb = man["reps"], len(man["layers"]), man["calib_bytes"]
+    fetch = _segments(_dispatches(args.fetch), nl, reps)
+    write = _segments(_dispatches(args.write), nl, reps)
+    mfma = _segments(_dispatches(args.mfma), nl, reps)
+    trace = _segments(_dispatches(args.trace, "trace"), nl, reps)
+
+    def mean(xs):
+        xs = xs[1:] if len(xs) > 2 else xs  # the first launch of a group warms the instruction cache
+        return sum(xs) / len(xs)
+
+    out = []
+    if args.title:
+        out.append(args.title)
+    if args.command:
+        out.append("commands:\n" + args.command)
+    out.append("")
+    out.append("HBM MB = (FETCH_SIZE + WRITE_SIZE) per launch, scaled by the calibration copy of %d MiB "
+               "(read and written) preceding each layer; ideal = input + weights + output once; tiled = the "
+               "planner's per-tile staging bytes; paper = Eq. 1-4; MFMA = matrix-core busy fraction." % (cb >> 20))
+    out.append("%-34s %-34s %7s %7s %7s %7s %7s %6s %5s | %7s %7s %7s %5s" % (
+        "layer", "fused kernel", "us", "HBM_MB", "ideal", "tiled", "paper", "HBM/id", "MFMA",
+        "unf_us", "unf_HBM", "unf_id", "HBM/id"))
+    rows = []
+    for li, L in enumerate(man["layers"]):
+        res = {}
+        for role, k in (("fused", 1), ("dw", 2), ("pw", 3)):
+            fcal = mean([d[2]["FETCH_SIZE"] for d in fetch[li][0]])
+            wcal = mean([d[2]["WRITE_SIZE"] for d in write[li][0]])
+            rb = mean([d[2]["FETCH_SIZE"] for d in fetch[li][k]]) / fcal * cb
+            wb = mean([d[2]["WRITE_SIZE"] for d in write[li][k]]) / wcal * cb
+            us = mean([d[2] for d in trace[li][k]]) / 1e3
+            busy = mean([d[2].get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0) for d in mfma[li][k]])
+            res[role] = {"us": us, "hbm": rb + wb, "read": rb, "write": wb,
+                         "mfma": busy / (1024 * us * 1e3 * 2.4), "kernel": fetch[li][k][0][1]}
+        f, dwr, pwr = res["fused"], res["dw"], res["pw"]
+        fi, ui = L["fused"]["bytes_ideal"], L["dw"]["bytes_ideal"] + L["pw"]["bytes_ideal"]
+        uhbm = dwr["hbm"] + pwr["hbm"]
+        out.append("%-34s %-34s %7.2f %7.2f %7.2f %7.2f %7.2f %6.2f %5.2f | %7.2f %7.2f %7.2f %5.2f" % (
+            L["layer"][:34], L["fused"]["variant"][:34], f["us"], f["hbm"] / 1e6, fi / 1e6,
+            L["fused"]["bytes_tiled"] / 1e6, L["fused"]["bytes_paper"] / 1e6, f["hbm"] / fi, f["mfma"],
+            dwr["us"] + pwr["us"], uhbm / 1e6, ui / 1e6, uhbm / ui))
+        rows.append({"layer": L["layer"], "fused": dict(f, plan=L["fused"]), "dw": dict(dwr, plan=L["dw"]),
+                     "pw": dict(pwr, plan=L["pw"])})
+    print("\n".join(out))
+    if args.json:
+        with open(args.json, "w") as fh:
+            json.dump(rows, fh, indent=1)
 
 
 def stats(args):
@@ -130,8 +235,18 @@ def main():
     t.add_argument("--split", action="store_true", help="the split-plan instance of the variant")
     t.add_argument("--calib-bytes", type=int, default=256 << 20)
     t.add_argument("--out", default=os.path.join(ROOT, "profiles", "traffic.json"))
+    t.add_argument("--kernel", default="", help="demangled kernel name (default: from the variant name)")
+    l = sub.add_parser("layers")
+    l.add_argument("--manifest", required=True)
+    l.add_argument("--fetch", required=True)
+    l.add_argument("--write", required=True)
+    l.add_argument("--mfma", required=True)
+    l.add_argument("--trace", required=True)
+    l.add_argument("--title", default="")
+    l.add_argument("--command", default="")
+    l.add_argument("--json", default="")
     a = ap.parse_args()
-    (stats if a.cmd == "stats" else traffic)(a)
+    {"stats": stats, "traffic": traffic, "layers": layers}[a.cmd](a)
 
 
 if __name__ == "__main__":

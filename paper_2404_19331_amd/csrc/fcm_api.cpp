@@ -48,7 +48,7 @@ const Variant* all_variants(int* count) {
                                      variants_v3_dw_bf16, variants_v3_dw_f32, variants_v3_dw_i8,
                                      variants_v4_pwpw_i8, variants_v4_pwpw_bf16, variants_v4_pwpw_f32,
                                      variants_v5_dwpw_bf16_s1, variants_v5_dwpw_bf16_s2, variants_v5_pwdw_bf16,
-                                     variants_v6_f32};
+                                     variants_v6_f32, variants_v7_bf16};
     for (auto fn : fns) {
       int n = 0;
       const Variant* t = fn(&n);
@@ -266,7 +266,7 @@ static fcm_status run(int op, const fcm_desc* d, const Tensors& t, const fcm_pla
     a.vec_w2 = aligned16(t.w[1]) && (g.cm * e) % 16 == 0;
   }
   a.cus = device_cus();
-  a.grid_cap = (v.gen == 3 || v.gen == 5) ? p.workgroups : 0;
+  a.grid_cap = (v.gen == 3 || v.gen == 5 || v.gen == 7) ? p.workgroups : 0;
   a.depth = p.depth;
   if (v.gen >= 2) {
     a.L = LdsLayout{};

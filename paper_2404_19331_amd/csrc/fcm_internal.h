@@ -274,6 +274,31 @@ FCM_HD constexpr Lds5 lds5(int dt, int mode, int K, int IH, int IW, int COB, int
   return L;
 }
 
+// Deep DW->PW kernels (k_deep7, bf16, 3x3): LDS bytes. Three ring slots of the haloed
+// window and two depthwise output exchange buffers, both as four planes of 8 channels
+// (16 bytes per position: a wave reading one plane at consecutive positions touches every
+// bank once), the PW bias block of 64 * CTW channels (fp32), and all C input channels'
+// depthwise weights ([C][3][3] bf16) and biases (fp32), each in whole KiB. Window
+// positions are rounded up to 64 (one LDS-DMA copy fills 64 positions of one plane).
+struct Lds7 {
+  int nqp, win_plane, win_bytes, exch_off, exch_plane, exch_bytes, pwb_off, dww_off, dwb_off, total;
+};
+FCM_HD constexpr Lds7 lds7(int S, int TH, int TW, int CTW, int C) {
+  Lds7 L{};
+  const int IH = (TH - 1) * S + 3, IW = (TW - 1) * S + 3;
+  L.nqp = round_up(IH * IW, 64);
+  L.win_plane = 16 * L.nqp;
+  L.win_bytes = 4 * L.win_plane;
+  L.exch_off = 3 * L.win_bytes;
+  L.exch_plane = (TH * TW + 15) / 16 * 16 * 16;
+  L.exch_bytes = 4 * L.exch_plane;
+  L.pwb_off = L.exch_off + 2 * L.exch_bytes;
+  L.dww_off = L.pwb_off + round_up(64 * CTW * 4, 1024);
+  L.dwb_off = L.dww_off + round_up(C * 18, 1024);
+  L.total = L.dwb_off + round_up(C * 4, 1024);
+  return L;
+}
+
 // Whole-module fp32 kernels for small batches (k_small6): module selector and the LDS
 // layout, in floats, for the run-time channel counts (host and device compute it alike).
 enum { M6_DWPW = 0, M6_PWDW = 1, M6_PWDWPW = 2 };
@@ -383,6 +408,8 @@ struct Variant {
                     //    one compiled output-channel block
                     // 6: fp32 whole-module kernels for small batches: compile-time tile,
                     //    every channel of every stage in one workgroup
+                    // 7: deep DW->PW kernels (bf16, 3x3): compile-time tile of at most 64
+                    //    pixels, one compiled output-channel block
   int pitch = 0;    // gen 3: LDS window row pitch in pixels (window width must not exceed it)
   int ks = 1;       // gen 3: 64-byte channel chunks per item; gen 4: 64-byte k-steps of the
                     // first convolution held in registers (input channels <= 64 * ks bytes);
@@ -400,6 +427,7 @@ const Variant* variants_v5_dwpw_bf16_s1(int* count);
 const Variant* variants_v5_dwpw_bf16_s2(int* count);
 const Variant* variants_v5_pwdw_bf16(int* count);
 const Variant* variants_v6_f32(int* count);
+const Variant* variants_v7_bf16(int* count);
 const Variant* variants_pwdwpw(int* count);
 const Variant* variants_v3_dwpw_bf16_s1(int* count);
 const Variant* variants_v3_dwpw_bf16_s2(int* count);

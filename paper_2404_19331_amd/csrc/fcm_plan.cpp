@@ -215,6 +215,18 @@ static int tiling_lds(const Variant& v, const Geom& g, int TH, int TW, int CB, i
     const int64_t bytes = 4 * (int64_t)lds6(mode, g.k, g.s, TH, TW, g.ci, g.cm, g.co).floats;
     return bytes > lds_per_wg ? lds_per_wg + 1 : (int)bytes;
   }
+  if (v.gen == 7) {
+    // NHWC, input channels in whole 32-channel chunks, whole 16-byte output granules,
+    // images and weights below 2^30 bytes (32-bit buffer offsets with room for an
+    // out-of-range scalar part), the compiled tile and channel block
+    if (g.layout != FCM_NHWC || g.family != FAM_DWPW) return 0;
+    if (g.ci % 32 || (g.co * g.elt) % 16) return 0;
+    if ((int64_t)g.h * g.w * g.ci * g.elt >= ((int64_t)1 << 30)) return 0;
+    if ((int64_t)g.ho * g.wo * g.co * g.elt >= ((int64_t)1 << 30)) return 0;
+    if ((int64_t)(g.co + COB) * g.ci * g.elt >= ((int64_t)1 << 30)) return 0;
+    if (CB != 64 / g.elt || COB != v.max_cob || TH != v.tile_h || TW != v.tile_w) return 0;
+    return lds7(g.s, TH, TW, v.max_cob / 64, g.ci).total;
+  }
   if (v.gen == 5) {
     // NHWC, 16-byte input channel rows, 32-bit buffer offsets, 64-byte chunk, run-time
     // tile of at most max_p pixels whose window fits the kernel's copy list
@@ -379,17 +391,19 @@ fcm_status evaluate_plan(const Geom& g, const fcm_desc* d, const fcm_hw_desc& hw
   if (wgs <= 0 || wgs > 0x7fffffff) return fail(FCM_EUNSUPPORTED, "plan: grid too large");
   const Bytes b = module_bytes(g, p->tile_h, p->tile_w, p->co_block);
   if (v.gen != 3 && p->splits > 1) return fail(FCM_EUNSUPPORTED, "plan: this kernel variant does not split");
-  if (v.gen == 5) {
+  if (v.gen == 5 || v.gen == 7) {
     // persistent: the workgroups resident at once (LDS-limited estimate; the launcher
     // also applies the compiled kernel's register-limited occupancy), at most one per
     // work tile; a caller's cap is kept
-    const int64_t per_cu = std::max<int64_t>(1, std::min<int64_t>(8, hw.lds_per_cu / lds));
+    // (the deep kernels' eight waves hold every VGPR of a CU: one workgroup per CU)
+    const int64_t per_cu =
+        v.gen == 7 ? 1 : std::max<int64_t>(1, std::min<int64_t>(8, hw.lds_per_cu / lds));
     int64_t grid = std::min<int64_t>(wgs, per_cu * hw.num_cus);
     if (p->workgroups > 0 && p->workgroups < grid) grid = p->workgroups;
     p->workgroups = (int32_t)grid;
     p->depth = v.ks;
     p->splits = 1;
-    p->waves = 4;
+    p->waves = v.gen == 7 ? 8 : 4;
     p->lds_bytes = lds;
     p->bytes_ideal = b.ideal;
     p->bytes_tiled = b.tiled;
@@ -674,6 +688,26 @@ static double small_time_estimate(const Variant& v, const Geom& g, const fcm_pla
   return kLaunch + rounds * (kFixed + kPerMfma * mfma + kPerWindowElt * xpt) / kClock;
 }
 
+// Time model of the deep DW->PW kernels (gen 7), in seconds: the launch with the first
+// loads and the last stores, then each workgroup's items (tile x 32-channel chunk) one
+// after another, an item costing a fixed part, the window copies of a depthwise wave and
+// the MFMA wave's output tiles (cycles fitted to MobileNetV1 layers 6-13 at batch 1 and 32
+// and the 14x14 token grid), scaled by the workgroups sharing a CU; never faster than the
+// module's HBM bytes.
+static double deep_time_estimate(const Variant& v, const Geom& g, const fcm_plan_t& p, const fcm_hw_desc& hw) {
+  constexpr double kLaunch = 3.0e-6, kItem = 600.0, kPerCopy = 250.0, kPerTile = 200.0, kClock = 2.4e9;
+  const int ctw = v.max_cob / 64;
+  const int iw = (v.tile_w - 1) * g.s + 3, ih = (v.tile_h - 1) * g.s + 3;
+  const int copies = ceil_div(ih * iw, 64);
+  const int nch = ceil_div(g.ci, 32);
+  const int64_t nwork = (int64_t)g.n * ceil_div(g.ho, v.tile_h) * ceil_div(g.wo, v.tile_w) * ceil_div(g.co, v.max_cob);
+  const int grid = std::max(1, (int)p.workgroups);
+  const double items = (double)ceil_div(nwork, (int64_t)grid) * nch;
+  const double share = std::max(1.0, (double)grid / hw.num_cus);
+  const double cyc = items * (kItem + kPerCopy * copies + kPerTile * ctw) * share;
+  return std::max(kLaunch + cyc / kClock, (double)p.bytes_ideal / 5.0e12);
+}
+
 double plan_time_estimate(const Geom& g, const fcm_plan_t& p, const fcm_hw_desc& hw) {
   int nv = 0;
   const Variant* vs = all_variants(&nv);
@@ -682,6 +716,7 @@ double plan_time_estimate(const Geom& g, const fcm_plan_t& p, const fcm_hw_desc&
   if (v.gen == 3) return persistent_time_estimate(v, g, p, hw);
   if (v.gen == 5) return streaming_time_estimate(v, g, p, hw);
   if (v.gen == 6) return small_time_estimate(v, g, p, hw);
+  if (v.gen == 7) return deep_time_estimate(v, g, p, hw);
   // the register kernel's structural model ranks its own plans; for comparisons with other
   // kernels the fitted figure bounds it from below
   if (v.gen == 4) return std::max(pwpw4_time_estimate(v, g, p, hw), linear_time_estimate(v, g, p));
@@ -722,8 +757,8 @@ static void collect(const Geom& g, const fcm_desc* d, const fcm_hw_desc& hw, int
     const Variant& v = vs[vi];
     if (!variant_matches(v, g)) continue;
     if (!in_set(v, kset)) continue;
-    if (v.gen == 5) {
-      // streaming kernels: one compiled tile and output-channel block each
+    if (v.gen == 5 || v.gen == 7) {
+      // streaming and deep kernels: one compiled tile and output-channel block each
       Cand c;
       memset(&c.p, 0, sizeof(c.p));
       c.p.op = g.op;
@@ -883,7 +918,7 @@ static fcm_status search(const Geom& g, const fcm_desc* d, const fcm_hw_desc& hw
     double best_t = 0;
     for (const Cand& c : cands) {
       const int gen = vs[c.p.variant].gen;
-      if (gen != 3 && gen != 5 && gen != 6) continue;
+      if (gen != 3 && gen != 5 && gen != 6 && gen != 7) continue;
       const double t = plan_time_estimate(g, c.p, hw);
       if (!best35 || t < best_t || (t == best_t && c.p.variant < best35->p.variant)) {
         best35 = &c;

@@ -582,16 +582,22 @@ def cpu_baseline(cases, target_s):
             "c1_single_thread_ms": round(1e3 * t_c1, 3)}
 
 
-def load_traffic(workload, kernel_name):
-    """HBM bytes per launch of a kernel from the rocprofv3 FETCH_SIZE / WRITE_SIZE runs
-    (profiles/traffic.json), only if they were taken on the current kernel sources."""
+def layer_shape(c):
+    """Geometry of a layer (what a kernel's traffic per launch depends on), as text."""
+    return "n%d %dx%d %d->%d k%d s%d" % (c.n, c.h, c.w, c.c_in, c.c_out, c.k, c.stride)
+
+
+def load_traffic(workload, kernel_name, shape):
+    """HBM bytes per launch of a kernel on layers of one shape, from the rocprofv3 FETCH_SIZE /
+    WRITE_SIZE runs (profiles/traffic.json), only if they were taken on the current kernel
+    sources and on that shape."""
     path = os.path.join(ROOT, "profiles", "traffic.json")
     if not os.path.exists(path):
         return None
     with open(path) as f:
         rec = json.load(f)
     ent = rec.get("%s|%s" % (workload, kernel_name))
-    if not ent or ent.get("source_hash") != kernel_source_hash():
+    if not ent or ent.get("source_hash") != kernel_source_hash() or ent.get("shape") != shape:
         return None
     return ent.get("bytes_per_launch")
 
@@ -668,14 +674,15 @@ def main():
 
     tot_bytes = sum(L.stats["bytes"] for L in layers)
     value = tot_bytes / (fused_ms * 1e-3) / 1e9
-    # dominant kernel: the compiled kernel (variant) taking the largest share of the fused
-    # step; its achieved rate = its algorithmic bytes (flops) per launch / its mean launch
-    # duration, over every layer it runs (each layer is launched equally often).
+    # dominant kernel: the compiled kernel (variant) on one layer shape taking the largest
+    # share of the fused step; its achieved rate = its algorithmic bytes (flops) per launch
+    # / its mean launch duration over those layers (each layer is launched equally often).
     groups = {}
     for i, L in enumerate(layers):
-        groups.setdefault(int(L.plan.variant), []).append(i)
-    dv = max(groups, key=lambda v: sum(fused_us[i] for i in groups[v]))
-    idx = groups[dv]
+        groups.setdefault((int(L.plan.variant), layer_shape(L.case)), []).append(i)
+    dkey = max(groups, key=lambda k: sum(fused_us[i] for i in groups[k]))
+    dv, dshape = dkey
+    idx = groups[dkey]
     t_us = sum(fused_us[i] for i in idx)
     g_bytes = sum(layers[i].stats["bytes"] for i in idx)
     g_flops = sum(layers[i].stats["flops"] for i in idx)
@@ -693,7 +700,8 @@ def main():
     rf["layers"] = [layers[i].case.name for i in idx]
     rf["bytes_per_launch"] = int(g_bytes / len(idx))
     rf["us_per_launch"] = round(t_us / len(idx), 3)
-    rf["traffic"] = load_traffic(a.workload, kname)
+    rf["shape"] = dshape
+    rf["traffic"] = load_traffic(a.workload, kname, dshape)
 
     per_layer = [layer_entry(fcm, L, fu, uu, ho) for L, fu, uu, ho in zip(layers, fused_us, unf_us, hot_us)]
     out = {

@@ -172,20 +172,35 @@ def time_calls(torch, calls, launches, repeats=3, stream=None):
     return sorted(out)[len(out) // 2]
 
 
-def fastest_plan(torch, plans, make_calls, agrees, launches=30, repeats=3):
+def fastest_plan(torch, plans, make_calls, agrees, launches=30, repeats=5, margin=0.05):
     """Time every plan of `plans` (the first is the planner's choice) and return
     (fastest plan, [(plan, microseconds or None), ...]). make_calls(plan) gives prepared
     launches over rotating buffers; agrees(plan) runs the plan once and says whether its
     output matches the planner's choice (bit-exact for int8, within rounding for floats):
-    a plan that does not is never chosen."""
+    a plan that does not is never chosen. The plans are timed in turn, `repeats` rounds,
+    each plan's median kept (drift over the rounds falls on every plan alike); another plan
+    replaces the planner's choice only when it is faster by more than `margin` (relative),
+    so that timing noise between near-equal plans does not change the choice from run to
+    run."""
+    calls = []
+    for i, p in enumerate(plans):
+        calls.append(None if i > 0 and not agrees(p) else make_calls(p))
+    samples = [[] for _ in plans]
+    for _ in range(repeats):
+        for i, c in enumerate(calls):
+            if c is not None:
+                samples[i].append(time_calls(torch, c, launches, 1))
     timed = []
     best, best_t = None, None
     for i, p in enumerate(plans):
-        if i > 0 and not agrees(p):
+        if calls[i] is None:
             timed.append((p, None))
             continue
-        t = time_calls(torch, make_calls(p), launches, repeats)
+        t = sorted(samples[i])[len(samples[i]) // 2]
         timed.append((p, t))
         if best is None or t < best_t:
             best, best_t = p, t
+    t0 = timed[0][1]
+    if best is not plans[0] and best_t > t0 * (1.0 - margin):
+        best = plans[0]
     return best, timed

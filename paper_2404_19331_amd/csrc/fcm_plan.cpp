@@ -400,6 +400,10 @@ fcm_status evaluate_plan(const Geom& g, const fcm_desc* d, const fcm_hw_desc& hw
         v.gen == 7 ? 1 : std::max<int64_t>(1, std::min<int64_t>(8, hw.lds_per_cu / lds));
     int64_t grid = std::min<int64_t>(wgs, per_cu * hw.num_cus);
     if (p->workgroups > 0 && p->workgroups < grid) grid = p->workgroups;
+    if (v.gen == 7) {  // as launched: a multiple of the output-channel blocks
+      const int64_t ncb = ceil_div(g.co, p->co_block);
+      grid = std::max<int64_t>(ncb, grid - grid % ncb);
+    }
     p->workgroups = (int32_t)grid;
     p->depth = v.ks;
     p->splits = 1;
@@ -691,21 +695,23 @@ static double small_time_estimate(const Variant& v, const Geom& g, const fcm_pla
 // Time model of the deep DW->PW kernels (gen 7), in seconds: the launch with the first
 // loads and the last stores, then each workgroup's items (tile x 32-channel chunk) one
 // after another, an item costing a fixed part, the window copies of a depthwise wave and
-// the MFMA wave's output tiles (cycles fitted to MobileNetV1 layers 6-13 at batch 1 and 32
-// and the 14x14 token grid), scaled by the workgroups sharing a CU; never faster than the
-// module's HBM bytes.
+// the MFMA wave's output tiles, and each work tile its epilogue, scaled by the workgroups
+// sharing a CU; or the module's HBM bytes at the rate these kernels reach, if slower
+// (cycles and rate fitted to MobileNetV1 layers 1-13 at batch 1 and 32 and the token
+// grids at batch 64).
 static double deep_time_estimate(const Variant& v, const Geom& g, const fcm_plan_t& p, const fcm_hw_desc& hw) {
-  constexpr double kLaunch = 3.0e-6, kItem = 600.0, kPerCopy = 250.0, kPerTile = 200.0, kClock = 2.4e9;
+  constexpr double kLaunch = 3.5e-6, kItem = 800.0, kPerCopy = 250.0, kPerTile = 100.0, kPerWork = 1000.0,
+                   kClock = 2.4e9, kRate = 3.0e12;
   const int ctw = v.max_cob / 64;
   const int iw = (v.tile_w - 1) * g.s + 3, ih = (v.tile_h - 1) * g.s + 3;
   const int copies = ceil_div(ih * iw, 64);
   const int nch = ceil_div(g.ci, 32);
   const int64_t nwork = (int64_t)g.n * ceil_div(g.ho, v.tile_h) * ceil_div(g.wo, v.tile_w) * ceil_div(g.co, v.max_cob);
   const int grid = std::max(1, (int)p.workgroups);
-  const double items = (double)ceil_div(nwork, (int64_t)grid) * nch;
+  const double tiles = (double)ceil_div(nwork, (int64_t)grid);
   const double share = std::max(1.0, (double)grid / hw.num_cus);
-  const double cyc = items * (kItem + kPerCopy * copies + kPerTile * ctw) * share;
-  return std::max(kLaunch + cyc / kClock, (double)p.bytes_ideal / 5.0e12);
+  const double cyc = (tiles * nch * (kItem + kPerCopy * copies + kPerTile * ctw) + tiles * kPerWork) * share;
+  return kLaunch + std::max(cyc / kClock, (double)p.bytes_ideal / kRate);
 }
 
 double plan_time_estimate(const Geom& g, const fcm_plan_t& p, const fcm_hw_desc& hw) {

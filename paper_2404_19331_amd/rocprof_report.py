@@ -40,13 +40,16 @@ _DT = {"f32": "TF32", "bf16": "TBF16", "i8": "TI8"}
 def kernel_symbol(variant, split=False):
     """Demangled kernel name of a variant: persistent, e.g. k_dwpw3<bf16,3,1,1,16,p16> ->
     void fcm::k_fused3<fcm::TBF16, 3, 1, 1, 16, 0, 16, 1, false>(fcm::KArgs) (the instance
-    of unsplit plans; split=True names the one of split plans); streaming (k_dwpw5<...>) and
-    whole-module (k_dwpw6<...>) variants map to their single instance."""
+    of unsplit plans; split=True names the one of split plans); streaming (k_dwpw5<...>),
+    whole-module (k_dwpw6<...>) and deep (k_dwpw7<...>) variants map to their single instance."""
     m5 = re.match(r"(k_\w+5)<(\w+),(\d+),(\d+),(\d+)x(\d+),ct(\d+),wc(\d+)>$", variant)
     if m5:  # streaming kernels: k_fused5<DT, K, S, MODE, TH, TW, CTW, WC>
         fam, dt, k, s, th, tw, ct, wc = m5.groups()
         mode = {"k_dwpw5": 0, "k_pw5": 1, "k_dw5": 2}[fam]
         return "void fcm::k_fused5<fcm::%s, %s, %s, %d, %s, %s, %s, %s>(fcm::KArgs)" % (_DT[dt], k, s, mode, th, tw, ct, wc)
+    m7 = re.match(r"k_dwpw7<bf16,3,(\d+),(\d+)x(\d+),ct(\d+)>$", variant)
+    if m7:  # deep kernels: k_deep7<S, TH, TW, CTW>
+        return "void fcm::k_deep7<%s, %s, %s, %s>(fcm::KArgs)" % m7.groups()
     m6 = re.match(r"(k_\w+6)<f32,(\d+),(\d+),(\d+)x(\d+)>$", variant)
     if m6:  # whole-module fp32 kernels: k_small6<MODE, K, S, TH, TW>
         fam, k, s, th, tw = m6.groups()
@@ -107,6 +110,8 @@ def traffic(args):
            "fetch_kib_per_launch": round(f_k, 1), "write_kib_per_launch": round(w_k, 1),
            "calib_fetch_kib": round(f_c, 1), "calib_write_kib": round(w_c, 1), "calib_bytes": args.calib_bytes,
            "source_hash": bench.kernel_source_hash()}
+    if args.shape:
+        ent["shape"] = args.shape
     rec = {}
     if os.path.exists(args.out):
         with open(args.out) as f:
@@ -236,6 +241,7 @@ def main():
     t.add_argument("--calib-bytes", type=int, default=256 << 20)
     t.add_argument("--out", default=os.path.join(ROOT, "profiles", "traffic.json"))
     t.add_argument("--kernel", default="", help="demangled kernel name (default: from the variant name)")
+    t.add_argument("--shape", default="", help="layer shape the run launched the kernel on (bench.py --layers)")
     l = sub.add_parser("layers")
     l.add_argument("--manifest", required=True)
     l.add_argument("--fetch", required=True)

@@ -35,7 +35,7 @@ int kernel_set(int op, const fcm_desc* d) {
 
 static const char* kset_message(int kset) {
   return kset == KSET_FIRST ? "per-channel requantisation runs on the first-generation kernels only"
-                            : "zero points run on the first-generation and PW->PW register kernels only";
+                            : "zero points run on the first-generation, int8 persistent and PW->PW register kernels only";
 }
 
 const Variant* all_variants(int* count) {

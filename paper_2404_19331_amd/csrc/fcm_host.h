@@ -14,8 +14,9 @@ namespace fcm {
 fcm_status fail(fcm_status st, const std::string& msg);
 
 // Kernel sets a descriptor may run on: the first-generation kernels always; with
-// KSET_DMA every kernel; with KSET_REG only (zero points) also the PW->PW register
-// kernel's instances of at most kZpMaxTiles output tiles.
+// KSET_DMA every kernel; with KSET_REG only (zero points) also the int8 persistent
+// kernels (unsplit plans) and the PW->PW register kernel's instances of at most
+// kZpMaxTiles output tiles.
 enum { KSET_FIRST = 0, KSET_DMA = 1, KSET_REG = 2, KSET_ALL = 3 };
 // The set an int8 descriptor's features allow: per-channel requantisation -> first
 // generation only; zero points -> first generation and the register kernel; else all.

@@ -47,11 +47,12 @@ typedef float f32x2_t __attribute__((ext_vector_type(2)));
 
 // Branch-free epilogue of a convolution stage. Float paths: activation as a clamp to
 // [lo, hi] (NONE: unbounded, RELU: [0, inf), RELU6: [0, 6]). Int8: requantisation
-// (round half to even of acc * mult / 2^shift) and a clamp to [qlo, qhi], which is the
-// saturation range with ReLU folded in (relu(clamp(q, a, b)) = clamp(q, max(a,0), max(b,0))).
+// (round half to even of acc * mult / 2^shift), plus the output zero point zp, and a clamp
+// to [qlo, qhi]: the saturation range with ReLU at real 0 (code zp) folded in,
+// max(clamp(q, a, b), zp) = clamp(q, max(a, zp), max(b, zp)).
 struct Epi3 {
   float lo, hi;
-  int32_t mult, shift, qlo, qhi;
+  int32_t mult, shift, qlo, qhi, zp;
 };
 __device__ __forceinline__ Epi3 make_epi3(int act, const Requant& rq) {
   Epi3 e;
@@ -59,8 +60,9 @@ __device__ __forceinline__ Epi3 make_epi3(int act, const Requant& rq) {
   e.hi = act == ACT_RELU6 ? 6.0f : __builtin_huge_valf();
   e.mult = rq.mult;
   e.shift = rq.shift;
-  e.qlo = act != ACT_NONE ? max(rq.qmin, 0) : rq.qmin;  // int8 ReLU6: its 6 is qmax
-  e.qhi = act != ACT_NONE ? max(rq.qmax, 0) : rq.qmax;
+  e.zp = rq.zp;
+  e.qlo = act != ACT_NONE ? max(rq.qmin, rq.zp) : rq.qmin;  // int8 ReLU6: its 6 is qmax
+  e.qhi = act != ACT_NONE ? max(rq.qmax, rq.zp) : rq.qmax;
   return e;
 }
 __device__ __forceinline__ float epi_f(float v, const Epi3& e) { return __builtin_amdgcn_fmed3f(v, e.lo, e.hi); }
@@ -68,7 +70,7 @@ __device__ __forceinline__ int32_t epi_i(int32_t acc, const Epi3& e) {
   const int64_t t = (int64_t)acc * e.mult;
   const int64_t half = ((int64_t)1 << e.shift) >> 1;
   const int64_t rnd = e.shift > 0 ? half - 1 + ((t >> e.shift) & 1) : 0;
-  int64_t q = (t + rnd) >> e.shift;
+  int64_t q = ((t + rnd) >> e.shift) + e.zp;
   q = q < e.qlo ? e.qlo : q;
   q = q > e.qhi ? e.qhi : q;
   return (int32_t)q;
@@ -180,7 +182,7 @@ __device__ __forceinline__ void wait_vm(int n) {
   }
 }
 
-template <class DT, int K, int S, int BPW, int CT, int MODE, int IWP, int KS, bool SPLIT>
+template <class DT, int K, int S, int BPW, int CT, int MODE, int IWP, int KS, bool SPLIT, bool ZP>
 __global__ __launch_bounds__(kThreads3) void k_fused3(KArgs a) {
   extern __shared__ __align__(16) char smem[];
   using T = typename DT::T;
@@ -290,6 +292,51 @@ __global__ __launch_bounds__(kThreads3) void k_fused3(KArgs a) {
     }
     int iss_slot = 0, iss_wt = wt0, iss_ch = u_lo(wt0), iss_hi = u_hi(wt0);
     Tile iss_t = decode(wt0 / SPL);
+    // Asymmetric int8 input (zero point zin): the window positions outside the image must
+    // hold zin (real 0), not the zeros the copies write there, and each depthwise sum loses
+    // zin x its channel's weight sum (folded into the bias). Once an item's copies have
+    // landed, each copy wave rewrites the out-of-image positions of its own rows, and
+    // wave 0 the item's depthwise biases; a second item iterator follows the issue one.
+    // (Every byte of a ring slot is a copy target, so no item data can ride along in it.)
+    const int zin = (ZP && HAS_DW) ? a.zin[0] : 0;
+    int fx_slot = 0, fx_wt = wt0, fx_ch = u_lo(wt0), fx_hi = u_hi(wt0);
+    Tile fx_t = iss_t;
+    auto fix_next = [&]() {
+      if (!ZP || zin == 0) return;
+      char* buf = bufp(fx_slot);
+      const int iy0 = fx_t.oy0 * SE - a.pad, ix0 = fx_t.ox0 * SE - a.pad;
+      fx_slot = next_slot(fx_slot);
+      if (++fx_ch == fx_hi && ++fx_wt < wt1) {
+        fx_ch = u_lo(fx_wt);
+        fx_hi = u_hi(fx_wt);
+        fx_t = decode(fx_wt / SPL);
+      }
+      if (iy0 < 0 || ix0 < 0 || iy0 + IH > a.H || ix0 + IW > a.W) {
+        const uint32_t fill = zp_fill<DT>(zin);
+        for (int wy = wy0; wy < wy1; ++wy) {
+          const bool rok = (unsigned)(iy0 + wy) < (unsigned)a.H;
+#pragma unroll
+          for (int j = 0; j < IPR; ++j) {
+            const int gx = ix0 + wxl[j];
+            if (rok && wxl[j] >= 0 && (unsigned)gx < (unsigned)a.W) continue;
+#pragma unroll
+            for (int s = 0; s < KS; ++s)
+              *(u32x4*)(buf + s * lay.plane_bytes + (wy * IPR + j) * 1024 + lane * 16) = u32x4{fill, fill, fill, fill};
+          }
+        }
+      }
+      if (wave == 0) {
+#pragma unroll
+        for (int s = 0; s < KS; ++s) {
+          const int8_t* rb = (const int8_t*)(buf + s * lay.plane_bytes + lay.raw_off) + lane * KK;
+          int32_t wsum = 0;
+#pragma unroll
+          for (int t = 0; t < KK; ++t) wsum += rb[t];
+          int32_t* bb = (int32_t*)(buf + lay.bias_off) + s * CB + lane;
+          *bb -= zin * wsum;
+        }
+      }
+    };
     auto issue_next = [&]() {
       char* buf = bufp(iss_slot);
       const int c0 = MODE == M3_DW ? iss_t.cb * CB : iss_ch * (CB * KS);
@@ -400,6 +447,7 @@ __global__ __launch_bounds__(kThreads3) void k_fused3(KArgs a) {
     const int ahead = min(nitems, D - 1);
     for (int i = 0; i < ahead; ++i) issue_next();
     wait_vm((ahead - 1) * mine);
+    fix_next();
     convert(0);
     wait_lgkm0();
     barrier3();
@@ -409,6 +457,7 @@ __global__ __launch_bounds__(kThreads3) void k_fused3(KArgs a) {
       if (it + D - 1 < nitems) issue_next();
       if (it + 1 < nitems) {
         wait_vm((min(nitems, it + D) - (it + 2)) * mine);
+        fix_next();
         convert(cv_slot);
       }
       cv_slot = next_slot(cv_slot);
@@ -436,6 +485,13 @@ __global__ __launch_bounds__(kThreads3) void k_fused3(KArgs a) {
   const int a_row = r16 * kRowB + ((g ^ (((r16 >> 3) & 1) << 1)) * 16);  // swizzled MFMA A slot
   const Epi3 ep_dw = make_epi3(a.act[0], a.rq[0]);
   const Epi3 ep_pw = MODE == M3_PW ? ep_dw : make_epi3(a.act[1], a.rq[1]);
+  // Asymmetric int8 PW input (zero point z_pw): every output channel loses z_pw x its
+  // weight-row sum, which each lane accumulates from its A operands (16 bytes of a row per
+  // chunk) and completes at the epilogue.
+  const int z_pw = (ZP && HAS_PW) ? a.zin[MODE == M3_PW ? 0 : 1] : 0;
+  int32_t rsp[CT];
+#pragma unroll
+  for (int i = 0; i < CT; ++i) rsp[i] = 0;
 
   AccV acc[BPW][CT];
 #pragma unroll
@@ -500,11 +556,23 @@ __global__ __launch_bounds__(kThreads3) void k_fused3(KArgs a) {
         }
         if constexpr (HAS_PW) {
           const char* wl = plane + lay.in_bytes;
+          auto contract = [&](auto rs_tag) {
 #pragma unroll
-          for (int i = 0; i < CT; ++i) {
-            const u32x4 av = *(const u32x4*)(wl + i * 1024 + a_row);
+            for (int i = 0; i < CT; ++i) {
+              const u32x4 av = *(const u32x4*)(wl + i * 1024 + a_row);
 #pragma unroll
-            for (int b = 0; b < NB; ++b) mma16(DT{}, acc[b][i], av, bop[b]);
+              for (int b = 0; b < NB; ++b) mma16(DT{}, acc[b][i], av, bop[b]);
+              if constexpr (decltype(rs_tag)::value) {
+#pragma unroll
+                for (int q = 0; q < 4; ++q) rsp[i] = __builtin_amdgcn_sdot4((int)av[q], 0x01010101, rsp[i], false);
+              }
+            }
+          };
+          if constexpr (ZP && !SPLIT) {
+            if (z_pw != 0) contract(std::true_type{});  // (uniform)
+            else contract(std::false_type{});
+          } else {
+            contract(std::false_type{});
           }
         }
       }
@@ -546,6 +614,26 @@ __global__ __launch_bounds__(kThreads3) void k_fused3(KArgs a) {
 #pragma unroll
           for (int i = 0; i < CT; ++i) acc[b][i] = AccV{0, 0, 0, 0};
       } else {
+        if constexpr (ZP) {
+          if (z_pw != 0) {
+            // row m of tile i: the four lanes l % 16 == m hold its quarters; then each
+            // accumulator lane takes rows 4g + v
+#pragma unroll
+            for (int i = 0; i < CT; ++i) {
+              int32_t s = rsp[i];
+              s += __shfl_xor(s, 16);
+              s += __shfl_xor(s, 32);
+#pragma unroll
+              for (int v = 0; v < 4; ++v) {
+                const int32_t r = __shfl(s, 4 * g + v);
+#pragma unroll
+                for (int b = 0; b < BPW; ++b) acc[b][i][v] -= z_pw * r;
+              }
+            }
+          }
+#pragma unroll
+          for (int i = 0; i < CT; ++i) rsp[i] = 0;
+        }
         // this lane's output granules k = 0 .. CT/OTPG - 1: channels co_blk + OGE * (4k + g) + [0, OGE)
         constexpr int NG = MODE == M3_DW ? 1 : CT / OTPG;
         const int co_blk = cur_t.cb * CoB;
@@ -682,16 +770,21 @@ __global__ __launch_bounds__(256) void k_combine3(KArgs a) {
 template <class DT, int K, int S, int BPW, int CT, int MODE, int IWP, int KS>
 int launch_fused3(const KArgs& a, int grid, void* stream) {
   const bool split = MODE != M3_DW && a.splits > 1;
-  auto fn = split ? k_fused3<DT, K, S, BPW, CT, MODE, IWP, KS, MODE != M3_DW>
-                  : k_fused3<DT, K, S, BPW, CT, MODE, IWP, KS, false>;
+  // the zero-point instance (int8, unsplit) only where an input of the module has one, so
+  // that symmetric int8 runs without its registers
+  constexpr bool kI8 = std::is_same<DT, TI8>::value;
+  const bool zp = kI8 && !split && (a.zin[0] != 0 || (MODE == M3_DWPW && a.zin[1] != 0));
+  auto fn = split ? k_fused3<DT, K, S, BPW, CT, MODE, IWP, KS, MODE != M3_DW, false>
+                  : zp ? k_fused3<DT, K, S, BPW, CT, MODE, IWP, KS, false, kI8>
+                       : k_fused3<DT, K, S, BPW, CT, MODE, IWP, KS, false, false>;
   const int lds = a.L.bytes;
   if (lds > 65536) {
     hipError_t e = hipFuncSetAttribute((const void*)fn, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
     if (e != hipSuccess) return (int)e;
   }
   // persistent grid: as many workgroups as are resident at once, at most one per work unit
-  static thread_local int cached_lds[2] = {-1, -1}, cached_occ[2] = {1, 1};
-  const int ci = split ? 1 : 0;
+  static thread_local int cached_lds[3] = {-1, -1, -1}, cached_occ[3] = {1, 1, 1};
+  const int ci = split ? 1 : zp ? 2 : 0;
   if (cached_lds[ci] != lds) {
     int occ = 0;
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, (const void*)fn, kThreads3, lds) != hipSuccess || occ < 1)

@@ -298,12 +298,14 @@ bool variant_needs_alignment(int variant) {
   return variant >= 0 && variant < nv && vs[variant].gen >= 2;
 }
 
-// Generations 2 and 3 need the full set; the register kernel (4) is also in KSET_REG
-// (zero points) for its instances of at most kZpMaxTiles output tiles.
+// Generations 2 and up need the full set; with zero points (KSET_REG) also the int8
+// persistent kernels (unsplit plans: evaluate_plan) and the register kernel's instances
+// of at most kZpMaxTiles output tiles.
 static bool in_set(const Variant& v, int kset) {
   if (v.gen < 2) return true;
   if (kset & KSET_DMA) return true;
-  return v.gen == 4 && (kset & KSET_REG) && v.max_cob <= 16 * kZpMaxTiles;
+  if (!(kset & KSET_REG)) return false;
+  return (v.gen == 3 && v.dtype == DT_I8) || (v.gen == 4 && v.max_cob <= 16 * kZpMaxTiles);
 }
 
 bool variant_in_set(int variant, int kset) {
@@ -417,6 +419,7 @@ fcm_status evaluate_plan(const Geom& g, const fcm_desc* d, const fcm_hw_desc& hw
   }
   if (v.gen == 3) {
     const int splits = p->splits > 1 ? p->splits : 1;
+    if (splits > 1 && g.zp) return fail(FCM_EUNSUPPORTED, "plan: zero points run on unsplit persistent plans");
     if (splits > 1) {
       if (v.family == FAM_DW) return fail(FCM_EUNSUPPORTED, "plan: a depthwise-only kernel does not split");
       const int ipt = ceil_div(g.ci, v.ks * (64 / g.elt));

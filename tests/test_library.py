@@ -254,11 +254,16 @@ def test_library_binds_to_the_hip_runtime_torch_loads():
 
 
 # --------------------------------------------------------------------------------------
-# Asymmetric int8 (zero points): planned on the first-generation kernels
+# Asymmetric int8 (zero points): planned on the first-generation kernels, the int8
+# persistent kernels (unsplit plans) and the PW->PW register kernel
 # --------------------------------------------------------------------------------------
 
 def _first_gen(v):
     return re.search(r"\d<", fcm.variant_name(v)) is None
+
+
+def _persistent_unsplit(p):
+    return re.match(r"k_(dwpw|dw|pw)3<i8,", fcm.variant_name(p.variant)) is not None and p.splits == 1
 
 
 ZP_SHAPES = {"dw_pw": (64, 64, 64, 3), "pw_dw": (32, 96, 96, 3), "pw_dw_pw": (32, 96, 32, 3),
@@ -273,7 +278,7 @@ def _zp_desc(op, zp_in=0, zps=(0, 0, 0), dtype="i8"):
 
 
 @pytest.mark.parametrize("op", list(ZP_SHAPES))
-def test_zero_points_plan_first_generation_kernels(op):
+def test_zero_points_plan_capable_kernels(op):
     stages = {"pw_dw_pw": 3, "dw": 1, "pw": 1}.get(op, 2)
     sym = fcm.plan(op, _zp_desc(op))
     if op in ("dw_pw", "pw_pw", "dw", "pw"):
@@ -284,6 +289,8 @@ def test_zero_points_plan_first_generation_kernels(op):
         name = fcm.variant_name(p.variant)
         if op == "pw_pw":  # the register kernel carries zero points (up to 192 output channels)
             assert name.startswith("k_pwpw4<i8,"), (zin, zps, name)
+        elif op in ("dw_pw", "dw", "pw"):  # the int8 persistent kernels, unsplit
+            assert _persistent_unsplit(p), (zin, zps, name, p.splits)
         else:
             assert _first_gen(p.variant), (zin, zps, name)
     # a zero point of a stage the module does not have is ignored, as are float types
@@ -315,18 +322,29 @@ def test_zero_points_validation_and_explicit_plans():
         with pytest.raises(fcm.FcmError) as e:
             fcm.plan("dw_pw", _zp_desc("dw_pw", zin, zps))
         assert e.value.status == EINVAL and "zero point" in str(e.value)
-    # an explicit plan on a newer kernel is refused for an asymmetric descriptor
+    # an explicit persistent plan is accepted for an asymmetric descriptor unsplit and
+    # refused split; one on a newer kernel without zero points (PW->DW streaming) is refused
     sym = fcm.plan("dw_pw", _zp_desc("dw_pw"))
-    assert not _first_gen(sym.variant)
+    assert re.match(r"k_dwpw3<i8,", fcm.variant_name(sym.variant))
+    un = fcm.plan_evaluate("dw_pw", _zp_desc("dw_pw", 3), sym.tile_h, sym.tile_w, sym.c_block, sym.co_block,
+                           sym.variant)
+    assert un.splits == 1
     with pytest.raises(fcm.FcmError) as e:
         fcm.plan_evaluate("dw_pw", _zp_desc("dw_pw", 3), sym.tile_h, sym.tile_w, sym.c_block, sym.co_block,
-                          sym.variant)
-    assert e.value.status == EUNSUPPORTED
+                          sym.variant, splits=2)
+    assert e.value.status == EUNSUPPORTED and "zero points" in str(e.value)
+    pd = fcm.plan("pw_dw", _zp_desc("pw_dw"))
+    if not _first_gen(pd.variant):
+        with pytest.raises(fcm.FcmError) as e:
+            fcm.plan_evaluate("pw_dw", _zp_desc("pw_dw", 3), pd.tile_h, pd.tile_w, pd.c_block, pd.co_block,
+                              pd.variant)
+        assert e.value.status == EUNSUPPORTED
 
 
 def test_chain_zero_points_reach_the_groups_they_touch():
-    """A zero point on one layer's output moves to the first-generation kernels exactly the
-    groups that write that tensor or read it; the others keep the symmetric plan."""
+    """A zero point on one layer's output moves to the zero-point kernels (first generation,
+    int8 persistent unsplit) exactly the groups that write that tensor or read it; the
+    others keep the symmetric plan."""
     layers = [dict(kind="pw", c_out=96, act="relu", rq=(1, 6, -128, 127)),
               dict(kind="dw", k=3, stride=1, pad=1, act="relu", rq=(1, 4, -128, 127)),
               dict(kind="pw", c_out=64, act="none", rq=(1, 7, -128, 127)),
@@ -340,12 +358,13 @@ def test_chain_zero_points_reach_the_groups_they_touch():
         p = fcm.chain_plan(fcm.chain_desc(4, 28, 28, 64, zl, "i8"), "unfused")
         for g, (first, op, plan) in enumerate(p.groups()):
             touched = first in (j, j + 1)  # unfused: one layer per group
-            assert _first_gen(plan.variant) or not touched, (j, first)
+            assert _first_gen(plan.variant) or _persistent_unsplit(plan) or not touched, (j, first)
             if not touched:
                 assert plan.as_dict() == sym.plan[g].as_dict()
     # the chain input's zero point reaches the first group only
     p = fcm.chain_plan(fcm.chain_desc(4, 28, 28, 64, layers, "i8", zp_in=-128), "unfused")
-    assert _first_gen(p.plan[0].variant) and p.plan[1].as_dict() == sym.plan[1].as_dict()
+    assert (_first_gen(p.plan[0].variant) or _persistent_unsplit(p.plan[0])) and \
+        p.plan[1].as_dict() == sym.plan[1].as_dict()
 
 
 def test_abi_struct_sizes_match_the_binding(tmp_path):
@@ -367,7 +386,7 @@ def test_zero_point_time_models_are_their_own():
     """First-generation kernels under zero points are priced by their own fitted figures:
     the same plan of the same shapes gets another estimate than symmetric, while a float
     descriptor (zero points ignored) keeps the symmetric one."""
-    for op in ("pw", "dw", "pw_dw_pw"):
+    for op in ("pw_dw", "pw_dw_pw"):
         sym = _zp_desc(op)
         asym = _zp_desc(op, -128, (5, 5, 5))
         p = fcm.plan(op, asym)

@@ -125,14 +125,16 @@ typedef struct {
   /* int8 per-channel requantisation of stage i (NULL = per-tensor rq[i]): DEVICE array of
    * 2 x (the stage's output channels) int32, the multipliers then the shifts (shifts in
    * [0, 62]); the clamp range stays rq[i].qmin / qmax. Such descriptors are planned and
-   * launched on the first-generation kernels only. Ignored for float types. */
+   * launched on the first-generation kernels and on the int8 persistent NHWC kernels
+   * (DW->PW, DW, PW); an explicit plan on another kernel fails with FCM_EUNSUPPORTED.
+   * Ignored for float types. */
   const int32_t* rq_channel[3];
   /* int8 zero point of the input x (the code of real 0, in [-128, 127]); the input of
    * stage i > 0 has the zero point of stage i-1's output, rq[i-1].zero_point. Descriptors
    * with a nonzero zero point anywhere are planned and launched on the first-generation
-   * kernels and on the PW->PW register kernel's instances of at most 192 output channels;
-   * an explicit plan on another kernel fails with FCM_EUNSUPPORTED. Ignored for float
-   * types. */
+   * kernels, on the int8 persistent NHWC kernels and on the PW->PW register kernel's
+   * instances of at most 192 output channels; an explicit plan on another kernel fails
+   * with FCM_EUNSUPPORTED. Ignored for float types. */
   int32_t zp_in;
 } fcm_desc;
 

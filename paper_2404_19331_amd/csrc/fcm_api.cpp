@@ -20,22 +20,28 @@ fcm_status fail(fcm_status st, const std::string& msg) {
   return st;
 }
 
-// int8 features not every kernel implements: per-channel requantisation (first-generation
-// kernels) and zero points (first-generation kernels and the PW->PW register kernel).
-int kernel_set(int op, const fcm_desc* d) {
-  if (!d || d->dtype != FCM_I8) return KSET_ALL;
+void int8_features(int op, const fcm_desc* d, int* zp, int* pc) {
+  *zp = *pc = 0;
+  if (!d || d->dtype != FCM_I8) return;
   const int stages = op == FCM_OP_PW_DW_PW ? 3 : ((op == FCM_OP_DW || op == FCM_OP_PW) ? 1 : 2);
-  bool zp = d->zp_in != 0;
+  *zp = d->zp_in != 0;
   for (int i = 0; i < stages; ++i) {
-    if (d->rq_channel[i]) return KSET_FIRST;
-    zp = zp || d->rq[i].zero_point != 0;
+    if (d->rq_channel[i]) *pc = 1;
+    if (d->rq[i].zero_point != 0) *zp = 1;
   }
-  return zp ? KSET_REG : KSET_ALL;
+}
+
+// int8 features not every kernel implements: per-channel requantisation (first-generation
+// and int8 persistent kernels) and zero points (those and the PW->PW register kernel).
+int kernel_set(int op, const fcm_desc* d) {
+  int zp, pc;
+  int8_features(op, d, &zp, &pc);
+  return pc ? KSET_PC : (zp ? KSET_REG : KSET_ALL);
 }
 
 static const char* kset_message(int kset) {
-  return kset == KSET_FIRST ? "per-channel requantisation runs on the first-generation kernels only"
-                            : "zero points run on the first-generation, int8 persistent and PW->PW register kernels only";
+  return kset == KSET_PC ? "per-channel requantisation runs on the first-generation and int8 persistent kernels only"
+                         : "zero points run on the first-generation, int8 persistent and PW->PW register kernels only";
 }
 
 const Variant* all_variants(int* count) {

@@ -15,12 +15,17 @@ fcm_status fail(fcm_status st, const std::string& msg);
 
 // Kernel sets a descriptor may run on: the first-generation kernels always; with
 // KSET_DMA every kernel; with KSET_REG only (zero points) also the int8 persistent
-// kernels (unsplit plans) and the PW->PW register kernel's instances of at most
+// kernels and the PW->PW register kernel's instances of at most
 // kZpMaxTiles output tiles.
-enum { KSET_FIRST = 0, KSET_DMA = 1, KSET_REG = 2, KSET_ALL = 3 };
-// The set an int8 descriptor's features allow: per-channel requantisation -> first
-// generation only; zero points -> first generation and the register kernel; else all.
+// KSET_PC (per-channel requantisation): the first-generation kernels and the int8
+// persistent kernels only.
+enum { KSET_FIRST = 0, KSET_DMA = 1, KSET_REG = 2, KSET_ALL = 3, KSET_PC = 4 };
+// The set an int8 descriptor's features allow: per-channel requantisation -> KSET_PC;
+// zero points -> KSET_REG; else all.
 int kernel_set(int op, const fcm_desc* d);
+// Whether an int8 descriptor has a nonzero zero point (zp) or per-channel requantisation
+// (pc) in any stage of module `op` (0 and 0 for float types).
+void int8_features(int op, const fcm_desc* d, int* zp, int* pc);
 // Whether compiled variant `variant` belongs to kernel set `kset`.
 bool variant_in_set(int variant, int kset);
 
@@ -37,6 +42,7 @@ struct Geom {
   int dtype, elt;
   int layout;
   int zp;               // int8 with a nonzero zero point in any stage (time models)
+  int pc;               // int8 with per-channel requantisation in any stage
 };
 Geom geometry(int op, const fcm_desc* d);
 

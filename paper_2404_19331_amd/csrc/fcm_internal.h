@@ -175,8 +175,10 @@ enum { M3_DWPW = 0, M3_PW = 1, M3_DW = 2 };
 // the input window of IH rows at a pitch of IWP pixels of 64 bytes; the pointwise weight
 // block (16*CT rows of 64 bytes); the depthwise weights of one chunk as 32-bit
 // dot-operand words [K*K][CB]; the raw depthwise weights as copied ([CB][K*K] elements,
-// whole KiB); and two KiB of biases (depthwise, then pointwise). `depth` buffers form
-// the ring (the copy wave runs depth - 1 items ahead).
+// whole KiB); and two KiB of biases (depthwise, then pointwise). With per-channel int8
+// requantisation (pc) three more KiB follow: the depthwise multipliers and shifts (half
+// a KiB each), then the pointwise multipliers and shifts (a KiB each). `depth` buffers
+// form the ring (the copy wave runs depth - 1 items ahead).
 constexpr int kCopyWaves3 = 2;  // copy waves (each issues about half of an item's copies)
 constexpr int kThreads3 = 64 * (kCopyWaves3 + 4);  // + four compute waves
 constexpr int kMaxDepth3 = 8;   // ring buffers at most
@@ -185,7 +187,7 @@ struct Lds3 {
 };
 // One buffer holds `ks` planes (one per 64-byte channel chunk of the item: window, PW
 // weights, DW dot-operand words, raw DW weights) and then the biases of the item.
-FCM_HD inline Lds3 lds3p(int dt, int K, int mode, int IH, int IWP, int CT, int depth = 2, int ks = 1) {
+FCM_HD inline Lds3 lds3p(int dt, int K, int mode, int IH, int IWP, int CT, int depth = 2, int ks = 1, int pc = 0) {
   Lds3 r;
   const int cb = kRowB / elt_size(dt);
   r.in_bytes = IH * IWP * kRowB;
@@ -197,7 +199,7 @@ FCM_HD inline Lds3 lds3p(int dt, int K, int mode, int IH, int IWP, int CT, int d
   if (mode != M3_PW) off += (64 * K * K + 1023) / 1024 * 1024;
   r.plane_bytes = off;
   r.bias_off = ks * off;
-  r.buf_bytes = r.bias_off + 2048;
+  r.buf_bytes = r.bias_off + (pc ? 2048 + 3072 : 2048);
   r.total = depth * r.buf_bytes;
   return r;
 }
@@ -210,34 +212,36 @@ FCM_HD inline bool splits_valid3(int ipt, int splits) {
 }
 
 // Copy instructions of one item (ks channel chunks) of a persistent kernel (host and
-// device), in issue order: raw DW weights of each chunk and the DW bias, window rows,
-// PW weight rows of each chunk, PW bias.
-FCM_HD inline int copies_per_item3(int mode, int K, int IH, int IWP, int CT, int ks = 1) {
+// device), in issue order: raw DW weights of each chunk and the DW bias (and with pc
+// the DW multipliers and shifts), window rows, PW weight rows of each chunk, PW bias
+// (and with pc the PW multipliers, then shifts).
+FCM_HD inline int ndw_copies3(int mode, int K, int ks, int pc) {
+  return mode != M3_PW ? ks * ((64 * K * K + 1023) / 1024) + 1 + (pc ? 1 : 0) : 0;
+}
+FCM_HD inline int copies_per_item3(int mode, int K, int IH, int IWP, int CT, int ks = 1, int pc = 0) {
   int n = ks * IH * (IWP / 16);
-  if (mode != M3_DW) n += ks * CT + 1;                          // PW weight rows, PW bias
-  if (mode != M3_PW) n += ks * ((64 * K * K + 1023) / 1024) + 1;  // raw DW weights, DW bias
-  return n;
+  if (mode != M3_DW) n += ks * CT + 1 + (pc ? 2 : 0);  // PW weight rows, PW bias (, scales)
+  return n + ndw_copies3(mode, K, ks, pc);
 }
 // Split of an item's copies between the two copy waves: wave 0 issues the DW weights
 // and bias (it converts them) and window rows [0, r0) of every chunk, wave 1 rows
 // [r0, IH), the PW weight rows and the PW bias; r0 balances the two counts.
-FCM_HD inline int rows_wave0_3(int mode, int K, int IH, int IWP, int CT, int ks = 1) {
+FCM_HD inline int rows_wave0_3(int mode, int K, int IH, int IWP, int CT, int ks = 1, int pc = 0) {
   const int ipr = (IWP / 16) * ks;
-  const int ndw = mode != M3_PW ? ks * ((64 * K * K + 1023) / 1024) + 1 : 0;
-  const int t = copies_per_item3(mode, K, IH, IWP, CT, ks);
+  const int ndw = ndw_copies3(mode, K, ks, pc);
+  const int t = copies_per_item3(mode, K, IH, IWP, CT, ks, pc);
   int r0 = (t - 2 * ndw + ipr) / (2 * ipr);
   r0 = r0 < 0 ? 0 : (r0 > IH ? IH : r0);
   return r0;
 }
-FCM_HD inline int copies_wave0_3(int mode, int K, int IH, int IWP, int CT, int ks = 1) {
-  const int ndw = mode != M3_PW ? ks * ((64 * K * K + 1023) / 1024) + 1 : 0;
-  return ndw + rows_wave0_3(mode, K, IH, IWP, CT, ks) * (IWP / 16) * ks;
+FCM_HD inline int copies_wave0_3(int mode, int K, int IH, int IWP, int CT, int ks = 1, int pc = 0) {
+  return ndw_copies3(mode, K, ks, pc) + rows_wave0_3(mode, K, IH, IWP, CT, ks, pc) * (IWP / 16) * ks;
 }
 // The larger per-wave share: a partial wait on the vector-memory counter covers at most
 // 63 outstanding copies of one wave.
-FCM_HD inline int copies_per_wave3(int mode, int K, int IH, int IWP, int CT, int ks = 1) {
-  const int t = copies_per_item3(mode, K, IH, IWP, CT, ks);
-  const int w0 = copies_wave0_3(mode, K, IH, IWP, CT, ks);
+FCM_HD inline int copies_per_wave3(int mode, int K, int IH, int IWP, int CT, int ks = 1, int pc = 0) {
+  const int t = copies_per_item3(mode, K, IH, IWP, CT, ks, pc);
+  const int w0 = copies_wave0_3(mode, K, IH, IWP, CT, ks, pc);
   return w0 > t - w0 ? w0 : t - w0;
 }
 
@@ -380,7 +384,7 @@ struct KArgs {
   int cus;       // compute units of the device
   int grid_cap;  // persistent kernels: at most this many workgroups (0 = no cap)
   const int32_t* rqc[3];  // int8 per-channel requantisation per stage ([2][channels]) or nullptr
-  int zin[3];             // int8 zero point of each stage's input (first-generation kernels)
+  int zin[3];             // int8 zero point of each stage's input
 };
 
 // One compiled kernel instance and the tilings it implements.

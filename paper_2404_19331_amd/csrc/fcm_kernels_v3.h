@@ -27,6 +27,13 @@
 //   MODE M3_PW: the DW stage is off (window = output tile); M3_DW: the PW stage is off,
 //   each lane writes its 16 bytes of depthwise output directly.
 //
+//   QX (int8 only): 1 adds zero points, 2 zero points and per-channel requantisation
+//   (multipliers and shifts staged with the biases). Each is a separate instance,
+//   launched only for descriptors that have the feature, so that the symmetric kernel
+//   keeps its registers. Split plans too: the pointwise zero-point term is linear, so
+//   each split subtracts its own channel range's share before writing its partial sums,
+//   and the second kernel requantises.
+//
 // LDS: a ring of a.depth buffers (the copy waves run a.depth - 1 items ahead of the
 // compute waves; deeper rings keep more bytes in flight per CU). Per buffer: window [npin pixels][64 B] (pixel q at 64 q, no padding;
 // stride-2 windows keep even and odd columns in separate halves so that the lanes of a
@@ -66,15 +73,19 @@ __device__ __forceinline__ Epi3 make_epi3(int act, const Requant& rq) {
   return e;
 }
 __device__ __forceinline__ float epi_f(float v, const Epi3& e) { return __builtin_amdgcn_fmed3f(v, e.lo, e.hi); }
-__device__ __forceinline__ int32_t epi_i(int32_t acc, const Epi3& e) {
-  const int64_t t = (int64_t)acc * e.mult;
-  const int64_t half = ((int64_t)1 << e.shift) >> 1;
-  const int64_t rnd = e.shift > 0 ? half - 1 + ((t >> e.shift) & 1) : 0;
-  int64_t q = ((t + rnd) >> e.shift) + e.zp;
+// (the multiplier and shift of the value's channel: the stage's, or per-channel ones)
+__device__ __forceinline__ int32_t epi_q(int32_t acc, int32_t mult, int32_t shift, const Epi3& e) {
+  const int64_t t = (int64_t)acc * mult;
+  const int64_t half = ((int64_t)1 << shift) >> 1;
+  const int64_t rnd = shift > 0 ? half - 1 + ((t >> shift) & 1) : 0;
+  int64_t q = ((t + rnd) >> shift) + e.zp;
   q = q < e.qlo ? e.qlo : q;
   q = q > e.qhi ? e.qhi : q;
   return (int32_t)q;
 }
+__device__ __forceinline__ int32_t epi_i(int32_t acc, const Epi3& e) { return epi_q(acc, e.mult, e.shift, e); }
+// A per-channel shift as the first-generation kernels take it: clamped to [0, 62].
+__device__ __forceinline__ int32_t pc_shift(uint32_t s) { return min(max((int32_t)s, 0), 62); }
 __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
   const f32x2_t v = {a, b};
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_t));
@@ -182,7 +193,7 @@ __device__ __forceinline__ void wait_vm(int n) {
   }
 }
 
-template <class DT, int K, int S, int BPW, int CT, int MODE, int IWP, int KS, bool SPLIT, bool ZP>
+template <class DT, int K, int S, int BPW, int CT, int MODE, int IWP, int KS, bool SPLIT, int QX>
 __global__ __launch_bounds__(kThreads3) void k_fused3(KArgs a) {
   extern __shared__ __align__(16) char smem[];
   using T = typename DT::T;
@@ -201,6 +212,8 @@ __global__ __launch_bounds__(kThreads3) void k_fused3(KArgs a) {
   static_assert(CPL * 4 == CB, "lane slot layout");
   static_assert(IWP % 16 == 0, "window pitch");
   static_assert(MODE != M3_DW || KS == 1, "a depthwise-only item is one chunk");
+  static_assert(QX == 0 || std::is_same<DT, TI8>::value, "zero points / per-channel: int8");
+  constexpr int PCQ = QX == 2 ? 1 : 0;  // per-channel multipliers and shifts staged
   // Output-channel order of the PW accumulators: lane (l % 16, g = l / 16) of tile i holds
   // values v = 0..3 of channel OGE * (4 * (i / OTPG) + g) + 4 * (i % OTPG) + v, so that the
   // OTPG tiles of each 16-byte output granule sit in one lane and the four lane groups
@@ -213,10 +226,13 @@ __global__ __launch_bounds__(kThreads3) void k_fused3(KArgs a) {
   const int TH = a.TH, TW = a.TW, P = TH * TW;
   const int IW = HAS_DW ? (TW - 1) * SE + KE : TW;
   const int IH = HAS_DW ? (TH - 1) * SE + KE : TH;
-  const Lds3 lay = lds3p(dtype_id<DT>(), KE, MODE, IH, IWP, CT, 2, KS);
+  const Lds3 lay = lds3p(dtype_id<DT>(), KE, MODE, IH, IWP, CT, 2, KS, PCQ);
+  if constexpr (PCQ) {
+    if ((a.depth < 2 ? 2 : a.depth) * lay.buf_bytes > a.L.bytes) return;  // (a plan for another layout)
+  }
   const int C = MODE == M3_DW ? a.Cm : a.Ci;
   const int nchunks = MODE == M3_DW ? 1 : ceil_div(C, CB * KS);  // items per work tile
-  const int per_item = copies_per_item3(MODE, KE, IH, IWP, CT, KS);
+  const int per_item = copies_per_item3(MODE, KE, IH, IWP, CT, KS, PCQ);
   // Work units: split u % SPL of work tile u / SPL runs items [u_lo(u), u_hi(u)).
   // (a separate instance: the partial-sum epilogue in the same loop costs the unsplit
   // kernel its schedule)
@@ -274,14 +290,19 @@ __global__ __launch_bounds__(kThreads3) void k_fused3(KArgs a) {
     // ===== copy waves: all copies, D - 1 items ahead of the compute waves. Wave 0 issues
     // the DW weights and bias (and converts them) and window rows [0, r0); wave 1 the
     // rows [r0, IH), the PW weight rows and the PW bias. =====
-    const int r0 = rows_wave0_3(MODE, KE, IH, IWP, CT, KS);
+    const int r0 = rows_wave0_3(MODE, KE, IH, IWP, CT, KS, PCQ);
     const int wy0 = wave == 0 ? 0 : r0, wy1 = wave == 0 ? r0 : IH;
-    const int w0n = copies_wave0_3(MODE, KE, IH, IWP, CT, KS);
+    const int w0n = copies_wave0_3(MODE, KE, IH, IWP, CT, KS, PCQ);
     const int mine = wave == 0 ? w0n : per_item - w0n;  // copies per item of this wave
     const rsrc_t rw = make_rsrc(wp, HAS_PW ? (uint32_t)((size_t)a.Co * a.Ci * DT::ELT) : 0u);
     const rsrc_t rwd = make_rsrc(wd, HAS_DW ? (uint32_t)((size_t)C * KK * DT::ELT) : 0u);
     const rsrc_t rbd = make_rsrc(bd ? bd : (const void*)wd, (HAS_DW && bd) ? (uint32_t)(C * 4) : 0u);
     const rsrc_t rbp = make_rsrc(bp ? bp : (const void*)wp, (HAS_PW && bp) ? (uint32_t)(a.Co * 4) : 0u);
+    // per-channel requantisation of each stage: [multipliers | shifts] of its channels
+    const int32_t* qd = PCQ && HAS_DW ? a.rqc[0] : nullptr;
+    const int32_t* qp = PCQ && HAS_PW ? a.rqc[MODE == M3_PW ? 0 : 1] : nullptr;
+    const rsrc_t rqd = make_rsrc(qd ? (const void*)qd : (const void*)wd, qd ? (uint32_t)(2 * C * 4) : 0u);
+    const rsrc_t rqp = make_rsrc(qp ? (const void*)qp : (const void*)wp, qp ? (uint32_t)(2 * a.Co * 4) : 0u);
     int wxl[IPR];
 #pragma unroll
     for (int j = 0; j < IPR; ++j) {
@@ -298,11 +319,11 @@ __global__ __launch_bounds__(kThreads3) void k_fused3(KArgs a) {
     // landed, each copy wave rewrites the out-of-image positions of its own rows, and
     // wave 0 the item's depthwise biases; a second item iterator follows the issue one.
     // (Every byte of a ring slot is a copy target, so no item data can ride along in it.)
-    const int zin = (ZP && HAS_DW) ? a.zin[0] : 0;
+    const int zin = (QX && HAS_DW) ? a.zin[0] : 0;
     int fx_slot = 0, fx_wt = wt0, fx_ch = u_lo(wt0), fx_hi = u_hi(wt0);
     Tile fx_t = iss_t;
     auto fix_next = [&]() {
-      if (!ZP || zin == 0) return;
+      if (!QX || zin == 0) return;
       char* buf = bufp(fx_slot);
       const int iy0 = fx_t.oy0 * SE - a.pad, ix0 = fx_t.ox0 * SE - a.pad;
       fx_slot = next_slot(fx_slot);
@@ -369,6 +390,11 @@ __global__ __launch_bounds__(kThreads3) void k_fused3(KArgs a) {
                   b < CB * KK * DT::ELT ? (uint32_t)((c0 + s * CB) * KK * DT::ELT + b) : kOob);
           }
         dma16(rbd, buf + lay.bias_off, lane * 16 < KS * CB * 4 ? (uint32_t)(c0 * 4 + lane * 16) : kOob);
+        if constexpr (PCQ) {  // lanes 0-31: multipliers of the item's channels, 32-63: their shifts
+          const int j = lane & 31, ch = c0 + 4 * j;
+          const bool ok = j * 16 < KS * CB * 4 && ch < C;
+          dma16(rqd, buf + lay.bias_off + 2048, ok ? (uint32_t)(((lane < 32 ? 0 : C) + ch) * 4) : kOob);
+        }
       }
       for (int wy = wy0; wy < wy1; ++wy) {
         const int gy = iy0 + wy;
@@ -395,6 +421,12 @@ __global__ __launch_bounds__(kThreads3) void k_fused3(KArgs a) {
                   woff + (uint32_t)((4 * OGE * (ct / OTPG) + 4 * (ct % OTPG)) * a.Ci * DT::ELT));
         }
         dma16(rbp, buf + lay.bias_off + 1024, lane * 16 < CoB * 4 ? (uint32_t)(co0 * 4 + lane * 16) : kOob);
+        if constexpr (PCQ) {  // multipliers, then shifts, of the block's output channels
+          const int ch = co0 + 4 * lane;
+          const bool ok = lane * 16 < CoB * 4 && ch < a.Co;
+          dma16(rqp, buf + lay.bias_off + 3072, ok ? (uint32_t)(ch * 4) : kOob);
+          dma16(rqp, buf + lay.bias_off + 4096, ok ? (uint32_t)((a.Co + ch) * 4) : kOob);
+        }
       }
       iss_slot = next_slot(iss_slot);
       if (++iss_ch == iss_hi && ++iss_wt < wt1) {
@@ -488,7 +520,9 @@ __global__ __launch_bounds__(kThreads3) void k_fused3(KArgs a) {
   // Asymmetric int8 PW input (zero point z_pw): every output channel loses z_pw x its
   // weight-row sum, which each lane accumulates from its A operands (16 bytes of a row per
   // chunk) and completes at the epilogue.
-  const int z_pw = (ZP && HAS_PW) ? a.zin[MODE == M3_PW ? 0 : 1] : 0;
+  const int z_pw = (QX && HAS_PW) ? a.zin[MODE == M3_PW ? 0 : 1] : 0;
+  const bool pc_dw = PCQ && HAS_DW && a.rqc[0] != nullptr;  // (uniform)
+  const bool pc_pw = PCQ && HAS_PW && a.rqc[MODE == M3_PW ? 0 : 1] != nullptr;
   int32_t rsp[CT];
 #pragma unroll
   for (int i = 0; i < CT; ++i) rsp[i] = 0;
@@ -548,8 +582,39 @@ __global__ __launch_bounds__(kThreads3) void k_fused3(KArgs a) {
               for (int b = 0; b < NB; ++b) D3::tap(dacc[b], *(const u32x4*)(xb[b] + toff), wv);
             }
           }
+          if constexpr (PCQ) {
+            if (pc_dw) {
+              // this lane's CPL channels of chunk s: multipliers, then (512 bytes on) shifts
+              const char* pm = buf + lay.bias_off + 2048 + (s * CB + g * CPL) * 4;
+              // One value at a time: each value's input is released by the previous
+              // result (a wave issues its vector instructions in order, so the chain costs
+              // no issue slots), which keeps the 64-bit temporaries of one value live
+              // instead of those of all NB x CPL.
+              int32_t tok = 0;
 #pragma unroll
-          for (int b = 0; b < NB; ++b) bop[b] = D3::finish(dacc[b], ep_dw);
+              for (int j = 0; j < 4; ++j) {
+                const u32x4 mv = *(const u32x4*)(pm + 16 * j), sv = *(const u32x4*)(pm + 512 + 16 * j);
+#pragma unroll
+                for (int b = 0; b < NB; ++b) {
+                  uint32_t wv = 0;
+#pragma unroll
+                  for (int e = 0; e < 4; ++e) {
+                    int32_t v = dacc[b][4 * j + e];
+                    asm volatile("" : "+v"(v) : "v"(tok));
+                    tok = epi_q(v, (int32_t)mv[e], pc_shift(sv[e]), ep_dw);
+                    wv |= ((uint32_t)tok & 0xffu) << (8 * e);
+                  }
+                  bop[b][j] = wv;
+                }
+              }
+            } else {
+#pragma unroll
+              for (int b = 0; b < NB; ++b) bop[b] = D3::finish(dacc[b], ep_dw);
+            }
+          } else {
+#pragma unroll
+            for (int b = 0; b < NB; ++b) bop[b] = D3::finish(dacc[b], ep_dw);
+          }
         } else {
 #pragma unroll
           for (int b = 0; b < NB; ++b) bop[b] = *(const u32x4*)(plane + base[b]);
@@ -568,7 +633,7 @@ __global__ __launch_bounds__(kThreads3) void k_fused3(KArgs a) {
               }
             }
           };
-          if constexpr (ZP && !SPLIT) {
+          if constexpr (QX != 0) {
             if (z_pw != 0) contract(std::true_type{});  // (uniform)
             else contract(std::false_type{});
           } else {
@@ -587,6 +652,27 @@ __global__ __launch_bounds__(kThreads3) void k_fused3(KArgs a) {
 
     if (ch + 1 == ch_hi) {
       // ---- epilogue of the work unit: straight from registers to global memory ----
+      if constexpr (QX != 0 && HAS_PW) {
+        if (z_pw != 0) {
+          // (a split: the weight-row sums over its own channel chunks) row m of tile i:
+          // the four lanes l % 16 == m hold its quarters; then each accumulator lane takes
+          // rows 4g + v
+#pragma unroll
+          for (int i = 0; i < CT; ++i) {
+            int32_t s = rsp[i];
+            s += __shfl_xor(s, 16);
+            s += __shfl_xor(s, 32);
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+              const int32_t r = __shfl(s, 4 * g + v);
+#pragma unroll
+              for (int b = 0; b < BPW; ++b) acc[b][i][v] -= z_pw * r;
+            }
+          }
+        }
+#pragma unroll
+        for (int i = 0; i < CT; ++i) rsp[i] = 0;
+      }
       if constexpr (MODE == M3_DW) {
         const int c = cur_t.cb * CB + g * CPL;
 #pragma unroll
@@ -614,26 +700,6 @@ __global__ __launch_bounds__(kThreads3) void k_fused3(KArgs a) {
 #pragma unroll
           for (int i = 0; i < CT; ++i) acc[b][i] = AccV{0, 0, 0, 0};
       } else {
-        if constexpr (ZP) {
-          if (z_pw != 0) {
-            // row m of tile i: the four lanes l % 16 == m hold its quarters; then each
-            // accumulator lane takes rows 4g + v
-#pragma unroll
-            for (int i = 0; i < CT; ++i) {
-              int32_t s = rsp[i];
-              s += __shfl_xor(s, 16);
-              s += __shfl_xor(s, 32);
-#pragma unroll
-              for (int v = 0; v < 4; ++v) {
-                const int32_t r = __shfl(s, 4 * g + v);
-#pragma unroll
-                for (int b = 0; b < BPW; ++b) acc[b][i][v] -= z_pw * r;
-              }
-            }
-          }
-#pragma unroll
-          for (int i = 0; i < CT; ++i) rsp[i] = 0;
-        }
         // this lane's output granules k = 0 .. CT/OTPG - 1: channels co_blk + OGE * (4k + g) + [0, OGE)
         constexpr int NG = MODE == M3_DW ? 1 : CT / OTPG;
         const int co_blk = cur_t.cb * CoB;
@@ -679,9 +745,19 @@ __global__ __launch_bounds__(kThreads3) void k_fused3(KArgs a) {
 #pragma unroll
               for (int w = 0; w < 4; ++w) {
                 uint32_t wv = 0;
+                if (PCQ && pc_pw) {
+                  // multipliers (then, a KiB on, shifts) of channels c0k + 4w + [0, 4)
+                  const char* pm = buf + lay.bias_off + 3072 + (OGE * (4 * k + g) + 4 * w) * 4;
+                  const u32x4 mv = *(const u32x4*)pm, sv = *(const u32x4*)(pm + 1024);
 #pragma unroll
-                for (int e = 0; e < 4; ++e)
-                  wv |= ((uint32_t)epi_i(acc[b][4 * k + w][e] + bias[k][4 * w + e], ep_pw) & 0xffu) << (8 * e);
+                  for (int e = 0; e < 4; ++e)
+                    wv |= ((uint32_t)epi_q(acc[b][4 * k + w][e] + bias[k][4 * w + e], (int32_t)mv[e], pc_shift(sv[e]),
+                                           ep_pw) & 0xffu) << (8 * e);
+                } else {
+#pragma unroll
+                  for (int e = 0; e < 4; ++e)
+                    wv |= ((uint32_t)epi_i(acc[b][4 * k + w][e] + bias[k][4 * w + e], ep_pw) & 0xffu) << (8 * e);
+                }
                 wd4[w] = wv;
               }
             }
@@ -749,13 +825,14 @@ __global__ __launch_bounds__(256) void k_combine3(KArgs a) {
   }
   const Epi3 ep = make_epi3(a.act[STAGE], a.rq[STAGE]);  // STAGE: index of the PW convolution
   const void* bp = STAGE == 0 ? a.b1 : a.b2;
+  const int32_t* pc = a.rqc[STAGE];  // int8 per-channel [multipliers | shifts] or nullptr
   T* y = (T*)a.y + (((size_t)n * a.Ho + oy) * a.Wo + ox) * a.Co + co;
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
     if (co + e >= a.Co) break;
     if constexpr (DT::ELT == 1) {
       const int32_t b = bp ? ((const int32_t*)bp)[co + e] : 0;
-      y[e] = (T)epi_i(sum[e] + b, ep);
+      y[e] = (T)(pc ? epi_q(sum[e] + b, pc[co + e], pc_shift((uint32_t)pc[a.Co + co + e]), ep) : epi_i(sum[e] + b, ep));
     } else {
       const float b = bp ? ((const float*)bp)[co + e] : 0.0f;
       const float o = epi_f(sum[e] + b, ep);
@@ -770,21 +847,28 @@ __global__ __launch_bounds__(256) void k_combine3(KArgs a) {
 template <class DT, int K, int S, int BPW, int CT, int MODE, int IWP, int KS>
 int launch_fused3(const KArgs& a, int grid, void* stream) {
   const bool split = MODE != M3_DW && a.splits > 1;
-  // the zero-point instance (int8, unsplit) only where an input of the module has one, so
-  // that symmetric int8 runs without its registers
+  // the zero-point (and per-channel) instances (int8) only where the module has
+  // the feature, so that symmetric int8 runs without their registers
   constexpr bool kI8 = std::is_same<DT, TI8>::value;
-  const bool zp = kI8 && !split && (a.zin[0] != 0 || (MODE == M3_DWPW && a.zin[1] != 0));
-  auto fn = split ? k_fused3<DT, K, S, BPW, CT, MODE, IWP, KS, MODE != M3_DW, false>
-                  : zp ? k_fused3<DT, K, S, BPW, CT, MODE, IWP, KS, false, kI8>
-                       : k_fused3<DT, K, S, BPW, CT, MODE, IWP, KS, false, false>;
+  const bool two = MODE == M3_DWPW;  // stages whose input zero point / requantisation count
+  const bool zp = a.zin[0] != 0 || (two && a.zin[1] != 0);
+  const bool pc = a.rqc[0] != nullptr || (two && a.rqc[1] != nullptr);
+  const int qx = !kI8 ? 0 : (pc ? 2 : (zp ? 1 : 0));
+  constexpr bool SP = MODE != M3_DW;  // (the depthwise-only kernel never splits)
+  auto fn = split ? (qx == 2   ? k_fused3<DT, K, S, BPW, CT, MODE, IWP, KS, SP, (kI8 ? 2 : 0)>
+                     : qx == 1 ? k_fused3<DT, K, S, BPW, CT, MODE, IWP, KS, SP, (kI8 ? 1 : 0)>
+                               : k_fused3<DT, K, S, BPW, CT, MODE, IWP, KS, SP, 0>)
+            : qx == 2 ? k_fused3<DT, K, S, BPW, CT, MODE, IWP, KS, false, (kI8 ? 2 : 0)>
+            : qx == 1 ? k_fused3<DT, K, S, BPW, CT, MODE, IWP, KS, false, (kI8 ? 1 : 0)>
+                      : k_fused3<DT, K, S, BPW, CT, MODE, IWP, KS, false, 0>;
   const int lds = a.L.bytes;
   if (lds > 65536) {
     hipError_t e = hipFuncSetAttribute((const void*)fn, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
     if (e != hipSuccess) return (int)e;
   }
   // persistent grid: as many workgroups as are resident at once, at most one per work unit
-  static thread_local int cached_lds[3] = {-1, -1, -1}, cached_occ[3] = {1, 1, 1};
-  const int ci = split ? 1 : zp ? 2 : 0;
+  static thread_local int cached_lds[6] = {-1, -1, -1, -1, -1, -1}, cached_occ[6] = {1, 1, 1, 1, 1, 1};
+  const int ci = (split ? 3 : 0) + qx;
   if (cached_lds[ci] != lds) {
     int occ = 0;
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, (const void*)fn, kThreads3, lds) != hipSuccess || occ < 1)

@@ -46,7 +46,7 @@ static int out_dim(int x, int k, int s, int p) { return (x + 2 * p - k) / s + 1;
 Geom geometry(int op, const fcm_desc* d) {
   Geom g = {};
   g.op = op;
-  g.zp = kernel_set(op, d) == KSET_REG ? 1 : 0;
+  int8_features(op, d, &g.zp, &g.pc);
   g.n = d->n;
   g.h = d->h;
   g.w = d->w;
@@ -264,13 +264,13 @@ static int tiling_lds(const Variant& v, const Geom& g, int TH, int TW, int CB, i
     const int IH = mode == M3_PW ? TH : (TH - 1) * g.s + g.k;
     if (IW > v.pitch) return 0;
     const int KE = mode == M3_PW ? 1 : g.k;
-    const int per_item = copies_per_wave3(mode, KE, IH, v.pitch, COB / 16, v.ks);
+    const int per_item = copies_per_wave3(mode, KE, IH, v.pitch, COB / 16, v.ks, g.pc);
     if (per_item > 63) return 0;
-    const int buf = lds3p(g.dtype, KE, mode, IH, v.pitch, COB / 16, 2, v.ks).buf_bytes;
+    const int buf = lds3p(g.dtype, KE, mode, IH, v.pitch, COB / 16, 2, v.ks, g.pc).buf_bytes;
     const int d = ring_depth3(*depth, buf, per_item, lds_per_wg);
     if (d == 0) return 0;
     *depth = d;
-    return lds3p(g.dtype, KE, mode, IH, v.pitch, COB / 16, d, v.ks).total;
+    return lds3p(g.dtype, KE, mode, IH, v.pitch, COB / 16, d, v.ks, g.pc).total;
   }
   switch (v.family) {
     case FAM_DWPW:
@@ -299,10 +299,11 @@ bool variant_needs_alignment(int variant) {
 }
 
 // Generations 2 and up need the full set; with zero points (KSET_REG) also the int8
-// persistent kernels (unsplit plans: evaluate_plan) and the register kernel's instances
-// of at most kZpMaxTiles output tiles.
+// persistent kernels and the register kernel's instances of at most kZpMaxTiles output
+// tiles; with per-channel requantisation (KSET_PC) the int8 persistent kernels.
 static bool in_set(const Variant& v, int kset) {
   if (v.gen < 2) return true;
+  if (kset == KSET_PC) return v.gen == 3 && v.dtype == DT_I8;
   if (kset & KSET_DMA) return true;
   if (!(kset & KSET_REG)) return false;
   return (v.gen == 3 && v.dtype == DT_I8) || (v.gen == 4 && v.max_cob <= 16 * kZpMaxTiles);
@@ -419,7 +420,6 @@ fcm_status evaluate_plan(const Geom& g, const fcm_desc* d, const fcm_hw_desc& hw
   }
   if (v.gen == 3) {
     const int splits = p->splits > 1 ? p->splits : 1;
-    if (splits > 1 && g.zp) return fail(FCM_EUNSUPPORTED, "plan: zero points run on unsplit persistent plans");
     if (splits > 1) {
       if (v.family == FAM_DW) return fail(FCM_EUNSUPPORTED, "plan: a depthwise-only kernel does not split");
       const int ipt = ceil_div(g.ci, v.ks * (64 / g.elt));
@@ -513,8 +513,8 @@ static double persistent_time_estimate(const Variant& v, const Geom& g, const fc
   const double mfmas = (double)v.ks * nb_max * ct * (g.elt == 4 ? 4 : 1);
   const double comp = kItem0 + kPerDot * dots + kPerMfma * mfmas;
   const double lds = kPerLdsKiB * v.ks * lds_kib;
-  const double prod = kCopy0 + kPerCopy * copies_per_wave3(mode, K, IH, v.pitch, ct, v.ks);
-  const double item_bytes = 1024.0 * copies_per_item3(mode, K, IH, v.pitch, ct, v.ks);
+  const double prod = kCopy0 + kPerCopy * copies_per_wave3(mode, K, IH, v.pitch, ct, v.ks, g.pc);
+  const double item_bytes = 1024.0 * copies_per_item3(mode, K, IH, v.pitch, ct, v.ks, g.pc);
   const int64_t grid = std::max<int64_t>(1, p.workgroups);
   const double wpc = std::max(1.0, (double)grid / hw.num_cus);
   const int depth = std::max(2, p.depth);

@@ -1,5 +1,7 @@
-"""GPU parity of the int8 persistent kernels (DW->PW, PW, DW) under zero points, bit-exact
-against the CPU oracle, forced through explicit unsplit plans.
+"""GPU parity of the int8 persistent kernels (DW->PW, PW, DW) under zero points and
+per-channel requantisation, bit-exact against the CPU oracle, forced through explicit
+plans, unsplit and split (channel chunks over several workgroups, partial sums combined
+by a second kernel).
 
 With an input zero point the copy waves rewrite the window positions outside the image
 with the input's code of real 0 once an item's copies have landed, and fold the input zero
@@ -11,6 +13,10 @@ several tile shapes (tiles on the image border and inside, ragged pixel blocks),
 depths and capped grids (a workgroup streams many tiles, so the rewrite follows the ring
 across tiles), channel counts with a ragged last chunk, zero points at the int8
 extremes, strides 1 and 2 and filters 3 and 5.
+
+Per-channel requantisation (a multiplier and a shift per output channel of a stage, staged
+beside the biases) runs on the same cases, on every stage or on one stage only, with and
+without the zero points: multipliers up to 2^30 (64-bit products), shifts from 0 to 62.
 """
 import pytest
 
@@ -18,6 +24,7 @@ from paper_2404_19331_amd import fcm
 from paper_2404_19331_amd.workloads import Case, make_inputs
 
 from gpu_util import dev_inputs, oracle_ref, run_fused, to_np
+import oracle
 
 import numpy as np
 
@@ -46,8 +53,11 @@ def _cases():
     return out
 
 
-def _plans(case):
+def _plans(case, rqc=()):
     desc = fcm.desc_from_case(case)
+    for i, t in enumerate(rqc):
+        if t is not None:
+            desc.rq_channel[i] = t.data_ptr()  # (rqc outlives the plans' use)
     plans = []
     for v in range(fcm.lib().fcm_variant_count()):
         name = fcm.variant_name(v)
@@ -61,6 +71,13 @@ def _plans(case):
                 except fcm.FcmError:
                     continue
                 assert p.splits == 1
+                plans.append(p)
+            for splits in (2, 3):  # each split subtracts its own share of the zero-point term
+                try:
+                    p = fcm.plan_evaluate(case.op, desc, th, tw, 64, cob, v, splits=splits)
+                except fcm.FcmError:
+                    continue
+                assert p.splits == splits
                 plans.append(p)
     return plans
 
@@ -77,11 +94,72 @@ def test_persistent_zero_points_match_oracle(case):
     d = dev_inputs(inp, case.dtype)
     plans = _plans(case)
     assert plans, "no persistent variant implements %s" % case.name
+    if case.c_in > 64 and case.op != "dw":
+        assert any(p.splits > 1 for p in plans), case.name  # not vacuous
     for p in plans:
         got = to_np(run_fused(case, d, plan=p))
-        assert np.array_equal(got, ref), "%s %s tile %dx%d grid %d depth %d: %d of %d differ" % (
-            case.name, fcm.variant_name(p.variant), p.tile_h, p.tile_w, p.workgroups, p.depth,
+        assert np.array_equal(got, ref), "%s %s tile %dx%d grid %d depth %d splits %d: %d of %d differ" % (
+            case.name, fcm.variant_name(p.variant), p.tile_h, p.tile_w, p.workgroups, p.depth, p.splits,
             int(np.sum(got != ref)), ref.size)
     # the planner's own plan for the asymmetric descriptor is a persistent one too
     p = fcm.plan(case.op, fcm.desc_from_case(case))
-    assert fcm.variant_name(p.variant).startswith(("k_dwpw3<i8,", "k_pw3<i8,", "k_dw3<i8,")) and p.splits == 1
+    assert fcm.variant_name(p.variant).startswith(("k_dwpw3<i8,", "k_pw3<i8,", "k_dw3<i8,"))
+
+
+def _stage_channels(case):
+    return {"dw_pw": [case.c_in, case.c_out], "dw": [case.c_in], "pw": [case.c_out]}[case.op]
+
+
+def _per_channel(n, seed):
+    """Multipliers and shifts of n channels: scales from about 2^-8 to 2^-2 with
+    multipliers up to 2^30, plus the edge channels (1, 0) (the accumulator itself,
+    saturated) and a shift of 62."""
+    rng = np.random.default_rng(seed)
+    mult = rng.integers(1, 1 << 30, n)
+    shift = np.floor(np.log2(mult)).astype(np.int64) + rng.integers(2, 9, n)
+    mult[0], shift[0] = 1, 0
+    if n > 5:
+        mult[5], shift[5] = (1 << 30) - 1, 62
+    return mult.astype(np.int64), np.clip(shift, 0, 62)
+
+
+PC_CASES = [c for c in CASES if c.h > 3]
+
+
+@pytest.mark.parametrize("stages", ["all", "first", "last"])
+@pytest.mark.parametrize("case", PC_CASES, ids=lambda c: c.name)
+def test_persistent_per_channel_requant_matches_oracle(case, stages):
+    import dataclasses
+    import torch
+    chans = _stage_channels(case)
+    if stages != "all" and len(chans) == 1:
+        pytest.skip("a one-stage module: every stage is the first and the last")
+    pcs = [_per_channel(n, 60 + 7 * i + len(case.name)) for i, n in enumerate(chans)]
+    if stages == "first":
+        pcs = [pcs[0]] + [None] * (len(pcs) - 1)
+    elif stages == "last":
+        pcs = [None] * (len(pcs) - 1) + [pcs[-1]]
+    rqc = [None if pc is None else torch.from_numpy(np.concatenate(pc).astype(np.int32)).cuda() for pc in pcs]
+    for zp in (True, False):
+        c = case if zp else dataclasses.replace(case, zp_in=0, rq=tuple(tuple(r[:4]) + (0,) for r in case.rq))
+        inp = make_inputs(c)
+        ref = oracle.run(c.op, dict(c.as_dict(), rq_channel=pcs), inp)
+        assert len(np.unique(ref)) > 8, c.name
+        d = dev_inputs(inp, c.dtype)
+        plans = _plans(c, rqc)
+        assert plans, c.name
+        if c.c_in > 64 and c.op != "dw":
+            assert any(p.splits > 1 for p in plans), c.name  # not vacuous
+        for p in plans:
+            got = to_np(run_fused(c, d, plan=p, rq_channel=rqc))
+            assert np.array_equal(got, ref), "%s zp %s pc %s %s tile %dx%d grid %d depth %d splits %d: %d of %d differ" % (
+                c.name, zp, stages, fcm.variant_name(p.variant), p.tile_h, p.tile_w, p.workgroups, p.depth, p.splits,
+                int(np.sum(got != ref)), ref.size)
+        # not vacuous: the stage scales change the result; the planner picks this kernel
+        assert not np.array_equal(to_np(run_fused(c, d)), ref)
+        desc = fcm.desc_from_case(c)
+        for i, t in enumerate(rqc):
+            if t is not None:
+                desc.rq_channel[i] = t.data_ptr()
+        p = fcm.plan(c.op, desc)
+        assert fcm.variant_name(p.variant).startswith(("k_dwpw3<i8,", "k_pw3<i8,", "k_dw3<i8,"))

@@ -1,7 +1,7 @@
 """GPU parity of asymmetric int8 (zero points) against the CPU oracle, bit-exact.
 
-Zero points run on the first-generation kernels, the int8 persistent kernels (unsplit
-plans; their own tests in test_gpu_v3_zero_points.py) and the PW->PW register kernel's
+Zero points run on the first-generation kernels, the int8 persistent kernels (their own
+tests in test_gpu_v3_zero_points.py) and the PW->PW register kernel's
 instances of at most 192 output channels. First generation: the window a depthwise stage reads is
 padded with its input's code of real 0, the depthwise sum and each pointwise contraction
 lose (input zero point) x (weight sum), the border of the PW -> DW intermediate holds the
@@ -75,7 +75,7 @@ def test_zero_point_parity(case):
     p = fcm.plan(case.op, fcm.desc_from_case(case))
     v = p.variant
     assert _first_gen(v) or (case.op == "pw_pw" and fcm.variant_name(v).startswith("k_pwpw4<i8,")) or \
-        (fcm.variant_name(v).startswith(("k_dwpw3<i8,", "k_pw3<i8,", "k_dw3<i8,")) and p.splits == 1), \
+        fcm.variant_name(v).startswith(("k_dwpw3<i8,", "k_pw3<i8,", "k_dw3<i8,")), \
         fcm.variant_name(v)
     if case.op not in ("dw", "pw"):
         assert np.array_equal(to_np(run_unfused(case, d)), ref), case.name + " (layer-by-layer)"

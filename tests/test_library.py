@@ -255,15 +255,15 @@ def test_library_binds_to_the_hip_runtime_torch_loads():
 
 # --------------------------------------------------------------------------------------
 # Asymmetric int8 (zero points): planned on the first-generation kernels, the int8
-# persistent kernels (unsplit plans) and the PW->PW register kernel
+# persistent kernels and the PW->PW register kernel
 # --------------------------------------------------------------------------------------
 
 def _first_gen(v):
     return re.search(r"\d<", fcm.variant_name(v)) is None
 
 
-def _persistent_unsplit(p):
-    return re.match(r"k_(dwpw|dw|pw)3<i8,", fcm.variant_name(p.variant)) is not None and p.splits == 1
+def _persistent(p):
+    return re.match(r"k_(dwpw|dw|pw)3<i8,", fcm.variant_name(p.variant)) is not None
 
 
 ZP_SHAPES = {"dw_pw": (64, 64, 64, 3), "pw_dw": (32, 96, 96, 3), "pw_dw_pw": (32, 96, 32, 3),
@@ -289,8 +289,8 @@ def test_zero_points_plan_capable_kernels(op):
         name = fcm.variant_name(p.variant)
         if op == "pw_pw":  # the register kernel carries zero points (up to 192 output channels)
             assert name.startswith("k_pwpw4<i8,"), (zin, zps, name)
-        elif op in ("dw_pw", "dw", "pw"):  # the int8 persistent kernels, unsplit
-            assert _persistent_unsplit(p), (zin, zps, name, p.splits)
+        elif op in ("dw_pw", "dw", "pw"):  # the int8 persistent kernels
+            assert _persistent(p), (zin, zps, name, p.splits)
         else:
             assert _first_gen(p.variant), (zin, zps, name)
     # a zero point of a stage the module does not have is ignored, as are float types
@@ -298,6 +298,41 @@ def test_zero_points_plan_capable_kernels(op):
         assert fcm.plan(op, _zp_desc(op, 0, (0, 0, 9) if stages == 2 else (0, 9, 9))).as_dict() == sym.as_dict()
     f = fcm.plan(op, _zp_desc(op, 5, (3, 3, 3), dtype="bf16"))
     assert f.as_dict() == fcm.plan(op, _zp_desc(op, dtype="bf16")).as_dict()
+
+
+def _pc_desc(op, stages, zp_in=0):
+    """A descriptor with per-channel requantisation on `stages`: for planning only (the
+    planner never dereferences the pointers, so stand-in addresses serve)."""
+    d = _zp_desc(op, zp_in)
+    for i in stages:
+        d.rq_channel[i] = 0x10000 * (i + 1)
+    return d
+
+
+@pytest.mark.parametrize("op", list(ZP_SHAPES))
+def test_per_channel_plan_capable_kernels(op):
+    """Per-channel requantisation plans on the int8 persistent kernels where they
+    implement the module (DW->PW, DW, PW), else on the first-generation kernels; the ring
+    slot grows by the three KiB of staged multipliers and shifts."""
+    stages = {"pw_dw_pw": 3, "dw": 1, "pw": 1}.get(op, 2)
+    sym = fcm.plan(op, _zp_desc(op))
+    for sel in ([0], [stages - 1], list(range(stages))):
+        for zin in (0, -5):
+            p = fcm.plan(op, _pc_desc(op, sel, zin))
+            name = fcm.variant_name(p.variant)
+            if op in ("dw_pw", "dw", "pw"):
+                assert _persistent(p), (sel, zin, name, p.splits)
+            else:
+                assert _first_gen(p.variant), (sel, zin, name)
+    # a stage the module does not have is ignored
+    if stages < 3:
+        assert fcm.plan(op, _pc_desc(op, [2])).as_dict() == sym.as_dict()
+    if op in ("dw_pw", "dw", "pw"):
+        pc = _pc_desc(op, [0])
+        a = fcm.plan_evaluate(op, _zp_desc(op), sym.tile_h, sym.tile_w, sym.c_block, sym.co_block, sym.variant,
+                              depth=2)
+        b = fcm.plan_evaluate(op, pc, sym.tile_h, sym.tile_w, sym.c_block, sym.co_block, sym.variant, depth=2)
+        assert b.lds_bytes - a.lds_bytes == 2 * 3072 and b.splits == 1
 
 
 def test_zero_points_on_the_register_kernel_up_to_192_output_channels():
@@ -322,17 +357,17 @@ def test_zero_points_validation_and_explicit_plans():
         with pytest.raises(fcm.FcmError) as e:
             fcm.plan("dw_pw", _zp_desc("dw_pw", zin, zps))
         assert e.value.status == EINVAL and "zero point" in str(e.value)
-    # an explicit persistent plan is accepted for an asymmetric descriptor unsplit and
-    # refused split; one on a newer kernel without zero points (PW->DW streaming) is refused
+    # an explicit persistent plan is accepted for an asymmetric descriptor, unsplit and
+    # split; one on a newer kernel without zero points (PW->DW streaming) is refused
     sym = fcm.plan("dw_pw", _zp_desc("dw_pw"))
     assert re.match(r"k_dwpw3<i8,", fcm.variant_name(sym.variant))
     un = fcm.plan_evaluate("dw_pw", _zp_desc("dw_pw", 3), sym.tile_h, sym.tile_w, sym.c_block, sym.co_block,
                            sym.variant)
     assert un.splits == 1
-    with pytest.raises(fcm.FcmError) as e:
-        fcm.plan_evaluate("dw_pw", _zp_desc("dw_pw", 3), sym.tile_h, sym.tile_w, sym.c_block, sym.co_block,
-                          sym.variant, splits=2)
-    assert e.value.status == EUNSUPPORTED and "zero points" in str(e.value)
+    wide = fcm.make_desc(4, 14, 14, 256, 256, 64, k=3, stride=1, pad=1, dtype="i8", layout="nhwc",
+                         rq=[(1, 6, -128, 127, 4)] * 3, zp_in=3)
+    sp = fcm.plan_evaluate("dw_pw", wide, 7, 7, 64, 64, sym.variant, splits=2)
+    assert sp.splits == 2 and fcm.workspace_bytes(wide, sp) > 0
     pd = fcm.plan("pw_dw", _zp_desc("pw_dw"))
     if not _first_gen(pd.variant):
         with pytest.raises(fcm.FcmError) as e:
@@ -343,7 +378,7 @@ def test_zero_points_validation_and_explicit_plans():
 
 def test_chain_zero_points_reach_the_groups_they_touch():
     """A zero point on one layer's output moves to the zero-point kernels (first generation,
-    int8 persistent unsplit) exactly the groups that write that tensor or read it; the
+    int8 persistent) exactly the groups that write that tensor or read it; the
     others keep the symmetric plan."""
     layers = [dict(kind="pw", c_out=96, act="relu", rq=(1, 6, -128, 127)),
               dict(kind="dw", k=3, stride=1, pad=1, act="relu", rq=(1, 4, -128, 127)),
@@ -358,12 +393,12 @@ def test_chain_zero_points_reach_the_groups_they_touch():
         p = fcm.chain_plan(fcm.chain_desc(4, 28, 28, 64, zl, "i8"), "unfused")
         for g, (first, op, plan) in enumerate(p.groups()):
             touched = first in (j, j + 1)  # unfused: one layer per group
-            assert _first_gen(plan.variant) or _persistent_unsplit(plan) or not touched, (j, first)
+            assert _first_gen(plan.variant) or _persistent(plan) or not touched, (j, first)
             if not touched:
                 assert plan.as_dict() == sym.plan[g].as_dict()
     # the chain input's zero point reaches the first group only
     p = fcm.chain_plan(fcm.chain_desc(4, 28, 28, 64, layers, "i8", zp_in=-128), "unfused")
-    assert (_first_gen(p.plan[0].variant) or _persistent_unsplit(p.plan[0])) and \
+    assert (_first_gen(p.plan[0].variant) or _persistent(p.plan[0])) and \
         p.plan[1].as_dict() == sym.plan[1].as_dict()
 
 

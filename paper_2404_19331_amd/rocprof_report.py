@@ -37,10 +37,11 @@ _MODE = {"k_dwpw3": 0, "k_pw3": 1, "k_dw3": 2}
 _DT = {"f32": "TF32", "bf16": "TBF16", "i8": "TI8"}
 
 
-def kernel_symbol(variant, split=False):
+def kernel_symbol(variant, split=False, qx=0):
     """Demangled kernel name of a variant: persistent, e.g. k_dwpw3<bf16,3,1,1,16,p16> ->
-    void fcm::k_fused3<fcm::TBF16, 3, 1, 1, 16, 0, 16, 1, false>(fcm::KArgs) (the instance
-    of unsplit plans; split=True names the one of split plans); streaming (k_dwpw5<...>),
+    void fcm::k_fused3<fcm::TBF16, 3, 1, 1, 16, 0, 16, 1, false, 0>(fcm::KArgs) (the instance
+    of unsplit symmetric plans; split=True names the one of split plans, qx = 1 / 2 the int8
+    instances with zero points / with per-channel requantisation); streaming (k_dwpw5<...>),
     whole-module (k_dwpw6<...>) and deep (k_dwpw7<...>) variants map to their single instance."""
     m5 = re.match(r"(k_\w+5)<(\w+),(\d+),(\d+),(\d+)x(\d+),ct(\d+),wc(\d+)>$", variant)
     if m5:  # streaming kernels: k_fused5<DT, K, S, MODE, TH, TW, CTW, WC>
@@ -61,8 +62,8 @@ def kernel_symbol(variant, split=False):
     fam, dt, k, s, bpw, ct, pitch, ks = m.groups()
     if fam == "k_pw3":
         k = s = "1"
-    return "void fcm::k_fused3<fcm::%s, %s, %s, %s, %s, %d, %s, %s, %s>(fcm::KArgs)" % (
-        _DT[dt], k, s, bpw, ct, _MODE[fam], pitch, ks or "1", "true" if split else "false")
+    return "void fcm::k_fused3<fcm::%s, %s, %s, %s, %s, %d, %s, %s, %s, %d>(fcm::KArgs)" % (
+        _DT[dt], k, s, bpw, ct, _MODE[fam], pitch, ks or "1", "true" if split else "false", qx)
 
 
 def read_counters(path):

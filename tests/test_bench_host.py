@@ -46,3 +46,33 @@ def test_bench_refuses_more_than_one_gpu():
     r = subprocess.run([sys.executable, "bench.py", "--gpus", "4"], cwd=bench.ROOT, capture_output=True, text=True,
                        timeout=120)
     assert r.returncode == 2 and "one GPU" in r.stderr
+
+
+def test_profile_tooling_names_compiled_kernels():
+    """rocprof_report.kernel_symbol maps every persistent, streaming, whole-module and deep
+    variant (and the split and int8 feature instances of the persistent ones) to a kernel
+    the library contains, so that per-kernel statistics and traffic find their rows."""
+    import os
+    import re
+    from paper_2404_19331_amd import fcm, rocprof_report
+    lib = os.path.join(os.path.dirname(fcm.__file__), "libfcm.so")
+    out = subprocess.run(["nm", "-C", lib], capture_output=True, text=True, check=True).stdout
+    stubs = {m.group(1) for m in re.finditer(r"__device_stub__(k_\w+<[^>]*>)\(fcm::KArgs\)", out)}
+    checked = 0
+    for v in range(fcm.lib().fcm_variant_count()):
+        name = fcm.variant_name(v)
+        if not re.match(r"k_\w+[3567]<", name):
+            continue
+        forms = [dict()]
+        if re.match(r"k_\w+3<", name):
+            if not name.startswith("k_dw3<"):
+                forms.append(dict(split=True))
+            if "<i8," in name:
+                forms += [dict(qx=1), dict(qx=2)] + ([dict(split=True, qx=1), dict(split=True, qx=2)]
+                                                     if not name.startswith("k_dw3<") else [])
+        for kw in forms:
+            sym = rocprof_report.kernel_symbol(name, **kw)
+            body = re.match(r"void fcm::(k_\w+<.*>)\(fcm::KArgs\)$", sym).group(1)
+            assert body in stubs, (name, kw, sym)
+            checked += 1
+    assert checked > 50

@@ -14,6 +14,10 @@
       --kernel gives the demangled kernel name (as the stats table prints it) for variants
       whose name kernel_symbol does not map.
 
+  python -m paper_2404_19331_amd.rocprof_report counters CSV [CSV ...] --kernel SUBSTRING [--title T]
+          [--command C]
+      mean per dispatch of every counter of `rocprofv3 --pmc` runs, for the kernels whose
+      demangled name contains SUBSTRING, one row per kernel and counter
   python -m paper_2404_19331_amd.rocprof_report layers --manifest MANIFEST_JSON --fetch CSV
           --write CSV --mfma CSV --trace KERNEL_TRACE_CSV [--title T] [--command C]
       per-layer table of a `profile_layers` run: for the fused module and for its two
@@ -225,6 +229,27 @@ def stats(args):
     print("\n".join(out))
 
 
+def counters(a):
+    rows = defaultdict(list)
+    for path in a.csv:
+        vals, _ = read_counters(path)
+        for (kernel, counter), v in vals.items():
+            if a.kernel in kernel:
+                rows[(kernel, counter)] += v
+    out = []
+    if a.title:
+        out.append(a.title)
+    if a.command:
+        out.append("command: " + a.command)
+    if out:
+        out.append("")
+    out.append("%-60s %-34s %10s %16s" % ("kernel", "counter", "dispatches", "mean per dispatch"))
+    for (kernel, counter) in sorted(rows):
+        v = rows[(kernel, counter)]
+        out.append("%-60s %-34s %10d %16.1f" % (kernel[:60], counter, len(v), sum(v) / len(v)))
+    print("\n".join(out))
+
+
 def main():
     ap = argparse.ArgumentParser()
     sub = ap.add_subparsers(dest="cmd", required=True)
@@ -243,6 +268,11 @@ def main():
     t.add_argument("--out", default=os.path.join(ROOT, "profiles", "traffic.json"))
     t.add_argument("--kernel", default="", help="demangled kernel name (default: from the variant name)")
     t.add_argument("--shape", default="", help="layer shape the run launched the kernel on (bench.py --layers)")
+    c = sub.add_parser("counters")
+    c.add_argument("csv", nargs="+")
+    c.add_argument("--kernel", required=True)
+    c.add_argument("--title", default="")
+    c.add_argument("--command", default="")
     l = sub.add_parser("layers")
     l.add_argument("--manifest", required=True)
     l.add_argument("--fetch", required=True)
@@ -253,7 +283,7 @@ def main():
     l.add_argument("--command", default="")
     l.add_argument("--json", default="")
     a = ap.parse_args()
-    {"stats": stats, "traffic": traffic, "layers": layers}[a.cmd](a)
+    {"stats": stats, "traffic": traffic, "counters": counters, "layers": layers}[a.cmd](a)
 
 
 if __name__ == "__main__":

@@ -416,7 +416,7 @@ NOALLOC_SCRATCH_BYTES = 16 << 20  # FCM_NOALLOC_SCRATCH_BYTES
 
 
 def dw_pw_noalloc(x, w_dw, w_pw, b_dw=None, b_pw=None, *, stride=1, pad=None, act=("none", "none"), rq=None,
-                  layout="nchw", plan=None, out=None, stream=None, zp_in=0):
+                  rq_channel=None, layout="nchw", plan=None, out=None, stream=None, zp_in=0):
     """DW -> PW module through fcm_dw_pw_noalloc: a split plan's partial sums go to the
     library's fixed per-GPU array instead of a workspace (pass `out` to allocate nothing
     here either). Calls overlapping on one GPU race on that array."""
@@ -426,7 +426,7 @@ def dw_pw_noalloc(x, w_dw, w_pw, b_dw=None, b_pw=None, *, stride=1, pad=None, ac
     pad = (k - 1) // 2 if pad is None else pad
     co = int(w_pw.shape[0])
     _prep(x, [w_dw, w_pw], [b_dw, b_pw], dt)
-    d = make_desc(n, h, w, c, c, co, k, stride, pad, dt, layout, act, rq, zp_in=zp_in)
+    d = make_desc(n, h, w, c, c, co, k, stride, pad, dt, layout, act, rq, rq_channel=rq_channel, zp_in=zp_in)
     ho, wo = out_hw(h, w, k, stride, pad)
     y = _out(x, layout, n, co, ho, wo, out)
     return _call(lib().fcm_dw_pw_noalloc, (ctypes.byref(d), _ptr(x), _ptr(w_dw), _ptr(b_dw), _ptr(w_pw), _ptr(b_pw),

@@ -279,23 +279,23 @@ FCM_HD constexpr Lds5 lds5(int dt, int mode, int K, int IH, int IW, int COB, int
 }
 
 // Deep DW->PW kernels (k_deep7, bf16, 3x3): LDS bytes. Three ring slots of the haloed
-// window and two depthwise output exchange buffers, both as four planes of 8 channels
-// (16 bytes per position: a wave reading one plane at consecutive positions touches every
-// bank once), the PW bias block of 64 * CTW channels (fp32), and all C input channels'
+// window and two depthwise output exchange buffers, both as 4 KC planes of 8 channels
+// (KC 32-channel chunks per item; 16 bytes per position: a wave reading one plane at
+// consecutive positions touches every bank once), the PW bias block of 64 * CTW channels (fp32), and all C input channels'
 // depthwise weights ([C][3][3] bf16) and biases (fp32), each in whole KiB. Window
 // positions are rounded up to 64 (one LDS-DMA copy fills 64 positions of one plane).
 struct Lds7 {
   int nqp, win_plane, win_bytes, exch_off, exch_plane, exch_bytes, pwb_off, dww_off, dwb_off, total;
 };
-FCM_HD constexpr Lds7 lds7(int S, int TH, int TW, int CTW, int C) {
+FCM_HD constexpr Lds7 lds7(int S, int TH, int TW, int CTW, int C, int KC = 1) {
   Lds7 L{};
   const int IH = (TH - 1) * S + 3, IW = (TW - 1) * S + 3;
   L.nqp = round_up(IH * IW, 64);
   L.win_plane = 16 * L.nqp;
-  L.win_bytes = 4 * L.win_plane;
+  L.win_bytes = 4 * KC * L.win_plane;
   L.exch_off = 3 * L.win_bytes;
   L.exch_plane = (TH * TW + 15) / 16 * 16 * 16;
-  L.exch_bytes = 4 * L.exch_plane;
+  L.exch_bytes = 4 * KC * L.exch_plane;
   L.pwb_off = L.exch_off + 2 * L.exch_bytes;
   L.dww_off = L.pwb_off + round_up(64 * CTW * 4, 1024);
   L.dwb_off = L.dww_off + round_up(C * 18, 1024);
@@ -419,6 +419,7 @@ struct Variant {
                     // first convolution held in registers (input channels <= 64 * ks bytes);
                     // gen 5: LDS ring slots
   int wc = 1;       // gen 5: waves across output channels (1, 2 or 4)
+  int kc = 1;       // gen 7: 32-channel chunks per item (1 or 2)
 };
 
 // Compiled variants of each translation unit, and all of them in a fixed order

@@ -1,16 +1,17 @@
 // fcm_kernels_v7.h -- DW->PW for deep layers (bf16, 3x3, many channels, small images).
 //
-// k_deep7<S, TH, TW, CTW>
+// k_deep7<S, TH, TW, CTW, KC>
 //   Persistent, eight waves, one workgroup per CU. A workgroup owns a block of COB = 64 * CTW
 //   output channels and computes a sequence of work tiles (image, TH x TW output tile, at
 //   most 64 pixels), each over the input channels in chunks of 32 (one MFMA k-step); an
-//   item is one chunk of one tile. Such layers are bound neither by HBM nor by the matrix
-//   cores but by the instruction streams of the waves, the latency of their loads and the
-//   LDS traffic, so the work of an item is split over two kinds of waves, one of each on
-//   every SIMD, so that one's vector ALU work and LDS reads overlap the other's MFMAs:
-//   * Depthwise waves (0..3, wave d = 8-channel slot d of the chunk, lane = output pixel):
-//     copy their own channel plane of the haloed window of item i + 3 into a ring of three
-//     LDS slots (LDS-DMA; LDS planes of 8 channels, so that a wave's reads at consecutive
+//   item is KC chunks of one tile (two halve the barriers and waits per channel). Such
+//   layers are bound neither by HBM nor by the matrix cores but by the instruction
+//   streams of the waves, the latency of their loads and the LDS traffic, so the work of
+//   an item is split over two kinds of waves, one of each on every SIMD, so that one's
+//   vector ALU work and LDS reads overlap the other's MFMAs:
+//   * Depthwise waves (0..3, wave d = 8-channel slot d of each chunk, lane = output
+//     pixel): copy their own channel plane of each chunk of the haloed window of item
+//     i + 3 into a ring of three LDS slots (LDS-DMA; LDS planes of 8 channels, so that a wave's reads at consecutive
 //     positions are free of bank conflicts), compute the stencil of item i + 1 and write it to an LDS
 //     exchange buffer (two of them, planes of 8 channels: the MFMA B-operand layout). All
 //     depthwise weights and biases are copied into LDS once; per item the 72 weights of a
@@ -102,7 +103,7 @@ __device__ __forceinline__ void buf_store_nt16(const u32x4& v, rsrc_t r, uint32_
   __builtin_amdgcn_raw_buffer_store_b128(v, r, off, 0, 2);
 }
 
-template <int S, int TH, int TW, int CTW>
+template <int S, int TH, int TW, int CTW, int KC>
 __global__ __launch_bounds__(kThreads7) void k_deep7(KArgs a) {
   extern __shared__ __align__(16) char smem[];
   constexpr int K = 3, ELT = 2, CB = 32;
@@ -112,16 +113,16 @@ __global__ __launch_bounds__(kThreads7) void k_deep7(KArgs a) {
   constexpr int IH = (TH - 1) * S + K, IW = (TW - 1) * S + K;
   constexpr int IWE = S == 2 ? (IW + 1) / 2 : IW;  // stride 2: even columns first, then odd
   constexpr int NQ = IH * IW;
-  constexpr Lds7 lay = lds7(S, TH, TW, CTW, 0);  // (the C-dependent offsets below)
-  constexpr int ND = 4;               // depthwise waves, one 8-channel plane each
+  constexpr Lds7 lay = lds7(S, TH, TW, CTW, 0, KC);  // (the C-dependent offsets below)
+  constexpr int ND = 4;               // depthwise waves, one 8-channel plane of each chunk
   constexpr int NWW = lay.nqp / 64;   // window copies (1 KiB: 64 positions) per wave
   static_assert(NWW <= kWinPerWave5, "window copies per wave");
   constexpr int COB = 64 * CTW;
   constexpr int OGE = 8, OTPG = 2, NGW = CTW / OTPG;
   static_assert(CTW % OTPG == 0, "whole output granules per lane");
   constexpr int NST = NB * NGW;  // epilogue stores per MFMA wave
-  const int C = a.Ci;  // a multiple of the chunk
-  const int nch = C / CB;
+  const int C = a.Ci;  // a multiple of the item's KC chunks
+  const int nch = C / (CB * KC);  // items per tile
 
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
@@ -217,13 +218,17 @@ __global__ __launch_bounds__(kThreads7) void k_deep7(KArgs a) {
         }
       }
     };
-    // window of the next item into ring slot SLOT; an item at or beyond nit loads zeros
+    // window of the next item into ring slot SLOT (plane wd of each of its KC chunks at
+    // planes wd, wd + 4, ..); an item at or beyond nit loads zeros
     auto issue = [&](int slot, bool valid) {
       if (valid && w_c == 0) window_tile();
-      const uint32_t soff = valid ? wsoff + (uint32_t)(w_c * CB * ELT) : kOobS;
 #pragma unroll
-      for (int k = 0; k < NWW; ++k)
-        dma16s(rx, smem + slot * lay.win_bytes + wd * lay.win_plane + k * 1024, woff[k], soff);
+      for (int s = 0; s < KC; ++s) {
+        const uint32_t soff = valid ? wsoff + (uint32_t)((w_c * KC + s) * CB * ELT) : kOobS;
+#pragma unroll
+        for (int k = 0; k < NWW; ++k)
+          dma16s(rx, smem + slot * lay.win_bytes + (wd + ND * s) * lay.win_plane + k * 1024, woff[k], soff);
+      }
       if (valid && ++w_c == nch) {
         w_c = 0;
         advance(wt);
@@ -243,35 +248,39 @@ __global__ __launch_bounds__(kThreads7) void k_deep7(KArgs a) {
                               : (r16 < 11 ? dwb_off + 8 * wd * 4 + 16 * (r16 - 9) : lay.dww_off);
     int d_c = 0;  // chunk of the next depthwise item
     auto depthwise = [&](int slot, int e) {
-      const u32x4 wv = *(const u32x4*)(smem + wboff + (r16 < 9 ? d_c * CB * 18 : (r16 < 11 ? d_c * CB * 4 : 0)));
-      const u32x4& bv = wv;
+#pragma unroll
+      for (int s = 0; s < KC; ++s) {
+        const int dc = d_c * KC + s;  // chunk of the tile
+        const u32x4 wv = *(const u32x4*)(smem + wboff + (r16 < 9 ? dc * CB * 18 : (r16 < 11 ? dc * CB * 4 : 0)));
+        const u32x4& bv = wv;
+        const char* xb = smem + slot * lay.win_bytes + xoff + s * ND * lay.win_plane;
+        u32x4 xv[9];
+#pragma unroll
+        for (int ky = 0; ky < K; ++ky)
+#pragma unroll
+          for (int kx = 0; kx < K; ++kx) {
+            const int toff = (ky * IW + (S == 2 ? ((kx & 1) ? IWE + (kx >> 1) : (kx >> 1)) : kx)) * 16;
+            xv[ky * K + kx] = *(const u32x4*)(xb + toff);
+          }
+        float acc[8];
+        acc[0] = bcast7<9>(bv[0]);
+        acc[1] = bcast7<9>(bv[1]);
+        acc[2] = bcast7<9>(bv[2]);
+        acc[3] = bcast7<9>(bv[3]);
+        acc[4] = bcast7<10>(bv[0]);
+        acc[5] = bcast7<10>(bv[1]);
+        acc[6] = bcast7<10>(bv[2]);
+        acc[7] = bcast7<10>(bv[3]);
+        static_for7<0, 8>([&](auto jc) {
+          constexpr int J = decltype(jc)::value;
+          dw_channel7<J>(acc[J], xv, wv);
+        });
+        u32x4 out;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) out[j] = pack_bf16x2(epi_f(acc[2 * j], ep_dw), epi_f(acc[2 * j + 1], ep_dw));
+        if (lane < NB * 16) *(u32x4*)(smem + woutoff + e * lay.exch_bytes + s * ND * lay.exch_plane) = out;
+      }
       if (++d_c == nch) d_c = 0;
-      const char* xb = smem + slot * lay.win_bytes + xoff;
-      u32x4 xv[9];
-#pragma unroll
-      for (int ky = 0; ky < K; ++ky)
-#pragma unroll
-        for (int kx = 0; kx < K; ++kx) {
-          const int toff = (ky * IW + (S == 2 ? ((kx & 1) ? IWE + (kx >> 1) : (kx >> 1)) : kx)) * 16;
-          xv[ky * K + kx] = *(const u32x4*)(xb + toff);
-        }
-      float acc[8];
-      acc[0] = bcast7<9>(bv[0]);
-      acc[1] = bcast7<9>(bv[1]);
-      acc[2] = bcast7<9>(bv[2]);
-      acc[3] = bcast7<9>(bv[3]);
-      acc[4] = bcast7<10>(bv[0]);
-      acc[5] = bcast7<10>(bv[1]);
-      acc[6] = bcast7<10>(bv[2]);
-      acc[7] = bcast7<10>(bv[3]);
-      static_for7<0, 8>([&](auto jc) {
-        constexpr int J = decltype(jc)::value;
-        dw_channel7<J>(acc[J], xv, wv);
-      });
-      u32x4 out;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) out[j] = pack_bf16x2(epi_f(acc[2 * j], ep_dw), epi_f(acc[2 * j + 1], ep_dw));
-      if (lane < NB * 16) *(u32x4*)(smem + woutoff + e * lay.exch_bytes) = out;
     };
 
     // the weights and biases of every channel (1 KiB copies over the four waves, first),
@@ -285,7 +294,7 @@ __global__ __launch_bounds__(kThreads7) void k_deep7(KArgs a) {
         else dma16(rdb, smem + dwb_off + (j - nbw) * 1024, (uint32_t)((j - nbw) * 1024 + lane * 16));
       }
     }
-    constexpr int NIS = NWW;  // loads per item
+    constexpr int NIS = NWW * KC;  // loads per item
     issue(0, true);
     issue(1, 1 < nit);
     issue(2, 2 < nit);
@@ -317,11 +326,14 @@ __global__ __launch_bounds__(kThreads7) void k_deep7(KArgs a) {
       const int co = co0 + OGE * (4 * (ti / OTPG) + (r16 >> 2)) + 4 * (ti % OTPG) + (r16 & 3);
       aoff[i] = co < a.Co ? (uint32_t)(co * a.Ci * ELT + g * 16) : kOob;
     }
-    int a_c = 0;  // chunk of the next A operands to load
-    auto load_a = [&](u32x4 (&dst)[CTW], bool valid) {
-      const uint32_t k0 = valid ? (uint32_t)(a_c * CB * ELT) : kOobS;
+    int a_c = 0;  // item of the next A operands to load
+    auto load_a = [&](u32x4 (&dst)[KC][CTW], bool valid) {
 #pragma unroll
-      for (int i = 0; i < CTW; ++i) dst[i] = buf_load16s(rw, aoff[i], k0);
+      for (int s = 0; s < KC; ++s) {
+        const uint32_t k0 = valid ? (uint32_t)((a_c * KC + s) * CB * ELT) : kOobS;
+#pragma unroll
+        for (int i = 0; i < CTW; ++i) dst[s][i] = buf_load16s(rw, aoff[i], k0);
+      }
       if (++a_c == nch) a_c = 0;
     };
     // epilogue of a finished tile, straight from the accumulators
@@ -386,24 +398,29 @@ __global__ __launch_bounds__(kThreads7) void k_deep7(KArgs a) {
         if (j * 1024 + lane * 16 < COB * 4)
           dma16(rbp, smem + lay.pwb_off + j * 1024, (uint32_t)(co0 * 4 + j * 1024 + lane * 16));
     }
-    u32x4 am[3][CTW];
+    constexpr int NA = KC * CTW;  // A loads per item
+    u32x4 am[3][KC][CTW];
     load_a(am[0], true);
     load_a(am[1], 1 < nit);
     barrier3();
-    wait_vm_n<CTW>();  // A operands of item 0 (and the bias block)
+    wait_vm_n<NA>();  // A operands of item 0 (and the bias block)
     barrier3();
     run_items([&](auto setc, int it) {
       constexpr int SET = decltype(setc)::value;
       constexpr int S2 = (SET + 2) % 3;
       const char* ex = smem + lay.exch_off + (it & 1) * lay.exch_bytes + g * lay.exch_plane + r16 * 16;
-      u32x4 bop[NB];
+      u32x4 bop[KC][NB];
 #pragma unroll
-      for (int b = 0; b < NB; ++b) bop[b] = *(const u32x4*)(ex + b * 256);
+      for (int s = 0; s < KC; ++s)
+#pragma unroll
+        for (int b = 0; b < NB; ++b) bop[s][b] = *(const u32x4*)(ex + s * ND * lay.exch_plane + b * 256);
       load_a(am[S2], it + 2 < nit);
 #pragma unroll
-      for (int i = 0; i < CTW; ++i)
+      for (int s = 0; s < KC; ++s)
 #pragma unroll
-        for (int b = 0; b < NB; ++b) mma16(TBF16{}, acc[b][i], am[SET][i], bop[b]);
+        for (int i = 0; i < CTW; ++i)
+#pragma unroll
+          for (int b = 0; b < NB; ++b) mma16(TBF16{}, acc[b][i], am[SET][s][i], bop[s][b]);
       bool stored = false;
       if (++m_c == nch) {
         epilogue();
@@ -412,17 +429,17 @@ __global__ __launch_bounds__(kThreads7) void k_deep7(KArgs a) {
         advance(mt);
       }
       // A operands of item it + 1 are in: everything but this body's loads and stores
-      if (stored) wait_vm_n<CTW + NST>();
-      else wait_vm_n<CTW>();
+      if (stored) wait_vm_n<NA + NST>();
+      else wait_vm_n<NA>();
       wait_lgkm0();
       barrier3();
     });
   }
 }
 
-template <int S, int TH, int TW, int CTW>
+template <int S, int TH, int TW, int CTW, int KC>
 int launch_deep7(const KArgs& a, int grid, void* stream) {
-  auto fn = k_deep7<S, TH, TW, CTW>;
+  auto fn = k_deep7<S, TH, TW, CTW, KC>;
   const int lds = a.L.bytes;
   if (lds > 65536) {
     hipError_t e = hipFuncSetAttribute((const void*)fn, hipFuncAttributeMaxDynamicSharedMemorySize, lds);

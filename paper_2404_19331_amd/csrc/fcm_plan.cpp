@@ -220,12 +220,12 @@ static int tiling_lds(const Variant& v, const Geom& g, int TH, int TW, int CB, i
     // images and weights below 2^30 bytes (32-bit buffer offsets with room for an
     // out-of-range scalar part), the compiled tile and channel block
     if (g.layout != FCM_NHWC || g.family != FAM_DWPW) return 0;
-    if (g.ci % 32 || (g.co * g.elt) % 16) return 0;
+    if (g.ci % (32 * v.kc) || (g.co * g.elt) % 16) return 0;
     if ((int64_t)g.h * g.w * g.ci * g.elt >= ((int64_t)1 << 30)) return 0;
     if ((int64_t)g.ho * g.wo * g.co * g.elt >= ((int64_t)1 << 30)) return 0;
     if ((int64_t)(g.co + COB) * g.ci * g.elt >= ((int64_t)1 << 30)) return 0;
     if (CB != 64 / g.elt || COB != v.max_cob || TH != v.tile_h || TW != v.tile_w) return 0;
-    return lds7(g.s, TH, TW, v.max_cob / 64, g.ci).total;
+    return lds7(g.s, TH, TW, v.max_cob / 64, g.ci, v.kc).total;
   }
   if (v.gen == 5) {
     // NHWC, 16-byte input channel rows, 32-bit buffer offsets, 64-byte chunk, run-time
@@ -713,7 +713,11 @@ static double deep_time_estimate(const Variant& v, const Geom& g, const fcm_plan
   const int grid = std::max(1, (int)p.workgroups);
   const double tiles = (double)ceil_div(nwork, (int64_t)grid);
   const double share = std::max(1.0, (double)grid / hw.num_cus);
-  const double cyc = (tiles * nch * (kItem + kPerCopy * copies + kPerTile * ctw) + tiles * kPerWork) * share;
+  // per 32-channel chunk; items of two chunks pay the per-item part (barrier, waits) once,
+  // which measured faster only for long stride-1 chunk streams (7x7x1024: 21.5 against
+  // 23.0 us) and slower with stride 2 or few chunks (the larger items' copies)
+  const double item = kItem * (v.kc == 2 ? (g.s == 1 && g.ci >= 1024 ? 0.8 : 1.2) : 1.0);
+  const double cyc = (tiles * nch * (item + kPerCopy * copies + kPerTile * ctw) + tiles * kPerWork) * share;
   return kLaunch + std::max(cyc / kClock, (double)p.bytes_ideal / kRate);
 }
 

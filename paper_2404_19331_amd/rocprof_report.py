@@ -52,9 +52,10 @@ def kernel_symbol(variant, split=False, qx=0):
         fam, dt, k, s, th, tw, ct, wc = m5.groups()
         mode = {"k_dwpw5": 0, "k_pw5": 1, "k_dw5": 2}[fam]
         return "void fcm::k_fused5<fcm::%s, %s, %s, %d, %s, %s, %s, %s>(fcm::KArgs)" % (_DT[dt], k, s, mode, th, tw, ct, wc)
-    m7 = re.match(r"k_dwpw7<bf16,3,(\d+),(\d+)x(\d+),ct(\d+)>$", variant)
-    if m7:  # deep kernels: k_deep7<S, TH, TW, CTW>
-        return "void fcm::k_deep7<%s, %s, %s, %s>(fcm::KArgs)" % m7.groups()
+    m7 = re.match(r"k_dwpw7<bf16,3,(\d+),(\d+)x(\d+),ct(\d+)(?:,k(\d+))?>$", variant)
+    if m7:  # deep kernels: k_deep7<S, TH, TW, CTW, KC>
+        s7, th, tw, ct, kc = m7.groups()
+        return "void fcm::k_deep7<%s, %s, %s, %s, %s>(fcm::KArgs)" % (s7, th, tw, ct, kc or "1")
     m6 = re.match(r"(k_\w+6)<f32,(\d+),(\d+),(\d+)x(\d+)>$", variant)
     if m6:  # whole-module fp32 kernels: k_small6<MODE, K, S, TH, TW>
         fam, k, s, th, tw = m6.groups()

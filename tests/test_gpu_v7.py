@@ -5,8 +5,9 @@ workgroup streams many tiles and chunks through its three-deep load pipeline, th
 epilogue of one tile overlapping the next tile's loads), on images with ragged tiles,
 chunk counts per workgroup that are and are not multiples of three, a ragged last
 output-channel block, biases and activations; compared with the CPU oracle at the bf16
-tolerance. Input channels not in whole 32-channel chunks are not offered to these
-kernels (checked on the CPU with the planner).
+tolerance. Input channels not in whole 32-channel chunks (64-channel pairs for the
+two-chunk instances) are not offered to these kernels (checked on the CPU with the
+planner).
 """
 import re
 

@@ -817,29 +817,59 @@ __global__ __launch_bounds__(256) void k_combine3(KArgs a) {
   if (oy >= a.Ho || ox >= a.Wo || co >= a.Co) return;
   const size_t slice = (size_t)ntile * P * CoB;
   const Acc* src = (const Acc*)a.ws + ((size_t)wtile * P + p) * CoB + 4 * q;
+  // the slices are read eight at a time, all eight loads in flight together, and added in
+  // split order
   Acc sum[4] = {0, 0, 0, 0};
-  for (int s = 0; s < SPL; ++s) {
-    const typename DT::AccV v = *(const typename DT::AccV*)(src + s * slice);
+  for (int s0 = 0; s0 < SPL; s0 += 8) {
+    typename DT::AccV v[8];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) sum[e] += v[e];
+    for (int j = 0; j < 8; ++j)
+      if (s0 + j < SPL) v[j] = *(const typename DT::AccV*)(src + (s0 + j) * slice);
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+      if (s0 + j < SPL) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) sum[e] += v[j][e];
+      }
   }
   const Epi3 ep = make_epi3(a.act[STAGE], a.rq[STAGE]);  // STAGE: index of the PW convolution
   const void* bp = STAGE == 0 ? a.b1 : a.b2;
   const int32_t* pc = a.rqc[STAGE];  // int8 per-channel [multipliers | shifts] or nullptr
-  T* y = (T*)a.y + (((size_t)n * a.Ho + oy) * a.Wo + ox) * a.Co + co;
+  const size_t yo = (((size_t)n * a.Ho + oy) * a.Wo + ox) * a.Co + co;  // element offset
+  T* y = (T*)a.y + yo;
+  const int ne = a.Co - co < 4 ? a.Co - co : 4;
+  uint32_t out[4];  // the four results' bit patterns
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
-    if (co + e >= a.Co) break;
+    out[e] = 0u;
+    if (e >= ne) break;
     if constexpr (DT::ELT == 1) {
       const int32_t b = bp ? ((const int32_t*)bp)[co + e] : 0;
-      y[e] = (T)(pc ? epi_q(sum[e] + b, pc[co + e], pc_shift((uint32_t)pc[a.Co + co + e]), ep) : epi_i(sum[e] + b, ep));
+      out[e] = (uint32_t)(pc ? epi_q(sum[e] + b, pc[co + e], pc_shift((uint32_t)pc[a.Co + co + e]), ep)
+                             : epi_i(sum[e] + b, ep)) & 0xffu;
     } else {
       const float b = bp ? ((const float*)bp)[co + e] : 0.0f;
       const float o = epi_f(sum[e] + b, ep);
-      if constexpr (DT::ELT == 4)
-        y[e] = o;
+      out[e] = DT::ELT == 4 ? __float_as_uint(o) : (pack_bf16x2(o, 0.0f) & 0xffffu);
+    }
+  }
+  if (ne == 4 && (uintptr_t)y % (4 * DT::ELT) == 0) {  // one aligned store of the four results
+    if constexpr (DT::ELT == 1)
+      *(uint32_t*)y = out[0] | (out[1] << 8) | (out[2] << 16) | (out[3] << 24);
+    else if constexpr (DT::ELT == 2)
+      *(u32x2*)y = u32x2{out[0] | (out[1] << 16), out[2] | (out[3] << 16)};
+    else
+      *(u32x4*)y = u32x4{out[0], out[1], out[2], out[3]};
+  } else {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      if (e >= ne) break;
+      if constexpr (DT::ELT == 1)
+        y[e] = (T)out[e];
+      else if constexpr (DT::ELT == 2)
+        *(uint16_t*)(y + e) = (uint16_t)out[e];
       else
-        *(uint16_t*)(y + e) = (uint16_t)(pack_bf16x2(o, 0.0f) & 0xffffu);
+        y[e] = __uint_as_float(out[e]);
     }
   }
 }

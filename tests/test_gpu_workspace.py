@@ -76,3 +76,20 @@ def test_split_plans_float_match_the_oracle(dt):
     for splits in (2, 4, 8):
         got = to_np(run_fused(case, d, plan=_split_plan(case, splits)))
         assert_close(got, ref, dt, "%s splits %d" % (case.name, splits))
+
+
+@pytest.mark.parametrize("dt,co", [("f32", 18), ("f32", 20), ("bf16", 18), ("bf16", 36)])
+def test_split_plans_ragged_output_channels(dt, co):
+    """The combine kernel stores four output channels per thread with one aligned store, and
+    one by one where c_out leaves a partial group of four (c_out % 4 != 0): both match the
+    oracle at every split count."""
+    case = Case("dw_pw", 2, 9, 11, 256, 256, co, 3, 1, 1, dt, "nhwc", ("relu", "none", "none"), bias=True,
+                dist_x="n01", seed=4300 + co, name="split-%s-co%d" % (dt, co))
+    inp = make_inputs(case)
+    ref = oracle_ref(case, inp)
+    d = dev_inputs(inp, case.dtype)
+    for splits in (2, 4, 8):
+        p = _split_plan(case, splits)
+        assert p.splits == splits
+        got = to_np(run_fused(case, d, plan=p))
+        assert_close(got, ref, dt, "%s splits %d" % (case.name, splits))

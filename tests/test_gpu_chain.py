@@ -1,10 +1,11 @@
 """GPU parity of whole chains (FusePlanner over a network, Sec. IV): the MobileNetV2 body
 (51 DW/PW layers after the stem, no skip connections) planned three ways -- least
 Eq. 1-4 bytes, least modelled time, every layer alone -- and run through fcm_chain_run,
-against the CPU oracle applied layer by layer. int8 is bit-exact end to end; float
-chains are compared at the parity tolerance over their first stages (rounding of each
-layer's result to bfloat16 in a different order can flip a last bit that later layers
-carry along, so the full float chains are compared between the three plans instead)."""
+against the CPU oracle applied layer by layer. int8 is bit-exact end to end. Float chains
+are compared with the oracle at the parity tolerance over their first stages, and the full
+bf16 body kernel by kernel, each kernel fed the device's own output of the kernel before:
+rounding a layer's result to bfloat16 in a different order can flip a last bit that later
+layers carry along, so end to end the full float chains are compared between the plans."""
 import numpy as np
 import pytest
 
@@ -65,3 +66,37 @@ def test_autotuned_chain_plan_runs_bit_exact():
     assert plan.num_groups >= 1 and len(timed) >= len(spec.layers)
     got = fcm.chain_run(d, plan, dev[0], dev[1], dev[2])
     assert np.array_equal(to_np(got), ref)
+
+
+@pytest.mark.parametrize("objective", OBJECTIVES)
+def test_bf16_full_chain_each_kernel_against_oracle(objective):
+    """Every kernel of the full bf16 MobileNetV2 body at its true depth: the planned chain runs
+    one group (kernel) at a time, each group fed the device's own output of the group
+    before, and each group's output is compared with the oracle applied to that group's
+    layers on the same input, so no rounding carries from one kernel into the next
+    comparison."""
+    import dataclasses
+    from paper_2404_19331_amd import fcm
+    spec = mobilenetv2_chain(n=2, dtype="bf16")
+    host, dev = _dev(spec)
+    d = fcm.chain_desc(spec.n, spec.h, spec.w, spec.c, spec.layers, spec.dtype, spec.layout)
+    plan = fcm.chain_plan(d, objective)
+    firsts = [plan.first[i] for i in range(plan.num_groups)] + [len(spec.layers)]
+    assert firsts[0] == 0 and all(a < b for a, b in zip(firsts, firsts[1:]))
+    x = dev[0]
+    h, w, c = spec.h, spec.w, spec.c
+    for g in range(plan.num_groups):
+        a, b = firsts[g], firsts[g + 1]
+        sub = dataclasses.replace(spec, h=h, w=w, c=c, layers=spec.layers[a:b])
+        sd = fcm.chain_desc(sub.n, h, w, c, sub.layers, sub.dtype, sub.layout)
+        sp = fcm.ChainPlan()
+        sp.objective, sp.num_groups, sp.first[0], sp.op[0], sp.plan[0] = plan.objective, 1, 0, plan.op[g], plan.plan[g]
+        y = fcm.chain_run(sd, sp, x, dev[1][a:b], dev[2][a:b])
+        ref = oracle_chain(sub, to_np(x), host[1][a:b], host[2][a:b])
+        assert_close(to_np(y), ref, "bf16", "%s plan, kernel %d (layers %d..%d)" % (objective, g, a, b - 1))
+        x = y
+        for L in sub.layers:
+            if L["kind"] == "dw":
+                h, w = fcm.out_hw(h, w, L["k"], L["stride"], L["pad"])
+            else:
+                c = L["c_out"]
